@@ -1,0 +1,234 @@
+#!/usr/bin/env python3
+"""Throughput of the STCA forward under request level batching on one MI355X.
+
+One step = one stca_forward over the whole batch (history K/V projection of
+every layer, then per layer the fused multi-target attention and the target
+update), inputs already resident in HBM.  Prints one JSON line:
+targets scored per second, the dominant kernel against its roofline (HIP
+events recorded on the library's stream around every launch of the timed
+steps), and the fp64 CPU oracle timed on a bounded sample of the same workload.
+
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--ablation]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+from paper_2511_06077_amd import accounting, stca  # noqa: E402
+from paper_2511_06077_amd import workload as W  # noqa: E402
+
+PEAK_HBM_GBS = 8000.0
+PEAK_BF16_TFLOPS = 2500.0
+PEAK_FP32_TFLOPS = 157.3
+
+
+def log(msg: str) -> None:
+    print(msg, file=sys.stderr, flush=True)
+
+
+def kernel_work(label: str, b: W.Batch, es: int):
+    """Algorithmic (flop, bytes) of one launch of a kernel, from the method's
+    compulsory work (accounting.stage_costs) divided over launches."""
+    wl = b.wl
+    c = accounting.stage_costs(b.hist_len, b.n_tgt, wl.d_model, wl.n_layers, es)
+    n = wl.n_layers
+    if label == "proj":
+        # all layers in one launch; rows of requests without targets still count
+        Ls = float(b.hist_len.sum())
+        return 4.0 * Ls * wl.d_model ** 2 * n, es * Ls * wl.d_model * (1 + 2 * n)
+    if label == "attn":
+        return c["attn"]["flop"] / n, c["attn"]["bytes"] / n
+    if label == "update":
+        return c["update"]["flop"] / n, 0.0
+    return 0.0, 0.0
+
+
+def roofline_entry(label, ms, flop, byts, peak_tf):
+    t_mfma = flop / (peak_tf * 1e12) if flop else 0.0
+    t_hbm = byts / (PEAK_HBM_GBS * 1e9) if byts else 0.0
+    if t_mfma >= t_hbm:
+        ach = flop / (ms * 1e-3) / 1e12
+        return {"bound": "mfma", "achieved": ach, "peak": peak_tf, "unit": "TFLOP/s", "frac": ach / peak_tf,
+                "traffic": None}
+    ach = byts / (ms * 1e-3) / 1e9
+    return {"bound": "hbm", "achieved": ach, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": ach / PEAK_HBM_GBS,
+            "traffic": None}
+
+
+def cpu_baseline(wl: W.Workload, budget_s: float):
+    """The fp64 oracle, as it is, on requests of the same workload taken in
+    order until the time budget is spent."""
+    from oracle import stca_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = os.cpu_count() or 1
+    L, m = W.request_shapes(wl)
+    done_t, done_r, spent = 0, 0, 0.0
+    for r in range(wl.n_requests):
+        sub = W.make_batch(wl, requests=[r], with_grad=False, threads=1)
+        inp = sub.f64()
+        t0 = time.perf_counter()
+        O.forward(inp, keep=False)
+        spent += time.perf_counter() - t0
+        done_t += int(m[r])
+        done_r += 1
+        if spent >= budget_s:
+            break
+    return {"value": done_t / spent, "unit": "targets/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {done_r} of {wl.n_requests} requests of {wl.name} ({done_t} targets), "
+                      f"{spent:.1f} s of fp64 CPU work"}
+
+
+def timed_forward(db, steps: int, warmup: int):
+    import torch
+    dev = db.device
+    stream = torch.cuda.current_stream(dev)
+    for _ in range(warmup):
+        db.forward()
+    torch.cuda.synchronize(dev)
+    nl = stca.stca_forward_launch_count(db.dims, db.batch)
+    evs = [stca.HipEvents(nl + 1) for _ in range(steps)]
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize(dev)
+    start.record(stream)
+    for k in range(steps):
+        stca.stca_forward_profiled(db.dims, db.batch, db.hist, db.tgt, db.weights, db.out, None, db.ws,
+                                   db.ws_bytes, stream.cuda_stream, evs[k].ev, evs[k].labels)
+    end.record(stream)
+    torch.cuda.synchronize(dev)
+    total_ms = start.elapsed_time(end)
+    per = {}
+    for e in evs:
+        for k in range(nl):
+            lab = e.label(k)
+            per.setdefault(lab, []).append(e.elapsed_ms(k, k + 1))
+    for e in evs:
+        e.close()
+    return total_ms, per
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    ap.add_argument("--ablation", action="store_true",
+                    help="also time one target per request and the instance-wise (non-RLB) layout")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (the STCA path needs no collectives; requests shard with "
+              f"zero communication); got --gpus {args.gpus}, WORLD_SIZE={world}", file=sys.stderr)
+        return 2
+
+    import torch
+    from paper_2511_06077_amd.device import DeviceBatch
+    wl = W.WORKLOADS[args.workload]
+    t0 = time.time()
+    b = W.make_batch(wl, with_grad=False)
+    log(f"[bench] generated {wl.name}: {b.n_hist} history rows, {b.n_tgt_total} targets ({time.time() - t0:.1f} s)")
+    db = DeviceBatch(b, device="cuda:0")
+    log(f"[bench] workspace {db.ws_bytes / 2**30:.2f} GiB; path {stca.stca_path(db.dims)}")
+    total_ms, per = timed_forward(db, args.steps, args.warmup)
+    ms_step = total_ms / args.steps
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step")
+
+    es = 2 if wl.dtype == "bf16" else 4
+    peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    kernels = {}
+    for lab, v in per.items():
+        launches = len(v) // args.steps
+        ms = float(np.mean(v))
+        flop, byts = kernel_work(lab, b, es)
+        ent = {"launches_per_step": launches, "ms_per_launch": ms, "ms_per_step": ms * launches}
+        if flop or byts:
+            ent.update({"tflops": flop / (ms * 1e-3) / 1e12, "gbs": byts / (ms * 1e-3) / 1e9,
+                        "mfma_frac": flop / (ms * 1e-3) / 1e12 / peak_tf,
+                        "hbm_frac": byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS})
+        kernels[lab] = ent
+    dom = max((k for k in kernels if kernel_work(k, b, es) != (0.0, 0.0)),
+              key=lambda k: kernels[k]["ms_per_step"])
+    flop, byts = kernel_work(dom, b, es)
+    roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, peak_tf)
+    roof["kernel"] = dom
+    c = accounting.stage_costs(b.hist_len, b.n_tgt, wl.d_model, wl.n_layers, es)
+    roof_ms = sum(max(v["flop"] / (peak_tf * 1e12), v["bytes"] / (PEAK_HBM_GBS * 1e9)) for v in c.values()) * 1e3
+    value = b.n_tgt_total / (ms_step * 1e-3)
+    rec = {
+        "metric": "targets scored/sec, STCA forward",
+        "value": value,
+        "unit": "targets/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32",
+        "data": "synthetic",
+        "config": {"workload": wl.name, "requests": wl.n_requests,
+                   "targets_per_request": wl.n_targets or list(wl.tgt_range),
+                   "hist_len": wl.hist_len or list(wl.hist_range), "d_model": wl.d_model,
+                   "heads": wl.n_heads, "layers": wl.n_layers, "ffn_hidden": wl.ffn_hidden},
+        "roofline": roof,
+        "path_roofline": {"ms": roof_ms, "frac": roof_ms / ms_step,
+                          "targets_per_s": b.n_tgt_total / (roof_ms * 1e-3)},
+        "kernels": kernels,
+    }
+    if args.ablation:
+        rec["ablation"] = ablation(wl, args)
+    del db
+    torch.cuda.empty_cache()
+    if args.cpu_seconds > 0:
+        log("[bench] timing the CPU oracle")
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+def ablation(wl: W.Workload, args):
+    """The same kernels on (a) one target per request and (b) the instance-wise
+    layout: every target its own request with a copy of the history."""
+    import torch
+    from paper_2511_06077_amd.device import DeviceBatch
+    out = {}
+    if wl.n_targets > 1 and wl.hist_range is None:
+        one = W.Workload(wl.name + "_m1", wl.n_requests, wl.d_model, wl.n_heads, wl.n_layers, wl.dtype, wl.seed,
+                         hist_len=wl.hist_len, n_targets=1)
+        db = DeviceBatch(W.make_batch(one), device="cuda:0")
+        ms, _ = timed_forward(db, max(3, args.steps // 4), 1)
+        ms /= max(3, args.steps // 4)
+        out["one_target_per_request"] = {"ms_per_step": ms, "targets_per_s": one.n_requests / (ms * 1e-3)}
+        del db
+        torch.cuda.empty_cache()
+    # instance-wise layout on a slice of requests that fits comfortably, scaled
+    b = W.make_batch(wl, requests=list(range(min(wl.n_requests, 8))), with_grad=False)
+    nb = W.replicate_per_target(b)
+    for name, bb in (("rlb_slice", b), ("non_rlb_slice", nb)):
+        db = DeviceBatch(bb, device="cuda:0")
+        ms, _ = timed_forward(db, 3, 1)
+        ms /= 3
+        out[name] = {"requests": int(b.n_requests), "targets": int(bb.n_tgt_total), "ms": ms,
+                     "targets_per_s": bb.n_tgt_total / (ms * 1e-3)}
+        del db
+        torch.cuda.empty_cache()
+    out["rlb_speedup_on_slice"] = out["non_rlb_slice"]["ms"] / out["rlb_slice"]["ms"]
+    return out
+
+
+if __name__ == "__main__":
+    sys.exit(main())

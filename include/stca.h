@@ -1,0 +1,180 @@
+/*
+ * stca.h - C ABI of the MI355X (gfx950) STCA library.
+ *
+ * Stacked Target-to-History Cross Attention under Request Level Batching:
+ * every target (candidate item) of a request attends, with a single query per
+ * head, to that request's whole history, layer after layer (paper Sec. 3.1,
+ * "Multi-head target-to-history cross attention" and Eq. layer-output).
+ * The history of a request is projected to the per-layer K/V once and the
+ * projection is shared by all of that request's targets (Sec. 3.2, App. A.3).
+ * Ragged batches are packed without padding; per-request offset arrays mark
+ * the segments (App. A.4, the index-based ragged target attention).
+ *
+ * Layer (the benchmark workloads' form of the stacked update, Sec. 3.1
+ * "Stacking" replaced by a residual FFN; biases omitted as in the paper):
+ *   s^(0)   = x_t
+ *   q       = s^(i) W_Q^i                          head j: columns [j d_h, (j+1) d_h)
+ *   a_j     = softmax(q_j (X W_K^i)_j^T / sqrt(d_h)) (X W_V^i)_j      over the request's history X
+ *   u       = s^(i) + [a_1 | ... | a_h] W_O^i
+ *   s^(i+1) = u + ReLU(u W_1^i) W_2^i
+ *   out     = s^(n)
+ *
+ * Conventions shared by every entry point:
+ *  - All tensor pointers are device pointers unless named *_host, and must be
+ *    16-byte aligned.  Matrices are row-major; y = x W (W is [d_in][d_out]).
+ *  - Weights are stacked per layer: wq, wk, wv, wo [n_layers][d][d],
+ *    w1 [n_layers][d][ffn_hidden], w2 [n_layers][ffn_hidden][d].
+ *  - Storage dtype (STCA_F32 or STCA_BF16) applies to hist, tgt, the weights,
+ *    out and dout; accumulation is always fp32; gradients are fp32.
+ *  - Request r owns hist rows [hist_off[r], hist_off[r+1]) and tgt rows
+ *    [tgt_off[r], tgt_off[r+1]).  offsets[0] = 0, non-decreasing,
+ *    offsets[R] = n_hist / n_tgt.  A request with targets must have at least
+ *    one history row; a request with no targets is legal and produces nothing.
+ *  - The caller owns every buffer.  The library never allocates, frees or
+ *    synchronises: all work is enqueued on `stream`, and calls return before it
+ *    runs.  Calls on different streams need distinct workspaces.
+ *  - Errors found on the host are returned before anything is enqueued.
+ *    Offsets are checked on the host when the *_host copies are given;
+ *    otherwise the device scheduler checks them, produces no work for a bad
+ *    request and records STCA_ERR_INVALID_ARG in the workspace, readable with
+ *    stca_device_status().  No exception crosses the ABI.
+ */
+#ifndef STCA_H_
+#define STCA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  STCA_OK = 0,
+  STCA_ERR_INVALID_ARG = -1, /* bad pointer, size or offsets */
+  STCA_ERR_UNSUPPORTED = -2, /* valid but not implemented shape/dtype */
+  STCA_ERR_WORKSPACE = -3,   /* workspace or saved buffer too small */
+  STCA_ERR_HIP = -4          /* a HIP runtime call or launch failed */
+} stca_status_t;
+
+typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
+
+/* Model shape.  d_model % n_heads == 0 and ffn_hidden a multiple of 32.
+ * STCA_BF16 with d_head = d_model / n_heads = 32 and d_model in {64, 128, 256}
+ * runs on the bf16 MFMA kernels; every other shape with d_head in
+ * {8, 16, 32, 64} (either dtype) runs on the generic fp32-arithmetic kernels
+ * (stca_path tells which). */
+typedef struct {
+  int32_t d_model;
+  int32_t n_heads;
+  int32_t n_layers;
+  int32_t ffn_hidden;
+  int32_t dtype; /* stca_dtype_t */
+} stca_dims_t;
+
+/* A packed ragged batch (App. A.4: flattened rows plus segment boundaries). */
+typedef struct {
+  int32_t n_requests;           /* R >= 1 */
+  int64_t n_hist;               /* total history rows, < 2^31 */
+  int64_t n_tgt;                /* total target rows, < 2^31 */
+  const int32_t* hist_off;      /* device [R+1] */
+  const int32_t* tgt_off;       /* device [R+1] */
+  const int32_t* hist_off_host; /* optional host copy [R+1]: enables host checks and exact sizing */
+  const int32_t* tgt_off_host;  /* optional host copy [R+1] */
+} stca_batch_t;
+
+/* Per-layer weights (paper Sec. 3.1: W_Q, W_K, W_V, W_O; the FFN W_1, W_2). */
+typedef struct {
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const void* wo;
+  const void* w1;
+  const void* w2;
+} stca_weights_t;
+
+/* Weight gradients, fp32, same shapes as the weights; overwritten. */
+typedef struct {
+  float* dwq;
+  float* dwk;
+  float* dwv;
+  float* dwo;
+  float* dw1;
+  float* dw2;
+} stca_wgrads_t;
+
+/* Byte offsets into the `saved` buffer (all fp32 unless stated), for reading
+ * per-layer intermediates back.  Each per-layer tensor is stacked on a leading
+ * layer axis: s [n][n_tgt][d] (layer input state), a [n][n_tgt][d] (head
+ * concatenation before W_O), u [n][n_tgt][d] (state after the attention
+ * residual), lse [n][n_tgt][h] (natural log-sum-exp of each head's scores).
+ * kv is opaque (the projected history in the kernels' own layout). */
+typedef struct {
+  size_t s, a, u, lse, kv;
+  size_t total;
+} stca_saved_layout_t;
+
+/* Workspace bytes needed by stca_forward (with_backward = 0) or stca_backward
+ * (with_backward = 1).  Returns 0 for invalid or unsupported arguments. */
+size_t stca_workspace_size(const stca_dims_t* dims, const stca_batch_t* batch, int with_backward);
+
+/* Bytes of the `saved` buffer that stca_forward fills for stca_backward. */
+size_t stca_saved_size(const stca_dims_t* dims, const stca_batch_t* batch);
+
+/* Offsets of the saved tensors; returns STCA_ERR_INVALID_ARG / UNSUPPORTED
+ * like the other calls. */
+stca_status_t stca_saved_layout(const stca_dims_t* dims, const stca_batch_t* batch,
+                                stca_saved_layout_t* layout);
+
+/* Forward pass: out[n_tgt][d] (storage dtype) = s^(n) for every target.
+ *  hist  [n_hist][d], tgt [n_tgt][d]  storage dtype, device
+ *  saved nullable; when given (stca_saved_size bytes) the per-layer
+ *        intermediates and the projected history are kept for stca_backward
+ *  ws    device workspace of ws_bytes >= stca_workspace_size(dims, batch, 0) */
+stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch,
+                           const void* hist, const void* tgt, const stca_weights_t* w,
+                           void* out, void* saved, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/* Backward pass of f = sum_t <dout_t, out_t> given the `saved` buffer of a
+ * stca_forward call on the same inputs.  Writes (overwrites) dhist [n_hist][d],
+ * dtgt [n_tgt][d] and all weight gradients, fp32.  dout is [n_tgt][d] in the
+ * storage dtype.  ws_bytes >= stca_workspace_size(dims, batch, 1). */
+stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch,
+                            const void* hist, const void* tgt, const stca_weights_t* w,
+                            const void* saved, const void* dout, float* dhist, float* dtgt,
+                            const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
+                            hipStream_t stream);
+
+/* Measurement variant of stca_forward: the same work, plus hipEventRecord on
+ * `stream` around every kernel launch so a caller can time each kernel on the
+ * stream it runs on.  events[0] is recorded before the first launch and
+ * events[k+1] right after launch k; n_events must be at least
+ * stca_forward_launch_count(dims, batch) + 1.  labels (nullable, n_events - 1
+ * entries) receive static kernel names ("proj", "attn", "update", ...).
+ * The events must have been created by the caller (hipEventCreate). */
+int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch);
+stca_status_t stca_forward_profiled(const stca_dims_t* dims, const stca_batch_t* batch,
+                                    const void* hist, const void* tgt, const stca_weights_t* w,
+                                    void* out, void* saved, void* ws, size_t ws_bytes,
+                                    hipStream_t stream, hipEvent_t* events, int n_events,
+                                    const char** labels);
+
+/* Reads (synchronising on `stream`) the status the device scheduler recorded
+ * in `ws` during the last call that used it: STCA_OK or STCA_ERR_INVALID_ARG. */
+stca_status_t stca_device_status(const void* ws, hipStream_t stream);
+
+/* Static description of a status code. */
+const char* stca_status_string(stca_status_t status);
+
+/* Which kernel family a shape runs on: 1 = bf16 MFMA path, 0 = generic fp32
+ * path, negative = a status code for invalid or unsupported dims. */
+int stca_path(const stca_dims_t* dims);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* STCA_H_ */

@@ -1,0 +1,542 @@
+// C ABI of the STCA library: argument checks, workspace/saved layouts and the
+// launch sequences of the forward and backward passes.
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <cstring>
+
+#include "common.h"
+#include "fast.h"
+#include "internal.h"
+
+using namespace stca;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+
+struct Bump {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    size_t o = off;
+    off = round_up(static_cast<int64_t>(off + bytes), kAlign);
+    return o;
+  }
+};
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// 1 = bf16 MFMA path, 0 = generic, <0 = status
+int path_of(const stca_dims_t* d) {
+  if (!d) return STCA_ERR_INVALID_ARG;
+  if (d->d_model <= 0 || d->n_heads <= 0 || d->n_layers <= 0 || d->ffn_hidden <= 0 ||
+      d->d_model % d->n_heads != 0 || (d->dtype != STCA_F32 && d->dtype != STCA_BF16))
+    return STCA_ERR_INVALID_ARG;
+  const int dh = d->d_model / d->n_heads;
+  if (d->ffn_hidden % 32 != 0) return STCA_ERR_UNSUPPORTED;
+  if (d->dtype == STCA_BF16 && dh == 32 && (d->d_model == 64 || d->d_model == 128 || d->d_model == 256))
+    return 1;
+  if (dh == 8 || dh == 16 || dh == 32 || dh == 64) return 0;
+  return STCA_ERR_UNSUPPORTED;
+}
+
+stca_status_t check_batch(const stca_batch_t* b) {
+  if (!b || b->n_requests < 1 || b->n_hist < 0 || b->n_tgt < 0 || b->n_hist >= (int64_t(1) << 31) ||
+      b->n_tgt >= (int64_t(1) << 31) || !b->hist_off || !b->tgt_off)
+    return STCA_ERR_INVALID_ARG;
+  if ((b->hist_off_host == nullptr) != (b->tgt_off_host == nullptr)) return STCA_ERR_INVALID_ARG;
+  if (b->hist_off_host) {
+    const int32_t *h = b->hist_off_host, *t = b->tgt_off_host;
+    if (h[0] != 0 || t[0] != 0 || h[b->n_requests] != b->n_hist || t[b->n_requests] != b->n_tgt)
+      return STCA_ERR_INVALID_ARG;
+    for (int r = 0; r < b->n_requests; ++r) {
+      if (h[r + 1] < h[r] || t[r + 1] < t[r]) return STCA_ERR_INVALID_ARG;
+      if (t[r + 1] > t[r] && h[r + 1] == h[r]) return STCA_ERR_INVALID_ARG;
+    }
+  }
+  return STCA_OK;
+}
+
+int device_cus() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+// Chunk length (in 32-row blocks) of the split over history rows: aim at about
+// four attention units per CU.  STCA_CHUNK_BLOCKS overrides it (a tuning and
+// testing knob: forcing small chunks exercises the partial-result merge).
+int chunk_blocks_for(const stca_batch_t* b, int n_cu) {
+  if (const char* e = std::getenv("STCA_CHUNK_BLOCKS")) {
+    int v = std::atoi(e);
+    if (v >= 1) return v;
+  }
+  const int64_t nb = ceil_div(b->n_hist, kBlockTokens);
+  int64_t c = ceil_div(nb, 4 * static_cast<int64_t>(n_cu));
+  if (c < 8) c = 8;
+  if (c > (1 << 20)) c = 1 << 20;
+  return static_cast<int>(c);
+}
+
+int64_t max_units_for(const stca_batch_t* b, int chunk_blocks) {
+  if (b->hist_off_host)
+    return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks);
+  return (ceil_div(b->n_tgt, kTargetGroup) + b->n_requests) * kMaxChunks;
+}
+
+int ffn_chunk(int F) {
+  for (int c : {512, 256, 128, 64, 32})
+    if (F % c == 0) return c;
+  return 32;
+}
+
+struct Layout {
+  int path;
+  int d, h, n, F, dh;
+  int64_t nh, nt, nblocks;
+  int chunk_blocks;
+  int64_t max_units;
+  // common
+  size_t hdr, units, tchunks, part_acc, part_ml, state_a, state_b;
+  // fast
+  size_t qn, wkp, wvp, wop, w1p, w2p, wqp, kv;
+  // generic forward
+  size_t kv32, q32, abuf, ubuf, hid;
+  // backward (generic)
+  size_t pre, dhid, ds, du, da, dq, ds2, dkv32, dq_part;
+  size_t total;
+};
+
+bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backward, bool with_saved, Layout* L) {
+  const int p = path_of(dims);
+  if (p < 0 || check_batch(b) != STCA_OK) return false;
+  L->path = p;
+  L->d = dims->d_model;
+  L->h = dims->n_heads;
+  L->n = dims->n_layers;
+  L->F = dims->ffn_hidden;
+  L->dh = L->d / L->h;
+  L->nh = b->n_hist;
+  L->nt = b->n_tgt;
+  L->nblocks = ceil_div(b->n_hist, kBlockTokens);
+  L->chunk_blocks = chunk_blocks_for(b, device_cus());
+  L->max_units = max_units_for(b, L->chunk_blocks);
+  const size_t d = L->d, nt = L->nt, nh = L->nh, F = L->F, n = L->n;
+  Bump m;
+  L->hdr = m.take(sizeof(WsHeader));
+  L->units = m.take(sizeof(Unit) * (L->max_units + 1));
+  L->tchunks = m.take(4 * (nt + 1));
+  L->state_a = m.take(4 * nt * d);
+  L->state_b = m.take(4 * nt * d);
+  if (!with_backward) {
+    L->part_acc = m.take(4 * kMaxChunks * nt * d);
+    L->part_ml = m.take(8 * kMaxChunks * nt * L->h);
+    if (p == 1) {
+      L->qn = m.take(2 * nt * d);
+      L->wkp = m.take(2 * n * d * d);
+      L->wvp = m.take(2 * n * d * d);
+      L->wop = m.take(2 * n * d * d);
+      L->wqp = m.take(2 * n * d * d);
+      L->w1p = m.take(2 * n * d * F);
+      L->w2p = m.take(2 * n * d * F);
+      L->kv = with_saved ? 0 : m.take(2 * n * L->nblocks * kBlockTokens * 2 * d);
+    } else {
+      L->kv32 = m.take(4 * nh * 2 * d);
+      L->q32 = m.take(4 * nt * d);
+      L->abuf = m.take(4 * nt * d);
+      L->ubuf = m.take(4 * nt * d);
+      L->hid = m.take(4 * nt * F);
+    }
+  } else {
+    L->kv32 = m.take(4 * nh * 2 * d);
+    L->dkv32 = m.take(4 * nh * 2 * d);
+    L->q32 = m.take(4 * nt * d);
+    L->hid = m.take(4 * nt * F);
+    L->pre = m.take(4 * nt * F);
+    L->dhid = m.take(4 * nt * F);
+    L->ds = m.take(4 * nt * d);
+    L->du = m.take(4 * nt * d);
+    L->da = m.take(4 * nt * d);
+    L->dq = m.take(4 * nt * d);
+    L->ds2 = m.take(4 * nt * d);
+    L->dq_part = m.take(4 * kMaxChunks * nt * d);
+  }
+  L->total = m.off;
+  return true;
+}
+
+bool saved_layout(const stca_dims_t* dims, const stca_batch_t* b, stca_saved_layout_t* s) {
+  const int p = path_of(dims);
+  if (p < 0 || check_batch(b) != STCA_OK) return false;
+  const size_t d = dims->d_model, nt = b->n_tgt, n = dims->n_layers, h = dims->n_heads;
+  Bump m;
+  s->s = m.take(4 * n * nt * d);
+  s->a = m.take(4 * n * nt * d);
+  s->u = m.take(4 * n * nt * d);
+  s->lse = m.take(4 * n * nt * h);
+  s->kv = p == 1 ? m.take(2 * n * ceil_div(b->n_hist, kBlockTokens) * kBlockTokens * 2 * d) : m.off;
+  s->total = m.off;
+  return true;
+}
+
+template <typename T>
+T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+template <typename T>
+const T* at(const void* base, size_t off) {
+  return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+
+// Optional per-launch event recording for measurement: ev[0] is recorded
+// before the first launch and ev[k+1] right after launch k.
+struct Rec {
+  hipEvent_t* ev = nullptr;
+  int n = 0, k = 0;
+  const char** labels = nullptr;
+  hipStream_t st = nullptr;
+  hipError_t start() {
+    if (!ev) return hipSuccess;
+    if (k >= n) return hipErrorInvalidValue;
+    return hipEventRecord(ev[k++], st);
+  }
+  hipError_t mark(const char* name) {
+    if (!ev) return hipSuccess;
+    if (k >= n) return hipErrorInvalidValue;
+    if (labels) labels[k - 1] = name;
+    return hipEventRecord(ev[k++], st);
+  }
+};
+
+#define HIPCHK(x)                             \
+  do {                                        \
+    if ((x) != hipSuccess) return STCA_ERR_HIP; \
+  } while (0)
+
+stca_status_t check_common(const stca_dims_t* dims, const stca_batch_t* b, const void* hist, const void* tgt,
+                           const stca_weights_t* w, void* ws) {
+  const int p = path_of(dims);
+  if (p < 0) return static_cast<stca_status_t>(p);
+  stca_status_t st = check_batch(b);
+  if (st != STCA_OK) return st;
+  if (!w || !ws || (b->n_hist > 0 && !hist) || (b->n_tgt > 0 && !tgt)) return STCA_ERR_INVALID_ARG;
+  const void* ptrs[] = {hist, tgt, w->wq, w->wk, w->wv, w->wo, w->w1, w->w2, ws};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
+  if (!w->wq || !w->wk || !w->wv || !w->wo || !w->w1 || !w->w2) return STCA_ERR_INVALID_ARG;
+  return STCA_OK;
+}
+
+// ---------------------------------------------------------------- forward
+stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* hist, const void* tgt,
+                           const stca_weights_t* w, void* out, void* saved, const stca_saved_layout_t& SL,
+                           void* ws, hipStream_t st, Rec& rec) {
+  HIPCHK(rec.start());
+  const int d = L.d, n = L.n, F = L.F;
+  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  Unit* units = at<Unit>(ws, L.units);
+  int32_t* tch = at<int32_t>(ws, L.tchunks);
+  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, units, L.max_units,
+                      tch, hdr, st)); HIPCHK(rec.mark("sched"));
+  HIPCHK(fast_pack(w->wk, at<char>(ws, L.wkp), n, d, d, st)); HIPCHK(rec.mark("pack_wk"));
+  HIPCHK(fast_pack(w->wv, at<char>(ws, L.wvp), n, d, d, st)); HIPCHK(rec.mark("pack_wv"));
+  HIPCHK(fast_pack(w->wo, at<char>(ws, L.wop), n, d, d, st)); HIPCHK(rec.mark("pack_wo"));
+  HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, st)); HIPCHK(rec.mark("pack_wq"));
+  HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, st)); HIPCHK(rec.mark("pack_w1"));
+  HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, st)); HIPCHK(rec.mark("pack_w2"));
+  char* kv = saved ? at<char>(saved, SL.kv) : at<char>(ws, L.kv);
+  if (L.nh > 0)
+    HIPCHK(fast_proj(d, hist, L.nh, L.nblocks, at<char>(ws, L.wkp), at<char>(ws, L.wvp), kv, n,
+                     fast_proj_parts(n, L.nblocks, device_cus()), st)); HIPCHK(rec.mark("proj"));
+  const size_t kv_layer = (size_t)L.nblocks * kBlockTokens * 2 * d * 2;
+  FastUpdate f{};
+  f.n_layers = n;
+  f.F = F;
+  f.FC = ffn_chunk(F);
+  f.n_tgt = L.nt;
+  f.tgt = tgt;
+  f.tchunks = tch;
+  f.part_acc = at<float>(ws, L.part_acc);
+  f.part_ml = at<char>(ws, L.part_ml);
+  f.QN = at<char>(ws, L.qn);
+  f.WoP = at<char>(ws, L.wop);
+  f.W1P = at<char>(ws, L.w1p);
+  f.W2P = at<char>(ws, L.w2p);
+  f.WqP = at<char>(ws, L.wqp);
+  f.out = out;
+  // s^(i) lives in saved.s[i] when saving, else alternates between two buffers
+  auto state = [&](int i) -> float* {
+    if (saved) return at<float>(saved, SL.s) + (size_t)i * L.nt * d;
+    return at<float>(ws, (i % 2) ? L.state_b : L.state_a);
+  };
+  f.mode = 0;
+  f.layer = 0;
+  f.s_out = state(0);
+  HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
+  const int grid = static_cast<int>(std::min<int64_t>(L.max_units, 8 * (int64_t)device_cus()));
+  for (int i = 0; i < n; ++i) {
+    HIPCHK(fast_attn(d, units, hdr, grid, f.QN, kv + i * kv_layer, at<float>(ws, L.part_acc), at<char>(ws, L.part_ml), L.nt,
+                     st)); HIPCHK(rec.mark("attn"));
+    f.mode = 1;
+    f.layer = i;
+    f.s_in = state(i);
+    f.s_out = i + 1 < n ? state(i + 1) : nullptr;
+    f.save_a = saved ? at<float>(saved, SL.a) + (size_t)i * L.nt * d : nullptr;
+    f.save_u = saved ? at<float>(saved, SL.u) + (size_t)i * L.nt * d : nullptr;
+    f.save_lse = saved ? at<float>(saved, SL.lse) + (size_t)i * L.nt * L.h : nullptr;
+    HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
+  }
+  return STCA_OK;
+}
+
+stca_status_t forward_generic(const Layout& L, int bf, const stca_batch_t* b, const void* hist, const void* tgt,
+                              const stca_weights_t* w, void* out, void* saved, const stca_saved_layout_t& SL,
+                              void* ws, hipStream_t st, Rec& rec) {
+  HIPCHK(rec.start());
+  const int d = L.d, n = L.n, F = L.F, h = L.h;
+  const size_t es = bf ? 2 : 4;
+  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  Unit* units = at<Unit>(ws, L.units);
+  int32_t* tch = at<int32_t>(ws, L.tchunks);
+  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, units, L.max_units,
+                      tch, hdr, st)); HIPCHK(rec.mark("sched"));
+  float* kv = at<float>(ws, L.kv32);
+  float* q = at<float>(ws, L.q32);
+  float* hid = at<float>(ws, L.hid);
+  float* pacc = at<float>(ws, L.part_acc);
+  float* pml = at<float>(ws, L.part_ml);
+  auto state = [&](int i) -> float* {
+    if (saved && i < n) return at<float>(saved, SL.s) + (size_t)i * L.nt * d;
+    return at<float>(ws, (i % 2) ? L.state_b : L.state_a);
+  };
+  auto W = [&](const void* base, int i, size_t per) { return static_cast<const char*>(base) + i * per * es; };
+  HIPCHK(convert(bf, 0, tgt, state(0), L.nt * d, st)); HIPCHK(rec.mark("convert_in"));
+  const float qscale = kLog2e / std::sqrt(static_cast<float>(L.dh));
+  for (int i = 0; i < n; ++i) {
+    float* s = state(i);
+    float* a = saved ? at<float>(saved, SL.a) + (size_t)i * L.nt * d : at<float>(ws, L.abuf);
+    float* u = saved ? at<float>(saved, SL.u) + (size_t)i * L.nt * d : at<float>(ws, L.ubuf);
+    float* lse = saved ? at<float>(saved, SL.lse) + (size_t)i * L.nt * h : nullptr;
+    HIPCHK(gemm_generic(bf, bf, L.nh, d, d, hist, d, 0, W(w->wk, i, (size_t)d * d), d, 0, kv, 2 * d, 1.f,
+                        kEpiStore, nullptr, 0, nullptr, 0, st)); HIPCHK(rec.mark("gemm_k"));
+    HIPCHK(gemm_generic(bf, bf, L.nh, d, d, hist, d, 0, W(w->wv, i, (size_t)d * d), d, 0, kv + d, 2 * d, 1.f,
+                        kEpiStore, nullptr, 0, nullptr, 0, st)); HIPCHK(rec.mark("gemm_v"));
+    HIPCHK(gemm_generic(0, bf, L.nt, d, d, s, d, 0, W(w->wq, i, (size_t)d * d), d, 0, q, d, qscale, kEpiStore,
+                        nullptr, 0, nullptr, 0, st)); HIPCHK(rec.mark("gemm_q"));
+    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, pacc, pml, L.nt, st)); HIPCHK(rec.mark("attn"));
+    HIPCHK(merge_generic(L.dh, h, L.nt, tch, pacc, pml, a, lse, st)); HIPCHK(rec.mark("merge"));
+    HIPCHK(gemm_generic(0, bf, L.nt, d, d, a, d, 0, W(w->wo, i, (size_t)d * d), d, 0, u, d, 1.f, kEpiAddRes, s, d,
+                        nullptr, 0, st)); HIPCHK(rec.mark("gemm_o"));
+    HIPCHK(gemm_generic(0, bf, L.nt, F, d, u, d, 0, W(w->w1, i, (size_t)d * F), F, 0, hid, F, 1.f, kEpiRelu,
+                        nullptr, 0, nullptr, 0, st)); HIPCHK(rec.mark("gemm_ffn1"));
+    HIPCHK(gemm_generic(0, bf, L.nt, d, F, hid, F, 0, W(w->w2, i, (size_t)d * F), d, 0, state(i + 1), d, 1.f,
+                        kEpiAddRes, u, d, nullptr, 0, st)); HIPCHK(rec.mark("gemm_ffn2"));
+  }
+  HIPCHK(convert(0, bf, state(n), out, L.nt * d, st)); HIPCHK(rec.mark("convert_out"));
+  return STCA_OK;
+}
+
+// --------------------------------------------------------------- backward
+stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, const void* hist,
+                               const stca_weights_t* w, const void* saved, const stca_saved_layout_t& SL,
+                               const void* dout, float* dhist, float* dtgt, const stca_wgrads_t* dw, void* ws,
+                               hipStream_t st) {
+  const int d = L.d, n = L.n, F = L.F, h = L.h;
+  const int64_t nt = L.nt, nh = L.nh;
+  const size_t es = bf ? 2 : 4;
+  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  Unit* units = at<Unit>(ws, L.units);
+  int32_t* tch = at<int32_t>(ws, L.tchunks);
+  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, units, L.max_units, tch,
+                      hdr, st));
+  float* kv = at<float>(ws, L.kv32);
+  float* dkv = at<float>(ws, L.dkv32);
+  float* q = at<float>(ws, L.q32);
+  float* hid = at<float>(ws, L.hid);
+  float* pre = at<float>(ws, L.pre);
+  float* dhid = at<float>(ws, L.dhid);
+  float* ds = at<float>(ws, L.ds);
+  float* du = at<float>(ws, L.du);
+  float* da = at<float>(ws, L.da);
+  float* dq = at<float>(ws, L.dq);
+  float* ds2 = at<float>(ws, L.ds2);
+  float* dqp = at<float>(ws, L.dq_part);
+  auto W = [&](const void* base, int i, size_t per) { return static_cast<const char*>(base) + i * per * es; };
+  auto S = [&](size_t off, int i, size_t per) { return at<float>(saved, off) + (size_t)i * per; };
+  HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
+  HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
+  const float qscale = kLog2e / std::sqrt(static_cast<float>(L.dh));
+  for (int i = n - 1; i >= 0; --i) {
+    const float* s = S(SL.s, i, nt * d);
+    const float* a = S(SL.a, i, nt * d);
+    const float* u = S(SL.u, i, nt * d);
+    const float* lse = S(SL.lse, i, nt * h);
+    const void* W1 = W(w->w1, i, (size_t)d * F);
+    const void* W2 = W(w->w2, i, (size_t)d * F);
+    const void* Wo = W(w->wo, i, (size_t)d * d);
+    const void* Wq = W(w->wq, i, (size_t)d * d);
+    const void* Wk = W(w->wk, i, (size_t)d * d);
+    const void* Wv = W(w->wv, i, (size_t)d * d);
+    // s' = u + ReLU(u W1) W2
+    HIPCHK(gemm_generic(0, bf, nt, F, d, u, d, 0, W1, F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0, pre, 0, st));
+    HIPCHK(gemm_generic(0, 0, F, d, nt, hid, F, 1, ds, d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, kEpiStore,
+                        nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm_generic(0, bf, nt, F, d, ds, d, 0, W2, d, 1, dhid, F, 1.f, kEpiStore, nullptr, 0, nullptr, 0, st));
+    HIPCHK(relu_mask_mul(dhid, pre, nt * F, st));
+    HIPCHK(gemm_generic(0, 0, d, F, nt, u, d, 1, dhid, F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, kEpiStore,
+                        nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, F, dhid, F, 0, W1, F, 1, du, d, 1.f, kEpiAddRes, ds, d, nullptr, 0, st));
+    // u = s + a Wo
+    HIPCHK(gemm_generic(0, 0, d, d, nt, a, d, 1, du, d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, kEpiStore,
+                        nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, d, du, d, 0, Wo, d, 1, da, d, 1.f, kEpiStore, nullptr, 0, nullptr, 0, st));
+    // attention (K, V and q recomputed)
+    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr, 0,
+                        st));
+    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr,
+                        0, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, d, s, d, 0, Wq, d, 0, q, d, qscale, kEpiStore, nullptr, 0, nullptr, 0, st));
+    HIPCHK(fill_f32(dkv, 0.f, nh * 2 * d, st));
+    HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, a, da, lse, dqp, dkv, nt, st));
+    HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
+    // q = s Wq
+    HIPCHK(gemm_generic(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore,
+                        nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr, 0, st));
+    // K = X Wk, V = X Wv
+    HIPCHK(gemm_generic(bf, 0, d, d, nh, hist, d, 1, dkv, 2 * d, 0, dw->dwk + (size_t)i * d * d, d, 1.f,
+                        kEpiStore, nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm_generic(bf, 0, d, d, nh, hist, d, 1, dkv + d, 2 * d, 0, dw->dwv + (size_t)i * d * d, d, 1.f,
+                        kEpiStore, nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm_generic(0, bf, nh, d, d, dkv, 2 * d, 0, Wk, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0, nullptr, 1,
+                        st));
+    HIPCHK(gemm_generic(0, bf, nh, d, d, dkv + d, 2 * d, 0, Wv, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0, nullptr,
+                        1, st));
+    std::swap(ds, ds2);
+  }
+  HIPCHK(convert(0, 0, ds, dtgt, nt * d, st));
+  return STCA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int stca_path(const stca_dims_t* dims) { return path_of(dims); }
+
+size_t stca_workspace_size(const stca_dims_t* dims, const stca_batch_t* batch, int with_backward) {
+  Layout L;
+  if (!make_layout(dims, batch, with_backward, false, &L)) return 0;
+  return L.total;
+}
+
+size_t stca_saved_size(const stca_dims_t* dims, const stca_batch_t* batch) {
+  stca_saved_layout_t s;
+  if (!saved_layout(dims, batch, &s)) return 0;
+  return s.total;
+}
+
+stca_status_t stca_saved_layout(const stca_dims_t* dims, const stca_batch_t* batch, stca_saved_layout_t* layout) {
+  if (!layout) return STCA_ERR_INVALID_ARG;
+  const int p = path_of(dims);
+  if (p < 0) return static_cast<stca_status_t>(p);
+  stca_status_t st = check_batch(batch);
+  if (st != STCA_OK) return st;
+  saved_layout(dims, batch, layout);
+  return STCA_OK;
+}
+
+stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist, const void* tgt,
+                           const stca_weights_t* w, void* out, void* saved, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  stca_status_t st = check_common(dims, batch, hist, tgt, w, ws);
+  if (st != STCA_OK) return st;
+  if ((batch->n_tgt > 0 && !out) || (out && !aligned16(out)) || (saved && !aligned16(saved)))
+    return STCA_ERR_INVALID_ARG;
+  Layout L;
+  make_layout(dims, batch, 0, saved != nullptr, &L);
+  if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
+  stca_saved_layout_t SL{};
+  saved_layout(dims, batch, &SL);
+  Rec rec;
+  if (L.path == 1) return forward_fast(L, batch, hist, tgt, w, out, saved, SL, ws, stream, rec);
+  return forward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, out, saved, SL, ws, stream, rec);
+}
+
+int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
+  Layout L;
+  if (!make_layout(dims, batch, 0, false, &L)) return -1;
+  if (L.path == 1) return 1 + 6 + 1 + 1 + 2 * L.n;
+  return 1 + 1 + 8 * L.n + 1;
+}
+
+stca_status_t stca_forward_profiled(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist,
+                                    const void* tgt, const stca_weights_t* w, void* out, void* saved, void* ws,
+                                    size_t ws_bytes, hipStream_t stream, hipEvent_t* events, int n_events,
+                                    const char** labels) {
+  stca_status_t st = check_common(dims, batch, hist, tgt, w, ws);
+  if (st != STCA_OK) return st;
+  if ((batch->n_tgt > 0 && !out) || (out && !aligned16(out)) || (saved && !aligned16(saved)) || !events)
+    return STCA_ERR_INVALID_ARG;
+  Layout L;
+  make_layout(dims, batch, 0, saved != nullptr, &L);
+  if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
+  if (n_events < stca_forward_launch_count(dims, batch) + 1) return STCA_ERR_INVALID_ARG;
+  stca_saved_layout_t SL{};
+  saved_layout(dims, batch, &SL);
+  Rec rec;
+  rec.ev = events;
+  rec.n = n_events;
+  rec.labels = labels;
+  rec.st = stream;
+  if (L.path == 1) return forward_fast(L, batch, hist, tgt, w, out, saved, SL, ws, stream, rec);
+  return forward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, out, saved, SL, ws, stream, rec);
+}
+
+stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist, const void* tgt,
+                            const stca_weights_t* w, const void* saved, const void* dout, float* dhist,
+                            float* dtgt, const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
+                            hipStream_t stream) {
+  stca_status_t st = check_common(dims, batch, hist, tgt, w, ws);
+  if (st != STCA_OK) return st;
+  if (!saved || !dw || (batch->n_tgt > 0 && (!dout || !dtgt)) || (batch->n_hist > 0 && !dhist))
+    return STCA_ERR_INVALID_ARG;
+  if (!dw->dwq || !dw->dwk || !dw->dwv || !dw->dwo || !dw->dw1 || !dw->dw2) return STCA_ERR_INVALID_ARG;
+  const void* ptrs[] = {saved, dout, dhist, dtgt, dw->dwq, dw->dwk, dw->dwv, dw->dwo, dw->dw1, dw->dw2};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
+  Layout L;
+  make_layout(dims, batch, 1, true, &L);
+  if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
+  stca_saved_layout_t SL{};
+  saved_layout(dims, batch, &SL);
+  return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, w, saved, SL, dout, dhist, dtgt, dw, ws,
+                          stream);
+}
+
+stca_status_t stca_device_status(const void* ws, hipStream_t stream) {
+  if (!ws) return STCA_ERR_INVALID_ARG;
+  WsHeader h;
+  if (hipMemcpyAsync(&h, ws, sizeof(h), hipMemcpyDeviceToHost, stream) != hipSuccess) return STCA_ERR_HIP;
+  if (hipStreamSynchronize(stream) != hipSuccess) return STCA_ERR_HIP;
+  return static_cast<stca_status_t>(h.status);
+}
+
+const char* stca_status_string(stca_status_t s) {
+  switch (s) {
+    case STCA_OK: return "ok";
+    case STCA_ERR_INVALID_ARG: return "invalid argument";
+    case STCA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
+    case STCA_ERR_WORKSPACE: return "workspace or saved buffer too small";
+    case STCA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+}  // extern "C"

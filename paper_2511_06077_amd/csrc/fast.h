@@ -1,0 +1,36 @@
+// Launchers of the bf16 MFMA path (fast.hip).
+#pragma once
+
+#include "common.h"
+
+namespace stca {
+
+struct FastUpdate {
+  int mode;      // 0: s^(0) = x_t and Q^(0); 1: combine + update after `layer`
+  int layer, n_layers, F, FC;
+  int64_t n_tgt;
+  const void* tgt;
+  const int32_t* tchunks;
+  const float* part_acc;
+  const void* part_ml;
+  const float* s_in;
+  float* s_out;
+  float *save_a, *save_u, *save_lse;
+  void* out;
+  void* QN;
+  const void *WoP, *W1P, *W2P, *WqP;
+};
+
+// Repack W [n_layers][K][N] (bf16) into MFMA operand order.
+hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, hipStream_t st);
+int fast_proj_parts(int n_layers, int64_t n_blocks, int n_cu);
+// K1: history -> K/V of every layer, in the attention kernel's operand layout.
+hipError_t fast_proj(int D, const void* X, int64_t n_hist, int64_t n_blocks, const void* WkP, const void* WvP,
+                     void* KV, int n_layers, int parts, hipStream_t st);
+// K3: one layer's fused multi-target attention over the scheduled units.
+hipError_t fast_attn(int D, const Unit* units, const WsHeader* hdr, int grid, const void* QN, const void* KVl,
+                     float* part_acc, void* part_ml, int64_t n_tgt, hipStream_t st);
+// K4: combine partials, W_O, residual FFN, next queries.
+hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st);
+
+}  // namespace stca

@@ -1,0 +1,537 @@
+// bf16 MFMA path for d_h = 32 (gfx950 / CDNA4): history K/V projection (K1),
+// fused multi-target cross attention (K3) and fused target update (K4).
+//
+// All three use v_mfma_f32_32x32x16_bf16.  For that instruction lane l holds
+//   A operand: A[i = l%32][k = 8*(l/32) .. +7]           (8 bf16)
+//   B operand: B[k = 8*(l/32) .. +7][j = l%32]           (8 bf16)
+//   result   : D[i = 8*(v/4) + 4*(l/32) + v%4][j = l%32] for v = 0..15 (fp32)
+// The projected history is written in exactly the register order the
+// attention kernel's MFMAs consume, so every K/V operand fetch of the
+// attention kernel is one fully coalesced 16-byte-per-lane load and no LDS
+// round trip is needed:
+//
+//   KV[layer][block of 32 rows][head][K s=0 | K s=1 | V u=0 | V u=1][64 lanes][8 bf16]
+//
+//   K, slice s : lane (row l%32, hi = l/32) holds K[row][16s + 4hi + {0,1,2,3,8,9,10,11}]
+//   V, slice u : lane (col l%32, hi)        holds V[16u + 4hi + {0,1,2,3,8,9,10,11}][col]
+//
+// The attention kernel computes S^T = K Q^T (rows = history items, columns =
+// targets), so a lane holds 16 scores of one target and the softmax maximum is
+// an in-register reduction plus one exchange with lane l^32.  The dimension
+// order inside K's slices is a permutation of the head's 32 dimensions; the
+// queries are stored with the same permutation (QN below), which leaves q.k
+// unchanged.  The item order inside V's slices matches the order in which
+// S^T's result registers hold items, so P^T feeds the P.V MFMA as its B
+// operand straight from registers.
+//
+//   QN[target][head][32]: position 16s + 8hi + i holds dimension
+//       16s + 4hi + (i < 4 ? i : i + 4), scaled by log2(e)/sqrt(d_h)
+//
+// Weights are repacked once per call into the same operand order
+// ("packed": [N/32][K/16][64 lanes][8 bf16] with lane (n = l%32, hi) holding
+// W[16ks + 8hi .. +7][32nb + n]), which serves both as an A operand of D^T and
+// as a B operand of D.
+#include "common.h"
+#include "fast.h"
+
+namespace stca {
+
+namespace {
+
+constexpr int DH = 32;
+
+__device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 pack8(const f32x16& a, int off) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<__bf16>(a[off + i]);
+  return r;
+}
+
+__device__ __forceinline__ bf16x8 zero8() {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<__bf16>(0.f);
+  return r;
+}
+
+// ------------------------------------------------------------- repacking
+// W: [layers][K][N] bf16 row-major -> P: [layers][N/32][K/16][64][8].
+__global__ void pack_kernel(const bf16_bits* __restrict__ W, bf16x8* __restrict__ P, int K, int N,
+                            int64_t per_layer_groups) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int layer = blockIdx.y;
+  if (g >= per_layer_groups) return;
+  const int lane = g % 64;
+  const int64_t rest = g / 64;
+  const int ks = rest % (K / 16);
+  const int nb = rest / (K / 16);
+  const int n = nb * 32 + lane % 32;
+  const int k0 = ks * 16 + 8 * (lane / 32);
+  const bf16_bits* w = W + (int64_t)layer * K * N;
+  bf16x8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = __builtin_bit_cast(__bf16, w[(int64_t)(k0 + e) * N + n]);
+  P[(int64_t)layer * per_layer_groups + g] = r;
+}
+
+// ------------------------------------------------------ K1: projection
+// Grid: n_layers * parts workgroups, one wave per head.  Each wave keeps its
+// head's W_K and W_V columns in registers for the whole kernel; the
+// workgroup streams its share of 32-row history blocks through a
+// double-buffered LDS tile (one global read of X per block, shared by all
+// heads).  Workgroups on the same XCD (id % 8) are given the same history
+// rows for all layers, so the re-reads of X by the other layers hit that XCD's L2.
+template <int D>
+__global__ __launch_bounds__(64 * (D / 32)) void proj_kernel(const bf16_bits* __restrict__ X, int64_t n_hist,
+                                                             int64_t n_blocks, const bf16x8* __restrict__ WkP,
+                                                             const bf16x8* __restrict__ WvP,
+                                                             bf16x8* __restrict__ KV, int n_layers, int parts) {
+  constexpr int H = D / DH;
+  constexpr int KS = D / 16;
+  constexpr int ROW = D + 8;             // padded LDS row (bf16): conflict-free 16 B reads
+  constexpr int CHUNKS = 32 * D / 8;     // 16-byte chunks per block
+  constexpr int NT = 64 * H;
+  static_assert(CHUNKS == 2 * NT, "two chunks per thread");
+  __shared__ __attribute__((aligned(16))) bf16_bits xs[2][32 * ROW];
+
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int id = blockIdx.x;
+  const int slot = id / 8;
+  const int layer = slot % n_layers;
+  const int part = (slot / n_layers) * 8 + id % 8;
+  const int64_t bb = (int64_t)part * n_blocks / parts;
+  const int64_t be = (int64_t)(part + 1) * n_blocks / parts;
+  if (bb >= be) return;
+
+  bf16x8 wk[KS], wv[KS];
+  {
+    const bf16x8* pk = WkP + ((int64_t)(layer * H + wave) * KS) * 64 + lane;
+    const bf16x8* pv = WvP + ((int64_t)(layer * H + wave) * KS) * 64 + lane;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      wk[ks] = pk[ks * 64];
+      wv[ks] = pv[ks * 64];
+    }
+  }
+
+  auto load = [&](int64_t b, uint4 (&r)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + i * NT;
+      const int row = c / (D / 8), col8 = c % (D / 8);
+      const int64_t grow = b * 32 + row;
+      r[i] = grow < n_hist ? *reinterpret_cast<const uint4*>(X + grow * D + col8 * 8) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto stash = [&](int buf, const uint4 (&r)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + i * NT;
+      const int row = c / (D / 8), col8 = c % (D / 8);
+      *reinterpret_cast<uint4*>(&xs[buf][row * ROW + col8 * 8]) = r[i];
+    }
+  };
+
+  uint4 nxt[2];
+  load(bb, nxt);
+  stash(0, nxt);
+  __syncthreads();
+  const int trow = lane % 32, hi = lane / 32;
+  for (int64_t b = bb; b < be; ++b) {
+    const int cur = (b - bb) & 1;
+    if (b + 1 < be) load(b + 1, nxt);
+    f32x16 ak = {}, av = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 xo = *reinterpret_cast<const bf16x8*>(&xs[cur][trow * ROW + ks * 16 + hi * 8]);
+      ak = mfma(wk[ks], xo, ak);  // K^T block: rows = head dims, cols = history rows
+      av = mfma(xo, wv[ks], av);  // V block:   rows = history rows, cols = head dims
+    }
+    bf16x8* out = KV + (((int64_t)layer * n_blocks + b) * H + wave) * 4 * 64 + lane;
+    out[0] = pack8(ak, 0);
+    out[64] = pack8(ak, 8);
+    out[128] = pack8(av, 0);
+    out[192] = pack8(av, 8);
+    if (b + 1 < be) stash(cur ^ 1, nxt);
+    __syncthreads();
+  }
+}
+
+// ----------------------------------------------- K3: fused attention
+// One workgroup per unit (a request's target group x a chunk of its history
+// blocks), one wave per head.  All of the unit's targets (up to 64: two
+// 32-wide column groups) are held by every wave, so each K/V byte is read
+// from HBM once per unit whatever the number of targets.  Online softmax in
+// log2 units; the result is an unnormalised partial (acc, max, sum) per
+// (chunk, target, head), merged by the update kernel.
+template <int H, int NG>
+__device__ __forceinline__ void attn_unit(const Unit& un, const bf16x8* __restrict__ QN,
+                                          const bf16x8* __restrict__ KVl, float* __restrict__ part_acc,
+                                          float2* __restrict__ part_ml, int64_t n_tgt) {
+  constexpr int D = H * DH;
+  const int j = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tcol = lane % 32, hi = lane / 32;
+  bf16x8 qop[NG][2];
+  f32x16 O[NG];
+  float m[NG], l[NG];
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const int tt = g * 32 + tcol;
+    const bool ok = tt < un.nt;
+    const bf16x8* q = QN + ((int64_t)(un.t0 + tt) * D + j * DH) / 8;
+    qop[g][0] = ok ? q[hi] : zero8();
+    qop[g][1] = ok ? q[2 + hi] : zero8();
+    O[g] = f32x16{};
+    m[g] = -INFINITY;
+    l[g] = 0.f;
+  }
+  const bf16x8* base = KVl + (int64_t)j * 4 * 64 + lane;
+  auto ld = [&](int64_t b, bf16x8 (&r)[4]) {
+    const bf16x8* p = base + b * (H * 4 * 64);
+    r[0] = p[0];
+    r[1] = p[64];
+    r[2] = p[128];
+    r[3] = p[192];
+  };
+  bf16x8 nx[4], cu[4];
+  ld(un.b0, nx);
+  for (int b = un.b0; b < un.b1; ++b) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cu[i] = nx[i];
+    if (b + 1 < un.b1) ld(b + 1, nx);
+    const bool full = b * 32 >= un.l0 && b * 32 + 32 <= un.l1;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      f32x16 s = mfma(cu[0], qop[g][0], f32x16{});
+      s = mfma(cu[1], qop[g][1], s);
+      if (!full) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int tok = b * 32 + 8 * (v / 4) + 4 * hi + (v % 4);
+          if (tok < un.l0 || tok >= un.l1) s[v] = -INFINITY;
+        }
+      }
+      float bm = s[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) bm = fmaxf(bm, s[v]);
+      bm = fmaxf(bm, __shfl_xor(bm, 32));
+      const float mn = fmaxf(m[g], bm);
+      const float sc = exp2f(m[g] - mn);
+      m[g] = mn;
+      float ps = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        s[v] = exp2f(s[v] - mn);
+        ps += s[v];
+      }
+      l[g] = l[g] * sc + ps;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) O[g][v] *= sc;
+      O[g] = mfma(cu[2], pack8(s, 0), O[g]);
+      O[g] = mfma(cu[3], pack8(s, 8), O[g]);
+    }
+  }
+#pragma unroll
+  for (int g = 0; g < NG; ++g) {
+    const float lt = l[g] + __shfl_xor(l[g], 32);
+    const int tt = g * 32 + tcol;
+    if (tt < un.nt) {
+      const int64_t row = (int64_t)un.c * n_tgt + un.t0 + tt;
+      float* pa = part_acc + row * D + j * DH + 4 * hi;
+#pragma unroll
+      for (int gg = 0; gg < 4; ++gg)
+        *reinterpret_cast<float4*>(pa + 8 * gg) =
+            make_float4(O[g][4 * gg], O[g][4 * gg + 1], O[g][4 * gg + 2], O[g][4 * gg + 3]);
+      if (hi == 0) part_ml[row * H + j] = make_float2(m[g], lt);
+    }
+  }
+}
+
+template <int H>
+__global__ __launch_bounds__(64 * H) void attn_kernel(const Unit* __restrict__ units,
+                                                      const WsHeader* __restrict__ hdr,
+                                                      const bf16x8* __restrict__ QN,
+                                                      const bf16x8* __restrict__ KVl, float* __restrict__ part_acc,
+                                                      float2* __restrict__ part_ml, int64_t n_tgt) {
+  const int nu = hdr->n_units;
+  for (int u = blockIdx.x; u < nu; u += gridDim.x) {
+    const Unit un = units[u];
+    if (un.nt > 32)
+      attn_unit<H, 2>(un, QN, KVl, part_acc, part_ml, n_tgt);
+    else
+      attn_unit<H, 1>(un, QN, KVl, part_acc, part_ml, n_tgt);
+  }
+}
+
+// ------------------------------------------------ K4: target update
+// One workgroup per 32 targets, one wave per 32 output dimensions.
+// mode 0 (init): s^(0) = x_t, Q^(0) = x_t W_Q^0.
+// mode 1 (layer i): merge the attention partials into a, then
+//   u = s + a W_O;  s' = u + ReLU(u W_1) W_2;  Q' = s' W_Q^{i+1} (if i+1 < n).
+// Activations go through LDS as bf16 MFMA operands; the state stays fp32.
+struct UpdateArgs {
+  int mode, layer, n_layers, F, FC;  // FC: hidden columns staged in LDS at a time
+  int64_t n_tgt;
+  const bf16_bits* tgt;        // mode 0
+  const int32_t* tchunks;      // mode 1
+  const float* part_acc;       // mode 1
+  const float2* part_ml;       // mode 1
+  const float* s_in;           // mode 1: layer input state
+  float* s_out;                // next state (fp32)
+  float* save_a;               // nullable [n_tgt][D]
+  float* save_u;               // nullable
+  float* save_lse;             // nullable [n_tgt][H]
+  bf16_bits* out;              // final layer output, nullable
+  bf16x8* QN;                  // next queries
+  const bf16x8 *WoP, *W1P, *W2P, *WqP;  // packed, all layers
+};
+
+template <int D>
+__global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
+  constexpr int NW = D / 32;
+  constexpr int H = D / DH;
+  constexpr int KS = D / 16;
+  constexpr int AROW = D + 8;
+  extern __shared__ __attribute__((aligned(16))) bf16_bits lds[];
+  bf16_bits* act = lds;                 // [32][AROW]
+  bf16_bits* hid = lds + 32 * AROW;     // [32][FC + 8]
+  const int HROW = A.FC + 8;
+  const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tcol = lane % 32, hi = lane / 32;
+  const int64_t tb = (int64_t)blockIdx.x * 32;
+  const int64_t t = tb + tcol;
+  const bool tok = t < A.n_tgt;
+
+  // fp32 result of D^T tile: lane holds dims 32w + 4hi + 8g + k for g, k < 4
+  auto store_f32 = [&](float* dst, const f32x16& v) {
+    float* p = dst + t * D + 32 * w + 4 * hi;
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4*>(p + 8 * g) = make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
+  };
+  auto put_act = [&](bf16_bits* buf, int row_len, int col0, const f32x16& v) {
+    bf16_bits* p = buf + tcol * row_len + col0 + 4 * hi;
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      uint2 pk;
+      pk.x = (uint32_t)from_f32<bf16_bits>(v[4 * g]) | ((uint32_t)from_f32<bf16_bits>(v[4 * g + 1]) << 16);
+      pk.y = (uint32_t)from_f32<bf16_bits>(v[4 * g + 2]) | ((uint32_t)from_f32<bf16_bits>(v[4 * g + 3]) << 16);
+      *reinterpret_cast<uint2*>(p + 8 * g) = pk;
+    }
+  };
+  auto gemm = [&](const bf16x8* Wp, const bf16_bits* src, int src_row, int ksteps) {
+    f32x16 acc = {};
+    const bf16_bits* b = src + tcol * src_row + 8 * hi;
+#pragma unroll 4
+    for (int ks = 0; ks < ksteps; ++ks)
+      acc = mfma(Wp[ks * 64 + lane], *reinterpret_cast<const bf16x8*>(b + ks * 16), acc);
+    return acc;
+  };
+
+  f32x16 s_next;
+  if (A.mode == 0) {
+    // stage x_t rows into LDS and write s^(0)
+    for (int c = threadIdx.x; c < 32 * D / 8; c += 64 * NW) {
+      const int row = c / (D / 8), col8 = c % (D / 8);
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (tb + row < A.n_tgt) v = *reinterpret_cast<const uint4*>(A.tgt + (tb + row) * D + col8 * 8);
+      *reinterpret_cast<uint4*>(act + row * AROW + col8 * 8) = v;
+      if (tb + row < A.n_tgt) {
+        const bf16_bits* e = reinterpret_cast<const bf16_bits*>(&v);
+        float* so = A.s_out + (tb + row) * D + col8 * 8;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) so[i] = __uint_as_float((uint32_t)e[i] << 16);
+      }
+    }
+    __syncthreads();
+  } else {
+    // merge partials: one thread per (target, head, quarter of the head)
+    for (int it = threadIdx.x; it < 32 * H * 4; it += 64 * NW) {
+      const int row = it / (H * 4), j = (it / 4) % H, qq = it % 4;
+      const int64_t tt = tb + row;
+      float av[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      if (tt < A.n_tgt) {
+        const int nch = A.tchunks[tt];
+        float M = -INFINITY;
+        for (int c = 0; c < nch; ++c) M = fmaxf(M, A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j].x);
+        float L = 0.f;
+        for (int c = 0; c < nch; ++c) {
+          const float2 ml = A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j];
+          const float wc = exp2f(ml.x - M);
+          L += wc * ml.y;
+          const float4* pa =
+              reinterpret_cast<const float4*>(A.part_acc + ((int64_t)c * A.n_tgt + tt) * D + j * DH + qq * 8);
+          const float4 x0 = pa[0], x1 = pa[1];
+          av[0] += wc * x0.x; av[1] += wc * x0.y; av[2] += wc * x0.z; av[3] += wc * x0.w;
+          av[4] += wc * x1.x; av[5] += wc * x1.y; av[6] += wc * x1.z; av[7] += wc * x1.w;
+        }
+        const float inv = 1.f / L;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) av[i] *= inv;
+        if (A.save_a) {
+          float4* sa = reinterpret_cast<float4*>(A.save_a + tt * D + j * DH + qq * 8);
+          sa[0] = make_float4(av[0], av[1], av[2], av[3]);
+          sa[1] = make_float4(av[4], av[5], av[6], av[7]);
+        }
+        if (A.save_lse && qq == 0) A.save_lse[tt * H + j] = (M + log2f(L)) * kLn2;
+      }
+      bf16_bits* p = act + row * AROW + j * DH + qq * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) p[i] = from_f32<bf16_bits>(av[i]);
+    }
+    __syncthreads();
+    const int KSF = A.F / 16;
+    // u = s + a W_O
+    f32x16 u = gemm(A.WoP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, AROW, KS);
+    if (tok) {
+      const float* sp = A.s_in + t * D + 32 * w + 4 * hi;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const float4 sv = *reinterpret_cast<const float4*>(sp + 8 * g);
+        u[4 * g] += sv.x; u[4 * g + 1] += sv.y; u[4 * g + 2] += sv.z; u[4 * g + 3] += sv.w;
+      }
+      if (A.save_u) store_f32(A.save_u, u);
+    }
+    __syncthreads();
+    put_act(act, AROW, 32 * w, u);
+    __syncthreads();
+    // s' = u + ReLU(u W_1) W_2, the hidden layer taken FC columns at a time
+    s_next = u;
+    for (int c0 = 0; c0 < A.F; c0 += A.FC) {
+      for (int nb = w; nb < A.FC / 32; nb += NW) {
+        f32x16 h = gemm(A.W1P + ((int64_t)A.layer * (A.F / 32) + c0 / 32 + nb) * KS * 64, act, AROW, KS);
+#pragma unroll
+        for (int v = 0; v < 16; ++v) h[v] = fmaxf(h[v], 0.f);
+        put_act(hid, HROW, 32 * nb, h);
+      }
+      __syncthreads();
+      const f32x16 y = gemm(A.W2P + ((int64_t)(A.layer * NW + w) * KSF + c0 / 16) * 64, hid, HROW, A.FC / 16);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) s_next[v] += y[v];
+      __syncthreads();
+    }
+    if (tok) {
+      if (A.layer + 1 < A.n_layers) {
+        store_f32(A.s_out, s_next);
+      } else {
+        bf16_bits* p = A.out + t * D + 32 * w + 4 * hi;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          uint2 pk;
+          pk.x = (uint32_t)from_f32<bf16_bits>(s_next[4 * g]) |
+                 ((uint32_t)from_f32<bf16_bits>(s_next[4 * g + 1]) << 16);
+          pk.y = (uint32_t)from_f32<bf16_bits>(s_next[4 * g + 2]) |
+                 ((uint32_t)from_f32<bf16_bits>(s_next[4 * g + 3]) << 16);
+          *reinterpret_cast<uint2*>(p + 8 * g) = pk;
+        }
+      }
+    }
+    if (A.layer + 1 >= A.n_layers) return;
+    put_act(act, AROW, 32 * w, s_next);  // act (u) was last read before the previous barrier
+    __syncthreads();
+  }
+  // next queries: Q = s W_Q^{next}, scaled into log2 units, permuted (QN layout)
+  const int ql = A.mode == 0 ? 0 : A.layer + 1;
+  f32x16 q = gemm(A.WqP + ((int64_t)(ql * NW + w) * KS) * 64, act, AROW, KS);
+  const float qs = kLog2e * 0.17677669529663687f;  // log2(e) / sqrt(32)
+#pragma unroll
+  for (int v = 0; v < 16; ++v) q[v] *= qs;
+  if (tok) {
+    bf16x8* qn = A.QN + (t * D + 32 * w) / 8;
+    qn[hi] = pack8(q, 0);
+    qn[2 + hi] = pack8(q, 8);
+  }
+}
+
+}  // namespace
+
+// ------------------------------------------------------------ launchers
+hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, hipStream_t st) {
+  const int64_t groups = (int64_t)(N / 32) * (K / 16) * 64;
+  dim3 g(static_cast<unsigned>(ceil_div(groups, 256)), n_layers);
+  hipLaunchKernelGGL(pack_kernel, g, dim3(256), 0, st, (const bf16_bits*)W, (bf16x8*)P, K, N, groups);
+  return hipGetLastError();
+}
+
+int fast_proj_parts(int n_layers, int64_t n_blocks, int n_cu) {
+  // workgroups = n_layers * parts; parts a multiple of 8 (XCD grouping), about
+  // one resident workgroup per CU, and at least one block per part
+  int64_t parts = round_up(ceil_div(n_cu, n_layers), 8);
+  while (parts > 8 && parts > n_blocks) parts -= 8;
+  return static_cast<int>(parts);
+}
+
+hipError_t fast_proj(int D, const void* X, int64_t n_hist, int64_t n_blocks, const void* WkP, const void* WvP,
+                     void* KV, int n_layers, int parts, hipStream_t st) {
+  dim3 g(static_cast<unsigned>(n_layers * parts));
+#define STCA_PROJ(DD)                                                                                       \
+  hipLaunchKernelGGL(proj_kernel<DD>, g, dim3(64 * (DD / 32)), 0, st, (const bf16_bits*)X, n_hist, n_blocks, \
+                     (const bf16x8*)WkP, (const bf16x8*)WvP, (bf16x8*)KV, n_layers, parts)
+  switch (D) {
+    case 64: STCA_PROJ(64); break;
+    case 128: STCA_PROJ(128); break;
+    case 256: STCA_PROJ(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_PROJ
+  return hipGetLastError();
+}
+
+hipError_t fast_attn(int D, const Unit* units, const WsHeader* hdr, int grid, const void* QN, const void* KVl,
+                     float* part_acc, void* part_ml, int64_t n_tgt, hipStream_t st) {
+  if (grid == 0) return hipSuccess;
+#define STCA_ATTN(HH)                                                                                \
+  hipLaunchKernelGGL(attn_kernel<HH>, dim3(grid), dim3(64 * HH), 0, st, units, hdr, (const bf16x8*)QN, \
+                     (const bf16x8*)KVl, part_acc, (float2*)part_ml, n_tgt)
+  switch (D) {
+    case 64: STCA_ATTN(2); break;
+    case 128: STCA_ATTN(4); break;
+    case 256: STCA_ATTN(8); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_ATTN
+  return hipGetLastError();
+}
+
+hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st) {
+  UpdateArgs A;
+  A.mode = f.mode;
+  A.layer = f.layer;
+  A.n_layers = f.n_layers;
+  A.F = f.F;
+  A.FC = f.FC;
+  A.n_tgt = f.n_tgt;
+  A.tgt = (const bf16_bits*)f.tgt;
+  A.tchunks = f.tchunks;
+  A.part_acc = f.part_acc;
+  A.part_ml = (const float2*)f.part_ml;
+  A.s_in = f.s_in;
+  A.s_out = f.s_out;
+  A.save_a = f.save_a;
+  A.save_u = f.save_u;
+  A.save_lse = f.save_lse;
+  A.out = (bf16_bits*)f.out;
+  A.QN = (bf16x8*)f.QN;
+  A.WoP = (const bf16x8*)f.WoP;
+  A.W1P = (const bf16x8*)f.W1P;
+  A.W2P = (const bf16x8*)f.W2P;
+  A.WqP = (const bf16x8*)f.WqP;
+  if (f.n_tgt == 0) return hipSuccess;
+  dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
+  const size_t lds = (size_t)32 * (D + 8) * 2 + (f.mode == 0 ? 0 : (size_t)32 * (f.FC + 8) * 2);
+#define STCA_UPD(DD) hipLaunchKernelGGL(update_kernel<DD>, g, dim3(64 * (DD / 32)), lds, st, A)
+  switch (D) {
+    case 64: STCA_UPD(64); break;
+    case 128: STCA_UPD(128); break;
+    case 256: STCA_UPD(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_UPD
+  return hipGetLastError();
+}
+
+}  // namespace stca

@@ -1,0 +1,390 @@
+// Generic fp32-arithmetic kernels: any supported head width, fp32 or bf16
+// storage.  They serve the fp32 storage type (whose tolerance bf16 MFMA
+// arithmetic cannot meet) and the backward pass's small target-side GEMMs.
+// Plain SIMT code with LDS tiling; the bf16 hot path has its own MFMA kernels.
+#include "common.h"
+#include "internal.h"
+
+namespace stca {
+
+namespace {
+
+template <typename T>
+__device__ __forceinline__ float ld(const T* p, int64_t i) {
+  return to_f32(p[i]);
+}
+
+// ---------------------------------------------------------------- GEMM
+constexpr int GT = 64;  // output tile edge
+constexpr int GK = 16;  // k step
+
+template <typename TA, typename TB>
+__global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA* __restrict__ A,
+                                                   int64_t lda, int transA, const TB* __restrict__ B,
+                                                   int64_t ldb, int transB, float* __restrict__ C,
+                                                   int64_t ldc, float alpha, int epi,
+                                                   const float* __restrict__ R, int64_t ldr,
+                                                   float* __restrict__ C2, int accumulate) {
+  __shared__ float As[GK][GT + 4];
+  __shared__ float Bs[GK][GT + 4];
+  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += GK) {
+    for (int e = threadIdx.x; e < GT * GK; e += 256) {
+      // A tile: rows m0..m0+63, cols k0..k0+15, stored As[k][m]
+      int mm = e % GT, kk = e / GT;
+      int gm = m0 + mm, gk = k0 + kk;
+      float v = 0.f;
+      if (gm < M && gk < K) v = transA ? ld(A, (int64_t)gk * lda + gm) : ld(A, (int64_t)gm * lda + gk);
+      As[kk][mm] = v;
+      int nn = e % GT;
+      int gn = n0 + nn;
+      float w = 0.f;
+      if (gn < N && gk < K) w = transB ? ld(B, (int64_t)gn * ldb + gk) : ld(B, (int64_t)gk * ldb + gn);
+      Bs[kk][nn] = w;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < GK; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int gm = m0 + ty * 4 + i;
+    if (gm >= M) continue;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int gn = n0 + tx * 4 + j;
+      if (gn >= N) continue;
+      float v = alpha * acc[i][j];
+      float* c = C + (int64_t)gm * ldc + gn;
+      if (epi == kEpiAddRes) v += R[(int64_t)gm * ldr + gn];
+      if (epi == kEpiRelu) {
+        if (C2) C2[(int64_t)gm * ldc + gn] = v;
+        v = fmaxf(v, 0.f);
+      }
+      *c = accumulate ? *c + v : v;
+    }
+  }
+}
+
+// ------------------------------------------------------------ attention
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
+  return v;
+}
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+// One workgroup per (unit, head); each wave takes targets w, w+4, ...; lanes
+// stride over the unit's history rows with an online softmax, then merge.
+// Q is pre-scaled by log2(e)/sqrt(d_h), so scores are in log2 units.
+template <int DH>
+__global__ __launch_bounds__(256) void attn_generic_kernel(const Unit* __restrict__ units,
+                                                           const WsHeader* __restrict__ hdr,
+                                                           const float* __restrict__ Q,
+                                                           const float* __restrict__ KV, int d,
+                                                           float* __restrict__ part_acc,
+                                                           float* __restrict__ part_ml, int64_t n_tgt,
+                                                           int n_heads) {
+  const int u = blockIdx.x;
+  if (u >= hdr->n_units) return;
+  const Unit un = units[u];
+  const int j = blockIdx.y;
+  const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
+  const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
+  for (int tt = w; tt < un.nt; tt += 4) {
+    const int64_t t = un.t0 + tt;
+    float q[DH];
+#pragma unroll
+    for (int e = 0; e < DH; ++e) q[e] = Q[t * d + j * DH + e];
+    float m = -INFINITY, l = 0.f, acc[DH];
+#pragma unroll
+    for (int e = 0; e < DH; ++e) acc[e] = 0.f;
+    for (int tok = lo + lane; tok < hi; tok += 64) {
+      const float* krow = KV + (int64_t)tok * 2 * d + j * DH;
+      const float* vrow = krow + d;
+      float s = 0.f;
+#pragma unroll
+      for (int e = 0; e < DH; ++e) s = fmaf(q[e], krow[e], s);
+      const float mn = fmaxf(m, s);
+      const float sc = exp2f(m - mn);
+      const float p = exp2f(s - mn);
+      l = l * sc + p;
+#pragma unroll
+      for (int e = 0; e < DH; ++e) acc[e] = fmaf(p, vrow[e], acc[e] * sc);
+      m = mn;
+    }
+    const float M = wave_max(m);
+    const float f = (m == -INFINITY) ? 0.f : exp2f(m - M);
+    const float L = wave_sum(l * f);
+    float* pa = part_acc + ((int64_t)un.c * n_tgt + t) * d + j * DH;
+#pragma unroll
+    for (int e = 0; e < DH; ++e) {
+      const float v = wave_sum(acc[e] * f);
+      if (lane == 0) pa[e] = v;
+    }
+    if (lane == 0) {
+      float* pm = part_ml + (((int64_t)un.c * n_tgt + t) * n_heads + j) * 2;
+      pm[0] = M;
+      pm[1] = L;
+    }
+  }
+}
+
+// Merge the per-chunk partial results of every (target, head).
+__global__ void merge_generic_kernel(int dh, int n_heads, int64_t n_tgt, const int32_t* __restrict__ tchunks,
+                                     const float* __restrict__ part_acc, const float* __restrict__ part_ml,
+                                     float* __restrict__ a, float* __restrict__ lse) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n_tgt * n_heads) return;
+  const int64_t t = idx / n_heads;
+  const int j = idx % n_heads;
+  const int d = dh * n_heads;
+  const int nch = tchunks[t];
+  float M = -INFINITY;
+  for (int c = 0; c < nch; ++c) M = fmaxf(M, part_ml[(((int64_t)c * n_tgt + t) * n_heads + j) * 2]);
+  float L = 0.f;
+  for (int c = 0; c < nch; ++c) {
+    const float* pm = part_ml + (((int64_t)c * n_tgt + t) * n_heads + j) * 2;
+    L += exp2f(pm[0] - M) * pm[1];
+  }
+  const float inv = 1.f / L;
+  for (int e = 0; e < dh; ++e) {
+    float v = 0.f;
+    for (int c = 0; c < nch; ++c) {
+      const float wc = exp2f(part_ml[(((int64_t)c * n_tgt + t) * n_heads + j) * 2] - M);
+      v += wc * part_acc[((int64_t)c * n_tgt + t) * d + j * dh + e];
+    }
+    a[t * d + j * dh + e] = v * inv;
+  }
+  if (lse) lse[t * n_heads + j] = (M + log2f(L)) * kLn2;
+}
+
+// ------------------------------------------------- attention backward
+// One workgroup per (unit, head).  Lanes own history rows (a 64-row tile at a
+// time) and accumulate dK, dV over all of the unit's targets; dq of each
+// target is reduced over the wave and accumulated in LDS, then written as this
+// chunk's partial.  dK/dV of a row can receive contributions from several
+// target groups of the same request, so they are added atomically.
+template <int DH>
+__global__ __launch_bounds__(256) void attn_bwd_generic_kernel(
+    const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const float* __restrict__ Q,
+    const float* __restrict__ KV, int d, const float* __restrict__ a, const float* __restrict__ da,
+    const float* __restrict__ lse, float* __restrict__ dq_part, float* __restrict__ dKV, int64_t n_tgt,
+    int n_heads) {
+  __shared__ float dq_s[kTargetGroup][DH];
+  __shared__ float Dt_s[kTargetGroup];
+  const int u = blockIdx.x;
+  if (u >= hdr->n_units) return;
+  const Unit un = units[u];
+  const int j = blockIdx.y;
+  const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
+  const float scale = 1.f / sqrtf((float)DH);  // Q holds q * log2(e) / sqrt(d_h)
+  for (int e = threadIdx.x; e < kTargetGroup * DH; e += 256) dq_s[e / DH][e % DH] = 0.f;
+  for (int tt = threadIdx.x; tt < un.nt; tt += 256) {
+    const int64_t t = un.t0 + tt;
+    float D = 0.f;
+    for (int e = 0; e < DH; ++e) D += da[t * d + j * DH + e] * a[t * d + j * DH + e];
+    Dt_s[tt] = D;
+  }
+  __syncthreads();
+  const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
+  for (int base = lo + w * 64; base < hi; base += 256) {
+    const int tok = base + lane;
+    const bool on = tok < hi;
+    float k[DH], v[DH], dk[DH], dv[DH];
+#pragma unroll
+    for (int e = 0; e < DH; ++e) {
+      k[e] = on ? KV[(int64_t)tok * 2 * d + j * DH + e] : 0.f;
+      v[e] = on ? KV[(int64_t)tok * 2 * d + d + j * DH + e] : 0.f;
+      dk[e] = 0.f;
+      dv[e] = 0.f;
+    }
+    for (int tt = 0; tt < un.nt; ++tt) {
+      const int64_t t = un.t0 + tt;
+      const float* q = Q + t * d + j * DH;
+      const float* dat = da + t * d + j * DH;
+      float s = 0.f, dp = 0.f;
+#pragma unroll
+      for (int e = 0; e < DH; ++e) {
+        s = fmaf(q[e], k[e], s);
+        dp = fmaf(dat[e], v[e], dp);
+      }
+      const float p = on ? exp2f(s - lse[t * n_heads + j] * kLog2e) : 0.f;
+      const float de = p * (dp - Dt_s[tt]);
+#pragma unroll
+      for (int e = 0; e < DH; ++e) {
+        dv[e] = fmaf(p, dat[e], dv[e]);
+        // q holds log2(e)/sqrt(d_h) times the true query, so de*q/sqrt(d_h)
+        // of the true query is de*q*ln(2): the ln(2) is applied once below
+        dk[e] = fmaf(de, q[e], dk[e]);
+      }
+#pragma unroll
+      for (int e = 0; e < DH; ++e) {
+        const float g = wave_sum(de * k[e]);
+        if (lane == 0) atomicAdd(&dq_s[tt][e], g * scale);
+      }
+    }
+    if (on) {
+#pragma unroll
+      for (int e = 0; e < DH; ++e) {
+        atomicAdd(&dKV[(int64_t)tok * 2 * d + j * DH + e], dk[e] * kLn2);
+        atomicAdd(&dKV[(int64_t)tok * 2 * d + d + j * DH + e], dv[e]);
+      }
+    }
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < un.nt * DH; e += 256) {
+    const int tt = e / DH, ee = e % DH;
+    dq_part[((int64_t)un.c * n_tgt + un.t0 + tt) * d + j * DH + ee] = dq_s[tt][ee];
+  }
+}
+
+__global__ void reduce_chunks_kernel(int64_t n_tgt, int d, const int32_t* __restrict__ tchunks,
+                                     const float* __restrict__ part, float* __restrict__ out, float scale) {
+  const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (idx >= n_tgt * d) return;
+  const int64_t t = idx / d;
+  float v = 0.f;
+  for (int c = 0; c < tchunks[t]; ++c) v += part[(int64_t)c * n_tgt * d + idx];
+  out[idx] = v * scale;
+}
+
+__global__ void relu_mask_kernel(float* __restrict__ dh, const float* __restrict__ pre, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n && !(pre[i] > 0.f)) dh[i] = 0.f;
+}
+
+template <typename S, typename D>
+__global__ void convert_kernel(const S* __restrict__ src, D* __restrict__ dst, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = from_f32<D>(to_f32(src[i]));
+}
+
+__global__ void fill_kernel(float* __restrict__ dst, float v, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = v;
+}
+
+inline dim3 grid1(int64_t n, int b) { return dim3(static_cast<unsigned>(ceil_div(n, b))); }
+
+}  // namespace
+
+hipError_t gemm_generic(int a_bf16, int b_bf16, int M, int N, int K, const void* A, int64_t lda,
+                        int transA, const void* B, int64_t ldb, int transB, float* C, int64_t ldc,
+                        float alpha, GemmEpi epi, const float* R, int64_t ldr, float* C2,
+                        int accumulate, hipStream_t st) {
+  if (M == 0 || N == 0) return hipSuccess;
+  dim3 g(static_cast<unsigned>(ceil_div(N, GT)), static_cast<unsigned>(ceil_div(M, GT)));
+#define STCA_GEMM(TA, TB)                                                                          \
+  hipLaunchKernelGGL((gemm_kernel<TA, TB>), g, dim3(256), 0, st, M, N, K, (const TA*)A, lda, transA, \
+                     (const TB*)B, ldb, transB, C, ldc, alpha, (int)epi, R, ldr, C2, accumulate)
+  if (a_bf16 && b_bf16) STCA_GEMM(bf16_bits, bf16_bits);
+  else if (a_bf16) STCA_GEMM(bf16_bits, float);
+  else if (b_bf16) STCA_GEMM(float, bf16_bits);
+  else STCA_GEMM(float, float);
+#undef STCA_GEMM
+  return hipGetLastError();
+}
+
+hipError_t attn_generic(int d_head, int n_heads, const Unit* units, int64_t max_units, const WsHeader* hdr,
+                        const float* Q, const float* KV, int d, float* part_acc, float* part_ml,
+                        int64_t n_tgt, hipStream_t st) {
+  if (max_units == 0) return hipSuccess;
+  dim3 g(static_cast<unsigned>(max_units), n_heads);
+#define STCA_ATT(DH)                                                                                    \
+  hipLaunchKernelGGL(attn_generic_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, part_acc, part_ml, \
+                     n_tgt, n_heads)
+  switch (d_head) {
+    case 8: STCA_ATT(8); break;
+    case 16: STCA_ATT(16); break;
+    case 32: STCA_ATT(32); break;
+    case 64: STCA_ATT(64); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_ATT
+  return hipGetLastError();
+}
+
+hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* tchunks, const float* part_acc,
+                         const float* part_ml, float* a, float* lse, hipStream_t st) {
+  if (n_tgt == 0) return hipSuccess;
+  hipLaunchKernelGGL(merge_generic_kernel, grid1(n_tgt * n_heads, 256), dim3(256), 0, st, d_head, n_heads,
+                     n_tgt, tchunks, part_acc, part_ml, a, lse);
+  return hipGetLastError();
+}
+
+hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
+                            const WsHeader* hdr, const float* Q, const float* KV, int d, const float* a,
+                            const float* da, const float* lse, float* dq_part, float* dKV, int64_t n_tgt,
+                            hipStream_t st) {
+  if (max_units == 0) return hipSuccess;
+  dim3 g(static_cast<unsigned>(max_units), n_heads);
+#define STCA_ATTB(DH)                                                                                 \
+  hipLaunchKernelGGL(attn_bwd_generic_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, \
+                     dq_part, dKV, n_tgt, n_heads)
+  switch (d_head) {
+    case 8: STCA_ATTB(8); break;
+    case 16: STCA_ATTB(16); break;
+    case 32: STCA_ATTB(32); break;
+    case 64: STCA_ATTB(64); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_ATTB
+  return hipGetLastError();
+}
+
+hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const float* part, float* out,
+                         float scale, hipStream_t st) {
+  if (n_tgt == 0) return hipSuccess;
+  hipLaunchKernelGGL(reduce_chunks_kernel, grid1(n_tgt * d, 256), dim3(256), 0, st, n_tgt, d, tchunks, part,
+                     out, scale);
+  return hipGetLastError();
+}
+
+hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(relu_mask_kernel, grid1(n, 256), dim3(256), 0, st, dh, pre, n);
+  return hipGetLastError();
+}
+
+hipError_t convert(int src_bf16, int dst_bf16, const void* src, void* dst, int64_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  dim3 g = grid1(n, 256);
+  if (src_bf16 && dst_bf16)
+    hipLaunchKernelGGL((convert_kernel<bf16_bits, bf16_bits>), g, dim3(256), 0, st, (const bf16_bits*)src,
+                       (bf16_bits*)dst, n);
+  else if (src_bf16)
+    hipLaunchKernelGGL((convert_kernel<bf16_bits, float>), g, dim3(256), 0, st, (const bf16_bits*)src,
+                       (float*)dst, n);
+  else if (dst_bf16)
+    hipLaunchKernelGGL((convert_kernel<float, bf16_bits>), g, dim3(256), 0, st, (const float*)src,
+                       (bf16_bits*)dst, n);
+  else
+    hipLaunchKernelGGL((convert_kernel<float, float>), g, dim3(256), 0, st, (const float*)src, (float*)dst, n);
+  return hipGetLastError();
+}
+
+hipError_t fill_f32(float* dst, float v, int64_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_kernel, grid1(n, 256), dim3(256), 0, st, dst, v, n);
+  return hipGetLastError();
+}
+
+}  // namespace stca

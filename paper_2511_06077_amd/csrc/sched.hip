@@ -1,0 +1,140 @@
+// Varlen scheduler: device offsets -> attention work units.
+//
+// The ragged batch is packed without padding and segmented by per-request
+// offsets (App. A.4, index-based ragged target attention).  Each request's
+// history rows are covered by whole 32-row blocks of the packed history
+// ([floor(h0/32), ceil(h1/32))); the blocks are cut into at most kMaxChunks
+// chunks of about `chunk_blocks` blocks, and the request's targets into groups
+// of kTargetGroup.  One unit = (target group, chunk).  Every target's chunk
+// count is recorded so the combine step knows how many partial results to merge.
+//
+// One workgroup of 1024 threads; each thread owns a contiguous run of requests.
+// Invalid segments produce no units and set the workspace status, so no later
+// kernel reads outside the buffers whatever the offsets hold.
+#include "common.h"
+#include "internal.h"
+
+namespace stca {
+
+namespace {
+
+constexpr int kSchedThreads = 1024;
+
+struct ReqPlan {
+  int32_t h0, h1, t0, t1, nch, cb, ng, bl;
+  bool ok;
+};
+
+__device__ ReqPlan plan_request(const int32_t* hoff, const int32_t* toff, int r, int64_t n_hist,
+                                int64_t n_tgt, int chunk_blocks) {
+  ReqPlan p{};
+  p.h0 = hoff[r];
+  p.h1 = hoff[r + 1];
+  p.t0 = toff[r];
+  p.t1 = toff[r + 1];
+  p.ok = p.h0 >= 0 && p.h0 <= p.h1 && p.h1 <= n_hist && p.t0 >= 0 && p.t0 <= p.t1 && p.t1 <= n_tgt &&
+         (p.t1 == p.t0 || p.h1 > p.h0);
+  p.nch = 0;
+  p.ng = 0;
+  if (!p.ok || p.t1 == p.t0) return p;
+  p.bl = p.h0 / kBlockTokens;
+  const int32_t bh = static_cast<int32_t>(ceil_div(p.h1, kBlockTokens));
+  const int32_t nb = bh - p.bl;
+  int32_t nch = static_cast<int32_t>(ceil_div(nb, chunk_blocks));
+  nch = nch < 1 ? 1 : (nch > kMaxChunks ? kMaxChunks : nch);
+  p.cb = static_cast<int32_t>(ceil_div(nb, nch));
+  p.nch = static_cast<int32_t>(ceil_div(nb, p.cb));  // no empty chunk
+  p.ng = static_cast<int32_t>(ceil_div(p.t1 - p.t0, kTargetGroup));
+  return p;
+}
+
+__global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __restrict__ hoff,
+                                                              const int32_t* __restrict__ toff, int R,
+                                                              int64_t n_hist, int64_t n_tgt,
+                                                              int chunk_blocks, Unit* __restrict__ units,
+                                                              int64_t max_units,
+                                                              int32_t* __restrict__ tchunks,
+                                                              WsHeader* __restrict__ hdr) {
+  __shared__ int64_t scan[kSchedThreads];
+  __shared__ int bad;
+  const int tid = threadIdx.x;
+  if (tid == 0) bad = (hoff[0] != 0 || toff[0] != 0 || hoff[R] != n_hist || toff[R] != n_tgt) ? 1 : 0;
+  for (int64_t t = tid; t < n_tgt; t += kSchedThreads) tchunks[t] = 0;
+  __syncthreads();
+
+  const int per = static_cast<int>(ceil_div(R, kSchedThreads));
+  const int rb = tid * per;
+  const int re = min(R, rb + per);
+  int64_t mine = 0;
+  bool any_bad = false;
+  for (int r = rb; r < re; ++r) {
+    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks);
+    any_bad |= !p.ok;
+    mine += static_cast<int64_t>(p.nch) * p.ng;
+  }
+  if (any_bad) atomicOr(&bad, 1);
+  // inclusive scan over threads (Hillis-Steele; the request count per thread
+  // is small, so this is not on any critical path)
+  scan[tid] = mine;
+  __syncthreads();
+  for (int off = 1; off < kSchedThreads; off <<= 1) {
+    int64_t v = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
+  }
+  int64_t u = scan[tid] - mine;
+  const int64_t total = scan[kSchedThreads - 1];
+  for (int r = rb; r < re; ++r) {
+    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks);
+    if (p.nch == 0) continue;
+    const int32_t bh = static_cast<int32_t>(ceil_div(p.h1, kBlockTokens));
+    for (int g = 0; g < p.ng; ++g) {
+      for (int c = 0; c < p.nch; ++c, ++u) {
+        if (u >= max_units) continue;
+        Unit un;
+        un.r = r;
+        un.t0 = p.t0 + g * kTargetGroup;
+        un.nt = min(kTargetGroup, p.t1 - un.t0);
+        un.c = c;
+        un.b0 = p.bl + c * p.cb;
+        un.b1 = min(un.b0 + p.cb, bh);
+        un.l0 = p.h0;
+        un.l1 = p.h1;
+        units[u] = un;
+      }
+    }
+    for (int t = p.t0; t < p.t1; ++t) tchunks[t] = p.nch;
+  }
+  if (tid == 0) {
+    hdr->n_units = static_cast<int32_t>(total < max_units ? total : max_units);
+    hdr->status = (bad || total > max_units) ? STCA_ERR_INVALID_ARG : STCA_OK;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
+                        int chunk_blocks, Unit* units, int64_t max_units, int32_t* tchunks,
+                        WsHeader* hdr, hipStream_t st) {
+  hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(kSchedThreads), 0, st, hoff, toff, R, n_hist, n_tgt,
+                     chunk_blocks, units, max_units, tchunks, hdr);
+  return hipGetLastError();
+}
+
+// Host mirror of plan_request for exact unit counts when host offsets exist.
+int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks) {
+  int64_t n = 0;
+  for (int r = 0; r < R; ++r) {
+    const int64_t h0 = hoff[r], h1 = hoff[r + 1], t0 = toff[r], t1 = toff[r + 1];
+    if (t1 == t0) continue;
+    const int64_t nb = ceil_div(h1, kBlockTokens) - h0 / kBlockTokens;
+    int64_t nch = ceil_div(nb, chunk_blocks);
+    nch = nch < 1 ? 1 : (nch > kMaxChunks ? kMaxChunks : nch);
+    const int64_t cb = ceil_div(nb, nch);
+    n += ceil_div(nb, cb) * ceil_div(t1 - t0, kTargetGroup);
+  }
+  return n;
+}
+
+}  // namespace stca

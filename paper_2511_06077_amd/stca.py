@@ -1,0 +1,228 @@
+"""Thin ctypes binding of libstca.so (the C ABI in include/stca.h).
+
+Argument marshalling only: torch tensors supply device memory and the stream;
+every step of the computation runs in the library's HIP kernels.  There is no
+fallback: if the library is missing, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(PKG, "libstca.so")
+
+STCA_OK, STCA_ERR_INVALID_ARG, STCA_ERR_UNSUPPORTED, STCA_ERR_WORKSPACE, STCA_ERR_HIP = 0, -1, -2, -3, -4
+STCA_F32, STCA_BF16 = 0, 1
+
+EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca_forward", "stca_backward",
+            "stca_device_status", "stca_status_string", "stca_path", "stca_forward_launch_count",
+            "stca_forward_profiled")
+
+
+class stca_dims_t(ctypes.Structure):
+    _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_layers", ctypes.c_int32),
+                ("ffn_hidden", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class stca_batch_t(ctypes.Structure):
+    _fields_ = [("n_requests", ctypes.c_int32), ("n_hist", ctypes.c_int64), ("n_tgt", ctypes.c_int64),
+                ("hist_off", ctypes.c_void_p), ("tgt_off", ctypes.c_void_p),
+                ("hist_off_host", ctypes.c_void_p), ("tgt_off_host", ctypes.c_void_p)]
+
+
+class stca_weights_t(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_void_p) for k in ("wq", "wk", "wv", "wo", "w1", "w2")]
+
+
+class stca_wgrads_t(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_void_p) for k in ("dwq", "dwk", "dwv", "dwo", "dw1", "dw2")]
+
+
+class stca_saved_layout_t(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_size_t) for k in ("s", "a", "u", "lse", "kv", "total")]
+
+
+class StcaError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        super().__init__(f"{where}: {status_string(status)} ({status})")
+        self.status = status
+
+
+_lib = None
+
+
+def lib():
+    """Load libstca.so (built in-tree by paper_2511_06077_amd.build)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_2511_06077_amd.build`")
+        # torch ships its own HIP runtime (soname libamdhip64.so.7, needed by
+        # torch as libamdhip64.so): load it first so that libstca binds to the
+        # same runtime instead of pulling in a second copy.
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
+        L = ctypes.CDLL(LIB_PATH)
+        P = ctypes.POINTER
+        L.stca_workspace_size.restype = ctypes.c_size_t
+        L.stca_workspace_size.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_int]
+        L.stca_saved_size.restype = ctypes.c_size_t
+        L.stca_saved_size.argtypes = [P(stca_dims_t), P(stca_batch_t)]
+        L.stca_saved_layout.restype = ctypes.c_int
+        L.stca_saved_layout.argtypes = [P(stca_dims_t), P(stca_batch_t), P(stca_saved_layout_t)]
+        L.stca_forward.restype = ctypes.c_int
+        L.stca_forward.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                   P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                   ctypes.c_size_t, ctypes.c_void_p]
+        L.stca_backward.restype = ctypes.c_int
+        L.stca_backward.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                    P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                    ctypes.c_void_p, P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t,
+                                    ctypes.c_void_p]
+        L.stca_device_status.restype = ctypes.c_int
+        L.stca_device_status.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        L.stca_status_string.restype = ctypes.c_char_p
+        L.stca_status_string.argtypes = [ctypes.c_int]
+        L.stca_path.restype = ctypes.c_int
+        L.stca_path.argtypes = [P(stca_dims_t)]
+        L.stca_forward_launch_count.restype = ctypes.c_int
+        L.stca_forward_launch_count.argtypes = [P(stca_dims_t), P(stca_batch_t)]
+        L.stca_forward_profiled.restype = ctypes.c_int
+        L.stca_forward_profiled.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                            P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                            ctypes.c_size_t, ctypes.c_void_p, P(ctypes.c_void_p), ctypes.c_int,
+                                            P(ctypes.c_char_p)]
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().stca_status_string(int(status)).decode()
+
+
+def _ptr(t) -> Optional[int]:
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def dims(d_model: int, n_heads: int, n_layers: int, ffn_hidden: int, dtype: int) -> stca_dims_t:
+    return stca_dims_t(d_model, n_heads, n_layers, ffn_hidden, dtype)
+
+
+def batch(n_requests: int, n_hist: int, n_tgt: int, hist_off, tgt_off, hist_off_host=None,
+          tgt_off_host=None) -> stca_batch_t:
+    """hist_off / tgt_off: device int32 tensors; *_host: optional contiguous
+    int32 numpy arrays (kept alive by the caller)."""
+    def host(a):
+        return None if a is None else a.ctypes.data
+    return stca_batch_t(n_requests, n_hist, n_tgt, _ptr(hist_off), _ptr(tgt_off), host(hist_off_host),
+                        host(tgt_off_host))
+
+
+def weights(wq, wk, wv, wo, w1, w2) -> stca_weights_t:
+    return stca_weights_t(*(_ptr(t) for t in (wq, wk, wv, wo, w1, w2)))
+
+
+def wgrads(dwq, dwk, dwv, dwo, dw1, dw2) -> stca_wgrads_t:
+    return stca_wgrads_t(*(_ptr(t) for t in (dwq, dwk, dwv, dwo, dw1, dw2)))
+
+
+def stca_path(d: stca_dims_t) -> int:
+    return lib().stca_path(ctypes.byref(d))
+
+
+def stca_workspace_size(d: stca_dims_t, b: stca_batch_t, with_backward: bool = False) -> int:
+    return lib().stca_workspace_size(ctypes.byref(d), ctypes.byref(b), int(with_backward))
+
+
+def stca_saved_size(d: stca_dims_t, b: stca_batch_t) -> int:
+    return lib().stca_saved_size(ctypes.byref(d), ctypes.byref(b))
+
+
+def stca_saved_layout(d: stca_dims_t, b: stca_batch_t) -> stca_saved_layout_t:
+    out = stca_saved_layout_t()
+    st = lib().stca_saved_layout(ctypes.byref(d), ctypes.byref(b), ctypes.byref(out))
+    if st != STCA_OK:
+        raise StcaError(st, "stca_saved_layout")
+    return out
+
+
+def stca_forward(d, b, hist, tgt, w, out, saved, ws, ws_bytes: int, stream=None, check: bool = True) -> int:
+    st = lib().stca_forward(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w), _ptr(out),
+                            _ptr(saved), _ptr(ws), int(ws_bytes), _ptr(stream))
+    if check and st != STCA_OK:
+        raise StcaError(st, "stca_forward")
+    return st
+
+
+def stca_backward(d, b, hist, tgt, w, saved, dout, dhist, dtgt, dw, ws, ws_bytes: int, stream=None,
+                  check: bool = True) -> int:
+    st = lib().stca_backward(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w), _ptr(saved),
+                             _ptr(dout), _ptr(dhist), _ptr(dtgt), ctypes.byref(dw), _ptr(ws), int(ws_bytes),
+                             _ptr(stream))
+    if check and st != STCA_OK:
+        raise StcaError(st, "stca_backward")
+    return st
+
+
+def stca_device_status(ws, stream=None) -> int:
+    return lib().stca_device_status(_ptr(ws), _ptr(stream))
+
+
+def stca_forward_launch_count(d: stca_dims_t, b: stca_batch_t) -> int:
+    return lib().stca_forward_launch_count(ctypes.byref(d), ctypes.byref(b))
+
+
+def stca_forward_profiled(d, b, hist, tgt, w, out, saved, ws, ws_bytes: int, stream, events, labels=None) -> int:
+    """events: a ctypes array of hipEvent_t (see HipEvents); labels: optional
+    ctypes array of c_char_p receiving kernel names."""
+    st = lib().stca_forward_profiled(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w),
+                                     _ptr(out), _ptr(saved), _ptr(ws), int(ws_bytes), _ptr(stream), events,
+                                     len(events), labels)
+    if st != STCA_OK:
+        raise StcaError(st, "stca_forward_profiled")
+    return st
+
+
+class HipEvents:
+    """A set of HIP events created through the HIP runtime (for timing kernels
+    on the stream the library launches them on)."""
+
+    def __init__(self, n: int):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = (ctypes.c_void_p * n)()
+        for i in range(n):
+            e = ctypes.c_void_p()
+            if self.hip.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev[i] = e
+        self.labels = (ctypes.c_char_p * max(1, n - 1))()
+
+    def elapsed_ms(self, i: int, j: int) -> float:
+        if self.hip.hipEventSynchronize(self.ev[j]) != 0:
+            raise RuntimeError("hipEventSynchronize failed")
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), self.ev[i], self.ev[j]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def label(self, k: int) -> str:
+        v = self.labels[k]
+        return v.decode() if v else "?"
+
+    def close(self):
+        for i in range(len(self.ev)):
+            if self.ev[i]:
+                self.hip.hipEventDestroy(self.ev[i])
+                self.ev[i] = None

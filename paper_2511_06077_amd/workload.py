@@ -254,3 +254,25 @@ def replicate_per_target(b: Batch) -> Batch:
     ones = np.ones(int(reps.sum()), dtype=np.int64)
     return Batch(b.wl, np.repeat(b.requests, reps), L, ones, offsets(L), offsets(ones),
                  b.hist[idx], b.tgt.copy(), b.weights, None if b.grad_out is None else b.grad_out.copy())
+
+
+def make_custom_batch(name: str, hist_len: Sequence[int], n_tgt: Sequence[int], *, d_model: int, n_heads: int,
+                      n_layers: int, dtype: str, seed: int, scale_q: float = 1.0, with_grad: bool = False) -> Batch:
+    """A batch with explicitly listed per-request history lengths and target
+    counts (edge cases: tails, empty target segments, single-row histories),
+    drawn with the same per-request streams as the named workloads."""
+    L = np.asarray(hist_len, dtype=np.int64)
+    m = np.asarray(n_tgt, dtype=np.int64)
+    wl = Workload(name, len(L), d_model, n_heads, n_layers, dtype, seed, backward=with_grad)
+    hoff, toff = offsets(L), offsets(m)
+    sdt = np.uint16 if dtype == "bf16" else np.float32
+    hist = np.empty((int(hoff[-1]), d_model), dtype=sdt)
+    tgt = np.empty((int(toff[-1]), d_model), dtype=sdt)
+    grad = np.empty((int(toff[-1]), d_model), dtype=sdt) if with_grad else None
+    for r in range(len(L)):
+        x, t = _request_rows(wl, r, int(L[r]), int(m[r]))
+        hist[hoff[r]:hoff[r + 1]] = x
+        tgt[toff[r]:toff[r + 1]] = t
+        if grad is not None:
+            grad[toff[r]:toff[r + 1]] = _request_grad(wl, r, int(m[r]))
+    return Batch(wl, np.arange(len(L)), L, m, hoff, toff, hist, tgt, make_weights(wl, scale_q), grad)

@@ -1,0 +1,125 @@
+"""The C-ABI library loads, exports every declared entry point, and rejects
+bad arguments on the host before any launch (runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2511_06077_amd import stca
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "stca.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(stca_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert "stca_forward" in names and "stca_backward" in names
+    lib = stca.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(stca.EXPORTED) <= set(names)
+
+
+def test_status_strings():
+    for s in (0, -1, -2, -3, -4):
+        assert stca.status_string(s)
+
+
+def fake_batch(hoff, toff):
+    hoff = np.asarray(hoff, dtype=np.int32)
+    toff = np.asarray(toff, dtype=np.int32)
+    # device pointers are never dereferenced on these paths
+    return stca.batch(len(hoff) - 1, int(hoff[-1]), int(toff[-1]), 0x10000, 0x20000, hoff, toff), (hoff, toff)
+
+
+GOOD_DIMS = dict(d_model=256, n_heads=8, n_layers=4, ffn_hidden=1024, dtype=stca.STCA_BF16)
+
+
+def dims(**kw):
+    a = dict(GOOD_DIMS)
+    a.update(kw)
+    return stca.dims(a["d_model"], a["n_heads"], a["n_layers"], a["ffn_hidden"], a["dtype"])
+
+
+def fake_weights():
+    return stca.weights(*([0x100000] * 6))
+
+
+def call_forward(d, b, ws_bytes=1 << 40, hist=0x200000, tgt=0x300000, out=0x400000, ws=0x500000):
+    return stca.stca_forward(d, b, hist, tgt, fake_weights(), out, None, ws, ws_bytes, None, check=False)
+
+
+def test_path_selection():
+    assert stca.stca_path(dims()) == 1
+    assert stca.stca_path(dims(d_model=128, n_heads=4)) == 1
+    assert stca.stca_path(dims(dtype=stca.STCA_F32)) == 0
+    assert stca.stca_path(dims(d_model=64, n_heads=2, dtype=stca.STCA_F32)) == 0
+    assert stca.stca_path(dims(n_heads=16)) == 0  # bf16, d_h = 16: generic kernels
+    assert stca.stca_path(dims(n_heads=7)) == stca.STCA_ERR_INVALID_ARG
+    assert stca.stca_path(dims(ffn_hidden=100)) == stca.STCA_ERR_UNSUPPORTED
+    assert stca.stca_path(dims(n_heads=2)) == stca.STCA_ERR_UNSUPPORTED  # d_h = 128
+    assert stca.stca_path(dims(dtype=7)) == stca.STCA_ERR_INVALID_ARG
+
+
+@pytest.mark.parametrize("hoff,toff", [
+    ([0, 5, 3, 8], [0, 1, 2, 3]),       # decreasing history offsets
+    ([0, 5, 5, 8], [0, 1, 2, 3]),       # request 1 has a target but no history
+    ([1, 5, 6, 8], [0, 1, 2, 3]),       # offsets[0] != 0
+    ([0, 5, 6, 8], [0, 2, 1, 3]),       # decreasing target offsets
+])
+def test_invalid_host_offsets_rejected(hoff, toff):
+    b, keep = fake_batch(hoff, toff)
+    assert stca.stca_workspace_size(dims(), b) == 0
+    assert call_forward(dims(), b) == stca.STCA_ERR_INVALID_ARG
+
+
+def test_empty_target_segments_are_legal():
+    b, keep = fake_batch([0, 5, 5, 8], [0, 1, 1, 3])
+    assert stca.stca_workspace_size(dims(), b) > 0
+
+
+def test_workspace_too_small_and_bad_pointers():
+    b, keep = fake_batch([0, 40, 100], [0, 3, 9])
+    need = stca.stca_workspace_size(dims(), b)
+    assert need > 0
+    assert call_forward(dims(), b, ws_bytes=need - 1) == stca.STCA_ERR_WORKSPACE
+    assert call_forward(dims(), b, hist=0x200004) == stca.STCA_ERR_INVALID_ARG  # misaligned
+    assert call_forward(dims(), b, tgt=0) == stca.STCA_ERR_INVALID_ARG
+    assert call_forward(dims(), b, out=0) == stca.STCA_ERR_INVALID_ARG
+    assert call_forward(dims(), b, ws=0) == stca.STCA_ERR_INVALID_ARG
+    assert call_forward(dims(n_heads=7), b) == stca.STCA_ERR_INVALID_ARG
+    assert call_forward(dims(n_heads=2), b) == stca.STCA_ERR_UNSUPPORTED
+
+
+def test_backward_argument_checks():
+    b, keep = fake_batch([0, 40, 100], [0, 3, 9])
+    dw = stca.wgrads(*([0x600000] * 6))
+    args = (dims(), b, 0x200000, 0x300000, fake_weights())
+    st = stca.stca_backward(*args, None, 0x700000, 0x800000, 0x900000, dw, 0x500000, 1 << 40, check=False)
+    assert st == stca.STCA_ERR_INVALID_ARG  # saved is required
+    need = stca.stca_workspace_size(dims(), b, True)
+    st = stca.stca_backward(*args, 0xA00000, 0x700000, 0x800000, 0x900000, dw, 0x500000, need - 1, check=False)
+    assert st == stca.STCA_ERR_WORKSPACE
+    bad_dw = stca.wgrads(0x600000, 0, 0x600000, 0x600000, 0x600000, 0x600000)
+    st = stca.stca_backward(*args, 0xA00000, 0x700000, 0x800000, 0x900000, bad_dw, 0x500000, need, check=False)
+    assert st == stca.STCA_ERR_INVALID_ARG
+
+
+def test_saved_layout_is_disjoint_and_sized():
+    b, keep = fake_batch([0, 40, 100], [0, 3, 9])
+    lay = stca.stca_saved_layout(dims(), b)
+    nt, d, n, h = 9, 256, 4, 8
+    assert lay.a >= lay.s + 4 * n * nt * d
+    assert lay.u >= lay.a + 4 * n * nt * d
+    assert lay.lse >= lay.u + 4 * n * nt * d
+    assert lay.kv >= lay.lse + 4 * n * nt * h
+    assert lay.total == stca.stca_saved_size(dims(), b)
+    assert lay.total >= lay.kv + 2 * n * 128 * 2 * d  # 100 rows -> 4 blocks of 32
