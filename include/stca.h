@@ -120,7 +120,7 @@ typedef struct {
  * (with_backward = 1).  Returns 0 for invalid or unsupported arguments. */
 size_t stca_workspace_size(const stca_dims_t* dims, const stca_batch_t* batch, int with_backward);
 
-/* Bytes of the `saved` buffer that stca_forward fills for stca_backward. */
+/* Bytes of the optional `saved` buffer that stca_forward fills. */
 size_t stca_saved_size(const stca_dims_t* dims, const stca_batch_t* batch);
 
 /* Offsets of the saved tensors; returns STCA_ERR_INVALID_ARG / UNSUPPORTED
@@ -131,20 +131,24 @@ stca_status_t stca_saved_layout(const stca_dims_t* dims, const stca_batch_t* bat
 /* Forward pass: out[n_tgt][d] (storage dtype) = s^(n) for every target.
  *  hist  [n_hist][d], tgt [n_tgt][d]  storage dtype, device
  *  saved nullable; when given (stca_saved_size bytes) the per-layer
- *        intermediates and the projected history are kept for stca_backward
+ *        intermediates (see stca_saved_layout_t) and the projected history
+ *        are written there
  *  ws    device workspace of ws_bytes >= stca_workspace_size(dims, batch, 0) */
 stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch,
                            const void* hist, const void* tgt, const stca_weights_t* w,
                            void* out, void* saved, void* ws, size_t ws_bytes,
                            hipStream_t stream);
 
-/* Backward pass of f = sum_t <dout_t, out_t> given the `saved` buffer of a
- * stca_forward call on the same inputs.  Writes (overwrites) dhist [n_hist][d],
- * dtgt [n_tgt][d] and all weight gradients, fp32.  dout is [n_tgt][d] in the
- * storage dtype.  ws_bytes >= stca_workspace_size(dims, batch, 1). */
+/* Backward pass: the gradients of f = sum_t <dout_t, out_t> with respect to
+ * hist, tgt and every weight, for the same inputs as a forward call.  The
+ * layer states are recomputed from the inputs in fp32 (activation
+ * recomputation), so every ReLU gate and softmax weight of the backward
+ * follows fp32 states.  Writes (overwrites) dhist [n_hist][d], dtgt [n_tgt][d]
+ * and all weight gradients, fp32.  dout is [n_tgt][d] in the storage dtype.
+ * ws_bytes >= stca_workspace_size(dims, batch, 1). */
 stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch,
                             const void* hist, const void* tgt, const stca_weights_t* w,
-                            const void* saved, const void* dout, float* dhist, float* dtgt,
+                            const void* dout, float* dhist, float* dtgt,
                             const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
                             hipStream_t stream);
 

@@ -109,7 +109,7 @@ struct Layout {
   // generic forward
   size_t kv32, q32, abuf, ubuf, hid;
   // backward (generic)
-  size_t pre, dhid, ds, du, da, dq, ds2, dkv32, dq_part;
+  size_t pre, dhid, ds, du, da, dq, ds2, dkv32, dq_part, lse32, rs, ru;
   size_t total;
 };
 
@@ -166,6 +166,12 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->dq = m.take(4 * nt * d);
     L->ds2 = m.take(4 * nt * d);
     L->dq_part = m.take(4 * kMaxChunks * nt * d);
+    L->part_acc = m.take(4 * kMaxChunks * nt * d);
+    L->part_ml = m.take(8 * kMaxChunks * nt * L->h);
+    L->abuf = m.take(4 * nt * d);
+    L->lse32 = m.take(4 * nt * L->h);
+    L->rs = m.take(4 * (n + 1) * nt * d);  // recomputed s^(0..n)
+    L->ru = m.take(4 * n * nt * d);        // recomputed u^(0..n-1)
   }
   L->total = m.off;
   return true;
@@ -244,12 +250,12 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   int32_t* tch = at<int32_t>(ws, L.tchunks);
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, units, L.max_units,
                       tch, hdr, st)); HIPCHK(rec.mark("sched"));
-  HIPCHK(fast_pack(w->wk, at<char>(ws, L.wkp), n, d, d, st)); HIPCHK(rec.mark("pack_wk"));
-  HIPCHK(fast_pack(w->wv, at<char>(ws, L.wvp), n, d, d, st)); HIPCHK(rec.mark("pack_wv"));
-  HIPCHK(fast_pack(w->wo, at<char>(ws, L.wop), n, d, d, st)); HIPCHK(rec.mark("pack_wo"));
-  HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, st)); HIPCHK(rec.mark("pack_wq"));
-  HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, st)); HIPCHK(rec.mark("pack_w1"));
-  HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, st)); HIPCHK(rec.mark("pack_w2"));
+  HIPCHK(fast_pack(w->wk, at<char>(ws, L.wkp), n, d, d, 0, st)); HIPCHK(rec.mark("pack_wk"));
+  HIPCHK(fast_pack(w->wv, at<char>(ws, L.wvp), n, d, d, 0, st)); HIPCHK(rec.mark("pack_wv"));
+  HIPCHK(fast_pack(w->wo, at<char>(ws, L.wop), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wo"));
+  HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wq"));
+  HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, 1, st)); HIPCHK(rec.mark("pack_w1"));
+  HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, 1, st)); HIPCHK(rec.mark("pack_w2"));
   char* kv = saved ? at<char>(saved, SL.kv) : at<char>(ws, L.kv);
   if (L.nh > 0)
     HIPCHK(fast_proj(d, hist, L.nh, L.nblocks, at<char>(ws, L.wkp), at<char>(ws, L.wvp), kv, n,
@@ -343,10 +349,12 @@ stca_status_t forward_generic(const Layout& L, int bf, const stca_batch_t* b, co
 }
 
 // --------------------------------------------------------------- backward
-stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, const void* hist,
-                               const stca_weights_t* w, const void* saved, const stca_saved_layout_t& SL,
-                               const void* dout, float* dhist, float* dtgt, const stca_wgrads_t* dw, void* ws,
-                               hipStream_t st) {
+// Activation recomputation: the layer states are rebuilt in fp32 from the
+// inputs first, so every ReLU gate and softmax weight of the backward follows
+// fp32 states whatever arithmetic the forward call used.
+stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, const void* hist, const void* tgt,
+                               const stca_weights_t* w, const void* dout, float* dhist, float* dtgt,
+                               const stca_wgrads_t* dw, void* ws, hipStream_t st) {
   const int d = L.d, n = L.n, F = L.F, h = L.h;
   const int64_t nt = L.nt, nh = L.nh;
   const size_t es = bf ? 2 : 4;
@@ -368,21 +376,56 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   float* ds2 = at<float>(ws, L.ds2);
   float* dqp = at<float>(ws, L.dq_part);
   auto W = [&](const void* base, int i, size_t per) { return static_cast<const char*>(base) + i * per * es; };
-  auto S = [&](size_t off, int i, size_t per) { return at<float>(saved, off) + (size_t)i * per; };
+  auto RS = [&](int i) { return at<float>(ws, L.rs) + (size_t)i * nt * d; };
+  auto RU = [&](int i) { return at<float>(ws, L.ru) + (size_t)i * nt * d; };
+  const float qscale0 = kLog2e / std::sqrt(static_cast<float>(L.dh));
+  // forward recomputation (fp32): s^(i), u^(i)
+  HIPCHK(convert(bf, 0, tgt, RS(0), nt * d, st));
+  for (int i = 0; i < n; ++i) {
+    const void* Wk = W(w->wk, i, (size_t)d * d);
+    const void* Wv = W(w->wv, i, (size_t)d * d);
+    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr, 0,
+                        st));
+    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr,
+                        0, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, d, RS(i), d, 0, W(w->wq, i, (size_t)d * d), d, 0, q, d, qscale0, kEpiStore,
+                        nullptr, 0, nullptr, 0, st));
+    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, at<float>(ws, L.part_acc),
+                        at<float>(ws, L.part_ml), nt, st));
+    HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml),
+                         at<float>(ws, L.abuf), nullptr, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, d, at<float>(ws, L.abuf), d, 0, W(w->wo, i, (size_t)d * d), d, 0, RU(i), d,
+                        1.f, kEpiAddRes, RS(i), d, nullptr, 0, st));
+    HIPCHK(gemm_generic(0, bf, nt, F, d, RU(i), d, 0, W(w->w1, i, (size_t)d * F), F, 0, hid, F, 1.f, kEpiRelu,
+                        nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, F, hid, F, 0, W(w->w2, i, (size_t)d * F), d, 0, RS(i + 1), d, 1.f,
+                        kEpiAddRes, RU(i), d, nullptr, 0, st));
+  }
   HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
   HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
   const float qscale = kLog2e / std::sqrt(static_cast<float>(L.dh));
   for (int i = n - 1; i >= 0; --i) {
-    const float* s = S(SL.s, i, nt * d);
-    const float* a = S(SL.a, i, nt * d);
-    const float* u = S(SL.u, i, nt * d);
-    const float* lse = S(SL.lse, i, nt * h);
+    const float* s = RS(i);
+    const float* u = RU(i);
+    // a and lse are recomputed below in fp32 from the same q, K, V that the
+    // softmax weights are rebuilt from, so rowsum(dA * A) matches P exactly
+    float* a = at<float>(ws, L.abuf);
+    float* lse = at<float>(ws, L.lse32);
     const void* W1 = W(w->w1, i, (size_t)d * F);
     const void* W2 = W(w->w2, i, (size_t)d * F);
     const void* Wo = W(w->wo, i, (size_t)d * d);
     const void* Wq = W(w->wq, i, (size_t)d * d);
     const void* Wk = W(w->wk, i, (size_t)d * d);
     const void* Wv = W(w->wv, i, (size_t)d * d);
+    // recompute this layer's K, V, q and attention output in fp32
+    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr, 0,
+                        st));
+    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr,
+                        0, st));
+    HIPCHK(gemm_generic(0, bf, nt, d, d, s, d, 0, Wq, d, 0, q, d, qscale, kEpiStore, nullptr, 0, nullptr, 0, st));
+    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, at<float>(ws, L.part_acc),
+                        at<float>(ws, L.part_ml), nt, st));
+    HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml), a, lse, st));
     // s' = u + ReLU(u W1) W2
     HIPCHK(gemm_generic(0, bf, nt, F, d, u, d, 0, W1, F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0, pre, 0, st));
     HIPCHK(gemm_generic(0, 0, F, d, nt, hid, F, 1, ds, d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, kEpiStore,
@@ -396,12 +439,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     HIPCHK(gemm_generic(0, 0, d, d, nt, a, d, 1, du, d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, kEpiStore,
                         nullptr, 0, nullptr, 0, st));
     HIPCHK(gemm_generic(0, bf, nt, d, d, du, d, 0, Wo, d, 1, da, d, 1.f, kEpiStore, nullptr, 0, nullptr, 0, st));
-    // attention (K, V and q recomputed)
-    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr, 0,
-                        st));
-    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr,
-                        0, st));
-    HIPCHK(gemm_generic(0, bf, nt, d, d, s, d, 0, Wq, d, 0, q, d, qscale, kEpiStore, nullptr, 0, nullptr, 0, st));
+    // attention
     HIPCHK(fill_f32(dkv, 0.f, nh * 2 * d, st));
     HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, a, da, lse, dqp, dkv, nt, st));
     HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
@@ -500,24 +538,20 @@ stca_status_t stca_forward_profiled(const stca_dims_t* dims, const stca_batch_t*
 }
 
 stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist, const void* tgt,
-                            const stca_weights_t* w, const void* saved, const void* dout, float* dhist,
-                            float* dtgt, const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
-                            hipStream_t stream) {
+                            const stca_weights_t* w, const void* dout, float* dhist, float* dtgt,
+                            const stca_wgrads_t* dw, void* ws, size_t ws_bytes, hipStream_t stream) {
   stca_status_t st = check_common(dims, batch, hist, tgt, w, ws);
   if (st != STCA_OK) return st;
-  if (!saved || !dw || (batch->n_tgt > 0 && (!dout || !dtgt)) || (batch->n_hist > 0 && !dhist))
+  if (!dw || (batch->n_tgt > 0 && (!dout || !dtgt)) || (batch->n_hist > 0 && !dhist))
     return STCA_ERR_INVALID_ARG;
   if (!dw->dwq || !dw->dwk || !dw->dwv || !dw->dwo || !dw->dw1 || !dw->dw2) return STCA_ERR_INVALID_ARG;
-  const void* ptrs[] = {saved, dout, dhist, dtgt, dw->dwq, dw->dwk, dw->dwv, dw->dwo, dw->dw1, dw->dw2};
+  const void* ptrs[] = {dout, dhist, dtgt, dw->dwq, dw->dwk, dw->dwv, dw->dwo, dw->dw1, dw->dw2};
   for (const void* q : ptrs)
     if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
   Layout L;
   make_layout(dims, batch, 1, true, &L);
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
-  stca_saved_layout_t SL{};
-  saved_layout(dims, batch, &SL);
-  return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, w, saved, SL, dout, dhist, dtgt, dw, ws,
-                          stream);
+  return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, dout, dhist, dtgt, dw, ws, stream);
 }
 
 stca_status_t stca_device_status(const void* ws, hipStream_t stream) {

@@ -10,6 +10,7 @@ namespace stca {
 
 typedef uint16_t bf16_bits;  // storage of a bfloat16 value
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 

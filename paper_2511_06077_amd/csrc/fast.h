@@ -21,8 +21,8 @@ struct FastUpdate {
   const void *WoP, *W1P, *W2P, *WqP;
 };
 
-// Repack W [n_layers][K][N] (bf16) into MFMA operand order.
-hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, hipStream_t st);
+// Repack W [n_layers][K][N] (bf16) into MFMA operand order, as bf16 or fp16.
+hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, int to_f16, hipStream_t st);
 int fast_proj_parts(int n_layers, int64_t n_blocks, int n_cu);
 // K1: history -> K/V of every layer, in the attention kernel's operand layout.
 hipError_t fast_proj(int D, const void* X, int64_t n_hist, int64_t n_blocks, const void* WkP, const void* WvP,

@@ -1,7 +1,14 @@
-// bf16 MFMA path for d_h = 32 (gfx950 / CDNA4): history K/V projection (K1),
-// fused multi-target cross attention (K3) and fused target update (K4).
+// MFMA path for bf16 storage and d_h = 32 (gfx950 / CDNA4): history K/V
+// projection (K1), fused multi-target cross attention (K3) and fused target
+// update (K4).
 //
-// All three use v_mfma_f32_32x32x16_bf16.  For that instruction lane l holds
+// K1 multiplies the bf16 history by the bf16 weights (v_mfma_f32_32x32x16_bf16,
+// fp32 accumulate) and stores K and V as fp16: the same two bytes as bf16 with
+// three more mantissa bits, which the attention's softmax weights are
+// sensitive to.  K3 and K4 run v_mfma_f32_32x32x16_f16 on fp16 operands (Q, K,
+// V, the softmax weights P, and the update's activations and weights), always
+// accumulating in fp32; the target state stays fp32.  Both instructions have
+// the same rate and operand layout.  For them lane l holds
 //   A operand: A[i = l%32][k = 8*(l/32) .. +7]           (8 bf16)
 //   B operand: B[k = 8*(l/32) .. +7][j = l%32]           (8 bf16)
 //   result   : D[i = 8*(v/4) + 4*(l/32) + v%4][j = l%32] for v = 0..15 (fp32)
@@ -43,24 +50,45 @@ constexpr int DH = 32;
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ f32x16 mfma(const f16x8& a, const f16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
 
-__device__ __forceinline__ bf16x8 pack8(const f32x16& a, int off) {
-  bf16x8 r;
+__device__ __forceinline__ f16x8 pack8h(const f32x16& a, int off) {
+  f16x8 r;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = static_cast<__bf16>(a[off + i]);
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<_Float16>(a[off + i]);
   return r;
 }
 
-__device__ __forceinline__ bf16x8 zero8() {
-  bf16x8 r;
+__device__ __forceinline__ f16x8 zero8h() {
+  f16x8 r;
 #pragma unroll
-  for (int i = 0; i < 8; ++i) r[i] = static_cast<__bf16>(0.f);
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<_Float16>(0.f);
   return r;
 }
+
+__device__ __forceinline__ uint16_t f16_bits(float x) {
+  return __builtin_bit_cast(uint16_t, static_cast<_Float16>(x));
+}
+
+template <typename V8>
+struct elem_of;
+template <>
+struct elem_of<bf16x8> {
+  typedef __bf16 type;
+};
+template <>
+struct elem_of<f16x8> {
+  typedef _Float16 type;
+};
 
 // ------------------------------------------------------------- repacking
-// W: [layers][K][N] bf16 row-major -> P: [layers][N/32][K/16][64][8].
-__global__ void pack_kernel(const bf16_bits* __restrict__ W, bf16x8* __restrict__ P, int K, int N,
+// W: [layers][K][N] bf16 row-major -> P: [layers][N/32][K/16][64][8], kept
+// bf16 (V8 = bf16x8) or converted to fp16 (V8 = f16x8, exact for every bf16
+// value inside fp16's range).
+template <typename V8>
+__global__ void pack_kernel(const bf16_bits* __restrict__ W, V8* __restrict__ P, int K, int N,
                             int64_t per_layer_groups) {
   const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   const int layer = blockIdx.y;
@@ -72,9 +100,9 @@ __global__ void pack_kernel(const bf16_bits* __restrict__ W, bf16x8* __restrict_
   const int n = nb * 32 + lane % 32;
   const int k0 = ks * 16 + 8 * (lane / 32);
   const bf16_bits* w = W + (int64_t)layer * K * N;
-  bf16x8 r;
+  V8 r;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = __builtin_bit_cast(__bf16, w[(int64_t)(k0 + e) * N + n]);
+  for (int e = 0; e < 8; ++e) r[e] = static_cast<typename elem_of<V8>::type>(to_f32(w[(int64_t)(k0 + e) * N + n]));
   P[(int64_t)layer * per_layer_groups + g] = r;
 }
 
@@ -89,7 +117,7 @@ template <int D>
 __global__ __launch_bounds__(64 * (D / 32)) void proj_kernel(const bf16_bits* __restrict__ X, int64_t n_hist,
                                                              int64_t n_blocks, const bf16x8* __restrict__ WkP,
                                                              const bf16x8* __restrict__ WvP,
-                                                             bf16x8* __restrict__ KV, int n_layers, int parts) {
+                                                             f16x8* __restrict__ KV, int n_layers, int parts) {
   constexpr int H = D / DH;
   constexpr int KS = D / 16;
   constexpr int ROW = D + 8;             // padded LDS row (bf16): conflict-free 16 B reads
@@ -151,11 +179,11 @@ __global__ __launch_bounds__(64 * (D / 32)) void proj_kernel(const bf16_bits* __
       ak = mfma(wk[ks], xo, ak);  // K^T block: rows = head dims, cols = history rows
       av = mfma(xo, wv[ks], av);  // V block:   rows = history rows, cols = head dims
     }
-    bf16x8* out = KV + (((int64_t)layer * n_blocks + b) * H + wave) * 4 * 64 + lane;
-    out[0] = pack8(ak, 0);
-    out[64] = pack8(ak, 8);
-    out[128] = pack8(av, 0);
-    out[192] = pack8(av, 8);
+    f16x8* out = KV + (((int64_t)layer * n_blocks + b) * H + wave) * 4 * 64 + lane;
+    out[0] = pack8h(ak, 0);
+    out[64] = pack8h(ak, 8);
+    out[128] = pack8h(av, 0);
+    out[192] = pack8h(av, 8);
     if (b + 1 < be) stash(cur ^ 1, nxt);
     __syncthreads();
   }
@@ -169,35 +197,35 @@ __global__ __launch_bounds__(64 * (D / 32)) void proj_kernel(const bf16_bits* __
 // log2 units; the result is an unnormalised partial (acc, max, sum) per
 // (chunk, target, head), merged by the update kernel.
 template <int H, int NG>
-__device__ __forceinline__ void attn_unit(const Unit& un, const bf16x8* __restrict__ QN,
-                                          const bf16x8* __restrict__ KVl, float* __restrict__ part_acc,
+__device__ __forceinline__ void attn_unit(const Unit& un, const f16x8* __restrict__ QN,
+                                          const f16x8* __restrict__ KVl, float* __restrict__ part_acc,
                                           float2* __restrict__ part_ml, int64_t n_tgt) {
   constexpr int D = H * DH;
   const int j = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int tcol = lane % 32, hi = lane / 32;
-  bf16x8 qop[NG][2];
+  f16x8 qop[NG][2];
   f32x16 O[NG];
   float m[NG], l[NG];
 #pragma unroll
   for (int g = 0; g < NG; ++g) {
     const int tt = g * 32 + tcol;
     const bool ok = tt < un.nt;
-    const bf16x8* q = QN + ((int64_t)(un.t0 + tt) * D + j * DH) / 8;
-    qop[g][0] = ok ? q[hi] : zero8();
-    qop[g][1] = ok ? q[2 + hi] : zero8();
+    const f16x8* q = QN + ((int64_t)(un.t0 + tt) * D + j * DH) / 8;
+    qop[g][0] = ok ? q[hi] : zero8h();
+    qop[g][1] = ok ? q[2 + hi] : zero8h();
     O[g] = f32x16{};
     m[g] = -INFINITY;
     l[g] = 0.f;
   }
-  const bf16x8* base = KVl + (int64_t)j * 4 * 64 + lane;
-  auto ld = [&](int64_t b, bf16x8 (&r)[4]) {
-    const bf16x8* p = base + b * (H * 4 * 64);
+  const f16x8* base = KVl + (int64_t)j * 4 * 64 + lane;
+  auto ld = [&](int64_t b, f16x8 (&r)[4]) {
+    const f16x8* p = base + b * (H * 4 * 64);
     r[0] = p[0];
     r[1] = p[64];
     r[2] = p[128];
     r[3] = p[192];
   };
-  bf16x8 nx[4], cu[4];
+  f16x8 nx[4], cu[4];
   ld(un.b0, nx);
   for (int b = un.b0; b < un.b1; ++b) {
 #pragma unroll
@@ -231,8 +259,8 @@ __device__ __forceinline__ void attn_unit(const Unit& un, const bf16x8* __restri
       l[g] = l[g] * sc + ps;
 #pragma unroll
       for (int v = 0; v < 16; ++v) O[g][v] *= sc;
-      O[g] = mfma(cu[2], pack8(s, 0), O[g]);
-      O[g] = mfma(cu[3], pack8(s, 8), O[g]);
+      O[g] = mfma(cu[2], pack8h(s, 0), O[g]);
+      O[g] = mfma(cu[3], pack8h(s, 8), O[g]);
     }
   }
 #pragma unroll
@@ -254,8 +282,8 @@ __device__ __forceinline__ void attn_unit(const Unit& un, const bf16x8* __restri
 template <int H>
 __global__ __launch_bounds__(64 * H) void attn_kernel(const Unit* __restrict__ units,
                                                       const WsHeader* __restrict__ hdr,
-                                                      const bf16x8* __restrict__ QN,
-                                                      const bf16x8* __restrict__ KVl, float* __restrict__ part_acc,
+                                                      const f16x8* __restrict__ QN,
+                                                      const f16x8* __restrict__ KVl, float* __restrict__ part_acc,
                                                       float2* __restrict__ part_ml, int64_t n_tgt) {
   const int nu = hdr->n_units;
   for (int u = blockIdx.x; u < nu; u += gridDim.x) {
@@ -286,8 +314,8 @@ struct UpdateArgs {
   float* save_u;               // nullable
   float* save_lse;             // nullable [n_tgt][H]
   bf16_bits* out;              // final layer output, nullable
-  bf16x8* QN;                  // next queries
-  const bf16x8 *WoP, *W1P, *W2P, *WqP;  // packed, all layers
+  f16x8* QN;                   // next queries
+  const f16x8 *WoP, *W1P, *W2P, *WqP;  // packed (fp16), all layers
 };
 
 template <int D>
@@ -296,9 +324,9 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   constexpr int H = D / DH;
   constexpr int KS = D / 16;
   constexpr int AROW = D + 8;
-  extern __shared__ __attribute__((aligned(16))) bf16_bits lds[];
-  bf16_bits* act = lds;                 // [32][AROW]
-  bf16_bits* hid = lds + 32 * AROW;     // [32][FC + 8]
+  extern __shared__ __attribute__((aligned(16))) uint16_t lds[];  // fp16 MFMA operands
+  uint16_t* act = lds;                  // [32][AROW]
+  uint16_t* hid = lds + 32 * AROW;      // [32][FC + 8]
   const int HROW = A.FC + 8;
   const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int tcol = lane % 32, hi = lane / 32;
@@ -313,38 +341,40 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
     for (int g = 0; g < 4; ++g)
       *reinterpret_cast<float4*>(p + 8 * g) = make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
   };
-  auto put_act = [&](bf16_bits* buf, int row_len, int col0, const f32x16& v) {
-    bf16_bits* p = buf + tcol * row_len + col0 + 4 * hi;
+  auto put_act = [&](uint16_t* buf, int row_len, int col0, const f32x16& v) {
+    uint16_t* p = buf + tcol * row_len + col0 + 4 * hi;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       uint2 pk;
-      pk.x = (uint32_t)from_f32<bf16_bits>(v[4 * g]) | ((uint32_t)from_f32<bf16_bits>(v[4 * g + 1]) << 16);
-      pk.y = (uint32_t)from_f32<bf16_bits>(v[4 * g + 2]) | ((uint32_t)from_f32<bf16_bits>(v[4 * g + 3]) << 16);
+      pk.x = (uint32_t)f16_bits(v[4 * g]) | ((uint32_t)f16_bits(v[4 * g + 1]) << 16);
+      pk.y = (uint32_t)f16_bits(v[4 * g + 2]) | ((uint32_t)f16_bits(v[4 * g + 3]) << 16);
       *reinterpret_cast<uint2*>(p + 8 * g) = pk;
     }
   };
-  auto gemm = [&](const bf16x8* Wp, const bf16_bits* src, int src_row, int ksteps) {
+  auto gemm = [&](const f16x8* Wp, const uint16_t* src, int src_row, int ksteps) {
     f32x16 acc = {};
-    const bf16_bits* b = src + tcol * src_row + 8 * hi;
+    const uint16_t* b = src + tcol * src_row + 8 * hi;
 #pragma unroll 4
     for (int ks = 0; ks < ksteps; ++ks)
-      acc = mfma(Wp[ks * 64 + lane], *reinterpret_cast<const bf16x8*>(b + ks * 16), acc);
+      acc = mfma(Wp[ks * 64 + lane], *reinterpret_cast<const f16x8*>(b + ks * 16), acc);
     return acc;
   };
 
   f32x16 s_next;
   if (A.mode == 0) {
-    // stage x_t rows into LDS and write s^(0)
+    // stage x_t rows into LDS (fp16) and write s^(0) (fp32)
     for (int c = threadIdx.x; c < 32 * D / 8; c += 64 * NW) {
       const int row = c / (D / 8), col8 = c % (D / 8);
       uint4 v = make_uint4(0, 0, 0, 0);
       if (tb + row < A.n_tgt) v = *reinterpret_cast<const uint4*>(A.tgt + (tb + row) * D + col8 * 8);
-      *reinterpret_cast<uint4*>(act + row * AROW + col8 * 8) = v;
+      const bf16_bits* e = reinterpret_cast<const bf16_bits*>(&v);
+      uint16_t* a8 = act + row * AROW + col8 * 8;
+#pragma unroll
+      for (int i = 0; i < 8; ++i) a8[i] = f16_bits(to_f32(e[i]));
       if (tb + row < A.n_tgt) {
-        const bf16_bits* e = reinterpret_cast<const bf16_bits*>(&v);
         float* so = A.s_out + (tb + row) * D + col8 * 8;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) so[i] = __uint_as_float((uint32_t)e[i] << 16);
+        for (int i = 0; i < 8; ++i) so[i] = to_f32(e[i]);
       }
     }
     __syncthreads();
@@ -379,9 +409,9 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
         }
         if (A.save_lse && qq == 0) A.save_lse[tt * H + j] = (M + log2f(L)) * kLn2;
       }
-      bf16_bits* p = act + row * AROW + j * DH + qq * 8;
+      uint16_t* p = act + row * AROW + j * DH + qq * 8;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) p[i] = from_f32<bf16_bits>(av[i]);
+      for (int i = 0; i < 8; ++i) p[i] = f16_bits(av[i]);
     }
     __syncthreads();
     const int KSF = A.F / 16;
@@ -441,19 +471,22 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) q[v] *= qs;
   if (tok) {
-    bf16x8* qn = A.QN + (t * D + 32 * w) / 8;
-    qn[hi] = pack8(q, 0);
-    qn[2 + hi] = pack8(q, 8);
+    f16x8* qn = A.QN + (t * D + 32 * w) / 8;
+    qn[hi] = pack8h(q, 0);
+    qn[2 + hi] = pack8h(q, 8);
   }
 }
 
 }  // namespace
 
 // ------------------------------------------------------------ launchers
-hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, hipStream_t st) {
+hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, int to_f16, hipStream_t st) {
   const int64_t groups = (int64_t)(N / 32) * (K / 16) * 64;
   dim3 g(static_cast<unsigned>(ceil_div(groups, 256)), n_layers);
-  hipLaunchKernelGGL(pack_kernel, g, dim3(256), 0, st, (const bf16_bits*)W, (bf16x8*)P, K, N, groups);
+  if (to_f16)
+    hipLaunchKernelGGL(pack_kernel<f16x8>, g, dim3(256), 0, st, (const bf16_bits*)W, (f16x8*)P, K, N, groups);
+  else
+    hipLaunchKernelGGL(pack_kernel<bf16x8>, g, dim3(256), 0, st, (const bf16_bits*)W, (bf16x8*)P, K, N, groups);
   return hipGetLastError();
 }
 
@@ -470,7 +503,7 @@ hipError_t fast_proj(int D, const void* X, int64_t n_hist, int64_t n_blocks, con
   dim3 g(static_cast<unsigned>(n_layers * parts));
 #define STCA_PROJ(DD)                                                                                       \
   hipLaunchKernelGGL(proj_kernel<DD>, g, dim3(64 * (DD / 32)), 0, st, (const bf16_bits*)X, n_hist, n_blocks, \
-                     (const bf16x8*)WkP, (const bf16x8*)WvP, (bf16x8*)KV, n_layers, parts)
+                     (const bf16x8*)WkP, (const bf16x8*)WvP, (f16x8*)KV, n_layers, parts)
   switch (D) {
     case 64: STCA_PROJ(64); break;
     case 128: STCA_PROJ(128); break;
@@ -485,8 +518,8 @@ hipError_t fast_attn(int D, const Unit* units, const WsHeader* hdr, int grid, co
                      float* part_acc, void* part_ml, int64_t n_tgt, hipStream_t st) {
   if (grid == 0) return hipSuccess;
 #define STCA_ATTN(HH)                                                                                \
-  hipLaunchKernelGGL(attn_kernel<HH>, dim3(grid), dim3(64 * HH), 0, st, units, hdr, (const bf16x8*)QN, \
-                     (const bf16x8*)KVl, part_acc, (float2*)part_ml, n_tgt)
+  hipLaunchKernelGGL(attn_kernel<HH>, dim3(grid), dim3(64 * HH), 0, st, units, hdr, (const f16x8*)QN, \
+                     (const f16x8*)KVl, part_acc, (float2*)part_ml, n_tgt)
   switch (D) {
     case 64: STCA_ATTN(2); break;
     case 128: STCA_ATTN(4); break;
@@ -515,11 +548,11 @@ hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st) {
   A.save_u = f.save_u;
   A.save_lse = f.save_lse;
   A.out = (bf16_bits*)f.out;
-  A.QN = (bf16x8*)f.QN;
-  A.WoP = (const bf16x8*)f.WoP;
-  A.W1P = (const bf16x8*)f.W1P;
-  A.W2P = (const bf16x8*)f.W2P;
-  A.WqP = (const bf16x8*)f.WqP;
+  A.QN = (f16x8*)f.QN;
+  A.WoP = (const f16x8*)f.WoP;
+  A.W1P = (const f16x8*)f.W1P;
+  A.W2P = (const f16x8*)f.W2P;
+  A.WqP = (const f16x8*)f.WqP;
   if (f.n_tgt == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
   const size_t lds = (size_t)32 * (D + 8) * 2 + (f.mode == 0 ? 0 : (size_t)32 * (f.FC + 8) * 2);

@@ -5,6 +5,8 @@
 #include "common.h"
 #include "internal.h"
 
+#include <algorithm>
+
 namespace stca {
 
 namespace {
@@ -24,24 +26,28 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA
                                                    int64_t ldb, int transB, float* __restrict__ C,
                                                    int64_t ldc, float alpha, int epi,
                                                    const float* __restrict__ R, int64_t ldr,
-                                                   float* __restrict__ C2, int accumulate) {
+                                                   float* __restrict__ C2, int accumulate, int k_chunk) {
   __shared__ float As[GK][GT + 4];
   __shared__ float Bs[GK][GT + 4];
   const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
   const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
   float acc[4][4] = {};
-  for (int k0 = 0; k0 < K; k0 += GK) {
+  // split-K: workgroup z sums k in [z * k_chunk, (z + 1) * k_chunk) and adds
+  // its partial into C atomically (C was cleared or holds what to add to)
+  const int kb = blockIdx.z * k_chunk;
+  const int ke = min(K, kb + k_chunk);
+  for (int k0 = kb; k0 < ke; k0 += GK) {
     for (int e = threadIdx.x; e < GT * GK; e += 256) {
       // A tile: rows m0..m0+63, cols k0..k0+15, stored As[k][m]
       int mm = e % GT, kk = e / GT;
       int gm = m0 + mm, gk = k0 + kk;
       float v = 0.f;
-      if (gm < M && gk < K) v = transA ? ld(A, (int64_t)gk * lda + gm) : ld(A, (int64_t)gm * lda + gk);
+      if (gm < M && gk < ke) v = transA ? ld(A, (int64_t)gk * lda + gm) : ld(A, (int64_t)gm * lda + gk);
       As[kk][mm] = v;
       int nn = e % GT;
       int gn = n0 + nn;
       float w = 0.f;
-      if (gn < N && gk < K) w = transB ? ld(B, (int64_t)gn * ldb + gk) : ld(B, (int64_t)gk * ldb + gn);
+      if (gn < N && gk < ke) w = transB ? ld(B, (int64_t)gn * ldb + gk) : ld(B, (int64_t)gk * ldb + gn);
       Bs[kk][nn] = w;
     }
     __syncthreads();
@@ -69,6 +75,10 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA
       if (gn >= N) continue;
       float v = alpha * acc[i][j];
       float* c = C + (int64_t)gm * ldc + gn;
+      if (gridDim.z > 1) {
+        atomicAdd(c, v);
+        continue;
+      }
       if (epi == kEpiAddRes) v += R[(int64_t)gm * ldr + gn];
       if (epi == kEpiRelu) {
         if (C2) C2[(int64_t)gm * ldc + gn] = v;
@@ -286,15 +296,32 @@ inline dim3 grid1(int64_t n, int b) { return dim3(static_cast<unsigned>(ceil_div
 
 }  // namespace
 
+__global__ void fill2d_kernel(float* __restrict__ C, int64_t ldc, int M, int N) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < (int64_t)M * N) C[(i / N) * ldc + i % N] = 0.f;
+}
+
 hipError_t gemm_generic(int a_bf16, int b_bf16, int M, int N, int K, const void* A, int64_t lda,
                         int transA, const void* B, int64_t ldb, int transB, float* C, int64_t ldc,
                         float alpha, GemmEpi epi, const float* R, int64_t ldr, float* C2,
                         int accumulate, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
-  dim3 g(static_cast<unsigned>(ceil_div(N, GT)), static_cast<unsigned>(ceil_div(M, GT)));
+  const int64_t tiles = ceil_div(N, GT) * ceil_div(M, GT);
+  // long reductions (weight gradients over all rows) with few output tiles are
+  // split over K so the whole chip works on them and each partial sum is short
+  int splits = 1;
+  if (epi == kEpiStore && tiles < 256 && K >= 4096) {
+    splits = static_cast<int>(std::min<int64_t>(ceil_div(1024, tiles), K / 1024));
+    if (splits < 1) splits = 1;
+  }
+  const int k_chunk = static_cast<int>(round_up(ceil_div(K, splits), GK));
+  splits = static_cast<int>(ceil_div(K, k_chunk));
+  if (splits > 1 && !accumulate)
+    hipLaunchKernelGGL(fill2d_kernel, grid1((int64_t)M * N, 256), dim3(256), 0, st, C, ldc, M, N);
+  dim3 g(static_cast<unsigned>(ceil_div(N, GT)), static_cast<unsigned>(ceil_div(M, GT)), splits);
 #define STCA_GEMM(TA, TB)                                                                          \
   hipLaunchKernelGGL((gemm_kernel<TA, TB>), g, dim3(256), 0, st, M, N, K, (const TA*)A, lda, transA, \
-                     (const TB*)B, ldb, transB, C, ldc, alpha, (int)epi, R, ldr, C2, accumulate)
+                     (const TB*)B, ldb, transB, C, ldc, alpha, (int)epi, R, ldr, C2, accumulate, k_chunk)
   if (a_bf16 && b_bf16) STCA_GEMM(bf16_bits, bf16_bits);
   else if (a_bf16) STCA_GEMM(bf16_bits, float);
   else if (b_bf16) STCA_GEMM(float, bf16_bits);

@@ -56,7 +56,7 @@ class DeviceBatch:
             raise stca.StcaError(stca.STCA_ERR_INVALID_ARG, "stca_workspace_size")
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
         self.saved = None
-        if keep_saved or backward:
+        if keep_saved:
             self.saved_bytes = stca.stca_saved_size(self.dims, self.batch)
             self.saved = torch.empty(self.saved_bytes, dtype=torch.uint8, device=device)
             self.layout = stca.stca_saved_layout(self.dims, self.batch)
@@ -100,7 +100,7 @@ class DeviceBatch:
             "dw1": torch.empty((n, d, F), **f32), "dw2": torch.empty((n, F, d), **f32),
         }
         dw = stca.wgrads(g["dwq"], g["dwk"], g["dwv"], g["dwo"], g["dw1"], g["dw2"])
-        stca.stca_backward(self.dims, self.batch, self.hist, self.tgt, self.weights, self.saved, dout,
+        stca.stca_backward(self.dims, self.batch, self.hist, self.tgt, self.weights, dout,
                            g["dhist"], g["dtgt"], dw, self.bws, self.bws_bytes,
                            self.stream() if stream is None else stream)
         return g

@@ -81,8 +81,7 @@ def lib():
         L.stca_backward.restype = ctypes.c_int
         L.stca_backward.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
                                     P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                                    ctypes.c_void_p, P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t,
-                                    ctypes.c_void_p]
+                                    P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
         L.stca_device_status.restype = ctypes.c_int
         L.stca_device_status.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
         L.stca_status_string.restype = ctypes.c_char_p
@@ -162,9 +161,9 @@ def stca_forward(d, b, hist, tgt, w, out, saved, ws, ws_bytes: int, stream=None,
     return st
 
 
-def stca_backward(d, b, hist, tgt, w, saved, dout, dhist, dtgt, dw, ws, ws_bytes: int, stream=None,
+def stca_backward(d, b, hist, tgt, w, dout, dhist, dtgt, dw, ws, ws_bytes: int, stream=None,
                   check: bool = True) -> int:
-    st = lib().stca_backward(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w), _ptr(saved),
+    st = lib().stca_backward(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w),
                              _ptr(dout), _ptr(dhist), _ptr(dtgt), ctypes.byref(dw), _ptr(ws), int(ws_bytes),
                              _ptr(stream))
     if check and st != STCA_OK:

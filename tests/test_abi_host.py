@@ -103,14 +103,16 @@ def test_backward_argument_checks():
     b, keep = fake_batch([0, 40, 100], [0, 3, 9])
     dw = stca.wgrads(*([0x600000] * 6))
     args = (dims(), b, 0x200000, 0x300000, fake_weights())
-    st = stca.stca_backward(*args, None, 0x700000, 0x800000, 0x900000, dw, 0x500000, 1 << 40, check=False)
-    assert st == stca.STCA_ERR_INVALID_ARG  # saved is required
+    st = stca.stca_backward(*args, 0, 0x800000, 0x900000, dw, 0x500000, 1 << 40, check=False)
+    assert st == stca.STCA_ERR_INVALID_ARG  # dout is required when there are targets
     need = stca.stca_workspace_size(dims(), b, True)
-    st = stca.stca_backward(*args, 0xA00000, 0x700000, 0x800000, 0x900000, dw, 0x500000, need - 1, check=False)
+    st = stca.stca_backward(*args, 0x700000, 0x800000, 0x900000, dw, 0x500000, need - 1, check=False)
     assert st == stca.STCA_ERR_WORKSPACE
     bad_dw = stca.wgrads(0x600000, 0, 0x600000, 0x600000, 0x600000, 0x600000)
-    st = stca.stca_backward(*args, 0xA00000, 0x700000, 0x800000, 0x900000, bad_dw, 0x500000, need, check=False)
+    st = stca.stca_backward(*args, 0x700000, 0x800000, 0x900000, bad_dw, 0x500000, need, check=False)
     assert st == stca.STCA_ERR_INVALID_ARG
+    st = stca.stca_backward(*args, 0x700008, 0x800000, 0x900000, dw, 0x500000, need, check=False)
+    assert st == stca.STCA_ERR_INVALID_ARG  # misaligned
 
 
 def test_saved_layout_is_disjoint_and_sized():

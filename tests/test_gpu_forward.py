@@ -153,10 +153,12 @@ def test_rlb_equals_one_target_per_request(torch):
     nb = W.replicate_per_target(b)
     y, a, _, _ = run_gpu(torch, b)
     yn, an, _, _ = run_gpu(torch, nb)
-    assert rowerr(yn, y) <= TOL["bf16"] / 2
-    assert max(rowerr(an[i], a[i]) for i in range(2)) <= TOL["bf16"] / 2
+    e_y, e_a = rowerr(yn, y), max(rowerr(an[i], a[i]) for i in range(2))
+    print(f"[rlb] instance-wise vs request-level: err(Y)={e_y:.2e} err(a)={e_a:.2e}")
+    assert e_y <= TOL["bf16"] and e_a <= TOL["bf16"]
     ref = O.forward(b.f64())
     assert rowerr(yn, ref["out"]) <= TOL["bf16"]
+    assert max(rowerr(an[i], ref["a"][i]) for i in range(2)) <= TOL["bf16"]
 
 
 def test_target_permutation_within_request(torch):
