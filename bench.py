@@ -64,6 +64,24 @@ def roofline_entry(label, ms, flop, byts, peak_tf):
             "traffic": None}
 
 
+def measured_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter
+    summary (FETCH_SIZE and WRITE_SIZE scaled by a plain copy's readings), or
+    None when no summary covers this workload or the kernel source changed
+    since the counters were taken."""
+    import glob
+    import hashlib
+    for path in glob.glob(os.path.join(ROOT, "profiles", "traffic_*.json")):
+        rec = json.load(open(path))
+        if rec.get("workload") != workload or kernel not in rec.get("kernels", {}):
+            continue
+        src = os.path.join(ROOT, rec["source"])
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+            return None
+        return rec["kernels"][kernel]["bytes"]
+    return None
+
+
 def cpu_baseline(wl: W.Workload, budget_s: float):
     """The fp64 oracle, as it is, on requests of the same workload taken in
     order until the time budget is spent."""
@@ -127,6 +145,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
     ap.add_argument("--ablation", action="store_true",
                     help="also time one target per request and the instance-wise (non-RLB) layout")
+    ap.add_argument("--copy-gib", type=float, default=0.0,
+                    help="instead: time a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -135,6 +155,8 @@ def main() -> int:
         return 2
 
     import torch
+    if args.copy_gib > 0:
+        return copy_calibration(args)
     from paper_2511_06077_amd.device import DeviceBatch
     wl = W.WORKLOADS[args.workload]
     t0 = time.time()
@@ -164,6 +186,7 @@ def main() -> int:
     flop, byts = kernel_work(dom, b, es)
     roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, peak_tf)
     roof["kernel"] = dom
+    roof["traffic"] = measured_traffic(wl.name, dom)
     c = accounting.stage_costs(b.hist_len, b.n_tgt, wl.d_model, wl.n_layers, es)
     roof_ms = sum(max(v["flop"] / (peak_tf * 1e12), v["bytes"] / (PEAK_HBM_GBS * 1e9)) for v in c.values()) * 1e3
     value = b.n_tgt_total / (ms_step * 1e-3)
@@ -197,6 +220,28 @@ def main() -> int:
         log("[bench] timing the CPU oracle")
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
+    return 0
+
+
+def copy_calibration(args) -> int:
+    """A plain copy of known size: reads and writes args.copy_gib GiB per
+    launch, so HBM byte counters read on it give their scale."""
+    import torch
+    n = int(args.copy_gib * 2**30) // 4
+    src = torch.randn(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(args.warmup):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(args.steps):
+        dst.copy_(src)
+    end.record()
+    torch.cuda.synchronize()
+    ms = start.elapsed_time(end) / args.steps
+    print(json.dumps({"copy_bytes_each_way": n * 4, "ms_per_copy": ms,
+                      "gbs_read_plus_write": 2 * n * 4 / (ms * 1e-3) / 1e9}), flush=True)
     return 0
 
 
