@@ -47,6 +47,15 @@ def kernel_work(label: str, b: W.Batch, es: int):
         return 4.0 * Ls * wl.d_model ** 2 * n, es * Ls * wl.d_model * (1 + 2 * n)
     if label == "attn":
         return c["attn"]["flop"] / n, c["attn"]["bytes"] / n
+    if label in ("fused", "fused_wide"):
+        # one layer: project the rows of the requests this launch serves
+        # (X read once) and attend; units with up to 32 targets go to "fused"
+        L = b.hist_len.astype(np.float64)
+        m = b.n_tgt.astype(np.float64)
+        sel = (m > 0) & ((m <= 32) if label == "fused" else (m > 32))
+        d = wl.d_model
+        return (4.0 * L[sel].sum() * d * d + 4.0 * (m[sel] * L[sel]).sum() * d,
+                es * L[sel].sum() * d)
     if label == "update":
         return c["update"]["flop"] / n, 0.0
     return 0.0, 0.0
@@ -108,6 +117,22 @@ def cpu_baseline(wl: W.Workload, budget_s: float):
                       f"{spent:.1f} s of fp64 CPU work"}
 
 
+def plain_forward(db, steps: int, warmup: int) -> float:
+    """The same K steps without per-kernel events: total milliseconds."""
+    import torch
+    stream = torch.cuda.current_stream(db.device)
+    for _ in range(warmup):
+        db.forward()
+    torch.cuda.synchronize(db.device)
+    start, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for _ in range(steps):
+        db.forward()
+    end.record(stream)
+    torch.cuda.synchronize(db.device)
+    return start.elapsed_time(end)
+
+
 def timed_forward(db, steps: int, warmup: int):
     import torch
     dev = db.device
@@ -166,7 +191,8 @@ def main() -> int:
     log(f"[bench] workspace {db.ws_bytes / 2**30:.2f} GiB; path {stca.stca_path(db.dims)}")
     total_ms, per = timed_forward(db, args.steps, args.warmup)
     ms_step = total_ms / args.steps
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step")
+    plain_ms = plain_forward(db, args.steps, 1) / args.steps
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step with per-kernel events, {plain_ms:.3f} without")
 
     es = 2 if wl.dtype == "bf16" else 4
     peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
@@ -183,6 +209,7 @@ def main() -> int:
         kernels[lab] = ent
     dom = max((k for k in kernels if kernel_work(k, b, es) != (0.0, 0.0)),
               key=lambda k: kernels[k]["ms_per_step"])
+    kv_mode = os.environ.get("STCA_KV", "fused")
     flop, byts = kernel_work(dom, b, es)
     roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, peak_tf)
     roof["kernel"] = dom
@@ -203,7 +230,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": wl.name, "requests": wl.n_requests,
+        "config": {"workload": wl.name, "kv": kv_mode, "requests": wl.n_requests,
                    "targets_per_request": wl.n_targets or list(wl.tgt_range),
                    "hist_len": wl.hist_len or list(wl.hist_range), "d_model": wl.d_model,
                    "heads": wl.n_heads, "layers": wl.n_layers, "ffn_hidden": wl.ffn_hidden},
@@ -211,6 +238,7 @@ def main() -> int:
         "path_roofline": {"ms": roof_ms, "frac": roof_ms / ms_step,
                           "targets_per_s": b.n_tgt_total / (roof_ms * 1e-3)},
         "kernels": kernels,
+        "ms_per_step_without_kernel_events": plain_ms,
     }
     if args.ablation:
         rec["ablation"] = ablation(wl, args)
@@ -251,6 +279,19 @@ def ablation(wl: W.Workload, args):
     import torch
     from paper_2511_06077_amd.device import DeviceBatch
     out = {}
+    if os.environ.get("STCA_KV") != "materialize":
+        os.environ["STCA_KV"] = "materialize"
+        try:
+            db = DeviceBatch(W.make_batch(wl, with_grad=False), device="cuda:0")
+            ms, per = timed_forward(db, max(3, args.steps // 4), 1)
+            ms /= max(3, args.steps // 4)
+            out["materialized_kv"] = {"ms_per_step": ms, "targets_per_s": db.b.n_tgt_total / (ms * 1e-3),
+                                      "kernels_ms_per_step": {k: float(np.sum(v)) / max(3, args.steps // 4)
+                                                              for k, v in per.items()}}
+            del db
+            torch.cuda.empty_cache()
+        finally:
+            del os.environ["STCA_KV"]
     if wl.n_targets > 1 and wl.hist_range is None:
         one = W.Workload(wl.name + "_m1", wl.n_requests, wl.d_model, wl.n_heads, wl.n_layers, wl.dtype, wl.seed,
                          hist_len=wl.hist_len, n_targets=1)

@@ -62,8 +62,8 @@ typedef enum {
 typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
 
 /* Model shape.  d_model % n_heads == 0 and ffn_hidden a multiple of 32.
- * STCA_BF16 with d_head = d_model / n_heads = 32 and d_model in {64, 128, 256}
- * runs on the bf16 MFMA kernels; every other shape with d_head in
+ * STCA_BF16 with d_head = d_model / n_heads = 32, d_model in {64, 128, 256}
+ * and ffn_hidden a multiple of 64 runs on the bf16 MFMA kernels; every other shape with d_head in
  * {8, 16, 32, 64} (either dtype) runs on the generic fp32-arithmetic kernels
  * (stca_path tells which). */
 typedef struct {
@@ -109,10 +109,9 @@ typedef struct {
  * per-layer intermediates back.  Each per-layer tensor is stacked on a leading
  * layer axis: s [n][n_tgt][d] (layer input state), a [n][n_tgt][d] (head
  * concatenation before W_O), u [n][n_tgt][d] (state after the attention
- * residual), lse [n][n_tgt][h] (natural log-sum-exp of each head's scores).
- * kv is opaque (the projected history in the kernels' own layout). */
+ * residual), lse [n][n_tgt][h] (natural log-sum-exp of each head's scores). */
 typedef struct {
-  size_t s, a, u, lse, kv;
+  size_t s, a, u, lse;
   size_t total;
 } stca_saved_layout_t;
 
@@ -131,9 +130,12 @@ stca_status_t stca_saved_layout(const stca_dims_t* dims, const stca_batch_t* bat
 /* Forward pass: out[n_tgt][d] (storage dtype) = s^(n) for every target.
  *  hist  [n_hist][d], tgt [n_tgt][d]  storage dtype, device
  *  saved nullable; when given (stca_saved_size bytes) the per-layer
- *        intermediates (see stca_saved_layout_t) and the projected history
- *        are written there
- *  ws    device workspace of ws_bytes >= stca_workspace_size(dims, batch, 0) */
+ *        intermediates (see stca_saved_layout_t) are written there
+ *  ws    device workspace of ws_bytes >= stca_workspace_size(dims, batch, 0)
+ * On the bf16 MFMA path each layer's K/V is projected inside the attention
+ * kernel and never stored; with the environment variable STCA_KV=materialize
+ * (read at every call, including stca_workspace_size) one GEMM first writes
+ * every layer's K/V to the workspace and the attention streams it. */
 stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch,
                            const void* hist, const void* tgt, const stca_weights_t* w,
                            void* out, void* saved, void* ws, size_t ws_bytes,

@@ -34,7 +34,8 @@ int path_of(const stca_dims_t* d) {
     return STCA_ERR_INVALID_ARG;
   const int dh = d->d_model / d->n_heads;
   if (d->ffn_hidden % 32 != 0) return STCA_ERR_UNSUPPORTED;
-  if (d->dtype == STCA_BF16 && dh == 32 && (d->d_model == 64 || d->d_model == 128 || d->d_model == 256))
+  if (d->dtype == STCA_BF16 && dh == 32 && (d->d_model == 64 || d->d_model == 128 || d->d_model == 256) &&
+      d->ffn_hidden % 64 == 0)
     return 1;
   if (dh == 8 || dh == 16 || dh == 32 || dh == 64) return 0;
   return STCA_ERR_UNSUPPORTED;
@@ -84,16 +85,26 @@ int chunk_blocks_for(const stca_batch_t* b, int n_cu) {
   return static_cast<int>(c);
 }
 
+// The bf16 path projects the history inside the attention kernel by default
+// (K/V never reach HBM).  STCA_KV=materialize selects the two-kernel form
+// instead: one GEMM writes every layer's K/V, then the attention streams it.
+bool materialize_kv() {
+  const char* e = std::getenv("STCA_KV");
+  return e && std::strcmp(e, "materialize") == 0;
+}
+
 int64_t max_units_for(const stca_batch_t* b, int chunk_blocks) {
   if (b->hist_off_host)
     return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks);
   return (ceil_div(b->n_tgt, kTargetGroup) + b->n_requests) * kMaxChunks;
 }
 
+// hidden columns staged in LDS at a time by the update kernel (F % 64 == 0 on
+// that path, so the chunk is a multiple of 64: four MFMA k-steps or more)
 int ffn_chunk(int F) {
-  for (int c : {512, 256, 128, 64, 32})
+  for (int c : {512, 256, 128, 64})
     if (F % c == 0) return c;
-  return 32;
+  return 64;
 }
 
 struct Layout {
@@ -102,6 +113,7 @@ struct Layout {
   int64_t nh, nt, nblocks;
   int chunk_blocks;
   int64_t max_units;
+  bool any_narrow, any_wide;  // requests with 1..32 / 33+ targets (both true without host offsets)
   // common
   size_t hdr, units, tchunks, part_acc, part_ml, state_a, state_b;
   // fast
@@ -127,6 +139,18 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
   L->chunk_blocks = chunk_blocks_for(b, device_cus());
   L->max_units = max_units_for(b, L->chunk_blocks);
+  L->any_narrow = L->any_wide = true;
+  if (b->tgt_off_host) {
+    L->any_narrow = L->any_wide = false;
+    for (int r = 0; r < b->n_requests; ++r) {
+      const int64_t m = b->tgt_off_host[r + 1] - b->tgt_off_host[r];
+      // target groups are kTargetGroup wide; the last group of a request is what may be narrow
+      for (int64_t g0 = 0; g0 < m; g0 += kTargetGroup) {
+        if (m - g0 > 32) L->any_wide = true;
+        else L->any_narrow = true;
+      }
+    }
+  }
   const size_t d = L->d, nt = L->nt, nh = L->nh, F = L->F, n = L->n;
   Bump m;
   L->hdr = m.take(sizeof(WsHeader));
@@ -145,7 +169,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->wqp = m.take(2 * n * d * d);
       L->w1p = m.take(2 * n * d * F);
       L->w2p = m.take(2 * n * d * F);
-      L->kv = with_saved ? 0 : m.take(2 * n * L->nblocks * kBlockTokens * 2 * d);
+      L->kv = materialize_kv() ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
     } else {
       L->kv32 = m.take(4 * nh * 2 * d);
       L->q32 = m.take(4 * nt * d);
@@ -186,7 +210,6 @@ bool saved_layout(const stca_dims_t* dims, const stca_batch_t* b, stca_saved_lay
   s->a = m.take(4 * n * nt * d);
   s->u = m.take(4 * n * nt * d);
   s->lse = m.take(4 * n * nt * h);
-  s->kv = p == 1 ? m.take(2 * n * ceil_div(b->n_hist, kBlockTokens) * kBlockTokens * 2 * d) : m.off;
   s->total = m.off;
   return true;
 }
@@ -256,10 +279,14 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wq"));
   HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, 1, st)); HIPCHK(rec.mark("pack_w1"));
   HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, 1, st)); HIPCHK(rec.mark("pack_w2"));
-  char* kv = saved ? at<char>(saved, SL.kv) : at<char>(ws, L.kv);
-  if (L.nh > 0)
-    HIPCHK(fast_proj(d, hist, L.nh, L.nblocks, at<char>(ws, L.wkp), at<char>(ws, L.wvp), kv, n,
-                     fast_proj_parts(n, L.nblocks, device_cus()), st)); HIPCHK(rec.mark("proj"));
+  const bool mat = materialize_kv();
+  char* kv = at<char>(ws, L.kv);
+  if (mat) {
+    if (L.nh > 0)
+      HIPCHK(fast_proj(d, hist, L.nh, L.nblocks, at<char>(ws, L.wkp), at<char>(ws, L.wvp), kv, n,
+                       fast_proj_parts(n, L.nblocks, device_cus()), st));
+    HIPCHK(rec.mark("proj"));
+  }
   const size_t kv_layer = (size_t)L.nblocks * kBlockTokens * 2 * d * 2;
   FastUpdate f{};
   f.n_layers = n;
@@ -286,9 +313,25 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   f.s_out = state(0);
   HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
   const int grid = static_cast<int>(std::min<int64_t>(L.max_units, 8 * (int64_t)device_cus()));
+  // the fused kernel keeps one workgroup per CU resident (two 256-VGPR waves
+  // per SIMD) and loops over its units, loading its weight columns once
+  const int fgrid = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(L.max_units, device_cus())));
   for (int i = 0; i < n; ++i) {
-    HIPCHK(fast_attn(d, units, hdr, grid, f.QN, kv + i * kv_layer, at<float>(ws, L.part_acc), at<char>(ws, L.part_ml), L.nt,
-                     st)); HIPCHK(rec.mark("attn"));
+    if (mat) {
+      HIPCHK(fast_attn(d, units, hdr, grid, f.QN, kv + i * kv_layer, at<float>(ws, L.part_acc),
+                       at<char>(ws, L.part_ml), L.nt, st));
+      HIPCHK(rec.mark("attn"));
+    } else {
+      for (int wide = 0; wide < 2; ++wide) {
+        if (!(wide ? L.any_wide : L.any_narrow)) {  // no request of this width: nothing to launch
+          HIPCHK(rec.mark(wide ? "fused_wide" : "fused"));
+          continue;
+        }
+        HIPCHK(fast_fused(d, wide, units, hdr, fgrid, f.QN, hist, L.nh, at<char>(ws, L.wkp), at<char>(ws, L.wvp), i,
+                          at<float>(ws, L.part_acc), at<char>(ws, L.part_ml), L.nt, st));
+        HIPCHK(rec.mark(wide ? "fused_wide" : "fused"));
+      }
+    }
     f.mode = 1;
     f.layer = i;
     f.s_in = state(i);
@@ -510,7 +553,7 @@ stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch, c
 int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
   Layout L;
   if (!make_layout(dims, batch, 0, false, &L)) return -1;
-  if (L.path == 1) return 1 + 6 + 1 + 1 + 2 * L.n;
+  if (L.path == 1) return materialize_kv() ? 1 + 6 + 1 + 1 + 2 * L.n : 1 + 6 + 1 + 3 * L.n;
   return 1 + 1 + 8 * L.n + 1;
 }
 

@@ -29,9 +29,10 @@ struct Unit {
 
 // Header at the start of every workspace.
 struct WsHeader {
-  int32_t status;   // stca_status_t recorded by the device scheduler
-  int32_t n_units;  // units the scheduler emitted
-  int32_t pad[62];
+  int32_t status;    // stca_status_t recorded by the device scheduler
+  int32_t n_units;   // units the scheduler emitted
+  int32_t n_narrow;  // units [0, n_narrow) have at most 32 targets, the rest more
+  int32_t pad[61];
 };
 
 __device__ __forceinline__ float to_f32(float x) { return x; }

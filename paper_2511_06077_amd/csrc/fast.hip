@@ -68,6 +68,11 @@ __device__ __forceinline__ f16x8 zero8h() {
   return r;
 }
 
+// 2^x with the hardware instruction alone: the arguments are max-subtracted
+// scores (<= 0), whose results below 2^-126 may flush to zero without effect
+// on the softmax, so the library's denormal-safe expansion is not needed.
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 __device__ __forceinline__ uint16_t f16_bits(float x) {
   return __builtin_bit_cast(uint16_t, static_cast<_Float16>(x));
 }
@@ -189,34 +194,100 @@ __global__ __launch_bounds__(64 * (D / 32)) void proj_kernel(const bf16_bits* __
   }
 }
 
-// ----------------------------------------------- K3: fused attention
+// ------------------------------------------ online softmax over blocks
+// State of one wave (one head) for all of a unit's targets (up to 64: two
+// 32-wide column groups).  Online softmax in log2 units; the result is an
+// unnormalised partial (acc, max, sum) per (chunk, target, head), merged by
+// the update kernel.
+template <int H, int NG>
+struct Online {
+  f16x8 qop[NG][2];
+  f32x16 O[NG];
+  float m[NG], l[NG];
+
+  __device__ __forceinline__ void init(const Unit& un, const f16x8* __restrict__ QN, int j, int tcol, int hi) {
+    constexpr int D = H * DH;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const int tt = g * 32 + tcol;
+      const bool ok = tt < un.nt;
+      const f16x8* q = QN + ((int64_t)(un.t0 + tt) * D + j * DH) / 8;
+      qop[g][0] = ok ? q[hi] : zero8h();
+      qop[g][1] = ok ? q[2 + hi] : zero8h();
+      O[g] = f32x16{};
+      m[g] = -INFINITY;
+      l[g] = 0.f;
+    }
+  }
+
+  // kv: K slices 0, 1 and V slices 0, 1 of history block b (operand order)
+  __device__ __forceinline__ void step(const f16x8 (&kv)[4], int b, const Unit& un, int hi) {
+    const bool full = b * 32 >= un.l0 && b * 32 + 32 <= un.l1;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      f32x16 s = mfma(kv[0], qop[g][0], f32x16{});
+      s = mfma(kv[1], qop[g][1], s);
+      if (!full) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int tok = b * 32 + 8 * (v / 4) + 4 * hi + (v % 4);
+          if (tok < un.l0 || tok >= un.l1) s[v] = -INFINITY;
+        }
+      }
+      float bm = s[0];
+#pragma unroll
+      for (int v = 1; v < 16; ++v) bm = fmaxf(bm, s[v]);
+      bm = fmaxf(bm, __shfl_xor(bm, 32));
+      const float mn = fmaxf(m[g], bm);
+      const float sc = fast_exp2(m[g] - mn);
+      m[g] = mn;
+      float ps = 0.f;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        s[v] = fast_exp2(s[v] - mn);
+        ps += s[v];
+      }
+      l[g] = l[g] * sc + ps;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) O[g][v] *= sc;
+      O[g] = mfma(kv[2], pack8h(s, 0), O[g]);
+      O[g] = mfma(kv[3], pack8h(s, 8), O[g]);
+    }
+  }
+
+  __device__ __forceinline__ void finish(const Unit& un, int j, int tcol, int hi, float* __restrict__ part_acc,
+                                         float2* __restrict__ part_ml, int64_t n_tgt) {
+    constexpr int D = H * DH;
+#pragma unroll
+    for (int g = 0; g < NG; ++g) {
+      const float lt = l[g] + __shfl_xor(l[g], 32);
+      const int tt = g * 32 + tcol;
+      if (tt < un.nt) {
+        const int64_t row = (int64_t)un.c * n_tgt + un.t0 + tt;
+        float* pa = part_acc + row * D + j * DH + 4 * hi;
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg)
+          *reinterpret_cast<float4*>(pa + 8 * gg) =
+              make_float4(O[g][4 * gg], O[g][4 * gg + 1], O[g][4 * gg + 2], O[g][4 * gg + 3]);
+        if (hi == 0) part_ml[row * H + j] = make_float2(m[g], lt);
+      }
+    }
+  }
+};
+
+// ------------------------------------ K3: attention over materialised K/V
 // One workgroup per unit (a request's target group x a chunk of its history
-// blocks), one wave per head.  All of the unit's targets (up to 64: two
-// 32-wide column groups) are held by every wave, so each K/V byte is read
-// from HBM once per unit whatever the number of targets.  Online softmax in
-// log2 units; the result is an unnormalised partial (acc, max, sum) per
-// (chunk, target, head), merged by the update kernel.
+// blocks), one wave per head.  All of the unit's targets are held by every
+// wave, so each K/V byte is read from HBM once per unit whatever the number
+// of targets.  K/V blocks are double-buffered in registers.
 template <int H, int NG>
 __device__ __forceinline__ void attn_unit(const Unit& un, const f16x8* __restrict__ QN,
                                           const f16x8* __restrict__ KVl, float* __restrict__ part_acc,
                                           float2* __restrict__ part_ml, int64_t n_tgt) {
-  constexpr int D = H * DH;
   const int j = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int tcol = lane % 32, hi = lane / 32;
-  f16x8 qop[NG][2];
-  f32x16 O[NG];
-  float m[NG], l[NG];
-#pragma unroll
-  for (int g = 0; g < NG; ++g) {
-    const int tt = g * 32 + tcol;
-    const bool ok = tt < un.nt;
-    const f16x8* q = QN + ((int64_t)(un.t0 + tt) * D + j * DH) / 8;
-    qop[g][0] = ok ? q[hi] : zero8h();
-    qop[g][1] = ok ? q[2 + hi] : zero8h();
-    O[g] = f32x16{};
-    m[g] = -INFINITY;
-    l[g] = 0.f;
-  }
+  Online<H, NG> st;
+  st.init(un, QN, j, tcol, hi);
   const f16x8* base = KVl + (int64_t)j * 4 * 64 + lane;
   auto ld = [&](int64_t b, f16x8 (&r)[4]) {
     const f16x8* p = base + b * (H * 4 * 64);
@@ -231,52 +302,9 @@ __device__ __forceinline__ void attn_unit(const Unit& un, const f16x8* __restric
 #pragma unroll
     for (int i = 0; i < 4; ++i) cu[i] = nx[i];
     if (b + 1 < un.b1) ld(b + 1, nx);
-    const bool full = b * 32 >= un.l0 && b * 32 + 32 <= un.l1;
-#pragma unroll
-    for (int g = 0; g < NG; ++g) {
-      f32x16 s = mfma(cu[0], qop[g][0], f32x16{});
-      s = mfma(cu[1], qop[g][1], s);
-      if (!full) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int tok = b * 32 + 8 * (v / 4) + 4 * hi + (v % 4);
-          if (tok < un.l0 || tok >= un.l1) s[v] = -INFINITY;
-        }
-      }
-      float bm = s[0];
-#pragma unroll
-      for (int v = 1; v < 16; ++v) bm = fmaxf(bm, s[v]);
-      bm = fmaxf(bm, __shfl_xor(bm, 32));
-      const float mn = fmaxf(m[g], bm);
-      const float sc = exp2f(m[g] - mn);
-      m[g] = mn;
-      float ps = 0.f;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        s[v] = exp2f(s[v] - mn);
-        ps += s[v];
-      }
-      l[g] = l[g] * sc + ps;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) O[g][v] *= sc;
-      O[g] = mfma(cu[2], pack8h(s, 0), O[g]);
-      O[g] = mfma(cu[3], pack8h(s, 8), O[g]);
-    }
+    st.step(cu, b, un, hi);
   }
-#pragma unroll
-  for (int g = 0; g < NG; ++g) {
-    const float lt = l[g] + __shfl_xor(l[g], 32);
-    const int tt = g * 32 + tcol;
-    if (tt < un.nt) {
-      const int64_t row = (int64_t)un.c * n_tgt + un.t0 + tt;
-      float* pa = part_acc + row * D + j * DH + 4 * hi;
-#pragma unroll
-      for (int gg = 0; gg < 4; ++gg)
-        *reinterpret_cast<float4*>(pa + 8 * gg) =
-            make_float4(O[g][4 * gg], O[g][4 * gg + 1], O[g][4 * gg + 2], O[g][4 * gg + 3]);
-      if (hi == 0) part_ml[row * H + j] = make_float2(m[g], lt);
-    }
-  }
+  st.finish(un, j, tcol, hi, part_acc, part_ml, n_tgt);
 }
 
 template <int H>
@@ -293,6 +321,103 @@ __global__ __launch_bounds__(64 * H) void attn_kernel(const Unit* __restrict__ u
     else
       attn_unit<H, 1>(un, QN, KVl, part_acc, part_ml, n_tgt);
   }
+}
+
+// ------------------------- K13: projection fused into the attention
+// The same attention, but each 32-row history block is projected to this
+// layer's K and V inside the kernel and consumed from registers: nothing is
+// written to HBM, and the history is read once per layer instead of K and V
+// being written once and read back.  One wave per head keeps its W_K and W_V
+// columns in registers for the whole (persistent) kernel; the workgroup
+// stages each X block through a double-buffered LDS tile shared by all heads.
+// The projection's result registers are exactly the attention's operand
+// order (see the layout note at the top), so they are converted to fp16 in
+// place and fed to the score and P.V MFMAs.
+template <int H, int NG>
+__device__ __forceinline__ void fused_unit(const Unit& un, const f16x8* __restrict__ QN,
+                                           const bf16_bits* __restrict__ X, int64_t n_hist,
+                                           const bf16x8 (&wk)[H * DH / 16], const bf16x8 (&wv)[H * DH / 16],
+                                           bf16_bits (*xs)[32 * (H * DH + 8)], float* __restrict__ part_acc,
+                                           float2* __restrict__ part_ml, int64_t n_tgt) {
+  constexpr int D = H * DH;
+  constexpr int KS = D / 16;
+  constexpr int ROW = D + 8;
+  constexpr int NT = 64 * H;
+  const int j = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tcol = lane % 32, hi = lane / 32;
+  auto load = [&](int64_t b, uint4 (&r)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + i * NT;
+      const int row = c / (D / 8), col8 = c % (D / 8);
+      const int64_t grow = b * 32 + row;
+      r[i] = grow < n_hist ? *reinterpret_cast<const uint4*>(X + grow * D + col8 * 8) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto stash = [&](int buf, const uint4 (&r)[2]) {
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int c = threadIdx.x + i * NT;
+      const int row = c / (D / 8), col8 = c % (D / 8);
+      *reinterpret_cast<uint4*>(&xs[buf][row * ROW + col8 * 8]) = r[i];
+    }
+  };
+  Online<H, NG> st;
+  st.init(un, QN, j, tcol, hi);
+  uint4 nxt[2];
+  load(un.b0, nxt);
+  stash(0, nxt);
+  __syncthreads();
+  for (int b = un.b0; b < un.b1; ++b) {
+    const int cur = (b - un.b0) & 1;
+    if (b + 1 < un.b1) load(b + 1, nxt);
+    f32x16 ak = {}, av = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 xo = *reinterpret_cast<const bf16x8*>(&xs[cur][tcol * ROW + ks * 16 + hi * 8]);
+      ak = mfma(wk[ks], xo, ak);
+      av = mfma(xo, wv[ks], av);
+    }
+    const f16x8 kv[4] = {pack8h(ak, 0), pack8h(ak, 8), pack8h(av, 0), pack8h(av, 8)};
+    st.step(kv, b, un, hi);
+    if (b + 1 < un.b1) stash(cur ^ 1, nxt);
+    __syncthreads();
+  }
+  st.finish(un, j, tcol, hi, part_acc, part_ml, n_tgt);
+}
+
+// Instantiated once per target-group width NG (units with up to 32 targets,
+// and units with 33..64), so each variant gets its own register allocation;
+// the scheduler lists each width's units as one contiguous range.
+template <int D, int NG>
+__global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __restrict__ units,
+                                                              const WsHeader* __restrict__ hdr,
+                                                              const f16x8* __restrict__ QN,
+                                                              const bf16_bits* __restrict__ X, int64_t n_hist,
+                                                              const bf16x8* __restrict__ WkP,
+                                                              const bf16x8* __restrict__ WvP, int layer,
+                                                              float* __restrict__ part_acc,
+                                                              float2* __restrict__ part_ml, int64_t n_tgt) {
+  constexpr int H = D / DH;
+  constexpr int KS = D / 16;
+  __shared__ __attribute__((aligned(16))) bf16_bits xs[2][32 * (D + 8)];
+  // this width's units: [0, n_narrow) or [n_narrow, n_units)
+  const int ub = NG == 1 ? 0 : hdr->n_narrow;
+  const int ue = NG == 1 ? hdr->n_narrow : hdr->n_units;
+  if (ub + static_cast<int>(blockIdx.x) >= ue) return;
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  bf16x8 wk[KS], wv[KS];
+  {
+    const bf16x8* pk = WkP + ((int64_t)(layer * H + wave) * KS) * 64 + lane;
+    const bf16x8* pv = WvP + ((int64_t)(layer * H + wave) * KS) * 64 + lane;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      wk[ks] = pk[ks * 64];
+      wv[ks] = pv[ks * 64];
+    }
+  }
+  for (int u = ub + blockIdx.x; u < ue; u += gridDim.x)
+    fused_unit<H, NG>(units[u], QN, X, n_hist, wk, wv, xs, part_acc, part_ml, n_tgt);
 }
 
 // ------------------------------------------------ K4: target update
@@ -351,12 +476,27 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       *reinterpret_cast<uint2*>(p + 8 * g) = pk;
     }
   };
+  // acc = W^T act^T over `ksteps` k-steps (a multiple of 4).  The weight
+  // operands come from L2; they are fetched four k-steps ahead so the loop
+  // is not one L2 round trip per MFMA.
   auto gemm = [&](const f16x8* Wp, const uint16_t* src, int src_row, int ksteps) {
     f32x16 acc = {};
     const uint16_t* b = src + tcol * src_row + 8 * hi;
-#pragma unroll 4
-    for (int ks = 0; ks < ksteps; ++ks)
-      acc = mfma(Wp[ks * 64 + lane], *reinterpret_cast<const f16x8*>(b + ks * 16), acc);
+    const f16x8* w = Wp + lane;
+    f16x8 cur[4], nxt[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) cur[i] = w[i * 64];
+    for (int k0 = 0; k0 < ksteps; k0 += 4) {
+      if (k0 + 4 < ksteps) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) nxt[i] = w[(k0 + 4 + i) * 64];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        acc = mfma(cur[i], *reinterpret_cast<const f16x8*>(b + (k0 + i) * 16), acc);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) cur[i] = nxt[i];
+    }
     return acc;
   };
 
@@ -379,39 +519,67 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
     }
     __syncthreads();
   } else {
-    // merge partials: one thread per (target, head, quarter of the head)
-    for (int it = threadIdx.x; it < 32 * H * 4; it += 64 * NW) {
-      const int row = it / (H * 4), j = (it / 4) % H, qq = it % 4;
+    // merge partials: two threads per (target, head), 16 dimensions each.
+    // Every chunk's (max, sum) is requested at once and the accumulators four
+    // chunks at a time, so the merge costs a few memory round trips.
+    {
+      const int pair = threadIdx.x >> 1, half = threadIdx.x & 1;
+      const int row = pair / H, j = pair % H;
       const int64_t tt = tb + row;
-      float av[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+      float av[16];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) av[i] = 0.f;
       if (tt < A.n_tgt) {
         const int nch = A.tchunks[tt];
-        float M = -INFINITY;
-        for (int c = 0; c < nch; ++c) M = fmaxf(M, A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j].x);
-        float L = 0.f;
-        for (int c = 0; c < nch; ++c) {
-          const float2 ml = A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j];
-          const float wc = exp2f(ml.x - M);
-          L += wc * ml.y;
-          const float4* pa =
-              reinterpret_cast<const float4*>(A.part_acc + ((int64_t)c * A.n_tgt + tt) * D + j * DH + qq * 8);
-          const float4 x0 = pa[0], x1 = pa[1];
-          av[0] += wc * x0.x; av[1] += wc * x0.y; av[2] += wc * x0.z; av[3] += wc * x0.w;
-          av[4] += wc * x1.x; av[5] += wc * x1.y; av[6] += wc * x1.z; av[7] += wc * x1.w;
+        float2 ml[kMaxChunks];
+#pragma unroll
+        for (int c = 0; c < kMaxChunks; ++c)
+          ml[c] = c < nch ? A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j] : make_float2(-INFINITY, 0.f);
+        float M = ml[0].x;
+#pragma unroll
+        for (int c = 1; c < kMaxChunks; ++c) M = fmaxf(M, ml[c].x);
+        float L = 0.f, wc[kMaxChunks];
+#pragma unroll
+        for (int c = 0; c < kMaxChunks; ++c) {
+          wc[c] = c < nch ? exp2f(ml[c].x - M) : 0.f;
+          L += wc[c] * ml[c].y;
+        }
+#pragma unroll
+        for (int c0 = 0; c0 < kMaxChunks; c0 += 4) {
+          if (c0 >= nch) break;
+          float4 x[4][4];
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const float4* pa = reinterpret_cast<const float4*>(
+                A.part_acc + ((int64_t)(c0 + cc) * A.n_tgt + tt) * D + j * DH + half * 16);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) x[cc][q] = c0 + cc < nch ? pa[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc) {
+            const float w = wc[c0 + cc];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              av[4 * q] += w * x[cc][q].x;
+              av[4 * q + 1] += w * x[cc][q].y;
+              av[4 * q + 2] += w * x[cc][q].z;
+              av[4 * q + 3] += w * x[cc][q].w;
+            }
+          }
         }
         const float inv = 1.f / L;
 #pragma unroll
-        for (int i = 0; i < 8; ++i) av[i] *= inv;
+        for (int i = 0; i < 16; ++i) av[i] *= inv;
         if (A.save_a) {
-          float4* sa = reinterpret_cast<float4*>(A.save_a + tt * D + j * DH + qq * 8);
-          sa[0] = make_float4(av[0], av[1], av[2], av[3]);
-          sa[1] = make_float4(av[4], av[5], av[6], av[7]);
-        }
-        if (A.save_lse && qq == 0) A.save_lse[tt * H + j] = (M + log2f(L)) * kLn2;
-      }
-      uint16_t* p = act + row * AROW + j * DH + qq * 8;
+          float4* sa = reinterpret_cast<float4*>(A.save_a + tt * D + j * DH + half * 16);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) p[i] = f16_bits(av[i]);
+          for (int q = 0; q < 4; ++q) sa[q] = make_float4(av[4 * q], av[4 * q + 1], av[4 * q + 2], av[4 * q + 3]);
+        }
+        if (A.save_lse && half == 0) A.save_lse[tt * H + j] = (M + log2f(L)) * kLn2;
+      }
+      uint16_t* p = act + row * AROW + j * DH + half * 16;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) p[i] = f16_bits(av[i]);
     }
     __syncthreads();
     const int KSF = A.F / 16;
@@ -527,6 +695,27 @@ hipError_t fast_attn(int D, const Unit* units, const WsHeader* hdr, int grid, co
     default: return hipErrorInvalidValue;
   }
 #undef STCA_ATTN
+  return hipGetLastError();
+}
+
+hipError_t fast_fused(int D, int wide, const Unit* units, const WsHeader* hdr, int grid, const void* QN,
+                      const void* X, int64_t n_hist, const void* WkP, const void* WvP, int layer, float* part_acc,
+                      void* part_ml, int64_t n_tgt, hipStream_t st) {
+  if (grid == 0) return hipSuccess;
+#define STCA_FUSED1(DD, NG)                                                                                  \
+  hipLaunchKernelGGL((fused_kernel<DD, NG>), dim3(grid), dim3(64 * (DD / 32)), 0, st, units, hdr,                \
+                     (const f16x8*)QN, (const bf16_bits*)X, n_hist, (const bf16x8*)WkP, (const bf16x8*)WvP, layer, \
+                     part_acc, (float2*)part_ml, n_tgt)
+#define STCA_FUSED(DD) \
+  if (wide) STCA_FUSED1(DD, 2); else STCA_FUSED1(DD, 1)
+  switch (D) {
+    case 64: STCA_FUSED(64); break;
+    case 128: STCA_FUSED(128); break;
+    case 256: STCA_FUSED(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_FUSED
+#undef STCA_FUSED1
   return hipGetLastError();
 }
 

@@ -5,8 +5,11 @@
 // history rows are covered by whole 32-row blocks of the packed history
 // ([floor(h0/32), ceil(h1/32))); the blocks are cut into at most kMaxChunks
 // chunks of about `chunk_blocks` blocks, and the request's targets into groups
-// of kTargetGroup.  One unit = (target group, chunk).  Every target's chunk
-// count is recorded so the combine step knows how many partial results to merge.
+// of kTargetGroup.  One unit = (target group, chunk).  Units of groups with at
+// most 32 targets are listed first, the wider ones after them, so kernels
+// specialised on the group width each get one contiguous range.  Every
+// target's chunk count is recorded so the combine step knows how many partial
+// results to merge.
 //
 // One workgroup of 1024 threads; each thread owns a contiguous run of requests.
 // Invalid segments produce no units and set the workspace status, so no later
@@ -48,6 +51,23 @@ __device__ ReqPlan plan_request(const int32_t* hoff, const int32_t* toff, int r,
   return p;
 }
 
+__device__ __forceinline__ int group_size(const ReqPlan& p, int g) {
+  return min(kTargetGroup, p.t1 - (p.t0 + g * kTargetGroup));
+}
+
+__device__ int64_t block_scan(int64_t* scan, int64_t mine) {
+  const int tid = threadIdx.x;
+  scan[tid] = mine;
+  __syncthreads();
+  for (int off = 1; off < kSchedThreads; off <<= 1) {
+    int64_t v = tid >= off ? scan[tid - off] : 0;
+    __syncthreads();
+    scan[tid] += v;
+    __syncthreads();
+  }
+  return scan[tid] - mine;  // exclusive prefix; scan[kSchedThreads - 1] holds the total
+}
+
 __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __restrict__ hoff,
                                                               const int32_t* __restrict__ toff, int R,
                                                               int64_t n_hist, int64_t n_tgt,
@@ -65,49 +85,44 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
   const int per = static_cast<int>(ceil_div(R, kSchedThreads));
   const int rb = tid * per;
   const int re = min(R, rb + per);
-  int64_t mine = 0;
+  int64_t narrow = 0, wide = 0;
   bool any_bad = false;
   for (int r = rb; r < re; ++r) {
     ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks);
     any_bad |= !p.ok;
-    mine += static_cast<int64_t>(p.nch) * p.ng;
+    for (int g = 0; g < p.ng; ++g) (group_size(p, g) > 32 ? wide : narrow) += p.nch;
   }
   if (any_bad) atomicOr(&bad, 1);
-  // inclusive scan over threads (Hillis-Steele; the request count per thread
-  // is small, so this is not on any critical path)
-  scan[tid] = mine;
+  int64_t un = block_scan(scan, narrow);
+  const int64_t total_narrow = scan[kSchedThreads - 1];
   __syncthreads();
-  for (int off = 1; off < kSchedThreads; off <<= 1) {
-    int64_t v = tid >= off ? scan[tid - off] : 0;
-    __syncthreads();
-    scan[tid] += v;
-    __syncthreads();
-  }
-  int64_t u = scan[tid] - mine;
-  const int64_t total = scan[kSchedThreads - 1];
+  int64_t uw = total_narrow + block_scan(scan, wide);
+  const int64_t total = total_narrow + scan[kSchedThreads - 1];
   for (int r = rb; r < re; ++r) {
     ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks);
     if (p.nch == 0) continue;
     const int32_t bh = static_cast<int32_t>(ceil_div(p.h1, kBlockTokens));
     for (int g = 0; g < p.ng; ++g) {
+      int64_t& u = group_size(p, g) > 32 ? uw : un;
       for (int c = 0; c < p.nch; ++c, ++u) {
         if (u >= max_units) continue;
-        Unit un;
-        un.r = r;
-        un.t0 = p.t0 + g * kTargetGroup;
-        un.nt = min(kTargetGroup, p.t1 - un.t0);
-        un.c = c;
-        un.b0 = p.bl + c * p.cb;
-        un.b1 = min(un.b0 + p.cb, bh);
-        un.l0 = p.h0;
-        un.l1 = p.h1;
-        units[u] = un;
+        Unit un_;
+        un_.r = r;
+        un_.t0 = p.t0 + g * kTargetGroup;
+        un_.nt = group_size(p, g);
+        un_.c = c;
+        un_.b0 = p.bl + c * p.cb;
+        un_.b1 = min(un_.b0 + p.cb, bh);
+        un_.l0 = p.h0;
+        un_.l1 = p.h1;
+        units[u] = un_;
       }
     }
     for (int t = p.t0; t < p.t1; ++t) tchunks[t] = p.nch;
   }
   if (tid == 0) {
     hdr->n_units = static_cast<int32_t>(total < max_units ? total : max_units);
+    hdr->n_narrow = static_cast<int32_t>(total_narrow < max_units ? total_narrow : max_units);
     hdr->status = (bad || total > max_units) ? STCA_ERR_INVALID_ARG : STCA_OK;
   }
 }

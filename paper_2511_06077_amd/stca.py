@@ -41,7 +41,7 @@ class stca_wgrads_t(ctypes.Structure):
 
 
 class stca_saved_layout_t(ctypes.Structure):
-    _fields_ = [(k, ctypes.c_size_t) for k in ("s", "a", "u", "lse", "kv", "total")]
+    _fields_ = [(k, ctypes.c_size_t) for k in ("s", "a", "u", "lse", "total")]
 
 
 class StcaError(RuntimeError):

@@ -65,6 +65,7 @@ def test_path_selection():
     assert stca.stca_path(dims(n_heads=16)) == 0  # bf16, d_h = 16: generic kernels
     assert stca.stca_path(dims(n_heads=7)) == stca.STCA_ERR_INVALID_ARG
     assert stca.stca_path(dims(ffn_hidden=100)) == stca.STCA_ERR_UNSUPPORTED
+    assert stca.stca_path(dims(ffn_hidden=96)) == 0  # not a multiple of 64: generic kernels
     assert stca.stca_path(dims(n_heads=2)) == stca.STCA_ERR_UNSUPPORTED  # d_h = 128
     assert stca.stca_path(dims(dtype=7)) == stca.STCA_ERR_INVALID_ARG
 
@@ -122,6 +123,13 @@ def test_saved_layout_is_disjoint_and_sized():
     assert lay.a >= lay.s + 4 * n * nt * d
     assert lay.u >= lay.a + 4 * n * nt * d
     assert lay.lse >= lay.u + 4 * n * nt * d
-    assert lay.kv >= lay.lse + 4 * n * nt * h
+    assert lay.total >= lay.lse + 4 * n * nt * h
     assert lay.total == stca.stca_saved_size(dims(), b)
-    assert lay.total >= lay.kv + 2 * n * 128 * 2 * d  # 100 rows -> 4 blocks of 32
+
+
+def test_materialized_kv_needs_workspace_for_every_layer(monkeypatch):
+    b, keep = fake_batch([0, 40, 100], [0, 3, 9])
+    fused = stca.stca_workspace_size(dims(), b)
+    monkeypatch.setenv("STCA_KV", "materialize")
+    mat = stca.stca_workspace_size(dims(), b)
+    assert mat >= fused + 2 * 4 * 128 * 2 * 256  # 100 rows -> 4 blocks of 32, K and V, 4 layers, fp16

@@ -59,6 +59,14 @@ def check_against_oracle(b, y, a, lse, tol, rows=None):
     assert e_l <= 50 * tol, e_l
 
 
+@pytest.fixture(params=["fused", "materialize"])
+def kv_mode(request, monkeypatch):
+    """Both bf16 forms: K/V projected inside the attention kernel, or written
+    to HBM by one GEMM and streamed by the attention kernel."""
+    monkeypatch.setenv("STCA_KV", request.param)
+    return request.param
+
+
 @pytest.fixture
 def chunk_override(monkeypatch):
     def set_(v):
@@ -78,7 +86,7 @@ def test_tiny_f32_full_parity(torch, chunk_override, chunk):
 
 
 @pytest.mark.parametrize("chunk", [None, 2, 5])
-def test_uniform_bf16_full_parity(torch, chunk_override, chunk):
+def test_uniform_bf16_full_parity(torch, chunk_override, kv_mode, chunk):
     chunk_override(chunk)
     b = W.make_batch(W.WORKLOADS["uniform_bf16_R64_m16_L1024_d128"])
     y, a, lse, _ = run_gpu(torch, b)
@@ -92,7 +100,7 @@ EDGE_M = [1, 17, 0, 64, 33, 32, 1, 15, 2, 0, 31, 16]
 @pytest.mark.parametrize("dtype,d,h,n", [("bf16", 256, 8, 2), ("bf16", 64, 2, 2), ("f32", 64, 2, 2),
                                          ("bf16", 128, 8, 1), ("f32", 128, 2, 1)])
 @pytest.mark.parametrize("chunk", [None, 1])
-def test_edge_tails(torch, chunk_override, dtype, d, h, n, chunk):
+def test_edge_tails(torch, chunk_override, kv_mode, dtype, d, h, n, chunk):
     """Ragged tails: histories of 1..1023 rows not aligned to 32-row blocks,
     0..64 targets (empty target segments included), several paths."""
     chunk_override(chunk)
@@ -102,7 +110,7 @@ def test_edge_tails(torch, chunk_override, dtype, d, h, n, chunk):
 
 
 @pytest.mark.parametrize("dtype,scale", [("bf16", 1.5), ("f32", 8.0)])
-def test_peaked_softmax(torch, chunk_override, dtype, scale):
+def test_peaked_softmax(torch, chunk_override, kv_mode, dtype, scale):
     """W_Q scaled up: sharper attention and larger running-max jumps between
     blocks.  fp32 storage is held to 1e-4 at x8 (near one-hot).  bf16 storage
     rounds each score by about 2^-8 |e| (Q and K are bf16 MFMA operands), which
@@ -145,7 +153,7 @@ def test_zero_scores_give_mean_of_v(torch):
             np.testing.assert_allclose(lse[i, t0:t1], np.log(X.shape[0]), atol=1e-4)
 
 
-def test_rlb_equals_one_target_per_request(torch):
+def test_rlb_equals_one_target_per_request(torch, kv_mode):
     """RLB changes only the layout: one request with m targets gives the same
     results as m requests each holding a copy of the history."""
     b = W.make_custom_batch("rlb", [500, 130, 64], [20, 33, 5], d_model=256, n_heads=8, n_layers=2,
@@ -171,7 +179,7 @@ def test_target_permutation_within_request(torch):
     np.testing.assert_array_equal(yp, y[perm])
 
 
-def test_repeat_runs_are_bitwise_identical(torch):
+def test_repeat_runs_are_bitwise_identical(torch, kv_mode):
     b = W.make_batch(W.WORKLOADS["uniform_bf16_R64_m16_L1024_d128"])
     from paper_2511_06077_amd.device import DeviceBatch
     db = DeviceBatch(b)
@@ -215,13 +223,13 @@ def _sampled_parity(torch, name, n_sample, seed):
     check_against_oracle(sub, y, a, lse, TOL[wl.dtype], rows=rows)
 
 
-def test_long_history_sampled_parity(torch):
+def test_long_history_sampled_parity(torch, kv_mode):
     """128 requests x 32 targets, L = 10240: full run on the GPU, oracle on a
     seeded sample of requests (requests are independent)."""
     _sampled_parity(torch, "long_bf16_R128_m32_L10240_d256", 6, 0)
 
 
-def test_ragged_sampled_parity(torch):
+def test_ragged_sampled_parity(torch, kv_mode):
     _sampled_parity(torch, "ragged_bf16_R256_L512-10240_m1-64_d256", 12, 1)
 
 
