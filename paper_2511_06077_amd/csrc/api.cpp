@@ -313,8 +313,9 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   f.s_out = state(0);
   HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
   const int grid = static_cast<int>(std::min<int64_t>(L.max_units, 8 * (int64_t)device_cus()));
-  // the fused kernel keeps one workgroup per CU resident (two 256-VGPR waves
-  // per SIMD) and loops over its units, loading its weight columns once
+  // the fused kernel keeps two half-head workgroups per CU resident (two
+  // 256-VGPR waves per SIMD) and loops over its units, loading its weight
+  // columns once: one workgroup pair ("stream") per CU
   const int fgrid = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(L.max_units, device_cus())));
   for (int i = 0; i < n; ++i) {
     if (mat) {

@@ -31,9 +31,10 @@ hipError_t fast_proj(int D, const void* X, int64_t n_hist, int64_t n_blocks, con
 hipError_t fast_attn(int D, const Unit* units, const WsHeader* hdr, int grid, const void* QN, const void* KVl,
                      float* part_acc, void* part_ml, int64_t n_tgt, hipStream_t st);
 // K13: one layer's attention with the history projected inside the kernel
-// (no K/V in HBM); persistent over the scheduled units.  wide = 0 runs the
-// units with up to 32 targets, wide = 1 those with 33..64.
-hipError_t fast_fused(int D, int wide, const Unit* units, const WsHeader* hdr, int grid, const void* QN,
+// (no K/V in HBM); persistent over the scheduled units with `streams`
+// workgroup pairs.  wide = 0 runs the units with up to 32 targets, wide = 1
+// those with 33..64.
+hipError_t fast_fused(int D, int wide, const Unit* units, const WsHeader* hdr, int streams, const void* QN,
                       const void* X, int64_t n_hist, const void* WkP, const void* WvP, int layer, float* part_acc,
                       void* part_ml, int64_t n_tgt, hipStream_t st);
 // K4: combine partials, W_O, residual FFN, next queries.

@@ -46,6 +46,7 @@ namespace stca {
 namespace {
 
 constexpr int DH = 32;
+constexpr float kSlack = 8.f;  // log2 units: softmax weights stay <= 256 between rescales
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -238,18 +239,25 @@ struct Online {
 #pragma unroll
       for (int v = 1; v < 16; ++v) bm = fmaxf(bm, s[v]);
       bm = fmaxf(bm, __shfl_xor(bm, 32));
-      const float mn = fmaxf(m[g], bm);
-      const float sc = fast_exp2(m[g] - mn);
-      m[g] = mn;
+      // Threshold rescaling: the reference maximum m only moves when some
+      // score of the wave exceeds it by more than kSlack (log2 units), so the
+      // weights 2^(s - m) stay <= 2^kSlack (fine in fp16 and in the fp32 sums)
+      // and the rescale of O and l is skipped for most blocks.
+      if (__builtin_amdgcn_ballot_w64(bm > m[g] + kSlack)) {
+        const float mn = fmaxf(m[g], bm);
+        const float sc = fast_exp2(m[g] - mn);
+        m[g] = mn;
+        l[g] *= sc;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) O[g][v] *= sc;
+      }
       float ps = 0.f;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        s[v] = fast_exp2(s[v] - mn);
+        s[v] = fast_exp2(s[v] - m[g]);
         ps += s[v];
       }
-      l[g] = l[g] * sc + ps;
-#pragma unroll
-      for (int v = 0; v < 16; ++v) O[g][v] *= sc;
+      l[g] += ps;
       O[g] = mfma(kv[2], pack8h(s, 0), O[g]);
       O[g] = mfma(kv[3], pack8h(s, 8), O[g]);
     }

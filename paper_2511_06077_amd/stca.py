@@ -196,15 +196,18 @@ class HipEvents:
 
     def __init__(self, n: int):
         self.hip = ctypes.CDLL("libamdhip64.so")
-        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
         self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
         self.hip.hipEventSynchronize.argtypes = [ctypes.c_void_p]
         self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
         self.ev = (ctypes.c_void_p * n)()
         for i in range(n):
             e = ctypes.c_void_p()
-            if self.hip.hipEventCreate(ctypes.byref(e)) != 0:
-                raise RuntimeError("hipEventCreate failed")
+            # timing-only events: no system-scope fence (cache writeback and
+            # invalidate) when recorded, which would otherwise slow the
+            # kernels around every marker
+            if self.hip.hipEventCreateWithFlags(ctypes.byref(e), 0x20000000) != 0:  # hipEventDisableSystemFence
+                raise RuntimeError("hipEventCreateWithFlags failed")
             self.ev[i] = e
         self.labels = (ctypes.c_char_p * max(1, n - 1))()
 
