@@ -170,6 +170,8 @@ def main() -> int:
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
     ap.add_argument("--ablation", action="store_true",
                     help="also time one target per request and the instance-wise (non-RLB) layout")
+    ap.add_argument("--backward", action="store_true",
+                    help="time forward + backward steps (the training window workload by default)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead: time a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -182,6 +184,8 @@ def main() -> int:
     import torch
     if args.copy_gib > 0:
         return copy_calibration(args)
+    if args.backward:
+        return train_step(args)
     from paper_2511_06077_amd.device import DeviceBatch
     wl = W.WORKLOADS[args.workload]
     t0 = time.time()
@@ -248,6 +252,44 @@ def main() -> int:
         log("[bench] timing the CPU oracle")
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
+    return 0
+
+
+def train_step(args) -> int:
+    """Forward + backward of the training window: one step = stca_forward then
+    stca_backward (all gradients) over the whole batch, inputs resident."""
+    import torch
+    from paper_2511_06077_amd.device import DeviceBatch, to_device
+    name = args.workload if args.workload != W.HEADLINE else "train_bf16_R256_m16_L2048_d256"
+    wl = W.WORKLOADS[name]
+    b = W.make_batch(wl, with_grad=True)
+    db = DeviceBatch(b, device="cuda:0", backward=True)
+    dout = to_device(b.grad_out, "cuda:0")
+    for _ in range(args.warmup):
+        db.forward()
+        db.backward(dout)
+    torch.cuda.synchronize()
+    stream = torch.cuda.current_stream()
+    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    e[0].record(stream)
+    for _ in range(args.steps):
+        db.forward()
+    e[1].record(stream)
+    for _ in range(args.steps):
+        db.backward(dout)
+    e[2].record(stream)
+    torch.cuda.synchronize()
+    fwd = e[0].elapsed_time(e[1]) / args.steps
+    bwd = e[1].elapsed_time(e[2]) / args.steps
+    ms = fwd + bwd
+    print(json.dumps({
+        "metric": "targets trained/sec, STCA forward+backward", "value": b.n_tgt_total / (ms * 1e-3),
+        "unit": "targets/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16" if wl.dtype == "bf16" else "f32", "data": "synthetic",
+        "config": {"workload": wl.name, "requests": wl.n_requests, "targets_per_request": wl.n_targets,
+                   "hist_len": wl.hist_len, "d_model": wl.d_model, "heads": wl.n_heads, "layers": wl.n_layers},
+        "forward_ms": fwd, "backward_ms": bwd}), flush=True)
     return 0
 
 

@@ -63,7 +63,7 @@ typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
 
 /* Model shape.  d_model % n_heads == 0 and ffn_hidden a multiple of 32.
  * STCA_BF16 with d_head = d_model / n_heads = 32, d_model in {64, 128, 256}
- * and ffn_hidden a multiple of 64 runs on the bf16 MFMA kernels; every other shape with d_head in
+ * and ffn_hidden a multiple of 256 runs on the bf16 MFMA kernels; every other shape with d_head in
  * {8, 16, 32, 64} (either dtype) runs on the generic fp32-arithmetic kernels
  * (stca_path tells which). */
 typedef struct {

@@ -35,7 +35,7 @@ int path_of(const stca_dims_t* d) {
   const int dh = d->d_model / d->n_heads;
   if (d->ffn_hidden % 32 != 0) return STCA_ERR_UNSUPPORTED;
   if (d->dtype == STCA_BF16 && dh == 32 && (d->d_model == 64 || d->d_model == 128 || d->d_model == 256) &&
-      d->ffn_hidden % 64 == 0)
+      d->ffn_hidden % 256 == 0)
     return 1;
   if (dh == 8 || dh == 16 || dh == 32 || dh == 64) return 0;
   return STCA_ERR_UNSUPPORTED;
@@ -97,14 +97,6 @@ int64_t max_units_for(const stca_batch_t* b, int chunk_blocks) {
   if (b->hist_off_host)
     return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks);
   return (ceil_div(b->n_tgt, kTargetGroup) + b->n_requests) * kMaxChunks;
-}
-
-// hidden columns staged in LDS at a time by the update kernel (F % 64 == 0 on
-// that path, so the chunk is a multiple of 64: four MFMA k-steps or more)
-int ffn_chunk(int F) {
-  for (int c : {512, 256, 128, 64})
-    if (F % c == 0) return c;
-  return 64;
 }
 
 struct Layout {
@@ -291,7 +283,6 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   FastUpdate f{};
   f.n_layers = n;
   f.F = F;
-  f.FC = ffn_chunk(F);
   f.n_tgt = L.nt;
   f.tgt = tgt;
   f.tchunks = tch;
@@ -420,6 +411,16 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   float* ds2 = at<float>(ws, L.ds2);
   float* dqp = at<float>(ws, L.dq_part);
   auto W = [&](const void* base, int i, size_t per) { return static_cast<const char*>(base) + i * per * es; };
+  // history-side products (rows = history items): MFMA with bf16 operands when
+  // the inputs are bf16, the fp32 SIMT GEMM otherwise (fp32 storage keeps
+  // fp32 arithmetic throughout)
+  auto hgemm = [&](int a_bf, int b_bf, int M, int N, int K, const void* A, int64_t lda, int tA, const void* B,
+                   int64_t ldb, int tB, float* C, int64_t ldc, int accumulate) {
+    if (bf)
+      return gemm_mfma(a_bf, b_bf, M, N, K, A, lda, tA, B, ldb, tB, C, ldc, 1.f, accumulate, st);
+    return gemm_generic(a_bf, b_bf, M, N, K, A, lda, tA, B, ldb, tB, C, ldc, 1.f, kEpiStore, nullptr, 0, nullptr,
+                        accumulate, st);
+  };
   auto RS = [&](int i) { return at<float>(ws, L.rs) + (size_t)i * nt * d; };
   auto RU = [&](int i) { return at<float>(ws, L.ru) + (size_t)i * nt * d; };
   const float qscale0 = kLog2e / std::sqrt(static_cast<float>(L.dh));
@@ -428,10 +429,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   for (int i = 0; i < n; ++i) {
     const void* Wk = W(w->wk, i, (size_t)d * d);
     const void* Wv = W(w->wv, i, (size_t)d * d);
-    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr, 0,
-                        st));
-    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr,
-                        0, st));
+    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 0));
+    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 0));
     HIPCHK(gemm_generic(0, bf, nt, d, d, RS(i), d, 0, W(w->wq, i, (size_t)d * d), d, 0, q, d, qscale0, kEpiStore,
                         nullptr, 0, nullptr, 0, st));
     HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, at<float>(ws, L.part_acc),
@@ -462,10 +461,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     const void* Wk = W(w->wk, i, (size_t)d * d);
     const void* Wv = W(w->wv, i, (size_t)d * d);
     // recompute this layer's K, V, q and attention output in fp32
-    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr, 0,
-                        st));
-    HIPCHK(gemm_generic(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 1.f, kEpiStore, nullptr, 0, nullptr,
-                        0, st));
+    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 0));
+    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 0));
     HIPCHK(gemm_generic(0, bf, nt, d, d, s, d, 0, Wq, d, 0, q, d, qscale, kEpiStore, nullptr, 0, nullptr, 0, st));
     HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, at<float>(ws, L.part_acc),
                         at<float>(ws, L.part_ml), nt, st));
@@ -492,14 +489,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                         nullptr, 0, nullptr, 0, st));
     HIPCHK(gemm_generic(0, bf, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr, 0, st));
     // K = X Wk, V = X Wv
-    HIPCHK(gemm_generic(bf, 0, d, d, nh, hist, d, 1, dkv, 2 * d, 0, dw->dwk + (size_t)i * d * d, d, 1.f,
-                        kEpiStore, nullptr, 0, nullptr, 0, st));
-    HIPCHK(gemm_generic(bf, 0, d, d, nh, hist, d, 1, dkv + d, 2 * d, 0, dw->dwv + (size_t)i * d * d, d, 1.f,
-                        kEpiStore, nullptr, 0, nullptr, 0, st));
-    HIPCHK(gemm_generic(0, bf, nh, d, d, dkv, 2 * d, 0, Wk, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0, nullptr, 1,
-                        st));
-    HIPCHK(gemm_generic(0, bf, nh, d, d, dkv + d, 2 * d, 0, Wv, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0, nullptr,
-                        1, st));
+    HIPCHK(hgemm(bf, 0, d, d, nh, hist, d, 1, dkv, 2 * d, 0, dw->dwk + (size_t)i * d * d, d, 0));
+    HIPCHK(hgemm(bf, 0, d, d, nh, hist, d, 1, dkv + d, 2 * d, 0, dw->dwv + (size_t)i * d * d, d, 0));
+    HIPCHK(hgemm(0, bf, nh, d, d, dkv, 2 * d, 0, Wk, d, 1, dhist, d, 1));
+    HIPCHK(hgemm(0, bf, nh, d, d, dkv + d, 2 * d, 0, Wv, d, 1, dhist, d, 1));
     std::swap(ds, ds2);
   }
   HIPCHK(convert(0, 0, ds, dtgt, nt * d, st));

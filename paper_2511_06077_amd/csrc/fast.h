@@ -7,7 +7,7 @@ namespace stca {
 
 struct FastUpdate {
   int mode;      // 0: s^(0) = x_t and Q^(0); 1: combine + update after `layer`
-  int layer, n_layers, F, FC;
+  int layer, n_layers, F;
   int64_t n_tgt;
   const void* tgt;
   const int32_t* tchunks;

@@ -38,6 +38,8 @@
 // ("packed": [N/32][K/16][64 lanes][8 bf16] with lane (n = l%32, hi) holding
 // W[16ks + 8hi .. +7][32nb + n]), which serves both as an A operand of D^T and
 // as a B operand of D.
+#include <type_traits>
+
 #include "common.h"
 #include "fast.h"
 
@@ -46,7 +48,8 @@ namespace stca {
 namespace {
 
 constexpr int DH = 32;
-constexpr float kSlack = 8.f;  // log2 units: softmax weights stay <= 256 between rescales
+constexpr float kSlack = 8.f;
+constexpr int kFfnChunk = 256;  // update kernel: FFN hidden columns per LDS stage (F % 256 == 0)  // log2 units: softmax weights stay <= 256 between rescales
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -435,7 +438,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
 //   u = s + a W_O;  s' = u + ReLU(u W_1) W_2;  Q' = s' W_Q^{i+1} (if i+1 < n).
 // Activations go through LDS as bf16 MFMA operands; the state stays fp32.
 struct UpdateArgs {
-  int mode, layer, n_layers, F, FC;  // FC: hidden columns staged in LDS at a time
+  int mode, layer, n_layers, F;
   int64_t n_tgt;
   const bf16_bits* tgt;        // mode 0
   const int32_t* tchunks;      // mode 1
@@ -460,7 +463,8 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];  // fp16 MFMA operands
   uint16_t* act = lds;                  // [32][AROW]
   uint16_t* hid = lds + 32 * AROW;      // [32][FC + 8]
-  const int HROW = A.FC + 8;
+  constexpr int FC = kFfnChunk;        // hidden columns staged in LDS at a time
+  constexpr int HROW = FC + 8;
   const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int tcol = lane % 32, hi = lane / 32;
   const int64_t tb = (int64_t)blockIdx.x * 32;
@@ -484,29 +488,24 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       *reinterpret_cast<uint2*>(p + 8 * g) = pk;
     }
   };
-  // acc = W^T act^T over `ksteps` k-steps (a multiple of 4).  The weight
-  // operands come from L2; they are fetched four k-steps ahead so the loop
-  // is not one L2 round trip per MFMA.
-  auto gemm = [&](const f16x8* Wp, const uint16_t* src, int src_row, int ksteps) {
-    f32x16 acc = {};
+  // acc = W^T act^T over KSTEPS k-steps.  The weight operands stream from L2;
+  // with the step count known at compile time every load of the product is
+  // issued before the first MFMA waits on it, so a product costs about one
+  // L2 round trip instead of one per MFMA.
+  auto gemm = [&](auto ksteps_tag, const f16x8* Wp, const uint16_t* src, int src_row) {
+    constexpr int KSTEPS = decltype(ksteps_tag)::value;
     const uint16_t* b = src + tcol * src_row + 8 * hi;
     const f16x8* w = Wp + lane;
-    f16x8 cur[4], nxt[4];
+    f16x8 wr[KSTEPS];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) cur[i] = w[i * 64];
-    for (int k0 = 0; k0 < ksteps; k0 += 4) {
-      if (k0 + 4 < ksteps) {
+    for (int k = 0; k < KSTEPS; ++k) wr[k] = w[k * 64];
+    f32x16 acc = {};
 #pragma unroll
-        for (int i = 0; i < 4; ++i) nxt[i] = w[(k0 + 4 + i) * 64];
-      }
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        acc = mfma(cur[i], *reinterpret_cast<const f16x8*>(b + (k0 + i) * 16), acc);
-#pragma unroll
-      for (int i = 0; i < 4; ++i) cur[i] = nxt[i];
-    }
+    for (int k = 0; k < KSTEPS; ++k) acc = mfma(wr[k], *reinterpret_cast<const f16x8*>(b + k * 16), acc);
     return acc;
   };
+  using KSd = std::integral_constant<int, KS>;
+  using KSc = std::integral_constant<int, FC / 16>;
 
   f32x16 s_next;
   if (A.mode == 0) {
@@ -592,7 +591,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
     __syncthreads();
     const int KSF = A.F / 16;
     // u = s + a W_O
-    f32x16 u = gemm(A.WoP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, AROW, KS);
+    f32x16 u = gemm(KSd{}, A.WoP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, AROW);
     if (tok) {
       const float* sp = A.s_in + t * D + 32 * w + 4 * hi;
 #pragma unroll
@@ -607,15 +606,16 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
     __syncthreads();
     // s' = u + ReLU(u W_1) W_2, the hidden layer taken FC columns at a time
     s_next = u;
-    for (int c0 = 0; c0 < A.F; c0 += A.FC) {
-      for (int nb = w; nb < A.FC / 32; nb += NW) {
-        f32x16 h = gemm(A.W1P + ((int64_t)A.layer * (A.F / 32) + c0 / 32 + nb) * KS * 64, act, AROW, KS);
+    for (int c0 = 0; c0 < A.F; c0 += FC) {
+#pragma unroll
+      for (int nb = w; nb < FC / 32; nb += NW) {
+        f32x16 h = gemm(KSd{}, A.W1P + ((int64_t)A.layer * (A.F / 32) + c0 / 32 + nb) * KS * 64, act, AROW);
 #pragma unroll
         for (int v = 0; v < 16; ++v) h[v] = fmaxf(h[v], 0.f);
         put_act(hid, HROW, 32 * nb, h);
       }
       __syncthreads();
-      const f32x16 y = gemm(A.W2P + ((int64_t)(A.layer * NW + w) * KSF + c0 / 16) * 64, hid, HROW, A.FC / 16);
+      const f32x16 y = gemm(KSc{}, A.W2P + ((int64_t)(A.layer * NW + w) * KSF + c0 / 16) * 64, hid, HROW);
 #pragma unroll
       for (int v = 0; v < 16; ++v) s_next[v] += y[v];
       __syncthreads();
@@ -642,7 +642,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   }
   // next queries: Q = s W_Q^{next}, scaled into log2 units, permuted (QN layout)
   const int ql = A.mode == 0 ? 0 : A.layer + 1;
-  f32x16 q = gemm(A.WqP + ((int64_t)(ql * NW + w) * KS) * 64, act, AROW, KS);
+  f32x16 q = gemm(KSd{}, A.WqP + ((int64_t)(ql * NW + w) * KS) * 64, act, AROW);
   const float qs = kLog2e * 0.17677669529663687f;  // log2(e) / sqrt(32)
 #pragma unroll
   for (int v = 0; v < 16; ++v) q[v] *= qs;
@@ -733,7 +733,6 @@ hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st) {
   A.layer = f.layer;
   A.n_layers = f.n_layers;
   A.F = f.F;
-  A.FC = f.FC;
   A.n_tgt = f.n_tgt;
   A.tgt = (const bf16_bits*)f.tgt;
   A.tchunks = f.tchunks;
@@ -752,7 +751,7 @@ hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st) {
   A.WqP = (const f16x8*)f.WqP;
   if (f.n_tgt == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
-  const size_t lds = (size_t)32 * (D + 8) * 2 + (f.mode == 0 ? 0 : (size_t)32 * (f.FC + 8) * 2);
+  const size_t lds = (size_t)32 * (D + 8) * 2 + (f.mode == 0 ? 0 : (size_t)32 * (kFfnChunk + 8) * 2);
 #define STCA_UPD(DD) hipLaunchKernelGGL(update_kernel<DD>, g, dim3(64 * (DD / 32)), lds, st, A)
   switch (D) {
     case 64: STCA_UPD(64); break;

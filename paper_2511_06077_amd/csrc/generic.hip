@@ -90,20 +90,35 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA
 }
 
 // ------------------------------------------------------------ attention
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  return v;
+// Exact fp32 attention for the generic path and the backward pass.
+//
+// Lane layouts avoid reductions across lanes inside the token loops:
+//  * target lanes: lane = (target t, stream st), 64 / TP streams for TP =
+//    16, 32 or 64 target slots; each lane keeps its own target's state and
+//    visits every (64 / TP)-th token of its wave's share of a 64-row K/V tile
+//    staged in LDS (rows of one token are read by many lanes at once, which
+//    LDS serves as broadcasts);
+//  * token lanes: lane = history row; the targets' vectors are broadcast from
+//    LDS.
+// A workgroup (4 waves) handles one (unit, head).
+constexpr int kTile = 64;
+
+__device__ __forceinline__ int target_slots(int nt) { return nt <= 16 ? 16 : (nt <= 32 ? 32 : 64); }
+
+template <int DH>
+__device__ __forceinline__ void stage_kv_tile(float (*kt)[DH + 1], float (*vt)[DH + 1], const float* __restrict__ KV,
+                                              int d, int j, int base, int lo, int hi) {
+  for (int e = threadIdx.x; e < kTile * DH; e += 256) {
+    const int r = e / DH, c = e % DH;
+    const int tok = base + r;
+    const bool on = tok >= lo && tok < hi;
+    kt[r][c] = on ? KV[(int64_t)tok * 2 * d + j * DH + c] : 0.f;
+    vt[r][c] = on ? KV[(int64_t)tok * 2 * d + d + j * DH + c] : 0.f;
+  }
 }
 
-// One workgroup per (unit, head); each wave takes targets w, w+4, ...; lanes
-// stride over the unit's history rows with an online softmax, then merge.
-// Q is pre-scaled by log2(e)/sqrt(d_h), so scores are in log2 units.
+// Online-softmax partial (acc, max, sum) per (chunk, target, head); Q holds
+// the queries pre-scaled by log2(e)/sqrt(d_h), so scores are in log2 units.
 template <int DH>
 __global__ __launch_bounds__(256) void attn_generic_kernel(const Unit* __restrict__ units,
                                                            const WsHeader* __restrict__ hdr,
@@ -112,47 +127,75 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(const Unit* __restric
                                                            float* __restrict__ part_acc,
                                                            float* __restrict__ part_ml, int64_t n_tgt,
                                                            int n_heads) {
+  __shared__ float kt[kTile][DH + 1], vt[kTile][DH + 1];
+  __shared__ float red[4][64][DH + 2];
   const int u = blockIdx.x;
   if (u >= hdr->n_units) return;
   const Unit un = units[u];
   const int j = blockIdx.y;
   const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
+  const int TP = target_slots(un.nt), S = 64 / TP;
+  const int tt = lane % TP, st = lane / TP;
+  const bool live = tt < un.nt;
+  float q[DH], acc[DH];
+#pragma unroll
+  for (int e = 0; e < DH; ++e) {
+    q[e] = live ? Q[(int64_t)(un.t0 + tt) * d + j * DH + e] : 0.f;
+    acc[e] = 0.f;
+  }
+  float m = -INFINITY, l = 0.f;
   const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
-  for (int tt = w; tt < un.nt; tt += 4) {
-    const int64_t t = un.t0 + tt;
-    float q[DH];
+  for (int base = lo; base < hi; base += kTile) {
+    __syncthreads();
+    stage_kv_tile<DH>(kt, vt, KV, d, j, base, lo, hi);
+    __syncthreads();
+    for (int r = w * 16 + st; r < w * 16 + 16; r += S) {
+      if (base + r >= hi) break;
+      float sc = 0.f;
 #pragma unroll
-    for (int e = 0; e < DH; ++e) q[e] = Q[t * d + j * DH + e];
-    float m = -INFINITY, l = 0.f, acc[DH];
+      for (int e = 0; e < DH; ++e) sc = fmaf(q[e], kt[r][e], sc);
+      const float mn = fmaxf(m, sc);
+      const float f = exp2f(m - mn);
+      const float p = exp2f(sc - mn);
+      l = l * f + p;
 #pragma unroll
-    for (int e = 0; e < DH; ++e) acc[e] = 0.f;
-    for (int tok = lo + lane; tok < hi; tok += 64) {
-      const float* krow = KV + (int64_t)tok * 2 * d + j * DH;
-      const float* vrow = krow + d;
-      float s = 0.f;
-#pragma unroll
-      for (int e = 0; e < DH; ++e) s = fmaf(q[e], krow[e], s);
-      const float mn = fmaxf(m, s);
-      const float sc = exp2f(m - mn);
-      const float p = exp2f(s - mn);
-      l = l * sc + p;
-#pragma unroll
-      for (int e = 0; e < DH; ++e) acc[e] = fmaf(p, vrow[e], acc[e] * sc);
+      for (int e = 0; e < DH; ++e) acc[e] = fmaf(p, vt[r][e], acc[e] * f);
       m = mn;
     }
-    const float M = wave_max(m);
-    const float f = (m == -INFINITY) ? 0.f : exp2f(m - M);
-    const float L = wave_sum(l * f);
-    float* pa = part_acc + ((int64_t)un.c * n_tgt + t) * d + j * DH;
+  }
+  // merge the streams of each target (lanes tt + k TP), then the four waves
+  for (int o = TP; o < 64; o <<= 1) {
+    const float mo = __shfl_xor(m, o), lo_ = __shfl_xor(l, o);
+    const float mn = fmaxf(m, mo);
+    const float fa = m == -INFINITY ? 0.f : exp2f(m - mn), fb = mo == -INFINITY ? 0.f : exp2f(mo - mn);
+    l = l * fa + lo_ * fb;
 #pragma unroll
-    for (int e = 0; e < DH; ++e) {
-      const float v = wave_sum(acc[e] * f);
-      if (lane == 0) pa[e] = v;
+    for (int e = 0; e < DH; ++e) acc[e] = acc[e] * fa + __shfl_xor(acc[e], o) * fb;
+    m = mn;
+  }
+  if (st == 0) {
+    red[w][tt][0] = m;
+    red[w][tt][1] = l;
+#pragma unroll
+    for (int e = 0; e < DH; ++e) red[w][tt][2 + e] = acc[e];
+  }
+  __syncthreads();
+  for (int it = threadIdx.x; it < un.nt * (DH + 1); it += 256) {
+    const int t = it / (DH + 1), e = it % (DH + 1);  // e == DH: (max, sum)
+    float M = -INFINITY;
+    for (int ww = 0; ww < 4; ++ww) M = fmaxf(M, red[ww][t][0]);
+    float v = 0.f;
+    for (int ww = 0; ww < 4; ++ww) {
+      const float mw = red[ww][t][0];
+      const float f = mw == -INFINITY ? 0.f : exp2f(mw - M);
+      v += f * (e == DH ? red[ww][t][1] : red[ww][t][2 + e]);
     }
-    if (lane == 0) {
-      float* pm = part_ml + (((int64_t)un.c * n_tgt + t) * n_heads + j) * 2;
-      pm[0] = M;
-      pm[1] = L;
+    const int64_t row = (int64_t)un.c * n_tgt + un.t0 + t;
+    if (e == DH) {
+      part_ml[(row * n_heads + j) * 2] = M;
+      part_ml[(row * n_heads + j) * 2 + 1] = v;
+    } else {
+      part_acc[row * d + j * DH + e] = v;
     }
   }
 }
@@ -187,82 +230,126 @@ __global__ void merge_generic_kernel(int dh, int n_heads, int64_t n_tgt, const i
 }
 
 // ------------------------------------------------- attention backward
-// One workgroup per (unit, head).  Lanes own history rows (a 64-row tile at a
-// time) and accumulate dK, dV over all of the unit's targets; dq of each
-// target is reduced over the wave and accumulated in LDS, then written as this
-// chunk's partial.  dK/dV of a row can receive contributions from several
-// target groups of the same request, so they are added atomically.
+// With p = softmax weight, dp = dA . v, D = rowsum(dA * A):
+//   de = p (dp - D);  dq = sum_rows de k / sqrt(d_h);  dk = sum_targets de q / sqrt(d_h);
+//   dv = sum_targets p dA.
+// dK/dV: token lanes (each lane owns one history row and loops over the
+// unit's targets).  dq: target lanes.  The rows of one request can be shared
+// by several target groups, so dK/dV are added atomically.
 template <int DH>
-__global__ __launch_bounds__(256) void attn_bwd_generic_kernel(
+__global__ __launch_bounds__(256) void attn_bwd_kv_kernel(
     const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const float* __restrict__ Q,
     const float* __restrict__ KV, int d, const float* __restrict__ a, const float* __restrict__ da,
-    const float* __restrict__ lse, float* __restrict__ dq_part, float* __restrict__ dKV, int64_t n_tgt,
-    int n_heads) {
-  __shared__ float dq_s[kTargetGroup][DH];
-  __shared__ float Dt_s[kTargetGroup];
+    const float* __restrict__ lse, float* __restrict__ dKV, int n_heads) {
+  __shared__ float qs[kTargetGroup][DH], das[kTargetGroup][DH], cs[kTargetGroup][2];
+  const int u = blockIdx.x;
+  if (u >= hdr->n_units) return;
+  const Unit un = units[u];
+  const int j = blockIdx.y;
+  for (int e = threadIdx.x; e < un.nt * DH; e += 256) {
+    const int64_t t = un.t0 + e / DH;
+    qs[e / DH][e % DH] = Q[t * d + j * DH + e % DH];
+    das[e / DH][e % DH] = da[t * d + j * DH + e % DH];
+  }
+  for (int tt = threadIdx.x; tt < un.nt; tt += 256) {
+    const int64_t t = un.t0 + tt;
+    float D = 0.f;
+    for (int e = 0; e < DH; ++e) D += da[t * d + j * DH + e] * a[t * d + j * DH + e];
+    cs[tt][0] = lse[t * n_heads + j] * kLog2e;
+    cs[tt][1] = D;
+  }
+  __syncthreads();
+  const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
+  for (int tok = lo + threadIdx.x; tok < hi; tok += 256) {
+    float k[DH], v[DH], dk[DH], dv[DH];
+#pragma unroll
+    for (int e = 0; e < DH; ++e) {
+      k[e] = KV[(int64_t)tok * 2 * d + j * DH + e];
+      v[e] = KV[(int64_t)tok * 2 * d + d + j * DH + e];
+      dk[e] = 0.f;
+      dv[e] = 0.f;
+    }
+    for (int tt = 0; tt < un.nt; ++tt) {
+      float s = 0.f, dp = 0.f;
+#pragma unroll
+      for (int e = 0; e < DH; ++e) {
+        s = fmaf(qs[tt][e], k[e], s);
+        dp = fmaf(das[tt][e], v[e], dp);
+      }
+      const float p = exp2f(s - cs[tt][0]);
+      const float de = p * (dp - cs[tt][1]);
+#pragma unroll
+      for (int e = 0; e < DH; ++e) {
+        dk[e] = fmaf(de, qs[tt][e], dk[e]);
+        dv[e] = fmaf(p, das[tt][e], dv[e]);
+      }
+    }
+    // Q holds log2(e)/sqrt(d_h) times the true query: dk of the true query
+    // is de q / sqrt(d_h) = de * (stored q) * ln 2
+#pragma unroll
+    for (int e = 0; e < DH; ++e) {
+      atomicAdd(&dKV[(int64_t)tok * 2 * d + j * DH + e], dk[e] * kLn2);
+      atomicAdd(&dKV[(int64_t)tok * 2 * d + d + j * DH + e], dv[e]);
+    }
+  }
+}
+
+template <int DH>
+__global__ __launch_bounds__(256) void attn_bwd_q_kernel(
+    const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const float* __restrict__ Q,
+    const float* __restrict__ KV, int d, const float* __restrict__ a, const float* __restrict__ da,
+    const float* __restrict__ lse, float* __restrict__ dq_part, int64_t n_tgt, int n_heads) {
+  __shared__ float kt[kTile][DH + 1], vt[kTile][DH + 1];
+  __shared__ float red[4][64][DH];
   const int u = blockIdx.x;
   if (u >= hdr->n_units) return;
   const Unit un = units[u];
   const int j = blockIdx.y;
   const int lane = threadIdx.x % 64, w = threadIdx.x / 64;
-  const float scale = 1.f / sqrtf((float)DH);  // Q holds q * log2(e) / sqrt(d_h)
-  for (int e = threadIdx.x; e < kTargetGroup * DH; e += 256) dq_s[e / DH][e % DH] = 0.f;
-  for (int tt = threadIdx.x; tt < un.nt; tt += 256) {
-    const int64_t t = un.t0 + tt;
-    float D = 0.f;
-    for (int e = 0; e < DH; ++e) D += da[t * d + j * DH + e] * a[t * d + j * DH + e];
-    Dt_s[tt] = D;
+  const int TP = target_slots(un.nt), S = 64 / TP;
+  const int tt = lane % TP, st = lane / TP;
+  const bool live = tt < un.nt;
+  const int64_t t = un.t0 + (live ? tt : 0);
+  float q[DH], dat[DH], dq[DH];
+  float D = 0.f;
+#pragma unroll
+  for (int e = 0; e < DH; ++e) {
+    q[e] = live ? Q[t * d + j * DH + e] : 0.f;
+    dat[e] = live ? da[t * d + j * DH + e] : 0.f;
+    D += live ? dat[e] * a[t * d + j * DH + e] : 0.f;
+    dq[e] = 0.f;
   }
-  __syncthreads();
+  const float ls = live ? lse[t * n_heads + j] * kLog2e : 0.f;
   const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
-  for (int base = lo + w * 64; base < hi; base += 256) {
-    const int tok = base + lane;
-    const bool on = tok < hi;
-    float k[DH], v[DH], dk[DH], dv[DH];
-#pragma unroll
-    for (int e = 0; e < DH; ++e) {
-      k[e] = on ? KV[(int64_t)tok * 2 * d + j * DH + e] : 0.f;
-      v[e] = on ? KV[(int64_t)tok * 2 * d + d + j * DH + e] : 0.f;
-      dk[e] = 0.f;
-      dv[e] = 0.f;
-    }
-    for (int tt = 0; tt < un.nt; ++tt) {
-      const int64_t t = un.t0 + tt;
-      const float* q = Q + t * d + j * DH;
-      const float* dat = da + t * d + j * DH;
-      float s = 0.f, dp = 0.f;
+  for (int base = lo; base < hi; base += kTile) {
+    __syncthreads();
+    stage_kv_tile<DH>(kt, vt, KV, d, j, base, lo, hi);
+    __syncthreads();
+    for (int r = w * 16 + st; r < w * 16 + 16; r += S) {
+      if (base + r >= hi) break;
+      float sc = 0.f, dp = 0.f;
 #pragma unroll
       for (int e = 0; e < DH; ++e) {
-        s = fmaf(q[e], k[e], s);
-        dp = fmaf(dat[e], v[e], dp);
+        sc = fmaf(q[e], kt[r][e], sc);
+        dp = fmaf(dat[e], vt[r][e], dp);
       }
-      const float p = on ? exp2f(s - lse[t * n_heads + j] * kLog2e) : 0.f;
-      const float de = p * (dp - Dt_s[tt]);
+      const float de = live ? exp2f(sc - ls) * (dp - D) : 0.f;
 #pragma unroll
-      for (int e = 0; e < DH; ++e) {
-        dv[e] = fmaf(p, dat[e], dv[e]);
-        // q holds log2(e)/sqrt(d_h) times the true query, so de*q/sqrt(d_h)
-        // of the true query is de*q*ln(2): the ln(2) is applied once below
-        dk[e] = fmaf(de, q[e], dk[e]);
-      }
-#pragma unroll
-      for (int e = 0; e < DH; ++e) {
-        const float g = wave_sum(de * k[e]);
-        if (lane == 0) atomicAdd(&dq_s[tt][e], g * scale);
-      }
-    }
-    if (on) {
-#pragma unroll
-      for (int e = 0; e < DH; ++e) {
-        atomicAdd(&dKV[(int64_t)tok * 2 * d + j * DH + e], dk[e] * kLn2);
-        atomicAdd(&dKV[(int64_t)tok * 2 * d + d + j * DH + e], dv[e]);
-      }
+      for (int e = 0; e < DH; ++e) dq[e] = fmaf(de, kt[r][e], dq[e]);
     }
   }
+  for (int o = TP; o < 64; o <<= 1)
+#pragma unroll
+    for (int e = 0; e < DH; ++e) dq[e] += __shfl_xor(dq[e], o);
+  if (st == 0)
+#pragma unroll
+    for (int e = 0; e < DH; ++e) red[w][tt][e] = dq[e];
   __syncthreads();
-  for (int e = threadIdx.x; e < un.nt * DH; e += 256) {
-    const int tt = e / DH, ee = e % DH;
-    dq_part[((int64_t)un.c * n_tgt + un.t0 + tt) * d + j * DH + ee] = dq_s[tt][ee];
+  const float scale = 1.f / sqrtf((float)DH);
+  for (int it = threadIdx.x; it < un.nt * DH; it += 256) {
+    const int t2 = it / DH, e = it % DH;
+    const float v = red[0][t2][e] + red[1][t2][e] + red[2][t2][e] + red[3][t2][e];
+    dq_part[((int64_t)un.c * n_tgt + un.t0 + t2) * d + j * DH + e] = v * scale;
   }
 }
 
@@ -363,9 +450,11 @@ hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t 
                             hipStream_t st) {
   if (max_units == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(max_units), n_heads);
-#define STCA_ATTB(DH)                                                                                 \
-  hipLaunchKernelGGL(attn_bwd_generic_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, \
-                     dq_part, dKV, n_tgt, n_heads)
+#define STCA_ATTB(DH)                                                                                     \
+  hipLaunchKernelGGL(attn_bwd_kv_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, dKV,    \
+                     n_heads);                                                                            \
+  hipLaunchKernelGGL(attn_bwd_q_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, dq_part, \
+                     n_tgt, n_heads)
   switch (d_head) {
     case 8: STCA_ATTB(8); break;
     case 16: STCA_ATTB(16); break;

@@ -20,6 +20,13 @@ hipError_t gemm_generic(int a_bf16, int b_bf16, int M, int N, int K, const void*
                         int transA, const void* B, int64_t ldb, int transB, float* C, int64_t ldc,
                         float alpha, GemmEpi epi, const float* R, int64_t ldr, float* C2,
                         int accumulate, hipStream_t st);
+// MFMA GEMM with bf16 operands (fp32 operands rounded to bf16 when staged)
+// and fp32 accumulation/output; same operand conventions as gemm_generic
+// (kEpiStore only, optional accumulate).  For the backward's history-side
+// products on bf16 inputs.
+hipError_t gemm_mfma(int a_bf16, int b_bf16, int M, int N, int K, const void* A, int64_t lda, int transA,
+                     const void* B, int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate,
+                     hipStream_t st);
 hipError_t attn_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
                         const WsHeader* hdr, const float* Q, const float* KV, int d,
                         float* part_acc, float* part_ml, int64_t n_tgt, hipStream_t st);

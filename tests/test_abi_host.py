@@ -65,7 +65,8 @@ def test_path_selection():
     assert stca.stca_path(dims(n_heads=16)) == 0  # bf16, d_h = 16: generic kernels
     assert stca.stca_path(dims(n_heads=7)) == stca.STCA_ERR_INVALID_ARG
     assert stca.stca_path(dims(ffn_hidden=100)) == stca.STCA_ERR_UNSUPPORTED
-    assert stca.stca_path(dims(ffn_hidden=96)) == 0  # not a multiple of 64: generic kernels
+    assert stca.stca_path(dims(ffn_hidden=96)) == 0  # not a multiple of 256: generic kernels
+    assert stca.stca_path(dims(ffn_hidden=768)) == 1
     assert stca.stca_path(dims(n_heads=2)) == stca.STCA_ERR_UNSUPPORTED  # d_h = 128
     assert stca.stca_path(dims(dtype=7)) == stca.STCA_ERR_INVALID_ARG
 
