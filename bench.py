@@ -1,12 +1,13 @@
 #!/usr/bin/env python3
 """Throughput of the STCA forward under request level batching on one MI355X.
 
-One step = one stca_forward over the whole batch (history K/V projection of
-every layer, then per layer the fused multi-target attention and the target
-update), inputs already resident in HBM.  Prints one JSON line:
-targets scored per second, the dominant kernel against its roofline (HIP
-events recorded on the library's stream around every launch of the timed
-steps), and the fp64 CPU oracle timed on a bounded sample of the same workload.
+One step = one stca_forward over the whole batch (per layer: the history K/V
+projection fused into the multi-target attention, then the target update),
+inputs already resident in HBM.  Prints one JSON line: targets scored per
+second over the K timed steps, the dominant kernel against its roofline (HIP
+events recorded on the library's stream around every launch, in a second pass
+of K steps so that the events stay out of the timed region), and the fp64 CPU
+oracle timed on a bounded sample of the same workload.
 
     python bench.py [--steps K] [--warmup W] [--workload NAME] [--ablation]
 """
@@ -117,6 +118,20 @@ def cpu_baseline(wl: W.Workload, budget_s: float):
                       f"{spent:.1f} s of fp64 CPU work"}
 
 
+def settle(run, seconds: float) -> int:
+    """Untimed steps for `seconds` of wall time before the warm-up proper: the
+    GPU clock ramps up over the first tens of milliseconds of sustained work,
+    which a few warm-up steps do not cover."""
+    import torch
+    n, t0 = 0, time.perf_counter()
+    while time.perf_counter() - t0 < seconds:
+        for _ in range(8):
+            run()
+        n += 8
+        torch.cuda.synchronize()
+    return n
+
+
 def plain_forward(db, steps: int, warmup: int) -> float:
     """The same K steps without per-kernel events: total milliseconds."""
     import torch
@@ -164,10 +179,12 @@ def timed_forward(db, steps: int, warmup: int):
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    ap.add_argument("--settle-seconds", type=float, default=1.0,
+                    help="untimed steps for this long before the warm-up (GPU clock ramp)")
     ap.add_argument("--ablation", action="store_true",
                     help="also time one target per request and the instance-wise (non-RLB) layout")
     ap.add_argument("--backward", action="store_true",
@@ -193,10 +210,16 @@ def main() -> int:
     log(f"[bench] generated {wl.name}: {b.n_hist} history rows, {b.n_tgt_total} targets ({time.time() - t0:.1f} s)")
     db = DeviceBatch(b, device="cuda:0")
     log(f"[bench] workspace {db.ws_bytes / 2**30:.2f} GiB; path {stca.stca_path(db.dims)}")
-    total_ms, per = timed_forward(db, args.steps, args.warmup)
-    ms_step = total_ms / args.steps
-    plain_ms = plain_forward(db, args.steps, 1) / args.steps
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step with per-kernel events, {plain_ms:.3f} without")
+    n_settle = settle(db.forward, args.settle_seconds)
+    log(f"[bench] {n_settle} settling steps")
+    # the timed region: W warm-up steps, then exactly K plain steps
+    ms_step = plain_forward(db, args.steps, args.warmup) / args.steps
+    # per-kernel durations: the same K steps again with a HIP event recorded
+    # on the library's stream around every launch (the events themselves add
+    # a few microseconds per launch, so they stay out of the timed region)
+    ev_total_ms, per = timed_forward(db, args.steps, 1)
+    ev_ms = ev_total_ms / args.steps
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step; {ev_ms:.3f} with per-kernel events")
 
     es = 2 if wl.dtype == "bf16" else 4
     peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
@@ -242,7 +265,8 @@ def main() -> int:
         "path_roofline": {"ms": roof_ms, "frac": roof_ms / ms_step,
                           "targets_per_s": b.n_tgt_total / (roof_ms * 1e-3)},
         "kernels": kernels,
-        "ms_per_step_without_kernel_events": plain_ms,
+        "ms_per_step_with_kernel_events": ev_ms,
+        "settle_steps": n_settle,
     }
     if args.ablation:
         rec["ablation"] = ablation(wl, args)
@@ -265,6 +289,12 @@ def train_step(args) -> int:
     b = W.make_batch(wl, with_grad=True)
     db = DeviceBatch(b, device="cuda:0", backward=True)
     dout = to_device(b.grad_out, "cuda:0")
+
+    def step():
+        db.forward()
+        db.backward(dout)
+
+    settle(step, args.settle_seconds)
     for _ in range(args.warmup):
         db.forward()
         db.backward(dout)
