@@ -113,7 +113,8 @@ struct Layout {
   // generic forward
   size_t kv32, q32, abuf, ubuf, hid;
   // backward (generic)
-  size_t pre, dhid, ds, du, da, dq, ds2, dkv32, dq_part, lse32, rs, ru;
+  size_t pre, dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
+  int64_t gpart_floats;
   size_t total;
 };
 
@@ -170,9 +171,17 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->hid = m.take(4 * nt * F);
     }
   } else {
-    L->kv32 = m.take(4 * nh * 2 * d);
-    L->dkv32 = m.take(4 * nh * 2 * d);
-    L->q32 = m.take(4 * nt * d);
+    const bool bf = dims->dtype == STCA_BF16;
+    L->kvs = m.take(4 * n * nh * 2 * d);  // every layer's K | V rows, fp32
+    L->dkv = m.take((bf ? 2 : 4) * nh * 2 * d);
+    L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;  // [W_K | W_V] per layer
+    L->dwkv = bf ? m.take(4 * d * 2 * d) : 0;
+    L->gpart_floats = bf ? gemm_mfma_part_floats(static_cast<int>(d), static_cast<int>(2 * d),
+                                                  static_cast<int>(nh)) : 0;
+    L->gpart = bf ? m.take(4 * L->gpart_floats) : 0;
+    L->rq = m.take(4 * n * nt * d);  // per-layer queries, attention outputs, lse
+    L->ra = m.take(4 * n * nt * d);
+    L->rl = m.take(4 * n * nt * L->h);
     L->hid = m.take(4 * nt * F);
     L->pre = m.take(4 * nt * F);
     L->dhid = m.take(4 * nt * F);
@@ -184,8 +193,6 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->dq_part = m.take(4 * kMaxChunks * nt * d);
     L->part_acc = m.take(4 * kMaxChunks * nt * d);
     L->part_ml = m.take(8 * kMaxChunks * nt * L->h);
-    L->abuf = m.take(4 * nt * d);
-    L->lse32 = m.take(4 * nt * L->h);
     L->rs = m.take(4 * (n + 1) * nt * d);  // recomputed s^(0..n)
     L->ru = m.take(4 * n * nt * d);        // recomputed u^(0..n-1)
   }
@@ -398,9 +405,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   int32_t* tch = at<int32_t>(ws, L.tchunks);
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, units, L.max_units, tch,
                       hdr, st));
-  float* kv = at<float>(ws, L.kv32);
-  float* dkv = at<float>(ws, L.dkv32);
-  float* q = at<float>(ws, L.q32);
+  void* dkv = at<char>(ws, L.dkv);
   float* hid = at<float>(ws, L.hid);
   float* pre = at<float>(ws, L.pre);
   float* dhid = at<float>(ws, L.dhid);
@@ -411,88 +416,119 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   float* ds2 = at<float>(ws, L.ds2);
   float* dqp = at<float>(ws, L.dq_part);
   auto W = [&](const void* base, int i, size_t per) { return static_cast<const char*>(base) + i * per * es; };
-  // history-side products (rows = history items): MFMA with bf16 operands when
-  // the inputs are bf16, the fp32 SIMT GEMM otherwise (fp32 storage keeps
-  // fp32 arithmetic throughout)
-  auto hgemm = [&](int a_bf, int b_bf, int M, int N, int K, const void* A, int64_t lda, int tA, const void* B,
-                   int64_t ldb, int tB, float* C, int64_t ldc, int accumulate) {
-    if (bf)
-      return gemm_mfma(a_bf, b_bf, M, N, K, A, lda, tA, B, ldb, tB, C, ldc, 1.f, accumulate, st);
-    return gemm_generic(a_bf, b_bf, M, N, K, A, lda, tA, B, ldb, tB, C, ldc, 1.f, kEpiStore, nullptr, 0, nullptr,
-                        accumulate, st);
+  auto per_layer = [&](size_t off, int i, size_t per) { return at<float>(ws, off) + (size_t)i * per; };
+  auto RS = [&](int i) { return per_layer(L.rs, i, nt * d); };
+  auto RU = [&](int i) { return per_layer(L.ru, i, nt * d); };
+  auto RQ = [&](int i) { return per_layer(L.rq, i, nt * d); };
+  auto RA = [&](int i) { return per_layer(L.ra, i, nt * d); };
+  auto RL = [&](int i) { return per_layer(L.rl, i, nt * h); };
+  auto KVS = [&](int i) { return per_layer(L.kvs, i, nh * 2 * d); };
+  auto WKV = [&](int i) { return at<bf16_bits>(ws, L.wkv) + (size_t)i * d * 2 * d; };
+  auto gemm = [&](int a_bf, int b_bf, int M, int N, int K, const void* A, int64_t lda, int tA, const void* B,
+                  int64_t ldb, int tB, float* C, int64_t ldc, float alpha, GemmEpi epi, const float* R,
+                  int64_t ldr, float* C2) {
+    return gemm_generic(a_bf, b_bf, M, N, K, A, lda, tA, B, ldb, tB, C, ldc, alpha, epi, R, ldr, C2, 0, st);
   };
-  auto RS = [&](int i) { return at<float>(ws, L.rs) + (size_t)i * nt * d; };
-  auto RU = [&](int i) { return at<float>(ws, L.ru) + (size_t)i * nt * d; };
-  const float qscale0 = kLog2e / std::sqrt(static_cast<float>(L.dh));
-  // forward recomputation (fp32): s^(i), u^(i)
+  const float qscale = kLog2e / std::sqrt(static_cast<float>(L.dh));
+  // History-side products (rows = history items) on bf16 inputs run on the
+  // MFMA GEMM with [W_K | W_V] packed side by side, so K and V of a layer come
+  // from one product; fp32 inputs keep fp32 arithmetic (SIMT GEMM).
+  if (bf) {
+    for (int i = 0; i < n; ++i) {
+      HIPCHK(hipMemcpy2DAsync(WKV(i), 2 * d * 2, W(w->wk, i, (size_t)d * d), d * 2, d * 2, d,
+                              hipMemcpyDeviceToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(WKV(i) + d, 2 * d * 2, W(w->wv, i, (size_t)d * d), d * 2, d * 2, d,
+                              hipMemcpyDeviceToDevice, st));
+    }
+  }
+  // forward recomputation in fp32: s^(i), u^(i), and per layer K|V, the
+  // scaled queries, the attention output and its lse
   HIPCHK(convert(bf, 0, tgt, RS(0), nt * d, st));
   for (int i = 0; i < n; ++i) {
-    const void* Wk = W(w->wk, i, (size_t)d * d);
-    const void* Wv = W(w->wv, i, (size_t)d * d);
-    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 0));
-    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 0));
-    HIPCHK(gemm_generic(0, bf, nt, d, d, RS(i), d, 0, W(w->wq, i, (size_t)d * d), d, 0, q, d, qscale0, kEpiStore,
-                        nullptr, 0, nullptr, 0, st));
-    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, at<float>(ws, L.part_acc),
+    float* kv = KVS(i);
+    if (bf) {
+      HIPCHK(gemm_mfma(static_cast<int>(nh), 2 * d, d, static_cast<const bf16_bits*>(hist), d, 0, WKV(i), 2 * d,
+                       0, kv, 2 * d, 1.f, 0, nullptr, 0, st));
+    } else {
+      HIPCHK(gemm(0, 0, nh, d, d, hist, d, 0, W(w->wk, i, (size_t)d * d), d, 0, kv, 2 * d, 1.f, kEpiStore,
+                  nullptr, 0, nullptr));
+      HIPCHK(gemm(0, 0, nh, d, d, hist, d, 0, W(w->wv, i, (size_t)d * d), d, 0, kv + d, 2 * d, 1.f, kEpiStore,
+                  nullptr, 0, nullptr));
+    }
+    HIPCHK(gemm(0, bf, nt, d, d, RS(i), d, 0, W(w->wq, i, (size_t)d * d), d, 0, RQ(i), d, qscale, kEpiStore,
+                nullptr, 0, nullptr));
+    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, RQ(i), kv, d, at<float>(ws, L.part_acc),
                         at<float>(ws, L.part_ml), nt, st));
-    HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml),
-                         at<float>(ws, L.abuf), nullptr, st));
-    HIPCHK(gemm_generic(0, bf, nt, d, d, at<float>(ws, L.abuf), d, 0, W(w->wo, i, (size_t)d * d), d, 0, RU(i), d,
-                        1.f, kEpiAddRes, RS(i), d, nullptr, 0, st));
-    HIPCHK(gemm_generic(0, bf, nt, F, d, RU(i), d, 0, W(w->w1, i, (size_t)d * F), F, 0, hid, F, 1.f, kEpiRelu,
-                        nullptr, 0, nullptr, 0, st));
-    HIPCHK(gemm_generic(0, bf, nt, d, F, hid, F, 0, W(w->w2, i, (size_t)d * F), d, 0, RS(i + 1), d, 1.f,
-                        kEpiAddRes, RU(i), d, nullptr, 0, st));
+    HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml), RA(i), RL(i),
+                         st));
+    HIPCHK(gemm(0, bf, nt, d, d, RA(i), d, 0, W(w->wo, i, (size_t)d * d), d, 0, RU(i), d, 1.f, kEpiAddRes, RS(i),
+                d, nullptr));
+    HIPCHK(gemm(0, bf, nt, F, d, RU(i), d, 0, W(w->w1, i, (size_t)d * F), F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0,
+                nullptr));
+    HIPCHK(gemm(0, bf, nt, d, F, hid, F, 0, W(w->w2, i, (size_t)d * F), d, 0, RS(i + 1), d, 1.f, kEpiAddRes,
+                RU(i), d, nullptr));
   }
   HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
-  HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
-  const float qscale = kLog2e / std::sqrt(static_cast<float>(L.dh));
+  // rows of requests without targets keep a zero gradient
+  HIPCHK(fill_f32(static_cast<float*>(dkv), 0.f, nh * 2 * d * static_cast<int64_t>(es) / 4, st));
+  if (!bf) HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
   for (int i = n - 1; i >= 0; --i) {
     const float* s = RS(i);
     const float* u = RU(i);
-    // a and lse are recomputed below in fp32 from the same q, K, V that the
-    // softmax weights are rebuilt from, so rowsum(dA * A) matches P exactly
-    float* a = at<float>(ws, L.abuf);
-    float* lse = at<float>(ws, L.lse32);
+    const float* a = RA(i);
+    const float* kv = KVS(i);
     const void* W1 = W(w->w1, i, (size_t)d * F);
     const void* W2 = W(w->w2, i, (size_t)d * F);
     const void* Wo = W(w->wo, i, (size_t)d * d);
     const void* Wq = W(w->wq, i, (size_t)d * d);
-    const void* Wk = W(w->wk, i, (size_t)d * d);
-    const void* Wv = W(w->wv, i, (size_t)d * d);
-    // recompute this layer's K, V, q and attention output in fp32
-    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wk, d, 0, kv, 2 * d, 0));
-    HIPCHK(hgemm(bf, bf, nh, d, d, hist, d, 0, Wv, d, 0, kv + d, 2 * d, 0));
-    HIPCHK(gemm_generic(0, bf, nt, d, d, s, d, 0, Wq, d, 0, q, d, qscale, kEpiStore, nullptr, 0, nullptr, 0, st));
-    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, at<float>(ws, L.part_acc),
-                        at<float>(ws, L.part_ml), nt, st));
-    HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml), a, lse, st));
     // s' = u + ReLU(u W1) W2
-    HIPCHK(gemm_generic(0, bf, nt, F, d, u, d, 0, W1, F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0, pre, 0, st));
-    HIPCHK(gemm_generic(0, 0, F, d, nt, hid, F, 1, ds, d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, kEpiStore,
-                        nullptr, 0, nullptr, 0, st));
-    HIPCHK(gemm_generic(0, bf, nt, F, d, ds, d, 0, W2, d, 1, dhid, F, 1.f, kEpiStore, nullptr, 0, nullptr, 0, st));
+    HIPCHK(gemm(0, bf, nt, F, d, u, d, 0, W1, F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0, pre));
+    HIPCHK(gemm(0, 0, F, d, nt, hid, F, 1, ds, d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, kEpiStore, nullptr, 0,
+                nullptr));
+    HIPCHK(gemm(0, bf, nt, F, d, ds, d, 0, W2, d, 1, dhid, F, 1.f, kEpiStore, nullptr, 0, nullptr));
     HIPCHK(relu_mask_mul(dhid, pre, nt * F, st));
-    HIPCHK(gemm_generic(0, 0, d, F, nt, u, d, 1, dhid, F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, kEpiStore,
-                        nullptr, 0, nullptr, 0, st));
-    HIPCHK(gemm_generic(0, bf, nt, d, F, dhid, F, 0, W1, F, 1, du, d, 1.f, kEpiAddRes, ds, d, nullptr, 0, st));
+    HIPCHK(gemm(0, 0, d, F, nt, u, d, 1, dhid, F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, kEpiStore, nullptr, 0,
+                nullptr));
+    HIPCHK(gemm(0, bf, nt, d, F, dhid, F, 0, W1, F, 1, du, d, 1.f, kEpiAddRes, ds, d, nullptr));
     // u = s + a Wo
-    HIPCHK(gemm_generic(0, 0, d, d, nt, a, d, 1, du, d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, kEpiStore,
-                        nullptr, 0, nullptr, 0, st));
-    HIPCHK(gemm_generic(0, bf, nt, d, d, du, d, 0, Wo, d, 1, da, d, 1.f, kEpiStore, nullptr, 0, nullptr, 0, st));
-    // attention
-    HIPCHK(fill_f32(dkv, 0.f, nh * 2 * d, st));
-    HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, q, kv, d, a, da, lse, dqp, dkv, nt, st));
+    HIPCHK(gemm(0, 0, d, d, nt, a, d, 1, du, d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
+                nullptr));
+    HIPCHK(gemm(0, bf, nt, d, d, du, d, 0, Wo, d, 1, da, d, 1.f, kEpiStore, nullptr, 0, nullptr));
+    // attention (softmax weights rebuilt from the same q, K, V and lse that
+    // gave a, so rowsum(dA * A) matches them)
+    HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, b->tgt_off, RQ(i), kv, d, a, da, RL(i), dqp, dkv, bf,
+                            nt, st));
     HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
     // q = s Wq
-    HIPCHK(gemm_generic(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore,
-                        nullptr, 0, nullptr, 0, st));
-    HIPCHK(gemm_generic(0, bf, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr, 0, st));
-    // K = X Wk, V = X Wv
-    HIPCHK(hgemm(bf, 0, d, d, nh, hist, d, 1, dkv, 2 * d, 0, dw->dwk + (size_t)i * d * d, d, 0));
-    HIPCHK(hgemm(bf, 0, d, d, nh, hist, d, 1, dkv + d, 2 * d, 0, dw->dwv + (size_t)i * d * d, d, 0));
-    HIPCHK(hgemm(0, bf, nh, d, d, dkv, 2 * d, 0, Wk, d, 1, dhist, d, 1));
-    HIPCHK(hgemm(0, bf, nh, d, d, dkv + d, 2 * d, 0, Wv, d, 1, dhist, d, 1));
+    HIPCHK(gemm(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
+                nullptr));
+    HIPCHK(gemm(0, bf, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr));
+    // [K | V] = X [W_K | W_V]
+    if (bf) {
+      const bf16_bits* X = static_cast<const bf16_bits*>(hist);
+      const bf16_bits* dKV = static_cast<const bf16_bits*>(dkv);
+      float* dwkv = at<float>(ws, L.dwkv);
+      HIPCHK(gemm_mfma(d, 2 * d, static_cast<int>(nh), X, d, 1, dKV, 2 * d, 0, dwkv, 2 * d, 1.f, 0,
+                       at<float>(ws, L.gpart), L.gpart_floats, st));
+      HIPCHK(hipMemcpy2DAsync(dw->dwk + (size_t)i * d * d, d * 4, dwkv, 2 * d * 4, d * 4, d,
+                              hipMemcpyDeviceToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(dw->dwv + (size_t)i * d * d, d * 4, dwkv + d, 2 * d * 4, d * 4, d,
+                              hipMemcpyDeviceToDevice, st));
+      HIPCHK(gemm_mfma(static_cast<int>(nh), d, 2 * d, dKV, 2 * d, 0, WKV(i), 2 * d, 1, dhist, d, 1.f,
+                       i != n - 1, nullptr, 0, st));
+    } else {
+      const float* dKV = static_cast<const float*>(dkv);
+      const void* Wk = W(w->wk, i, (size_t)d * d);
+      const void* Wv = W(w->wv, i, (size_t)d * d);
+      HIPCHK(gemm(0, 0, d, d, nh, hist, d, 1, dKV, 2 * d, 0, dw->dwk + (size_t)i * d * d, d, 1.f, kEpiStore,
+                  nullptr, 0, nullptr));
+      HIPCHK(gemm(0, 0, d, d, nh, hist, d, 1, dKV + d, 2 * d, 0, dw->dwv + (size_t)i * d * d, d, 1.f, kEpiStore,
+                  nullptr, 0, nullptr));
+      HIPCHK(gemm_generic(0, 0, nh, d, d, dKV, 2 * d, 0, Wk, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0, nullptr, 1,
+                          st));
+      HIPCHK(gemm_generic(0, 0, nh, d, d, dKV + d, 2 * d, 0, Wv, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0,
+                          nullptr, 1, st));
+    }
     std::swap(ds, ds2);
   }
   HIPCHK(convert(0, 0, ds, dtgt, nt * d, st));

@@ -1,15 +1,21 @@
-// General MFMA GEMM for the backward pass's history-side products:
+// MFMA GEMM with bf16 operands and fp32 accumulation for the backward pass's
+// history-side products:
 //   C[M,N] (fp32) = alpha * op(A) op(B)  (+ C when accumulating)
-// A and B are bf16 or fp32 (fp32 operands are rounded to bf16 as they are
-// staged), either may be read transposed.  Products: the per-layer K/V of the
-// history (X W_K, X W_V; bf16 inputs, exact up to fp32 accumulation), the
-// history gradient (dX += dK W_K^T + dV W_V^T) and the projection weight
-// gradients (dW_K = X^T dK, dW_V = X^T dV, split over the long K dimension).
+// Products: the per-layer K/V of the history ([K | V] = X [W_K | W_V], one
+// product for both), the projection weight gradients ([dW_K | dW_V] =
+// X^T [dK | dV], K = history rows, split over K) and the history gradient
+// (dX += [dK | dV] [W_K | W_V]^T).
 //
 // 128 x 128 output tile per workgroup of four waves (2 x 2), each wave 64 x 64
-// as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles; 32-deep k tiles staged in LDS with
-// k contiguous per row (16-byte operand reads, rows padded against bank
-// conflicts).
+// as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  64-deep k tiles go global ->
+// registers (16-byte loads, the next tile's loads in flight while the current
+// one is multiplied) -> LDS (double-buffered, rows with k contiguous and
+// padded by 16 bytes) -> MFMA operands (16-byte LDS reads).  An operand whose
+// source has k contiguous is copied row by row; one whose source has the row
+// index contiguous is transposed on its way into LDS.  Tiles are handed to the
+// eight XCDs in contiguous ranges, so the tiles that share a row block of A
+// (and, split over K, every tile of one K range) run on one XCD and share its
+// L2.  A split over K writes per-split partial tiles that a second kernel sums.
 #include <algorithm>
 
 #include "common.h"
@@ -19,143 +25,194 @@ namespace stca {
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 32;
-constexpr int LROW = BK + 8;  // padded LDS row (bf16)
+constexpr int BM = 128, BN = 128, BK = 64;
+constexpr int LROW = BK + 8;  // padded LDS row, in bf16 elements (144 bytes)
+constexpr int kXcds = 8;
+
+typedef unsigned short u16x8 __attribute__((ext_vector_type(8)));
 
 __device__ __forceinline__ f32x16 mfma_bf(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-template <typename T>
-__device__ __forceinline__ __bf16 as_bf16(T v);
-template <>
-__device__ __forceinline__ __bf16 as_bf16<bf16_bits>(bf16_bits v) {
-  return __builtin_bit_cast(__bf16, v);
-}
-template <>
-__device__ __forceinline__ __bf16 as_bf16<float>(float v) {
-  return static_cast<__bf16>(v);  // round to nearest even
+// One operand tile: 128 rows x 64 k = 1024 vectors of 8 bf16, four per thread.
+// kcontig: element (row, k) at src[row * ld + k]; else at src[k * ld + row].
+// Vectors are whole or absent: the caller guarantees that the contiguous
+// extent (K, or the row count) is a multiple of 8 and chunk ends are multiples
+// of BK.
+template <bool kcontig>
+__device__ __forceinline__ void load_tile(u16x8 (&r)[4], const bf16_bits* __restrict__ src, int64_t ld, int row0,
+                                          int nrows, int k0, int kend) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int v = threadIdx.x + 256 * i;
+    bool ok;
+    int64_t off;
+    if (kcontig) {
+      const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
+      ok = row0 + row < nrows && k0 + kk < kend;
+      off = (int64_t)(row0 + row) * ld + k0 + kk;
+    } else {
+      const int kk = v / (BM / 8), row = (v % (BM / 8)) * 8;
+      ok = k0 + kk < kend && row0 + row < nrows;
+      off = (int64_t)(k0 + kk) * ld + row0 + row;
+    }
+    r[i] = ok ? *reinterpret_cast<const u16x8*>(src + off) : u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+  }
 }
 
-// Stage a [rows x BK] operand tile into LDS as rows with k contiguous.
-// "row" is M for A and N for B.  kmajor: the source holds element (row, k) at
-// src[k * ld + row] (k-major); otherwise at src[row * ld + k].
-template <typename T>
-__device__ __forceinline__ void stage(__bf16* __restrict__ lds, const T* __restrict__ src, int64_t ld, bool kmajor,
-                                      int row0, int nrows, int k0, int nk) {
-  // 128 rows x 32 k = 4096 elements, 256 threads: 16 elements each, as two
-  // runs of 8 consecutive source elements
+template <bool kcontig>
+__device__ __forceinline__ void store_tile(bf16_bits* __restrict__ lds, const u16x8 (&r)[4]) {
 #pragma unroll
-  for (int r = 0; r < 2; ++r) {
-    const int run = threadIdx.x + r * 256;  // 512 runs of 8
-    if (!kmajor) {
-      const int row = run / (BK / 8), kk = (run % (BK / 8)) * 8;
-      __bf16 v[8];
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool ok = row0 + row < nrows && k0 + kk + e < nk;
-        v[e] = ok ? as_bf16<T>(src[(int64_t)(row0 + row) * ld + k0 + kk + e]) : static_cast<__bf16>(0.f);
-      }
-#pragma unroll
-      for (int e = 0; e < 8; ++e) lds[row * LROW + kk + e] = v[e];
+  for (int i = 0; i < 4; ++i) {
+    const int v = threadIdx.x + 256 * i;
+    if (kcontig) {
+      const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
+      *reinterpret_cast<u16x8*>(lds + row * LROW + kk) = r[i];
     } else {
-      const int kk = run / (BM / 8), row = (run % (BM / 8)) * 8;
+      const int kk = v / (BM / 8), row = (v % (BM / 8)) * 8;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const bool ok = row0 + row + e < nrows && k0 + kk < nk;
-        lds[(row + e) * LROW + kk] =
-            ok ? as_bf16<T>(src[(int64_t)(k0 + kk) * ld + row0 + row + e]) : static_cast<__bf16>(0.f);
-      }
+      for (int e = 0; e < 8; ++e) lds[(row + e) * LROW + kk] = r[i][e];
     }
   }
 }
 
-template <typename TA, typename TB>
-__global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, const TA* __restrict__ A, int64_t lda,
-                                                        int transA, const TB* __restrict__ B, int64_t ldb,
-                                                        int transB, float* __restrict__ C, int64_t ldc, float alpha,
-                                                        int accumulate, int k_chunk) {
-  __shared__ __attribute__((aligned(16))) __bf16 As[BM * LROW];
-  __shared__ __attribute__((aligned(16))) __bf16 Bs[BN * LROW];
+// op(A) element (m, k): A[m * lda + k] if A_KC else A[k * lda + m].
+// op(B) element (k, n): B[n * ldb + k] if B_KC else B[k * ldb + n].
+template <bool A_KC, bool B_KC>
+__global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, const bf16_bits* __restrict__ A,
+                                                        int64_t lda, const bf16_bits* __restrict__ B, int64_t ldb,
+                                                        float* __restrict__ C, int64_t ldc, float alpha,
+                                                        int accumulate, int k_chunk, int n_tiles_m, int n_tiles_n,
+                                                        int n_work, float* __restrict__ part) {
+  __shared__ __attribute__((aligned(16))) bf16_bits As[2][BM * LROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits Bs[2][BN * LROW];
+  // contiguous range of work items per XCD (workgroups are dealt to XCDs
+  // round robin by their linear index)
+  const int lid = blockIdx.x;
+  const int per = gridDim.x / kXcds;
+  const int w_id = (lid % kXcds) * per + lid / kXcds;
+  if (w_id >= n_work) return;
+  const int tiles = n_tiles_m * n_tiles_n;
+  const int split = w_id / tiles, t = w_id % tiles;
+  const int m0 = (t / n_tiles_n) * BM, n0 = (t % n_tiles_n) * BN;
+  const int kb = split * k_chunk;
+  const int ke = min(K, kb + k_chunk);
+
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int wm = (wave / 2) * 64, wn = (wave % 2) * 64;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int kb = blockIdx.z * k_chunk;
-  const int ke = min(K, kb + k_chunk);
-  f32x16 acc[2][2] = {};
   const int r32 = lane % 32, hi = lane / 32;
+  f32x16 acc[2][2] = {};
+  u16x8 ra[4], rb[4];
+  load_tile<A_KC>(ra, A, lda, m0, M, kb, ke);
+  load_tile<B_KC>(rb, B, ldb, n0, N, kb, ke);
+  store_tile<A_KC>(As[0], ra);
+  store_tile<B_KC>(Bs[0], rb);
+  __syncthreads();
+  int cur = 0;
   for (int k0 = kb; k0 < ke; k0 += BK) {
-    // A: op(A) element (m, k) is A[m][k] (not transposed) or A[k][m]
-    stage<TA>(As, A, lda, transA != 0, m0, M, k0, ke);
-    // B: op(B) element (k, n) is B[k][n] (not transposed: k-major as a
-    // [n][k] tile) or B[n][k]
-    stage<TB>(Bs, B, ldb, transB == 0, n0, N, k0, ke);
-    __syncthreads();
+    const bool more = k0 + BK < ke;
+    if (more) {
+      load_tile<A_KC>(ra, A, lda, m0, M, k0 + BK, ke);
+      load_tile<B_KC>(rb, B, ldb, n0, N, k0 + BK, ke);
+    }
+    const bf16_bits* as = As[cur];
+    const bf16_bits* bs = Bs[cur];
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       bf16x8 a[2], b[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        a[i] = *reinterpret_cast<const bf16x8*>(&As[(wm + 32 * i + r32) * LROW + ks * 16 + hi * 8]);
-        b[i] = *reinterpret_cast<const bf16x8*>(&Bs[(wn + 32 * i + r32) * LROW + ks * 16 + hi * 8]);
+        a[i] = *reinterpret_cast<const bf16x8*>(as + (wm + 32 * i + r32) * LROW + ks * 16 + hi * 8);
+        b[i] = *reinterpret_cast<const bf16x8*>(bs + (wn + 32 * i + r32) * LROW + ks * 16 + hi * 8);
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int jj = 0; jj < 2; ++jj) acc[i][jj] = mfma_bf(a[i], b[jj], acc[i][jj]);
+        for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf(a[i], b[j], acc[i][j]);
+    }
+    if (more) {
+      store_tile<A_KC>(As[cur ^ 1], ra);
+      store_tile<B_KC>(Bs[cur ^ 1], rb);
     }
     __syncthreads();
+    cur ^= 1;
   }
   // result lane layout: column n = lane % 32, rows 8 (v / 4) + 4 hi + v % 4
+  float* out = part ? part + (int64_t)split * M * N : C;
+  const int64_t ldo = part ? N : ldc;
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int jj = 0; jj < 2; ++jj) {
-      const int n = n0 + wn + 32 * jj + r32;
+    for (int j = 0; j < 2; ++j) {
+      const int n = n0 + wn + 32 * j + r32;
       if (n >= N) continue;
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int m = m0 + wm + 32 * i + 8 * (v / 4) + 4 * hi + (v % 4);
         if (m >= M) continue;
-        float* c = C + (int64_t)m * ldc + n;
-        const float x = alpha * acc[i][jj][v];
-        if (gridDim.z > 1)
-          atomicAdd(c, x);
+        float* c = out + (int64_t)m * ldo + n;
+        if (part)
+          *c = acc[i][j][v];
         else
-          *c = accumulate ? *c + x : x;
+          *c = accumulate ? *c + alpha * acc[i][j][v] : alpha * acc[i][j][v];
       }
     }
 }
 
-__global__ void zero2d_kernel(float* __restrict__ C, int64_t ldc, int M, int N) {
+__global__ void split_sum_kernel(const float* __restrict__ part, int splits, int M, int N, float* __restrict__ C,
+                                 int64_t ldc, float alpha, int accumulate) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < (int64_t)M * N) C[(i / N) * ldc + i % N] = 0.f;
+  if (i >= (int64_t)M * N) return;
+  float s = 0.f;
+  for (int k = 0; k < splits; ++k) s += part[(int64_t)k * M * N + i];
+  float* c = C + (i / N) * ldc + i % N;
+  *c = accumulate ? *c + alpha * s : alpha * s;
 }
+
+bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace
 
-hipError_t gemm_mfma(int a_bf16, int b_bf16, int M, int N, int K, const void* A, int64_t lda, int transA,
-                     const void* B, int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate,
-                     hipStream_t st) {
-  if (M == 0 || N == 0) return hipSuccess;
+int64_t gemm_mfma_part_floats(int M, int N, int K) {
   const int64_t tiles = ceil_div(M, BM) * ceil_div(N, BN);
+  if (tiles >= 256 || K < 8192) return 0;
+  return std::min<int64_t>(ceil_div(1024, tiles), K / 2048) * M * N;
+}
+
+hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
+                     int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
+                     int64_t part_floats, hipStream_t st) {
+  if (M == 0 || N == 0) return hipSuccess;
+  const bool a_kc = !transA, b_kc = transB;
+  // whole 16-byte vectors: the contiguous extent of each operand is a
+  // multiple of 8 elements and every row starts 16-byte aligned
+  if ((a_kc ? K : M) % 8 || (b_kc ? K : N) % 8 || lda % 8 || ldb % 8 || !al16(A) || !al16(B))
+    return hipErrorInvalidValue;
+  const int tm = static_cast<int>(ceil_div(M, BM)), tn = static_cast<int>(ceil_div(N, BN));
+  const int64_t tiles = (int64_t)tm * tn;
   int splits = 1;
-  if (tiles < 256 && K >= 8192) splits = static_cast<int>(std::min<int64_t>(ceil_div(512, tiles), K / 4096));
-  if (splits < 1) splits = 1;
-  const int k_chunk = static_cast<int>(round_up(ceil_div(K, splits), BK));
+  if (part && tiles < 256 && K >= 8192) {
+    splits = static_cast<int>(std::min<int64_t>(ceil_div(1024, tiles), K / 2048));
+    while (splits > 1 && (int64_t)splits * M * N > part_floats) --splits;
+  }
+  const int k_chunk = std::max(BK, static_cast<int>(round_up(ceil_div(K, splits), BK)));
   splits = static_cast<int>(ceil_div(K, k_chunk));
-  if (splits > 1 && !accumulate)
-    hipLaunchKernelGGL(zero2d_kernel, dim3(static_cast<unsigned>(ceil_div((int64_t)M * N, 256))), dim3(256), 0, st,
-                       C, ldc, M, N);
-  dim3 g(static_cast<unsigned>(ceil_div(N, BN)), static_cast<unsigned>(ceil_div(M, BM)), splits);
-#define STCA_MG(TA, TB)                                                                                 \
-  hipLaunchKernelGGL((mfma_gemm_kernel<TA, TB>), g, dim3(256), 0, st, M, N, K, (const TA*)A, lda, transA, \
-                     (const TB*)B, ldb, transB, C, ldc, alpha, accumulate, k_chunk)
-  if (a_bf16 && b_bf16) STCA_MG(bf16_bits, bf16_bits);
-  else if (a_bf16) STCA_MG(bf16_bits, float);
-  else if (b_bf16) STCA_MG(float, bf16_bits);
-  else STCA_MG(float, float);
+  float* p = splits > 1 ? part : nullptr;
+  const int64_t work = tiles * splits;
+  const int64_t grid = round_up(work, kXcds);
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
+#define STCA_MG(AK, BKC)                                                                                    \
+  hipLaunchKernelGGL((mfma_gemm_kernel<AK, BKC>), dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, M, N, \
+                     K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, tm, tn, static_cast<int>(work), p)
+  if (a_kc && b_kc) STCA_MG(true, true);
+  else if (a_kc) STCA_MG(true, false);
+  else if (b_kc) STCA_MG(false, true);
+  else STCA_MG(false, false);
 #undef STCA_MG
+  if (p)
+    hipLaunchKernelGGL(split_sum_kernel, dim3(static_cast<unsigned>(ceil_div((int64_t)M * N, 256))), dim3(256), 0,
+                       st, p, splits, M, N, C, ldc, alpha, accumulate);
   return hipGetLastError();
 }
 

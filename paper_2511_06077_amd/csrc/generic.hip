@@ -96,8 +96,8 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA
 //  * target lanes: lane = (target t, stream st), 64 / TP streams for TP =
 //    16, 32 or 64 target slots; each lane keeps its own target's state and
 //    visits every (64 / TP)-th token of its wave's share of a 64-row K/V tile
-//    staged in LDS (rows of one token are read by many lanes at once, which
-//    LDS serves as broadcasts);
+//    staged in LDS (one row is read by many lanes at once, which LDS serves as
+//    a broadcast; rows are padded to keep 16-byte reads conflict-free);
 //  * token lanes: lane = history row; the targets' vectors are broadcast from
 //    LDS.
 // A workgroup (4 waves) handles one (unit, head).
@@ -106,14 +106,50 @@ constexpr int kTile = 64;
 __device__ __forceinline__ int target_slots(int nt) { return nt <= 16 ? 16 : (nt <= 32 ? 32 : 64); }
 
 template <int DH>
-__device__ __forceinline__ void stage_kv_tile(float (*kt)[DH + 1], float (*vt)[DH + 1], const float* __restrict__ KV,
-                                              int d, int j, int base, int lo, int hi) {
-  for (int e = threadIdx.x; e < kTile * DH; e += 256) {
-    const int r = e / DH, c = e % DH;
+struct KvTile {
+  float k[kTile][DH + 4];
+  float v[kTile][DH + 4];
+};
+
+template <int DH>
+__device__ __forceinline__ void stage_kv_tile(KvTile<DH>& T, const float* __restrict__ KV, int d, int j, int base,
+                                              int lo, int hi) {
+  for (int e = threadIdx.x; e < kTile * DH / 4; e += 256) {
+    const int r = e / (DH / 4), c = (e % (DH / 4)) * 4;
     const int tok = base + r;
     const bool on = tok >= lo && tok < hi;
-    kt[r][c] = on ? KV[(int64_t)tok * 2 * d + j * DH + c] : 0.f;
-    vt[r][c] = on ? KV[(int64_t)tok * 2 * d + d + j * DH + c] : 0.f;
+    const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+    *reinterpret_cast<float4*>(&T.k[r][c]) =
+        on ? *reinterpret_cast<const float4*>(KV + (int64_t)tok * 2 * d + j * DH + c) : z;
+    *reinterpret_cast<float4*>(&T.v[r][c]) =
+        on ? *reinterpret_cast<const float4*>(KV + (int64_t)tok * 2 * d + d + j * DH + c) : z;
+  }
+}
+
+template <int DH>
+__device__ __forceinline__ float dot_row(const float (&x)[DH], const float* __restrict__ row) {
+  float s = 0.f;
+#pragma unroll
+  for (int e = 0; e < DH; e += 4) {
+    const float4 r = *reinterpret_cast<const float4*>(row + e);
+    s = fmaf(x[e], r.x, s);
+    s = fmaf(x[e + 1], r.y, s);
+    s = fmaf(x[e + 2], r.z, s);
+    s = fmaf(x[e + 3], r.w, s);
+  }
+  return s;
+}
+
+// acc = acc * f + p * row
+template <int DH>
+__device__ __forceinline__ void axpby_row(float (&acc)[DH], float f, float p, const float* __restrict__ row) {
+#pragma unroll
+  for (int e = 0; e < DH; e += 4) {
+    const float4 r = *reinterpret_cast<const float4*>(row + e);
+    acc[e] = fmaf(p, r.x, acc[e] * f);
+    acc[e + 1] = fmaf(p, r.y, acc[e + 1] * f);
+    acc[e + 2] = fmaf(p, r.z, acc[e + 2] * f);
+    acc[e + 3] = fmaf(p, r.w, acc[e + 3] * f);
   }
 }
 
@@ -127,7 +163,7 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(const Unit* __restric
                                                            float* __restrict__ part_acc,
                                                            float* __restrict__ part_ml, int64_t n_tgt,
                                                            int n_heads) {
-  __shared__ float kt[kTile][DH + 1], vt[kTile][DH + 1];
+  __shared__ __attribute__((aligned(16))) KvTile<DH> T;
   __shared__ float red[4][64][DH + 2];
   const int u = blockIdx.x;
   if (u >= hdr->n_units) return;
@@ -147,19 +183,16 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(const Unit* __restric
   const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
   for (int base = lo; base < hi; base += kTile) {
     __syncthreads();
-    stage_kv_tile<DH>(kt, vt, KV, d, j, base, lo, hi);
+    stage_kv_tile<DH>(T, KV, d, j, base, lo, hi);
     __syncthreads();
     for (int r = w * 16 + st; r < w * 16 + 16; r += S) {
       if (base + r >= hi) break;
-      float sc = 0.f;
-#pragma unroll
-      for (int e = 0; e < DH; ++e) sc = fmaf(q[e], kt[r][e], sc);
+      const float sc = dot_row<DH>(q, T.k[r]);
       const float mn = fmaxf(m, sc);
       const float f = exp2f(m - mn);
       const float p = exp2f(sc - mn);
       l = l * f + p;
-#pragma unroll
-      for (int e = 0; e < DH; ++e) acc[e] = fmaf(p, vt[r][e], acc[e] * f);
+      axpby_row<DH>(acc, f, p, T.v[r]);
       m = mn;
     }
   }
@@ -233,63 +266,100 @@ __global__ void merge_generic_kernel(int dh, int n_heads, int64_t n_tgt, const i
 // With p = softmax weight, dp = dA . v, D = rowsum(dA * A):
 //   de = p (dp - D);  dq = sum_rows de k / sqrt(d_h);  dk = sum_targets de q / sqrt(d_h);
 //   dv = sum_targets p dA.
-// dK/dV: token lanes (each lane owns one history row and loops over the
-// unit's targets).  dq: target lanes.  The rows of one request can be shared
-// by several target groups, so dK/dV are added atomically.
-template <int DH>
+// dK/dV: token lanes; each history row's gradient is summed over every target
+// of its request by one thread (the unit of the request's first target group
+// does it, in batches of kTargetGroup targets), so it is written, not added.
+// dq: target lanes.
+
+template <typename T>
+__device__ __forceinline__ void store_row(T* dst, const float* v, int n, float scale);
+template <>
+__device__ __forceinline__ void store_row<float>(float* dst, const float* v, int n, float scale) {
+  for (int e = 0; e < n; e += 4)
+    *reinterpret_cast<float4*>(dst + e) = make_float4(v[e] * scale, v[e + 1] * scale, v[e + 2] * scale,
+                                                      v[e + 3] * scale);
+}
+template <>
+__device__ __forceinline__ void store_row<bf16_bits>(bf16_bits* dst, const float* v, int n, float scale) {
+  for (int e = 0; e < n; e += 4) {
+    ushort4 o;
+    o.x = from_f32<bf16_bits>(v[e] * scale);
+    o.y = from_f32<bf16_bits>(v[e + 1] * scale);
+    o.z = from_f32<bf16_bits>(v[e + 2] * scale);
+    o.w = from_f32<bf16_bits>(v[e + 3] * scale);
+    *reinterpret_cast<ushort4*>(dst + e) = o;
+  }
+}
+
+template <int DH, typename OT>
 __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(
-    const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const float* __restrict__ Q,
-    const float* __restrict__ KV, int d, const float* __restrict__ a, const float* __restrict__ da,
-    const float* __restrict__ lse, float* __restrict__ dKV, int n_heads) {
-  __shared__ float qs[kTargetGroup][DH], das[kTargetGroup][DH], cs[kTargetGroup][2];
+    const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const int32_t* __restrict__ toff,
+    const float* __restrict__ Q, const float* __restrict__ KV, int d, const float* __restrict__ a,
+    const float* __restrict__ da, const float* __restrict__ lse, OT* __restrict__ dKV, int n_heads) {
+  __shared__ __attribute__((aligned(16))) float qs[kTargetGroup][DH];
+  __shared__ __attribute__((aligned(16))) float das[kTargetGroup][DH];
+  __shared__ float cs[kTargetGroup][2];
   const int u = blockIdx.x;
   if (u >= hdr->n_units) return;
   const Unit un = units[u];
+  const int T0 = toff[un.r], T1 = toff[un.r + 1];
+  if (un.t0 != T0) return;  // not the request's first target group
   const int j = blockIdx.y;
-  for (int e = threadIdx.x; e < un.nt * DH; e += 256) {
-    const int64_t t = un.t0 + e / DH;
-    qs[e / DH][e % DH] = Q[t * d + j * DH + e % DH];
-    das[e / DH][e % DH] = da[t * d + j * DH + e % DH];
-  }
-  for (int tt = threadIdx.x; tt < un.nt; tt += 256) {
-    const int64_t t = un.t0 + tt;
-    float D = 0.f;
-    for (int e = 0; e < DH; ++e) D += da[t * d + j * DH + e] * a[t * d + j * DH + e];
-    cs[tt][0] = lse[t * n_heads + j] * kLog2e;
-    cs[tt][1] = D;
-  }
+  const int nbatch = static_cast<int>(ceil_div(T1 - T0, kTargetGroup));
+  auto stage = [&](int tb) {
+    const int nb = min(kTargetGroup, T1 - tb);
+    for (int e = threadIdx.x; e < nb * DH; e += 256) {
+      const int64_t t = tb + e / DH;
+      qs[e / DH][e % DH] = Q[t * d + j * DH + e % DH];
+      das[e / DH][e % DH] = da[t * d + j * DH + e % DH];
+    }
+    for (int tt = threadIdx.x; tt < nb; tt += 256) {
+      const int64_t t = tb + tt;
+      float D = 0.f;
+      for (int e = 0; e < DH; ++e) D += da[t * d + j * DH + e] * a[t * d + j * DH + e];
+      cs[tt][0] = lse[t * n_heads + j] * kLog2e;
+      cs[tt][1] = D;
+    }
+  };
+  if (nbatch == 1) stage(T0);
   __syncthreads();
   const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
-  for (int tok = lo + threadIdx.x; tok < hi; tok += 256) {
+  for (int base = lo; base < hi; base += 256) {
+    const int tok = base + threadIdx.x;
+    const bool on = tok < hi;
     float k[DH], v[DH], dk[DH], dv[DH];
 #pragma unroll
-    for (int e = 0; e < DH; ++e) {
-      k[e] = KV[(int64_t)tok * 2 * d + j * DH + e];
-      v[e] = KV[(int64_t)tok * 2 * d + d + j * DH + e];
-      dk[e] = 0.f;
-      dv[e] = 0.f;
+    for (int e = 0; e < DH; e += 4) {
+      const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float4 kk = on ? *reinterpret_cast<const float4*>(KV + (int64_t)tok * 2 * d + j * DH + e) : z;
+      const float4 vv = on ? *reinterpret_cast<const float4*>(KV + (int64_t)tok * 2 * d + d + j * DH + e) : z;
+      k[e] = kk.x, k[e + 1] = kk.y, k[e + 2] = kk.z, k[e + 3] = kk.w;
+      v[e] = vv.x, v[e + 1] = vv.y, v[e + 2] = vv.z, v[e + 3] = vv.w;
     }
-    for (int tt = 0; tt < un.nt; ++tt) {
-      float s = 0.f, dp = 0.f;
 #pragma unroll
-      for (int e = 0; e < DH; ++e) {
-        s = fmaf(qs[tt][e], k[e], s);
-        dp = fmaf(das[tt][e], v[e], dp);
+    for (int e = 0; e < DH; ++e) dk[e] = dv[e] = 0.f;
+    for (int bt = 0; bt < nbatch; ++bt) {
+      const int tb = T0 + bt * kTargetGroup;
+      if (nbatch > 1) {
+        __syncthreads();
+        stage(tb);
+        __syncthreads();
       }
-      const float p = exp2f(s - cs[tt][0]);
-      const float de = p * (dp - cs[tt][1]);
-#pragma unroll
-      for (int e = 0; e < DH; ++e) {
-        dk[e] = fmaf(de, qs[tt][e], dk[e]);
-        dv[e] = fmaf(p, das[tt][e], dv[e]);
+      const int nb = min(kTargetGroup, T1 - tb);
+      for (int tt = 0; tt < nb; ++tt) {
+        const float s = dot_row<DH>(k, qs[tt]);
+        const float dp = dot_row<DH>(v, das[tt]);
+        const float p = exp2f(s - cs[tt][0]);
+        const float de = p * (dp - cs[tt][1]);
+        axpby_row<DH>(dk, 1.f, de, qs[tt]);
+        axpby_row<DH>(dv, 1.f, p, das[tt]);
       }
     }
     // Q holds log2(e)/sqrt(d_h) times the true query: dk of the true query
     // is de q / sqrt(d_h) = de * (stored q) * ln 2
-#pragma unroll
-    for (int e = 0; e < DH; ++e) {
-      atomicAdd(&dKV[(int64_t)tok * 2 * d + j * DH + e], dk[e] * kLn2);
-      atomicAdd(&dKV[(int64_t)tok * 2 * d + d + j * DH + e], dv[e]);
+    if (on) {
+      store_row<OT>(dKV + (int64_t)tok * 2 * d + j * DH, dk, DH, kLn2);
+      store_row<OT>(dKV + (int64_t)tok * 2 * d + d + j * DH, dv, DH, 1.f);
     }
   }
 }
@@ -299,7 +369,7 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(
     const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const float* __restrict__ Q,
     const float* __restrict__ KV, int d, const float* __restrict__ a, const float* __restrict__ da,
     const float* __restrict__ lse, float* __restrict__ dq_part, int64_t n_tgt, int n_heads) {
-  __shared__ float kt[kTile][DH + 1], vt[kTile][DH + 1];
+  __shared__ __attribute__((aligned(16))) KvTile<DH> T;
   __shared__ float red[4][64][DH];
   const int u = blockIdx.x;
   if (u >= hdr->n_units) return;
@@ -323,19 +393,14 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(
   const int lo = max(un.b0 * kBlockTokens, un.l0), hi = min(un.b1 * kBlockTokens, un.l1);
   for (int base = lo; base < hi; base += kTile) {
     __syncthreads();
-    stage_kv_tile<DH>(kt, vt, KV, d, j, base, lo, hi);
+    stage_kv_tile<DH>(T, KV, d, j, base, lo, hi);
     __syncthreads();
     for (int r = w * 16 + st; r < w * 16 + 16; r += S) {
       if (base + r >= hi) break;
-      float sc = 0.f, dp = 0.f;
-#pragma unroll
-      for (int e = 0; e < DH; ++e) {
-        sc = fmaf(q[e], kt[r][e], sc);
-        dp = fmaf(dat[e], vt[r][e], dp);
-      }
+      const float sc = dot_row<DH>(q, T.k[r]);
+      const float dp = dot_row<DH>(dat, T.v[r]);
       const float de = live ? exp2f(sc - ls) * (dp - D) : 0.f;
-#pragma unroll
-      for (int e = 0; e < DH; ++e) dq[e] = fmaf(de, kt[r][e], dq[e]);
+      axpby_row<DH>(dq, 1.f, de, T.k[r]);
     }
   }
   for (int o = TP; o < 64; o <<= 1)
@@ -445,15 +510,19 @@ hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* 
 }
 
 hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
-                            const WsHeader* hdr, const float* Q, const float* KV, int d, const float* a,
-                            const float* da, const float* lse, float* dq_part, float* dKV, int64_t n_tgt,
-                            hipStream_t st) {
+                            const WsHeader* hdr, const int32_t* toff, const float* Q, const float* KV, int d,
+                            const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
+                            int dkv_bf16, int64_t n_tgt, hipStream_t st) {
   if (max_units == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(max_units), n_heads);
-#define STCA_ATTB(DH)                                                                                     \
-  hipLaunchKernelGGL(attn_bwd_kv_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, dKV,    \
-                     n_heads);                                                                            \
-  hipLaunchKernelGGL(attn_bwd_q_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, dq_part, \
+#define STCA_ATTB(DH)                                                                                      \
+  if (dkv_bf16)                                                                                            \
+    hipLaunchKernelGGL((attn_bwd_kv_kernel<DH, bf16_bits>), g, dim3(256), 0, st, units, hdr, toff, Q, KV, d, a, \
+                       da, lse, static_cast<bf16_bits*>(dKV), n_heads);                                     \
+  else                                                                                                     \
+    hipLaunchKernelGGL((attn_bwd_kv_kernel<DH, float>), g, dim3(256), 0, st, units, hdr, toff, Q, KV, d, a, da, \
+                       lse, static_cast<float*>(dKV), n_heads);                                             \
+  hipLaunchKernelGGL(attn_bwd_q_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, dq_part,  \
                      n_tgt, n_heads)
   switch (d_head) {
     case 8: STCA_ATTB(8); break;

@@ -20,13 +20,17 @@ hipError_t gemm_generic(int a_bf16, int b_bf16, int M, int N, int K, const void*
                         int transA, const void* B, int64_t ldb, int transB, float* C, int64_t ldc,
                         float alpha, GemmEpi epi, const float* R, int64_t ldr, float* C2,
                         int accumulate, hipStream_t st);
-// MFMA GEMM with bf16 operands (fp32 operands rounded to bf16 when staged)
-// and fp32 accumulation/output; same operand conventions as gemm_generic
-// (kEpiStore only, optional accumulate).  For the backward's history-side
-// products on bf16 inputs.
-hipError_t gemm_mfma(int a_bf16, int b_bf16, int M, int N, int K, const void* A, int64_t lda, int transA,
-                     const void* B, int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate,
-                     hipStream_t st);
+// MFMA GEMM, bf16 operands, fp32 accumulation and output:
+// C = alpha op(A) op(B) (+ C when accumulating), operand conventions as in
+// gemm_generic.  The contiguous extent of each operand (K for A untransposed
+// and for B transposed, else M / N) and lda, ldb must be multiples of 8, A
+// and B 16-byte aligned (hipErrorInvalidValue otherwise).  Long-K products
+// with few output tiles split K when `part` holds splits * M * N floats
+// (gemm_mfma_part_floats gives the most any split asks for).
+int64_t gemm_mfma_part_floats(int M, int N, int K);
+hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
+                     int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
+                     int64_t part_floats, hipStream_t st);
 hipError_t attn_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
                         const WsHeader* hdr, const float* Q, const float* KV, int d,
                         float* part_acc, float* part_ml, int64_t n_tgt, hipStream_t st);
@@ -36,10 +40,13 @@ hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* 
 hipError_t convert(int src_bf16, int dst_bf16, const void* src, void* dst, int64_t n, hipStream_t st);
 hipError_t fill_f32(float* dst, float v, int64_t n, hipStream_t st);
 // generic backward pieces
+// dKV ([N_hist][2d], fp32 or bf16 when dkv_bf16) is written for every history
+// row of a request with targets; rows of requests without targets are left
+// untouched.
 hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
-                            const WsHeader* hdr, const float* Q, const float* KV, int d,
-                            const float* a, const float* da, const float* lse, float* dq_part,
-                            float* dKV, int64_t n_tgt, hipStream_t st);
+                            const WsHeader* hdr, const int32_t* toff, const float* Q, const float* KV, int d,
+                            const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
+                            int dkv_bf16, int64_t n_tgt, hipStream_t st);
 hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const float* part, float* out,
                          float scale, hipStream_t st);
 hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st);
