@@ -114,7 +114,8 @@ struct Layout {
   size_t kv32, q32, abuf, ubuf, hid;
   // backward (generic)
   size_t pre, dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
-  int64_t gpart_floats;
+  size_t xt, dkvt, wkvt;
+  int64_t gpart_floats, nh8;
   size_t total;
 };
 
@@ -174,10 +175,17 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     const bool bf = dims->dtype == STCA_BF16;
     L->kvs = m.take(4 * n * nh * 2 * d);  // every layer's K | V rows, fp32
     L->dkv = m.take((bf ? 2 : 4) * nh * 2 * d);
-    L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;  // [W_K | W_V] per layer
+    // bf16 history-side products: [W_K | W_V] per layer and its transpose,
+    // X^T and (dK | dV)^T with the history rows padded to a multiple of 8
+    L->nh8 = round_up(static_cast<int64_t>(nh), 8);
+    const size_t nh8 = static_cast<size_t>(L->nh8);
+    L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;
+    L->wkvt = bf ? m.take(2 * n * d * 2 * d) : 0;
+    L->xt = bf ? m.take(2 * d * nh8) : 0;
+    L->dkvt = bf ? m.take(2 * 2 * d * nh8) : 0;
     L->dwkv = bf ? m.take(4 * d * 2 * d) : 0;
     L->gpart_floats = bf ? gemm_mfma_part_floats(static_cast<int>(d), static_cast<int>(2 * d),
-                                                  static_cast<int>(nh)) : 0;
+                                                  static_cast<int>(nh8)) : 0;
     L->gpart = bf ? m.take(4 * L->gpart_floats) : 0;
     L->rq = m.take(4 * n * nt * d);  // per-layer queries, attention outputs, lse
     L->ra = m.take(4 * n * nt * d);
@@ -424,6 +432,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   auto RL = [&](int i) { return per_layer(L.rl, i, nt * h); };
   auto KVS = [&](int i) { return per_layer(L.kvs, i, nh * 2 * d); };
   auto WKV = [&](int i) { return at<bf16_bits>(ws, L.wkv) + (size_t)i * d * 2 * d; };
+  auto WKVT = [&](int i) { return at<bf16_bits>(ws, L.wkvt) + (size_t)i * d * 2 * d; };
+  bf16_bits* xt = bf ? at<bf16_bits>(ws, L.xt) : nullptr;
+  bf16_bits* dkvt = bf ? at<bf16_bits>(ws, L.dkvt) : nullptr;
+  const int nh8 = static_cast<int>(L.nh8);
   auto gemm = [&](int a_bf, int b_bf, int M, int N, int K, const void* A, int64_t lda, int tA, const void* B,
                   int64_t ldb, int tB, float* C, int64_t ldc, float alpha, GemmEpi epi, const float* R,
                   int64_t ldr, float* C2) {
@@ -432,14 +444,19 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   const float qscale = kLog2e / std::sqrt(static_cast<float>(L.dh));
   // History-side products (rows = history items) on bf16 inputs run on the
   // MFMA GEMM with [W_K | W_V] packed side by side, so K and V of a layer come
-  // from one product; fp32 inputs keep fp32 arithmetic (SIMT GEMM).
+  // from one product, and every operand arranged with k contiguous (copies
+  // of X^T, [W_K | W_V]^T and (dK | dV)^T); fp32 inputs keep fp32 products.
   if (bf) {
+    const bf16_bits* X = static_cast<const bf16_bits*>(hist);
     for (int i = 0; i < n; ++i) {
-      HIPCHK(hipMemcpy2DAsync(WKV(i), 2 * d * 2, W(w->wk, i, (size_t)d * d), d * 2, d * 2, d,
-                              hipMemcpyDeviceToDevice, st));
-      HIPCHK(hipMemcpy2DAsync(WKV(i) + d, 2 * d * 2, W(w->wv, i, (size_t)d * d), d * 2, d * 2, d,
-                              hipMemcpyDeviceToDevice, st));
+      const bf16_bits* Wk = reinterpret_cast<const bf16_bits*>(W(w->wk, i, (size_t)d * d));
+      const bf16_bits* Wv = reinterpret_cast<const bf16_bits*>(W(w->wv, i, (size_t)d * d));
+      HIPCHK(hipMemcpy2DAsync(WKV(i), 2 * d * 2, Wk, d * 2, d * 2, d, hipMemcpyDeviceToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(WKV(i) + d, 2 * d * 2, Wv, d * 2, d * 2, d, hipMemcpyDeviceToDevice, st));
+      HIPCHK(transpose_bf16(Wk, d, d, d, WKVT(i), d, d, st));
+      HIPCHK(transpose_bf16(Wv, d, d, d, WKVT(i) + (size_t)d * d, d, d, st));
     }
+    HIPCHK(transpose_bf16(X, d, static_cast<int>(nh), d, xt, nh8, nh8, st));
   }
   // forward recomputation in fp32: s^(i), u^(i), and per layer K|V, the
   // scaled queries, the attention output and its lse
@@ -447,8 +464,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   for (int i = 0; i < n; ++i) {
     float* kv = KVS(i);
     if (bf) {
-      HIPCHK(gemm_mfma(static_cast<int>(nh), 2 * d, d, static_cast<const bf16_bits*>(hist), d, 0, WKV(i), 2 * d,
-                       0, kv, 2 * d, 1.f, 0, nullptr, 0, st));
+      HIPCHK(gemm_mfma(static_cast<int>(nh), 2 * d, d, static_cast<const bf16_bits*>(hist), d, 0, WKVT(i), d, 1,
+                       kv, 2 * d, 1.f, 0, nullptr, 0, st));
     } else {
       HIPCHK(gemm(0, 0, nh, d, d, hist, d, 0, W(w->wk, i, (size_t)d * d), d, 0, kv, 2 * d, 1.f, kEpiStore,
                   nullptr, 0, nullptr));
@@ -471,6 +488,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
   // rows of requests without targets keep a zero gradient
   HIPCHK(fill_f32(static_cast<float*>(dkv), 0.f, nh * 2 * d * static_cast<int64_t>(es) / 4, st));
+  if (bf) HIPCHK(fill_f32(reinterpret_cast<float*>(dkvt), 0.f, (int64_t)2 * d * nh8 / 2, st));
   if (!bf) HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
   for (int i = n - 1; i >= 0; --i) {
     const float* s = RS(i);
@@ -497,7 +515,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     // attention (softmax weights rebuilt from the same q, K, V and lse that
     // gave a, so rowsum(dA * A) matches them)
     HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, b->tgt_off, RQ(i), kv, d, a, da, RL(i), dqp, dkv, bf,
-                            nt, st));
+                            dkvt, nh8, nt, st));
     HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
     // q = s Wq
     HIPCHK(gemm(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
@@ -505,11 +523,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     HIPCHK(gemm(0, bf, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr));
     // [K | V] = X [W_K | W_V]
     if (bf) {
-      const bf16_bits* X = static_cast<const bf16_bits*>(hist);
       const bf16_bits* dKV = static_cast<const bf16_bits*>(dkv);
       float* dwkv = at<float>(ws, L.dwkv);
-      HIPCHK(gemm_mfma(d, 2 * d, static_cast<int>(nh), X, d, 1, dKV, 2 * d, 0, dwkv, 2 * d, 1.f, 0,
-                       at<float>(ws, L.gpart), L.gpart_floats, st));
+      HIPCHK(gemm_mfma(d, 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, 2 * d, 1.f, 0, at<float>(ws, L.gpart),
+                       L.gpart_floats, st));
       HIPCHK(hipMemcpy2DAsync(dw->dwk + (size_t)i * d * d, d * 4, dwkv, 2 * d * 4, d * 4, d,
                               hipMemcpyDeviceToDevice, st));
       HIPCHK(hipMemcpy2DAsync(dw->dwv + (size_t)i * d * d, d * 4, dwkv + d, 2 * d * 4, d * 4, d,

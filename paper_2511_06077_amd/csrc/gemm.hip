@@ -9,10 +9,12 @@
 // 128 x 128 output tile per workgroup of four waves (2 x 2), each wave 64 x 64
 // as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  64-deep k tiles go global ->
 // registers (16-byte loads, the next tile's loads in flight while the current
-// one is multiplied) -> LDS (double-buffered, rows with k contiguous and
-// padded by 16 bytes) -> MFMA operands (16-byte LDS reads).  An operand whose
-// source has k contiguous is copied row by row; one whose source has the row
-// index contiguous is transposed on its way into LDS.  Tiles are handed to the
+// one is multiplied) -> LDS (rows with k contiguous, padded by 16 bytes; one
+// buffer, 37 KB, so four workgroups share a CU) -> MFMA operands (16-byte LDS
+// reads).  An operand whose source has k contiguous is copied row by row (the
+// form every product above is arranged in, with transposed copies of X, of the
+// weights and of dK|dV); one whose source has the row index contiguous is
+// transposed on its way into LDS.  Tiles are handed to the
 // eight XCDs in contiguous ranges, so the tiles that share a row block of A
 // (and, split over K, every tile of one K range) run on one XCD and share its
 // L2.  A split over K writes per-split partial tiles that a second kernel sums.
@@ -85,8 +87,8 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
                                                         float* __restrict__ C, int64_t ldc, float alpha,
                                                         int accumulate, int k_chunk, int n_tiles_m, int n_tiles_n,
                                                         int n_work, float* __restrict__ part) {
-  __shared__ __attribute__((aligned(16))) bf16_bits As[2][BM * LROW];
-  __shared__ __attribute__((aligned(16))) bf16_bits Bs[2][BN * LROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits As[BM * LROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits Bs[BN * LROW];
   // contiguous range of work items per XCD (workgroups are dealt to XCDs
   // round robin by their linear index)
   const int lid = blockIdx.x;
@@ -106,18 +108,17 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
   u16x8 ra[4], rb[4];
   load_tile<A_KC>(ra, A, lda, m0, M, kb, ke);
   load_tile<B_KC>(rb, B, ldb, n0, N, kb, ke);
-  store_tile<A_KC>(As[0], ra);
-  store_tile<B_KC>(Bs[0], rb);
+  store_tile<A_KC>(As, ra);
+  store_tile<B_KC>(Bs, rb);
   __syncthreads();
-  int cur = 0;
   for (int k0 = kb; k0 < ke; k0 += BK) {
     const bool more = k0 + BK < ke;
     if (more) {
       load_tile<A_KC>(ra, A, lda, m0, M, k0 + BK, ke);
       load_tile<B_KC>(rb, B, ldb, n0, N, k0 + BK, ke);
     }
-    const bf16_bits* as = As[cur];
-    const bf16_bits* bs = Bs[cur];
+    const bf16_bits* as = As;
+    const bf16_bits* bs = Bs;
 #pragma unroll
     for (int ks = 0; ks < BK / 16; ++ks) {
       bf16x8 a[2], b[2];
@@ -131,12 +132,12 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
 #pragma unroll
         for (int j = 0; j < 2; ++j) acc[i][j] = mfma_bf(a[i], b[j], acc[i][j]);
     }
+    __syncthreads();
     if (more) {
-      store_tile<A_KC>(As[cur ^ 1], ra);
-      store_tile<B_KC>(Bs[cur ^ 1], rb);
+      store_tile<A_KC>(As, ra);
+      store_tile<B_KC>(Bs, rb);
     }
     __syncthreads();
-    cur ^= 1;
   }
   // result lane layout: column n = lane % 32, rows 8 (v / 4) + 4 hi + v % 4
   float* out = part ? part + (int64_t)split * M * N : C;
@@ -172,7 +173,33 @@ __global__ void split_sum_kernel(const float* __restrict__ part, int splits, int
 
 bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// dst[c * ldd + r] = src[r * lds + c] for r < R, c < C; dst columns r in
+// [R, Rp) are zeroed.  64 x 64 tiles through LDS.
+__global__ __launch_bounds__(256) void transpose_kernel(const bf16_bits* __restrict__ src, int64_t lds, int R, int C,
+                                                        bf16_bits* __restrict__ dst, int64_t ldd, int Rp) {
+  __shared__ bf16_bits t[64][65];
+  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int rr = e / 64, cc = e % 64;
+    t[rr][cc] = (r0 + rr < R && c0 + cc < C) ? src[(int64_t)(r0 + rr) * lds + c0 + cc] : bf16_bits(0);
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int cc = e / 64, rr = e % 64;
+    if (c0 + cc < C && r0 + rr < Rp) dst[(int64_t)(c0 + cc) * ldd + r0 + rr] = t[rr][cc];
+  }
+}
+
 }  // namespace
+
+hipError_t transpose_bf16(const bf16_bits* src, int64_t lds, int R, int C, bf16_bits* dst, int64_t ldd, int Rp,
+                          hipStream_t st) {
+  if (Rp == 0 || C == 0) return hipSuccess;
+  hipLaunchKernelGGL(transpose_kernel, dim3(static_cast<unsigned>(ceil_div(Rp, 64)),
+                                            static_cast<unsigned>(ceil_div(C, 64))),
+                     dim3(256), 0, st, src, lds, R, C, dst, ldd, Rp);
+  return hipGetLastError();
+}
 
 int64_t gemm_mfma_part_floats(int M, int N, int K) {
   const int64_t tiles = ceil_div(M, BM) * ceil_div(N, BN);

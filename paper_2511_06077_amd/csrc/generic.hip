@@ -17,8 +17,13 @@ __device__ __forceinline__ float ld(const T* p, int64_t i) {
 }
 
 // ---------------------------------------------------------------- GEMM
+// fp32 products (operands fp32 or bf16, widened exactly) on the fp32 MFMA,
+// v_mfma_f32_32x32x2_f32: 64 x 64 output tile per workgroup of four waves,
+// each wave a 32 x 32 quarter; 32-deep k tiles staged in LDS as [k][m] and
+// [k][n], the next tile's global loads in flight during the current tile's
+// MFMAs.
 constexpr int GT = 64;  // output tile edge
-constexpr int GK = 16;  // k step
+constexpr int GK = 32;  // k step
 
 template <typename TA, typename TB>
 __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA* __restrict__ A,
@@ -27,65 +32,79 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA
                                                    int64_t ldc, float alpha, int epi,
                                                    const float* __restrict__ R, int64_t ldr,
                                                    float* __restrict__ C2, int accumulate, int k_chunk) {
-  __shared__ float As[GK][GT + 4];
-  __shared__ float Bs[GK][GT + 4];
-  const int tx = threadIdx.x % 16, ty = threadIdx.x / 16;
+  __shared__ float As[GK][GT + 1];
+  __shared__ float Bs[GK][GT + 1];
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int wm = (wave / 2) * 32, wn = (wave % 2) * 32;
+  const int r32 = lane % 32, hi = lane / 32;
   const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
-  float acc[4][4] = {};
+  f32x16 acc = {};
   // split-K: workgroup z sums k in [z * k_chunk, (z + 1) * k_chunk) and adds
   // its partial into C atomically (C was cleared or holds what to add to)
   const int kb = blockIdx.z * k_chunk;
   const int ke = min(K, kb + k_chunk);
+  constexpr int PER = GT * GK / 256;
+  float ra[PER], rb[PER];
+  // Consecutive threads walk each source's contiguous index, so global reads
+  // coalesce.
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      const int mm = transA ? e % GT : e / GK, kk = transA ? e / GT : e % GK;
+      const int gm = m0 + mm, gk = k0 + kk;
+      ra[i] = (gm < M && gk < ke) ? (transA ? ld(A, (int64_t)gk * lda + gm) : ld(A, (int64_t)gm * lda + gk)) : 0.f;
+      const int nn = transB ? e / GK : e % GT, kb2 = transB ? e % GK : e / GT;
+      const int gn = n0 + nn, gk2 = k0 + kb2;
+      rb[i] = (gn < N && gk2 < ke) ? (transB ? ld(B, (int64_t)gn * ldb + gk2) : ld(B, (int64_t)gk2 * ldb + gn))
+                                   : 0.f;
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int e = threadIdx.x + 256 * i;
+      const int mm = transA ? e % GT : e / GK, kk = transA ? e / GT : e % GK;
+      As[kk][mm] = ra[i];
+      const int nn = transB ? e / GK : e % GT, kb2 = transB ? e % GK : e / GT;
+      Bs[kb2][nn] = rb[i];
+    }
+  };
+  load(kb);
+  store();
+  __syncthreads();
   for (int k0 = kb; k0 < ke; k0 += GK) {
-    for (int e = threadIdx.x; e < GT * GK; e += 256) {
-      // A tile: rows m0..m0+63, cols k0..k0+15, stored As[k][m]
-      int mm = e % GT, kk = e / GT;
-      int gm = m0 + mm, gk = k0 + kk;
-      float v = 0.f;
-      if (gm < M && gk < ke) v = transA ? ld(A, (int64_t)gk * lda + gm) : ld(A, (int64_t)gm * lda + gk);
-      As[kk][mm] = v;
-      int nn = e % GT;
-      int gn = n0 + nn;
-      float w = 0.f;
-      if (gn < N && gk < ke) w = transB ? ld(B, (int64_t)gn * ldb + gk) : ld(B, (int64_t)gk * ldb + gn);
-      Bs[kk][nn] = w;
-    }
+    const bool more = k0 + GK < ke;
+    if (more) load(k0 + GK);
+    // operand lane l holds A[m = l % 32][k = l / 32] and B[k = l / 32][n = l % 32]
+#pragma unroll
+    for (int kk = 0; kk < GK; kk += 2)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(As[kk + hi][wm + r32], Bs[kk + hi][wn + r32], acc, 0, 0, 0);
     __syncthreads();
-#pragma unroll
-    for (int kk = 0; kk < GK; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    if (more) {
+      store();
+      __syncthreads();
     }
-    __syncthreads();
   }
+  // result lane layout: column n = lane % 32, rows 8 (v / 4) + 4 hi + v % 4
+  const int gn = n0 + wn + r32;
+  if (gn >= N) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int gm = m0 + ty * 4 + i;
+  for (int v = 0; v < 16; ++v) {
+    const int gm = m0 + wm + 8 * (v / 4) + 4 * hi + (v % 4);
     if (gm >= M) continue;
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int gn = n0 + tx * 4 + j;
-      if (gn >= N) continue;
-      float v = alpha * acc[i][j];
-      float* c = C + (int64_t)gm * ldc + gn;
-      if (gridDim.z > 1) {
-        atomicAdd(c, v);
-        continue;
-      }
-      if (epi == kEpiAddRes) v += R[(int64_t)gm * ldr + gn];
-      if (epi == kEpiRelu) {
-        if (C2) C2[(int64_t)gm * ldc + gn] = v;
-        v = fmaxf(v, 0.f);
-      }
-      *c = accumulate ? *c + v : v;
+    float x = alpha * acc[v];
+    float* c = C + (int64_t)gm * ldc + gn;
+    if (gridDim.z > 1) {
+      atomicAdd(c, x);
+      continue;
     }
+    if (epi == kEpiAddRes) x += R[(int64_t)gm * ldr + gn];
+    if (epi == kEpiRelu) {
+      if (C2) C2[(int64_t)gm * ldc + gn] = x;
+      x = fmaxf(x, 0.f);
+    }
+    *c = accumulate ? *c + x : x;
   }
 }
 
@@ -295,7 +314,8 @@ template <int DH, typename OT>
 __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(
     const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const int32_t* __restrict__ toff,
     const float* __restrict__ Q, const float* __restrict__ KV, int d, const float* __restrict__ a,
-    const float* __restrict__ da, const float* __restrict__ lse, OT* __restrict__ dKV, int n_heads) {
+    const float* __restrict__ da, const float* __restrict__ lse, OT* __restrict__ dKV,
+    bf16_bits* __restrict__ dKVT, int64_t ldt, int n_heads) {
   __shared__ __attribute__((aligned(16))) float qs[kTargetGroup][DH];
   __shared__ __attribute__((aligned(16))) float das[kTargetGroup][DH];
   __shared__ float cs[kTargetGroup][2];
@@ -360,6 +380,13 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(
     if (on) {
       store_row<OT>(dKV + (int64_t)tok * 2 * d + j * DH, dk, DH, kLn2);
       store_row<OT>(dKV + (int64_t)tok * 2 * d + d + j * DH, dv, DH, 1.f);
+      if (dKVT) {  // transposed copy: consecutive lanes write consecutive rows
+#pragma unroll
+        for (int e = 0; e < DH; ++e) {
+          dKVT[(int64_t)(j * DH + e) * ldt + tok] = from_f32<bf16_bits>(dk[e] * kLn2);
+          dKVT[(int64_t)(d + j * DH + e) * ldt + tok] = from_f32<bf16_bits>(dv[e]);
+        }
+      }
     }
   }
 }
@@ -462,8 +489,8 @@ hipError_t gemm_generic(int a_bf16, int b_bf16, int M, int N, int K, const void*
   // long reductions (weight gradients over all rows) with few output tiles are
   // split over K so the whole chip works on them and each partial sum is short
   int splits = 1;
-  if (epi == kEpiStore && tiles < 256 && K >= 4096) {
-    splits = static_cast<int>(std::min<int64_t>(ceil_div(1024, tiles), K / 1024));
+  if (epi == kEpiStore && tiles < 256 && K >= 1024) {
+    splits = static_cast<int>(std::min<int64_t>(ceil_div(512, tiles), K / 512));
     if (splits < 1) splits = 1;
   }
   const int k_chunk = static_cast<int>(round_up(ceil_div(K, splits), GK));
@@ -512,16 +539,16 @@ hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* 
 hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
                             const WsHeader* hdr, const int32_t* toff, const float* Q, const float* KV, int d,
                             const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
-                            int dkv_bf16, int64_t n_tgt, hipStream_t st) {
+                            int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt, hipStream_t st) {
   if (max_units == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(max_units), n_heads);
 #define STCA_ATTB(DH)                                                                                      \
   if (dkv_bf16)                                                                                            \
     hipLaunchKernelGGL((attn_bwd_kv_kernel<DH, bf16_bits>), g, dim3(256), 0, st, units, hdr, toff, Q, KV, d, a, \
-                       da, lse, static_cast<bf16_bits*>(dKV), n_heads);                                     \
+                       da, lse, static_cast<bf16_bits*>(dKV), dKVT, ldt, n_heads);                          \
   else                                                                                                     \
     hipLaunchKernelGGL((attn_bwd_kv_kernel<DH, float>), g, dim3(256), 0, st, units, hdr, toff, Q, KV, d, a, da, \
-                       lse, static_cast<float*>(dKV), n_heads);                                             \
+                       lse, static_cast<float*>(dKV), nullptr, 0, n_heads);                                 \
   hipLaunchKernelGGL(attn_bwd_q_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, dq_part,  \
                      n_tgt, n_heads)
   switch (d_head) {

@@ -31,6 +31,10 @@ int64_t gemm_mfma_part_floats(int M, int N, int K);
 hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
                      int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
                      int64_t part_floats, hipStream_t st);
+// dst[c][r] = src[r][c] (bf16; R x C source, row pitches lds / ldd); dst
+// columns R..Rp-1 are zeroed.
+hipError_t transpose_bf16(const bf16_bits* src, int64_t lds, int R, int C, bf16_bits* dst, int64_t ldd, int Rp,
+                          hipStream_t st);
 hipError_t attn_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
                         const WsHeader* hdr, const float* Q, const float* KV, int d,
                         float* part_acc, float* part_ml, int64_t n_tgt, hipStream_t st);
@@ -41,12 +45,13 @@ hipError_t convert(int src_bf16, int dst_bf16, const void* src, void* dst, int64
 hipError_t fill_f32(float* dst, float v, int64_t n, hipStream_t st);
 // generic backward pieces
 // dKV ([N_hist][2d], fp32 or bf16 when dkv_bf16) is written for every history
-// row of a request with targets; rows of requests without targets are left
+// row of a request with targets, and with bf16 also its transpose dKVT
+// ([2d][ldt]) when dKVT is not null; rows of requests without targets are left
 // untouched.
 hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
                             const WsHeader* hdr, const int32_t* toff, const float* Q, const float* KV, int d,
                             const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
-                            int dkv_bf16, int64_t n_tgt, hipStream_t st);
+                            int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt, hipStream_t st);
 hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const float* part, float* out,
                          float scale, hipStream_t st);
 hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st);
