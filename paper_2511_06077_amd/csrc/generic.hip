@@ -513,6 +513,8 @@ hipError_t attn_generic(int d_head, int n_heads, const Unit* units, int64_t max_
                         const float* Q, const float* KV, int d, float* part_acc, float* part_ml,
                         int64_t n_tgt, hipStream_t st) {
   if (max_units == 0) return hipSuccess;
+  if (attn_mfma_supported(d_head))
+    return attn_fwd_mfma(d_head, n_heads, units, max_units, hdr, Q, KV, d, part_acc, part_ml, n_tgt, st);
   dim3 g(static_cast<unsigned>(max_units), n_heads);
 #define STCA_ATT(DH)                                                                                    \
   hipLaunchKernelGGL(attn_generic_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, part_acc, part_ml, \
@@ -541,6 +543,9 @@ hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t 
                             const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
                             int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt, hipStream_t st) {
   if (max_units == 0) return hipSuccess;
+  if (attn_mfma_supported(d_head))
+    return attn_bwd_mfma(d_head, n_heads, units, max_units, hdr, toff, Q, KV, d, a, da, lse, dq_part, dKV, dkv_bf16,
+                         dKVT, ldt, n_tgt, st);
   dim3 g(static_cast<unsigned>(max_units), n_heads);
 #define STCA_ATTB(DH)                                                                                      \
   if (dkv_bf16)                                                                                            \

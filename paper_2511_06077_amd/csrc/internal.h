@@ -52,6 +52,17 @@ hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t 
                             const WsHeader* hdr, const int32_t* toff, const float* Q, const float* KV, int d,
                             const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
                             int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt, hipStream_t st);
+// Exact fp32 attention on the fp32 matrix cores (attn_mfma.hip) for d_h in
+// {16, 32, 64}: the same outputs as attn_generic / attn_bwd_generic, which
+// dispatch to them.
+bool attn_mfma_supported(int d_head);
+hipError_t attn_fwd_mfma(int d_head, int n_heads, const Unit* units, int64_t max_units, const WsHeader* hdr,
+                         const float* Q, const float* KV, int d, float* part_acc, float* part_ml, int64_t n_tgt,
+                         hipStream_t st);
+hipError_t attn_bwd_mfma(int d_head, int n_heads, const Unit* units, int64_t max_units, const WsHeader* hdr,
+                         const int32_t* toff, const float* Q, const float* KV, int d, const float* a, const float* da,
+                         const float* lse, float* dq_part, void* dKV, int dkv_bf16, bf16_bits* dKVT, int64_t ldt,
+                         int64_t n_tgt, hipStream_t st);
 hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const float* part, float* out,
                          float scale, hipStream_t st);
 hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st);
