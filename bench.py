@@ -243,6 +243,15 @@ def main() -> int:
     roof["traffic"] = measured_traffic(wl.name, dom)
     c = accounting.stage_costs(b.hist_len, b.n_tgt, wl.d_model, wl.n_layers, es)
     roof_ms = sum(max(v["flop"] / (peak_tf * 1e12), v["bytes"] / (PEAK_HBM_GBS * 1e9)) for v in c.values()) * 1e3
+    # the same bound for the fused design, whose only compulsory history
+    # traffic is one read of X per layer (K and V never reach HBM)
+    L = b.hist_len[b.n_tgt > 0].astype(np.float64)
+    m = b.n_tgt[b.n_tgt > 0].astype(np.float64)
+    dm = wl.d_model
+    fused_flop = wl.n_layers * (4.0 * L.sum() * dm * dm + 4.0 * (m * L).sum() * dm)
+    fused_bytes = wl.n_layers * es * L.sum() * dm
+    design_ms = (max(fused_flop / (peak_tf * 1e12), fused_bytes / (PEAK_HBM_GBS * 1e9))
+                 + c["update"]["flop"] / (peak_tf * 1e12)) * 1e3
     value = b.n_tgt_total / (ms_step * 1e-3)
     rec = {
         "metric": "targets scored/sec, STCA forward",
@@ -264,6 +273,8 @@ def main() -> int:
         "roofline": roof,
         "path_roofline": {"ms": roof_ms, "frac": roof_ms / ms_step,
                           "targets_per_s": b.n_tgt_total / (roof_ms * 1e-3)},
+        "fused_design_roofline": {"ms": design_ms, "frac": design_ms / ms_step,
+                                  "targets_per_s": b.n_tgt_total / (design_ms * 1e-3)},
         "kernels": kernels,
         "ms_per_step_with_kernel_events": ev_ms,
         "settle_steps": n_settle,
@@ -279,9 +290,36 @@ def main() -> int:
     return 0
 
 
+def backward_phase_work(label: str, b: W.Batch):
+    """Algorithmic (flop, bytes, peak TFLOP/s) of one occurrence of a backward
+    phase (stca_backward_profiled's markers), per layer, as the kernels are
+    designed: history-side products on bf16 operands (bf16 MFMA peak) with
+    fp32 K|V (fp32 attention on the fp32 MFMA, 157.3 TFLOP/s), dK|dV in bf16
+    (row-major and transposed)."""
+    wl = b.wl
+    d, F = wl.d_model, wl.ffn_hidden
+    Ls = float(b.hist_len[b.n_tgt > 0].sum())
+    mL = float((b.n_tgt.astype(np.float64) * b.hist_len).sum())
+    mt = float(b.n_tgt.sum())
+    if label == "kv_gemm":
+        return 4 * Ls * d * d, 2 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
+    if label == "dw_kv":
+        return 4 * Ls * d * d, 2 * Ls * d + 4 * Ls * d, PEAK_BF16_TFLOPS
+    if label == "dx":
+        return 4 * Ls * d * d, 4 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
+    if label == "attn_fwd":
+        return 4 * mL * d, 8 * Ls * d, PEAK_FP32_TFLOPS
+    if label == "attn_bwd":
+        return 10 * mL * d, 8 * Ls * d + 8 * Ls * d, PEAK_FP32_TFLOPS
+    if label == "target_gemm":  # 14 target-side products per layer over 4 markers
+        return 14 * mt * (d * d + d * F) * 2 / 4, 0.0, PEAK_FP32_TFLOPS
+    return 0.0, 0.0, 0.0
+
+
 def train_step(args) -> int:
     """Forward + backward of the training window: one step = stca_forward then
-    stca_backward (all gradients) over the whole batch, inputs resident."""
+    stca_backward (all gradients) over the whole batch, inputs resident.  The
+    backward's phases are then timed with HIP events in a second pass."""
     import torch
     from paper_2511_06077_amd.device import DeviceBatch, to_device
     name = args.workload if args.workload != W.HEADLINE else "train_bf16_R256_m16_L2048_d256"
@@ -296,8 +334,7 @@ def train_step(args) -> int:
 
     settle(step, args.settle_seconds)
     for _ in range(args.warmup):
-        db.forward()
-        db.backward(dout)
+        step()
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
@@ -312,6 +349,35 @@ def train_step(args) -> int:
     fwd = e[0].elapsed_time(e[1]) / args.steps
     bwd = e[1].elapsed_time(e[2]) / args.steps
     ms = fwd + bwd
+    # backward phases, timed on the library's stream
+    g = db.backward(dout)
+    dw = stca.wgrads(g["dwq"], g["dwk"], g["dwv"], g["dwo"], g["dw1"], g["dw2"])
+    nl = stca.stca_backward_launch_count(db.dims, db.batch)
+    per = {}
+    for _ in range(args.steps):
+        ev = stca.HipEvents(nl + 1)
+        stca.stca_backward_profiled(db.dims, db.batch, db.hist, db.tgt, db.weights, dout, g["dhist"], g["dtgt"],
+                                    dw, db.bws, db.bws_bytes, stream.cuda_stream, ev.ev, ev.labels)
+        torch.cuda.synchronize()
+        for k in range(nl):
+            per.setdefault(ev.label(k), []).append(ev.elapsed_ms(k, k + 1))
+        ev.close()
+    phases = {}
+    for lab, v in per.items():
+        occ = len(v) // args.steps
+        t = float(np.mean(v))
+        ent = {"per_step": occ, "ms_each": t, "ms_per_step": t * occ}
+        flop, byts, peak = backward_phase_work(lab, b)
+        if flop:
+            ent.update({"tflops": flop / (t * 1e-3) / 1e12, "gbs": byts / (t * 1e-3) / 1e9,
+                        "mfma_frac": flop / (t * 1e-3) / 1e12 / peak, "hbm_frac": byts / (t * 1e-3) / 1e9 / PEAK_HBM_GBS})
+        phases[lab] = ent
+    dom = max((k for k in phases if backward_phase_work(k, b)[0]), key=lambda k: phases[k]["ms_per_step"])
+    flop, byts, peak = backward_phase_work(dom, b)
+    roof = roofline_entry(dom, phases[dom]["ms_each"], flop, byts, peak)
+    roof["kernel"] = dom
+    bound_ms = sum(max(f / (pk * 1e12), by / (PEAK_HBM_GBS * 1e9)) * phases[k]["per_step"] * 1e3
+                   for k in phases for f, by, pk in [backward_phase_work(k, b)] if f)
     print(json.dumps({
         "metric": "targets trained/sec, STCA forward+backward", "value": b.n_tgt_total / (ms * 1e-3),
         "unit": "targets/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
@@ -319,7 +385,8 @@ def train_step(args) -> int:
         "dtype": "bf16" if wl.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": wl.name, "requests": wl.n_requests, "targets_per_request": wl.n_targets,
                    "hist_len": wl.hist_len, "d_model": wl.d_model, "heads": wl.n_heads, "layers": wl.n_layers},
-        "forward_ms": fwd, "backward_ms": bwd}), flush=True)
+        "forward_ms": fwd, "backward_ms": bwd, "backward_roofline": roof,
+        "backward_phase_bound_ms": bound_ms, "backward_phases": phases}), flush=True)
     return 0
 
 

@@ -168,6 +168,20 @@ stca_status_t stca_forward_profiled(const stca_dims_t* dims, const stca_batch_t*
                                     hipStream_t stream, hipEvent_t* events, int n_events,
                                     const char** labels);
 
+/* Measurement variant of stca_backward: the same work, plus hipEventRecord on
+ * `stream` at phase boundaries.  events[0] is recorded before the first
+ * launch and events[k+1] at the end of phase k; labels (nullable) receive the
+ * phase names ("sched", "prep", "kv_gemm", "attn_fwd", "target_gemm",
+ * "attn_bwd", "dw_kv", "dx", "out").  n_events must be at least
+ * stca_backward_launch_count(dims, batch) + 1; the events are the caller's. */
+int stca_backward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch);
+stca_status_t stca_backward_profiled(const stca_dims_t* dims, const stca_batch_t* batch,
+                                     const void* hist, const void* tgt, const stca_weights_t* w,
+                                     const void* dout, float* dhist, float* dtgt,
+                                     const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
+                                     hipStream_t stream, hipEvent_t* events, int n_events,
+                                     const char** labels);
+
 /* Reads (synchronising on `stream`) the status the device scheduler recorded
  * in `ws` during the last call that used it: STCA_OK or STCA_ERR_INVALID_ARG. */
 stca_status_t stca_device_status(const void* ws, hipStream_t stream);

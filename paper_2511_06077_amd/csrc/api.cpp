@@ -404,15 +404,17 @@ stca_status_t forward_generic(const Layout& L, int bf, const stca_batch_t* b, co
 // fp32 states whatever arithmetic the forward call used.
 stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, const void* hist, const void* tgt,
                                const stca_weights_t* w, const void* dout, float* dhist, float* dtgt,
-                               const stca_wgrads_t* dw, void* ws, hipStream_t st) {
+                               const stca_wgrads_t* dw, void* ws, hipStream_t st, Rec& rec) {
   const int d = L.d, n = L.n, F = L.F, h = L.h;
   const int64_t nt = L.nt, nh = L.nh;
   const size_t es = bf ? 2 : 4;
   WsHeader* hdr = at<WsHeader>(ws, L.hdr);
   Unit* units = at<Unit>(ws, L.units);
   int32_t* tch = at<int32_t>(ws, L.tchunks);
+  HIPCHK(rec.start());
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, units, L.max_units, tch,
                       hdr, st));
+  HIPCHK(rec.mark("sched"));
   void* dkv = at<char>(ws, L.dkv);
   float* hid = at<float>(ws, L.hid);
   float* pre = at<float>(ws, L.pre);
@@ -458,6 +460,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     }
     HIPCHK(transpose_bf16(X, d, static_cast<int>(nh), d, xt, nh8, nh8, st));
   }
+  HIPCHK(rec.mark("prep"));
   // forward recomputation in fp32: s^(i), u^(i), and per layer K|V, the
   // scaled queries, the attention output and its lse
   HIPCHK(convert(bf, 0, tgt, RS(0), nt * d, st));
@@ -472,24 +475,29 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       HIPCHK(gemm(0, 0, nh, d, d, hist, d, 0, W(w->wv, i, (size_t)d * d), d, 0, kv + d, 2 * d, 1.f, kEpiStore,
                   nullptr, 0, nullptr));
     }
+    HIPCHK(rec.mark("kv_gemm"));
     HIPCHK(gemm(0, bf, nt, d, d, RS(i), d, 0, W(w->wq, i, (size_t)d * d), d, 0, RQ(i), d, qscale, kEpiStore,
                 nullptr, 0, nullptr));
+    HIPCHK(rec.mark("target_gemm"));
     HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, RQ(i), kv, d, at<float>(ws, L.part_acc),
                         at<float>(ws, L.part_ml), nt, st));
     HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml), RA(i), RL(i),
                          st));
+    HIPCHK(rec.mark("attn_fwd"));
     HIPCHK(gemm(0, bf, nt, d, d, RA(i), d, 0, W(w->wo, i, (size_t)d * d), d, 0, RU(i), d, 1.f, kEpiAddRes, RS(i),
                 d, nullptr));
     HIPCHK(gemm(0, bf, nt, F, d, RU(i), d, 0, W(w->w1, i, (size_t)d * F), F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0,
                 nullptr));
     HIPCHK(gemm(0, bf, nt, d, F, hid, F, 0, W(w->w2, i, (size_t)d * F), d, 0, RS(i + 1), d, 1.f, kEpiAddRes,
                 RU(i), d, nullptr));
+    HIPCHK(rec.mark("target_gemm"));
   }
   HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
   // rows of requests without targets keep a zero gradient
   HIPCHK(fill_f32(static_cast<float*>(dkv), 0.f, nh * 2 * d * static_cast<int64_t>(es) / 4, st));
   if (bf) HIPCHK(fill_f32(reinterpret_cast<float*>(dkvt), 0.f, (int64_t)2 * d * nh8 / 2, st));
   if (!bf) HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
+  HIPCHK(rec.mark("prep"));
   for (int i = n - 1; i >= 0; --i) {
     const float* s = RS(i);
     const float* u = RU(i);
@@ -512,15 +520,18 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     HIPCHK(gemm(0, 0, d, d, nt, a, d, 1, du, d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
                 nullptr));
     HIPCHK(gemm(0, bf, nt, d, d, du, d, 0, Wo, d, 1, da, d, 1.f, kEpiStore, nullptr, 0, nullptr));
+    HIPCHK(rec.mark("target_gemm"));
     // attention (softmax weights rebuilt from the same q, K, V and lse that
     // gave a, so rowsum(dA * A) matches them)
     HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, b->tgt_off, RQ(i), kv, d, a, da, RL(i), dqp, dkv, bf,
                             dkvt, nh8, nt, st));
     HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
+    HIPCHK(rec.mark("attn_bwd"));
     // q = s Wq
     HIPCHK(gemm(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
                 nullptr));
     HIPCHK(gemm(0, bf, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr));
+    HIPCHK(rec.mark("target_gemm"));
     // [K | V] = X [W_K | W_V]
     if (bf) {
       const bf16_bits* dKV = static_cast<const bf16_bits*>(dkv);
@@ -531,8 +542,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                               hipMemcpyDeviceToDevice, st));
       HIPCHK(hipMemcpy2DAsync(dw->dwv + (size_t)i * d * d, d * 4, dwkv + d, 2 * d * 4, d * 4, d,
                               hipMemcpyDeviceToDevice, st));
+      HIPCHK(rec.mark("dw_kv"));
       HIPCHK(gemm_mfma(static_cast<int>(nh), d, 2 * d, dKV, 2 * d, 0, WKV(i), 2 * d, 1, dhist, d, 1.f,
                        i != n - 1, nullptr, 0, st));
+      HIPCHK(rec.mark("dx"));
     } else {
       const float* dKV = static_cast<const float*>(dkv);
       const void* Wk = W(w->wk, i, (size_t)d * d);
@@ -541,14 +554,17 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                   nullptr, 0, nullptr));
       HIPCHK(gemm(0, 0, d, d, nh, hist, d, 1, dKV + d, 2 * d, 0, dw->dwv + (size_t)i * d * d, d, 1.f, kEpiStore,
                   nullptr, 0, nullptr));
+      HIPCHK(rec.mark("dw_kv"));
       HIPCHK(gemm_generic(0, 0, nh, d, d, dKV, 2 * d, 0, Wk, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0, nullptr, 1,
                           st));
       HIPCHK(gemm_generic(0, 0, nh, d, d, dKV + d, 2 * d, 0, Wv, d, 1, dhist, d, 1.f, kEpiStore, nullptr, 0,
                           nullptr, 1, st));
+      HIPCHK(rec.mark("dx"));
     }
     std::swap(ds, ds2);
   }
   HIPCHK(convert(0, 0, ds, dtgt, nt * d, st));
+  HIPCHK(rec.mark("out"));
   return STCA_OK;
 }
 
@@ -641,7 +657,38 @@ stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch, 
   Layout L;
   make_layout(dims, batch, 1, true, &L);
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
-  return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, dout, dhist, dtgt, dw, ws, stream);
+  Rec none;
+  return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, dout, dhist, dtgt, dw, ws, stream, none);
+}
+
+int stca_backward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
+  Layout L;
+  if (!make_layout(dims, batch, 1, true, &L)) return -1;
+  return 4 + 9 * L.n;
+}
+
+stca_status_t stca_backward_profiled(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist,
+                                     const void* tgt, const stca_weights_t* w, const void* dout, float* dhist,
+                                     float* dtgt, const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
+                                     hipStream_t stream, hipEvent_t* events, int n_events, const char** labels) {
+  if (!events || n_events < stca_backward_launch_count(dims, batch) + 1) return STCA_ERR_INVALID_ARG;
+  stca_status_t st = check_common(dims, batch, hist, tgt, w, ws);
+  if (st != STCA_OK) return st;
+  if (!dw || (batch->n_tgt > 0 && (!dout || !dtgt)) || (batch->n_hist > 0 && !dhist))
+    return STCA_ERR_INVALID_ARG;
+  if (!dw->dwq || !dw->dwk || !dw->dwv || !dw->dwo || !dw->dw1 || !dw->dw2) return STCA_ERR_INVALID_ARG;
+  const void* ptrs[] = {dout, dhist, dtgt, dw->dwq, dw->dwk, dw->dwv, dw->dwo, dw->dw1, dw->dw2};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
+  Layout L;
+  make_layout(dims, batch, 1, true, &L);
+  if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
+  Rec rec;
+  rec.ev = events;
+  rec.n = n_events;
+  rec.labels = labels;
+  rec.st = stream;
+  return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, dout, dhist, dtgt, dw, ws, stream, rec);
 }
 
 stca_status_t stca_device_status(const void* ws, hipStream_t stream) {

@@ -18,7 +18,7 @@ STCA_F32, STCA_BF16 = 0, 1
 
 EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca_forward", "stca_backward",
             "stca_device_status", "stca_status_string", "stca_path", "stca_forward_launch_count",
-            "stca_forward_profiled")
+            "stca_forward_profiled", "stca_backward_launch_count", "stca_backward_profiled")
 
 
 class stca_dims_t(ctypes.Structure):
@@ -95,6 +95,13 @@ def lib():
                                             P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                             ctypes.c_size_t, ctypes.c_void_p, P(ctypes.c_void_p), ctypes.c_int,
                                             P(ctypes.c_char_p)]
+        L.stca_backward_launch_count.restype = ctypes.c_int
+        L.stca_backward_launch_count.argtypes = [P(stca_dims_t), P(stca_batch_t)]
+        L.stca_backward_profiled.restype = ctypes.c_int
+        L.stca_backward_profiled.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                             P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                             P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                             P(ctypes.c_void_p), ctypes.c_int, P(ctypes.c_char_p)]
         _lib = L
     return _lib
 
@@ -187,6 +194,21 @@ def stca_forward_profiled(d, b, hist, tgt, w, out, saved, ws, ws_bytes: int, str
                                      len(events), labels)
     if st != STCA_OK:
         raise StcaError(st, "stca_forward_profiled")
+    return st
+
+
+def stca_backward_launch_count(d: stca_dims_t, b: stca_batch_t) -> int:
+    return lib().stca_backward_launch_count(ctypes.byref(d), ctypes.byref(b))
+
+
+def stca_backward_profiled(d, b, hist, tgt, w, dout, dhist, dtgt, dw, ws, ws_bytes: int, stream, events,
+                           labels=None) -> int:
+    """As stca_backward, with events recorded at phase boundaries (see HipEvents)."""
+    st = lib().stca_backward_profiled(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w),
+                                      _ptr(dout), _ptr(dhist), _ptr(dtgt), ctypes.byref(dw), _ptr(ws), int(ws_bytes),
+                                      _ptr(stream), events, len(events), labels)
+    if st != STCA_OK:
+        raise StcaError(st, "stca_backward_profiled")
     return st
 
 
