@@ -93,10 +93,26 @@ bool materialize_kv() {
   return e && std::strcmp(e, "materialize") == 0;
 }
 
-int64_t max_units_for(const stca_batch_t* b, int chunk_blocks) {
+// The bf16 path evaluates attention in the reordered form (scores u . x with
+// u = q W_K^j^T, output (P X) W_V^j; no K/V at all) when every request has
+// at most 32 / H targets, which the host offsets must show; the standard form
+// otherwise.  STCA_ATTN=standard / reordered forces either (reordered still
+// needs host offsets and at most 32 / H targets per request, else standard).
+bool reordered_for(const stca_dims_t* dims, const stca_batch_t* b) {
+  const char* e = std::getenv("STCA_ATTN");
+  if (e && std::strcmp(e, "standard") == 0) return false;
+  if (!b->tgt_off_host) return false;
+  const int cap = 32 / (dims->d_model / dims->n_heads == 32 ? dims->n_heads : 1 << 30);
+  if (cap < 1) return false;
+  for (int r = 0; r < b->n_requests; ++r)
+    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > cap) return false;
+  return true;
+}
+
+int64_t max_units_for(const stca_batch_t* b, int chunk_blocks, int group) {
   if (b->hist_off_host)
-    return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks);
-  return (ceil_div(b->n_tgt, kTargetGroup) + b->n_requests) * kMaxChunks;
+    return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks, group);
+  return (ceil_div(b->n_tgt, group) + b->n_requests) * kMaxChunks;
 }
 
 struct Layout {
@@ -106,10 +122,14 @@ struct Layout {
   int chunk_blocks;
   int64_t max_units;
   bool any_narrow, any_wide;  // requests with 1..32 / 33+ targets (both true without host offsets)
+  bool reord;                 // reordered attention (bf16 path)
+  int group;                  // targets per attention unit
   // common
   size_t hdr, units, tchunks, part_acc, part_ml, state_a, state_b;
   // fast
   size_t qn, wkp, wvp, wop, w1p, w2p, wqp, kv;
+  // reordered
+  size_t un, part_y, a2, ml2, tch2, wvp16;
   // generic forward
   size_t kv32, q32, abuf, ubuf, hid;
   // backward (generic)
@@ -132,7 +152,9 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
   L->nt = b->n_tgt;
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
   L->chunk_blocks = chunk_blocks_for(b, device_cus());
-  L->max_units = max_units_for(b, L->chunk_blocks);
+  L->reord = p == 1 && !with_backward && reordered_for(dims, b);
+  L->group = L->reord ? 32 / L->h : kTargetGroup;
+  L->max_units = max_units_for(b, L->chunk_blocks, L->group);
   L->any_narrow = L->any_wide = true;
   if (b->tgt_off_host) {
     L->any_narrow = L->any_wide = false;
@@ -163,7 +185,16 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->wqp = m.take(2 * n * d * d);
       L->w1p = m.take(2 * n * d * F);
       L->w2p = m.take(2 * n * d * F);
-      L->kv = materialize_kv() ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
+      L->kv = materialize_kv() && !L->reord ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
+      if (L->reord) {
+        const size_t h = L->h;
+        L->un = m.take(2 * nt * h * d);
+        L->part_y = m.take(4 * kMaxChunks * nt * h * d);
+        L->a2 = m.take(4 * nt * d);
+        L->ml2 = m.take(8 * nt * h);
+        L->tch2 = m.take(4 * (nt + 1));
+        L->wvp16 = m.take(2 * n * d * d);
+      }
     } else {
       L->kv32 = m.take(4 * nh * 2 * d);
       L->q32 = m.take(4 * nt * d);
@@ -270,6 +301,69 @@ stca_status_t check_common(const stca_dims_t* dims, const stca_batch_t* b, const
 }
 
 // ---------------------------------------------------------------- forward
+// Reordered form (App. A.2.2): per layer U = Q W_K^j^T, attention over X,
+// merge with W_V^j, then the same target update as the standard form.
+stca_status_t forward_reordered(const Layout& L, const stca_batch_t* b, const void* hist, const void* tgt,
+                                const stca_weights_t* w, void* out, void* saved, const stca_saved_layout_t& SL,
+                                void* ws, hipStream_t st, Rec& rec) {
+  const int d = L.d, n = L.n, F = L.F;
+  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
+  Unit* units = at<Unit>(ws, L.units);
+  int32_t* tch = at<int32_t>(ws, L.tchunks);
+  HIPCHK(fast_pack(w->wv, at<char>(ws, L.wvp16), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wv"));
+  HIPCHK(fast_pack(w->wo, at<char>(ws, L.wop), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wo"));
+  HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wq"));
+  HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, 1, st)); HIPCHK(rec.mark("pack_w1"));
+  HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, 1, st)); HIPCHK(rec.mark("pack_w2"));
+  FastUpdate f{};
+  f.n_layers = n;
+  f.F = F;
+  f.n_tgt = L.nt;
+  f.tgt = tgt;
+  f.tchunks = at<int32_t>(ws, L.tch2);
+  f.part_acc = at<float>(ws, L.a2);
+  f.part_ml = at<char>(ws, L.ml2);
+  f.QN = at<char>(ws, L.qn);
+  f.WoP = at<char>(ws, L.wop);
+  f.W1P = at<char>(ws, L.w1p);
+  f.W2P = at<char>(ws, L.w2p);
+  f.WqP = at<char>(ws, L.wqp);
+  f.out = out;
+  auto state = [&](int i) -> float* {
+    if (saved) return at<float>(saved, SL.s) + (size_t)i * L.nt * d;
+    return at<float>(ws, (i % 2) ? L.state_b : L.state_a);
+  };
+  const size_t wlayer = (size_t)d * d * 2;  // bytes of one layer's bf16 W_K
+  f.mode = 0;
+  f.layer = 0;
+  f.s_out = state(0);
+  HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
+  HIPCHK(fast_reord_qu(d, f.QN, w->wk, at<char>(ws, L.un), L.nt, st)); HIPCHK(rec.mark("reord_u"));
+  for (int i = 0; i < n; ++i) {
+    HIPCHK(fast_reord_attn(d, units, hdr, L.max_units, at<char>(ws, L.un), hist, L.nh, at<float>(ws, L.part_y),
+                           at<char>(ws, L.part_ml), L.nt, st));
+    HIPCHK(rec.mark("reord_attn"));
+    HIPCHK(fast_reord_merge(d, at<float>(ws, L.part_y), at<char>(ws, L.part_ml), tch, at<char>(ws, L.wvp16), i,
+                            at<float>(ws, L.a2), at<char>(ws, L.ml2), at<int32_t>(ws, L.tch2),
+                            saved ? at<float>(saved, SL.lse) + (size_t)i * L.nt * L.h : nullptr, L.nt, st));
+    HIPCHK(rec.mark("reord_merge"));
+    f.mode = 1;
+    f.layer = i;
+    f.s_in = state(i);
+    f.s_out = i + 1 < n ? state(i + 1) : nullptr;
+    f.save_a = saved ? at<float>(saved, SL.a) + (size_t)i * L.nt * d : nullptr;
+    f.save_u = saved ? at<float>(saved, SL.u) + (size_t)i * L.nt * d : nullptr;
+    f.save_lse = nullptr;  // written by the merge
+    HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
+    if (i + 1 < n) {
+      HIPCHK(fast_reord_qu(d, f.QN, static_cast<const char*>(w->wk) + (i + 1) * wlayer, at<char>(ws, L.un), L.nt,
+                           st));
+      HIPCHK(rec.mark("reord_u"));
+    }
+  }
+  return STCA_OK;
+}
+
 stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* hist, const void* tgt,
                            const stca_weights_t* w, void* out, void* saved, const stca_saved_layout_t& SL,
                            void* ws, hipStream_t st, Rec& rec) {
@@ -278,8 +372,9 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   WsHeader* hdr = at<WsHeader>(ws, L.hdr);
   Unit* units = at<Unit>(ws, L.units);
   int32_t* tch = at<int32_t>(ws, L.tchunks);
-  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, units, L.max_units,
+  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, L.group, units, L.max_units,
                       tch, hdr, st)); HIPCHK(rec.mark("sched"));
+  if (L.reord) return forward_reordered(L, b, hist, tgt, w, out, saved, SL, ws, st, rec);
   HIPCHK(fast_pack(w->wk, at<char>(ws, L.wkp), n, d, d, 0, st)); HIPCHK(rec.mark("pack_wk"));
   HIPCHK(fast_pack(w->wv, at<char>(ws, L.wvp), n, d, d, 0, st)); HIPCHK(rec.mark("pack_wv"));
   HIPCHK(fast_pack(w->wo, at<char>(ws, L.wop), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wo"));
@@ -360,7 +455,7 @@ stca_status_t forward_generic(const Layout& L, int bf, const stca_batch_t* b, co
   WsHeader* hdr = at<WsHeader>(ws, L.hdr);
   Unit* units = at<Unit>(ws, L.units);
   int32_t* tch = at<int32_t>(ws, L.tchunks);
-  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, units, L.max_units,
+  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, L.group, units, L.max_units,
                       tch, hdr, st)); HIPCHK(rec.mark("sched"));
   float* kv = at<float>(ws, L.kv32);
   float* q = at<float>(ws, L.q32);
@@ -412,7 +507,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   Unit* units = at<Unit>(ws, L.units);
   int32_t* tch = at<int32_t>(ws, L.tchunks);
   HIPCHK(rec.start());
-  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, units, L.max_units, tch,
+  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, L.group, units, L.max_units, tch,
                       hdr, st));
   HIPCHK(rec.mark("sched"));
   void* dkv = at<char>(ws, L.dkv);
@@ -616,6 +711,7 @@ stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch, c
 int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
   Layout L;
   if (!make_layout(dims, batch, 0, false, &L)) return -1;
+  if (L.path == 1 && L.reord) return 1 + 5 + 1 + 1 + 4 * L.n - 1;
   if (L.path == 1) return materialize_kv() ? 1 + 6 + 1 + 1 + 2 * L.n : 1 + 6 + 1 + 3 * L.n;
   return 1 + 1 + 8 * L.n + 1;
 }

@@ -40,4 +40,18 @@ hipError_t fast_fused(int D, int wide, const Unit* units, const WsHeader* hdr, i
 // K4: combine partials, W_O, residual FFN, next queries.
 hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st);
 
+// Reordered single-query attention (reordered.hip) for units of at most
+// 32 / H targets: U = per-head Q W_K^j^T (fp16 [n_tgt][H][D]), the attention
+// over X writing per-chunk y partials ([16][n_tgt][H][D] fp32 and (max, sum)
+// [16][n_tgt][H]), and the merge that forms a = y W_V^j (fp32 [n_tgt][D]) with
+// single-chunk records (ml_out (0, 1), tch_out 1) for fast_update.
+size_t reord_attn_lds(int D);
+hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, int64_t n_tgt, hipStream_t st);
+hipError_t fast_reord_attn(int D, const Unit* units, const WsHeader* hdr, int64_t max_units, const void* UN,
+                           const void* X, int64_t n_hist, float* part_y, void* part_ml, int64_t n_tgt,
+                           hipStream_t st);
+hipError_t fast_reord_merge(int D, const float* part_y, const void* part_ml, const int32_t* tchunks,
+                            const void* WvP16, int layer, float* a_out, void* ml_out, int32_t* tch_out,
+                            float* save_lse, int64_t n_tgt, hipStream_t st);
+
 }  // namespace stca

@@ -6,10 +6,11 @@
 namespace stca {
 
 // ---- scheduler (sched.hip)
+// `group`: targets per unit (1..kTargetGroup).
 hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
-                        int chunk_blocks, Unit* units, int64_t max_units, int32_t* tchunks,
+                        int chunk_blocks, int group, Unit* units, int64_t max_units, int32_t* tchunks,
                         WsHeader* hdr, hipStream_t st);
-int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks);
+int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks, int group);
 
 // ---- generic fp32-arithmetic path (generic.hip)
 enum GemmEpi { kEpiStore = 0, kEpiAddRes = 1, kEpiRelu = 2 };

@@ -1,0 +1,442 @@
+// Reordered single-query attention under RLB (App. A.2.2, Eq. attn-optimized)
+// for requests with few targets, bf16 storage, d_h = 32.
+//
+// Per target t and head j the score of history row x is
+//   q_tj . (x W_K^j) = (q_tj W_K^j^T) . x = u_tj . x,
+// and the head output is a_tj = (sum_l p_tjl x_l) W_V^j = y_tj W_V^j.  With
+// u_tj formed once per (target, head) on the target side, the history is
+// read as it is: no K or V exists, and a request's work on its history is
+// 4 (m h) L d flop instead of the projection's 4 L d^2 + 4 m L d.  With few
+// targets (m h < d) that is far less, and the pass is bound by one read of X
+// per layer.
+//
+//   reord_qu_kernel:    U[t][j][:] = Q[t][head j] W_K^j^T (fp16, scaled as Q)
+//   reord_attn_kernel:  per unit, rows (t, j) of up to 32: S^T = X U^T,
+//                       online softmax, Y^T += X^T P^T; partial y per chunk
+//   reord_merge_kernel: y_tj = merged partials, a_tj = y_tj W_V^j (fp32),
+//                       handed to the target update as a single chunk
+//
+// MFMA lane layouts are those of v_mfma_f32_32x32x16_f16 (see fast.hip).  X
+// is bf16 in HBM and converted to fp16 in registers (exact for values in
+// fp16's normal range), so every product runs on fp16 operands with fp32
+// accumulation, like the standard path's attention.
+#include "common.h"
+#include "fast.h"
+
+namespace stca {
+
+namespace {
+
+constexpr int DH = 32;
+constexpr float kSlack = 8.f;  // log2 units: softmax weights stay <= 256 between rescales
+constexpr int kWaves = 4;      // X blocks per round of the attention workgroup (two waves each)
+
+// X tile in LDS: the 32 rows in 1 KB segments (512 / D rows each, as one
+// wave's direct global-to-LDS load fills them), segments padded by 16 bytes,
+// which spreads the rows over the banks while keeping every operand address
+// a per-lane base plus a compile-time offset.
+constexpr int kSegPitch = 1024 + 16;
+__host__ __device__ constexpr size_t reord_tile_bytes(int D) { return (size_t)(D / 16) * kSegPitch; }
+// attention kernel LDS: the pairs' double-buffered X tiles (later the merge
+// area), then the unit's U rows
+__host__ __device__ constexpr size_t reord_main_lds(int D) {
+  return (size_t)kWaves * 2 * reord_tile_bytes(D) > (size_t)kWaves * 32 * (D + 2) * 4
+             ? (size_t)kWaves * 2 * reord_tile_bytes(D)
+             : (size_t)kWaves * 32 * (D + 2) * 4;
+}
+
+__device__ __forceinline__ f32x16 mfma16(const f16x8& a, const f16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f16x8 pack8(const f32x16& a, int off) {
+  f16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<_Float16>(a[off + i]);
+  return r;
+}
+
+__device__ __forceinline__ f16x8 zero8() {
+  f16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<_Float16>(0.f);
+  return r;
+}
+
+__device__ __forceinline__ _Float16 bf_to_h(bf16_bits x) { return static_cast<_Float16>(to_f32(x)); }
+
+__device__ __forceinline__ f16x8 bf8_to_h8(const uint4& v) {
+  const bf16_bits* e = reinterpret_cast<const bf16_bits*>(&v);
+  f16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = bf_to_h(e[i]);
+  return r;
+}
+
+// ------------------------------------------------------------------- U
+// One wave per (32 targets, head j).  U^T tile (32 model dims x 32 targets) =
+// W_K^j (dims x head dims) Q_j^T: the B operand is the wave's slice of the
+// permuted QN row (k-step s holds head dims 16 s + 4 hi + {0..3, 8..11}), the A
+// operand W_K[dim][32 j + the same head dims].
+template <int D>
+__global__ __launch_bounds__(64) void reord_qu_kernel(const f16x8* __restrict__ QN, const bf16_bits* __restrict__ Wk,
+                                                      f16x8* __restrict__ UN, int64_t n_tgt) {
+  constexpr int H = D / DH;
+  const int j = blockIdx.y;
+  const int lane = threadIdx.x;
+  const int tcol = lane % 32, hi = lane / 32;
+  const int64_t t = (int64_t)blockIdx.x * 32 + tcol;
+  const bool live = t < n_tgt;
+  f16x8 qb[2];
+#pragma unroll
+  for (int s = 0; s < 2; ++s) qb[s] = live ? QN[(t * D + 32 * j + 16 * s + 8 * hi) / 8] : zero8();
+#pragma unroll
+  for (int dt = 0; dt < D / 32; ++dt) {
+    const int dim = 32 * dt + tcol;
+    f32x16 acc = {};
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const bf16_bits* w = Wk + (int64_t)dim * D + 32 * j + 16 * s + 4 * hi;
+      const ushort4 lo4 = *reinterpret_cast<const ushort4*>(w);
+      const ushort4 hi4 = *reinterpret_cast<const ushort4*>(w + 8);
+      f16x8 a;
+      a[0] = bf_to_h(lo4.x), a[1] = bf_to_h(lo4.y), a[2] = bf_to_h(lo4.z), a[3] = bf_to_h(lo4.w);
+      a[4] = bf_to_h(hi4.x), a[5] = bf_to_h(hi4.y), a[6] = bf_to_h(hi4.z), a[7] = bf_to_h(hi4.w);
+      acc = mfma16(a, qb[s], acc);
+    }
+    // lane holds U[t][j][32 dt + 8 g + 4 hi + k] for g, k < 4
+    if (live) {
+      _Float16* u = reinterpret_cast<_Float16*>(UN) + (t * H + j) * D + 32 * dt + 4 * hi;
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+        h4 o;
+        o[0] = static_cast<_Float16>(acc[4 * g]);
+        o[1] = static_cast<_Float16>(acc[4 * g + 1]);
+        o[2] = static_cast<_Float16>(acc[4 * g + 2]);
+        o[3] = static_cast<_Float16>(acc[4 * g + 3]);
+        *reinterpret_cast<h4*>(u + 8 * g) = o;
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ attention
+// One workgroup per unit (request, target group of up to 32 / H targets,
+// history chunk): its rows r = t H + j (at most 32) are the 32 columns of
+// every tile.  Eight waves in four pairs; in each round the pairs take the
+// next four 32-row X blocks (direct global-to-LDS loads into a per-pair
+// double buffer, the next round's blocks in flight while this round's are
+// used).  Both waves of a pair form
+// the block's scores; each accumulates half of the d columns of Y.  Every
+// pair keeps its own online-softmax state; the pairs' partials are merged at
+// the end.
+//   S^T (32 history rows x 32 rows (t, j)) = X U^T, K = d: A = X row operand,
+//   B = U rows (staged once in LDS).
+//   Y^T (d x 32) += X^T P^T, K = 32 history rows: B = P^T from the S^T
+//   registers (k-step s: rows 16 s + 4 hi + {0..3, 8..11}), A = X^T gathered
+//   from the LDS tile for the same history rows.
+template <int D>
+__global__ __launch_bounds__(128 * kWaves) void reord_attn_kernel(const Unit* __restrict__ units,
+                                                                  const WsHeader* __restrict__ hdr,
+                                                                  const f16x8* __restrict__ UN,
+                                                                  const bf16_bits* __restrict__ X, int64_t n_hist,
+                                                                  float* __restrict__ part_y,
+                                                                  float2* __restrict__ part_ml, int64_t n_tgt) {
+  constexpr int H = D / DH;
+  constexpr int KS = D / 16;
+  constexpr int CPR = D / 8;          // 16-byte chunks per X row
+  constexpr int NDT = D / 32;         // 32-dim tiles of Y^T
+  constexpr int HALF = NDT / 2;       // tiles per wave of a pair
+  constexpr int PER = 32 * CPR / 64;  // 1 KB segments per block
+  constexpr int RPS = 512 / D;        // rows per segment
+  constexpr int NT = 128 * kWaves;
+  constexpr int TB = static_cast<int>(reord_tile_bytes(D));
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int u = blockIdx.x;
+  if (u >= hdr->n_units) return;
+  const Unit un = units[u];
+  const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int pw = w % kWaves, half = w / kWaves;
+  const int tcol = lane % 32, hi = lane / 32;
+  const int R = un.nt * H;
+  unsigned char* xb = smem + (size_t)pw * 2 * TB;
+  // byte offset of element (row, col) in a tile
+  auto xoff = [](int row, int col) { return (row / RPS) * kSegPitch + (row % RPS) * 2 * D + col * 2; };
+  // the unit's U rows (fp16, padded), past the X tiles and the merge area
+  constexpr int UROW = D + 8;
+  _Float16* us = reinterpret_cast<_Float16*>(smem + reord_main_lds(D));
+  for (int e = threadIdx.x; e < 32 * (D / 8); e += NT) {
+    const int row = e / (D / 8), c8 = e % (D / 8);
+    const f16x8 v = row < R ? UN[((int64_t)un.t0 * H + row) * (D / 8) + c8] : zero8();
+    *reinterpret_cast<f16x8*>(us + row * UROW + c8 * 8) = v;
+  }
+  const _Float16* urow = us + tcol * UROW + 8 * hi;
+  f32x16 Y[HALF];
+#pragma unroll
+  for (int dt = 0; dt < HALF; ++dt) Y[dt] = f32x16{};
+  float m = -INFINITY, l = 0.f;
+  const int rounds = (un.b1 - un.b0 + kWaves - 1) / kWaves;
+  // this pair's block of round r: each wave of the pair loads half of it
+  auto dma = [&](int r, int buf) {
+    const int b = un.b0 + r * kWaves + pw;
+    if (b >= un.b1) return;
+#pragma unroll
+    for (int i = half * (PER / 2); i < (half + 1) * (PER / 2); ++i) {
+      const int p = i * 64 + lane;
+      const int row = p / CPR, c = p % CPR;
+      const int64_t grow = min((int64_t)b * 32 + row, n_hist - 1);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(X + grow * D + c * 8),
+                                       (void __attribute__((address_space(3)))*)(xb + buf * TB + i * kSegPitch), 16,
+                                       0, 0);
+    }
+  };
+  dma(0, 0);
+  for (int r = 0; r < rounds; ++r) {
+    const int cur = r & 1;
+    // round r's blocks have landed (every wave waited for its own loads), and
+    // every wave is done with the buffers of round r - 1
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (r + 1 < rounds) dma(r + 1, cur ^ 1);
+    const int b = un.b0 + r * kWaves + pw;
+    if (b >= un.b1) continue;
+    const unsigned char* xt = xb + cur * TB;
+    f32x16 s = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const uint4 raw = *reinterpret_cast<const uint4*>(xt + xoff(tcol, 16 * ks + 8 * hi));
+      s = mfma16(bf8_to_h8(raw), *reinterpret_cast<const f16x8*>(urow + 16 * ks), s);
+    }
+    if (b * 32 < un.l0 || b * 32 + 32 > un.l1) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int tok = b * 32 + 8 * (v / 4) + 4 * hi + (v % 4);
+        s[v] = (tok < un.l0 || tok >= un.l1) ? -INFINITY : s[v];
+      }
+    }
+    float bm = s[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) bm = fmaxf(bm, s[v]);
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    // per-lane threshold rescale: the reference max moves only when the block
+    // maximum exceeds it by kSlack (every block has a valid row, so bm is finite)
+    const float mn = bm > m + kSlack ? bm : m;
+    const float sc = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+    m = mn;
+    float ps = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      s[v] = __builtin_amdgcn_exp2f(s[v] - mn);
+      ps += s[v];
+    }
+    l = l * sc + ps;
+    const f16x8 p0 = pack8(s, 0), p1 = pack8(s, 8);
+#pragma unroll
+    for (int dt = 0; dt < HALF; ++dt) {
+      f32x16 acc = Y[dt] * sc;
+      const int dim = 32 * (half * HALF + dt) + tcol;
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        f16x8 a;
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int row = 16 * k2 + 4 * hi + (i < 4 ? i : i + 4);
+          a[i] = bf_to_h(*reinterpret_cast<const bf16_bits*>(xt + xoff(row, dim)));
+        }
+        acc = mfma16(a, k2 == 0 ? p0 : p1, acc);
+      }
+      Y[dt] = acc;
+      // two gathers in flight at a time: hoisting all of them would take
+      // eight registers per element
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  // merge the four pairs (the X tiles are dead: their LDS holds the partials)
+  __syncthreads();
+  float* red = reinterpret_cast<float*>(smem);  // [kWaves][32][D + 2]
+  const float lt = l + __shfl_xor(l, 32);
+  float* rw = red + ((size_t)pw * 32 + tcol) * (D + 2);
+  if (hi == 0 && half == 0) {
+    rw[0] = m;
+    rw[1] = lt;
+  }
+#pragma unroll
+  for (int dt = 0; dt < HALF; ++dt)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) rw[2 + 32 * (half * HALF + dt) + 8 * (v / 4) + 4 * hi + (v % 4)] = Y[dt][v];
+  __syncthreads();
+  for (int it = threadIdx.x; it < R * (D + 1); it += NT) {
+    const int row = it / (D + 1), e = it % (D + 1);  // e == D: (max, sum)
+    float M = -INFINITY;
+    for (int pp = 0; pp < kWaves; ++pp) M = fmaxf(M, red[((size_t)pp * 32 + row) * (D + 2)]);
+    float val = 0.f;
+    for (int pp = 0; pp < kWaves; ++pp) {
+      const float* rr = red + ((size_t)pp * 32 + row) * (D + 2);
+      const float f = rr[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(rr[0] - M);
+      val += f * (e == D ? rr[1] : rr[2 + e]);
+    }
+    const int t = row / H, j = row % H;
+    const int64_t prow = ((int64_t)un.c * n_tgt + un.t0 + t) * H + j;
+    if (e == D)
+      part_ml[prow] = make_float2(M, val);
+    else
+      part_y[prow * D + e] = val;
+  }
+}
+
+// ---------------------------------------------------------------- merge
+// One wave per (32 targets, head j): it merges the chunk partials of y_tj
+// into fp16 rows in LDS (two lanes per target, half of the d columns each),
+// then forms a_j^T = W_V^j^T y_j^T (A operand: the packed fp16 W_V, whose
+// column block j is head j) and writes a (fp32) with a single-chunk
+// (max 0, sum 1) record per (target, head) for the update kernel.
+template <int D>
+__global__ __launch_bounds__(64) void reord_merge_kernel(const float* __restrict__ part_y,
+                                                        const float2* __restrict__ part_ml,
+                                                        const int32_t* __restrict__ tchunks,
+                                                        const f16x8* __restrict__ WvP16, int layer,
+                                                        float* __restrict__ a_out, float2* __restrict__ ml_out,
+                                                        int32_t* __restrict__ tch_out, float* __restrict__ save_lse,
+                                                        int64_t n_tgt) {
+  constexpr int H = D / DH;
+  constexpr int KS = D / 16;
+  constexpr int YROW = D + 8;  // padded fp16 row
+  __shared__ __attribute__((aligned(16))) uint16_t ys[32 * YROW];
+  const int64_t tb = (int64_t)blockIdx.x * 32;
+  const int j = blockIdx.y;
+  const int lane = threadIdx.x;
+  {
+    const int row = lane / 2, part = lane % 2;  // columns [part D/2, (part + 1) D/2)
+    const int64_t t = tb + row;
+    uint16_t* y = ys + row * YROW + part * (D / 2);
+    if (t < n_tgt) {
+      const int nch = tchunks[t];
+      float M = -INFINITY;
+      for (int c = 0; c < nch; ++c) M = fmaxf(M, part_ml[((int64_t)c * n_tgt + t) * H + j].x);
+      float L = 0.f;
+      for (int c = 0; c < nch; ++c) L += __builtin_amdgcn_exp2f(part_ml[((int64_t)c * n_tgt + t) * H + j].x - M) *
+                                         part_ml[((int64_t)c * n_tgt + t) * H + j].y;
+      const float inv = 1.f / L;
+      for (int c0 = 0; c0 < D / 2; c0 += 16) {
+        float acc[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[i] = 0.f;
+        for (int c = 0; c < nch; ++c) {
+          const float2 ml = part_ml[((int64_t)c * n_tgt + t) * H + j];
+          const float wc = __builtin_amdgcn_exp2f(ml.x - M) * inv;
+          const float4* py = reinterpret_cast<const float4*>(part_y + (((int64_t)c * n_tgt + t) * H + j) * D +
+                                                             part * (D / 2) + c0);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const float4 v = py[q];
+            acc[4 * q] += wc * v.x, acc[4 * q + 1] += wc * v.y, acc[4 * q + 2] += wc * v.z, acc[4 * q + 3] += wc * v.w;
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 16; ++i) y[c0 + i] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(acc[i]));
+      }
+      if (part == 0) {
+        if (save_lse) save_lse[t * H + j] = (M + log2f(L)) * kLn2;
+        ml_out[t * H + j] = make_float2(0.f, 1.f);
+        if (j == 0) tch_out[t] = 1;
+      }
+    } else {
+      for (int i = 0; i < D / 2; ++i) y[i] = 0;
+    }
+  }
+  __syncthreads();
+  const int tcol = lane % 32, hi = lane / 32;
+  const f16x8* wp = WvP16 + ((int64_t)(layer * H + j) * KS) * 64 + lane;
+  const uint16_t* yb = ys + tcol * YROW + 8 * hi;
+  f16x8 wr[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) wr[ks] = wp[ks * 64];
+  f32x16 acc = {};
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) acc = mfma16(wr[ks], *reinterpret_cast<const f16x8*>(yb + 16 * ks), acc);
+  // lane holds a[t][32 j + 8 g + 4 hi + k] for g, k < 4
+  const int64_t t = tb + tcol;
+  if (t < n_tgt) {
+    float* ap = a_out + t * D + 32 * j + 4 * hi;
+#pragma unroll
+    for (int g = 0; g < 4; ++g)
+      *reinterpret_cast<float4*>(ap + 8 * g) = make_float4(acc[4 * g], acc[4 * g + 1], acc[4 * g + 2], acc[4 * g + 3]);
+  }
+}
+
+template <typename K>
+hipError_t allow_lds(K kernel, size_t bytes) {
+  static int set_for[64] = {0};  // per device: bytes granted so far
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev >= 0 && dev < 64 && set_for[dev] >= static_cast<int>(bytes)) return hipSuccess;
+  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                          static_cast<int>(bytes));
+  if (e == hipSuccess && dev >= 0 && dev < 64) set_for[dev] = static_cast<int>(bytes);
+  return e;
+}
+
+}  // namespace
+
+size_t reord_attn_lds(int D) { return reord_main_lds(D) + (size_t)32 * (D + 8) * 2; }
+
+hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, int64_t n_tgt, hipStream_t st) {
+  if (n_tgt == 0) return hipSuccess;
+  dim3 g(static_cast<unsigned>(ceil_div(n_tgt, 32)), D / DH);
+#define STCA_QU(DD)                                                                                              \
+  hipLaunchKernelGGL(reord_qu_kernel<DD>, g, dim3(64), 0, st, (const f16x8*)QN, (const bf16_bits*)Wk_layer, \
+                     (f16x8*)UN, n_tgt)
+  switch (D) {
+    case 64: STCA_QU(64); break;
+    case 128: STCA_QU(128); break;
+    case 256: STCA_QU(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_QU
+  return hipGetLastError();
+}
+
+hipError_t fast_reord_attn(int D, const Unit* units, const WsHeader* hdr, int64_t max_units, const void* UN,
+                           const void* X, int64_t n_hist, float* part_y, void* part_ml, int64_t n_tgt,
+                           hipStream_t st) {
+  if (max_units == 0) return hipSuccess;
+  const size_t lds = reord_attn_lds(D);
+#define STCA_RA(DD)                                                                                               \
+  do {                                                                                                            \
+    hipError_t e = allow_lds(reord_attn_kernel<DD>, lds);                                                         \
+    if (e != hipSuccess) return e;                                                                                \
+    hipLaunchKernelGGL(reord_attn_kernel<DD>, dim3(static_cast<unsigned>(max_units)), dim3(128 * kWaves), lds, st, \
+                       units, hdr, (const f16x8*)UN, (const bf16_bits*)X, n_hist, part_y, (float2*)part_ml,      \
+                       n_tgt);                                                                                    \
+  } while (0)
+  switch (D) {
+    case 64: STCA_RA(64); break;
+    case 128: STCA_RA(128); break;
+    case 256: STCA_RA(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_RA
+  return hipGetLastError();
+}
+
+hipError_t fast_reord_merge(int D, const float* part_y, const void* part_ml, const int32_t* tchunks,
+                            const void* WvP16, int layer, float* a_out, void* ml_out, int32_t* tch_out,
+                            float* save_lse, int64_t n_tgt, hipStream_t st) {
+  if (n_tgt == 0) return hipSuccess;
+  dim3 g(static_cast<unsigned>(ceil_div(n_tgt, 32)), D / DH);
+#define STCA_RM(DD)                                                                                             \
+  hipLaunchKernelGGL(reord_merge_kernel<DD>, g, dim3(64), 0, st, part_y, (const float2*)part_ml, tchunks,      \
+                     (const f16x8*)WvP16, layer, a_out, (float2*)ml_out, tch_out, save_lse, n_tgt)
+  switch (D) {
+    case 64: STCA_RM(64); break;
+    case 128: STCA_RM(128); break;
+    case 256: STCA_RM(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_RM
+  return hipGetLastError();
+}
+
+}  // namespace stca

@@ -5,7 +5,7 @@
 // history rows are covered by whole 32-row blocks of the packed history
 // ([floor(h0/32), ceil(h1/32))); the blocks are cut into at most kMaxChunks
 // chunks of about `chunk_blocks` blocks, and the request's targets into groups
-// of kTargetGroup.  One unit = (target group, chunk).  Units of groups with at
+// of `group` (at most kTargetGroup).  One unit = (target group, chunk).  Units of groups with at
 // most 32 targets are listed first, the wider ones after them, so kernels
 // specialised on the group width each get one contiguous range.  Every
 // target's chunk count is recorded so the combine step knows how many partial
@@ -29,7 +29,7 @@ struct ReqPlan {
 };
 
 __device__ ReqPlan plan_request(const int32_t* hoff, const int32_t* toff, int r, int64_t n_hist,
-                                int64_t n_tgt, int chunk_blocks) {
+                                int64_t n_tgt, int chunk_blocks, int group) {
   ReqPlan p{};
   p.h0 = hoff[r];
   p.h1 = hoff[r + 1];
@@ -47,12 +47,12 @@ __device__ ReqPlan plan_request(const int32_t* hoff, const int32_t* toff, int r,
   nch = nch < 1 ? 1 : (nch > kMaxChunks ? kMaxChunks : nch);
   p.cb = static_cast<int32_t>(ceil_div(nb, nch));
   p.nch = static_cast<int32_t>(ceil_div(nb, p.cb));  // no empty chunk
-  p.ng = static_cast<int32_t>(ceil_div(p.t1 - p.t0, kTargetGroup));
+  p.ng = static_cast<int32_t>(ceil_div(p.t1 - p.t0, group));
   return p;
 }
 
-__device__ __forceinline__ int group_size(const ReqPlan& p, int g) {
-  return min(kTargetGroup, p.t1 - (p.t0 + g * kTargetGroup));
+__device__ __forceinline__ int group_size(const ReqPlan& p, int g, int group) {
+  return min(group, p.t1 - (p.t0 + g * group));
 }
 
 __device__ int64_t block_scan(int64_t* scan, int64_t mine) {
@@ -71,7 +71,8 @@ __device__ int64_t block_scan(int64_t* scan, int64_t mine) {
 __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __restrict__ hoff,
                                                               const int32_t* __restrict__ toff, int R,
                                                               int64_t n_hist, int64_t n_tgt,
-                                                              int chunk_blocks, Unit* __restrict__ units,
+                                                              int chunk_blocks, int group,
+                                                              Unit* __restrict__ units,
                                                               int64_t max_units,
                                                               int32_t* __restrict__ tchunks,
                                                               WsHeader* __restrict__ hdr) {
@@ -88,9 +89,9 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
   int64_t narrow = 0, wide = 0;
   bool any_bad = false;
   for (int r = rb; r < re; ++r) {
-    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks);
+    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks, group);
     any_bad |= !p.ok;
-    for (int g = 0; g < p.ng; ++g) (group_size(p, g) > 32 ? wide : narrow) += p.nch;
+    for (int g = 0; g < p.ng; ++g) (group_size(p, g, group) > 32 ? wide : narrow) += p.nch;
   }
   if (any_bad) atomicOr(&bad, 1);
   int64_t un = block_scan(scan, narrow);
@@ -99,17 +100,17 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
   int64_t uw = total_narrow + block_scan(scan, wide);
   const int64_t total = total_narrow + scan[kSchedThreads - 1];
   for (int r = rb; r < re; ++r) {
-    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks);
+    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks, group);
     if (p.nch == 0) continue;
     const int32_t bh = static_cast<int32_t>(ceil_div(p.h1, kBlockTokens));
     for (int g = 0; g < p.ng; ++g) {
-      int64_t& u = group_size(p, g) > 32 ? uw : un;
+      int64_t& u = group_size(p, g, group) > 32 ? uw : un;
       for (int c = 0; c < p.nch; ++c, ++u) {
         if (u >= max_units) continue;
         Unit un_;
         un_.r = r;
-        un_.t0 = p.t0 + g * kTargetGroup;
-        un_.nt = group_size(p, g);
+        un_.t0 = p.t0 + g * group;
+        un_.nt = group_size(p, g, group);
         un_.c = c;
         un_.b0 = p.bl + c * p.cb;
         un_.b1 = min(un_.b0 + p.cb, bh);
@@ -130,15 +131,16 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
 }  // namespace
 
 hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
-                        int chunk_blocks, Unit* units, int64_t max_units, int32_t* tchunks,
+                        int chunk_blocks, int group, Unit* units, int64_t max_units, int32_t* tchunks,
                         WsHeader* hdr, hipStream_t st) {
+  if (group < 1 || group > kTargetGroup) return hipErrorInvalidValue;
   hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(kSchedThreads), 0, st, hoff, toff, R, n_hist, n_tgt,
-                     chunk_blocks, units, max_units, tchunks, hdr);
+                     chunk_blocks, group, units, max_units, tchunks, hdr);
   return hipGetLastError();
 }
 
 // Host mirror of plan_request for exact unit counts when host offsets exist.
-int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks) {
+int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks, int group) {
   int64_t n = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t h0 = hoff[r], h1 = hoff[r + 1], t0 = toff[r], t1 = toff[r + 1];
@@ -147,7 +149,7 @@ int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int ch
     int64_t nch = ceil_div(nb, chunk_blocks);
     nch = nch < 1 ? 1 : (nch > kMaxChunks ? kMaxChunks : nch);
     const int64_t cb = ceil_div(nb, nch);
-    n += ceil_div(nb, cb) * ceil_div(t1 - t0, kTargetGroup);
+    n += ceil_div(nb, cb) * ceil_div(t1 - t0, group);
   }
   return n;
 }

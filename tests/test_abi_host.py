@@ -134,3 +134,21 @@ def test_materialized_kv_needs_workspace_for_every_layer(monkeypatch):
     monkeypatch.setenv("STCA_KV", "materialize")
     mat = stca.stca_workspace_size(dims(), b)
     assert mat >= fused + 2 * 4 * 128 * 2 * 256  # 100 rows -> 4 blocks of 32, K and V, 4 layers, fp16
+
+
+def test_reordered_form_selection(monkeypatch):
+    """Requests with at most 32 / h targets (host offsets known) run the
+    reordered attention: its launch sequence is 7 + 4 n launches against the
+    standard form's 8 + 3 n."""
+    monkeypatch.delenv("STCA_ATTN", raising=False)
+    monkeypatch.delenv("STCA_KV", raising=False)
+    n = GOOD_DIMS["n_layers"]
+    small, keep1 = fake_batch([0, 40, 100, 101], [0, 4, 5, 8])   # m = 4, 1, 3 <= 32 / 8
+    wide, keep2 = fake_batch([0, 40, 100], [0, 5, 9])            # m = 5
+    assert stca.stca_forward_launch_count(dims(), small) == 7 + 4 * n
+    assert stca.stca_forward_launch_count(dims(), wide) == 8 + 3 * n
+    assert stca.stca_forward_launch_count(dims(d_model=128, n_heads=4), wide) == 7 + 4 * n  # 32 / 4 = 8
+    nohost = stca.batch(3, 101, 8, 0x10000, 0x20000, None, None)
+    assert stca.stca_forward_launch_count(dims(), nohost) == 8 + 3 * n
+    monkeypatch.setenv("STCA_ATTN", "standard")
+    assert stca.stca_forward_launch_count(dims(), small) == 8 + 3 * n
