@@ -432,14 +432,24 @@ def ablation(wl: W.Workload, args):
         finally:
             del os.environ["STCA_KV"]
     if wl.n_targets > 1 and wl.hist_range is None:
+        # one target per request: the reordered attention (App. A.2.2), and
+        # the standard form on the same batch
         one = W.Workload(wl.name + "_m1", wl.n_requests, wl.d_model, wl.n_heads, wl.n_layers, wl.dtype, wl.seed,
                          hist_len=wl.hist_len, n_targets=1)
-        db = DeviceBatch(W.make_batch(one), device="cuda:0")
-        ms, _ = timed_forward(db, max(3, args.steps // 4), 1)
-        ms /= max(3, args.steps // 4)
-        out["one_target_per_request"] = {"ms_per_step": ms, "targets_per_s": one.n_requests / (ms * 1e-3)}
-        del db
-        torch.cuda.empty_cache()
+        bo = W.make_batch(one)
+        for key, mode in (("one_target_per_request", None), ("one_target_per_request_standard", "standard")):
+            if mode:
+                os.environ["STCA_ATTN"] = mode
+            try:
+                db = DeviceBatch(bo, device="cuda:0")
+                k = max(3, args.steps // 4)
+                ms = plain_forward(db, k, 2) / k
+                out[key] = {"ms_per_step": ms, "targets_per_s": one.n_requests / (ms * 1e-3),
+                            "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
+                del db
+                torch.cuda.empty_cache()
+            finally:
+                os.environ.pop("STCA_ATTN", None)
     # instance-wise layout on a slice of requests that fits comfortably, scaled
     b = W.make_batch(wl, requests=list(range(min(wl.n_requests, 8))), with_grad=False)
     nb = W.replicate_per_target(b)

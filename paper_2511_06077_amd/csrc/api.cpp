@@ -71,15 +71,18 @@ int device_cus() {
 }
 
 // Chunk length (in 32-row blocks) of the split over history rows: aim at about
-// four attention units per CU.  STCA_CHUNK_BLOCKS overrides it (a tuning and
-// testing knob: forcing small chunks exercises the partial-result merge).
-int chunk_blocks_for(const stca_batch_t* b, int n_cu) {
+// `per_cu` attention units per CU (four for the standard form; one for the
+// reordered form, whose units stream X with little work per block and whose
+// merge cost grows with the chunk count).  STCA_CHUNK_BLOCKS overrides it (a
+// tuning and testing knob: forcing small chunks exercises the partial-result
+// merge).
+int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu) {
   if (const char* e = std::getenv("STCA_CHUNK_BLOCKS")) {
     int v = std::atoi(e);
     if (v >= 1) return v;
   }
   const int64_t nb = ceil_div(b->n_hist, kBlockTokens);
-  int64_t c = ceil_div(nb, 4 * static_cast<int64_t>(n_cu));
+  int64_t c = ceil_div(nb, per_cu * static_cast<int64_t>(n_cu));
   if (c < 8) c = 8;
   if (c > (1 << 20)) c = 1 << 20;
   return static_cast<int>(c);
@@ -151,8 +154,8 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
   L->nh = b->n_hist;
   L->nt = b->n_tgt;
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
-  L->chunk_blocks = chunk_blocks_for(b, device_cus());
   L->reord = p == 1 && !with_backward && reordered_for(dims, b);
+  L->chunk_blocks = chunk_blocks_for(b, device_cus(), L->reord ? 1 : 4);
   L->group = L->reord ? 32 / L->h : kTargetGroup;
   L->max_units = max_units_for(b, L->chunk_blocks, L->group);
   L->any_narrow = L->any_wide = true;
@@ -188,7 +191,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->kv = materialize_kv() && !L->reord ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
       if (L->reord) {
         const size_t h = L->h;
-        L->un = m.take(2 * nt * h * d);
+        L->un = m.take(2 * 2 * nt * h * d);  // bf16 hi and lo terms
         L->part_y = m.take(4 * kMaxChunks * nt * h * d);
         L->a2 = m.take(4 * nt * d);
         L->ml2 = m.take(8 * nt * h);

@@ -41,7 +41,8 @@ hipError_t fast_fused(int D, int wide, const Unit* units, const WsHeader* hdr, i
 hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st);
 
 // Reordered single-query attention (reordered.hip) for units of at most
-// 32 / H targets: U = per-head Q W_K^j^T (fp16 [n_tgt][H][D]), the attention
+// 32 / H targets: U = per-head Q W_K^j^T (bf16 hi and lo terms
+// [n_tgt][H][2][D]), the attention
 // over X writing per-chunk y partials ([16][n_tgt][H][D] fp32 and (max, sum)
 // [16][n_tgt][H]), and the merge that forms a = y W_V^j (fp32 [n_tgt][D]) with
 // single-chunk records (ml_out (0, 1), tch_out 1) for fast_update.

@@ -16,10 +16,12 @@
 //   reord_merge_kernel: y_tj = merged partials, a_tj = y_tj W_V^j (fp32),
 //                       handed to the target update as a single chunk
 //
-// MFMA lane layouts are those of v_mfma_f32_32x32x16_f16 (see fast.hip).  X
-// is bf16 in HBM and converted to fp16 in registers (exact for values in
-// fp16's normal range), so every product runs on fp16 operands with fp32
-// accumulation, like the standard path's attention.
+// MFMA lane layouts are those of v_mfma_f32_32x32x16_bf16 (see fast.hip).
+// X enters every product as the bf16 it is stored in, with no conversion.
+// The other operands, U and the softmax weights P, are fp32 values carried
+// as two bf16 terms (hi = bf16(v), lo = bf16(v - hi), about 16 significant
+// bits), each product taken twice: more precise than one fp16 operand, and
+// cheaper than converting X.
 #include "common.h"
 #include "fast.h"
 
@@ -47,6 +49,20 @@ __host__ __device__ constexpr size_t reord_main_lds(int D) {
 
 __device__ __forceinline__ f32x16 mfma16(const f16x8& a, const f16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mfmab(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// v ~ hi + lo, both bf16 (round to nearest even)
+__device__ __forceinline__ __bf16 bf_hi(float v) { return static_cast<__bf16>(v); }
+__device__ __forceinline__ __bf16 bf_lo(float v, __bf16 hi) { return static_cast<__bf16>(v - static_cast<float>(hi)); }
+
+__device__ __forceinline__ bf16x8 zero8b() {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<__bf16>(0.f);
+  return r;
 }
 
 __device__ __forceinline__ f16x8 pack8(const f32x16& a, int off) {
@@ -80,7 +96,7 @@ __device__ __forceinline__ f16x8 bf8_to_h8(const uint4& v) {
 // operand W_K[dim][32 j + the same head dims].
 template <int D>
 __global__ __launch_bounds__(64) void reord_qu_kernel(const f16x8* __restrict__ QN, const bf16_bits* __restrict__ Wk,
-                                                      f16x8* __restrict__ UN, int64_t n_tgt) {
+                                                      __bf16* __restrict__ UN, int64_t n_tgt) {
   constexpr int H = D / DH;
   const int j = blockIdx.y;
   const int lane = threadIdx.x;
@@ -104,18 +120,21 @@ __global__ __launch_bounds__(64) void reord_qu_kernel(const f16x8* __restrict__ 
       a[4] = bf_to_h(hi4.x), a[5] = bf_to_h(hi4.y), a[6] = bf_to_h(hi4.z), a[7] = bf_to_h(hi4.w);
       acc = mfma16(a, qb[s], acc);
     }
-    // lane holds U[t][j][32 dt + 8 g + 4 hi + k] for g, k < 4
+    // lane holds U[t][j][32 dt + 8 g + 4 hi + k] for g, k < 4; row (t, j) of
+    // UN holds the hi terms, then the lo terms
     if (live) {
-      _Float16* u = reinterpret_cast<_Float16*>(UN) + (t * H + j) * D + 32 * dt + 4 * hi;
+      __bf16* u = UN + (t * H + j) * 2 * D + 32 * dt + 4 * hi;
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
-        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-        h4 o;
-        o[0] = static_cast<_Float16>(acc[4 * g]);
-        o[1] = static_cast<_Float16>(acc[4 * g + 1]);
-        o[2] = static_cast<_Float16>(acc[4 * g + 2]);
-        o[3] = static_cast<_Float16>(acc[4 * g + 3]);
-        *reinterpret_cast<h4*>(u + 8 * g) = o;
+        typedef __bf16 b4 __attribute__((ext_vector_type(4)));
+        b4 h, l;
+#pragma unroll
+        for (int k = 0; k < 4; ++k) {
+          h[k] = bf_hi(acc[4 * g + k]);
+          l[k] = bf_lo(acc[4 * g + k], h[k]);
+        }
+        *reinterpret_cast<b4*>(u + 8 * g) = h;
+        *reinterpret_cast<b4*>(u + D + 8 * g) = l;
       }
     }
   }
@@ -139,7 +158,7 @@ __global__ __launch_bounds__(64) void reord_qu_kernel(const f16x8* __restrict__ 
 template <int D>
 __global__ __launch_bounds__(128 * kWaves) void reord_attn_kernel(const Unit* __restrict__ units,
                                                                   const WsHeader* __restrict__ hdr,
-                                                                  const f16x8* __restrict__ UN,
+                                                                  const __bf16* __restrict__ UN,
                                                                   const bf16_bits* __restrict__ X, int64_t n_hist,
                                                                   float* __restrict__ part_y,
                                                                   float2* __restrict__ part_ml, int64_t n_tgt) {
@@ -163,15 +182,24 @@ __global__ __launch_bounds__(128 * kWaves) void reord_attn_kernel(const Unit* __
   unsigned char* xb = smem + (size_t)pw * 2 * TB;
   // byte offset of element (row, col) in a tile
   auto xoff = [](int row, int col) { return (row / RPS) * kSegPitch + (row % RPS) * 2 * D + col * 2; };
-  // the unit's U rows (fp16, padded), past the X tiles and the merge area
+  // the unit's U: hi terms in registers (B operand: row tcol, model dims
+  // 16 ks + 8 hi ..), lo terms staged in LDS (padded rows) past the X tiles
+  // and the merge area
   constexpr int UROW = D + 8;
-  _Float16* us = reinterpret_cast<_Float16*>(smem + reord_main_lds(D));
+  __bf16* us = reinterpret_cast<__bf16*>(smem + reord_main_lds(D));
   for (int e = threadIdx.x; e < 32 * (D / 8); e += NT) {
     const int row = e / (D / 8), c8 = e % (D / 8);
-    const f16x8 v = row < R ? UN[((int64_t)un.t0 * H + row) * (D / 8) + c8] : zero8();
-    *reinterpret_cast<f16x8*>(us + row * UROW + c8 * 8) = v;
+    const bf16x8 v = row < R ? *reinterpret_cast<const bf16x8*>(UN + ((int64_t)un.t0 * H + row) * 2 * D + D + c8 * 8)
+                             : zero8b();
+    *reinterpret_cast<bf16x8*>(us + row * UROW + c8 * 8) = v;
   }
-  const _Float16* urow = us + tcol * UROW + 8 * hi;
+  const __bf16* ulo = us + tcol * UROW + 8 * hi;
+  bf16x8 uhi[KS];
+  {
+    const __bf16* up = UN + ((int64_t)un.t0 * H + tcol) * 2 * D + 8 * hi;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) uhi[ks] = tcol < R ? *reinterpret_cast<const bf16x8*>(up + 16 * ks) : zero8b();
+  }
   f32x16 Y[HALF];
 #pragma unroll
   for (int dt = 0; dt < HALF; ++dt) Y[dt] = f32x16{};
@@ -205,8 +233,9 @@ __global__ __launch_bounds__(128 * kWaves) void reord_attn_kernel(const Unit* __
     f32x16 s = {};
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
-      const uint4 raw = *reinterpret_cast<const uint4*>(xt + xoff(tcol, 16 * ks + 8 * hi));
-      s = mfma16(bf8_to_h8(raw), *reinterpret_cast<const f16x8*>(urow + 16 * ks), s);
+      const bf16x8 xr = *reinterpret_cast<const bf16x8*>(xt + xoff(tcol, 16 * ks + 8 * hi));
+      s = mfmab(xr, uhi[ks], s);
+      s = mfmab(xr, *reinterpret_cast<const bf16x8*>(ulo + 16 * ks), s);
     }
     if (b * 32 < un.l0 || b * 32 + 32 > un.l1) {
 #pragma unroll
@@ -231,20 +260,27 @@ __global__ __launch_bounds__(128 * kWaves) void reord_attn_kernel(const Unit* __
       ps += s[v];
     }
     l = l * sc + ps;
-    const f16x8 p0 = pack8(s, 0), p1 = pack8(s, 8);
+    bf16x8 ph[2], pl[2];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const __bf16 h = bf_hi(s[i]);
+      ph[i / 8][i % 8] = h;
+      pl[i / 8][i % 8] = bf_lo(s[i], h);
+    }
 #pragma unroll
     for (int dt = 0; dt < HALF; ++dt) {
       f32x16 acc = Y[dt] * sc;
       const int dim = 32 * (half * HALF + dt) + tcol;
 #pragma unroll
       for (int k2 = 0; k2 < 2; ++k2) {
-        f16x8 a;
+        bf16x8 a;
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
           const int row = 16 * k2 + 4 * hi + (i < 4 ? i : i + 4);
-          a[i] = bf_to_h(*reinterpret_cast<const bf16_bits*>(xt + xoff(row, dim)));
+          a[i] = *reinterpret_cast<const __bf16*>(xt + xoff(row, dim));
         }
-        acc = mfma16(a, k2 == 0 ? p0 : p1, acc);
+        acc = mfmab(a, ph[k2], acc);
+        acc = mfmab(a, pl[k2], acc);
       }
       Y[dt] = acc;
       // two gathers in flight at a time: hoisting all of them would take
@@ -387,7 +423,7 @@ hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, 
   dim3 g(static_cast<unsigned>(ceil_div(n_tgt, 32)), D / DH);
 #define STCA_QU(DD)                                                                                              \
   hipLaunchKernelGGL(reord_qu_kernel<DD>, g, dim3(64), 0, st, (const f16x8*)QN, (const bf16_bits*)Wk_layer, \
-                     (f16x8*)UN, n_tgt)
+                     (__bf16*)UN, n_tgt)
   switch (D) {
     case 64: STCA_QU(64); break;
     case 128: STCA_QU(128); break;
@@ -408,7 +444,7 @@ hipError_t fast_reord_attn(int D, const Unit* units, const WsHeader* hdr, int64_
     hipError_t e = allow_lds(reord_attn_kernel<DD>, lds);                                                         \
     if (e != hipSuccess) return e;                                                                                \
     hipLaunchKernelGGL(reord_attn_kernel<DD>, dim3(static_cast<unsigned>(max_units)), dim3(128 * kWaves), lds, st, \
-                       units, hdr, (const f16x8*)UN, (const bf16_bits*)X, n_hist, part_y, (float2*)part_ml,      \
+                       units, hdr, (const __bf16*)UN, (const bf16_bits*)X, n_hist, part_y, (float2*)part_ml,     \
                        n_tgt);                                                                                    \
   } while (0)
   switch (D) {
