@@ -189,6 +189,8 @@ def main() -> int:
                     help="also time one target per request and the instance-wise (non-RLB) layout")
     ap.add_argument("--backward", action="store_true",
                     help="time forward + backward steps (the training window workload by default)")
+    ap.add_argument("--sl", action="store_true",
+                    help="with --backward: a stochastic-length batch (Beta lengths, alpha 0.02, L_avg 2048 of 10240)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead: time a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -324,7 +326,22 @@ def train_step(args) -> int:
     from paper_2511_06077_amd.device import DeviceBatch, to_device
     name = args.workload if args.workload != W.HEADLINE else "train_bf16_R256_m16_L2048_d256"
     wl = W.WORKLOADS[name]
-    b = W.make_batch(wl, with_grad=True)
+    sl_info = None
+    if args.sl:
+        # stochastic-length batch: full histories of L_infer = 10240 rows cut
+        # to Beta-sampled temporal suffixes (alpha = 0.02, L_avg = 2048)
+        from paper_2511_06077_amd import sl
+        full_wl = W.Workload(wl.name + "_L10240", wl.n_requests, wl.d_model, wl.n_heads, wl.n_layers, wl.dtype,
+                             wl.seed, hist_len=10240, n_targets=wl.n_targets, backward=True)
+        t0 = time.time()
+        full = W.make_batch(full_wl, with_grad=True)
+        b, sl_info = sl.sl_batch(full, wl.seed, alpha=0.02, l_min=8, l_avg=2048, l_max=10240)
+        del full
+        log(f"[bench] stochastic-length batch: {b.n_hist} of {wl.n_requests * 10240} rows kept "
+            f"({time.time() - t0:.1f} s)")
+        wl = b.wl
+    else:
+        b = W.make_batch(wl, with_grad=True)
     db = DeviceBatch(b, device="cuda:0", backward=True)
     dout = to_device(b.grad_out, "cuda:0")
 
@@ -385,6 +402,7 @@ def train_step(args) -> int:
         "dtype": "bf16" if wl.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": wl.name, "requests": wl.n_requests, "targets_per_request": wl.n_targets,
                    "hist_len": wl.hist_len, "d_model": wl.d_model, "heads": wl.n_heads, "layers": wl.n_layers},
+        "stochastic_length": sl_info,
         "forward_ms": fwd, "backward_ms": bwd, "backward_roofline": roof,
         "backward_phase_bound_ms": bound_ms, "backward_phases": phases}), flush=True)
     return 0

@@ -182,6 +182,38 @@ stca_status_t stca_backward_profiled(const stca_dims_t* dims, const stca_batch_t
                                      hipStream_t stream, hipEvent_t* events, int n_events,
                                      const char** labels);
 
+/* ---- Stochastic-length training batches (Sec. 3.3; App. "Extrapolation
+ * details": Beta sampling, Eq. beta-scale and Eq. beta; batch-level load
+ * balancing).  Host functions on host arrays; no GPU involved.
+ *
+ * stca_sl_beta: the Beta shape beta that makes E[L_raw] = l_avg (Eq. beta):
+ * alpha (l_max - l_avg) / (l_avg - l_min).  NaN unless alpha > 0 and
+ * 0 <= l_min < l_avg < l_max.
+ *
+ * stca_sl_sample: per request r, s ~ Beta(alpha, beta) from a counter-based
+ * stream keyed by (seed, r), L_raw = l_min + s (l_max - l_min) (written to
+ * l_raw[r] when l_raw is not NULL), and l_train[r] = L_raw rounded to the
+ * nearest multiple of 8, clamped to [max(8, l_min rounded), l_max].
+ *
+ * stca_sl_allocate: global length allocation under a token budget (the paper
+ * uses B * l_avg): l_keep[r] = min(l_full[r], l_train[r]); if their sum
+ * exceeds `budget`, every l_keep is capped at the largest multiple of 8 that
+ * brings the sum within it (at least 8).
+ *
+ * stca_sl_pack: sequence compaction with temporal-suffix selection.  full_off
+ * [n+1] segments the full histories; request r keeps its last l_keep[r] rows.
+ * Writes hist_off [n+1] of the packed layout and, when src_rows is not NULL,
+ * src_rows [hist_off[n]]: the full-history row each packed row comes from.
+ *
+ * All return STCA_ERR_INVALID_ARG on inconsistent arguments. */
+double stca_sl_beta(double alpha, int32_t l_min, int32_t l_avg, int32_t l_max);
+stca_status_t stca_sl_sample(uint64_t seed, int32_t n, double alpha, int32_t l_min, int32_t l_avg,
+                             int32_t l_max, double* l_raw, int32_t* l_train);
+stca_status_t stca_sl_allocate(int32_t n, const int32_t* l_full, const int32_t* l_train, int64_t budget,
+                               int32_t* l_keep);
+stca_status_t stca_sl_pack(int32_t n, const int32_t* full_off, const int32_t* l_keep, int32_t* hist_off,
+                           int32_t* src_rows);
+
 /* Reads (synchronising on `stream`) the status the device scheduler recorded
  * in `ws` during the last call that used it: STCA_OK or STCA_ERR_INVALID_ARG. */
 stca_status_t stca_device_status(const void* ws, hipStream_t stream);

@@ -18,7 +18,8 @@ STCA_F32, STCA_BF16 = 0, 1
 
 EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca_forward", "stca_backward",
             "stca_device_status", "stca_status_string", "stca_path", "stca_forward_launch_count",
-            "stca_forward_profiled", "stca_backward_launch_count", "stca_backward_profiled")
+            "stca_forward_profiled", "stca_backward_launch_count", "stca_backward_profiled",
+            "stca_sl_beta", "stca_sl_sample", "stca_sl_allocate", "stca_sl_pack")
 
 
 class stca_dims_t(ctypes.Structure):
@@ -102,6 +103,16 @@ def lib():
                                              P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                              P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                              P(ctypes.c_void_p), ctypes.c_int, P(ctypes.c_char_p)]
+        I32P = P(ctypes.c_int32)
+        L.stca_sl_beta.restype = ctypes.c_double
+        L.stca_sl_beta.argtypes = [ctypes.c_double, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
+        L.stca_sl_sample.restype = ctypes.c_int
+        L.stca_sl_sample.argtypes = [ctypes.c_uint64, ctypes.c_int32, ctypes.c_double, ctypes.c_int32, ctypes.c_int32,
+                                     ctypes.c_int32, P(ctypes.c_double), I32P]
+        L.stca_sl_allocate.restype = ctypes.c_int
+        L.stca_sl_allocate.argtypes = [ctypes.c_int32, I32P, I32P, ctypes.c_int64, I32P]
+        L.stca_sl_pack.restype = ctypes.c_int
+        L.stca_sl_pack.argtypes = [ctypes.c_int32, I32P, I32P, I32P, I32P]
         _lib = L
     return _lib
 
@@ -250,3 +261,48 @@ class HipEvents:
             if self.ev[i]:
                 self.hip.hipEventDestroy(self.ev[i])
                 self.ev[i] = None
+
+
+# ---- stochastic-length batches (host functions)
+def _i32p(a):
+    return None if a is None else a.ctypes.data_as(ctypes.POINTER(ctypes.c_int32))
+
+
+def sl_beta(alpha: float, l_min: int, l_avg: int, l_max: int) -> float:
+    return lib().stca_sl_beta(alpha, l_min, l_avg, l_max)
+
+
+def sl_sample(seed: int, n: int, alpha: float, l_min: int, l_avg: int, l_max: int):
+    """(l_raw float64 [n], l_train int32 [n])"""
+    import numpy as np
+    raw = np.empty(n, dtype=np.float64)
+    out = np.empty(n, dtype=np.int32)
+    st = lib().stca_sl_sample(seed, n, alpha, l_min, l_avg, l_max,
+                              raw.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), _i32p(out))
+    if st != STCA_OK:
+        raise StcaError(st, "stca_sl_sample")
+    return raw, out
+
+
+def sl_allocate(l_full, l_train, budget: int):
+    import numpy as np
+    l_full = np.ascontiguousarray(l_full, dtype=np.int32)
+    l_train = np.ascontiguousarray(l_train, dtype=np.int32)
+    out = np.empty_like(l_full)
+    st = lib().stca_sl_allocate(len(l_full), _i32p(l_full), _i32p(l_train), int(budget), _i32p(out))
+    if st != STCA_OK:
+        raise StcaError(st, "stca_sl_allocate")
+    return out
+
+
+def sl_pack(full_off, l_keep):
+    """(hist_off int32 [n+1], src_rows int32 [sum l_keep])"""
+    import numpy as np
+    full_off = np.ascontiguousarray(full_off, dtype=np.int32)
+    l_keep = np.ascontiguousarray(l_keep, dtype=np.int32)
+    hoff = np.empty(len(l_keep) + 1, dtype=np.int32)
+    src = np.empty(int(l_keep.sum()), dtype=np.int32)
+    st = lib().stca_sl_pack(len(l_keep), _i32p(full_off), _i32p(l_keep), _i32p(hoff), _i32p(src))
+    if st != STCA_OK:
+        raise StcaError(st, "stca_sl_pack")
+    return hoff, src

@@ -105,3 +105,20 @@ def test_training_window_gradients(torch, chunk_override):
         e = tensor_err(g[k], ga[k] + gb[k])
         print(f"[grad] linearity {k}: {e:.1e}", flush=True)
         assert e <= 1e-3, (k, e)
+
+
+def test_stochastic_length_batch(torch, chunk_override):
+    """A stochastic-length training batch (Beta lengths with alpha = 0.02,
+    temporal suffixes, token budget, packed): bimodal ragged histories from
+    8 rows to the full length.  Forward and every gradient against the oracle."""
+    from paper_2511_06077_amd import sl
+    from test_gpu_forward import check_against_oracle, run_gpu
+    chunk_override(None)
+    full = W.make_custom_batch("slfull", [2048] * 12, [4, 16, 1, 33, 8, 2, 16, 5, 64, 3, 1, 9], d_model=256,
+                               n_heads=8, n_layers=2, dtype="bf16", seed=42, with_grad=True)
+    b, info = sl.sl_batch(full, 17, alpha=0.02, l_min=8, l_avg=256, l_max=2048)
+    print(f"[sl] kept {info['kept_tokens']} of budget {info['budget']}, lengths {b.hist_len.tolist()}", flush=True)
+    assert info["kept_tokens"] <= info["budget"]
+    y, a, lse, _ = run_gpu(torch, b)
+    check_against_oracle(b, y, a, lse, TOL["bf16"])
+    check(b, gpu_grads(torch, b), TOL["bf16"])
