@@ -468,6 +468,27 @@ def ablation(wl: W.Workload, args):
                 torch.cuda.empty_cache()
             finally:
                 os.environ.pop("STCA_ATTN", None)
+    if wl.n_targets > 1 and wl.hist_range is None:
+        # the same number of targets as 16 requests of 256: K/V written once
+        # and read once per 128 targets, against the fused form's projection
+        # per 64-target group
+        many = W.Workload(wl.name + "_m256", max(1, wl.n_requests * wl.n_targets // 256), wl.d_model, wl.n_heads,
+                          wl.n_layers, wl.dtype, wl.seed, hist_len=wl.hist_len, n_targets=256)
+        bm = W.make_batch(many)
+        for key, mode in (("many_targets_per_request", None), ("many_targets_per_request_fused", "fused")):
+            if mode:
+                os.environ["STCA_KV"] = mode
+            try:
+                db = DeviceBatch(bm, device="cuda:0")
+                k = max(3, args.steps // 4)
+                ms = plain_forward(db, k, 2) / k
+                out[key] = {"requests": many.n_requests, "targets": bm.n_tgt_total, "ms_per_step": ms,
+                            "targets_per_s": bm.n_tgt_total / (ms * 1e-3),
+                            "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
+                del db
+                torch.cuda.empty_cache()
+            finally:
+                os.environ.pop("STCA_KV", None)
     # instance-wise layout on a slice of requests that fits comfortably, scaled
     b = W.make_batch(wl, requests=list(range(min(wl.n_requests, 8))), with_grad=False)
     nb = W.replicate_per_target(b)

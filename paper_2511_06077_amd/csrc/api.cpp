@@ -112,6 +112,20 @@ bool reordered_for(const stca_dims_t* dims, const stca_batch_t* b) {
   return true;
 }
 
+// Requests with more than kTargetGroup targets: the fused kernel would
+// project their history once per 64-target group, so the bf16 path writes
+// K/V once instead and runs the attention in units of up to kWideGroup
+// targets (K/V read once per 128 targets).  Needs host offsets; STCA_KV=fused
+// keeps the fused form.
+bool wide_groups_for(const stca_batch_t* b) {
+  const char* e = std::getenv("STCA_KV");
+  if (e && std::strcmp(e, "fused") == 0) return false;
+  if (!b->tgt_off_host) return false;
+  for (int r = 0; r < b->n_requests; ++r)
+    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > kTargetGroup) return true;
+  return false;
+}
+
 int64_t max_units_for(const stca_batch_t* b, int chunk_blocks, int group) {
   if (b->hist_off_host)
     return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks, group);
@@ -126,6 +140,7 @@ struct Layout {
   int64_t max_units;
   bool any_narrow, any_wide;  // requests with 1..32 / 33+ targets (both true without host offsets)
   bool reord;                 // reordered attention (bf16 path)
+  bool wide;                  // materialised K/V, units of up to kWideGroup targets (bf16 path)
   int group;                  // targets per attention unit
   // common
   size_t hdr, units, tchunks, part_acc, part_ml, state_a, state_b;
@@ -155,16 +170,17 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
   L->nt = b->n_tgt;
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
   L->reord = p == 1 && !with_backward && reordered_for(dims, b);
+  L->wide = p == 1 && !with_backward && !L->reord && wide_groups_for(b);
   L->chunk_blocks = chunk_blocks_for(b, device_cus(), L->reord ? 1 : 4);
-  L->group = L->reord ? 32 / L->h : kTargetGroup;
+  L->group = L->reord ? 32 / L->h : (L->wide ? kWideGroup : kTargetGroup);
   L->max_units = max_units_for(b, L->chunk_blocks, L->group);
   L->any_narrow = L->any_wide = true;
   if (b->tgt_off_host) {
     L->any_narrow = L->any_wide = false;
     for (int r = 0; r < b->n_requests; ++r) {
       const int64_t m = b->tgt_off_host[r + 1] - b->tgt_off_host[r];
-      // target groups are kTargetGroup wide; the last group of a request is what may be narrow
-      for (int64_t g0 = 0; g0 < m; g0 += kTargetGroup) {
+      // target groups are `group` wide; the last group of a request is what may be narrow
+      for (int64_t g0 = 0; g0 < m; g0 += L->group) {
         if (m - g0 > 32) L->any_wide = true;
         else L->any_narrow = true;
       }
@@ -188,7 +204,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->wqp = m.take(2 * n * d * d);
       L->w1p = m.take(2 * n * d * F);
       L->w2p = m.take(2 * n * d * F);
-      L->kv = materialize_kv() && !L->reord ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
+      L->kv = (materialize_kv() || L->wide) && !L->reord ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
       if (L->reord) {
         const size_t h = L->h;
         L->un = m.take(2 * 2 * nt * h * d);  // bf16 hi and lo terms
@@ -384,7 +400,7 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wq"));
   HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, 1, st)); HIPCHK(rec.mark("pack_w1"));
   HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, 1, st)); HIPCHK(rec.mark("pack_w2"));
-  const bool mat = materialize_kv();
+  const bool mat = materialize_kv() || L.wide;
   char* kv = at<char>(ws, L.kv);
   if (mat) {
     if (L.nh > 0)
@@ -715,7 +731,7 @@ int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch
   Layout L;
   if (!make_layout(dims, batch, 0, false, &L)) return -1;
   if (L.path == 1 && L.reord) return 1 + 5 + 1 + 1 + 4 * L.n - 1;
-  if (L.path == 1) return materialize_kv() ? 1 + 6 + 1 + 1 + 2 * L.n : 1 + 6 + 1 + 3 * L.n;
+  if (L.path == 1) return materialize_kv() || L.wide ? 1 + 6 + 1 + 1 + 2 * L.n : 1 + 6 + 1 + 3 * L.n;
   return 1 + 1 + 8 * L.n + 1;
 }
 

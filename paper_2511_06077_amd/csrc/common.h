@@ -16,6 +16,7 @@ typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kBlockTokens = 32;  // history rows per K/V block (one MFMA tile edge)
 constexpr int kTargetGroup = 64;  // targets one attention unit holds (two 32-wide MFMA column groups)
+constexpr int kWideGroup = 128;   // targets per unit of the materialised-K/V attention for m > 64
 constexpr int kMaxChunks = 16;    // at most this many history chunks per request
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;

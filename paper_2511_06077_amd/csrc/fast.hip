@@ -288,9 +288,9 @@ struct Online {
 
 // ------------------------------------ K3: attention over materialised K/V
 // One workgroup per unit (a request's target group x a chunk of its history
-// blocks), one wave per head.  All of the unit's targets are held by every
-// wave, so each K/V byte is read from HBM once per unit whatever the number
-// of targets.  K/V blocks are double-buffered in registers.
+// blocks), one wave per head.  All of the unit's targets (up to 128: four
+// 32-wide column groups) are held by every wave, so each K/V byte is read
+// from HBM once per unit whatever the number of targets.  K/V blocks are double-buffered in registers.
 template <int H, int NG>
 __device__ __forceinline__ void attn_unit(const Unit& un, const f16x8* __restrict__ QN,
                                           const f16x8* __restrict__ KVl, float* __restrict__ part_acc,
@@ -327,7 +327,9 @@ __global__ __launch_bounds__(64 * H) void attn_kernel(const Unit* __restrict__ u
   const int nu = hdr->n_units;
   for (int u = blockIdx.x; u < nu; u += gridDim.x) {
     const Unit un = units[u];
-    if (un.nt > 32)
+    if (un.nt > 64)
+      attn_unit<H, 4>(un, QN, KVl, part_acc, part_ml, n_tgt);
+    else if (un.nt > 32)
       attn_unit<H, 2>(un, QN, KVl, part_acc, part_ml, n_tgt);
     else
       attn_unit<H, 1>(un, QN, KVl, part_acc, part_ml, n_tgt);

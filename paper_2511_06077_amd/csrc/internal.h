@@ -6,7 +6,7 @@
 namespace stca {
 
 // ---- scheduler (sched.hip)
-// `group`: targets per unit (1..kTargetGroup).
+// `group`: targets per unit (1..kWideGroup).
 hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
                         int chunk_blocks, int group, Unit* units, int64_t max_units, int32_t* tchunks,
                         WsHeader* hdr, hipStream_t st);

@@ -5,7 +5,7 @@
 // history rows are covered by whole 32-row blocks of the packed history
 // ([floor(h0/32), ceil(h1/32))); the blocks are cut into at most kMaxChunks
 // chunks of about `chunk_blocks` blocks, and the request's targets into groups
-// of `group` (at most kTargetGroup).  One unit = (target group, chunk).  Units of groups with at
+// of `group` (at most kWideGroup).  One unit = (target group, chunk).  Units of groups with at
 // most 32 targets are listed first, the wider ones after them, so kernels
 // specialised on the group width each get one contiguous range.  Every
 // target's chunk count is recorded so the combine step knows how many partial
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
 hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
                         int chunk_blocks, int group, Unit* units, int64_t max_units, int32_t* tchunks,
                         WsHeader* hdr, hipStream_t st) {
-  if (group < 1 || group > kTargetGroup) return hipErrorInvalidValue;
+  if (group < 1 || group > kWideGroup) return hipErrorInvalidValue;
   hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(kSchedThreads), 0, st, hoff, toff, R, n_hist, n_tgt,
                      chunk_blocks, group, units, max_units, tchunks, hdr);
   return hipGetLastError();

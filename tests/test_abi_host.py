@@ -152,3 +152,17 @@ def test_reordered_form_selection(monkeypatch):
     assert stca.stca_forward_launch_count(dims(), nohost) == 8 + 3 * n
     monkeypatch.setenv("STCA_ATTN", "standard")
     assert stca.stca_forward_launch_count(dims(), small) == 8 + 3 * n
+
+
+def test_wide_groups_selection(monkeypatch):
+    """A request with more than 64 targets switches the bf16 path to K/V
+    written once (9 + 2 n launches); STCA_KV=fused keeps the fused form."""
+    monkeypatch.delenv("STCA_ATTN", raising=False)
+    monkeypatch.delenv("STCA_KV", raising=False)
+    n = GOOD_DIMS["n_layers"]
+    many, keep = fake_batch([0, 400, 500], [0, 65, 70])
+    few, keep2 = fake_batch([0, 400, 500], [0, 64, 70])
+    assert stca.stca_forward_launch_count(dims(), many) == 9 + 2 * n
+    assert stca.stca_forward_launch_count(dims(), few) == 8 + 3 * n
+    monkeypatch.setenv("STCA_KV", "fused")
+    assert stca.stca_forward_launch_count(dims(), many) == 8 + 3 * n
