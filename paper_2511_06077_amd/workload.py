@@ -24,7 +24,13 @@ workload seed so that any subset of requests can be regenerated alone):
   ``X_r ~ N(0, 1)`` (L_r x d) and then its target rows ``x_t ~ N(0, 1)``
   (m_r x d);
 * upstream gradient of request r: ``default_rng([seed, 3, r])`` draws
-  ``G_r ~ N(0, 1)`` (m_r x d).
+  ``G_r ~ N(0, 1)`` (m_r x d);
+* weights of the paper-exact stack (Sec. 3.1): ``default_rng([seed, 4])``
+  draws, layer by layer, the SwiGLU block ``W_u, W_v ~ N(0, 1/d)`` (d x rd)
+  and ``W_o ~ N(0, 1/(rd))`` (rd x d) with r = ffn_mult, then
+  ``W_Q, W_K, W_V, W_O ~ N(0, 1/d)``; then ``W_C^(k) ~ N(0, 1/(k d))``
+  (k d x d) for k = 2..M, ``W_Z ~ N(0, 1/((M+1) d))`` and the head block's
+  ``W_u, W_v ~ N(0, 1/d)``, ``W_o ~ N(0, 1/(rd))``.
 
 All draws are float32 (``standard_normal(dtype=float32)``); bf16 workloads then
 round every value to bfloat16 with round-to-nearest-even.  The exact stored
@@ -40,6 +46,8 @@ from typing import Dict, Optional, Sequence
 import numpy as np
 
 WEIGHT_NAMES = ("wq", "wk", "wv", "wo", "w1", "w2")
+# weights of the paper-exact stack, in the order of the C structure
+PAPER_WEIGHT_NAMES = ("ffn_u", "ffn_v", "ffn_o", "wq", "wk", "wv", "wo", "wc", "wz", "z_u", "z_v", "z_o")
 
 
 @dataclasses.dataclass(frozen=True)
@@ -187,6 +195,45 @@ def make_weights(wl: Workload, scale_q: float = 1.0) -> Dict[str, np.ndarray]:
     if scale_q != 1.0:
         out["wq"] = out["wq"] * np.float32(scale_q)
     return {k: _store(v, wl.dtype) for k, v in out.items()}
+
+
+def make_paper_weights(wl: Workload) -> Dict[str, np.ndarray]:
+    """Seeded weights of the paper-exact stack (storage encoding)."""
+    d, rd, M = wl.d_model, wl.ffn_hidden, wl.n_layers
+    rng = np.random.default_rng([wl.seed, 4])
+
+    def n(rows, cols, fan_in):
+        return rng.standard_normal((rows, cols), dtype=np.float32) / np.float32(np.sqrt(fan_in))
+    ws = {k: [] for k in ("ffn_u", "ffn_v", "ffn_o", "wq", "wk", "wv", "wo")}
+    for _ in range(M):
+        ws["ffn_u"].append(n(d, rd, d))
+        ws["ffn_v"].append(n(d, rd, d))
+        ws["ffn_o"].append(n(rd, d, rd))
+        for k in ("wq", "wk", "wv", "wo"):
+            ws[k].append(n(d, d, d))
+    out = {k: np.stack(v) for k, v in ws.items()}
+    wc = [n(k * d, d, k * d) for k in range(2, M + 1)]
+    out["wc"] = np.concatenate(wc) if wc else np.zeros((0, d), dtype=np.float32)
+    out["wz"] = n((M + 1) * d, d, (M + 1) * d)
+    out["z_u"] = n(d, rd, d)
+    out["z_v"] = n(d, rd, d)
+    out["z_o"] = n(rd, d, rd)
+    return {k: _store(v, wl.dtype) for k, v in out.items()}
+
+
+def paper_f64(b: "Batch", weights: Dict[str, np.ndarray]) -> dict:
+    """Exact float64 view of a batch with paper-exact weights, as the oracle
+    takes it."""
+    out = {
+        "hist": b.decode(b.hist),
+        "tgt": b.decode(b.tgt),
+        "hist_off": b.hist_off.astype(np.int64),
+        "tgt_off": b.tgt_off.astype(np.int64),
+        "n_heads": b.wl.n_heads,
+    }
+    for k in PAPER_WEIGHT_NAMES:
+        out[k] = b.decode(weights[k])
+    return out
 
 
 def _request_rows(wl: Workload, r: int, L: int, m: int):
