@@ -214,6 +214,79 @@ stca_status_t stca_sl_allocate(int32_t n, const int32_t* l_full, const int32_t* 
 stca_status_t stca_sl_pack(int32_t n, const int32_t* full_off, const int32_t* l_keep, int32_t* hist_off,
                            int32_t* src_rows);
 
+/* ---- Paper-exact layer stack (Sec. 3.1, "Input encoding", "Multi-head
+ * target-to-history cross attention", "Stacking and target-conditioned
+ * fusion", "Prediction head and objective").  With M = n_layers, F =
+ * ffn_hidden (= r d, the SwiGLU width) and SwiGLUFFN(x) = ((x W_u) *
+ * (x W_v * sigmoid(x W_v))) W_o (Eq. swigluffn, no biases):
+ *   X~^(i)    = LN(SwiGLUFFN^(i)(X))                          every history row, i = 1..M
+ *   q^(1)     = LN(SwiGLUFFN^(1)(x_t))
+ *   o^(i)     = [heads of the cross attention of q^(i) onto X~^(i)] W_O^(i)   (Eq. layer-output)
+ *   q^(i+1)   = LN(SwiGLUFFN^(i+1)([o^(1) || ... || o^(i) || x_t] W_C^(i+1)))  (Eq. fuse)
+ *   z         = SwiGLUFFN_z([o^(1) || ... || o^(M) || x_t] W_Z)
+ * LN normalises each row over its d features (biased variance, eps 1e-5,
+ * unit scale, zero shift).  SwiGLUFFN^(i) is one block per layer, used for
+ * both the history and the query input of layer i.  The attention heads,
+ * scale and per-request sharing are those of stca_forward.
+ *
+ * Weights (storage dtype, row-major, y = x W):
+ *   ffn_u, ffn_v [M][d][F], ffn_o [M][F][d]   SwiGLUFFN^(1..M)
+ *   wq, wk, wv, wo [M][d][d]
+ *   wc   W_C^(2), ..., W_C^(M) one after the other, W_C^(k) being k d rows
+ *        x d (rows in concatenation order, x_t's block last); NULL when M = 1
+ *   wz   [(M+1) d][d]
+ *   z_u, z_v [d][F], z_o [F][d]              the head's SwiGLU block
+ * Shapes: as stca_forward (stca_path tells the kernel family); on the bf16
+ * MFMA path the history transform runs as one fused SwiGLU + LayerNorm kernel
+ * per layer (the hidden activations never leave the registers) and the
+ * transformed history is stored in bf16 for the attention; the generic path
+ * keeps everything in fp32.  The target-side blocks run on fp32 arithmetic. */
+typedef struct {
+  const void* ffn_u;
+  const void* ffn_v;
+  const void* ffn_o;
+  const void* wq;
+  const void* wk;
+  const void* wv;
+  const void* wo;
+  const void* wc;
+  const void* wz;
+  const void* z_u;
+  const void* z_v;
+  const void* z_o;
+} stca_paper_weights_t;
+
+/* Byte offsets into the optional `saved` buffer of stca_forward_paper, fp32:
+ * q [M][n_tgt][d] (the layer queries q^(i)), a [M][n_tgt][d] (head
+ * concatenation before W_O), o [n_tgt][M d] (row t = o^(1) || ... || o^(M)),
+ * lse [M][n_tgt][h] (natural log-sum-exp of each head's scores) and xt
+ * [M][n_hist][d] (the transformed histories X~^(i)). */
+typedef struct {
+  size_t q, a, o, lse, xt;
+  size_t total;
+} stca_paper_saved_layout_t;
+
+size_t stca_paper_workspace_size(const stca_dims_t* dims, const stca_batch_t* batch);
+size_t stca_paper_saved_size(const stca_dims_t* dims, const stca_batch_t* batch);
+stca_status_t stca_paper_saved_layout(const stca_dims_t* dims, const stca_batch_t* batch,
+                                      stca_paper_saved_layout_t* layout);
+
+/* Forward pass of the paper-exact stack: z [n_tgt][d] (storage dtype) for
+ * every target.  hist, tgt, z, saved and ws as in stca_forward, with
+ * ws_bytes >= stca_paper_workspace_size(dims, batch) and saved (nullable)
+ * of stca_paper_saved_size bytes.  Errors as for stca_forward. */
+stca_status_t stca_forward_paper(const stca_dims_t* dims, const stca_batch_t* batch,
+                                 const void* hist, const void* tgt, const stca_paper_weights_t* w,
+                                 void* z, void* saved, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/* Measurement variant of stca_forward_paper (events and labels as in
+ * stca_forward_profiled; n_events >= stca_paper_launch_count + 1). */
+int stca_paper_launch_count(const stca_dims_t* dims, const stca_batch_t* batch);
+stca_status_t stca_forward_paper_profiled(const stca_dims_t* dims, const stca_batch_t* batch,
+                                          const void* hist, const void* tgt, const stca_paper_weights_t* w,
+                                          void* z, void* saved, void* ws, size_t ws_bytes, hipStream_t stream,
+                                          hipEvent_t* events, int n_events, const char** labels);
+
 /* Reads (synchronising on `stream`) the status the device scheduler recorded
  * in `ws` during the last call that used it: STCA_OK or STCA_ERR_INVALID_ARG. */
 stca_status_t stca_device_status(const void* ws, hipStream_t stream);

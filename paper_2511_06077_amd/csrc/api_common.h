@@ -1,0 +1,132 @@
+// Host-side helpers shared by the C-ABI translation units: workspace
+// bump allocation, argument checks, the attention split size and optional
+// per-launch event recording.
+#pragma once
+
+#include <cstdint>
+#include <cstdlib>
+#include <cstring>
+
+#include "common.h"
+#include "internal.h"
+
+namespace stca {
+namespace api {
+
+constexpr size_t kAlign = 256;
+
+struct Bump {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    size_t o = off;
+    off = round_up(static_cast<int64_t>(off + bytes), kAlign);
+    return o;
+  }
+};
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// 1 = bf16 MFMA path, 0 = generic, <0 = status
+inline int path_of(const stca_dims_t* d) {
+  if (!d) return STCA_ERR_INVALID_ARG;
+  if (d->d_model <= 0 || d->n_heads <= 0 || d->n_layers <= 0 || d->ffn_hidden <= 0 ||
+      d->d_model % d->n_heads != 0 || (d->dtype != STCA_F32 && d->dtype != STCA_BF16))
+    return STCA_ERR_INVALID_ARG;
+  const int dh = d->d_model / d->n_heads;
+  if (d->ffn_hidden % 32 != 0) return STCA_ERR_UNSUPPORTED;
+  if (d->dtype == STCA_BF16 && dh == 32 && (d->d_model == 64 || d->d_model == 128 || d->d_model == 256) &&
+      d->ffn_hidden % 256 == 0)
+    return 1;
+  if (dh == 8 || dh == 16 || dh == 32 || dh == 64) return 0;
+  return STCA_ERR_UNSUPPORTED;
+}
+
+inline stca_status_t check_batch(const stca_batch_t* b) {
+  if (!b || b->n_requests < 1 || b->n_hist < 0 || b->n_tgt < 0 || b->n_hist >= (int64_t(1) << 31) ||
+      b->n_tgt >= (int64_t(1) << 31) || !b->hist_off || !b->tgt_off)
+    return STCA_ERR_INVALID_ARG;
+  if ((b->hist_off_host == nullptr) != (b->tgt_off_host == nullptr)) return STCA_ERR_INVALID_ARG;
+  if (b->hist_off_host) {
+    const int32_t *h = b->hist_off_host, *t = b->tgt_off_host;
+    if (h[0] != 0 || t[0] != 0 || h[b->n_requests] != b->n_hist || t[b->n_requests] != b->n_tgt)
+      return STCA_ERR_INVALID_ARG;
+    for (int r = 0; r < b->n_requests; ++r) {
+      if (h[r + 1] < h[r] || t[r + 1] < t[r]) return STCA_ERR_INVALID_ARG;
+      if (t[r + 1] > t[r] && h[r + 1] == h[r]) return STCA_ERR_INVALID_ARG;
+    }
+  }
+  return STCA_OK;
+}
+
+inline int device_cus() {
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+// Chunk length (in 32-row blocks) of the split over history rows: aim at about
+// `per_cu` attention units per CU (four for the standard form; one for the
+// reordered form, whose units stream X with little work per block and whose
+// merge cost grows with the chunk count).  STCA_CHUNK_BLOCKS overrides it (a
+// tuning and testing knob: forcing small chunks exercises the partial-result
+// merge).
+inline int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu) {
+  if (const char* e = std::getenv("STCA_CHUNK_BLOCKS")) {
+    int v = std::atoi(e);
+    if (v >= 1) return v;
+  }
+  const int64_t nb = ceil_div(b->n_hist, kBlockTokens);
+  int64_t c = ceil_div(nb, per_cu * static_cast<int64_t>(n_cu));
+  if (c < 8) c = 8;
+  if (c > (1 << 20)) c = 1 << 20;
+  return static_cast<int>(c);
+}
+
+inline int64_t max_units_for(const stca_batch_t* b, int chunk_blocks, int group) {
+  if (b->hist_off_host)
+    return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks, group);
+  return (ceil_div(b->n_tgt, group) + b->n_requests) * kMaxChunks;
+}
+
+template <typename T>
+inline T* at(void* base, size_t off) {
+  return reinterpret_cast<T*>(static_cast<char*>(base) + off);
+}
+template <typename T>
+inline const T* at(const void* base, size_t off) {
+  return reinterpret_cast<const T*>(static_cast<const char*>(base) + off);
+}
+
+// Optional per-launch event recording for measurement: ev[0] is recorded
+// before the first launch and ev[k+1] right after launch k.
+struct Rec {
+  hipEvent_t* ev = nullptr;
+  int n = 0, k = 0;
+  const char** labels = nullptr;
+  hipStream_t st = nullptr;
+  hipError_t start() {
+    if (!ev) return hipSuccess;
+    if (k >= n) return hipErrorInvalidValue;
+    return hipEventRecord(ev[k++], st);
+  }
+  hipError_t mark(const char* name) {
+    if (!ev) return hipSuccess;
+    if (k >= n) return hipErrorInvalidValue;
+    if (labels) labels[k - 1] = name;
+    return hipEventRecord(ev[k++], st);
+  }
+};
+
+#define HIPCHK(x)                             \
+  do {                                        \
+    if ((x) != hipSuccess) return STCA_ERR_HIP; \
+  } while (0)
+
+}  // namespace api
+}  // namespace stca

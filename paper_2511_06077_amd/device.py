@@ -104,3 +104,58 @@ class DeviceBatch:
                            g["dhist"], g["dtgt"], dw, self.bws, self.bws_bytes,
                            self.stream() if stream is None else stream)
         return g
+
+
+class PaperDeviceBatch:
+    """A batch with paper-exact weights on the GPU, for stca_forward_paper."""
+
+    def __init__(self, b: Batch, weights: dict, device="cuda", keep_saved: bool = False,
+                 host_offsets: bool = True):
+        torch = _torch()
+        self.b = b
+        wl = b.wl
+        self.device = torch.device(device)
+        self.bf16 = wl.dtype == "bf16"
+        self.sdtype = torch.bfloat16 if self.bf16 else torch.float32
+        self.hist = to_device(b.hist, device)
+        self.tgt = to_device(b.tgt, device)
+        self.w = {k: (to_device(v, device) if v.size else None) for k, v in weights.items()}
+        self.hoff_h = np.ascontiguousarray(b.hist_off, dtype=np.int32)
+        self.toff_h = np.ascontiguousarray(b.tgt_off, dtype=np.int32)
+        self.hoff = torch.from_numpy(self.hoff_h).to(device)
+        self.toff = torch.from_numpy(self.toff_h).to(device)
+        self.dims = stca.dims(wl.d_model, wl.n_heads, wl.n_layers, wl.ffn_hidden,
+                              stca.STCA_BF16 if self.bf16 else stca.STCA_F32)
+        self.batch = stca.batch(b.n_requests, b.n_hist, b.n_tgt_total, self.hoff, self.toff,
+                                self.hoff_h if host_offsets else None, self.toff_h if host_offsets else None)
+        self.weights = stca.paper_weights(**self.w)
+        self.z = torch.empty((b.n_tgt_total, wl.d_model), dtype=self.sdtype, device=device)
+        self.ws_bytes = stca.stca_paper_workspace_size(self.dims, self.batch)
+        if self.ws_bytes == 0:
+            raise stca.StcaError(stca.STCA_ERR_INVALID_ARG, "stca_paper_workspace_size")
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        self.saved = None
+        if keep_saved:
+            self.saved = torch.empty(stca.stca_paper_saved_size(self.dims, self.batch), dtype=torch.uint8,
+                                     device=device)
+            self.layout = stca.stca_paper_saved_layout(self.dims, self.batch)
+
+    def stream(self):
+        return _torch().cuda.current_stream(self.device).cuda_stream
+
+    def forward(self, stream: Optional[int] = None):
+        stca.stca_forward_paper(self.dims, self.batch, self.hist, self.tgt, self.weights, self.z, self.saved,
+                                self.ws, self.ws_bytes, self.stream() if stream is None else stream)
+        return self.z
+
+    def saved_tensor(self, name: str):
+        """q, a -> [n, N_tgt, d]; o -> [N_tgt, n, d]; lse -> [n, N_tgt, h];
+        xt -> [n, N_hist, d] (fp32)."""
+        torch = _torch()
+        wl = self.b.wl
+        n, nt, nh, d = wl.n_layers, self.b.n_tgt_total, self.b.n_hist, wl.d_model
+        shape = {"q": (n, nt, d), "a": (n, nt, d), "o": (nt, n, d), "lse": (n, nt, wl.n_heads),
+                 "xt": (n, nh, d)}[name]
+        off = getattr(self.layout, name)
+        count = int(np.prod(shape))
+        return self.saved[off:off + 4 * count].view(torch.float32).view(*shape)

@@ -19,7 +19,10 @@ STCA_F32, STCA_BF16 = 0, 1
 EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca_forward", "stca_backward",
             "stca_device_status", "stca_status_string", "stca_path", "stca_forward_launch_count",
             "stca_forward_profiled", "stca_backward_launch_count", "stca_backward_profiled",
-            "stca_sl_beta", "stca_sl_sample", "stca_sl_allocate", "stca_sl_pack")
+            "stca_sl_beta", "stca_sl_sample", "stca_sl_allocate", "stca_sl_pack",
+            "stca_paper_workspace_size", "stca_paper_saved_size", "stca_paper_saved_layout", "stca_forward_paper",
+            "stca_paper_launch_count", "stca_forward_paper_profiled")
+PAPER_WEIGHT_FIELDS = ("ffn_u", "ffn_v", "ffn_o", "wq", "wk", "wv", "wo", "wc", "wz", "z_u", "z_v", "z_o")
 
 
 class stca_dims_t(ctypes.Structure):
@@ -43,6 +46,14 @@ class stca_wgrads_t(ctypes.Structure):
 
 class stca_saved_layout_t(ctypes.Structure):
     _fields_ = [(k, ctypes.c_size_t) for k in ("s", "a", "u", "lse", "total")]
+
+
+class stca_paper_weights_t(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_void_p) for k in PAPER_WEIGHT_FIELDS]
+
+
+class stca_paper_saved_layout_t(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_size_t) for k in ("q", "a", "o", "lse", "xt", "total")]
 
 
 class StcaError(RuntimeError):
@@ -113,6 +124,23 @@ def lib():
         L.stca_sl_allocate.argtypes = [ctypes.c_int32, I32P, I32P, ctypes.c_int64, I32P]
         L.stca_sl_pack.restype = ctypes.c_int
         L.stca_sl_pack.argtypes = [ctypes.c_int32, I32P, I32P, I32P, I32P]
+        L.stca_paper_workspace_size.restype = ctypes.c_size_t
+        L.stca_paper_workspace_size.argtypes = [P(stca_dims_t), P(stca_batch_t)]
+        L.stca_paper_saved_size.restype = ctypes.c_size_t
+        L.stca_paper_saved_size.argtypes = [P(stca_dims_t), P(stca_batch_t)]
+        L.stca_paper_saved_layout.restype = ctypes.c_int
+        L.stca_paper_saved_layout.argtypes = [P(stca_dims_t), P(stca_batch_t), P(stca_paper_saved_layout_t)]
+        L.stca_forward_paper.restype = ctypes.c_int
+        L.stca_forward_paper.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                         P(stca_paper_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_size_t, ctypes.c_void_p]
+        L.stca_paper_launch_count.restype = ctypes.c_int
+        L.stca_paper_launch_count.argtypes = [P(stca_dims_t), P(stca_batch_t)]
+        L.stca_forward_paper_profiled.restype = ctypes.c_int
+        L.stca_forward_paper_profiled.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                                  P(stca_paper_weights_t), ctypes.c_void_p, ctypes.c_void_p,
+                                                  ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                                  P(ctypes.c_void_p), ctypes.c_int, P(ctypes.c_char_p)]
         _lib = L
     return _lib
 
@@ -220,6 +248,49 @@ def stca_backward_profiled(d, b, hist, tgt, w, dout, dhist, dtgt, dw, ws, ws_byt
                                       _ptr(stream), events, len(events), labels)
     if st != STCA_OK:
         raise StcaError(st, "stca_backward_profiled")
+    return st
+
+
+# ---- paper-exact stack
+def paper_weights(**w) -> stca_paper_weights_t:
+    """Keyword arguments named as PAPER_WEIGHT_FIELDS (wc may be None for one layer)."""
+    return stca_paper_weights_t(*(_ptr(w.get(k)) for k in PAPER_WEIGHT_FIELDS))
+
+
+def stca_paper_workspace_size(d: stca_dims_t, b: stca_batch_t) -> int:
+    return lib().stca_paper_workspace_size(ctypes.byref(d), ctypes.byref(b))
+
+
+def stca_paper_saved_size(d: stca_dims_t, b: stca_batch_t) -> int:
+    return lib().stca_paper_saved_size(ctypes.byref(d), ctypes.byref(b))
+
+
+def stca_paper_saved_layout(d: stca_dims_t, b: stca_batch_t) -> stca_paper_saved_layout_t:
+    out = stca_paper_saved_layout_t()
+    st = lib().stca_paper_saved_layout(ctypes.byref(d), ctypes.byref(b), ctypes.byref(out))
+    if st != STCA_OK:
+        raise StcaError(st, "stca_paper_saved_layout")
+    return out
+
+
+def stca_forward_paper(d, b, hist, tgt, w, z, saved, ws, ws_bytes: int, stream=None, check: bool = True) -> int:
+    st = lib().stca_forward_paper(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w), _ptr(z),
+                                  _ptr(saved), _ptr(ws), int(ws_bytes), _ptr(stream))
+    if check and st != STCA_OK:
+        raise StcaError(st, "stca_forward_paper")
+    return st
+
+
+def stca_paper_launch_count(d: stca_dims_t, b: stca_batch_t) -> int:
+    return lib().stca_paper_launch_count(ctypes.byref(d), ctypes.byref(b))
+
+
+def stca_forward_paper_profiled(d, b, hist, tgt, w, z, saved, ws, ws_bytes: int, stream, events, labels=None) -> int:
+    st = lib().stca_forward_paper_profiled(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w),
+                                           _ptr(z), _ptr(saved), _ptr(ws), int(ws_bytes), _ptr(stream), events,
+                                           len(events), labels)
+    if st != STCA_OK:
+        raise StcaError(st, "stca_forward_paper_profiled")
     return st
 
 

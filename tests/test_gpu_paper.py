@@ -1,0 +1,146 @@
+"""GPU parity of the paper-exact stack (stca_forward_paper through the C ABI)
+against the fp64 paper oracle on the same seeded inputs.
+
+Compared: the head token z, and per layer the transformed history X~^(i), the
+query q^(i), the head concatenation a^(i), the layer summary o^(i) and the
+log-sum-exp.  Metric and bars as for the configuration-mode forward (per-row
+max-norm error; 1e-4 with fp32 storage, 2e-2 with bf16 storage).
+"""
+import numpy as np
+import pytest
+
+from oracle import stca_paper_oracle as P
+from paper_2511_06077_amd import workload as W
+from test_gpu_forward import TOL, rowerr
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    assert t.cuda.is_available(), "GPU tests need a GPU"
+    return t
+
+
+@pytest.fixture
+def chunk_override(monkeypatch):
+    def set_(v):
+        if v is None:
+            monkeypatch.delenv("STCA_CHUNK_BLOCKS", raising=False)
+        else:
+            monkeypatch.setenv("STCA_CHUNK_BLOCKS", str(v))
+    return set_
+
+
+def run_paper(torch, b, weights, keep_saved=True, host_offsets=True):
+    from paper_2511_06077_amd.device import PaperDeviceBatch
+    db = PaperDeviceBatch(b, weights, keep_saved=keep_saved, host_offsets=host_offsets)
+    z = db.forward()
+    torch.cuda.synchronize()
+    out = {"z": z.float().cpu().numpy().astype(np.float64)}
+    if keep_saved:
+        for k in ("q", "a", "o", "lse", "xt"):
+            out[k] = db.saved_tensor(k).cpu().numpy().astype(np.float64)
+    return out, db
+
+
+def check(b, weights, got, tol, tgt_rows=None, hist_rows=None, requests=None):
+    """Compare against the oracle; with `requests`, the oracle runs on those
+    requests alone (their rows tgt_rows / hist_rows of the GPU batch)."""
+    if requests is None:
+        ref = P.forward_paper(W.paper_f64(b, weights))
+        tgt_rows = slice(None)
+        hist_rows = slice(None)
+    else:
+        sub = W.make_batch(b.wl, requests=requests)
+        ref = P.forward_paper(W.paper_f64(sub, weights))
+    M = b.wl.n_layers
+    e = {"z": rowerr(got["z"][tgt_rows], ref["z"])}
+    if "a" in got:
+        e["a"] = max(rowerr(got["a"][i][tgt_rows], ref["a"][i]) for i in range(M))
+        e["q"] = max(rowerr(got["q"][i][tgt_rows], ref["q"][i]) for i in range(M))
+        e["o"] = max(rowerr(got["o"][tgt_rows, i], ref["o"][i]) for i in range(M))
+        e["xt"] = max(rowerr(got["xt"][i][hist_rows], ref["xt"][i]) for i in range(M))
+        e["lse"] = float(np.abs(got["lse"][:, tgt_rows] - ref["lse"]).max()) if ref["lse"].size else 0.0
+    print(f"[paper parity] {b.wl.name}: " + " ".join(f"err({k})={v:.2e}" for k, v in e.items()), flush=True)
+    for k, v in e.items():
+        assert v <= (50 * tol if k == "lse" else tol), (k, v)
+
+
+EDGE_L = [1, 7, 31, 32, 33, 63, 65, 200, 1023, 1, 40, 64, 129]
+EDGE_M = [1, 17, 0, 64, 33, 32, 1, 15, 2, 0, 31, 16, 70]
+
+
+@pytest.mark.parametrize("dtype,d,h,n,F", [("bf16", 256, 8, 2, 1024), ("bf16", 128, 4, 3, 512),
+                                           ("bf16", 64, 2, 1, 256), ("f32", 64, 2, 2, 256),
+                                           ("f32", 32, 2, 3, 64)])
+@pytest.mark.parametrize("chunk", [None, 1])
+def test_paper_edge_parity(torch, chunk_override, dtype, d, h, n, F, chunk):
+    """Ragged tails (history lengths not multiples of 32, 0..70 targets per
+    request, empty target segments) on both kernel families."""
+    chunk_override(chunk)
+    b = W.make_custom_batch("paper_edge", EDGE_L, EDGE_M, d_model=d, n_heads=h, n_layers=n, dtype=dtype, seed=61)
+    b.wl = W.Workload(b.wl.name, b.wl.n_requests, d, h, n, dtype, b.wl.seed, ffn_mult=F // d)
+    weights = W.make_paper_weights(b.wl)
+    got, db = run_paper(torch, b, weights)
+    from paper_2511_06077_amd import stca
+    assert stca.stca_path(db.dims) == (1 if dtype == "bf16" else 0)
+    check(b, weights, got, TOL[dtype])
+
+
+def test_paper_device_offsets(torch):
+    """Without host offsets (device scheduler only) the result is the same."""
+    b = W.make_custom_batch("paper_dev", [300, 64, 1000], [5, 40, 1], d_model=256, n_heads=8, n_layers=2,
+                            dtype="bf16", seed=62)
+    weights = W.make_paper_weights(b.wl)
+    got, _ = run_paper(torch, b, weights, keep_saved=False, host_offsets=False)
+    got2, _ = run_paper(torch, b, weights, keep_saved=False, host_offsets=True)
+    # the same kernels either way (split-K sums may round differently)
+    assert rowerr(got["z"], got2["z"]) <= 1e-2
+    check(b, weights, got, TOL["bf16"])
+
+
+def test_paper_headline_shape_sampled(torch):
+    """128 requests x 32 targets, L = 10240, d = 256, 8 heads, 4 layers, r = 4
+    (bf16), in the benchmark's launch configuration; the oracle checks two
+    sampled requests (requests are independent)."""
+    from paper_2511_06077_amd.device import PaperDeviceBatch
+    wl = W.WORKLOADS[W.HEADLINE]
+    b = W.make_batch(wl)
+    weights = W.make_paper_weights(wl)
+    db = PaperDeviceBatch(b, weights, keep_saved=True)
+    z = db.forward()
+    torch.cuda.synchronize()
+    np64 = lambda x: x.float().cpu().numpy().astype(np.float64)  # noqa: E731
+    for r in (5, 127):
+        t0, t1 = int(b.tgt_off[r]), int(b.tgt_off[r + 1])
+        h0, h1 = int(b.hist_off[r]), int(b.hist_off[r + 1])
+        got = {"z": np64(z[t0:t1]), "q": np64(db.saved_tensor("q")[:, t0:t1]),
+               "a": np64(db.saved_tensor("a")[:, t0:t1]), "o": np64(db.saved_tensor("o")[t0:t1]),
+               "lse": np64(db.saved_tensor("lse")[:, t0:t1]), "xt": np64(db.saved_tensor("xt")[:, h0:h1])}
+        check(b, weights, got, TOL["bf16"], tgt_rows=slice(None), hist_rows=slice(None), requests=[r])
+
+
+def test_paper_profiled_labels(torch):
+    from paper_2511_06077_amd import stca
+    b = W.make_custom_batch("paper_prof", [100, 37], [3, 9], d_model=128, n_heads=4, n_layers=3, dtype="bf16",
+                            seed=63)
+    weights = W.make_paper_weights(b.wl)
+    from paper_2511_06077_amd.device import PaperDeviceBatch
+    db = PaperDeviceBatch(b, weights)
+    n = stca.stca_paper_launch_count(db.dims, db.batch)
+    ev = stca.HipEvents(n + 1)
+    try:
+        stca.stca_forward_paper_profiled(db.dims, db.batch, db.hist, db.tgt, db.weights, db.z, None, db.ws,
+                                         db.ws_bytes, db.stream(), ev.ev, ev.labels)
+        torch.cuda.synchronize()
+        labels = [ev.label(k) for k in range(n)]
+        assert labels.count("swiglu_ln") == 3 and "?" not in labels
+        assert all(ev.elapsed_ms(0, k + 1) >= 0 for k in range(n))
+        z1 = db.z.float().cpu().numpy()
+        db.forward()
+        torch.cuda.synchronize()
+        assert np.array_equal(z1, db.z.float().cpu().numpy())
+    finally:
+        ev.close()
