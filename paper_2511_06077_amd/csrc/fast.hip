@@ -198,6 +198,27 @@ __global__ __launch_bounds__(64 * (D / 32)) void proj_kernel(const bf16_bits* __
   }
 }
 
+// Combine a value of lane l with that of lane l ^ 32 (v_permlane32_swap: a
+// VALU exchange between the two halves of the wave, no LDS round trip).
+__device__ __forceinline__ float max_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float sum_halves(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// Row order inside a 32-row history block as the fused kernel reads it from
+// LDS: MFMA row index i is history row RPS * (i % (32 / RPS)) + i / (32 / RPS)
+// (RPS = 1: identity).  With RPS rows per 1 KB LDS segment this sends the
+// eight lanes of each LDS read phase to eight different segments, i.e. to
+// distinct bank groups.
+template <int RPS>
+__device__ __forceinline__ int blk_row(int i) {
+  return RPS * (i % (32 / RPS)) + i / (32 / RPS);
+}
+
 // ------------------------------------------ online softmax over blocks
 // State of one wave (one head) for all of a unit's targets (up to 64: two
 // 32-wide column groups).  Online softmax in log2 units; the result is an
@@ -224,7 +245,9 @@ struct Online {
     }
   }
 
-  // kv: K slices 0, 1 and V slices 0, 1 of history block b (operand order)
+  // kv: K slices 0, 1 and V slices 0, 1 of history block b (operand order).
+  // MFMA row index i of the block holds history row b * 32 + blk_row<RPS>(i).
+  template <int RPS = 1>
   __device__ __forceinline__ void step(const f16x8 (&kv)[4], int b, const Unit& un, int hi) {
     const bool full = b * 32 >= un.l0 && b * 32 + 32 <= un.l1;
 #pragma unroll
@@ -234,14 +257,14 @@ struct Online {
       if (!full) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int tok = b * 32 + 8 * (v / 4) + 4 * hi + (v % 4);
+          const int tok = b * 32 + blk_row<RPS>(8 * (v / 4) + 4 * hi + (v % 4));
           if (tok < un.l0 || tok >= un.l1) s[v] = -INFINITY;
         }
       }
       float bm = s[0];
 #pragma unroll
       for (int v = 1; v < 16; ++v) bm = fmaxf(bm, s[v]);
-      bm = fmaxf(bm, __shfl_xor(bm, 32));
+      bm = max_halves(bm);
       // Threshold rescaling: the reference maximum m only moves when some
       // score of the wave exceeds it by more than kSlack (log2 units), so the
       // weights 2^(s - m) stay <= 2^kSlack (fine in fp16 and in the fp32 sums)
@@ -271,7 +294,7 @@ struct Online {
     constexpr int D = H * DH;
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
-      const float lt = l[g] + __shfl_xor(l[g], 32);
+      const float lt = sum_halves(l[g]);
       const int tt = g * 32 + tcol;
       if (tt < un.nt) {
         const int64_t row = (int64_t)un.c * n_tgt + un.t0 + tt;
@@ -341,67 +364,62 @@ __global__ __launch_bounds__(64 * H) void attn_kernel(const Unit* __restrict__ u
 // layer's K and V inside the kernel and consumed from registers: nothing is
 // written to HBM, and the history is read once per layer instead of K and V
 // being written once and read back.  One wave per head keeps its W_K and W_V
-// columns in registers for the whole (persistent) kernel; the workgroup
-// stages each X block through a double-buffered LDS tile shared by all heads.
-// The projection's result registers are exactly the attention's operand
-// order (see the layout note at the top), so they are converted to fp16 in
-// place and fed to the score and P.V MFMAs.
-template <int H, int NG>
-__device__ __forceinline__ void fused_unit(const Unit& un, const f16x8* __restrict__ QN,
-                                           const bf16_bits* __restrict__ X, int64_t n_hist,
-                                           const bf16x8 (&wk)[H * DH / 16], const bf16x8 (&wv)[H * DH / 16],
-                                           bf16_bits (*xs)[32 * (H * DH + 8)], float* __restrict__ part_acc,
-                                           float2* __restrict__ part_ml, int64_t n_tgt) {
-  constexpr int D = H * DH;
-  constexpr int KS = D / 16;
-  constexpr int ROW = D + 8;
-  constexpr int NT = 64 * H;
-  const int j = threadIdx.x / 64, lane = threadIdx.x % 64;
-  const int tcol = lane % 32, hi = lane / 32;
-  auto load = [&](int64_t b, uint4 (&r)[2]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = threadIdx.x + i * NT;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      const int64_t grow = b * 32 + row;
-      r[i] = grow < n_hist ? *reinterpret_cast<const uint4*>(X + grow * D + col8 * 8) : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto stash = [&](int buf, const uint4 (&r)[2]) {
-#pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const int c = threadIdx.x + i * NT;
-      const int row = c / (D / 8), col8 = c % (D / 8);
-      *reinterpret_cast<uint4*>(&xs[buf][row * ROW + col8 * 8]) = r[i];
-    }
-  };
-  Online<H, NG> st;
-  st.init(un, QN, j, tcol, hi);
-  uint4 nxt[2];
-  load(un.b0, nxt);
-  stash(0, nxt);
-  __syncthreads();
-  for (int b = un.b0; b < un.b1; ++b) {
-    const int cur = (b - un.b0) & 1;
-    if (b + 1 < un.b1) load(b + 1, nxt);
-    f32x16 ak = {}, av = {};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 xo = *reinterpret_cast<const bf16x8*>(&xs[cur][tcol * ROW + ks * 16 + hi * 8]);
-      ak = mfma(wk[ks], xo, ak);
-      av = mfma(xo, wv[ks], av);
-    }
-    const f16x8 kv[4] = {pack8h(ak, 0), pack8h(ak, 8), pack8h(av, 0), pack8h(av, 8)};
-    st.step(kv, b, un, hi);
-    if (b + 1 < un.b1) stash(cur ^ 1, nxt);
-    __syncthreads();
-  }
-  st.finish(un, j, tcol, hi, part_acc, part_ml, n_tgt);
+// columns in registers for the whole (persistent) kernel.  The projection's
+// result registers are exactly the attention's operand order (see the layout
+// note at the top), so they are converted to fp16 in place and fed to the
+// score and P.V MFMAs.
+//
+// The workgroup walks its units' blocks as one stream.  X blocks arrive by
+// direct global-to-LDS loads into a ring of kStages tiles, kStages - 1 blocks
+// ahead of the one in use (each wave loads two 1 KB segments of a block and
+// waits only for its own older loads; one barrier per block publishes the
+// tile and frees the slot read in the previous block).  A unit's queries
+// arrive the same way, one block ahead of the unit's first block, into one
+// of two LDS areas per wave (its head's slice).  No other global load is
+// issued inside the loop, so nothing else waits on the loads in flight.
+//
+// The per-block work is MFMA-heavy (the projection: 2 KS MFMAs per wave) and
+// then VALU-heavy (the softmax).  The two waves that share a SIMD run it
+// half a block out of phase: a wave of phase 0 projects block k and attends
+// to it; a wave of phase 1 first attends to block k - 1 (its K/V kept in
+// registers across the barrier), then projects block k.  So while one wave
+// of a SIMD is in its softmax, the other keeps the matrix core busy.  The
+// phase comes from each wave's rank among the workgroup's waves on its SIMD
+// (hardware SIMD id), whatever order the dispatcher assigned them in.
+constexpr int kStages = 4;
+constexpr int kSegPitch = 1024 + 16;  // one direct-load segment (64 lanes x 16 B) plus padding
+
+// s_waitcnt on vector memory: at most n (rounded down to even, <= 6) of this
+// wave's vector memory operations still outstanding; LDS operations drained.
+__device__ __forceinline__ void wait_vm(int n) {
+  // gfx9 immediate: vmcnt[3:0], expcnt[6:4] = 7 (no wait), lgkmcnt[11:8] = 0
+  if (n >= 6)
+    __builtin_amdgcn_s_waitcnt(0x0076);
+  else if (n >= 4)
+    __builtin_amdgcn_s_waitcnt(0x0074);
+  else if (n >= 2)
+    __builtin_amdgcn_s_waitcnt(0x0072);
+  else
+    __builtin_amdgcn_s_waitcnt(0x0070);
 }
 
-// Instantiated once per target-group width NG (units with up to 32 targets,
-// and units with 33..64), so each variant gets its own register allocation;
-// the scheduler lists each width's units as one contiguous range.
+// Direct global-to-LDS load of 16 bytes per lane: lane i's bytes land at
+// lds + 16 i (lds wave-uniform).  Issued as inline assembly so that the
+// compiler does not treat every later LDS read as possibly aliasing it (it
+// would wait for all loads in flight before each read); the kernel waits for
+// these loads itself (wait_vm).  The compiler's own vector-memory waits only
+// become more conservative, as the counter retires operations in order.
+__device__ __forceinline__ void dma16(const void* src, const unsigned char* lds) {
+  const uint32_t m0 =
+      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) unsigned char*)lds));
+  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(__builtin_amdgcn_readfirstlane(m0)));
+}
+
+// Workgroup barrier without the fences of __syncthreads (whose release would
+// wait for every load in flight, including the ring's prefetches); the memory
+// clobber keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void ring_barrier() { asm volatile("s_barrier" ::: "memory"); }
+
 template <int D, int NG>
 __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __restrict__ units,
                                                               const WsHeader* __restrict__ hdr,
@@ -413,12 +431,34 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
                                                               float2* __restrict__ part_ml, int64_t n_tgt) {
   constexpr int H = D / DH;
   constexpr int KS = D / 16;
-  __shared__ __attribute__((aligned(16))) bf16_bits xs[2][32 * (D + 8)];
+  constexpr int CPR = D / 8;        // 16-byte chunks per history row
+  constexpr int RPS = 64 / CPR;     // rows per 1 KB segment
+  constexpr int NS = 32 / RPS;      // segments per block (2 per wave)
+  constexpr int TILE = NS * kSegPitch;
+  constexpr int QA = NG * 32 * DH * 2;  // one wave's query slice of a unit (bytes)
+  static_assert(NS == 2 * H, "two segments per wave");
+  __shared__ __attribute__((aligned(16))) unsigned char xs[kStages * TILE];
+  __shared__ __attribute__((aligned(16))) unsigned char qs[2 * H * QA];
+  __shared__ int simd_waves[4];
+
   // this width's units: [0, n_narrow) or [n_narrow, n_units)
   const int ub = NG == 1 ? 0 : hdr->n_narrow;
   const int ue = NG == 1 ? hdr->n_narrow : hdr->n_units;
   if (ub + static_cast<int>(blockIdx.x) >= ue) return;
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tcol = lane % 32, hi = lane / 32;
+
+  if (threadIdx.x < 4) simd_waves[threadIdx.x] = 0;
+  __syncthreads();
+  int phase;
+  {
+    int simd;
+    asm volatile("s_getreg_b32 %0, hwreg(HW_REG_HW_ID, 4, 2)" : "=s"(simd));
+    int rank = 0;
+    if (lane == 0) rank = atomicAdd(&simd_waves[simd & 3], 1);
+    phase = __shfl(rank, 0) & 1;
+  }
+
   bf16x8 wk[KS], wv[KS];
   {
     const bf16x8* pk = WkP + ((int64_t)(layer * H + wave) * KS) * 64 + lane;
@@ -429,8 +469,157 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
       wv[ks] = pv[ks * 64];
     }
   }
-  for (int u = ub + blockIdx.x; u < ue; u += gridDim.x)
-    fused_unit<H, NG>(units[u], QN, X, n_hist, wk, wv, xs, part_acc, part_ml, n_tgt);
+
+  // ---- loads: this wave's parts of the ring's blocks and of the query slices
+  int lu = ub + blockIdx.x;  // load cursor: next (unit, block) to bring in
+  Unit lun = units[lu];
+  int lb = lun.b0;
+  int p_load = 0;   // blocks issued so far
+  int q_after = 0;  // blocks issued after the latest query slice
+  auto issue_x = [&]() {
+    if (lu >= ue) return;
+    unsigned char* slot = xs + (p_load % kStages) * TILE;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int seg = 2 * wave + i;
+      const int e = seg * 64 + lane;  // 16-byte chunk of the block
+      const int64_t grow = min((int64_t)lb * 32 + e / CPR, n_hist - 1);
+      dma16(X + grow * D + (e % CPR) * 8, slot + seg * kSegPitch);
+    }
+    ++p_load;
+    ++q_after;
+    if (++lb >= lun.b1) {
+      lu += gridDim.x;
+      if (lu < ue) {
+        lun = units[lu];
+        lb = lun.b0;
+      }
+    }
+  };
+  // queries of unit un (the ord-th of this workgroup): target rows of 64 bytes
+  // (this head's 32 fp16, QN order), 16 targets per wave load
+  auto issue_q = [&](const Unit& un, int ord) {
+    unsigned char* area = qs + ((ord & 1) * H + wave) * QA;
+#pragma unroll
+    for (int i = 0; i < 2 * NG; ++i) {
+      const int64_t t = min((int64_t)un.t0 + i * 16 + lane / 4, n_tgt - 1);
+      dma16(reinterpret_cast<const unsigned char*>(QN) + (t * D + wave * DH) * 2 + (lane % 4) * 16, area + i * 1024);
+    }
+    q_after = 0;
+  };
+  issue_q(lun, 0);
+#pragma unroll
+  for (int i = 0; i < kStages - 1; ++i) issue_x();
+  wait_vm(0);  // the weights are in registers (the loop issues no compiler-visible load)
+
+  // this lane's B operand row: MFMA column tcol reads history row blk_row<RPS>(tcol)
+  const int xrow = (tcol % NS) * kSegPitch + (tcol / NS) * (2 * D) + 16 * hi;
+  // The X operands are read kXAhead k-steps ahead of their MFMAs (scheduling
+  // barriers keep the compiler from sinking the reads next to their use), so
+  // an LDS round trip overlaps 2 kXAhead MFMAs of the same wave.
+  constexpr int kXAhead = 4;
+  auto project = [&](const unsigned char* tile, f16x8 (&kv)[4]) {
+    f32x16 ak = {}, av = {};
+    const unsigned char* xp = tile + xrow;
+    bf16x8 xo[kXAhead];
+#pragma unroll
+    for (int i = 0; i < kXAhead; ++i) xo[i] = *reinterpret_cast<const bf16x8*>(xp + 32 * i);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 x = xo[ks % kXAhead];
+      if (ks + kXAhead < KS) xo[ks % kXAhead] = *reinterpret_cast<const bf16x8*>(xp + 32 * (ks + kXAhead));
+      ak = mfma(wk[ks], x, ak);  // K^T block: rows = head dims, cols = history rows
+      av = mfma(x, wv[ks], av);  // V block:   rows = history rows, cols = head dims
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    kv[0] = pack8h(ak, 0);
+    kv[1] = pack8h(ak, 8);
+    kv[2] = pack8h(av, 0);
+    kv[3] = pack8h(av, 8);
+  };
+
+  // One wave's walk over the stream; PHASE 1 attends to each block one barrier
+  // step after projecting it.  Every wave passes the same number of barriers.
+  auto run = [&](auto phase_tag) {
+    constexpr int PHASE = decltype(phase_tag)::value;
+    Online<H, NG> st;
+    auto init = [&](const Unit& un, int ord) {
+      const unsigned char* area = qs + ((ord & 1) * H + wave) * QA;
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
+        const int tt = g * 32 + tcol;
+        const bool ok = tt < un.nt;
+        const f16x8* q = reinterpret_cast<const f16x8*>(area + tt * 64);
+        st.qop[g][0] = ok ? q[hi] : zero8h();
+        st.qop[g][1] = ok ? q[2 + hi] : zero8h();
+        st.O[g] = f32x16{};
+        st.m[g] = -INFINITY;
+        st.l[g] = 0.f;
+      }
+    };
+    // The matrix core issues the ready MFMA of the oldest wave first, so a
+    // projection (32 back-to-back MFMAs at D = 256) would hold off the other
+    // wave's few score and P.V MFMAs and leave both waves in their softmax at
+    // the same time.  The attention step runs at raised wave priority: its
+    // MFMAs go first and its VALU work overlaps the other wave's projection.
+    auto attend = [&](const f16x8 (&kv)[4], int b, const Unit& un) {
+      __builtin_amdgcn_s_setprio(1);
+      st.template step<RPS>(kv, b, un, hi);
+      __builtin_amdgcn_s_setprio(0);
+    };
+    int cu = ub + blockIdx.x;  // compute cursor: unit index, its ordinal, block
+    int ck = 0;
+    Unit cun = units[cu];
+    int cb = cun.b0;
+    f16x8 held[4];  // PHASE 1: K/V of block hb of unit hun, attended to in the next step
+    Unit hun = cun;
+    int hb = -1;
+    for (int p_use = 0; cu < ue; ++p_use) {
+      const bool first = cb == cun.b0, last = cb + 1 == cun.b1;
+      // this wave's part of block p_use (and, at a unit's first block, of its
+      // queries, issued one block earlier) has landed
+      const int ahead = 2 * (p_load - 1 - p_use);
+      wait_vm(first ? min(ahead, 2 * q_after) : ahead);
+      ring_barrier();  // everyone's parts; the slot of p_use - 1 is free
+      if (last && cu + static_cast<int>(gridDim.x) < ue) issue_q(units[cu + gridDim.x], ck + 1);
+      if (p_load < p_use + kStages) issue_x();
+      const unsigned char* tile = xs + (p_use % kStages) * TILE;
+      if (PHASE == 0) {
+        if (first) init(cun, ck);
+        f16x8 kv[4];
+        project(tile, kv);
+        attend(kv, cb, cun);
+        if (last) st.finish(cun, wave, tcol, hi, part_acc, part_ml, n_tgt);
+      } else {
+        if (hb >= 0) {
+          attend(held, hb, hun);
+          if (hb + 1 == hun.b1) st.finish(hun, wave, tcol, hi, part_acc, part_ml, n_tgt);
+        }
+        if (first) init(cun, ck);
+        project(tile, held);
+        hun = cun;
+        hb = cb;
+      }
+      if (last) {
+        cu += gridDim.x;
+        ++ck;
+        if (cu < ue) {
+          cun = units[cu];
+          cb = cun.b0;
+        }
+      } else {
+        ++cb;
+      }
+    }
+    if (PHASE == 1 && hb >= 0) {
+      attend(held, hb, hun);
+      st.finish(hun, wave, tcol, hi, part_acc, part_ml, n_tgt);
+    }
+  };
+  if (phase == 0)
+    run(std::integral_constant<int, 0>{});
+  else
+    run(std::integral_constant<int, 1>{});
 }
 
 // ------------------------------------------------ K4: target update
