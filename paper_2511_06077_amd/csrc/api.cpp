@@ -216,11 +216,16 @@ stca_status_t forward_reordered(const Layout& L, const stca_batch_t* b, const vo
   WsHeader* hdr = at<WsHeader>(ws, L.hdr);
   Unit* units = at<Unit>(ws, L.units);
   int32_t* tch = at<int32_t>(ws, L.tchunks);
-  HIPCHK(fast_pack(w->wv, at<char>(ws, L.wvp16), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wv"));
-  HIPCHK(fast_pack(w->wo, at<char>(ws, L.wop), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wo"));
-  HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wq"));
-  HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, 1, st)); HIPCHK(rec.mark("pack_w1"));
-  HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, 1, st)); HIPCHK(rec.mark("pack_w2"));
+  {
+    PackJobs pj{};
+    pj.job[0] = {w->wv, at<char>(ws, L.wvp16), d, d, 1};
+    pj.job[1] = {w->wo, at<char>(ws, L.wop), d, d, 1};
+    pj.job[2] = {w->wq, at<char>(ws, L.wqp), d, d, 1};
+    pj.job[3] = {w->w1, at<char>(ws, L.w1p), d, F, 1};
+    pj.job[4] = {w->w2, at<char>(ws, L.w2p), F, d, 1};
+    HIPCHK(fast_pack_many(pj, 5, n, st));
+    HIPCHK(rec.mark("pack"));
+  }
   FastUpdate f{};
   f.n_layers = n;
   f.F = F;
@@ -281,12 +286,17 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, L.group, units, L.max_units,
                       tch, hdr, st)); HIPCHK(rec.mark("sched"));
   if (L.reord) return forward_reordered(L, b, hist, tgt, w, out, saved, SL, ws, st, rec);
-  HIPCHK(fast_pack(w->wk, at<char>(ws, L.wkp), n, d, d, 0, st)); HIPCHK(rec.mark("pack_wk"));
-  HIPCHK(fast_pack(w->wv, at<char>(ws, L.wvp), n, d, d, 0, st)); HIPCHK(rec.mark("pack_wv"));
-  HIPCHK(fast_pack(w->wo, at<char>(ws, L.wop), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wo"));
-  HIPCHK(fast_pack(w->wq, at<char>(ws, L.wqp), n, d, d, 1, st)); HIPCHK(rec.mark("pack_wq"));
-  HIPCHK(fast_pack(w->w1, at<char>(ws, L.w1p), n, d, F, 1, st)); HIPCHK(rec.mark("pack_w1"));
-  HIPCHK(fast_pack(w->w2, at<char>(ws, L.w2p), n, F, d, 1, st)); HIPCHK(rec.mark("pack_w2"));
+  {
+    PackJobs pj{};
+    pj.job[0] = {w->wk, at<char>(ws, L.wkp), d, d, 0};
+    pj.job[1] = {w->wv, at<char>(ws, L.wvp), d, d, 0};
+    pj.job[2] = {w->wo, at<char>(ws, L.wop), d, d, 1};
+    pj.job[3] = {w->wq, at<char>(ws, L.wqp), d, d, 1};
+    pj.job[4] = {w->w1, at<char>(ws, L.w1p), d, F, 1};
+    pj.job[5] = {w->w2, at<char>(ws, L.w2p), F, d, 1};
+    HIPCHK(fast_pack_many(pj, 6, n, st));
+    HIPCHK(rec.mark("pack"));
+  }
   const bool mat = materialize_kv() || L.wide;
   char* kv = at<char>(ws, L.kv);
   if (mat) {
@@ -617,8 +627,9 @@ stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch, c
 int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
   Layout L;
   if (!make_layout(dims, batch, 0, false, &L)) return -1;
-  if (L.path == 1 && L.reord) return 1 + 5 + 1 + 1 + 4 * L.n - 1;
-  if (L.path == 1) return materialize_kv() || L.wide ? 1 + 6 + 1 + 1 + 2 * L.n : 1 + 6 + 1 + 3 * L.n;
+  // sched, one repack launch, the initial update, then per layer
+  if (L.path == 1 && L.reord) return 1 + 1 + 1 + 1 + 4 * L.n - 1;
+  if (L.path == 1) return materialize_kv() || L.wide ? 1 + 1 + 1 + 1 + 2 * L.n : 1 + 1 + 1 + 3 * L.n;
   return 1 + 1 + 8 * L.n + 1;
 }
 

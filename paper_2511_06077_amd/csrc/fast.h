@@ -23,6 +23,17 @@ struct FastUpdate {
 
 // Repack W [n_layers][K][N] (bf16) into MFMA operand order, as bf16 or fp16.
 hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, int to_f16, hipStream_t st);
+// The same for up to kMaxPackJobs weights (same layer count) in one launch.
+constexpr int kMaxPackJobs = 8;
+struct PackJob {
+  const void* src;
+  void* dst;
+  int K, N, to_f16;
+};
+struct PackJobs {
+  PackJob job[kMaxPackJobs];
+};
+hipError_t fast_pack_many(const PackJobs& jobs, int n_jobs, int n_layers, hipStream_t st);
 int fast_proj_parts(int n_layers, int64_t n_blocks, int n_cu);
 // K1: history -> K/V of every layer, in the attention kernel's operand layout.
 hipError_t fast_proj(int D, const void* X, int64_t n_hist, int64_t n_blocks, const void* WkP, const void* WvP,

@@ -38,6 +38,7 @@
 // ("packed": [N/32][K/16][64 lanes][8 bf16] with lane (n = l%32, hi) holding
 // W[16ks + 8hi .. +7][32nb + n]), which serves both as an A operand of D^T and
 // as a B operand of D.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -48,8 +49,7 @@ namespace stca {
 namespace {
 
 constexpr int DH = 32;
-constexpr float kSlack = 8.f;
-constexpr int kFfnChunk = 256;  // update kernel: FFN hidden columns per LDS stage (F % 256 == 0)  // log2 units: softmax weights stay <= 256 between rescales
+constexpr float kSlack = 8.f;  // log2 units: softmax weights stay <= 256 between rescales
 
 __device__ __forceinline__ f32x16 mfma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -113,6 +113,36 @@ __global__ void pack_kernel(const bf16_bits* __restrict__ W, V8* __restrict__ P,
 #pragma unroll
   for (int e = 0; e < 8; ++e) r[e] = static_cast<typename elem_of<V8>::type>(to_f32(w[(int64_t)(k0 + e) * N + n]));
   P[(int64_t)layer * per_layer_groups + g] = r;
+}
+
+// Several weights in one launch (blockIdx.z = job): the per-call repacking of
+// a forward costs one launch instead of one per weight.
+template <typename V8>
+__device__ __forceinline__ void pack_one(const bf16_bits* __restrict__ w, V8* __restrict__ P, int K, int N,
+                                         int64_t g) {
+  const int lane = g % 64;
+  const int64_t rest = g / 64;
+  const int ks = rest % (K / 16);
+  const int nb = rest / (K / 16);
+  const int n = nb * 32 + lane % 32;
+  const int k0 = ks * 16 + 8 * (lane / 32);
+  V8 r;
+#pragma unroll
+  for (int e = 0; e < 8; ++e) r[e] = static_cast<typename elem_of<V8>::type>(to_f32(w[(int64_t)(k0 + e) * N + n]));
+  P[g] = r;
+}
+
+__global__ void pack_many_kernel(PackJobs J) {
+  const int j = blockIdx.z, layer = blockIdx.y;
+  const int64_t groups = (int64_t)(J.job[j].N / 32) * (J.job[j].K / 16) * 64;
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (g >= groups) return;
+  const PackJob& b = J.job[j];
+  const bf16_bits* w = static_cast<const bf16_bits*>(b.src) + (int64_t)layer * b.K * b.N;
+  if (b.to_f16)
+    pack_one(w, static_cast<f16x8*>(b.dst) + (int64_t)layer * groups, b.K, b.N, g);
+  else
+    pack_one(w, static_cast<bf16x8*>(b.dst) + (int64_t)layer * groups, b.K, b.N, g);
 }
 
 // ------------------------------------------------------ K1: projection
@@ -627,7 +657,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
 // mode 0 (init): s^(0) = x_t, Q^(0) = x_t W_Q^0.
 // mode 1 (layer i): merge the attention partials into a, then
 //   u = s + a W_O;  s' = u + ReLU(u W_1) W_2;  Q' = s' W_Q^{i+1} (if i+1 < n).
-// Activations go through LDS as bf16 MFMA operands; the state stays fp32.
+// Activations go through LDS as fp16 MFMA operands; the state stays fp32.
 struct UpdateArgs {
   int mode, layer, n_layers, F;
   int64_t n_tgt;
@@ -645,7 +675,7 @@ struct UpdateArgs {
   const f16x8 *WoP, *W1P, *W2P, *WqP;  // packed (fp16), all layers
 };
 
-template <int D>
+template <int D, int NC>
 __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   constexpr int NW = D / 32;
   constexpr int H = D / DH;
@@ -653,9 +683,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   constexpr int AROW = D + 8;
   extern __shared__ __attribute__((aligned(16))) uint16_t lds[];  // fp16 MFMA operands
   uint16_t* act = lds;                  // [32][AROW]
-  uint16_t* hid = lds + 32 * AROW;      // [32][FC + 8]
-  constexpr int FC = kFfnChunk;        // hidden columns staged in LDS at a time
-  constexpr int HROW = FC + 8;
+  uint16_t* hid = lds + 32 * AROW;      // [32][AROW]: D hidden columns at a time
   const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int tcol = lane % 32, hi = lane / 32;
   const int64_t tb = (int64_t)blockIdx.x * 32;
@@ -669,8 +697,8 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
     for (int g = 0; g < 4; ++g)
       *reinterpret_cast<float4*>(p + 8 * g) = make_float4(v[4 * g], v[4 * g + 1], v[4 * g + 2], v[4 * g + 3]);
   };
-  auto put_act = [&](uint16_t* buf, int row_len, int col0, const f32x16& v) {
-    uint16_t* p = buf + tcol * row_len + col0 + 4 * hi;
+  auto put_act = [&](uint16_t* buf, int col0, const f32x16& v) {
+    uint16_t* p = buf + tcol * AROW + col0 + 4 * hi;
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       uint2 pk;
@@ -679,27 +707,41 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       *reinterpret_cast<uint2*>(p + 8 * g) = pk;
     }
   };
-  // acc = W^T act^T over KSTEPS k-steps.  The weight operands stream from L2;
-  // with the step count known at compile time every load of the product is
-  // issued before the first MFMA waits on it, so a product costs about one
-  // L2 round trip instead of one per MFMA.
-  auto gemm = [&](auto ksteps_tag, const f16x8* Wp, const uint16_t* src, int src_row) {
-    constexpr int KSTEPS = decltype(ksteps_tag)::value;
-    const uint16_t* b = src + tcol * src_row + 8 * hi;
-    const f16x8* w = Wp + lane;
-    f16x8 wr[KSTEPS];
+  // Every product of the update is one 32 x 32 tile per wave with KS k-steps:
+  // acc = W^T act^T.  With NC (hidden chunks, F / D) known at compile time,
+  // its weight operands (one KS-step tile, from L2) are loaded one product
+  // ahead into the other of two register sets, so an L2 round trip overlaps
+  // the previous product instead of preceding its own; a register set is
+  // refilled after an instruction that reads the result of the product that
+  // used it.  The chunk loop is then fully unrolled: the same prefetch in a
+  // loop with a run-time trip count gave wrong results.  NC = 0 (any other
+  // F) loads each product's weights right before it.
+  f16x8 wa[KS], wb[KS];
+  auto fetch = [&](f16x8 (&r)[KS], const f16x8* Wp) {
 #pragma unroll
-    for (int k = 0; k < KSTEPS; ++k) wr[k] = w[k * 64];
+    for (int k = 0; k < KS; ++k) r[k] = Wp[k * 64 + lane];
+  };
+  auto gemm = [&](const f16x8 (&r)[KS], const uint16_t* src) {
+    const uint16_t* b = src + tcol * AROW + 8 * hi;
     f32x16 acc = {};
 #pragma unroll
-    for (int k = 0; k < KSTEPS; ++k) acc = mfma(wr[k], *reinterpret_cast<const f16x8*>(b + k * 16), acc);
+    for (int k = 0; k < KS; ++k) acc = mfma(r[k], *reinterpret_cast<const f16x8*>(b + k * 16), acc);
     return acc;
   };
-  using KSd = std::integral_constant<int, KS>;
-  using KSc = std::integral_constant<int, FC / 16>;
+  auto gemm_from = [&](const f16x8* Wp, const uint16_t* src) {
+    f16x8 r[KS];
+    fetch(r, Wp);
+    return gemm(r, src);
+  };
+  constexpr bool PF = NC > 0;
+  const int nc = PF ? NC : A.F / D;  // hidden chunks of D columns
+  const int KSF = A.F / 16;
+  auto w1_tile = [&](int c) { return A.W1P + ((int64_t)A.layer * (A.F / 32) + c * NW + w) * KS * 64; };
+  auto w2_tile = [&](int c) { return A.W2P + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64; };
+  auto wq_tile = [&](int ql) { return A.WqP + ((int64_t)(ql * NW + w) * KS) * 64; };
 
-  f32x16 s_next;
   if (A.mode == 0) {
+    fetch(wb, wq_tile(0));
     // stage x_t rows into LDS (fp16) and write s^(0) (fp32)
     for (int c = threadIdx.x; c < 32 * D / 8; c += 64 * NW) {
       const int row = c / (D / 8), col8 = c % (D / 8);
@@ -717,6 +759,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
     }
     __syncthreads();
   } else {
+    fetch(wa, A.WoP + ((int64_t)(A.layer * NW + w) * KS) * 64);
     // merge partials: two threads per (target, head), 16 dimensions each.
     // Every chunk's (max, sum) is requested at once and the accumulators four
     // chunks at a time, so the merge costs a few memory round trips.
@@ -755,13 +798,13 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
           }
 #pragma unroll
           for (int cc = 0; cc < 4; ++cc) {
-            const float w = wc[c0 + cc];
+            const float wgt = wc[c0 + cc];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-              av[4 * q] += w * x[cc][q].x;
-              av[4 * q + 1] += w * x[cc][q].y;
-              av[4 * q + 2] += w * x[cc][q].z;
-              av[4 * q + 3] += w * x[cc][q].w;
+              av[4 * q] += wgt * x[cc][q].x;
+              av[4 * q + 1] += wgt * x[cc][q].y;
+              av[4 * q + 2] += wgt * x[cc][q].z;
+              av[4 * q + 3] += wgt * x[cc][q].w;
             }
           }
         }
@@ -780,9 +823,9 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       for (int i = 0; i < 16; ++i) p[i] = f16_bits(av[i]);
     }
     __syncthreads();
-    const int KSF = A.F / 16;
+    if (PF) fetch(wb, w1_tile(0));  // after the merge, whose registers it would otherwise share
     // u = s + a W_O
-    f32x16 u = gemm(KSd{}, A.WoP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, AROW);
+    f32x16 u = gemm(wa, act);
     if (tok) {
       const float* sp = A.s_in + t * D + 32 * w + 4 * hi;
 #pragma unroll
@@ -793,26 +836,36 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       if (A.save_u) store_f32(A.save_u, u);
     }
     __syncthreads();
-    put_act(act, AROW, 32 * w, u);
+    put_act(act, 32 * w, u);
+    __builtin_amdgcn_sched_barrier(0);
+    if (PF) fetch(wa, w2_tile(0));
     __syncthreads();
-    // s' = u + ReLU(u W_1) W_2, the hidden layer taken FC columns at a time
-    s_next = u;
-    for (int c0 = 0; c0 < A.F; c0 += FC) {
+    // s' = u + ReLU(u W_1) W_2, the hidden layer taken D columns at a time
+    f32x16 s_next = u;
+    const int ql = A.layer + 1 < A.n_layers ? A.layer + 1 : -1;
 #pragma unroll
-      for (int nb = w; nb < FC / 32; nb += NW) {
-        f32x16 h = gemm(KSd{}, A.W1P + ((int64_t)A.layer * (A.F / 32) + c0 / 32 + nb) * KS * 64, act, AROW);
+    for (int c = 0; c < (PF ? NC : nc); ++c) {
+      f32x16 h = PF ? gemm(wb, act) : gemm_from(w1_tile(c), act);  // this wave's 32 hidden columns of chunk c
 #pragma unroll
-        for (int v = 0; v < 16; ++v) h[v] = fmaxf(h[v], 0.f);
-        put_act(hid, HROW, 32 * nb, h);
+      for (int v = 0; v < 16; ++v) h[v] = fmaxf(h[v], 0.f);
+      __builtin_amdgcn_sched_barrier(0);
+      if (PF) {
+        if (c + 1 < nc)
+          fetch(wb, w1_tile(c + 1));
+        else if (ql >= 0)
+          fetch(wb, wq_tile(ql));
       }
+      put_act(hid, 32 * w, h);
       __syncthreads();
-      const f32x16 y = gemm(KSc{}, A.W2P + ((int64_t)(A.layer * NW + w) * KSF + c0 / 16) * 64, hid, HROW);
+      const f32x16 y = PF ? gemm(wa, hid) : gemm_from(w2_tile(c), hid);
 #pragma unroll
       for (int v = 0; v < 16; ++v) s_next[v] += y[v];
+      __builtin_amdgcn_sched_barrier(0);
+      if (PF && c + 1 < nc) fetch(wa, w2_tile(c + 1));
       __syncthreads();
     }
     if (tok) {
-      if (A.layer + 1 < A.n_layers) {
+      if (ql >= 0) {
         store_f32(A.s_out, s_next);
       } else {
         bf16_bits* p = A.out + t * D + 32 * w + 4 * hi;
@@ -827,13 +880,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
         }
       }
     }
-    if (A.layer + 1 >= A.n_layers) return;
-    put_act(act, AROW, 32 * w, s_next);  // act (u) was last read before the previous barrier
+    if (ql < 0) return;
+    put_act(act, 32 * w, s_next);  // act (u) was last read before the previous barrier
     __syncthreads();
   }
   // next queries: Q = s W_Q^{next}, scaled into log2 units, permuted (QN layout)
-  const int ql = A.mode == 0 ? 0 : A.layer + 1;
-  f32x16 q = gemm(KSd{}, A.WqP + ((int64_t)(ql * NW + w) * KS) * 64, act, AROW);
+  f32x16 q = PF || A.mode == 0 ? gemm(wb, act) : gemm_from(wq_tile(A.layer + 1), act);
   const float qs = kLog2e * 0.17677669529663687f;  // log2(e) / sqrt(32)
 #pragma unroll
   for (int v = 0; v < 16; ++v) q[v] *= qs;
@@ -854,6 +906,16 @@ hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, int to_
     hipLaunchKernelGGL(pack_kernel<f16x8>, g, dim3(256), 0, st, (const bf16_bits*)W, (f16x8*)P, K, N, groups);
   else
     hipLaunchKernelGGL(pack_kernel<bf16x8>, g, dim3(256), 0, st, (const bf16_bits*)W, (bf16x8*)P, K, N, groups);
+  return hipGetLastError();
+}
+
+hipError_t fast_pack_many(const PackJobs& jobs, int n_jobs, int n_layers, hipStream_t st) {
+  if (n_jobs < 1 || n_jobs > kMaxPackJobs) return hipErrorInvalidValue;
+  int64_t groups = 0;
+  for (int j = 0; j < n_jobs; ++j)
+    groups = std::max<int64_t>(groups, (int64_t)(jobs.job[j].N / 32) * (jobs.job[j].K / 16) * 64);
+  dim3 g(static_cast<unsigned>(ceil_div(groups, 256)), n_layers, n_jobs);
+  hipLaunchKernelGGL(pack_many_kernel, g, dim3(256), 0, st, jobs);
   return hipGetLastError();
 }
 
@@ -942,8 +1004,12 @@ hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st) {
   A.WqP = (const f16x8*)f.WqP;
   if (f.n_tgt == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
-  const size_t lds = (size_t)32 * (D + 8) * 2 + (f.mode == 0 ? 0 : (size_t)32 * (kFfnChunk + 8) * 2);
-#define STCA_UPD(DD) hipLaunchKernelGGL(update_kernel<DD>, g, dim3(64 * (DD / 32)), lds, st, A)
+  const size_t lds = (size_t)32 * (D + 8) * 2 * (f.mode == 0 ? 1 : 2);
+#define STCA_UPD(DD)                                                                         \
+  if (f.F == 4 * (DD))                                                                      \
+    hipLaunchKernelGGL((update_kernel<DD, 4>), g, dim3(64 * (DD / 32)), lds, st, A);        \
+  else                                                                                      \
+    hipLaunchKernelGGL((update_kernel<DD, 0>), g, dim3(64 * (DD / 32)), lds, st, A)
   switch (D) {
     case 64: STCA_UPD(64); break;
     case 128: STCA_UPD(128); break;

@@ -304,13 +304,14 @@ def replicate_per_target(b: Batch) -> Batch:
 
 
 def make_custom_batch(name: str, hist_len: Sequence[int], n_tgt: Sequence[int], *, d_model: int, n_heads: int,
-                      n_layers: int, dtype: str, seed: int, scale_q: float = 1.0, with_grad: bool = False) -> Batch:
+                      n_layers: int, dtype: str, seed: int, scale_q: float = 1.0, with_grad: bool = False,
+                      ffn_mult: int = 4) -> Batch:
     """A batch with explicitly listed per-request history lengths and target
     counts (edge cases: tails, empty target segments, single-row histories),
     drawn with the same per-request streams as the named workloads."""
     L = np.asarray(hist_len, dtype=np.int64)
     m = np.asarray(n_tgt, dtype=np.int64)
-    wl = Workload(name, len(L), d_model, n_heads, n_layers, dtype, seed, backward=with_grad)
+    wl = Workload(name, len(L), d_model, n_heads, n_layers, dtype, seed, backward=with_grad, ffn_mult=ffn_mult)
     hoff, toff = offsets(L), offsets(m)
     sdt = np.uint16 if dtype == "bf16" else np.float32
     hist = np.empty((int(hoff[-1]), d_model), dtype=sdt)

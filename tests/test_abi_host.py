@@ -138,31 +138,31 @@ def test_materialized_kv_needs_workspace_for_every_layer(monkeypatch):
 
 def test_reordered_form_selection(monkeypatch):
     """Requests with at most 32 / h targets (host offsets known) run the
-    reordered attention: its launch sequence is 7 + 4 n launches against the
-    standard form's 8 + 3 n."""
+    reordered attention: its launch sequence is 3 + 4 n launches against the
+    standard form's 3 + 3 n."""
     monkeypatch.delenv("STCA_ATTN", raising=False)
     monkeypatch.delenv("STCA_KV", raising=False)
     n = GOOD_DIMS["n_layers"]
     small, keep1 = fake_batch([0, 40, 100, 101], [0, 4, 5, 8])   # m = 4, 1, 3 <= 32 / 8
     wide, keep2 = fake_batch([0, 40, 100], [0, 5, 9])            # m = 5
-    assert stca.stca_forward_launch_count(dims(), small) == 7 + 4 * n
-    assert stca.stca_forward_launch_count(dims(), wide) == 8 + 3 * n
-    assert stca.stca_forward_launch_count(dims(d_model=128, n_heads=4), wide) == 7 + 4 * n  # 32 / 4 = 8
+    assert stca.stca_forward_launch_count(dims(), small) == 3 + 4 * n
+    assert stca.stca_forward_launch_count(dims(), wide) == 3 + 3 * n
+    assert stca.stca_forward_launch_count(dims(d_model=128, n_heads=4), wide) == 3 + 4 * n  # 32 / 4 = 8
     nohost = stca.batch(3, 101, 8, 0x10000, 0x20000, None, None)
-    assert stca.stca_forward_launch_count(dims(), nohost) == 8 + 3 * n
+    assert stca.stca_forward_launch_count(dims(), nohost) == 3 + 3 * n
     monkeypatch.setenv("STCA_ATTN", "standard")
-    assert stca.stca_forward_launch_count(dims(), small) == 8 + 3 * n
+    assert stca.stca_forward_launch_count(dims(), small) == 3 + 3 * n
 
 
 def test_wide_groups_selection(monkeypatch):
     """A request with more than 64 targets switches the bf16 path to K/V
-    written once (9 + 2 n launches); STCA_KV=fused keeps the fused form."""
+    written once (4 + 2 n launches); STCA_KV=fused keeps the fused form."""
     monkeypatch.delenv("STCA_ATTN", raising=False)
     monkeypatch.delenv("STCA_KV", raising=False)
     n = GOOD_DIMS["n_layers"]
     many, keep = fake_batch([0, 400, 500], [0, 65, 70])
     few, keep2 = fake_batch([0, 400, 500], [0, 64, 70])
-    assert stca.stca_forward_launch_count(dims(), many) == 9 + 2 * n
-    assert stca.stca_forward_launch_count(dims(), few) == 8 + 3 * n
+    assert stca.stca_forward_launch_count(dims(), many) == 4 + 2 * n
+    assert stca.stca_forward_launch_count(dims(), few) == 3 + 3 * n
     monkeypatch.setenv("STCA_KV", "fused")
-    assert stca.stca_forward_launch_count(dims(), many) == 8 + 3 * n
+    assert stca.stca_forward_launch_count(dims(), many) == 3 + 3 * n

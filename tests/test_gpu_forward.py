@@ -109,6 +109,16 @@ def test_edge_tails(torch, chunk_override, kv_mode, dtype, d, h, n, chunk):
     check_against_oracle(b, y, a, lse, TOL[dtype])
 
 
+@pytest.mark.parametrize("d,h,mult", [(256, 8, 2), (128, 4, 2), (128, 4, 6)])
+def test_ffn_width_other_than_4d(torch, kv_mode, d, h, mult):
+    """FFN hidden widths other than 4 d (multiples of 256 on the bf16 path):
+    the update kernel's FFN loop with a run-time chunk count."""
+    b = W.make_custom_batch("ffn", [200, 33, 64], [5, 17, 32], d_model=d, n_heads=h, n_layers=2, dtype="bf16",
+                            seed=13, ffn_mult=mult)
+    y, a, lse, _ = run_gpu(torch, b)
+    check_against_oracle(b, y, a, lse, TOL["bf16"])
+
+
 @pytest.mark.parametrize("dtype,scale", [("bf16", 1.5), ("f32", 8.0)])
 def test_peaked_softmax(torch, chunk_override, kv_mode, dtype, scale):
     """W_Q scaled up: sharper attention and larger running-max jumps between
