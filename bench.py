@@ -294,27 +294,34 @@ def main() -> int:
 
 def backward_phase_work(label: str, b: W.Batch):
     """Algorithmic (flop, bytes, peak TFLOP/s) of one occurrence of a backward
-    phase (stca_backward_profiled's markers), per layer, as the kernels are
-    designed: history-side products on bf16 operands (bf16 MFMA peak) with
-    fp32 K|V (fp32 attention on the fp32 MFMA, 157.3 TFLOP/s), dK|dV in bf16
-    (row-major and transposed)."""
+    phase (stca_backward_profiled's markers), as the kernels are designed:
+    history-side products on bf16 operands (bf16 MFMA peak) with fp32 K|V
+    (fp32 attention on the fp32 MFMA, 157.3 TFLOP/s), dK|dV in bf16
+    (row-major and transposed), every layer's [dW_K | dW_V] and dX formed once
+    after the layers (one occurrence each), target-side products in fp32 where
+    they decide ReLU gates and on bf16 operands otherwise."""
     wl = b.wl
-    d, F = wl.d_model, wl.ffn_hidden
+    d, F, n = wl.d_model, wl.ffn_hidden, wl.n_layers
     Ls = float(b.hist_len[b.n_tgt > 0].sum())
     mL = float((b.n_tgt.astype(np.float64) * b.hist_len).sum())
     mt = float(b.n_tgt.sum())
     if label == "kv_gemm":
         return 4 * Ls * d * d, 2 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
-    if label == "dw_kv":
-        return 4 * Ls * d * d, 2 * Ls * d + 4 * Ls * d, PEAK_BF16_TFLOPS
-    if label == "dx":
-        return 4 * Ls * d * d, 4 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
+    if label == "dw_kv":  # X^T read once, every layer's (dK | dV)^T
+        return n * 4 * Ls * d * d, 2 * Ls * d + n * 4 * Ls * d, PEAK_BF16_TFLOPS
+    if label == "dx":  # every layer's dK | dV read, dX written once (fp32)
+        return n * 4 * Ls * d * d, n * 4 * Ls * d + 4 * Ls * d, PEAK_BF16_TFLOPS
     if label == "attn_fwd":
         return 4 * mL * d, 8 * Ls * d, PEAK_FP32_TFLOPS
     if label == "attn_bwd":
         return 10 * mL * d, 8 * Ls * d + 8 * Ls * d, PEAK_FP32_TFLOPS
-    if label == "target_gemm":  # 14 target-side products per layer over 4 markers
-        return 14 * mt * (d * d + d * F) * 2 / 4, 0.0, PEAK_FP32_TFLOPS
+    if label == "target_gemm":
+        # per layer over 4 markers: fp32 products q, o (d x d) and FFN1, FFN2
+        # (d x F); bf16 products dW2, dH, dW1, du (d x F) and dWo, da, dWq, ds
+        # (d x d), counted at the fp32 peak by their time ratio
+        f32 = 2 * mt * (2 * d * d + 2 * d * F)
+        b16 = 2 * mt * (4 * d * F + 4 * d * d)
+        return (f32 + b16 * PEAK_FP32_TFLOPS / PEAK_BF16_TFLOPS) / 4, 0.0, PEAK_FP32_TFLOPS
     return 0.0, 0.0, 0.0
 
 

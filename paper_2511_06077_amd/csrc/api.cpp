@@ -72,8 +72,9 @@ struct Layout {
   // generic forward
   size_t kv32, q32, abuf, ubuf, hid;
   // backward (generic)
-  size_t pre, dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
+  size_t dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
   size_t xt, dkvt, wkvt;
+  size_t b_hid, b_dhid, b_ds, b_u, b_du, b_a, b_dq, b_s;  // bf16 copies of backward operands (bf16 path)
   int64_t gpart_floats, nh8;
   size_t total;
 };
@@ -145,7 +146,9 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
   } else {
     const bool bf = dims->dtype == STCA_BF16;
     L->kvs = m.take(4 * n * nh * 2 * d);  // every layer's K | V rows, fp32
-    L->dkv = m.take((bf ? 2 : 4) * nh * 2 * d);
+    // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
+    // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
+    L->dkv = m.take(bf ? 2 * nh * n * 2 * d : 4 * nh * 2 * d);
     // bf16 history-side products: [W_K | W_V] per layer and its transpose,
     // X^T and (dK | dV)^T with the history rows padded to a multiple of 8
     L->nh8 = round_up(static_cast<int64_t>(nh), 8);
@@ -153,16 +156,22 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;
     L->wkvt = bf ? m.take(2 * n * d * 2 * d) : 0;
     L->xt = bf ? m.take(2 * d * nh8) : 0;
-    L->dkvt = bf ? m.take(2 * 2 * d * nh8) : 0;
-    L->dwkv = bf ? m.take(4 * d * 2 * d) : 0;
-    L->gpart_floats = bf ? gemm_mfma_part_floats(static_cast<int>(d), static_cast<int>(2 * d),
-                                                  static_cast<int>(nh8)) : 0;
+    L->dkvt = bf ? m.take(2 * n * 2 * d * nh8) : 0;  // [n 2d][nh8]: every layer's (dK | dV)^T
+    L->dwkv = bf ? m.take(4 * d * n * 2 * d) : 0;   // [d][n 2d] fp32
+    // split-K partials: the largest of [dW_K | dW_V] (K = history rows) and
+    // the target-side weight gradients (K = targets)
+    L->gpart_floats = 0;
+    if (bf) {
+      const int di = static_cast<int>(d), Fi = static_cast<int>(F), nti = static_cast<int>(nt);
+      L->gpart_floats = std::max({gemm_mfma_part_floats(di, 2 * di * static_cast<int>(n), static_cast<int>(nh8)),
+                                  gemm_mfma_part_floats(Fi, di, nti), gemm_mfma_part_floats(di, Fi, nti),
+                                  gemm_mfma_part_floats(di, di, nti)});
+    }
     L->gpart = bf ? m.take(4 * L->gpart_floats) : 0;
     L->rq = m.take(4 * n * nt * d);  // per-layer queries, attention outputs, lse
     L->ra = m.take(4 * n * nt * d);
     L->rl = m.take(4 * n * nt * L->h);
-    L->hid = m.take(4 * nt * F);
-    L->pre = m.take(4 * nt * F);
+    L->hid = m.take(4 * n * nt * F);  // every layer's ReLU(u W_1) from the recomputation
     L->dhid = m.take(4 * nt * F);
     L->ds = m.take(4 * nt * d);
     L->du = m.take(4 * nt * d);
@@ -174,6 +183,16 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->part_ml = m.take(8 * kMaxChunks * nt * L->h);
     L->rs = m.take(4 * (n + 1) * nt * d);  // recomputed s^(0..n)
     L->ru = m.take(4 * n * nt * d);        // recomputed u^(0..n-1)
+    if (bf) {
+      L->b_hid = m.take(2 * nt * F);
+      L->b_dhid = m.take(2 * nt * F);
+      L->b_ds = m.take(2 * nt * d);
+      L->b_u = m.take(2 * nt * d);
+      L->b_du = m.take(2 * nt * d);
+      L->b_a = m.take(2 * nt * d);
+      L->b_dq = m.take(2 * nt * d);
+      L->b_s = m.take(2 * nt * d);
+    }
   }
   L->total = m.off;
   return true;
@@ -427,8 +446,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                       hdr, st));
   HIPCHK(rec.mark("sched"));
   void* dkv = at<char>(ws, L.dkv);
-  float* hid = at<float>(ws, L.hid);
-  float* pre = at<float>(ws, L.pre);
+  auto RH = [&](int i) { return at<float>(ws, L.hid) + (size_t)i * nt * F; };
   float* dhid = at<float>(ws, L.dhid);
   float* ds = at<float>(ws, L.ds);
   float* du = at<float>(ws, L.du);
@@ -444,7 +462,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   auto RA = [&](int i) { return per_layer(L.ra, i, nt * d); };
   auto RL = [&](int i) { return per_layer(L.rl, i, nt * h); };
   auto KVS = [&](int i) { return per_layer(L.kvs, i, nh * 2 * d); };
-  auto WKV = [&](int i) { return at<bf16_bits>(ws, L.wkv) + (size_t)i * d * 2 * d; };
+  // [W_K^0 | W_V^0 | W_K^1 | ...]: [d][n 2d], B operand of dX for every layer at once
+  bf16_bits* wkv_all = bf ? at<bf16_bits>(ws, L.wkv) : nullptr;
   auto WKVT = [&](int i) { return at<bf16_bits>(ws, L.wkvt) + (size_t)i * d * 2 * d; };
   bf16_bits* xt = bf ? at<bf16_bits>(ws, L.xt) : nullptr;
   bf16_bits* dkvt = bf ? at<bf16_bits>(ws, L.dkvt) : nullptr;
@@ -464,8 +483,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     for (int i = 0; i < n; ++i) {
       const bf16_bits* Wk = reinterpret_cast<const bf16_bits*>(W(w->wk, i, (size_t)d * d));
       const bf16_bits* Wv = reinterpret_cast<const bf16_bits*>(W(w->wv, i, (size_t)d * d));
-      HIPCHK(hipMemcpy2DAsync(WKV(i), 2 * d * 2, Wk, d * 2, d * 2, d, hipMemcpyDeviceToDevice, st));
-      HIPCHK(hipMemcpy2DAsync(WKV(i) + d, 2 * d * 2, Wv, d * 2, d * 2, d, hipMemcpyDeviceToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(wkv_all + (size_t)i * 2 * d, (size_t)n * 2 * d * 2, Wk, d * 2, d * 2, d,
+                              hipMemcpyDeviceToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(wkv_all + (size_t)i * 2 * d + d, (size_t)n * 2 * d * 2, Wv, d * 2, d * 2, d,
+                              hipMemcpyDeviceToDevice, st));
       HIPCHK(transpose_bf16(Wk, d, d, d, WKVT(i), d, d, st));
       HIPCHK(transpose_bf16(Wv, d, d, d, WKVT(i) + (size_t)d * d, d, d, st));
     }
@@ -497,17 +518,22 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     HIPCHK(rec.mark("attn_fwd"));
     HIPCHK(gemm(0, bf, nt, d, d, RA(i), d, 0, W(w->wo, i, (size_t)d * d), d, 0, RU(i), d, 1.f, kEpiAddRes, RS(i),
                 d, nullptr));
-    HIPCHK(gemm(0, bf, nt, F, d, RU(i), d, 0, W(w->w1, i, (size_t)d * F), F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0,
+    HIPCHK(gemm(0, bf, nt, F, d, RU(i), d, 0, W(w->w1, i, (size_t)d * F), F, 0, RH(i), F, 1.f, kEpiRelu, nullptr, 0,
                 nullptr));
-    HIPCHK(gemm(0, bf, nt, d, F, hid, F, 0, W(w->w2, i, (size_t)d * F), d, 0, RS(i + 1), d, 1.f, kEpiAddRes,
+    HIPCHK(gemm(0, bf, nt, d, F, RH(i), F, 0, W(w->w2, i, (size_t)d * F), d, 0, RS(i + 1), d, 1.f, kEpiAddRes,
                 RU(i), d, nullptr));
     HIPCHK(rec.mark("target_gemm"));
   }
   HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
-  // rows of requests without targets keep a zero gradient
-  HIPCHK(fill_f32(static_cast<float*>(dkv), 0.f, nh * 2 * d * static_cast<int64_t>(es) / 4, st));
-  if (bf) HIPCHK(fill_f32(reinterpret_cast<float*>(dkvt), 0.f, (int64_t)2 * d * nh8 / 2, st));
-  if (!bf) HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
+  // rows of requests without targets keep a zero gradient (and dK|dV^T's
+  // padding columns stay zero)
+  if (bf) {
+    HIPCHK(zero_untargeted(b->hist_off, b->tgt_off, b->n_requests, nh, static_cast<bf16_bits*>(dkv), n * 2 * d,
+                           n * 2 * d, dkvt, nh8, st));
+  } else {
+    HIPCHK(fill_f32(static_cast<float*>(dkv), 0.f, nh * 2 * d, st));
+    HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
+  }
   HIPCHK(rec.mark("prep"));
   for (int i = n - 1; i >= 0; --i) {
     const float* s = RS(i);
@@ -518,46 +544,78 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     const void* W2 = W(w->w2, i, (size_t)d * F);
     const void* Wo = W(w->wo, i, (size_t)d * d);
     const void* Wq = W(w->wq, i, (size_t)d * d);
-    // s' = u + ReLU(u W1) W2
-    HIPCHK(gemm(0, bf, nt, F, d, u, d, 0, W1, F, 0, hid, F, 1.f, kEpiRelu, nullptr, 0, pre));
-    HIPCHK(gemm(0, 0, F, d, nt, hid, F, 1, ds, d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, kEpiStore, nullptr, 0,
-                nullptr));
-    HIPCHK(gemm(0, bf, nt, F, d, ds, d, 0, W2, d, 1, dhid, F, 1.f, kEpiStore, nullptr, 0, nullptr));
-    HIPCHK(relu_mask_mul(dhid, pre, nt * F, st));
-    HIPCHK(gemm(0, 0, d, F, nt, u, d, 1, dhid, F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, kEpiStore, nullptr, 0,
-                nullptr));
-    HIPCHK(gemm(0, bf, nt, d, F, dhid, F, 0, W1, F, 1, du, d, 1.f, kEpiAddRes, ds, d, nullptr));
-    // u = s + a Wo
-    HIPCHK(gemm(0, 0, d, d, nt, a, d, 1, du, d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
-                nullptr));
-    HIPCHK(gemm(0, bf, nt, d, d, du, d, 0, Wo, d, 1, da, d, 1.f, kEpiStore, nullptr, 0, nullptr));
+    // s' = u + ReLU(u W1) W2.  The ReLU gates are those of the fp32
+    // recomputation (hid > 0 exactly where u W1 > 0); on the bf16 path the
+    // products that only carry gradients take bf16 copies of their fp32
+    // operands on the bf16 MFMA (fp32 sums), the others stay fp32.
+    const float* hid = RH(i);
+    if (bf) {
+      const int nti = static_cast<int>(nt);
+      float* gp = at<float>(ws, L.gpart);
+      const int64_t gpf = L.gpart_floats;
+      auto bcopy = [&](const float* src, size_t off, int64_t count) {
+        return convert(0, 1, src, at<bf16_bits>(ws, off), count, st);
+      };
+      auto B = [&](size_t off) { return at<bf16_bits>(ws, off); };
+      auto WB = [&](const void* p) { return static_cast<const bf16_bits*>(p); };
+      HIPCHK(bcopy(hid, L.b_hid, nt * F));
+      HIPCHK(bcopy(ds, L.b_ds, nt * d));
+      HIPCHK(bcopy(u, L.b_u, nt * d));
+      HIPCHK(bcopy(a, L.b_a, nt * d));
+      HIPCHK(gemm_mfma(F, d, nti, B(L.b_hid), F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, 0, gp, gpf,
+                       st));
+      HIPCHK(gemm_mfma(nti, F, d, B(L.b_ds), d, 0, WB(W2), d, 1, dhid, F, 1.f, 0, nullptr, 0, st));
+      HIPCHK(relu_mask_mul(dhid, hid, nt * F, st));
+      HIPCHK(bcopy(dhid, L.b_dhid, nt * F));
+      HIPCHK(gemm_mfma(d, F, nti, B(L.b_u), d, 1, B(L.b_dhid), F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, 0, gp, gpf,
+                       st));
+      HIPCHK(hipMemcpyAsync(du, ds, 4 * nt * d, hipMemcpyDeviceToDevice, st));
+      HIPCHK(gemm_mfma(nti, d, F, B(L.b_dhid), F, 0, WB(W1), F, 1, du, d, 1.f, 1, nullptr, 0, st));
+      // u = s + a Wo
+      HIPCHK(bcopy(du, L.b_du, nt * d));
+      HIPCHK(gemm_mfma(d, d, nti, B(L.b_a), d, 1, B(L.b_du), d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, 0, gp, gpf,
+                       st));
+      HIPCHK(gemm_mfma(nti, d, d, B(L.b_du), d, 0, WB(Wo), d, 1, da, d, 1.f, 0, nullptr, 0, st));
+    } else {
+      HIPCHK(gemm(0, 0, F, d, nt, hid, F, 1, ds, d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, kEpiStore, nullptr, 0,
+                  nullptr));
+      HIPCHK(gemm(0, 0, nt, F, d, ds, d, 0, W2, d, 1, dhid, F, 1.f, kEpiStore, nullptr, 0, nullptr));
+      HIPCHK(relu_mask_mul(dhid, hid, nt * F, st));
+      HIPCHK(gemm(0, 0, d, F, nt, u, d, 1, dhid, F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, kEpiStore, nullptr, 0,
+                  nullptr));
+      HIPCHK(gemm(0, 0, nt, d, F, dhid, F, 0, W1, F, 1, du, d, 1.f, kEpiAddRes, ds, d, nullptr));
+      // u = s + a Wo
+      HIPCHK(gemm(0, 0, d, d, nt, a, d, 1, du, d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
+                  nullptr));
+      HIPCHK(gemm(0, 0, nt, d, d, du, d, 0, Wo, d, 1, da, d, 1.f, kEpiStore, nullptr, 0, nullptr));
+    }
     HIPCHK(rec.mark("target_gemm"));
     // attention (softmax weights rebuilt from the same q, K, V and lse that
     // gave a, so rowsum(dA * A) matches them)
-    HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, b->tgt_off, RQ(i), kv, d, a, da, RL(i), dqp, dkv, bf,
-                            dkvt, nh8, nt, st));
+    void* dkv_i = bf ? static_cast<void*>(static_cast<bf16_bits*>(dkv) + (size_t)i * 2 * d) : dkv;
+    HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, b->tgt_off, RQ(i), kv, d, a, da, RL(i), dqp, dkv_i,
+                            bf ? n * 2 * d : 2 * d, bf, bf ? dkvt + (size_t)i * 2 * d * nh8 : nullptr, nh8, nt, st));
     HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
     HIPCHK(rec.mark("attn_bwd"));
     // q = s Wq
-    HIPCHK(gemm(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
-                nullptr));
-    HIPCHK(gemm(0, bf, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr));
-    HIPCHK(rec.mark("target_gemm"));
-    // [K | V] = X [W_K | W_V]
     if (bf) {
-      const bf16_bits* dKV = static_cast<const bf16_bits*>(dkv);
-      float* dwkv = at<float>(ws, L.dwkv);
-      HIPCHK(gemm_mfma(d, 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, 2 * d, 1.f, 0, at<float>(ws, L.gpart),
-                       L.gpart_floats, st));
-      HIPCHK(hipMemcpy2DAsync(dw->dwk + (size_t)i * d * d, d * 4, dwkv, 2 * d * 4, d * 4, d,
-                              hipMemcpyDeviceToDevice, st));
-      HIPCHK(hipMemcpy2DAsync(dw->dwv + (size_t)i * d * d, d * 4, dwkv + d, 2 * d * 4, d * 4, d,
-                              hipMemcpyDeviceToDevice, st));
-      HIPCHK(rec.mark("dw_kv"));
-      HIPCHK(gemm_mfma(static_cast<int>(nh), d, 2 * d, dKV, 2 * d, 0, WKV(i), 2 * d, 1, dhist, d, 1.f,
-                       i != n - 1, nullptr, 0, st));
-      HIPCHK(rec.mark("dx"));
+      const int nti = static_cast<int>(nt);
+      HIPCHK(convert(0, 1, dq, at<bf16_bits>(ws, L.b_dq), nt * d, st));
+      HIPCHK(convert(0, 1, s, at<bf16_bits>(ws, L.b_s), nt * d, st));
+      HIPCHK(gemm_mfma(d, d, nti, at<bf16_bits>(ws, L.b_s), d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,
+                       dw->dwq + (size_t)i * d * d, d, 1.f, 0, at<float>(ws, L.gpart), L.gpart_floats, st));
+      HIPCHK(hipMemcpyAsync(ds2, du, 4 * nt * d, hipMemcpyDeviceToDevice, st));
+      HIPCHK(gemm_mfma(nti, d, d, at<bf16_bits>(ws, L.b_dq), d, 0, static_cast<const bf16_bits*>(Wq), d, 1, ds2, d,
+                       1.f, 1, nullptr, 0, st));
     } else {
+      HIPCHK(gemm(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
+                  nullptr));
+      HIPCHK(gemm(0, 0, nt, d, d, dq, d, 0, Wq, d, 1, ds2, d, 1.f, kEpiAddRes, du, d, nullptr));
+    }
+    HIPCHK(rec.mark("target_gemm"));
+    // [K | V] = X [W_K | W_V]: on the bf16 path every layer's dK | dV is kept
+    // and the history-side gradients are formed once after the loop
+    if (!bf) {
       const float* dKV = static_cast<const float*>(dkv);
       const void* Wk = W(w->wk, i, (size_t)d * d);
       const void* Wv = W(w->wv, i, (size_t)d * d);
@@ -573,6 +631,24 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       HIPCHK(rec.mark("dx"));
     }
     std::swap(ds, ds2);
+  }
+  if (bf) {
+    // [dW_K^i | dW_V^i] for every layer = X^T [dK^i | dV^i] (one product over
+    // the history rows), then dX = sum_i [dK^i | dV^i] [W_K^i | W_V^i]^T as
+    // one product with K = n 2d, written once
+    float* dwkv = at<float>(ws, L.dwkv);
+    HIPCHK(gemm_mfma(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
+                     L.gpart_floats, st));
+    for (int i = 0; i < n; ++i) {
+      HIPCHK(hipMemcpy2DAsync(dw->dwk + (size_t)i * d * d, d * 4, dwkv + (size_t)i * 2 * d, (size_t)n * 2 * d * 4,
+                              d * 4, d, hipMemcpyDeviceToDevice, st));
+      HIPCHK(hipMemcpy2DAsync(dw->dwv + (size_t)i * d * d, d * 4, dwkv + (size_t)i * 2 * d + d,
+                              (size_t)n * 2 * d * 4, d * 4, d, hipMemcpyDeviceToDevice, st));
+    }
+    HIPCHK(rec.mark("dw_kv"));
+    HIPCHK(gemm_mfma(static_cast<int>(nh), d, n * 2 * d, static_cast<const bf16_bits*>(dkv), n * 2 * d, 0, wkv_all,
+                     n * 2 * d, 1, dhist, d, 1.f, 0, nullptr, 0, st));
+    HIPCHK(rec.mark("dx"));
   }
   HIPCHK(convert(0, 0, ds, dtgt, nt * d, st));
   HIPCHK(rec.mark("out"));
@@ -677,7 +753,9 @@ stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch, 
 int stca_backward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
   Layout L;
   if (!make_layout(dims, batch, 1, true, &L)) return -1;
-  return 4 + 9 * L.n;
+  // sched, prep, 4 per layer (recomputation), prep, then per layer 5 (fp32)
+  // or 3 plus the two history-side products of every layer (bf16), out
+  return dims->dtype == STCA_BF16 ? 6 + 7 * L.n : 4 + 9 * L.n;
 }
 
 stca_status_t stca_backward_profiled(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist,

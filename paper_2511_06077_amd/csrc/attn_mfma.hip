@@ -209,8 +209,8 @@ template <int DH, typename OT>
 __global__ __launch_bounds__(64 * kWaves) void attn_bwd_mfma_kernel(
     const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const int32_t* __restrict__ toff,
     const float* __restrict__ Q, const float* __restrict__ KV, int d, const float* __restrict__ a,
-    const float* __restrict__ da, const float* __restrict__ lse, OT* __restrict__ dKV, bf16_bits* __restrict__ dKVT,
-    int64_t ldt, float* __restrict__ dq_part, int64_t n_tgt, int n_heads) {
+    const float* __restrict__ da, const float* __restrict__ lse, OT* __restrict__ dKV, int64_t ldkv,
+    bf16_bits* __restrict__ dKVT, int64_t ldt, float* __restrict__ dq_part, int64_t n_tgt, int n_heads) {
   constexpr int DT = DH / 16;
   constexpr int KQ = DH / 4;
   __shared__ float pT[kWaves][kRows][17], eT[kWaves][kRows][17];
@@ -333,8 +333,8 @@ __global__ __launch_bounds__(64 * kWaves) void attn_bwd_mfma_kernel(
             kx[v] = dk[dt][v] * kLn2;
             vx[v] = dv[dt][v];
           }
-          OT* pk = dKV + (int64_t)tok * 2 * d + c;
-          OT* pv = dKV + (int64_t)tok * 2 * d + d + c;
+          OT* pk = dKV + (int64_t)tok * ldkv + c;
+          OT* pv = dKV + (int64_t)tok * ldkv + d + c;
           if (!first) add4(kx, pk), add4(vx, pv);
           store4(pk, kx);
           store4(pv, vx);
@@ -388,17 +388,18 @@ hipError_t attn_fwd_mfma(int d_head, int n_heads, const Unit* units, int64_t max
 
 hipError_t attn_bwd_mfma(int d_head, int n_heads, const Unit* units, int64_t max_units, const WsHeader* hdr,
                          const int32_t* toff, const float* Q, const float* KV, int d, const float* a, const float* da,
-                         const float* lse, float* dq_part, void* dKV, int dkv_bf16, bf16_bits* dKVT, int64_t ldt,
-                         int64_t n_tgt, hipStream_t st) {
+                         const float* lse, float* dq_part, void* dKV, int64_t ldkv, int dkv_bf16, bf16_bits* dKVT,
+                         int64_t ldt, int64_t n_tgt, hipStream_t st) {
   if (max_units == 0) return hipSuccess;
   dim3 grid(static_cast<unsigned>(max_units), n_heads);
 #define STCA_AB(DH)                                                                                                \
   if (dkv_bf16)                                                                                                    \
     hipLaunchKernelGGL((attn_bwd_mfma_kernel<DH, bf16_bits>), grid, dim3(64 * kWaves), 0, st, units, hdr, toff, Q, \
-                       KV, d, a, da, lse, static_cast<bf16_bits*>(dKV), dKVT, ldt, dq_part, n_tgt, n_heads);       \
+                       KV, d, a, da, lse, static_cast<bf16_bits*>(dKV), ldkv, dKVT, ldt, dq_part, n_tgt,          \
+                       n_heads);                                                                                   \
   else                                                                                                             \
     hipLaunchKernelGGL((attn_bwd_mfma_kernel<DH, float>), grid, dim3(64 * kWaves), 0, st, units, hdr, toff, Q, KV, \
-                       d, a, da, lse, static_cast<float*>(dKV), nullptr, 0, dq_part, n_tgt, n_heads)
+                       d, a, da, lse, static_cast<float*>(dKV), ldkv, nullptr, 0, dq_part, n_tgt, n_heads)
   switch (d_head) {
     case 16: STCA_AB(16); break;
     case 32: STCA_AB(32); break;

@@ -201,10 +201,19 @@ hipError_t transpose_bf16(const bf16_bits* src, int64_t lds, int R, int C, bf16_
   return hipGetLastError();
 }
 
-int64_t gemm_mfma_part_floats(int M, int N, int K) {
+namespace {
+// Splits over K of a product with few output tiles: enough partial tiles to
+// fill the chip (about 1024 workgroups), each split at least 256 deep.
+int64_t k_splits(int M, int N, int K) {
   const int64_t tiles = ceil_div(M, BM) * ceil_div(N, BN);
-  if (tiles >= 256 || K < 8192) return 0;
-  return std::min<int64_t>(ceil_div(1024, tiles), K / 2048) * M * N;
+  if (tiles >= 256 || K < 1024) return 1;
+  return std::max<int64_t>(1, std::min<int64_t>(ceil_div(1024, tiles), K / 256));
+}
+}  // namespace
+
+int64_t gemm_mfma_part_floats(int M, int N, int K) {
+  const int64_t s = k_splits(M, N, K);
+  return s > 1 ? s * M * N : 0;
 }
 
 hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
@@ -219,8 +228,8 @@ hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
   const int tm = static_cast<int>(ceil_div(M, BM)), tn = static_cast<int>(ceil_div(N, BN));
   const int64_t tiles = (int64_t)tm * tn;
   int splits = 1;
-  if (part && tiles < 256 && K >= 8192) {
-    splits = static_cast<int>(std::min<int64_t>(ceil_div(1024, tiles), K / 2048));
+  if (part) {
+    splits = static_cast<int>(k_splits(M, N, K));
     while (splits > 1 && (int64_t)splits * M * N > part_floats) --splits;
   }
   const int k_chunk = std::max(BK, static_cast<int>(round_up(ceil_div(K, splits), BK)));

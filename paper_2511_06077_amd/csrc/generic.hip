@@ -314,7 +314,7 @@ template <int DH, typename OT>
 __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(
     const Unit* __restrict__ units, const WsHeader* __restrict__ hdr, const int32_t* __restrict__ toff,
     const float* __restrict__ Q, const float* __restrict__ KV, int d, const float* __restrict__ a,
-    const float* __restrict__ da, const float* __restrict__ lse, OT* __restrict__ dKV,
+    const float* __restrict__ da, const float* __restrict__ lse, OT* __restrict__ dKV, int64_t ldkv,
     bf16_bits* __restrict__ dKVT, int64_t ldt, int n_heads) {
   __shared__ __attribute__((aligned(16))) float qs[kTargetGroup][DH];
   __shared__ __attribute__((aligned(16))) float das[kTargetGroup][DH];
@@ -378,8 +378,8 @@ __global__ __launch_bounds__(256) void attn_bwd_kv_kernel(
     // Q holds log2(e)/sqrt(d_h) times the true query: dk of the true query
     // is de q / sqrt(d_h) = de * (stored q) * ln 2
     if (on) {
-      store_row<OT>(dKV + (int64_t)tok * 2 * d + j * DH, dk, DH, kLn2);
-      store_row<OT>(dKV + (int64_t)tok * 2 * d + d + j * DH, dv, DH, 1.f);
+      store_row<OT>(dKV + (int64_t)tok * ldkv + j * DH, dk, DH, kLn2);
+      store_row<OT>(dKV + (int64_t)tok * ldkv + d + j * DH, dv, DH, 1.f);
       if (dKVT) {  // transposed copy: consecutive lanes write consecutive rows
 #pragma unroll
         for (int e = 0; e < DH; ++e) {
@@ -458,6 +458,29 @@ __global__ void reduce_chunks_kernel(int64_t n_tgt, int d, const int32_t* __rest
 __global__ void relu_mask_kernel(float* __restrict__ dh, const float* __restrict__ pre, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n && !(pre[i] > 0.f)) dh[i] = 0.f;
+}
+
+// One workgroup per request (and one more for dKVT's padding columns); the
+// row range is clamped to [0, n_hist), so malformed offsets write nothing
+// outside the buffers (the scheduler reports them).
+__global__ void zero_untargeted_kernel(const int32_t* __restrict__ hoff, const int32_t* __restrict__ toff,
+                                       int n_requests, int64_t n_hist, bf16_bits* __restrict__ dKV, int64_t ldkv,
+                                       int cols, bf16_bits* __restrict__ dKVT, int64_t ldt) {
+  const int r = blockIdx.x;
+  int64_t h0, h1;
+  if (r < n_requests) {
+    if (toff[r + 1] != toff[r]) return;
+    h0 = max<int64_t>(0, hoff[r]);
+    h1 = min<int64_t>(n_hist, hoff[r + 1]);
+    const int64_t cnt = (h1 - h0) * cols;
+    for (int64_t e = threadIdx.x; e < cnt; e += blockDim.x) dKV[(h0 + e / cols) * ldkv + e % cols] = 0;
+  } else {
+    h0 = n_hist;
+    h1 = ldt;
+  }
+  if (h1 <= h0) return;
+  const int64_t w = h1 - h0, cnt = w * cols;
+  for (int64_t e = threadIdx.x; e < cnt; e += blockDim.x) dKVT[(e / w) * ldt + h0 + e % w] = 0;
 }
 
 template <typename S, typename D>
@@ -541,19 +564,20 @@ hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* 
 hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
                             const WsHeader* hdr, const int32_t* toff, const float* Q, const float* KV, int d,
                             const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
-                            int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt, hipStream_t st) {
+                            int64_t ldkv, int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt,
+                            hipStream_t st) {
   if (max_units == 0) return hipSuccess;
   if (attn_mfma_supported(d_head))
-    return attn_bwd_mfma(d_head, n_heads, units, max_units, hdr, toff, Q, KV, d, a, da, lse, dq_part, dKV, dkv_bf16,
+    return attn_bwd_mfma(d_head, n_heads, units, max_units, hdr, toff, Q, KV, d, a, da, lse, dq_part, dKV, ldkv, dkv_bf16,
                          dKVT, ldt, n_tgt, st);
   dim3 g(static_cast<unsigned>(max_units), n_heads);
 #define STCA_ATTB(DH)                                                                                      \
   if (dkv_bf16)                                                                                            \
     hipLaunchKernelGGL((attn_bwd_kv_kernel<DH, bf16_bits>), g, dim3(256), 0, st, units, hdr, toff, Q, KV, d, a, \
-                       da, lse, static_cast<bf16_bits*>(dKV), dKVT, ldt, n_heads);                          \
+                       da, lse, static_cast<bf16_bits*>(dKV), ldkv, dKVT, ldt, n_heads);                    \
   else                                                                                                     \
     hipLaunchKernelGGL((attn_bwd_kv_kernel<DH, float>), g, dim3(256), 0, st, units, hdr, toff, Q, KV, d, a, da, \
-                       lse, static_cast<float*>(dKV), nullptr, 0, n_heads);                                 \
+                       lse, static_cast<float*>(dKV), ldkv, nullptr, 0, n_heads);                           \
   hipLaunchKernelGGL(attn_bwd_q_kernel<DH>, g, dim3(256), 0, st, units, hdr, Q, KV, d, a, da, lse, dq_part,  \
                      n_tgt, n_heads)
   switch (d_head) {
@@ -578,6 +602,13 @@ hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const flo
 hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(relu_mask_kernel, grid1(n, 256), dim3(256), 0, st, dh, pre, n);
+  return hipGetLastError();
+}
+
+hipError_t zero_untargeted(const int32_t* hoff, const int32_t* toff, int n_requests, int64_t n_hist,
+                           bf16_bits* dKV, int64_t ldkv, int cols, bf16_bits* dKVT, int64_t ldt, hipStream_t st) {
+  hipLaunchKernelGGL(zero_untargeted_kernel, dim3(static_cast<unsigned>(n_requests + 1)), dim3(256), 0, st, hoff,
+                     toff, n_requests, n_hist, dKV, ldkv, cols, dKVT, ldt);
   return hipGetLastError();
 }
 

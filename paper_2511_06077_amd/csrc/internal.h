@@ -45,14 +45,15 @@ hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* 
 hipError_t convert(int src_bf16, int dst_bf16, const void* src, void* dst, int64_t n, hipStream_t st);
 hipError_t fill_f32(float* dst, float v, int64_t n, hipStream_t st);
 // generic backward pieces
-// dKV ([N_hist][2d], fp32 or bf16 when dkv_bf16) is written for every history
-// row of a request with targets, and with bf16 also its transpose dKVT
-// ([2d][ldt]) when dKVT is not null; rows of requests without targets are left
-// untouched.
+// dKV ([N_hist] rows of 2d, row pitch ldkv elements; fp32 or bf16 when
+// dkv_bf16) is written for every history row of a request with targets, and
+// with bf16 also its transpose dKVT ([2d][ldt]) when dKVT is not null; rows of
+// requests without targets are left untouched.
 hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t max_units,
                             const WsHeader* hdr, const int32_t* toff, const float* Q, const float* KV, int d,
                             const float* a, const float* da, const float* lse, float* dq_part, void* dKV,
-                            int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt, hipStream_t st);
+                            int64_t ldkv, int dkv_bf16, bf16_bits* dKVT, int64_t ldt, int64_t n_tgt,
+                            hipStream_t st);
 // Exact fp32 attention on the fp32 matrix cores (attn_mfma.hip) for d_h in
 // {16, 32, 64}: the same outputs as attn_generic / attn_bwd_generic, which
 // dispatch to them.
@@ -62,10 +63,15 @@ hipError_t attn_fwd_mfma(int d_head, int n_heads, const Unit* units, int64_t max
                          hipStream_t st);
 hipError_t attn_bwd_mfma(int d_head, int n_heads, const Unit* units, int64_t max_units, const WsHeader* hdr,
                          const int32_t* toff, const float* Q, const float* KV, int d, const float* a, const float* da,
-                         const float* lse, float* dq_part, void* dKV, int dkv_bf16, bf16_bits* dKVT, int64_t ldt,
-                         int64_t n_tgt, hipStream_t st);
+                         const float* lse, float* dq_part, void* dKV, int64_t ldkv, int dkv_bf16, bf16_bits* dKVT,
+                         int64_t ldt, int64_t n_tgt, hipStream_t st);
 hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const float* part, float* out,
                          float scale, hipStream_t st);
 hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st);
+// Zero the history rows of requests without targets in dKV ([N_hist][ldkv]
+// bf16, columns [0, cols)) and the matching columns of dKVT ([cols][ldt]), and
+// dKVT's padding columns [n_hist, ldt).
+hipError_t zero_untargeted(const int32_t* hoff, const int32_t* toff, int n_requests, int64_t n_hist,
+                           bf16_bits* dKV, int64_t ldkv, int cols, bf16_bits* dKVT, int64_t ldt, hipStream_t st);
 
 }  // namespace stca
