@@ -191,6 +191,9 @@ def main() -> int:
                     help="time forward + backward steps (the training window workload by default)")
     ap.add_argument("--sl", action="store_true",
                     help="with --backward: a stochastic-length batch (Beta lengths, alpha 0.02, L_avg 2048 of 10240)")
+    ap.add_argument("--paper", action="store_true",
+                    help="instead: the paper-exact stack (stca_forward_paper: SwiGLU + LayerNorm history transform "
+                         "per layer, query fusion, head token z) on the same workload")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead: time a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -205,6 +208,8 @@ def main() -> int:
         return copy_calibration(args)
     if args.backward:
         return train_step(args)
+    if args.paper:
+        return paper_step(args)
     from paper_2511_06077_amd.device import DeviceBatch
     wl = W.WORKLOADS[args.workload]
     t0 = time.time()
@@ -288,6 +293,90 @@ def main() -> int:
     if args.cpu_seconds > 0:
         log("[bench] timing the CPU oracle")
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
+    print(json.dumps(rec), flush=True)
+    return 0
+
+
+def paper_kernel_work(label: str, b: W.Batch):
+    """Algorithmic (flop, bytes) of one launch of a kernel of the paper-exact
+    stack: swiglu_ln = one layer's SwiGLU block (u, v and o products, 6 d F
+    flop per history row) and LayerNorm over every history row, reading X and
+    writing the transformed history once (bf16); fused = that layer's K/V
+    projection of the transformed history and the attention (as the standard
+    stack's fused kernel)."""
+    wl = b.wl
+    d, F = wl.d_model, wl.ffn_hidden
+    Lall = float(b.hist_len.sum())
+    L = b.hist_len.astype(np.float64)
+    m = b.n_tgt.astype(np.float64)
+    sel = (m > 0) & (m <= 32)
+    if label == "swiglu_ln":
+        return 6.0 * Lall * d * F, 2.0 * Lall * d * 2
+    if label == "fused":
+        return 4.0 * L[sel].sum() * d * d + 4.0 * (m[sel] * L[sel]).sum() * d, 2.0 * L[sel].sum() * d
+    return 0.0, 0.0
+
+
+def paper_step(args) -> int:
+    """The paper-exact stack's forward (stca_forward_paper) on the workload:
+    per layer the history's SwiGLU + LayerNorm transform (fused MFMA kernel),
+    the fused projection + attention over it, and the target side (query
+    fusion with W_C, SwiGLU + LayerNorm, head token z).  Same timing protocol
+    as the standard stack: settling steps, W warm-up, K timed plain steps,
+    then K steps with per-kernel HIP events."""
+    import torch
+    from paper_2511_06077_amd.device import PaperDeviceBatch
+    wl = W.WORKLOADS[args.workload]
+    b = W.make_batch(wl, with_grad=False)
+    db = PaperDeviceBatch(b, W.make_paper_weights(wl), device="cuda:0")
+    log(f"[bench] paper stack {wl.name}: workspace {db.ws_bytes / 2**30:.2f} GiB")
+    n_settle = settle(db.forward, args.settle_seconds)
+    ms_step = plain_forward(db, args.steps, args.warmup) / args.steps
+    dev = db.device
+    stream = torch.cuda.current_stream(dev)
+    nl = stca.stca_paper_launch_count(db.dims, db.batch)
+    evs = [stca.HipEvents(nl + 1) for _ in range(args.steps)]
+    torch.cuda.synchronize(dev)
+    for k in range(args.steps):
+        stca.stca_forward_paper_profiled(db.dims, db.batch, db.hist, db.tgt, db.weights, db.z, None, db.ws,
+                                         db.ws_bytes, stream.cuda_stream, evs[k].ev, evs[k].labels)
+    torch.cuda.synchronize(dev)
+    per = {}
+    for e in evs:
+        for k in range(nl):
+            per.setdefault(e.label(k), []).append(e.elapsed_ms(k, k + 1))
+        e.close()
+    log(f"[bench] paper stack {args.steps} steps: {ms_step:.3f} ms/step")
+    kernels = {}
+    for lab, v in per.items():
+        launches = len(v) // args.steps
+        ms = float(np.mean(v))
+        flop, byts = paper_kernel_work(lab, b)
+        ent = {"launches_per_step": launches, "ms_per_launch": ms, "ms_per_step": ms * launches}
+        if flop or byts:
+            ent.update({"tflops": flop / (ms * 1e-3) / 1e12, "gbs": byts / (ms * 1e-3) / 1e9,
+                        "mfma_frac": flop / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                        "hbm_frac": byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS})
+        kernels[lab] = ent
+    dom = max((k for k in kernels if paper_kernel_work(k, b) != (0.0, 0.0)), key=lambda k: kernels[k]["ms_per_step"])
+    flop, byts = paper_kernel_work(dom, b)
+    roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, PEAK_BF16_TFLOPS)
+    roof["kernel"] = dom
+    roof["traffic"] = None
+    n = wl.n_layers
+    bound_ms = sum(max(paper_kernel_work(k, b)[0] / (PEAK_BF16_TFLOPS * 1e12),
+                       paper_kernel_work(k, b)[1] / (PEAK_HBM_GBS * 1e9)) for k in ("swiglu_ln", "fused")) * n * 1e3
+    rec = {"metric": "targets scored/sec, STCA forward (paper-exact stack)",
+           "value": b.n_tgt_total / (ms_step * 1e-3), "unit": "targets/s", "n_gpus": 1, "steps": args.steps,
+           "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True, "scaling": "weak",
+           "vs_baseline": None, "dtype": "bf16" if wl.dtype == "bf16" else "f32", "data": "synthetic",
+           "config": {"workload": wl.name + "_paper", "requests": wl.n_requests,
+                      "targets_per_request": wl.n_targets or list(wl.tgt_range),
+                      "hist_len": wl.hist_len or list(wl.hist_range), "d_model": wl.d_model, "heads": wl.n_heads,
+                      "layers": n, "ffn_hidden": wl.ffn_hidden},
+           "roofline": roof,
+           "history_side_roofline": {"ms": bound_ms, "frac": bound_ms / ms_step},
+           "kernels": kernels, "settle_steps": n_settle}
     print(json.dumps(rec), flush=True)
     return 0
 
