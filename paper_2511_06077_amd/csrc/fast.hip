@@ -277,11 +277,17 @@ struct Online {
 
   // kv: K slices 0, 1 and V slices 0, 1 of history block b (operand order).
   // MFMA row index i of the block holds history row b * 32 + blk_row<RPS>(i).
-  template <int RPS = 1>
-  __device__ __forceinline__ void step(const f16x8 (&kv)[4], int b, const Unit& un, int hi) {
+  // qload(g, qop[g]), when given, fills a column group's query operands right
+  // before its MFMAs (so only one group's are live at a time).
+  struct KeepQ {
+    __device__ __forceinline__ void operator()(int, f16x8 (&)[2]) const {}
+  };
+  template <int RPS = 1, typename QLoad = KeepQ>
+  __device__ __forceinline__ void step(const f16x8 (&kv)[4], int b, const Unit& un, int hi, QLoad qload = {}) {
     const bool full = b * 32 >= un.l0 && b * 32 + 32 <= un.l1;
 #pragma unroll
     for (int g = 0; g < NG; ++g) {
+      qload(g, qop[g]);
       f32x16 s = mfma(kv[0], qop[g][0], f32x16{});
       s = mfma(kv[1], qop[g][1], s);
       if (!full) {
@@ -400,7 +406,7 @@ __global__ __launch_bounds__(64 * H) void attn_kernel(const Unit* __restrict__ u
 // score and P.V MFMAs.
 //
 // The workgroup walks its units' blocks as one stream.  X blocks arrive by
-// direct global-to-LDS loads into a ring of kStages tiles, kStages - 1 blocks
+// direct global-to-LDS loads into a ring of kStages tiles (3 for NG = 2), one fewer blocks
 // ahead of the one in use (each wave loads two 1 KB segments of a block and
 // waits only for its own older loads; one barrier per block publishes the
 // tile and frees the slot read in the previous block).  A unit's queries
@@ -445,6 +451,14 @@ __device__ __forceinline__ void dma16(const void* src, const unsigned char* lds)
   asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(__builtin_amdgcn_readfirstlane(m0)));
 }
 
+// The value unchanged, but opaque to the compiler: quantities derived from it
+// are recomputed where used instead of being hoisted out of the loop and kept
+// live (or spilled) across it.
+__device__ __forceinline__ int opaque(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
+
 // Workgroup barrier without the fences of __syncthreads (whose release would
 // wait for every load in flight, including the ring's prefetches); the memory
 // clobber keeps the compiler from moving LDS accesses across it.
@@ -466,9 +480,16 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
   constexpr int NS = 32 / RPS;      // segments per block (2 per wave)
   constexpr int TILE = NS * kSegPitch;
   constexpr int QA = NG * 32 * DH * 2;  // one wave's query slice of a unit (bytes)
+  // NG = 1 keeps the unit's queries in registers from its first block on (two
+  // query areas suffice); NG = 2 reads them from LDS at every attention step
+  // (16 fewer VGPRs), so a unit's area must outlive its last step: three
+  // areas, and a ring of three tiles to stay within the LDS
+  constexpr bool QREG = NG == 1;
+  constexpr int NQA = QREG ? 2 : 3;
+  constexpr int STG = QREG ? kStages : 3;
   static_assert(NS == 2 * H, "two segments per wave");
-  __shared__ __attribute__((aligned(16))) unsigned char xs[kStages * TILE];
-  __shared__ __attribute__((aligned(16))) unsigned char qs[2 * H * QA];
+  __shared__ __attribute__((aligned(16))) unsigned char xs[STG * TILE];
+  __shared__ __attribute__((aligned(16))) unsigned char qs[NQA * H * QA];
   __shared__ int simd_waves[4];
 
   // this width's units: [0, n_narrow) or [n_narrow, n_units)
@@ -508,7 +529,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
   int q_after = 0;  // blocks issued after the latest query slice
   auto issue_x = [&]() {
     if (lu >= ue) return;
-    unsigned char* slot = xs + (p_load % kStages) * TILE;
+    unsigned char* slot = xs + (p_load % STG) * TILE;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
       const int seg = 2 * wave + i;
@@ -529,17 +550,18 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
   // queries of unit un (the ord-th of this workgroup): target rows of 64 bytes
   // (this head's 32 fp16, QN order), 16 targets per wave load
   auto issue_q = [&](const Unit& un, int ord) {
-    unsigned char* area = qs + ((ord & 1) * H + wave) * QA;
+    unsigned char* area = qs + ((ord % NQA) * H + wave) * QA;
+    const int ql = QREG ? lane : opaque(lane);
 #pragma unroll
     for (int i = 0; i < 2 * NG; ++i) {
-      const int64_t t = min((int64_t)un.t0 + i * 16 + lane / 4, n_tgt - 1);
-      dma16(reinterpret_cast<const unsigned char*>(QN) + (t * D + wave * DH) * 2 + (lane % 4) * 16, area + i * 1024);
+      const int64_t t = min((int64_t)un.t0 + i * 16 + ql / 4, n_tgt - 1);
+      dma16(reinterpret_cast<const unsigned char*>(QN) + (t * D + wave * DH) * 2 + (ql % 4) * 16, area + i * 1024);
     }
     q_after = 0;
   };
   issue_q(lun, 0);
 #pragma unroll
-  for (int i = 0; i < kStages - 1; ++i) issue_x();
+  for (int i = 0; i < STG - 1; ++i) issue_x();
   wait_vm(0);  // the weights are in registers (the loop issues no compiler-visible load)
 
   // this lane's B operand row: MFMA column tcol reads history row blk_row<RPS>(tcol)
@@ -547,7 +569,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
   // The X operands are read kXAhead k-steps ahead of their MFMAs (scheduling
   // barriers keep the compiler from sinking the reads next to their use), so
   // an LDS round trip overlaps 2 kXAhead MFMAs of the same wave.
-  constexpr int kXAhead = 4;
+  constexpr int kXAhead = NG == 1 ? 4 : 2;
   auto project = [&](const unsigned char* tile, f16x8 (&kv)[4]) {
     f32x16 ak = {}, av = {};
     const unsigned char* xp = tile + xrow;
@@ -573,8 +595,8 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
   auto run = [&](auto phase_tag) {
     constexpr int PHASE = decltype(phase_tag)::value;
     Online<H, NG> st;
-    auto init = [&](const Unit& un, int ord) {
-      const unsigned char* area = qs + ((ord & 1) * H + wave) * QA;
+    auto load_q = [&](const Unit& un, int ord) {
+      const unsigned char* area = qs + ((ord % NQA) * H + wave) * QA;
 #pragma unroll
       for (int g = 0; g < NG; ++g) {
         const int tt = g * 32 + tcol;
@@ -582,6 +604,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
         const f16x8* q = reinterpret_cast<const f16x8*>(area + tt * 64);
         st.qop[g][0] = ok ? q[hi] : zero8h();
         st.qop[g][1] = ok ? q[2 + hi] : zero8h();
+      }
+    };
+    auto init = [&](const Unit& un, int ord) {
+      if (QREG) load_q(un, ord);
+#pragma unroll
+      for (int g = 0; g < NG; ++g) {
         st.O[g] = f32x16{};
         st.m[g] = -INFINITY;
         st.l[g] = 0.f;
@@ -592,18 +620,35 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
     // wave's few score and P.V MFMAs and leave both waves in their softmax at
     // the same time.  The attention step runs at raised wave priority: its
     // MFMAs go first and its VALU work overlaps the other wave's projection.
-    auto attend = [&](const f16x8 (&kv)[4], int b, const Unit& un) {
+    auto attend = [&](const f16x8 (&kv)[4], int b, const Unit& un, int ord) {
       __builtin_amdgcn_s_setprio(1);
-      st.template step<RPS>(kv, b, un, hi);
+      if (QREG) {
+        st.template step<RPS>(kv, b, un, hi);
+      } else {
+        const unsigned char* area = qs + ((ord % NQA) * H + wave) * QA;
+        st.template step<RPS>(kv, b, un, hi, [&](int g, f16x8 (&q)[2]) {
+          const int tt = g * 32 + opaque(tcol);
+          const bool ok = tt < un.nt;
+          const f16x8* qp = reinterpret_cast<const f16x8*>(area + tt * 64);
+          q[0] = ok ? qp[hi] : zero8h();
+          q[1] = ok ? qp[2 + hi] : zero8h();
+        });
+      }
       __builtin_amdgcn_s_setprio(0);
+    };
+    auto fin = [&](const Unit& un) {
+      if (QREG)
+        st.finish(un, wave, tcol, hi, part_acc, part_ml, n_tgt);
+      else
+        st.finish(un, opaque(wave), opaque(tcol), opaque(hi), part_acc, part_ml, n_tgt);
     };
     int cu = ub + blockIdx.x;  // compute cursor: unit index, its ordinal, block
     int ck = 0;
     Unit cun = units[cu];
     int cb = cun.b0;
-    f16x8 held[4];  // PHASE 1: K/V of block hb of unit hun, attended to in the next step
+    f16x8 held[4];  // PHASE 1: K/V of block hb of unit hun (ordinal hk), attended to in the next step
     Unit hun = cun;
-    int hb = -1;
+    int hb = -1, hk = 0;
     for (int p_use = 0; cu < ue; ++p_use) {
       const bool first = cb == cun.b0, last = cb + 1 == cun.b1;
       // this wave's part of block p_use (and, at a unit's first block, of its
@@ -612,23 +657,24 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
       wait_vm(first ? min(ahead, 2 * q_after) : ahead);
       ring_barrier();  // everyone's parts; the slot of p_use - 1 is free
       if (last && cu + static_cast<int>(gridDim.x) < ue) issue_q(units[cu + gridDim.x], ck + 1);
-      if (p_load < p_use + kStages) issue_x();
-      const unsigned char* tile = xs + (p_use % kStages) * TILE;
+      if (p_load < p_use + STG) issue_x();
+      const unsigned char* tile = xs + (p_use % STG) * TILE;
       if (PHASE == 0) {
         if (first) init(cun, ck);
         f16x8 kv[4];
         project(tile, kv);
-        attend(kv, cb, cun);
-        if (last) st.finish(cun, wave, tcol, hi, part_acc, part_ml, n_tgt);
+        attend(kv, cb, cun, ck);
+        if (last) fin(cun);
       } else {
         if (hb >= 0) {
-          attend(held, hb, hun);
-          if (hb + 1 == hun.b1) st.finish(hun, wave, tcol, hi, part_acc, part_ml, n_tgt);
+          attend(held, hb, hun, hk);
+          if (hb + 1 == hun.b1) fin(hun);
         }
         if (first) init(cun, ck);
         project(tile, held);
         hun = cun;
         hb = cb;
+        hk = ck;
       }
       if (last) {
         cu += gridDim.x;
@@ -642,8 +688,8 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
       }
     }
     if (PHASE == 1 && hb >= 0) {
-      attend(held, hb, hun);
-      st.finish(hun, wave, tcol, hi, part_acc, part_ml, n_tgt);
+      attend(held, hb, hun, hk);
+      fin(hun);
     }
   };
   if (phase == 0)
