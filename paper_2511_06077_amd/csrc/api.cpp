@@ -53,6 +53,21 @@ bool wide_groups_for(const stca_batch_t* b) {
   return false;
 }
 
+// The bf16 backward projects the history inside its attention kernels (no
+// K/V copy in HBM) when d_h = 32 and every request has at most 32 targets,
+// which the host offsets must show; otherwise K | V are formed by a GEMM and
+// the attention runs exactly in fp32.  STCA_BWD=generic forces the latter.
+bool fused_bwd_for(const stca_dims_t* dims, const stca_batch_t* b) {
+  const char* e = std::getenv("STCA_BWD");
+  if (e && std::strcmp(e, "generic") == 0) return false;
+  if (dims->dtype != STCA_BF16 || dims->d_model / dims->n_heads != 32) return false;
+  if (dims->d_model != 64 && dims->d_model != 128 && dims->d_model != 256) return false;
+  if (!b->tgt_off_host) return false;
+  for (int r = 0; r < b->n_requests; ++r)
+    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > 32) return false;
+  return true;
+}
+
 struct Layout {
   int path;
   int d, h, n, F, dh;
@@ -62,6 +77,7 @@ struct Layout {
   bool any_narrow, any_wide;  // requests with 1..32 / 33+ targets (both true without host offsets)
   bool reord;                 // reordered attention (bf16 path)
   bool wide;                  // materialised K/V, units of up to kWideGroup targets (bf16 path)
+  bool bfused;                // backward with the history projection inside the attention kernels
   int group;                  // targets per attention unit
   // common
   size_t hdr, units, tchunks, part_acc, part_ml, state_a, state_b;
@@ -74,6 +90,7 @@ struct Layout {
   // backward (generic)
   size_t dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
   size_t xt, dkvt, wkvt;
+  size_t fwkp, fwvp;  // fused backward: packed W_K, W_V of every layer
   size_t b_hid, b_dhid, b_ds, b_u, b_du, b_a, b_dq, b_s;  // bf16 copies of backward operands (bf16 path)
   int64_t gpart_floats, nh8;
   size_t total;
@@ -92,6 +109,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
   L->nt = b->n_tgt;
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
   L->reord = p == 1 && !with_backward && reordered_for(dims, b);
+  L->bfused = false;
   L->wide = p == 1 && !with_backward && !L->reord && wide_groups_for(b);
   L->chunk_blocks = chunk_blocks_for(b, device_cus(), L->reord ? 1 : 4);
   L->group = L->reord ? 32 / L->h : (L->wide ? kWideGroup : kTargetGroup);
@@ -145,7 +163,12 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     }
   } else {
     const bool bf = dims->dtype == STCA_BF16;
-    L->kvs = m.take(4 * n * nh * 2 * d);  // every layer's K | V rows, fp32
+    L->bfused = bf && fused_bwd_for(dims, b);
+    L->kvs = L->bfused ? 0 : m.take(4 * n * nh * 2 * d);  // every layer's K | V rows, fp32
+    if (L->bfused) {
+      L->fwkp = m.take(2 * n * d * d);
+      L->fwvp = m.take(2 * n * d * d);
+    }
     // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
     // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
     L->dkv = m.take(bf ? 2 * nh * n * 2 * d : 4 * nh * 2 * d);
@@ -154,7 +177,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->nh8 = round_up(static_cast<int64_t>(nh), 8);
     const size_t nh8 = static_cast<size_t>(L->nh8);
     L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;
-    L->wkvt = bf ? m.take(2 * n * d * 2 * d) : 0;
+    L->wkvt = bf && !L->bfused ? m.take(2 * n * d * 2 * d) : 0;
     L->xt = bf ? m.take(2 * d * nh8) : 0;
     L->dkvt = bf ? m.take(2 * n * 2 * d * nh8) : 0;  // [n 2d][nh8]: every layer's (dK | dV)^T
     L->dwkv = bf ? m.take(4 * d * n * 2 * d) : 0;   // [d][n 2d] fp32
@@ -487,18 +510,30 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                               hipMemcpyDeviceToDevice, st));
       HIPCHK(hipMemcpy2DAsync(wkv_all + (size_t)i * 2 * d + d, (size_t)n * 2 * d * 2, Wv, d * 2, d * 2, d,
                               hipMemcpyDeviceToDevice, st));
-      HIPCHK(transpose_bf16(Wk, d, d, d, WKVT(i), d, d, st));
-      HIPCHK(transpose_bf16(Wv, d, d, d, WKVT(i) + (size_t)d * d, d, d, st));
+      if (!L.bfused) {
+        HIPCHK(transpose_bf16(Wk, d, d, d, WKVT(i), d, d, st));
+        HIPCHK(transpose_bf16(Wv, d, d, d, WKVT(i) + (size_t)d * d, d, d, st));
+      }
     }
     HIPCHK(transpose_bf16(X, d, static_cast<int>(nh), d, xt, nh8, nh8, st));
+    if (L.bfused) {
+      PackJobs pj{};
+      pj.job[0] = {w->wk, at<char>(ws, L.fwkp), d, d, 0};
+      pj.job[1] = {w->wv, at<char>(ws, L.fwvp), d, d, 0};
+      HIPCHK(fast_pack_many(pj, 2, n, st));
+    }
   }
+  // persistent grid of the fused kernels: one workgroup per CU
+  const int fgrid = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(L.max_units, device_cus())));
   HIPCHK(rec.mark("prep"));
   // forward recomputation in fp32: s^(i), u^(i), and per layer K|V, the
   // scaled queries, the attention output and its lse
   HIPCHK(convert(bf, 0, tgt, RS(0), nt * d, st));
   for (int i = 0; i < n; ++i) {
-    float* kv = KVS(i);
-    if (bf) {
+    float* kv = L.bfused ? nullptr : KVS(i);
+    if (L.bfused) {
+      // K | V stay inside the attention kernels
+    } else if (bf) {
       HIPCHK(gemm_mfma(static_cast<int>(nh), 2 * d, d, static_cast<const bf16_bits*>(hist), d, 0, WKVT(i), d, 1,
                        kv, 2 * d, 1.f, 0, nullptr, 0, st));
     } else {
@@ -507,12 +542,28 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       HIPCHK(gemm(0, 0, nh, d, d, hist, d, 0, W(w->wv, i, (size_t)d * d), d, 0, kv + d, 2 * d, 1.f, kEpiStore,
                   nullptr, 0, nullptr));
     }
-    HIPCHK(rec.mark("kv_gemm"));
+    if (!L.bfused) HIPCHK(rec.mark("kv_gemm"));
     HIPCHK(gemm(0, bf, nt, d, d, RS(i), d, 0, W(w->wq, i, (size_t)d * d), d, 0, RQ(i), d, qscale, kEpiStore,
                 nullptr, 0, nullptr));
     HIPCHK(rec.mark("target_gemm"));
-    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, RQ(i), kv, d, at<float>(ws, L.part_acc),
-                        at<float>(ws, L.part_ml), nt, st));
+    if (L.bfused) {
+      FastAttnFwdPrecise f{};
+      f.units = units;
+      f.hdr = hdr;
+      f.X = hist;
+      f.n_hist = nh;
+      f.WkP = at<char>(ws, L.fwkp);
+      f.WvP = at<char>(ws, L.fwvp);
+      f.layer = i;
+      f.Q = RQ(i);
+      f.part_acc = at<float>(ws, L.part_acc);
+      f.part_ml = at<char>(ws, L.part_ml);
+      f.n_tgt = nt;
+      HIPCHK(fast_attn_fwd_precise(d, f, fgrid, st));
+    } else {
+      HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, RQ(i), kv, d, at<float>(ws, L.part_acc),
+                          at<float>(ws, L.part_ml), nt, st));
+    }
     HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml), RA(i), RL(i),
                          st));
     HIPCHK(rec.mark("attn_fwd"));
@@ -539,7 +590,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     const float* s = RS(i);
     const float* u = RU(i);
     const float* a = RA(i);
-    const float* kv = KVS(i);
+    const float* kv = L.bfused ? nullptr : KVS(i);
     const void* W1 = W(w->w1, i, (size_t)d * F);
     const void* W2 = W(w->w2, i, (size_t)d * F);
     const void* Wo = W(w->wo, i, (size_t)d * d);
@@ -593,8 +644,31 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     // attention (softmax weights rebuilt from the same q, K, V and lse that
     // gave a, so rowsum(dA * A) matches them)
     void* dkv_i = bf ? static_cast<void*>(static_cast<bf16_bits*>(dkv) + (size_t)i * 2 * d) : dkv;
-    HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, b->tgt_off, RQ(i), kv, d, a, da, RL(i), dqp, dkv_i,
-                            bf ? n * 2 * d : 2 * d, bf, bf ? dkvt + (size_t)i * 2 * d * nh8 : nullptr, nh8, nt, st));
+    if (L.bfused) {
+      FastAttnBwd f{};
+      f.units = units;
+      f.hdr = hdr;
+      f.X = hist;
+      f.n_hist = nh;
+      f.WkP = at<char>(ws, L.fwkp);
+      f.WvP = at<char>(ws, L.fwvp);
+      f.layer = i;
+      f.Q = RQ(i);
+      f.a = a;
+      f.da = da;
+      f.lse = RL(i);
+      f.dKV = static_cast<bf16_bits*>(dkv_i);
+      f.ldkv = n * 2 * d;
+      f.dKVT = dkvt + (size_t)i * 2 * d * nh8;
+      f.ldt = nh8;
+      f.dq_part = dqp;
+      f.n_tgt = nt;
+      HIPCHK(fast_attn_bwd(d, f, fgrid, st));
+    } else {
+      HIPCHK(attn_bwd_generic(L.dh, h, units, L.max_units, hdr, b->tgt_off, RQ(i), kv, d, a, da, RL(i), dqp, dkv_i,
+                              bf ? n * 2 * d : 2 * d, bf, bf ? dkvt + (size_t)i * 2 * d * nh8 : nullptr, nh8, nt,
+                              st));
+    }
     HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
     HIPCHK(rec.mark("attn_bwd"));
     // q = s Wq
@@ -755,6 +829,7 @@ int stca_backward_launch_count(const stca_dims_t* dims, const stca_batch_t* batc
   if (!make_layout(dims, batch, 1, true, &L)) return -1;
   // sched, prep, 4 per layer (recomputation), prep, then per layer 5 (fp32)
   // or 3 plus the two history-side products of every layer (bf16), out
+  if (L.bfused) return 6 + 6 * L.n;  // no K|V product per layer
   return dims->dtype == STCA_BF16 ? 6 + 7 * L.n : 4 + 9 * L.n;
 }
 

@@ -51,6 +51,48 @@ hipError_t fast_fused(int D, int wide, const Unit* units, const WsHeader* hdr, i
 // K4: combine partials, W_O, residual FFN, next queries.
 hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st);
 
+// Attention backward with the history projection inside the kernel
+// (bwd_fused.hip), for units of at most 32 targets (one unit per history
+// chunk of a request): writes this layer's dK | dV rows ([N_hist] rows of
+// pitch ldkv, dK in columns [0, D), dV in [D, 2D)) and their transpose ([2D]
+// rows of pitch ldt) for the history rows of every unit, and each unit's dq
+// partial ([chunk][n_tgt][D], scaled by 1/sqrt(d_h)).  Q: fp32 queries scaled
+// by log2(e)/sqrt(d_h); a, da: attention output and its gradient; lse: the
+// forward's natural log-sum-exp per (target, head).
+struct FastAttnBwd {
+  const void* units;
+  const void* hdr;
+  const void* X;
+  int64_t n_hist;
+  const void *WkP, *WvP;
+  int layer;
+  const float *Q, *a, *da, *lse;
+  bf16_bits* dKV;
+  int64_t ldkv;
+  bf16_bits* dKVT;
+  int64_t ldt;
+  float* dq_part;
+  int64_t n_tgt;
+};
+hipError_t fast_attn_bwd(int D, const FastAttnBwd& f, int grid, hipStream_t st);
+// The forward attention recomputed for the backward (bwd_fused.hip), history
+// projected inside the kernel and the attention products evaluated to about
+// fp32 accuracy (two-term fp16 operands): the same per-chunk partials as
+// fast_fused, for units of at most 32 targets.
+struct FastAttnFwdPrecise {
+  const void* units;
+  const void* hdr;
+  const void* X;
+  int64_t n_hist;
+  const void *WkP, *WvP;
+  int layer;
+  const float* Q;  // [n_tgt][D], scaled by log2(e)/sqrt(d_h)
+  float* part_acc;
+  void* part_ml;
+  int64_t n_tgt;
+};
+hipError_t fast_attn_fwd_precise(int D, const FastAttnFwdPrecise& f, int grid, hipStream_t st);
+
 // Reordered single-query attention (reordered.hip) for units of at most
 // 32 / H targets: U = per-head Q W_K^j^T (bf16 hi and lo terms
 // [n_tgt][H][2][D]), the attention

@@ -166,3 +166,29 @@ def test_wide_groups_selection(monkeypatch):
     assert stca.stca_forward_launch_count(dims(), few) == 3 + 3 * n
     monkeypatch.setenv("STCA_KV", "fused")
     assert stca.stca_forward_launch_count(dims(), many) == 3 + 3 * n
+
+
+def test_fused_backward_selection(monkeypatch):
+    """The bf16 backward keeps K | V inside its attention kernels (6 + 6 n
+    phases, no K|V product per layer) when the host offsets show at most 32
+    targets per request; more targets, no host offsets, fp32 storage or
+    STCA_BWD=generic take the K|V product and the exact fp32 attention
+    (6 + 7 n, 4 + 9 n for fp32), and only that form sizes the fp32 K|V
+    buffer of every layer into the workspace."""
+    monkeypatch.delenv("STCA_BWD", raising=False)
+    n = GOOD_DIMS["n_layers"]
+    small, keep1 = fake_batch([0, 40, 100, 101], [0, 32, 33, 40])   # m = 32, 1, 7
+    big, keep2 = fake_batch([0, 40, 100], [0, 33, 40])               # m = 33
+    nohost = stca.batch(3, 101, 40, 0x10000, 0x20000, None, None)
+    assert stca.stca_backward_launch_count(dims(), small) == 6 + 6 * n
+    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4), small) == 6 + 6 * n
+    assert stca.stca_backward_launch_count(dims(d_model=64, n_heads=2), small) == 6 + 6 * n
+    assert stca.stca_backward_launch_count(dims(), big) == 6 + 7 * n
+    assert stca.stca_backward_launch_count(dims(), nohost) == 6 + 7 * n
+    assert stca.stca_backward_launch_count(dims(d_model=256, n_heads=4), small) == 6 + 7 * n  # d_h = 64
+    assert stca.stca_backward_launch_count(dims(dtype=stca.STCA_F32), small) == 4 + 9 * n
+    fused = stca.stca_workspace_size(dims(), small, True)
+    monkeypatch.setenv("STCA_BWD", "generic")
+    assert stca.stca_backward_launch_count(dims(), small) == 6 + 7 * n
+    generic = stca.stca_workspace_size(dims(), small, True)
+    assert generic >= fused + 4 * n * 101 * 2 * 256 - 2 * 2 * n * 256 * 256 - 2 * 40 * 256

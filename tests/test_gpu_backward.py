@@ -72,6 +72,36 @@ def test_ragged_tail_gradients(torch, chunk_override, dtype, d, h):
     check(b, gpu_grads(torch, b), TOL[dtype])
 
 
+@pytest.mark.parametrize("d,h", [(256, 8), (128, 4), (64, 2)])
+def test_fused_projection_gradients(torch, chunk_override, d, h):
+    """Requests of at most 32 targets: the backward projects the history
+    inside its attention kernels.  Ragged histories (one row, block tails,
+    blocks shared by two requests, a request without targets), several
+    history chunks per request, every gradient against the oracle."""
+    chunk_override(2)
+    b = W.make_custom_batch("gfused", [1, 33, 130, 64, 7, 300], [2, 31, 0, 17, 1, 32], d_model=d, n_heads=h,
+                            n_layers=2, dtype="bf16", seed=37, with_grad=True)
+    check(b, gpu_grads(torch, b), TOL["bf16"])
+
+
+def test_fused_and_generic_backward_agree(torch, chunk_override, monkeypatch):
+    """The same batch through the fused backward and through the K|V product
+    with the exact fp32 attention (STCA_BWD=generic): both within the bar of
+    the oracle, and within the bar of each other."""
+    chunk_override(None)
+    b = W.make_custom_batch("gboth", [512, 77, 1024, 5], [16, 3, 32, 1], d_model=256, n_heads=8, n_layers=4,
+                            dtype="bf16", seed=41, with_grad=True)
+    g_fused = gpu_grads(torch, b)
+    monkeypatch.setenv("STCA_BWD", "generic")
+    g_gen = gpu_grads(torch, b)
+    check(b, g_fused, TOL["bf16"])
+    check(b, g_gen, TOL["bf16"])
+    for k in GRADS:
+        e = tensor_err(g_fused[k], g_gen[k])
+        print(f"[grad] fused vs generic {k}: {e:.1e}", flush=True)
+        assert e <= TOL["bf16"], (k, e)
+
+
 def test_training_window_gradients(torch, chunk_override):
     """256 requests x 16 targets, L = 2048, d = 256, 4 layers (the training
     window).  History and target gradients are per request, so they are
