@@ -25,8 +25,8 @@ FLAGS = [
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     "-I", os.path.join(ROOT, "include"),
 ]
-SOURCES = ["sched.hip", "generic.hip", "attn_mfma.hip", "fast.hip", "bwd_fused.hip", "reordered.hip", "gemm.hip",
-           "paper.hip", "api.cpp", "api_paper.cpp", "sl_batch.cpp"]
+SOURCES = ["sched.hip", "generic.hip", "attn_mfma.hip", "fast.hip", "bwd_fused.hip", "bwd_update.hip",
+           "reordered.hip", "gemm.hip", "paper.hip", "api.cpp", "api_paper.cpp", "sl_batch.cpp"]
 
 
 def _compile(src: str, extra) -> str:

@@ -54,14 +54,17 @@ bool wide_groups_for(const stca_batch_t* b) {
 }
 
 // The bf16 backward projects the history inside its attention kernels (no
-// K/V copy in HBM) when d_h = 32 and every request has at most 32 targets,
-// which the host offsets must show; otherwise K | V are formed by a GEMM and
-// the attention runs exactly in fp32.  STCA_BWD=generic forces the latter.
+// K/V copy in HBM) and recomputes the target side in one kernel per layer
+// when d_h = 32, the FFN width is a multiple of d and every request has at
+// most 32 targets, which the host offsets must show; otherwise K | V are
+// formed by a GEMM, the attention runs exactly in fp32 and the target side as
+// separate GEMMs.  STCA_BWD=generic forces the latter.
 bool fused_bwd_for(const stca_dims_t* dims, const stca_batch_t* b) {
   const char* e = std::getenv("STCA_BWD");
   if (e && std::strcmp(e, "generic") == 0) return false;
   if (dims->dtype != STCA_BF16 || dims->d_model / dims->n_heads != 32) return false;
   if (dims->d_model != 64 && dims->d_model != 128 && dims->d_model != 256) return false;
+  if (dims->ffn_hidden % dims->d_model != 0) return false;
   if (!b->tgt_off_host) return false;
   for (int r = 0; r < b->n_requests; ++r)
     if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > 32) return false;
@@ -90,7 +93,7 @@ struct Layout {
   // backward (generic)
   size_t dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
   size_t xt, dkvt, wkvt;
-  size_t fwkp, fwvp;  // fused backward: packed W_K, W_V of every layer
+  size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp;  // fused backward: every layer's weights as bf16 operand tiles
   size_t b_hid, b_dhid, b_ds, b_u, b_du, b_a, b_dq, b_s;  // bf16 copies of backward operands (bf16 path)
   int64_t gpart_floats, nh8;
   size_t total;
@@ -168,6 +171,10 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     if (L->bfused) {
       L->fwkp = m.take(2 * n * d * d);
       L->fwvp = m.take(2 * n * d * d);
+      L->fwop = m.take(2 * n * d * d);
+      L->fwqp = m.take(2 * n * d * d);
+      L->fw1p = m.take(2 * n * d * F);
+      L->fw2p = m.take(2 * n * d * F);
     }
     // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
     // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
@@ -520,7 +527,11 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       PackJobs pj{};
       pj.job[0] = {w->wk, at<char>(ws, L.fwkp), d, d, 0};
       pj.job[1] = {w->wv, at<char>(ws, L.fwvp), d, d, 0};
-      HIPCHK(fast_pack_many(pj, 2, n, st));
+      pj.job[2] = {w->wo, at<char>(ws, L.fwop), d, d, 0};
+      pj.job[3] = {w->wq, at<char>(ws, L.fwqp), d, d, 0};
+      pj.job[4] = {w->w1, at<char>(ws, L.fw1p), d, F, 0};
+      pj.job[5] = {w->w2, at<char>(ws, L.fw2p), F, d, 0};
+      HIPCHK(fast_pack_many(pj, 6, n, st));
     }
   }
   // persistent grid of the fused kernels: one workgroup per CU
@@ -528,12 +539,57 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   HIPCHK(rec.mark("prep"));
   // forward recomputation in fp32: s^(i), u^(i), and per layer K|V, the
   // scaled queries, the attention output and its lse
-  HIPCHK(convert(bf, 0, tgt, RS(0), nt * d, st));
-  for (int i = 0; i < n; ++i) {
-    float* kv = L.bfused ? nullptr : KVS(i);
-    if (L.bfused) {
-      // K | V stay inside the attention kernels
-    } else if (bf) {
+  UpdatePrecise up{};
+  if (L.bfused) {
+    up.n_layers = n;
+    up.F = F;
+    up.n_tgt = nt;
+    up.tgt = static_cast<const bf16_bits*>(tgt);
+    up.tchunks = tch;
+    up.part_acc = at<float>(ws, L.part_acc);
+    up.part_ml = at<float2>(ws, L.part_ml);
+    up.WoP = at<char>(ws, L.fwop);
+    up.W1P = at<char>(ws, L.fw1p);
+    up.W2P = at<char>(ws, L.fw2p);
+    up.WqP = at<char>(ws, L.fwqp);
+    up.mode = 0;
+    up.s_out = RS(0);
+    up.q_out = RQ(0);
+    HIPCHK(fast_update_precise(d, up, st));
+    HIPCHK(rec.mark("target_gemm"));
+  } else {
+    HIPCHK(convert(bf, 0, tgt, RS(0), nt * d, st));
+  }
+  for (int i = 0; i < n && L.bfused; ++i) {
+    FastAttnFwdPrecise f{};
+    f.units = units;
+    f.hdr = hdr;
+    f.X = hist;
+    f.n_hist = nh;
+    f.WkP = at<char>(ws, L.fwkp);
+    f.WvP = at<char>(ws, L.fwvp);
+    f.layer = i;
+    f.Q = RQ(i);
+    f.part_acc = at<float>(ws, L.part_acc);
+    f.part_ml = at<char>(ws, L.part_ml);
+    f.n_tgt = nt;
+    HIPCHK(fast_attn_fwd_precise(d, f, fgrid, st));
+    HIPCHK(rec.mark("attn_fwd"));
+    up.mode = 1;
+    up.layer = i;
+    up.s_in = RS(i);
+    up.a_out = RA(i);
+    up.lse_out = RL(i);
+    up.u_out = RU(i);
+    up.h_out = RH(i);
+    up.s_out = RS(i + 1);
+    up.q_out = i + 1 < n ? RQ(i + 1) : nullptr;
+    HIPCHK(fast_update_precise(d, up, st));
+    HIPCHK(rec.mark("target_gemm"));
+  }
+  for (int i = 0; i < n && !L.bfused; ++i) {
+    float* kv = KVS(i);
+    if (bf) {
       HIPCHK(gemm_mfma(static_cast<int>(nh), 2 * d, d, static_cast<const bf16_bits*>(hist), d, 0, WKVT(i), d, 1,
                        kv, 2 * d, 1.f, 0, nullptr, 0, st));
     } else {
@@ -542,28 +598,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       HIPCHK(gemm(0, 0, nh, d, d, hist, d, 0, W(w->wv, i, (size_t)d * d), d, 0, kv + d, 2 * d, 1.f, kEpiStore,
                   nullptr, 0, nullptr));
     }
-    if (!L.bfused) HIPCHK(rec.mark("kv_gemm"));
+    HIPCHK(rec.mark("kv_gemm"));
     HIPCHK(gemm(0, bf, nt, d, d, RS(i), d, 0, W(w->wq, i, (size_t)d * d), d, 0, RQ(i), d, qscale, kEpiStore,
                 nullptr, 0, nullptr));
     HIPCHK(rec.mark("target_gemm"));
-    if (L.bfused) {
-      FastAttnFwdPrecise f{};
-      f.units = units;
-      f.hdr = hdr;
-      f.X = hist;
-      f.n_hist = nh;
-      f.WkP = at<char>(ws, L.fwkp);
-      f.WvP = at<char>(ws, L.fwvp);
-      f.layer = i;
-      f.Q = RQ(i);
-      f.part_acc = at<float>(ws, L.part_acc);
-      f.part_ml = at<char>(ws, L.part_ml);
-      f.n_tgt = nt;
-      HIPCHK(fast_attn_fwd_precise(d, f, fgrid, st));
-    } else {
-      HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, RQ(i), kv, d, at<float>(ws, L.part_acc),
-                          at<float>(ws, L.part_ml), nt, st));
-    }
+    HIPCHK(attn_generic(L.dh, h, units, L.max_units, hdr, RQ(i), kv, d, at<float>(ws, L.part_acc),
+                        at<float>(ws, L.part_ml), nt, st));
     HIPCHK(merge_generic(L.dh, h, nt, tch, at<float>(ws, L.part_acc), at<float>(ws, L.part_ml), RA(i), RL(i),
                          st));
     HIPCHK(rec.mark("attn_fwd"));
@@ -829,7 +869,9 @@ int stca_backward_launch_count(const stca_dims_t* dims, const stca_batch_t* batc
   if (!make_layout(dims, batch, 1, true, &L)) return -1;
   // sched, prep, 4 per layer (recomputation), prep, then per layer 5 (fp32)
   // or 3 plus the two history-side products of every layer (bf16), out
-  if (L.bfused) return 6 + 6 * L.n;  // no K|V product per layer
+  // fused: sched, prep, the initial update, 2 per layer (attention, update), prep,
+  // 3 per layer, dW_KV, dX, out
+  if (L.bfused) return 7 + 5 * L.n;
   return dims->dtype == STCA_BF16 ? 6 + 7 * L.n : 4 + 9 * L.n;
 }
 

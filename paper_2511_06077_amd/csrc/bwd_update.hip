@@ -1,0 +1,213 @@
+// Target-side recomputation of the backward pass, one launch per layer: the
+// merge of the attention partials into a (and its log-sum-exp), then
+//   u = s + a W_O,  h = ReLU(u W_1),  s' = u + h W_2,  q' = s' W_Q^{next}
+// (the layer output of Sec. 3.1 under the residual FFN stacking) for 32
+// targets per workgroup, keeping every intermediate the backward needs in
+// fp32.  These products decide the ReLU gates, so they are evaluated to fp32
+// accuracy on the bf16 matrix cores: each fp32 activation is split into three
+// bf16 terms (8 + 8 + 8 significant bits, the whole fp32 mantissa, over
+// fp32's exponent range) and multiplied with the bf16 weights term by term;
+// every product of two bf16 values is exact in fp32 and the sums are fp32.
+//
+// Each wave forms a 32 x 32 output tile (its 32 output columns for the
+// workgroup's 32 targets) as acc = W^T act^T: A operand = packed weight tile
+// (lane = output column), B operand = activations staged in LDS (lane =
+// target), result lane = target, element v = output column 8 (v/4) + 4 hi +
+// v%4.
+#include "common.h"
+#include "fast.h"
+
+namespace stca {
+
+namespace {
+
+constexpr int DH = 32;
+
+__device__ __forceinline__ f32x16 mma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePrecise A) {
+  constexpr int NW = D / 32;
+  constexpr int H = D / DH;
+  constexpr int KS = D / 16;
+  constexpr int AROW = D + 8;  // padded LDS row (bf16 elements)
+  // three bf16 terms of the 32 current activation rows, and of D hidden
+  // columns at a time
+  __shared__ __attribute__((aligned(16))) bf16_bits act[3][32 * AROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits hid[3][32 * AROW];
+  const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tcol = lane % 32, hi = lane / 32;
+  const int64_t tb = (int64_t)blockIdx.x * 32;
+  const int64_t t = tb + tcol;
+  const bool tok = t < A.n_tgt;
+  const int F = A.F;
+
+  // stage 4 consecutive fp32 values (row r, columns c..c+3) as three bf16 terms
+  auto put4 = [&](bf16_bits (*buf)[32 * AROW], int r, int c, float x0, float x1, float x2, float x3) {
+    const float x[4] = {x0, x1, x2, x3};
+    uint32_t pk[3][2];
+#pragma unroll
+    for (int e = 0; e < 4; e += 2) {
+      float a0 = x[e], a1 = x[e + 1];
+#pragma unroll
+      for (int term = 0; term < 3; ++term) {
+        const bf16_bits b0 = from_f32<bf16_bits>(a0), b1 = from_f32<bf16_bits>(a1);
+        pk[term][e / 2] = (uint32_t)b0 | ((uint32_t)b1 << 16);
+        a0 -= to_f32(b0);
+        a1 -= to_f32(b1);
+      }
+    }
+#pragma unroll
+    for (int term = 0; term < 3; ++term)
+      *reinterpret_cast<uint2*>(buf[term] + r * AROW + c) = make_uint2(pk[term][0], pk[term][1]);
+  };
+  // a wave's result tile (lane = target tcol, elements = columns col0 + 8 q + 4 hi + e)
+  auto put_tile = [&](bf16_bits (*buf)[32 * AROW], int col0, const f32x16& v) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      put4(buf, tcol, col0 + 8 * q + 4 * hi, v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  };
+  auto store_tile = [&](float* dst, int64_t ld, int col0, const f32x16& v) {
+    if (!tok) return;
+    float* p = dst + t * ld + col0 + 4 * hi;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<float4*>(p + 8 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  };
+  auto load_tile = [&](const float* src, int64_t ld, int col0) {
+    f32x16 v = {};
+    if (tok) {
+      const float* p = src + t * ld + col0 + 4 * hi;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 x = *reinterpret_cast<const float4*>(p + 8 * q);
+        v[4 * q] = x.x, v[4 * q + 1] = x.y, v[4 * q + 2] = x.z, v[4 * q + 3] = x.w;
+      }
+    }
+    return v;
+  };
+  // acc += W^T act^T over KS k-steps, packed weight tile Wp ([KS][64] vectors)
+  auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits (*src)[32 * AROW], f32x16 acc) {
+#pragma unroll 4
+    for (int k = 0; k < KS; ++k) {
+      const bf16x8 wt = Wp[k * 64 + lane];
+#pragma unroll
+      for (int term = 0; term < 3; ++term)
+        acc = mma(wt, *reinterpret_cast<const bf16x8*>(src[term] + tcol * AROW + 8 * hi + 16 * k), acc);
+    }
+    return acc;
+  };
+  const bf16x8* WoP = static_cast<const bf16x8*>(A.WoP);
+  const bf16x8* W1P = static_cast<const bf16x8*>(A.W1P);
+  const bf16x8* W2P = static_cast<const bf16x8*>(A.W2P);
+  const bf16x8* WqP = static_cast<const bf16x8*>(A.WqP);
+  const float qscale = kLog2e * rsqrtf(static_cast<float>(DH));
+
+  f32x16 s_next;
+  if (A.mode == 0) {
+    // s^(0) = x_t
+    for (int c = threadIdx.x; c < 32 * D / 4; c += 64 * NW) {
+      const int row = c / (D / 4), col = (c % (D / 4)) * 4;
+      float x[4] = {0.f, 0.f, 0.f, 0.f};
+      if (tb + row < A.n_tgt) {
+        const uint2 v = *reinterpret_cast<const uint2*>(A.tgt + (tb + row) * D + col);
+        x[0] = to_f32((bf16_bits)(v.x & 0xffff)), x[1] = to_f32((bf16_bits)(v.x >> 16));
+        x[2] = to_f32((bf16_bits)(v.y & 0xffff)), x[3] = to_f32((bf16_bits)(v.y >> 16));
+        *reinterpret_cast<float4*>(A.s_out + (tb + row) * D + col) = make_float4(x[0], x[1], x[2], x[3]);
+      }
+      put4(act, row, col, x[0], x[1], x[2], x[3]);
+    }
+    __syncthreads();
+  } else {
+    // merge the chunk partials: two threads per (target, head), 16 dims each
+    {
+      const int pair = threadIdx.x >> 1, half = threadIdx.x & 1;
+      for (int pp = pair; pp < 32 * H; pp += 32 * NW) {
+        const int row = pp / H, j = pp % H;
+        const int64_t tt = tb + row;
+        float av[16];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) av[i] = 0.f;
+        if (tt < A.n_tgt) {
+          const int nch = A.tchunks[tt];
+          float M = -INFINITY;
+          for (int c = 0; c < nch; ++c) M = fmaxf(M, A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j].x);
+          float L = 0.f;
+          for (int c = 0; c < nch; ++c) {
+            const float2 ml = A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j];
+            const float wc = exp2f(ml.x - M);
+            L += wc * ml.y;
+            const float4* pa =
+                reinterpret_cast<const float4*>(A.part_acc + ((int64_t)c * A.n_tgt + tt) * D + j * DH + half * 16);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              const float4 x = pa[q];
+              av[4 * q] += wc * x.x, av[4 * q + 1] += wc * x.y, av[4 * q + 2] += wc * x.z, av[4 * q + 3] += wc * x.w;
+            }
+          }
+          const float inv = 1.f / L;
+#pragma unroll
+          for (int i = 0; i < 16; ++i) av[i] *= inv;
+          float4* sa = reinterpret_cast<float4*>(A.a_out + tt * D + j * DH + half * 16);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) sa[q] = make_float4(av[4 * q], av[4 * q + 1], av[4 * q + 2], av[4 * q + 3]);
+          if (half == 0) A.lse_out[tt * H + j] = (M + log2f(L)) * kLn2;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+          put4(act, row, j * DH + half * 16 + 4 * q, av[4 * q], av[4 * q + 1], av[4 * q + 2], av[4 * q + 3]);
+      }
+    }
+    __syncthreads();
+    // u = s + a W_O
+    f32x16 u = gemm(WoP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, load_tile(A.s_in, D, 32 * w));
+    store_tile(A.u_out, D, 32 * w, u);
+    __syncthreads();  // every wave is done reading a
+    put_tile(act, 32 * w, u);
+    __syncthreads();
+    // s' = u + ReLU(u W_1) W_2, D hidden columns at a time
+    s_next = u;
+    const int KSF = F / 16;
+    for (int c = 0; c < F / D; ++c) {
+      f32x16 h = gemm(W1P + ((int64_t)A.layer * (F / 32) + c * NW + w) * KS * 64, act, f32x16{});
+#pragma unroll
+      for (int v = 0; v < 16; ++v) h[v] = fmaxf(h[v], 0.f);
+      store_tile(A.h_out, F, c * D + 32 * w, h);
+      put_tile(hid, 32 * w, h);
+      __syncthreads();
+      s_next = gemm(W2P + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64, hid, s_next);
+      __syncthreads();  // hid is rewritten by the next chunk
+    }
+    store_tile(A.s_out, D, 32 * w, s_next);
+    if (A.layer + 1 >= A.n_layers) return;
+    put_tile(act, 32 * w, s_next);  // act (u) was last read before the previous barrier
+    __syncthreads();
+  }
+  // next queries q' = s' W_Q^{next}, scaled into log2 units
+  const int ql = A.mode == 0 ? 0 : A.layer + 1;
+  f32x16 q = gemm(WqP + ((int64_t)(ql * NW + w) * KS) * 64, act, f32x16{});
+#pragma unroll
+  for (int v = 0; v < 16; ++v) q[v] *= qscale;
+  store_tile(A.q_out, D, 32 * w, q);
+}
+
+}  // namespace
+
+hipError_t fast_update_precise(int D, const UpdatePrecise& f, hipStream_t st) {
+  if (f.n_tgt == 0) return hipSuccess;
+  if (f.F % D != 0) return hipErrorInvalidValue;
+  dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
+#define STCA_UPDP(DD) hipLaunchKernelGGL(update_precise_kernel<DD>, g, dim3(64 * (DD / 32)), 0, st, f)
+  switch (D) {
+    case 64: STCA_UPDP(64); break;
+    case 128: STCA_UPDP(128); break;
+    case 256: STCA_UPDP(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_UPDP
+  return hipGetLastError();
+}
+
+}  // namespace stca

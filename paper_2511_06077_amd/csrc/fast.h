@@ -92,6 +92,25 @@ struct FastAttnFwdPrecise {
   int64_t n_tgt;
 };
 hipError_t fast_attn_fwd_precise(int D, const FastAttnFwdPrecise& f, int grid, hipStream_t st);
+// Target-side recomputation for the backward (bwd_update.hip), fp32-accurate
+// on the bf16 matrix cores.  mode 0: s^(0) = x_t (s_out), q^(0) (q_out).
+// mode 1 (layer): merge the partials into a (a_out) and lse (lse_out), u =
+// s_in + a W_O (u_out), h = ReLU(u W_1) (h_out, [n_tgt][F]), s' = u + h W_2
+// (s_out) and, before the last layer, q' (q_out).  Queries are scaled by
+// log2(e)/sqrt(d_h).  Weights packed as bf16 operand tiles (fast_pack_many
+// with to_f16 = 0); F a multiple of D.
+struct UpdatePrecise {
+  int mode, layer, n_layers, F;
+  int64_t n_tgt;
+  const bf16_bits* tgt;
+  const int32_t* tchunks;
+  const float* part_acc;
+  const float2* part_ml;
+  const float* s_in;
+  float *a_out, *lse_out, *u_out, *h_out, *s_out, *q_out;
+  const void *WoP, *W1P, *W2P, *WqP;
+};
+hipError_t fast_update_precise(int D, const UpdatePrecise& f, hipStream_t st);
 
 // Reordered single-query attention (reordered.hip) for units of at most
 // 32 / H targets: U = per-head Q W_K^j^T (bf16 hi and lo terms

@@ -169,10 +169,10 @@ def test_wide_groups_selection(monkeypatch):
 
 
 def test_fused_backward_selection(monkeypatch):
-    """The bf16 backward keeps K | V inside its attention kernels (6 + 6 n
+    """The bf16 backward keeps K | V inside its attention kernels (7 + 5 n
     phases, no K|V product per layer) when the host offsets show at most 32
-    targets per request; more targets, no host offsets, fp32 storage or
-    STCA_BWD=generic take the K|V product and the exact fp32 attention
+    targets per request; more targets, no host offsets, fp32 storage, an FFN
+    width that is not a multiple of d or STCA_BWD=generic take the K|V product and the exact fp32 attention
     (6 + 7 n, 4 + 9 n for fp32), and only that form sizes the fp32 K|V
     buffer of every layer into the workspace."""
     monkeypatch.delenv("STCA_BWD", raising=False)
@@ -180,15 +180,19 @@ def test_fused_backward_selection(monkeypatch):
     small, keep1 = fake_batch([0, 40, 100, 101], [0, 32, 33, 40])   # m = 32, 1, 7
     big, keep2 = fake_batch([0, 40, 100], [0, 33, 40])               # m = 33
     nohost = stca.batch(3, 101, 40, 0x10000, 0x20000, None, None)
-    assert stca.stca_backward_launch_count(dims(), small) == 6 + 6 * n
-    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4), small) == 6 + 6 * n
-    assert stca.stca_backward_launch_count(dims(d_model=64, n_heads=2), small) == 6 + 6 * n
+    assert stca.stca_backward_launch_count(dims(), small) == 7 + 5 * n
+    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4), small) == 7 + 5 * n
+    assert stca.stca_backward_launch_count(dims(d_model=64, n_heads=2), small) == 7 + 5 * n
     assert stca.stca_backward_launch_count(dims(), big) == 6 + 7 * n
     assert stca.stca_backward_launch_count(dims(), nohost) == 6 + 7 * n
     assert stca.stca_backward_launch_count(dims(d_model=256, n_heads=4), small) == 6 + 7 * n  # d_h = 64
     assert stca.stca_backward_launch_count(dims(dtype=stca.STCA_F32), small) == 4 + 9 * n
-    fused = stca.stca_workspace_size(dims(), small, True)
+    assert stca.stca_backward_launch_count(dims(ffn_hidden=3 * 128), small) == 6 + 7 * n  # F not a multiple of d
+    long, keep3 = fake_batch([0, 60000, 100000], [0, 32, 40])
+    d, F = GOOD_DIMS["d_model"], GOOD_DIMS["ffn_hidden"]
+    fused = stca.stca_workspace_size(dims(), long, True)
     monkeypatch.setenv("STCA_BWD", "generic")
     assert stca.stca_backward_launch_count(dims(), small) == 6 + 7 * n
-    generic = stca.stca_workspace_size(dims(), small, True)
-    assert generic >= fused + 4 * n * 101 * 2 * 256 - 2 * 2 * n * 256 * 256 - 2 * 40 * 256
+    generic = stca.stca_workspace_size(dims(), long, True)
+    # the fp32 K|V of every layer, less the fused form's packed weights
+    assert generic - fused >= 4 * n * 100000 * 2 * d - 2 * n * (4 * d * d + 2 * d * F)
