@@ -381,14 +381,19 @@ def paper_step(args) -> int:
     return 0
 
 
-def backward_phase_work(label: str, b: W.Batch):
+def backward_phase_work(label: str, b: W.Batch, fused: bool):
     """Algorithmic (flop, bytes, peak TFLOP/s) of one occurrence of a backward
-    phase (stca_backward_profiled's markers), as the kernels are designed:
-    history-side products on bf16 operands (bf16 MFMA peak) with fp32 K|V
-    (fp32 attention on the fp32 MFMA, 157.3 TFLOP/s), dK|dV in bf16
-    (row-major and transposed), every layer's [dW_K | dW_V] and dX formed once
-    after the layers (one occurrence each), target-side products in fp32 where
-    they decide ReLU gates and on bf16 operands otherwise."""
+    phase (stca_backward_profiled's markers), as the kernels are designed.
+
+    fused (requests of at most 32 targets): the recomputed attention and the
+    attention backward each project the history inside the kernel (X read
+    once per layer; K/V projection 4 L d^2 flop), on the bf16 matrix cores;
+    the attention backward writes dK | dV in bf16 in two layouts; the target
+    side (recomputation and gradients) runs on bf16 operands.  Otherwise:
+    the K|V product with fp32 output, the exact fp32 attention on the fp32
+    MFMA (157.3 TFLOP/s), target-side products in fp32 where they decide ReLU
+    gates.  Either way every layer's [dW_K | dW_V] and dX are formed once
+    after the layers."""
     wl = b.wl
     d, F, n = wl.d_model, wl.ffn_hidden, wl.n_layers
     Ls = float(b.hist_len[b.n_tgt > 0].sum())
@@ -401,10 +406,20 @@ def backward_phase_work(label: str, b: W.Batch):
     if label == "dx":  # every layer's dK | dV read, dX written once (fp32)
         return n * 4 * Ls * d * d, n * 4 * Ls * d + 4 * Ls * d, PEAK_BF16_TFLOPS
     if label == "attn_fwd":
+        if fused:
+            return 4 * Ls * d * d + 4 * mL * d, 2 * Ls * d, PEAK_BF16_TFLOPS
         return 4 * mL * d, 8 * Ls * d, PEAK_FP32_TFLOPS
     if label == "attn_bwd":
+        if fused:
+            return 4 * Ls * d * d + 10 * mL * d, 2 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
         return 10 * mL * d, 8 * Ls * d + 8 * Ls * d, PEAK_FP32_TFLOPS
     if label == "target_gemm":
+        if fused:
+            # per layer: the recomputation (W_O, W_1, W_2, W_Q) and the
+            # gradient products (dW2, dH, dW1, du, dWo, da, dWq, ds), over
+            # 13 markers for 4 layers (one initial, two per layer after)
+            per_layer = 2 * mt * (2 * d * d + 2 * d * F) + 2 * mt * (4 * d * F + 4 * d * d)
+            return per_layer * n / (1 + 3 * n), 0.0, PEAK_BF16_TFLOPS
         # per layer over 4 markers: fp32 products q, o (d x d) and FFN1, FFN2
         # (d x F); bf16 products dW2, dH, dW1, du (d x F) and dWo, da, dWq, ds
         # (d x d), counted at the fp32 peak by their time ratio
@@ -475,22 +490,23 @@ def train_step(args) -> int:
         for k in range(nl):
             per.setdefault(ev.label(k), []).append(ev.elapsed_ms(k, k + 1))
         ev.close()
+    fused = "kv_gemm" not in per  # the attention kernels project the history themselves
     phases = {}
     for lab, v in per.items():
         occ = len(v) // args.steps
         t = float(np.mean(v))
         ent = {"per_step": occ, "ms_each": t, "ms_per_step": t * occ}
-        flop, byts, peak = backward_phase_work(lab, b)
+        flop, byts, peak = backward_phase_work(lab, b, fused)
         if flop:
             ent.update({"tflops": flop / (t * 1e-3) / 1e12, "gbs": byts / (t * 1e-3) / 1e9,
                         "mfma_frac": flop / (t * 1e-3) / 1e12 / peak, "hbm_frac": byts / (t * 1e-3) / 1e9 / PEAK_HBM_GBS})
         phases[lab] = ent
-    dom = max((k for k in phases if backward_phase_work(k, b)[0]), key=lambda k: phases[k]["ms_per_step"])
-    flop, byts, peak = backward_phase_work(dom, b)
+    dom = max((k for k in phases if backward_phase_work(k, b, fused)[0]), key=lambda k: phases[k]["ms_per_step"])
+    flop, byts, peak = backward_phase_work(dom, b, fused)
     roof = roofline_entry(dom, phases[dom]["ms_each"], flop, byts, peak)
     roof["kernel"] = dom
     bound_ms = sum(max(f / (pk * 1e12), by / (PEAK_HBM_GBS * 1e9)) * phases[k]["per_step"] * 1e3
-                   for k in phases for f, by, pk in [backward_phase_work(k, b)] if f)
+                   for k in phases for f, by, pk in [backward_phase_work(k, b, fused)] if f)
     print(json.dumps({
         "metric": "targets trained/sec, STCA forward+backward", "value": b.n_tgt_total / (ms * 1e-3),
         "unit": "targets/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
