@@ -181,12 +181,16 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->dkv = m.take(bf ? 2 * nh * n * 2 * d : 4 * nh * 2 * d);
     // bf16 history-side products: [W_K | W_V] per layer and its transpose,
     // X^T and (dK | dV)^T with the history rows padded to a multiple of 8
-    L->nh8 = round_up(static_cast<int64_t>(nh), 8);
+    // rows of the transposed copies, padded (to whole 32-row blocks when the
+    // fused attention backward writes (dK | dV)^T in 32-row blocks)
+    L->nh8 = round_up(static_cast<int64_t>(nh), L->bfused ? 32 : 8);
     const size_t nh8 = static_cast<size_t>(L->nh8);
     L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;
     L->wkvt = bf && !L->bfused ? m.take(2 * n * d * 2 * d) : 0;
     L->xt = bf ? m.take(2 * d * nh8) : 0;
-    L->dkvt = bf ? m.take(2 * n * 2 * d * nh8) : 0;  // [n 2d][nh8]: every layer's (dK | dV)^T
+    // every layer's (dK | dV)^T: [n 2d][nh8], or for the fused backward in
+    // 32-row blocks, [nh8 / 32][n 2d][32]
+    L->dkvt = bf ? m.take(2 * n * 2 * d * nh8) : 0;
     L->dwkv = bf ? m.take(4 * d * n * 2 * d) : 0;   // [d][n 2d] fp32
     // split-K partials: the largest of [dW_K | dW_V] (K = history rows) and
     // the target-side weight gradients (K = targets)
@@ -620,7 +624,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   // padding columns stay zero)
   if (bf) {
     HIPCHK(zero_untargeted(b->hist_off, b->tgt_off, b->n_requests, nh, static_cast<bf16_bits*>(dkv), n * 2 * d,
-                           n * 2 * d, dkvt, nh8, st));
+                           n * 2 * d, dkvt, nh8, L.bfused ? 1 : 0, st));
   } else {
     HIPCHK(fill_f32(static_cast<float*>(dkv), 0.f, nh * 2 * d, st));
     HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
@@ -699,8 +703,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       f.lse = RL(i);
       f.dKV = static_cast<bf16_bits*>(dkv_i);
       f.ldkv = n * 2 * d;
-      f.dKVT = dkvt + (size_t)i * 2 * d * nh8;
-      f.ldt = nh8;
+      f.dKVT = dkvt;
+      f.ldt = n * 2 * d;
       f.dq_part = dqp;
       f.n_tgt = nt;
       HIPCHK(fast_attn_bwd(d, f, fgrid, st));
@@ -751,7 +755,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     // the history rows), then dX = sum_i [dK^i | dV^i] [W_K^i | W_V^i]^T as
     // one product with K = n 2d, written once
     float* dwkv = at<float>(ws, L.dwkv);
-    HIPCHK(gemm_mfma(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
+    HIPCHK(gemm_mfma(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, L.bfused ? n * 2 * d : nh8, L.bfused ? 2 : 1, dwkv,
+                     n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
                      L.gpart_floats, st));
     for (int i = 0; i < n; ++i) {
       HIPCHK(hipMemcpy2DAsync(dw->dwk + (size_t)i * d * d, d * 4, dwkv + (size_t)i * 2 * d, (size_t)n * 2 * d * 4,

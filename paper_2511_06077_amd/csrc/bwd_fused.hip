@@ -286,7 +286,9 @@ __global__ __launch_bounds__(64 * (D / 32)) void bwd_fused_kernel(FastAttnBwd A)
   };
   auto store_cols = [&](const f32x16& g, int col, int b, const Unit& un, bool full) {
     // g: lane = head dim col, element v = block row blk_row<RPS>(vrow(v, hi))
-    bf16_bits* p = dKVT + (int64_t)col * A.ldt + (int64_t)b * 32;
+    // (dK | dV)^T in 32-row blocks: this layer's column col of block b is
+    // 32 contiguous rows
+    bf16_bits* p = dKVT + ((int64_t)b * A.ldt + A.layer * 2 * D + col) * 32;
     if (full && (RPS == 2 || RPS == 4)) {
       // the lane's 16 rows form two runs of 8 consecutive rows
 #pragma unroll

@@ -63,6 +63,22 @@ __device__ __forceinline__ void load_tile(u16x8 (&r)[4], const bf16_bits* __rest
   }
 }
 
+// The same tile of an operand stored as its transpose in 32-row blocks:
+// element (row, k) at src[((k / 32) ld + row) 32 + k % 32]; vectors of 8 k
+// stay inside a block.
+__device__ __forceinline__ void load_tile_blk(u16x8 (&r)[4], const bf16_bits* __restrict__ src, int64_t ld,
+                                              int row0, int nrows, int k0, int kend) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int v = threadIdx.x + 256 * i;
+    const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
+    const int k = k0 + kk;
+    const bool ok = row0 + row < nrows && k < kend;
+    r[i] = ok ? *reinterpret_cast<const u16x8*>(src + (((int64_t)(k >> 5) * ld + row0 + row) << 5) + (k & 31))
+              : u16x8{0, 0, 0, 0, 0, 0, 0, 0};
+  }
+}
+
 template <bool kcontig>
 __device__ __forceinline__ void store_tile(bf16_bits* __restrict__ lds, const u16x8 (&r)[4]) {
 #pragma unroll
@@ -81,7 +97,7 @@ __device__ __forceinline__ void store_tile(bf16_bits* __restrict__ lds, const u1
 
 // op(A) element (m, k): A[m * lda + k] if A_KC else A[k * lda + m].
 // op(B) element (k, n): B[n * ldb + k] if B_KC else B[k * ldb + n].
-template <bool A_KC, bool B_KC>
+template <bool A_KC, bool B_KC, bool B_BLK = false>
 __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, const bf16_bits* __restrict__ A,
                                                         int64_t lda, const bf16_bits* __restrict__ B, int64_t ldb,
                                                         float* __restrict__ C, int64_t ldc, float alpha,
@@ -107,7 +123,10 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
   f32x16 acc[2][2] = {};
   u16x8 ra[4], rb[4];
   load_tile<A_KC>(ra, A, lda, m0, M, kb, ke);
-  load_tile<B_KC>(rb, B, ldb, n0, N, kb, ke);
+  if (B_BLK)
+    load_tile_blk(rb, B, ldb, n0, N, kb, ke);
+  else
+    load_tile<B_KC>(rb, B, ldb, n0, N, kb, ke);
   store_tile<A_KC>(As, ra);
   store_tile<B_KC>(Bs, rb);
   __syncthreads();
@@ -115,7 +134,10 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
     const bool more = k0 + BK < ke;
     if (more) {
       load_tile<A_KC>(ra, A, lda, m0, M, k0 + BK, ke);
-      load_tile<B_KC>(rb, B, ldb, n0, N, k0 + BK, ke);
+      if (B_BLK)
+        load_tile_blk(rb, B, ldb, n0, N, k0 + BK, ke);
+      else
+        load_tile<B_KC>(rb, B, ldb, n0, N, k0 + BK, ke);
     }
     const bf16_bits* as = As;
     const bf16_bits* bs = Bs;
@@ -220,11 +242,12 @@ hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
                      int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
                      int64_t part_floats, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
-  const bool a_kc = !transA, b_kc = transB;
+  const bool a_kc = !transA, b_kc = transB != 0, b_blk = transB == 2;
   // whole 16-byte vectors: the contiguous extent of each operand is a
   // multiple of 8 elements and every row starts 16-byte aligned
   if ((a_kc ? K : M) % 8 || (b_kc ? K : N) % 8 || lda % 8 || ldb % 8 || !al16(A) || !al16(B))
     return hipErrorInvalidValue;
+  if (b_blk && (K % 32 || !a_kc)) return hipErrorInvalidValue;
   const int tm = static_cast<int>(ceil_div(M, BM)), tn = static_cast<int>(ceil_div(N, BN));
   const int64_t tiles = (int64_t)tm * tn;
   int splits = 1;
@@ -241,7 +264,10 @@ hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
 #define STCA_MG(AK, BKC)                                                                                    \
   hipLaunchKernelGGL((mfma_gemm_kernel<AK, BKC>), dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, M, N, \
                      K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, tm, tn, static_cast<int>(work), p)
-  if (a_kc && b_kc) STCA_MG(true, true);
+  if (b_blk)
+    hipLaunchKernelGGL((mfma_gemm_kernel<true, true, true>), dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, M,
+                       N, K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, tm, tn, static_cast<int>(work), p);
+  else if (a_kc && b_kc) STCA_MG(true, true);
   else if (a_kc) STCA_MG(true, false);
   else if (b_kc) STCA_MG(false, true);
   else STCA_MG(false, false);

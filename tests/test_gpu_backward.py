@@ -117,7 +117,9 @@ def test_training_window_gradients(torch, chunk_override):
     wl = W.WORKLOADS["train_bf16_R256_m16_L2048_d256"]
     b = W.make_batch(wl)
     g = gpu_grads(torch, b)
-    req = np.sort(np.random.default_rng(3).choice(wl.n_requests, 4, replace=False))
+    # five requests: 10240 history rows, enough for the wide-tile split-K
+    # product that forms [dW_K | dW_V] at full size
+    req = np.sort(np.random.default_rng(3).choice(wl.n_requests, 5, replace=False))
     sub = W.make_batch(wl, requests=req)
     rows = {
         "dhist": np.concatenate([np.arange(b.hist_off[r], b.hist_off[r + 1]) for r in req]),
