@@ -93,7 +93,9 @@ struct Layout {
   // backward (generic)
   size_t dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
   size_t xt, dkvt, wkvt;
-  size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp;  // fused backward: every layer's weights as bf16 operand tiles
+  // fused backward: every layer's weights as bf16 operand tiles (and the
+  // transposes of W_2, W_1, W_O), bf16 copies of every layer's a, u, h, s
+  size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp, fw2t, fw1t, fwot, fa16, fu16, fh16, fs16;
   size_t b_hid, b_dhid, b_ds, b_u, b_du, b_a, b_dq, b_s;  // bf16 copies of backward operands (bf16 path)
   int64_t gpart_floats, nh8;
   size_t total;
@@ -175,6 +177,13 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->fwqp = m.take(2 * n * d * d);
       L->fw1p = m.take(2 * n * d * F);
       L->fw2p = m.take(2 * n * d * F);
+      L->fw2t = m.take(2 * n * d * F);
+      L->fw1t = m.take(2 * n * d * F);
+      L->fwot = m.take(2 * n * d * d);
+      L->fa16 = m.take(2 * n * nt * d);
+      L->fu16 = m.take(2 * n * nt * d);
+      L->fh16 = m.take(2 * n * nt * F);
+      L->fs16 = m.take(2 * n * nt * d);
     }
     // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
     // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
@@ -535,7 +544,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       pj.job[3] = {w->wq, at<char>(ws, L.fwqp), d, d, 0};
       pj.job[4] = {w->w1, at<char>(ws, L.fw1p), d, F, 0};
       pj.job[5] = {w->w2, at<char>(ws, L.fw2p), F, d, 0};
-      HIPCHK(fast_pack_many(pj, 6, n, st));
+      pj.job[6] = {w->w2, at<char>(ws, L.fw2t), d, F, 0, 1};
+      pj.job[7] = {w->w1, at<char>(ws, L.fw1t), F, d, 0, 1};
+      pj.job[8] = {w->wo, at<char>(ws, L.fwot), d, d, 0, 1};
+      HIPCHK(fast_pack_many(pj, 9, n, st));
     }
   }
   // persistent grid of the fused kernels: one workgroup per CU
@@ -559,6 +571,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     up.mode = 0;
     up.s_out = RS(0);
     up.q_out = RQ(0);
+    up.s16_out = at<bf16_bits>(ws, L.fs16);
     HIPCHK(fast_update_precise(d, up, st));
     HIPCHK(rec.mark("target_gemm"));
   } else {
@@ -588,6 +601,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     up.h_out = RH(i);
     up.s_out = RS(i + 1);
     up.q_out = i + 1 < n ? RQ(i + 1) : nullptr;
+    up.a16_out = at<bf16_bits>(ws, L.fa16) + (size_t)i * nt * d;
+    up.u16_out = at<bf16_bits>(ws, L.fu16) + (size_t)i * nt * d;
+    up.h16_out = at<bf16_bits>(ws, L.fh16) + (size_t)i * nt * F;
+    up.s16_out = i + 1 < n ? at<bf16_bits>(ws, L.fs16) + (size_t)(i + 1) * nt * d : nullptr;
     HIPCHK(fast_update_precise(d, up, st));
     HIPCHK(rec.mark("target_gemm"));
   }
@@ -644,7 +661,33 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     // products that only carry gradients take bf16 copies of their fp32
     // operands on the bf16 MFMA (fp32 sums), the others stay fp32.
     const float* hid = RH(i);
-    if (bf) {
+    if (L.bfused) {
+      const int nti = static_cast<int>(nt);
+      float* gp = at<float>(ws, L.gpart);
+      const int64_t gpf = L.gpart_floats;
+      auto B = [&](size_t off) { return at<bf16_bits>(ws, off); };
+      UpdateGrad ug{};
+      ug.layer = i;
+      ug.F = F;
+      ug.n_tgt = nt;
+      ug.ds = ds;
+      ug.h = hid;
+      ug.du_out = du;
+      ug.da_out = da;
+      ug.ds16_out = B(L.b_ds);
+      ug.dh16_out = B(L.b_dhid);
+      ug.du16_out = B(L.b_du);
+      ug.W2TP = at<char>(ws, L.fw2t);
+      ug.W1TP = at<char>(ws, L.fw1t);
+      ug.WoTP = at<char>(ws, L.fwot);
+      HIPCHK(fast_update_grad(d, ug, st));
+      HIPCHK(gemm_mfma(F, d, nti, B(L.fh16) + (size_t)i * nt * F, F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d,
+                       d, 1.f, 0, gp, gpf, st));
+      HIPCHK(gemm_mfma(d, F, nti, B(L.fu16) + (size_t)i * nt * d, d, 1, B(L.b_dhid), F, 0,
+                       dw->dw1 + (size_t)i * d * F, F, 1.f, 0, gp, gpf, st));
+      HIPCHK(gemm_mfma(d, d, nti, B(L.fa16) + (size_t)i * nt * d, d, 1, B(L.b_du), d, 0,
+                       dw->dwo + (size_t)i * d * d, d, 1.f, 0, gp, gpf, st));
+    } else if (bf) {
       const int nti = static_cast<int>(nt);
       float* gp = at<float>(ws, L.gpart);
       const int64_t gpf = L.gpart_floats;
@@ -719,8 +762,9 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     if (bf) {
       const int nti = static_cast<int>(nt);
       HIPCHK(convert(0, 1, dq, at<bf16_bits>(ws, L.b_dq), nt * d, st));
-      HIPCHK(convert(0, 1, s, at<bf16_bits>(ws, L.b_s), nt * d, st));
-      HIPCHK(gemm_mfma(d, d, nti, at<bf16_bits>(ws, L.b_s), d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,
+      const bf16_bits* s16 = L.bfused ? at<bf16_bits>(ws, L.fs16) + (size_t)i * nt * d : at<bf16_bits>(ws, L.b_s);
+      if (!L.bfused) HIPCHK(convert(0, 1, s, at<bf16_bits>(ws, L.b_s), nt * d, st));
+      HIPCHK(gemm_mfma(d, d, nti, s16, d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,
                        dw->dwq + (size_t)i * d * d, d, 1.f, 0, at<float>(ws, L.gpart), L.gpart_floats, st));
       HIPCHK(hipMemcpyAsync(ds2, du, 4 * nt * d, hipMemcpyDeviceToDevice, st));
       HIPCHK(gemm_mfma(nti, d, d, at<bf16_bits>(ws, L.b_dq), d, 0, static_cast<const bf16_bits*>(Wq), d, 1, ds2, d,

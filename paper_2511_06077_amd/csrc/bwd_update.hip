@@ -27,6 +27,10 @@ __device__ __forceinline__ f32x16 mma(const bf16x8& a, const bf16x8& b, const f3
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
+__device__ __forceinline__ uint32_t pack2(float x, float y) {
+  return (uint32_t)from_f32<bf16_bits>(x) | ((uint32_t)from_f32<bf16_bits>(y) << 16);
+}
+
 template <int D>
 __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePrecise A) {
   constexpr int NW = D / 32;
@@ -76,6 +80,14 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
     for (int q = 0; q < 4; ++q)
       *reinterpret_cast<float4*>(p + 8 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
   };
+  auto store_tile16 = [&](bf16_bits* dst, int64_t ld, int col0, const f32x16& v) {
+    if (!tok || !dst) return;
+    bf16_bits* p = dst + t * ld + col0 + 4 * hi;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<uint2*>(p + 8 * q) =
+          make_uint2(pack2(v[4 * q], v[4 * q + 1]), pack2(v[4 * q + 2], v[4 * q + 3]));
+  };
   auto load_tile = [&](const float* src, int64_t ld, int col0) {
     f32x16 v = {};
     if (tok) {
@@ -116,6 +128,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
         x[0] = to_f32((bf16_bits)(v.x & 0xffff)), x[1] = to_f32((bf16_bits)(v.x >> 16));
         x[2] = to_f32((bf16_bits)(v.y & 0xffff)), x[3] = to_f32((bf16_bits)(v.y >> 16));
         *reinterpret_cast<float4*>(A.s_out + (tb + row) * D + col) = make_float4(x[0], x[1], x[2], x[3]);
+        if (A.s16_out) *reinterpret_cast<uint2*>(A.s16_out + (tb + row) * D + col) = v;
       }
       put4(act, row, col, x[0], x[1], x[2], x[3]);
     }
@@ -153,6 +166,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
           float4* sa = reinterpret_cast<float4*>(A.a_out + tt * D + j * DH + half * 16);
 #pragma unroll
           for (int q = 0; q < 4; ++q) sa[q] = make_float4(av[4 * q], av[4 * q + 1], av[4 * q + 2], av[4 * q + 3]);
+          if (A.a16_out) {
+            uint2* s16 = reinterpret_cast<uint2*>(A.a16_out + tt * D + j * DH + half * 16);
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              s16[q] = make_uint2(pack2(av[4 * q], av[4 * q + 1]), pack2(av[4 * q + 2], av[4 * q + 3]));
+          }
           if (half == 0) A.lse_out[tt * H + j] = (M + log2f(L)) * kLn2;
         }
 #pragma unroll
@@ -164,6 +183,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
     // u = s + a W_O
     f32x16 u = gemm(WoP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, load_tile(A.s_in, D, 32 * w));
     store_tile(A.u_out, D, 32 * w, u);
+    store_tile16(A.u16_out, D, 32 * w, u);
     __syncthreads();  // every wave is done reading a
     put_tile(act, 32 * w, u);
     __syncthreads();
@@ -175,12 +195,14 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
 #pragma unroll
       for (int v = 0; v < 16; ++v) h[v] = fmaxf(h[v], 0.f);
       store_tile(A.h_out, F, c * D + 32 * w, h);
+      store_tile16(A.h16_out, F, c * D + 32 * w, h);
       put_tile(hid, 32 * w, h);
       __syncthreads();
       s_next = gemm(W2P + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64, hid, s_next);
       __syncthreads();  // hid is rewritten by the next chunk
     }
     store_tile(A.s_out, D, 32 * w, s_next);
+    store_tile16(A.s16_out, D, 32 * w, s_next);
     if (A.layer + 1 >= A.n_layers) return;
     put_tile(act, 32 * w, s_next);  // act (u) was last read before the previous barrier
     __syncthreads();
@@ -191,6 +213,99 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
 #pragma unroll
   for (int v = 0; v < 16; ++v) q[v] *= qscale;
   store_tile(A.q_out, D, 32 * w, q);
+}
+
+// Reverse of the update: dH = (ds W_2^T) where h > 0, du = ds + dH W_1^T,
+// da = du W_O^T.  Same tiling as the recomputation, one bf16 term per
+// activation (these products only carry gradients).
+template <int D>
+__global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A) {
+  constexpr int NW = D / 32;
+  constexpr int KS = D / 16;
+  constexpr int AROW = D + 8;
+  __shared__ __attribute__((aligned(16))) bf16_bits act[32 * AROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits hid[32 * AROW];
+  const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tcol = lane % 32, hi = lane / 32;
+  const int64_t tb = (int64_t)blockIdx.x * 32;
+  const int64_t t = tb + tcol;
+  const bool tok = t < A.n_tgt;
+  const int F = A.F;
+  const int KSF = F / 16;
+
+  auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits* src, f32x16 acc) {
+#pragma unroll 4
+    for (int k = 0; k < KS; ++k)
+      acc = mma(Wp[k * 64 + lane], *reinterpret_cast<const bf16x8*>(src + tcol * AROW + 8 * hi + 16 * k), acc);
+    return acc;
+  };
+  // a wave's tile (lane = target, elements = columns col0 + 8 q + 4 hi + e)
+  auto put_tile = [&](bf16_bits* buf, int col0, const f32x16& v) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<uint2*>(buf + tcol * AROW + col0 + 8 * q + 4 * hi) =
+          make_uint2(pack2(v[4 * q], v[4 * q + 1]), pack2(v[4 * q + 2], v[4 * q + 3]));
+  };
+  auto store16 = [&](bf16_bits* dst, int64_t ld, int col0, const f32x16& v) {
+    if (!tok) return;
+    bf16_bits* p = dst + t * ld + col0 + 4 * hi;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<uint2*>(p + 8 * q) =
+          make_uint2(pack2(v[4 * q], v[4 * q + 1]), pack2(v[4 * q + 2], v[4 * q + 3]));
+  };
+  auto store32 = [&](float* dst, int64_t ld, int col0, const f32x16& v) {
+    if (!tok) return;
+    float* p = dst + t * ld + col0 + 4 * hi;
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+      *reinterpret_cast<float4*>(p + 8 * q) = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+  };
+  auto load32 = [&](const float* src, int64_t ld, int col0) {
+    f32x16 v = {};
+    if (tok) {
+      const float* p = src + t * ld + col0 + 4 * hi;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float4 x = *reinterpret_cast<const float4*>(p + 8 * q);
+        v[4 * q] = x.x, v[4 * q + 1] = x.y, v[4 * q + 2] = x.z, v[4 * q + 3] = x.w;
+      }
+    }
+    return v;
+  };
+  const bf16x8* W2TP = static_cast<const bf16x8*>(A.W2TP);
+  const bf16x8* W1TP = static_cast<const bf16x8*>(A.W1TP);
+  const bf16x8* WoTP = static_cast<const bf16x8*>(A.WoTP);
+
+  // ds (bf16) into LDS, and its bf16 copy
+  for (int c = threadIdx.x; c < 32 * D / 4; c += 64 * NW) {
+    const int row = c / (D / 4), col = (c % (D / 4)) * 4;
+    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (tb + row < A.n_tgt) x = *reinterpret_cast<const float4*>(A.ds + (tb + row) * D + col);
+    const uint2 v = make_uint2(pack2(x.x, x.y), pack2(x.z, x.w));
+    *reinterpret_cast<uint2*>(act + row * AROW + col) = v;
+    if (tb + row < A.n_tgt) *reinterpret_cast<uint2*>(A.ds16_out + (tb + row) * D + col) = v;
+  }
+  __syncthreads();
+  f32x16 du = load32(A.ds, D, 32 * w);
+  for (int c = 0; c < F / D; ++c) {
+    const int col = c * D + 32 * w;
+    f32x16 dh = gemm(W2TP + ((int64_t)A.layer * (F / 32) + c * NW + w) * KS * 64, act, f32x16{});
+    const f32x16 h = load32(A.h, F, col);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) dh[v] = h[v] > 0.f ? dh[v] : 0.f;
+    store16(A.dh16_out, F, col, dh);
+    put_tile(hid, 32 * w, dh);
+    __syncthreads();
+    du = gemm(W1TP + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64, hid, du);
+    __syncthreads();  // hid is rewritten by the next chunk
+  }
+  store32(A.du_out, D, 32 * w, du);
+  store16(A.du16_out, D, 32 * w, du);
+  put_tile(act, 32 * w, du);  // act (ds) was last read before the previous barrier
+  __syncthreads();
+  const f32x16 da = gemm(WoTP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, f32x16{});
+  store32(A.da_out, D, 32 * w, da);
 }
 
 }  // namespace
@@ -207,6 +322,21 @@ hipError_t fast_update_precise(int D, const UpdatePrecise& f, hipStream_t st) {
     default: return hipErrorInvalidValue;
   }
 #undef STCA_UPDP
+  return hipGetLastError();
+}
+
+hipError_t fast_update_grad(int D, const UpdateGrad& f, hipStream_t st) {
+  if (f.n_tgt == 0) return hipSuccess;
+  if (f.F % D != 0) return hipErrorInvalidValue;
+  dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
+#define STCA_UPDG(DD) hipLaunchKernelGGL(update_grad_kernel<DD>, g, dim3(64 * (DD / 32)), 0, st, f)
+  switch (D) {
+    case 64: STCA_UPDG(64); break;
+    case 128: STCA_UPDG(128); break;
+    case 256: STCA_UPDG(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_UPDG
   return hipGetLastError();
 }
 

@@ -24,11 +24,12 @@ struct FastUpdate {
 // Repack W [n_layers][K][N] (bf16) into MFMA operand order, as bf16 or fp16.
 hipError_t fast_pack(const void* W, void* P, int n_layers, int K, int N, int to_f16, hipStream_t st);
 // The same for up to kMaxPackJobs weights (same layer count) in one launch.
-constexpr int kMaxPackJobs = 8;
+constexpr int kMaxPackJobs = 10;
 struct PackJob {
   const void* src;
   void* dst;
   int K, N, to_f16;
+  int trans;  // src holds the transpose ([N][K]): pack src^T
 };
 struct PackJobs {
   PackJob job[kMaxPackJobs];
@@ -101,6 +102,8 @@ hipError_t fast_attn_fwd_precise(int D, const FastAttnFwdPrecise& f, int grid, h
 // (s_out) and, before the last layer, q' (q_out).  Queries are scaled by
 // log2(e)/sqrt(d_h).  Weights packed as bf16 operand tiles (fast_pack_many
 // with to_f16 = 0); F a multiple of D.
+// The *16 outputs (nullable) are bf16 copies of a, u, h and s' (s^(0) in
+// mode 0) for the weight-gradient products.
 struct UpdatePrecise {
   int mode, layer, n_layers, F;
   int64_t n_tgt;
@@ -110,9 +113,25 @@ struct UpdatePrecise {
   const float2* part_ml;
   const float* s_in;
   float *a_out, *lse_out, *u_out, *h_out, *s_out, *q_out;
+  bf16_bits *a16_out, *u16_out, *h16_out, *s16_out;
   const void *WoP, *W1P, *W2P, *WqP;
 };
 hipError_t fast_update_precise(int D, const UpdatePrecise& f, hipStream_t st);
+// Reverse of one layer's target-side update (bwd_update.hip), per 32 targets:
+// dH = (ds W_2^T) masked where h > 0, du = ds + dH W_1^T, da = du W_O^T, on
+// bf16 operands with fp32 sums; writes dH and bf16 copies of ds and du for
+// the weight-gradient products.  Weights: the transposes of W_2, W_1, W_O
+// packed as bf16 operand tiles (PackJob.trans).
+struct UpdateGrad {
+  int layer, F;
+  int64_t n_tgt;
+  const float* ds;  // [n_tgt][D] gradient of s'
+  const float* h;   // [n_tgt][F] ReLU(u W_1) of the recomputation
+  float *du_out, *da_out;
+  bf16_bits *ds16_out, *dh16_out, *du16_out;
+  const void *W2TP, *W1TP, *WoTP;
+};
+hipError_t fast_update_grad(int D, const UpdateGrad& f, hipStream_t st);
 
 // Reordered single-query attention (reordered.hip) for units of at most
 // 32 / H targets: U = per-head Q W_K^j^T (bf16 hi and lo terms

@@ -119,7 +119,7 @@ __global__ void pack_kernel(const bf16_bits* __restrict__ W, V8* __restrict__ P,
 // a forward costs one launch instead of one per weight.
 template <typename V8>
 __device__ __forceinline__ void pack_one(const bf16_bits* __restrict__ w, V8* __restrict__ P, int K, int N,
-                                         int64_t g) {
+                                         int64_t g, bool trans) {
   const int lane = g % 64;
   const int64_t rest = g / 64;
   const int ks = rest % (K / 16);
@@ -128,7 +128,9 @@ __device__ __forceinline__ void pack_one(const bf16_bits* __restrict__ w, V8* __
   const int k0 = ks * 16 + 8 * (lane / 32);
   V8 r;
 #pragma unroll
-  for (int e = 0; e < 8; ++e) r[e] = static_cast<typename elem_of<V8>::type>(to_f32(w[(int64_t)(k0 + e) * N + n]));
+  for (int e = 0; e < 8; ++e)
+    r[e] = static_cast<typename elem_of<V8>::type>(
+        to_f32(w[trans ? (int64_t)n * K + k0 + e : (int64_t)(k0 + e) * N + n]));
   P[g] = r;
 }
 
@@ -140,9 +142,9 @@ __global__ void pack_many_kernel(PackJobs J) {
   const PackJob& b = J.job[j];
   const bf16_bits* w = static_cast<const bf16_bits*>(b.src) + (int64_t)layer * b.K * b.N;
   if (b.to_f16)
-    pack_one(w, static_cast<f16x8*>(b.dst) + (int64_t)layer * groups, b.K, b.N, g);
+    pack_one(w, static_cast<f16x8*>(b.dst) + (int64_t)layer * groups, b.K, b.N, g, b.trans != 0);
   else
-    pack_one(w, static_cast<bf16x8*>(b.dst) + (int64_t)layer * groups, b.K, b.N, g);
+    pack_one(w, static_cast<bf16x8*>(b.dst) + (int64_t)layer * groups, b.K, b.N, g, b.trans != 0);
 }
 
 // ------------------------------------------------------ K1: projection
