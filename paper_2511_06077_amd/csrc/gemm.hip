@@ -196,19 +196,49 @@ __global__ void split_sum_kernel(const float* __restrict__ part, int splits, int
 bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 // dst[c * ldd + r] = src[r * lds + c] for r < R, c < C; dst columns r in
-// [R, Rp) are zeroed.  64 x 64 tiles through LDS.
+// [R, Rp) are zeroed.  64 x 64 tiles through LDS with 16-byte global reads
+// and writes (eight consecutive columns in, eight consecutive rows out).
 __global__ __launch_bounds__(256) void transpose_kernel(const bf16_bits* __restrict__ src, int64_t lds, int R, int C,
                                                         bf16_bits* __restrict__ dst, int64_t ldd, int Rp) {
-  __shared__ bf16_bits t[64][65];
+  constexpr int TR = 64 + 2;  // padded LDS row (bf16): column reads spread over the banks
+  __shared__ bf16_bits t[64 * TR];
   const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int rr = e / 64, cc = e % 64;
-    t[rr][cc] = (r0 + rr < R && c0 + cc < C) ? src[(int64_t)(r0 + rr) * lds + c0 + cc] : bf16_bits(0);
+  const bool vec_in = (C % 8) == 0 && (lds % 8) == 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int v = threadIdx.x + 256 * i;
+    const int rr = v / 8, cc = (v % 8) * 8;
+    const int r = r0 + rr, c = c0 + cc;
+    u16x8 x = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (r < R) {
+      if (vec_in && c + 8 <= C) {
+        x = *reinterpret_cast<const u16x8*>(src + (int64_t)r * lds + c);
+      } else {
+#pragma unroll
+        for (int e = 0; e < 8; ++e) x[e] = c + e < C ? src[(int64_t)r * lds + c + e] : bf16_bits(0);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) t[rr * TR + cc + e] = x[e];
   }
   __syncthreads();
-  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
-    const int cc = e / 64, rr = e % 64;
-    if (c0 + cc < C && r0 + rr < Rp) dst[(int64_t)(c0 + cc) * ldd + r0 + rr] = t[rr][cc];
+  const bool vec_out = (ldd % 8) == 0 && (Rp % 8) == 0;
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const int v = threadIdx.x + 256 * i;
+    const int cc = v / 8, rr = (v % 8) * 8;
+    const int c = c0 + cc, r = r0 + rr;
+    if (c >= C || r >= Rp) continue;
+    u16x8 y;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) y[e] = t[(rr + e) * TR + cc];
+    if (vec_out && r + 8 <= Rp) {
+      *reinterpret_cast<u16x8*>(dst + (int64_t)c * ldd + r) = y;
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        if (r + e < Rp) dst[(int64_t)c * ldd + r + e] = y[e];
+    }
   }
 }
 
