@@ -4,7 +4,8 @@
 // pieces (gate, row LayerNorm, query packing for the fused attention kernel).
 //
 // History transform X~ = LN(SwiGLUFFN(X)), bf16 in and out, one workgroup of
-// four waves per 128 history rows, one wave per 32 rows:
+// eight waves (two per SIMD, so one wave's gate arithmetic overlaps the other's
+// MFMAs) per 256 history rows, one wave per 32 rows:
 //
 //   U^T = W_u^T X^T, V^T = W_v^T X^T   (32 hidden columns at a time, MFMA
 //                                       32x32x16 bf16, X^T held in registers)
@@ -19,7 +20,7 @@
 // repacked once per call into per-chunk operand order (32 hidden columns:
 // W_u^T fragments, W_v^T fragments, W_o^T fragments, contiguous) and each
 // chunk is copied into LDS with direct global-to-LDS loads, double buffered,
-// so the four waves share one copy.
+// so the eight waves share one copy.
 #include "common.h"
 #include "paper.h"
 
@@ -75,8 +76,11 @@ __global__ void swiglu_pack_kernel(const bf16_bits* __restrict__ Wu, const bf16_
   }
 }
 
+constexpr int kSwWaves = 8;  // waves per workgroup (two per SIMD), 32 rows each
+
 template <int D>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) void swiglu_ln_kernel(
+__global__ __launch_bounds__(kSwWaves * 64)
+__attribute__((amdgpu_waves_per_eu(kSwWaves / 4, kSwWaves / 4))) void swiglu_ln_kernel(
     const bf16_bits* __restrict__ X, int64_t n_rows, const unsigned char* __restrict__ Wp, int F,
     bf16_bits* __restrict__ out16, float* __restrict__ out32) {
   constexpr int KS = D / 16;       // k-steps of the up projections
@@ -86,7 +90,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];  // [2][CB]
   const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int tcol = lane % 32, hi = lane / 32;
-  const int64_t row = (int64_t)blockIdx.x * 128 + 32 * w + tcol;
+  const int64_t row = (int64_t)blockIdx.x * (32 * kSwWaves) + 32 * w + tcol;
   const bool live = row < n_rows;
 
   // X^T as B operands: lane (row, hi), k-step ks holds X[row][16ks + 8hi .. +7]
@@ -102,7 +106,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(1, 1))) voi
   auto dma = [&](int c, int buf) {
     const unsigned char* src = Wp + (size_t)c * CB + lane * 16;
     unsigned char* dst = smem + buf * CB;
-    for (int i = w; i < CB / 1024; i += 4)
+    for (int i = w; i < CB / 1024; i += kSwWaves)
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + i * 1024),
                                        (void __attribute__((address_space(3)))*)(dst + i * 1024), 16, 0, 0);
   };
@@ -249,13 +253,13 @@ hipError_t swiglu_ln(int D, const void* X, int64_t n_rows, const void* Wp_layer,
                      hipStream_t st) {
   if (n_rows == 0) return hipSuccess;
   if (F % 32) return hipErrorInvalidValue;
-  const dim3 grid(static_cast<unsigned>(ceil_div(n_rows, 128)));
+  const dim3 grid(static_cast<unsigned>(ceil_div(n_rows, 32 * kSwWaves)));
 #define STCA_SWIGLU(DD)                                                                                      \
   {                                                                                                          \
     const size_t lds = 2 * swiglu_chunk_bytes<DD>();                                                         \
     hipError_t e = allow_lds(swiglu_ln_kernel<DD>, lds);                                                     \
     if (e != hipSuccess) return e;                                                                           \
-    hipLaunchKernelGGL(swiglu_ln_kernel<DD>, grid, dim3(256), lds, st, (const bf16_bits*)X, n_rows,          \
+    hipLaunchKernelGGL(swiglu_ln_kernel<DD>, grid, dim3(64 * kSwWaves), lds, st, (const bf16_bits*)X, n_rows, \
                        (const unsigned char*)Wp_layer, F, (bf16_bits*)out16, out32);                         \
   }
   switch (D) {
