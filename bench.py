@@ -430,9 +430,11 @@ def backward_phase_work(label: str, b: W.Batch, fused: bool):
 
 
 def train_step(args) -> int:
-    """Forward + backward of the training window: one step = stca_forward then
-    stca_backward (all gradients) over the whole batch, inputs resident.  The
-    backward's phases are then timed with HIP events in a second pass."""
+    """Forward + backward of the training window: one step = the forward then
+    the backward (all gradients) over the whole batch, inputs resident
+    (stca_forward_train + stca_backward_record where the batch qualifies,
+    else stca_forward + stca_backward).  The recomputing backward's phases are
+    then timed with HIP events in a second pass."""
     import torch
     from paper_2511_06077_amd.device import DeviceBatch, to_device
     name = args.workload if args.workload != W.HEADLINE else "train_bf16_R256_m16_L2048_d256"
@@ -456,9 +458,24 @@ def train_step(args) -> int:
     db = DeviceBatch(b, device="cuda:0", backward=True)
     dout = to_device(b.grad_out, "cuda:0")
 
+    # A training step: the forward then the backward over the whole batch.
+    # Batches the fused backward takes run it as stca_forward_train (which
+    # keeps a training record) and stca_backward_record; the others as
+    # stca_forward and the recomputing stca_backward.
+    use_rec = db.record is not None
+
+    def fwd_call():
+        if use_rec:
+            db.forward_train()
+        else:
+            db.forward()
+
+    def bwd_call():
+        db.backward(dout, use_record=use_rec)
+
     def step():
-        db.forward()
-        db.backward(dout)
+        fwd_call()
+        bwd_call()
 
     settle(step, args.settle_seconds)
     for _ in range(args.warmup):
@@ -466,18 +483,29 @@ def train_step(args) -> int:
     torch.cuda.synchronize()
     stream = torch.cuda.current_stream()
     e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+    # forward and backward timed separately (each backward reads the record of
+    # the last forward_train, which stays valid across backward calls)
     e[0].record(stream)
     for _ in range(args.steps):
-        db.forward()
+        fwd_call()
     e[1].record(stream)
     for _ in range(args.steps):
-        db.backward(dout)
+        bwd_call()
     e[2].record(stream)
     torch.cuda.synchronize()
     fwd = e[0].elapsed_time(e[1]) / args.steps
     bwd = e[1].elapsed_time(e[2]) / args.steps
     ms = fwd + bwd
-    # backward phases, timed on the library's stream
+    # the recomputing backward (what stca_backward alone costs), for reference
+    e2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    e2[0].record(stream)
+    for _ in range(args.steps):
+        db.backward(dout)
+    e2[1].record(stream)
+    torch.cuda.synchronize()
+    bwd_recompute = e2[0].elapsed_time(e2[1]) / args.steps
+    # phases of the recomputing backward (stca_backward_profiled), timed on
+    # the library's stream
     g = db.backward(dout)
     dw = stca.wgrads(g["dwq"], g["dwk"], g["dwv"], g["dwo"], g["dw1"], g["dw2"])
     nl = stca.stca_backward_launch_count(db.dims, db.batch)
@@ -515,7 +543,8 @@ def train_step(args) -> int:
         "config": {"workload": wl.name, "requests": wl.n_requests, "targets_per_request": wl.n_targets,
                    "hist_len": wl.hist_len, "d_model": wl.d_model, "heads": wl.n_heads, "layers": wl.n_layers},
         "stochastic_length": sl_info,
-        "forward_ms": fwd, "backward_ms": bwd, "backward_roofline": roof,
+        "training_record": use_rec, "forward_ms": fwd, "backward_ms": bwd,
+        "backward_recomputing_ms": bwd_recompute, "backward_roofline": roof,
         "backward_phase_bound_ms": bound_ms, "backward_phases": phases}), flush=True)
     return 0
 

@@ -154,6 +154,33 @@ stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch,
                             const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
                             hipStream_t stream);
 
+/* Training step in two calls, for batches the fused backward takes (bf16,
+ * d_h = 32, FFN width a multiple of d, host offsets showing at most 32
+ * targets per request): the forward writes, besides out, a training record
+ * of the per-layer tensors the backward needs, computed to fp32 accuracy (so
+ * the ReLU gates follow fp32 states), and the backward reads it instead of
+ * recomputing them.
+ *
+ * stca_train_record_size: bytes of the record; 0 when the batch does not
+ * qualify or the arguments are invalid.
+ * stca_forward_train: out as stca_forward (evaluated to fp32 accuracy before
+ * the final rounding to the storage dtype); record (device, 16-byte aligned,
+ * stca_train_record_size bytes) is overwritten; ws as for stca_backward
+ * (ws_bytes >= stca_workspace_size(dims, batch, 1)).
+ * stca_backward_record: the same gradients as stca_backward for the inputs
+ * that produced `record` (which must not change in between), without the
+ * recomputation.  Both return STCA_ERR_UNSUPPORTED for batches that do not
+ * qualify; other errors as stca_forward / stca_backward. */
+size_t stca_train_record_size(const stca_dims_t* dims, const stca_batch_t* batch);
+stca_status_t stca_forward_train(const stca_dims_t* dims, const stca_batch_t* batch,
+                                 const void* hist, const void* tgt, const stca_weights_t* w,
+                                 void* out, void* record, void* ws, size_t ws_bytes, hipStream_t stream);
+stca_status_t stca_backward_record(const stca_dims_t* dims, const stca_batch_t* batch,
+                                   const void* hist, const void* tgt, const stca_weights_t* w,
+                                   const void* record, const void* dout, float* dhist, float* dtgt,
+                                   const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
+                                   hipStream_t stream);
+
 /* Measurement variant of stca_forward: the same work, plus hipEventRecord on
  * `stream` around every kernel launch so a caller can time each kernel on the
  * stream it runs on.  events[0] is recorded before the first launch and

@@ -94,12 +94,35 @@ struct Layout {
   size_t dhid, ds, du, da, dq, ds2, dkv, dq_part, rs, ru, rq, ra, rl, kvs, wkv, dwkv, gpart;
   size_t xt, dkvt, wkvt;
   // fused backward: every layer's weights as bf16 operand tiles (and the
-  // transposes of W_2, W_1, W_O), bf16 copies of every layer's a, u, h, s
-  size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp, fw2t, fw1t, fwot, fa16, fu16, fh16, fs16;
+  // transposes of W_2, W_1, W_O), and the region of the recomputed
+  // per-layer tensors (RecordLayout)
+  size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp, fw2t, fw1t, fwot, rec;
   size_t b_hid, b_dhid, b_ds, b_u, b_du, b_a, b_dq, b_s;  // bf16 copies of backward operands (bf16 path)
   int64_t gpart_floats, nh8;
   size_t total;
 };
+
+// The per-layer tensors the fused backward's reverse pass reads (a training
+// record): a, lse, the scaled queries and h = ReLU(u W_1) in fp32, and bf16
+// copies of a, u, h and the layer input s for the weight-gradient products.
+struct RecordLayout {
+  size_t a, lse, q, h, a16, u16, h16, s16, total;
+};
+RecordLayout record_layout(const Layout& L) {
+  const size_t d = L.d, h = L.h, F = L.F, n = L.n, nt = L.nt;
+  RecordLayout R;
+  Bump m;
+  R.a = m.take(4 * n * nt * d);
+  R.lse = m.take(4 * n * nt * h);
+  R.q = m.take(4 * n * nt * d);
+  R.h = m.take(4 * n * nt * F);
+  R.a16 = m.take(2 * n * nt * d);
+  R.u16 = m.take(2 * n * nt * d);
+  R.h16 = m.take(2 * n * nt * F);
+  R.s16 = m.take(2 * n * nt * d);
+  R.total = m.off;
+  return R;
+}
 
 bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backward, bool with_saved, Layout* L) {
   const int p = path_of(dims);
@@ -180,10 +203,6 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->fw2t = m.take(2 * n * d * F);
       L->fw1t = m.take(2 * n * d * F);
       L->fwot = m.take(2 * n * d * d);
-      L->fa16 = m.take(2 * n * nt * d);
-      L->fu16 = m.take(2 * n * nt * d);
-      L->fh16 = m.take(2 * n * nt * F);
-      L->fs16 = m.take(2 * n * nt * d);
     }
     // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
     // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
@@ -211,10 +230,14 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
                                   gemm_mfma_part_floats(di, di, nti)});
     }
     L->gpart = bf ? m.take(4 * L->gpart_floats) : 0;
-    L->rq = m.take(4 * n * nt * d);  // per-layer queries, attention outputs, lse
-    L->ra = m.take(4 * n * nt * d);
-    L->rl = m.take(4 * n * nt * L->h);
-    L->hid = m.take(4 * n * nt * F);  // every layer's ReLU(u W_1) from the recomputation
+    if (L->bfused) {
+      L->rec = m.take(record_layout(*L).total);
+    } else {
+      L->rq = m.take(4 * n * nt * d);  // per-layer queries, attention outputs, lse
+      L->ra = m.take(4 * n * nt * d);
+      L->rl = m.take(4 * n * nt * L->h);
+      L->hid = m.take(4 * n * nt * F);  // every layer's ReLU(u W_1) from the recomputation
+    }
     L->dhid = m.take(4 * nt * F);
     L->ds = m.take(4 * nt * d);
     L->du = m.take(4 * nt * d);
@@ -475,9 +498,14 @@ stca_status_t forward_generic(const Layout& L, int bf, const stca_batch_t* b, co
 // Activation recomputation: the layer states are rebuilt in fp32 from the
 // inputs first, so every ReLU gate and softmax weight of the backward follows
 // fp32 states whatever arithmetic the forward call used.
+// rec_out (fused form only): stop after the recomputation, which writes the
+// training record there and the output into `out` (the forward of a
+// training step).  rec_in (fused form only): skip the recomputation and read
+// the record written by such a call.
 stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, const void* hist, const void* tgt,
                                const stca_weights_t* w, const void* dout, float* dhist, float* dtgt,
-                               const stca_wgrads_t* dw, void* ws, hipStream_t st, Rec& rec) {
+                               const stca_wgrads_t* dw, void* ws, hipStream_t st, Rec& rec,
+                               const void* rec_in = nullptr, void* rec_out = nullptr, void* out = nullptr) {
   const int d = L.d, n = L.n, F = L.F, h = L.h;
   const int64_t nt = L.nt, nh = L.nh;
   const size_t es = bf ? 2 : 4;
@@ -489,7 +517,18 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                       hdr, st));
   HIPCHK(rec.mark("sched"));
   void* dkv = at<char>(ws, L.dkv);
-  auto RH = [&](int i) { return at<float>(ws, L.hid) + (size_t)i * nt * F; };
+  // the recomputed per-layer tensors: in the workspace, or the training record
+  const RecordLayout R = L.bfused ? record_layout(L) : RecordLayout{};
+  char* rb = !L.bfused ? nullptr
+                       : rec_in ? const_cast<char*>(static_cast<const char*>(rec_in))
+                                : rec_out ? static_cast<char*>(rec_out) : at<char>(ws, L.rec);
+  auto rec32 = [&](size_t off, int i, size_t per) { return reinterpret_cast<float*>(rb + off) + (size_t)i * per; };
+  auto rec16 = [&](size_t off, int i, size_t per) { return reinterpret_cast<bf16_bits*>(rb + off) + (size_t)i * per; };
+  auto RH = [&](int i) { return L.bfused ? rec32(R.h, i, nt * F) : at<float>(ws, L.hid) + (size_t)i * nt * F; };
+  auto FA16 = [&](int i) { return rec16(R.a16, i, nt * d); };
+  auto FU16 = [&](int i) { return rec16(R.u16, i, nt * d); };
+  auto FH16 = [&](int i) { return rec16(R.h16, i, nt * F); };
+  auto FS16 = [&](int i) { return rec16(R.s16, i, nt * d); };
   float* dhid = at<float>(ws, L.dhid);
   float* ds = at<float>(ws, L.ds);
   float* du = at<float>(ws, L.du);
@@ -501,9 +540,9 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   auto per_layer = [&](size_t off, int i, size_t per) { return at<float>(ws, off) + (size_t)i * per; };
   auto RS = [&](int i) { return per_layer(L.rs, i, nt * d); };
   auto RU = [&](int i) { return per_layer(L.ru, i, nt * d); };
-  auto RQ = [&](int i) { return per_layer(L.rq, i, nt * d); };
-  auto RA = [&](int i) { return per_layer(L.ra, i, nt * d); };
-  auto RL = [&](int i) { return per_layer(L.rl, i, nt * h); };
+  auto RQ = [&](int i) { return L.bfused ? rec32(R.q, i, nt * d) : per_layer(L.rq, i, nt * d); };
+  auto RA = [&](int i) { return L.bfused ? rec32(R.a, i, nt * d) : per_layer(L.ra, i, nt * d); };
+  auto RL = [&](int i) { return L.bfused ? rec32(R.lse, i, nt * h) : per_layer(L.rl, i, nt * h); };
   auto KVS = [&](int i) { return per_layer(L.kvs, i, nh * 2 * d); };
   // [W_K^0 | W_V^0 | W_K^1 | ...]: [d][n 2d], B operand of dX for every layer at once
   bf16_bits* wkv_all = bf ? at<bf16_bits>(ws, L.wkv) : nullptr;
@@ -523,7 +562,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   // of X^T, [W_K | W_V]^T and (dK | dV)^T); fp32 inputs keep fp32 products.
   if (bf) {
     const bf16_bits* X = static_cast<const bf16_bits*>(hist);
-    for (int i = 0; i < n; ++i) {
+    for (int i = 0; i < n && !rec_out; ++i) {
       const bf16_bits* Wk = reinterpret_cast<const bf16_bits*>(W(w->wk, i, (size_t)d * d));
       const bf16_bits* Wv = reinterpret_cast<const bf16_bits*>(W(w->wv, i, (size_t)d * d));
       HIPCHK(hipMemcpy2DAsync(wkv_all + (size_t)i * 2 * d, (size_t)n * 2 * d * 2, Wk, d * 2, d * 2, d,
@@ -535,7 +574,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
         HIPCHK(transpose_bf16(Wv, d, d, d, WKVT(i) + (size_t)d * d, d, d, st));
       }
     }
-    HIPCHK(transpose_bf16(X, d, static_cast<int>(nh), d, xt, nh8, nh8, st));
+    if (!rec_out) HIPCHK(transpose_bf16(X, d, static_cast<int>(nh), d, xt, nh8, nh8, st));
     if (L.bfused) {
       PackJobs pj{};
       pj.job[0] = {w->wk, at<char>(ws, L.fwkp), d, d, 0};
@@ -556,7 +595,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   // forward recomputation in fp32: s^(i), u^(i), and per layer K|V, the
   // scaled queries, the attention output and its lse
   UpdatePrecise up{};
-  if (L.bfused) {
+  if (L.bfused && !rec_in) {
     up.n_layers = n;
     up.F = F;
     up.n_tgt = nt;
@@ -571,13 +610,13 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     up.mode = 0;
     up.s_out = RS(0);
     up.q_out = RQ(0);
-    up.s16_out = at<bf16_bits>(ws, L.fs16);
+    up.s16_out = FS16(0);
     HIPCHK(fast_update_precise(d, up, st));
     HIPCHK(rec.mark("target_gemm"));
   } else {
     HIPCHK(convert(bf, 0, tgt, RS(0), nt * d, st));
   }
-  for (int i = 0; i < n && L.bfused; ++i) {
+  for (int i = 0; i < n && L.bfused && !rec_in; ++i) {
     FastAttnFwdPrecise f{};
     f.units = units;
     f.hdr = hdr;
@@ -601,10 +640,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     up.h_out = RH(i);
     up.s_out = RS(i + 1);
     up.q_out = i + 1 < n ? RQ(i + 1) : nullptr;
-    up.a16_out = at<bf16_bits>(ws, L.fa16) + (size_t)i * nt * d;
-    up.u16_out = at<bf16_bits>(ws, L.fu16) + (size_t)i * nt * d;
-    up.h16_out = at<bf16_bits>(ws, L.fh16) + (size_t)i * nt * F;
-    up.s16_out = i + 1 < n ? at<bf16_bits>(ws, L.fs16) + (size_t)(i + 1) * nt * d : nullptr;
+    up.a16_out = FA16(i);
+    up.u16_out = FU16(i);
+    up.h16_out = FH16(i);
+    up.s16_out = i + 1 < n ? FS16(i + 1) : nullptr;
     HIPCHK(fast_update_precise(d, up, st));
     HIPCHK(rec.mark("target_gemm"));
   }
@@ -635,6 +674,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     HIPCHK(gemm(0, bf, nt, d, F, RH(i), F, 0, W(w->w2, i, (size_t)d * F), d, 0, RS(i + 1), d, 1.f, kEpiAddRes,
                 RU(i), d, nullptr));
     HIPCHK(rec.mark("target_gemm"));
+  }
+  if (rec_out) {
+    // the forward of a training step: Y = s^(n) in the storage dtype
+    HIPCHK(convert(0, bf, RS(n), out, nt * d, st));
+    HIPCHK(rec.mark("out"));
+    return STCA_OK;
   }
   HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
   // rows of requests without targets keep a zero gradient (and dK|dV^T's
@@ -681,12 +726,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       ug.W1TP = at<char>(ws, L.fw1t);
       ug.WoTP = at<char>(ws, L.fwot);
       HIPCHK(fast_update_grad(d, ug, st));
-      HIPCHK(gemm_mfma(F, d, nti, B(L.fh16) + (size_t)i * nt * F, F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d,
-                       d, 1.f, 0, gp, gpf, st));
-      HIPCHK(gemm_mfma(d, F, nti, B(L.fu16) + (size_t)i * nt * d, d, 1, B(L.b_dhid), F, 0,
-                       dw->dw1 + (size_t)i * d * F, F, 1.f, 0, gp, gpf, st));
-      HIPCHK(gemm_mfma(d, d, nti, B(L.fa16) + (size_t)i * nt * d, d, 1, B(L.b_du), d, 0,
-                       dw->dwo + (size_t)i * d * d, d, 1.f, 0, gp, gpf, st));
+      HIPCHK(gemm_mfma(F, d, nti, FH16(i), F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, 0, gp, gpf,
+                       st));
+      HIPCHK(gemm_mfma(d, F, nti, FU16(i), d, 1, B(L.b_dhid), F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, 0, gp, gpf,
+                       st));
+      HIPCHK(gemm_mfma(d, d, nti, FA16(i), d, 1, B(L.b_du), d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, 0, gp, gpf,
+                       st));
     } else if (bf) {
       const int nti = static_cast<int>(nt);
       float* gp = at<float>(ws, L.gpart);
@@ -762,7 +807,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     if (bf) {
       const int nti = static_cast<int>(nt);
       HIPCHK(convert(0, 1, dq, at<bf16_bits>(ws, L.b_dq), nt * d, st));
-      const bf16_bits* s16 = L.bfused ? at<bf16_bits>(ws, L.fs16) + (size_t)i * nt * d : at<bf16_bits>(ws, L.b_s);
+      const bf16_bits* s16 = L.bfused ? FS16(i) : at<bf16_bits>(ws, L.b_s);
       if (!L.bfused) HIPCHK(convert(0, 1, s, at<bf16_bits>(ws, L.b_s), nt * d, st));
       HIPCHK(gemm_mfma(d, d, nti, s16, d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,
                        dw->dwq + (size_t)i * d * d, d, 1.f, 0, at<float>(ws, L.gpart), L.gpart_floats, st));
@@ -946,6 +991,49 @@ stca_status_t stca_backward_profiled(const stca_dims_t* dims, const stca_batch_t
   rec.labels = labels;
   rec.st = stream;
   return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, dout, dhist, dtgt, dw, ws, stream, rec);
+}
+
+size_t stca_train_record_size(const stca_dims_t* dims, const stca_batch_t* batch) {
+  Layout L;
+  if (!make_layout(dims, batch, 1, true, &L) || !L.bfused) return 0;
+  return record_layout(L).total;
+}
+
+stca_status_t stca_forward_train(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist,
+                                 const void* tgt, const stca_weights_t* w, void* out, void* record, void* ws,
+                                 size_t ws_bytes, hipStream_t stream) {
+  stca_status_t st = check_common(dims, batch, hist, tgt, w, ws);
+  if (st != STCA_OK) return st;
+  if ((batch->n_tgt > 0 && !out) || (out && !aligned16(out)) || !record || !aligned16(record))
+    return STCA_ERR_INVALID_ARG;
+  Layout L;
+  make_layout(dims, batch, 1, true, &L);
+  if (!L.bfused) return STCA_ERR_UNSUPPORTED;
+  if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
+  Rec none;
+  return backward_generic(L, 1, batch, hist, tgt, w, nullptr, nullptr, nullptr, nullptr, ws, stream, none, nullptr,
+                          record, out);
+}
+
+stca_status_t stca_backward_record(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist,
+                                   const void* tgt, const stca_weights_t* w, const void* record, const void* dout,
+                                   float* dhist, float* dtgt, const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
+                                   hipStream_t stream) {
+  stca_status_t st = check_common(dims, batch, hist, tgt, w, ws);
+  if (st != STCA_OK) return st;
+  if (!dw || (batch->n_tgt > 0 && (!dout || !dtgt)) || (batch->n_hist > 0 && !dhist) || !record ||
+      !aligned16(record))
+    return STCA_ERR_INVALID_ARG;
+  if (!dw->dwq || !dw->dwk || !dw->dwv || !dw->dwo || !dw->dw1 || !dw->dw2) return STCA_ERR_INVALID_ARG;
+  const void* ptrs[] = {dout, dhist, dtgt, dw->dwq, dw->dwk, dw->dwv, dw->dwo, dw->dw1, dw->dw2};
+  for (const void* q : ptrs)
+    if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
+  Layout L;
+  make_layout(dims, batch, 1, true, &L);
+  if (!L.bfused) return STCA_ERR_UNSUPPORTED;
+  if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
+  Rec none;
+  return backward_generic(L, 1, batch, hist, tgt, w, dout, dhist, dtgt, dw, ws, stream, none, record);
 }
 
 stca_status_t stca_device_status(const void* ws, hipStream_t stream) {

@@ -61,9 +61,15 @@ class DeviceBatch:
             self.saved = torch.empty(self.saved_bytes, dtype=torch.uint8, device=device)
             self.layout = stca.stca_saved_layout(self.dims, self.batch)
         self.bws = None
+        self.record = None
         if backward:
             self.bws_bytes = stca.stca_workspace_size(self.dims, self.batch, True)
             self.bws = torch.empty(self.bws_bytes, dtype=torch.uint8, device=device)
+            # training record for stca_forward_train / stca_backward_record
+            # (batches the fused backward takes)
+            rec = stca.stca_train_record_size(self.dims, self.batch)
+            if rec:
+                self.record = torch.empty(rec, dtype=torch.uint8, device=device)
 
     def stream(self):
         return _torch().cuda.current_stream(self.device).cuda_stream
@@ -87,7 +93,15 @@ class DeviceBatch:
         flat = self.saved[off:off + 4 * count].view(torch.float32)
         return flat.view(n, nt, cols)
 
-    def backward(self, dout, stream: Optional[int] = None):
+    def forward_train(self, stream: Optional[int] = None):
+        """Forward of a training step: out and the training record."""
+        stca.stca_forward_train(self.dims, self.batch, self.hist, self.tgt, self.weights, self.out, self.record,
+                                self.bws, self.bws_bytes, self.stream() if stream is None else stream)
+        return self.out
+
+    def backward(self, dout, stream: Optional[int] = None, use_record: bool = False):
+        """Gradients of sum <dout, out>; with use_record, from the record of the
+        last forward_train call instead of a recomputation."""
         torch = _torch()
         wl = self.b.wl
         d, F, n = wl.d_model, wl.ffn_hidden, wl.n_layers
@@ -100,9 +114,14 @@ class DeviceBatch:
             "dw1": torch.empty((n, d, F), **f32), "dw2": torch.empty((n, F, d), **f32),
         }
         dw = stca.wgrads(g["dwq"], g["dwk"], g["dwv"], g["dwo"], g["dw1"], g["dw2"])
-        stca.stca_backward(self.dims, self.batch, self.hist, self.tgt, self.weights, dout,
-                           g["dhist"], g["dtgt"], dw, self.bws, self.bws_bytes,
-                           self.stream() if stream is None else stream)
+        if use_record:
+            stca.stca_backward_record(self.dims, self.batch, self.hist, self.tgt, self.weights, self.record, dout,
+                                      g["dhist"], g["dtgt"], dw, self.bws, self.bws_bytes,
+                                      self.stream() if stream is None else stream)
+        else:
+            stca.stca_backward(self.dims, self.batch, self.hist, self.tgt, self.weights, dout,
+                               g["dhist"], g["dtgt"], dw, self.bws, self.bws_bytes,
+                               self.stream() if stream is None else stream)
         return g
 
 

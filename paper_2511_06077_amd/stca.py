@@ -21,7 +21,8 @@ EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca
             "stca_forward_profiled", "stca_backward_launch_count", "stca_backward_profiled",
             "stca_sl_beta", "stca_sl_sample", "stca_sl_allocate", "stca_sl_pack",
             "stca_paper_workspace_size", "stca_paper_saved_size", "stca_paper_saved_layout", "stca_forward_paper",
-            "stca_paper_launch_count", "stca_forward_paper_profiled")
+            "stca_paper_launch_count", "stca_forward_paper_profiled", "stca_train_record_size", "stca_forward_train",
+            "stca_backward_record")
 PAPER_WEIGHT_FIELDS = ("ffn_u", "ffn_v", "ffn_o", "wq", "wk", "wv", "wo", "wc", "wz", "z_u", "z_v", "z_o")
 
 
@@ -114,6 +115,17 @@ def lib():
                                              P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                              P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
                                              P(ctypes.c_void_p), ctypes.c_int, P(ctypes.c_char_p)]
+        L.stca_train_record_size.restype = ctypes.c_size_t
+        L.stca_train_record_size.argtypes = [P(stca_dims_t), P(stca_batch_t)]
+        L.stca_forward_train.restype = ctypes.c_int
+        L.stca_forward_train.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                         P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                         ctypes.c_size_t, ctypes.c_void_p]
+        L.stca_backward_record.restype = ctypes.c_int
+        L.stca_backward_record.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                           P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                           ctypes.c_void_p, P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t,
+                                           ctypes.c_void_p]
         I32P = P(ctypes.c_int32)
         L.stca_sl_beta.restype = ctypes.c_double
         L.stca_sl_beta.argtypes = [ctypes.c_double, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
@@ -214,6 +226,28 @@ def stca_backward(d, b, hist, tgt, w, dout, dhist, dtgt, dw, ws, ws_bytes: int, 
                              _ptr(stream))
     if check and st != STCA_OK:
         raise StcaError(st, "stca_backward")
+    return st
+
+
+def stca_train_record_size(d: stca_dims_t, b: stca_batch_t) -> int:
+    return lib().stca_train_record_size(ctypes.byref(d), ctypes.byref(b))
+
+
+def stca_forward_train(d, b, hist, tgt, w, out, record, ws, ws_bytes: int, stream=None, check: bool = True) -> int:
+    st = lib().stca_forward_train(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w),
+                                  _ptr(out), _ptr(record), _ptr(ws), int(ws_bytes), _ptr(stream))
+    if check and st != STCA_OK:
+        raise StcaError(st, "stca_forward_train")
+    return st
+
+
+def stca_backward_record(d, b, hist, tgt, w, record, dout, dhist, dtgt, dw, ws, ws_bytes: int, stream=None,
+                         check: bool = True) -> int:
+    st = lib().stca_backward_record(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w),
+                                    _ptr(record), _ptr(dout), _ptr(dhist), _ptr(dtgt), ctypes.byref(dw), _ptr(ws),
+                                    int(ws_bytes), _ptr(stream))
+    if check and st != STCA_OK:
+        raise StcaError(st, "stca_backward_record")
     return st
 
 

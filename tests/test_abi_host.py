@@ -188,6 +188,11 @@ def test_fused_backward_selection(monkeypatch):
     assert stca.stca_backward_launch_count(dims(d_model=256, n_heads=4), small) == 6 + 7 * n  # d_h = 64
     assert stca.stca_backward_launch_count(dims(dtype=stca.STCA_F32), small) == 4 + 9 * n
     assert stca.stca_backward_launch_count(dims(ffn_hidden=3 * 128), small) == 6 + 7 * n  # F not a multiple of d
+    # the training record exists exactly for the batches the fused form takes
+    assert stca.stca_train_record_size(dims(), small) > 0
+    assert stca.stca_train_record_size(dims(), big) == 0
+    assert stca.stca_train_record_size(dims(), nohost) == 0
+    assert stca.stca_train_record_size(dims(dtype=stca.STCA_F32), small) == 0
     long, keep3 = fake_batch([0, 60000, 100000], [0, 32, 40])
     d, F = GOOD_DIMS["d_model"], GOOD_DIMS["ffn_hidden"]
     fused = stca.stca_workspace_size(dims(), long, True)

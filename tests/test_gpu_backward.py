@@ -102,6 +102,35 @@ def test_fused_and_generic_backward_agree(torch, chunk_override, monkeypatch):
         assert e <= TOL["bf16"], (k, e)
 
 
+def test_training_record(torch, chunk_override):
+    """Training step in two calls: stca_forward_train's output against the
+    oracle, and stca_backward_record's gradients identical to the recomputing
+    stca_backward's (the same kernels on the same inputs), also after the
+    workspace was reused in between."""
+    from paper_2511_06077_amd.device import DeviceBatch, to_device
+    chunk_override(3)
+    b = W.make_custom_batch("grec", [1, 33, 130, 64, 7, 300], [2, 31, 0, 17, 1, 32], d_model=256, n_heads=8,
+                            n_layers=2, dtype="bf16", seed=43, with_grad=True)
+    db = DeviceBatch(b, backward=True)
+    assert db.record is not None
+    y = db.forward_train().float().cpu().numpy().astype(np.float64)
+    dout = to_device(b.grad_out, "cuda")
+    g_rec = db.backward(dout, use_record=True)
+    g_full = db.backward(dout)
+    g_rec2 = db.backward(dout, use_record=True)
+    torch.cuda.synchronize()
+    f = b.f64()
+    ref_y = O.forward(f, keep=False)["out"]
+    err = float(np.max(np.abs(y - ref_y).max(axis=1) / np.abs(ref_y).max(axis=1)))
+    print(f"[grad] forward_train y err {err:.1e}", flush=True)
+    assert err <= TOL["bf16"], err
+    for k in GRADS:
+        a, r, a2 = g_rec[k].cpu().numpy(), g_full[k].cpu().numpy(), g_rec2[k].cpu().numpy()
+        assert np.array_equal(a, r), k
+        assert np.array_equal(a, a2), k
+    check(b, {k: v.cpu().numpy().astype(np.float64) for k, v in g_rec.items()}, TOL["bf16"])
+
+
 def test_training_window_gradients(torch, chunk_override):
     """256 requests x 16 targets, L = 2048, d = 256, 4 layers (the training
     window).  History and target gradients are per request, so they are
