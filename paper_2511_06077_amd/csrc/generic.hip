@@ -1,7 +1,9 @@
 // Generic fp32-arithmetic kernels: any supported head width, fp32 or bf16
 // storage.  They serve the fp32 storage type (whose tolerance bf16 MFMA
 // arithmetic cannot meet) and the backward pass's small target-side GEMMs.
-// Plain SIMT code with LDS tiling; the bf16 hot path has its own MFMA kernels.
+// LDS-tiled kernels; products with bf16 weights run on the bf16 matrix cores
+// with the fp32 operand split into three bf16 terms (exact products), the
+// others on the fp32 matrix cores; the bf16 hot path has its own kernels.
 #include "common.h"
 #include "internal.h"
 
@@ -99,6 +101,128 @@ __global__ __launch_bounds__(256) void gemm_kernel(int M, int N, int K, const TA
       atomicAdd(c, x);
       continue;
     }
+    if (epi == kEpiAddRes) x += R[(int64_t)gm * ldr + gn];
+    if (epi == kEpiRelu) {
+      if (C2) C2[(int64_t)gm * ldc + gn] = x;
+      x = fmaxf(x, 0.f);
+    }
+    *c = accumulate ? *c + x : x;
+  }
+}
+
+// fp32-accurate products with bf16 weights on the bf16 matrix cores:
+// C = epi(alpha A B), A [M][K] fp32 (or bf16) row-major, B [K][N] bf16
+// row-major.  Each fp32 value of A is split into three bf16 terms (the whole
+// fp32 mantissa over fp32's exponent range); every product of two bf16
+// values is exact in fp32 and the MFMA sums are fp32, so the result matches
+// an fp32 product (a bf16 A is one term).  64 x 64 output tile per workgroup
+// of four waves (each one 32 x 32 v_mfma_f32_32x32x16_bf16 tile), 32-deep k
+// tiles double-buffered in LDS (A's terms as [m][k], B transposed to [n][k]).
+typedef unsigned short u16x8g __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x8g __attribute__((ext_vector_type(8)));
+constexpr int SBK = 32;
+constexpr int SROW = SBK + 8;  // padded LDS row (bf16 elements)
+
+template <typename TA>
+__global__ __launch_bounds__(256) void gemm_bf16w_kernel(int M, int N, int K, const TA* __restrict__ A, int64_t lda,
+                                                         const bf16_bits* __restrict__ B, int64_t ldb,
+                                                         float* __restrict__ C, int64_t ldc, float alpha, int epi,
+                                                         const float* __restrict__ R, int64_t ldr,
+                                                         float* __restrict__ C2, int accumulate) {
+  constexpr int TERMS = sizeof(TA) == 4 ? 3 : 1;
+  __shared__ __attribute__((aligned(16))) bf16_bits As[2][TERMS][GT * SROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits Bs[2][GT * SROW];
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int wm = (wave / 2) * 32, wn = (wave % 2) * 32;
+  const int r32 = lane % 32, hi = lane / 32;
+  const int m0 = blockIdx.y * GT, n0 = blockIdx.x * GT;
+  // this thread's share of a k tile: A (64 x 32) and B (32 x 64)
+  constexpr int AV = sizeof(TA) == 4 ? 2 : 1;  // 16-byte vectors of A per thread
+  float4 ra[2];
+  u16x8g ra16;
+  u16x8g rb;
+  auto load = [&](int k0) {
+    if (sizeof(TA) == 4) {
+#pragma unroll
+      for (int i = 0; i < AV; ++i) {
+        const int v = threadIdx.x + 256 * i;
+        const int row = v / (SBK / 4), kk = (v % (SBK / 4)) * 4;
+        const bool ok = m0 + row < M && k0 + kk < K;
+        ra[i] = ok ? *reinterpret_cast<const float4*>(reinterpret_cast<const float*>(A) + (int64_t)(m0 + row) * lda +
+                                                      k0 + kk)
+                   : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    } else {
+      const int row = threadIdx.x / (SBK / 8), kk = (threadIdx.x % (SBK / 8)) * 8;
+      const bool ok = m0 + row < M && k0 + kk < K;
+      ra16 = ok ? *reinterpret_cast<const u16x8g*>(reinterpret_cast<const bf16_bits*>(A) + (int64_t)(m0 + row) * lda +
+                                                   k0 + kk)
+                : u16x8g{0, 0, 0, 0, 0, 0, 0, 0};
+    }
+    const int kk = threadIdx.x / (GT / 8), nn = (threadIdx.x % (GT / 8)) * 8;
+    const bool ok = k0 + kk < K && n0 + nn < N;
+    rb = ok ? *reinterpret_cast<const u16x8g*>(B + (int64_t)(k0 + kk) * ldb + n0 + nn)
+            : u16x8g{0, 0, 0, 0, 0, 0, 0, 0};
+  };
+  auto store = [&](int buf) {
+    if (sizeof(TA) == 4) {
+#pragma unroll
+      for (int i = 0; i < AV; ++i) {
+        const int v = threadIdx.x + 256 * i;
+        const int row = v / (SBK / 4), kk = (v % (SBK / 4)) * 4;
+        float x[4] = {ra[i].x, ra[i].y, ra[i].z, ra[i].w};
+#pragma unroll
+        for (int t = 0; t < TERMS; ++t) {
+          uint2 pk;
+          bf16_bits b[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            b[e] = from_f32<bf16_bits>(x[e]);
+            x[e] -= to_f32(b[e]);
+          }
+          pk.x = (uint32_t)b[0] | ((uint32_t)b[1] << 16);
+          pk.y = (uint32_t)b[2] | ((uint32_t)b[3] << 16);
+          *reinterpret_cast<uint2*>(&As[buf][t][row * SROW + kk]) = pk;
+        }
+      }
+    } else {
+      const int row = threadIdx.x / (SBK / 8), kk = (threadIdx.x % (SBK / 8)) * 8;
+      *reinterpret_cast<u16x8g*>(&As[buf][0][row * SROW + kk]) = ra16;
+    }
+    const int kk = threadIdx.x / (GT / 8), nn = (threadIdx.x % (GT / 8)) * 8;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) Bs[buf][(nn + e) * SROW + kk] = rb[e];
+  };
+  f32x16 acc = {};
+  load(0);
+  store(0);
+  __syncthreads();
+  int buf = 0;
+  for (int k0 = 0; k0 < K; k0 += SBK) {
+    const bool more = k0 + SBK < K;
+    if (more) load(k0 + SBK);
+#pragma unroll
+    for (int ks = 0; ks < SBK / 16; ++ks) {
+      const bf16x8g b = *reinterpret_cast<const bf16x8g*>(&Bs[buf][(wn + r32) * SROW + ks * 16 + hi * 8]);
+#pragma unroll
+      for (int t = 0; t < TERMS; ++t) {
+        const bf16x8g a = *reinterpret_cast<const bf16x8g*>(&As[buf][t][(wm + r32) * SROW + ks * 16 + hi * 8]);
+        acc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, acc, 0, 0, 0);
+      }
+    }
+    if (more) store(buf ^ 1);  // that buffer was last read before the previous barrier
+    __syncthreads();
+    buf ^= 1;
+  }
+  // result lane layout: column n = lane % 32, rows 8 (v / 4) + 4 hi + v % 4
+  const int gn = n0 + wn + r32;
+  if (gn >= N) return;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) {
+    const int gm = m0 + wm + 8 * (v / 4) + 4 * hi + (v % 4);
+    if (gm >= M) continue;
+    float x = alpha * acc[v];
+    float* c = C + (int64_t)gm * ldc + gn;
     if (epi == kEpiAddRes) x += R[(int64_t)gm * ldr + gn];
     if (epi == kEpiRelu) {
       if (C2) C2[(int64_t)gm * ldc + gn] = x;
@@ -253,32 +377,36 @@ __global__ __launch_bounds__(256) void attn_generic_kernel(const Unit* __restric
 }
 
 // Merge the per-chunk partial results of every (target, head).
+// One thread per (target, head, 4 consecutive dims): every chunk's (max, sum)
+// and 16-byte slices of its accumulator, so a head's merge is d_h / 4 threads
+// reading whole cache lines instead of one thread walking d_h floats.
 __global__ void merge_generic_kernel(int dh, int n_heads, int64_t n_tgt, const int32_t* __restrict__ tchunks,
                                      const float* __restrict__ part_acc, const float* __restrict__ part_ml,
                                      float* __restrict__ a, float* __restrict__ lse) {
+  const int q4 = dh / 4;
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (idx >= n_tgt * n_heads) return;
-  const int64_t t = idx / n_heads;
-  const int j = idx % n_heads;
+  if (idx >= n_tgt * n_heads * q4) return;
+  const int64_t th = idx / q4;  // (target, head)
+  const int e = static_cast<int>(idx % q4) * 4;
+  const int64_t t = th / n_heads;
+  const int j = static_cast<int>(th % n_heads);
   const int d = dh * n_heads;
   const int nch = tchunks[t];
+  const float2* ml = reinterpret_cast<const float2*>(part_ml);
   float M = -INFINITY;
-  for (int c = 0; c < nch; ++c) M = fmaxf(M, part_ml[(((int64_t)c * n_tgt + t) * n_heads + j) * 2]);
+  for (int c = 0; c < nch; ++c) M = fmaxf(M, ml[((int64_t)c * n_tgt + t) * n_heads + j].x);
   float L = 0.f;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
   for (int c = 0; c < nch; ++c) {
-    const float* pm = part_ml + (((int64_t)c * n_tgt + t) * n_heads + j) * 2;
-    L += exp2f(pm[0] - M) * pm[1];
+    const float2 m = ml[((int64_t)c * n_tgt + t) * n_heads + j];
+    const float wc = exp2f(m.x - M);
+    L += wc * m.y;
+    const float4 x = *reinterpret_cast<const float4*>(part_acc + ((int64_t)c * n_tgt + t) * d + j * dh + e);
+    v.x += wc * x.x, v.y += wc * x.y, v.z += wc * x.z, v.w += wc * x.w;
   }
   const float inv = 1.f / L;
-  for (int e = 0; e < dh; ++e) {
-    float v = 0.f;
-    for (int c = 0; c < nch; ++c) {
-      const float wc = exp2f(part_ml[(((int64_t)c * n_tgt + t) * n_heads + j) * 2] - M);
-      v += wc * part_acc[((int64_t)c * n_tgt + t) * d + j * dh + e];
-    }
-    a[t * d + j * dh + e] = v * inv;
-  }
-  if (lse) lse[t * n_heads + j] = (M + log2f(L)) * kLn2;
+  *reinterpret_cast<float4*>(a + t * d + j * dh + e) = make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv);
+  if (lse && e == 0) lse[t * n_heads + j] = (M + log2f(L)) * kLn2;
 }
 
 // ------------------------------------------------- attention backward
@@ -521,6 +649,21 @@ hipError_t gemm_generic(int a_bf16, int b_bf16, int M, int N, int K, const void*
   }
   const int k_chunk = static_cast<int>(round_up(ceil_div(K, splits), GK));
   splits = static_cast<int>(ceil_div(K, k_chunk));
+  // bf16 weights, untransposed operands, no split: the bf16 matrix cores with
+  // A split into bf16 terms (whole 16-byte vectors: K, N and the leading
+  // dimensions multiples of 8, 16-byte aligned operands)
+  const auto al16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+  if (splits == 1 && b_bf16 && !transA && !transB && K % 8 == 0 && N % 8 == 0 && lda % 8 == 0 && ldb % 8 == 0 &&
+      al16(A) && al16(B)) {
+    dim3 g2(static_cast<unsigned>(ceil_div(N, GT)), static_cast<unsigned>(ceil_div(M, GT)));
+    if (a_bf16)
+      hipLaunchKernelGGL((gemm_bf16w_kernel<bf16_bits>), g2, dim3(256), 0, st, M, N, K, (const bf16_bits*)A, lda,
+                         (const bf16_bits*)B, ldb, C, ldc, alpha, (int)epi, R, ldr, C2, accumulate);
+    else
+      hipLaunchKernelGGL((gemm_bf16w_kernel<float>), g2, dim3(256), 0, st, M, N, K, (const float*)A, lda,
+                         (const bf16_bits*)B, ldb, C, ldc, alpha, (int)epi, R, ldr, C2, accumulate);
+    return hipGetLastError();
+  }
   if (splits > 1 && !accumulate)
     hipLaunchKernelGGL(fill2d_kernel, grid1((int64_t)M * N, 256), dim3(256), 0, st, C, ldc, M, N);
   dim3 g(static_cast<unsigned>(ceil_div(N, GT)), static_cast<unsigned>(ceil_div(M, GT)), splits);
@@ -559,8 +702,9 @@ hipError_t attn_generic(int d_head, int n_heads, const Unit* units, int64_t max_
 hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* tchunks, const float* part_acc,
                          const float* part_ml, float* a, float* lse, hipStream_t st) {
   if (n_tgt == 0) return hipSuccess;
-  hipLaunchKernelGGL(merge_generic_kernel, grid1(n_tgt * n_heads, 256), dim3(256), 0, st, d_head, n_heads,
-                     n_tgt, tchunks, part_acc, part_ml, a, lse);
+  if (d_head % 4) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(merge_generic_kernel, grid1(n_tgt * n_heads * (d_head / 4), 256), dim3(256), 0, st, d_head,
+                     n_heads, n_tgt, tchunks, part_acc, part_ml, a, lse);
   return hipGetLastError();
 }
 
@@ -571,8 +715,8 @@ hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t 
                             hipStream_t st) {
   if (max_units == 0) return hipSuccess;
   if (attn_mfma_supported(d_head))
-    return attn_bwd_mfma(d_head, n_heads, units, max_units, hdr, toff, Q, KV, d, a, da, lse, dq_part, dKV, ldkv, dkv_bf16,
-                         dKVT, ldt, n_tgt, st);
+    return attn_bwd_mfma(d_head, n_heads, units, max_units, hdr, toff, Q, KV, d, a, da, lse, dq_part, dKV, ldkv,
+                         dkv_bf16, dKVT, ldt, n_tgt, st);
   dim3 g(static_cast<unsigned>(max_units), n_heads);
 #define STCA_ATTB(DH)                                                                                      \
   if (dkv_bf16)                                                                                            \
