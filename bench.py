@@ -388,7 +388,8 @@ def backward_phase_work(label: str, b: W.Batch, fused: bool):
     fused (requests of at most 32 targets): the recomputed attention and the
     attention backward each project the history inside the kernel (X read
     once per layer; K/V projection 4 L d^2 flop), on the bf16 matrix cores;
-    the attention backward writes dK | dV in bf16 in two layouts; the target
+    the attention backward writes dK | dV once, row-major bf16 (read as they
+    are by both history-side products after the layers); the target
     side (recomputation and gradients) runs on bf16 operands.  Otherwise:
     the K|V product with fp32 output, the exact fp32 attention on the fp32
     MFMA (157.3 TFLOP/s), target-side products in fp32 where they decide ReLU
@@ -401,7 +402,7 @@ def backward_phase_work(label: str, b: W.Batch, fused: bool):
     mt = float(b.n_tgt.sum())
     if label == "kv_gemm":
         return 4 * Ls * d * d, 2 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
-    if label == "dw_kv":  # X^T read once, every layer's (dK | dV)^T
+    if label == "dw_kv":  # X (or X^T) read once, every layer's dK | dV (or its transpose)
         return n * 4 * Ls * d * d, 2 * Ls * d + n * 4 * Ls * d, PEAK_BF16_TFLOPS
     if label == "dx":  # every layer's dK | dV read, dX written once (fp32)
         return n * 4 * Ls * d * d, n * 4 * Ls * d + 4 * Ls * d, PEAK_BF16_TFLOPS
@@ -411,7 +412,7 @@ def backward_phase_work(label: str, b: W.Batch, fused: bool):
         return 4 * mL * d, 8 * Ls * d, PEAK_FP32_TFLOPS
     if label == "attn_bwd":
         if fused:
-            return 4 * Ls * d * d + 10 * mL * d, 2 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
+            return 4 * Ls * d * d + 10 * mL * d, 2 * Ls * d + 4 * Ls * d, PEAK_BF16_TFLOPS
         return 10 * mL * d, 8 * Ls * d + 8 * Ls * d, PEAK_FP32_TFLOPS
     if label == "target_gemm":
         if fused:

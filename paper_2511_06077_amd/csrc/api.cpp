@@ -207,18 +207,17 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
     // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
     L->dkv = m.take(bf ? 2 * nh * n * 2 * d : 4 * nh * 2 * d);
-    // bf16 history-side products: [W_K | W_V] per layer and its transpose,
-    // X^T and (dK | dV)^T with the history rows padded to a multiple of 8
-    // rows of the transposed copies, padded (to whole 32-row blocks when the
-    // fused attention backward writes (dK | dV)^T in 32-row blocks)
-    L->nh8 = round_up(static_cast<int64_t>(nh), L->bfused ? 32 : 8);
+    // bf16 history-side products: [W_K | W_V] per layer, and for the
+    // unfused form its transpose, X^T and every layer's (dK | dV)^T
+    // ([n 2d][nh8]) with the history rows padded to a multiple of 8 (the
+    // fused form's [dW_K | dW_V] reads X and dK | dV as they are)
+    L->nh8 = round_up(static_cast<int64_t>(nh), 8);
     const size_t nh8 = static_cast<size_t>(L->nh8);
+    const bool tcopies = bf && !L->bfused;
     L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;
-    L->wkvt = bf && !L->bfused ? m.take(2 * n * d * 2 * d) : 0;
-    L->xt = bf ? m.take(2 * d * nh8) : 0;
-    // every layer's (dK | dV)^T: [n 2d][nh8], or for the fused backward in
-    // 32-row blocks, [nh8 / 32][n 2d][32]
-    L->dkvt = bf ? m.take(2 * n * 2 * d * nh8) : 0;
+    L->wkvt = tcopies ? m.take(2 * n * d * 2 * d) : 0;
+    L->xt = tcopies ? m.take(2 * d * nh8) : 0;
+    L->dkvt = tcopies ? m.take(2 * n * 2 * d * nh8) : 0;
     L->dwkv = bf ? m.take(4 * d * n * 2 * d) : 0;   // [d][n 2d] fp32
     // split-K partials: the largest of [dW_K | dW_V] (K = history rows) and
     // the target-side weight gradients (K = targets)
@@ -547,8 +546,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   // [W_K^0 | W_V^0 | W_K^1 | ...]: [d][n 2d], B operand of dX for every layer at once
   bf16_bits* wkv_all = bf ? at<bf16_bits>(ws, L.wkv) : nullptr;
   auto WKVT = [&](int i) { return at<bf16_bits>(ws, L.wkvt) + (size_t)i * d * 2 * d; };
-  bf16_bits* xt = bf ? at<bf16_bits>(ws, L.xt) : nullptr;
-  bf16_bits* dkvt = bf ? at<bf16_bits>(ws, L.dkvt) : nullptr;
+  bf16_bits* xt = bf && !L.bfused ? at<bf16_bits>(ws, L.xt) : nullptr;
+  bf16_bits* dkvt = bf && !L.bfused ? at<bf16_bits>(ws, L.dkvt) : nullptr;
   const int nh8 = static_cast<int>(L.nh8);
   auto gemm = [&](int a_bf, int b_bf, int M, int N, int K, const void* A, int64_t lda, int tA, const void* B,
                   int64_t ldb, int tB, float* C, int64_t ldc, float alpha, GemmEpi epi, const float* R,
@@ -574,7 +573,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
         HIPCHK(transpose_bf16(Wv, d, d, d, WKVT(i) + (size_t)d * d, d, d, st));
       }
     }
-    if (!rec_out) HIPCHK(transpose_bf16(X, d, static_cast<int>(nh), d, xt, nh8, nh8, st));
+    if (!rec_out && !L.bfused) HIPCHK(transpose_bf16(X, d, static_cast<int>(nh), d, xt, nh8, nh8, st));
     if (L.bfused) {
       PackJobs pj{};
       pj.job[0] = {w->wk, at<char>(ws, L.fwkp), d, d, 0};
@@ -686,7 +685,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   // padding columns stay zero)
   if (bf) {
     HIPCHK(zero_untargeted(b->hist_off, b->tgt_off, b->n_requests, nh, static_cast<bf16_bits*>(dkv), n * 2 * d,
-                           n * 2 * d, dkvt, nh8, L.bfused ? 1 : 0, st));
+                           n * 2 * d, dkvt, nh8, st));
   } else {
     HIPCHK(fill_f32(static_cast<float*>(dkv), 0.f, nh * 2 * d, st));
     HIPCHK(fill_f32(dhist, 0.f, nh * d, st));
@@ -791,8 +790,6 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       f.lse = RL(i);
       f.dKV = static_cast<bf16_bits*>(dkv_i);
       f.ldkv = n * 2 * d;
-      f.dKVT = dkvt;
-      f.ldt = n * 2 * d;
       f.dq_part = dqp;
       f.n_tgt = nt;
       HIPCHK(fast_attn_bwd(d, f, fgrid, st));
@@ -841,12 +838,18 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   }
   if (bf) {
     // [dW_K^i | dW_V^i] for every layer = X^T [dK^i | dV^i] (one product over
-    // the history rows), then dX = sum_i [dK^i | dV^i] [W_K^i | W_V^i]^T as
-    // one product with K = n 2d, written once
+    // the history rows: the fused form reads X and dK | dV row-major, the
+    // unfused one their transposed copies), then
+    // dX = sum_i [dK^i | dV^i] [W_K^i | W_V^i]^T as one product with
+    // K = n 2d, written once
     float* dwkv = at<float>(ws, L.dwkv);
-    HIPCHK(gemm_mfma(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, L.bfused ? n * 2 * d : nh8, L.bfused ? 2 : 1, dwkv,
-                     n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
-                     L.gpart_floats, st));
+    if (L.bfused)
+      HIPCHK(gemm_mfma(d, n * 2 * d, static_cast<int>(nh), static_cast<const bf16_bits*>(hist), d, 1,
+                       static_cast<const bf16_bits*>(dkv), n * 2 * d, 0, dwkv, n * 2 * d, 1.f, 0,
+                       at<float>(ws, L.gpart), L.gpart_floats, st));
+    else
+      HIPCHK(gemm_mfma(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
+                       L.gpart_floats, st));
     for (int i = 0; i < n; ++i) {
       HIPCHK(hipMemcpy2DAsync(dw->dwk + (size_t)i * d * d, d * 4, dwkv + (size_t)i * 2 * d, (size_t)n * 2 * d * 4,
                               d * 4, d, hipMemcpyDeviceToDevice, st));

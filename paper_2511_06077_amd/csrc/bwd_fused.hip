@@ -268,10 +268,8 @@ __global__ __launch_bounds__(64 * (D / 32)) void bwd_fused_kernel(FastAttnBwd A)
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
   };
 
-  // rows [l0, l1) of block b: stores of this lane's row-major gradient row and
-  // of its transposed column
+  // stores of this lane's gradient row
   bf16_bits* __restrict__ dKV = A.dKV;
-  bf16_bits* __restrict__ dKVT = A.dKVT;
   auto store_rows = [&](const f32x16& g, int col0, int row, bool rok) {
     // g: lane = history row `row`, element v = head dim vrow(v, hi)
     if (!rok) return;
@@ -282,45 +280,6 @@ __global__ __launch_bounds__(64 * (D / 32)) void bwd_fused_kernel(FastAttnBwd A)
       w.x = pack2(g[4 * q], g[4 * q + 1]);
       w.y = pack2(g[4 * q + 2], g[4 * q + 3]);
       *reinterpret_cast<uint2*>(p + 8 * q) = w;
-    }
-  };
-  auto store_cols = [&](const f32x16& g, int col, int b, const Unit& un, bool full) {
-    // g: lane = head dim col, element v = block row blk_row<RPS>(vrow(v, hi))
-    // (dK | dV)^T in 32-row blocks: this layer's column col of block b is
-    // 32 contiguous rows
-    bf16_bits* p = dKVT + ((int64_t)b * A.ldt + A.layer * 2 * D + col) * 32;
-    if (full && (RPS == 2 || RPS == 4)) {
-      // the lane's 16 rows form two runs of 8 consecutive rows
-#pragma unroll
-      for (int run = 0; run < 2; ++run) {
-        float v8[8];
-#pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          // element holding row base + k of this run
-          int v;
-          if (RPS == 2) {
-            v = 4 * run + 8 * (k % 2) + k / 2;  // row 16 run + 8 hi + k
-          } else {
-            const int kk = 8 * run + k;  // row 16 hi + kk
-            v = 4 * (kk % 4) + kk / 4;
-          }
-          v8[k] = g[v];
-        }
-        const int base = RPS == 2 ? 8 * hi + 16 * run : 16 * hi + 8 * run;
-        uint4 w;
-        w.x = pack2(v8[0], v8[1]);
-        w.y = pack2(v8[2], v8[3]);
-        w.z = pack2(v8[4], v8[5]);
-        w.w = pack2(v8[6], v8[7]);
-        *reinterpret_cast<uint4*>(p + base) = w;
-      }
-    } else {
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int r = blk_row<RPS>(vrow(v, hi));
-        const int row = b * 32 + r;
-        if (row >= un.l0 && row < un.l1) p[r] = from_f32<bf16_bits>(g[v]);
-      }
     }
   };
 
@@ -375,7 +334,6 @@ __global__ __launch_bounds__(64 * (D / 32)) void bwd_fused_kernel(FastAttnBwd A)
     const bf16x8 pb[2] = {pack_b(s, 0), pack_b(s, 8)};
     const bf16x8 eb[2] = {pack_b(dp, 0), pack_b(dp, 8)};
     fence();
-    const bool full = cb * 32 >= cun.l0 && cb * 32 + 32 <= cun.l1;
     // dV^T = dA^T P and dK^T = Q^T dE (lane = row): row-major dK | dV
     {
       f32x16 g = mma(get_b(kDt), pb[0], f32x16{});
@@ -386,18 +344,6 @@ __global__ __launch_bounds__(64 * (D / 32)) void bwd_fused_kernel(FastAttnBwd A)
       g = mma(get_b(kQt + 1), eb[1], g);
       g *= kLn2;
       store_rows(g, wave * DH, row, rok);
-    }
-    fence();
-    // dV = P^T dA and dK = dE^T Q (lane = dim): the transposed copy
-    {
-      f32x16 g = mma(pb[0], get_b(kDt), f32x16{});
-      g = mma(pb[1], get_b(kDt + 1), g);
-      store_cols(g, D + wave * DH + tcol, cb, cun, full);
-      fence();
-      g = mma(eb[0], get_b(kQt), f32x16{});
-      g = mma(eb[1], get_b(kQt + 1), g);
-      g *= kLn2;
-      store_cols(g, wave * DH + tcol, cb, cun, full);
     }
     fence();
     // dQ += dE K: dE^T with rows in the elements (lane = target) from dE

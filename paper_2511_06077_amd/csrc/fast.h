@@ -55,10 +55,8 @@ hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st);
 // Attention backward with the history projection inside the kernel
 // (bwd_fused.hip), for units of at most 32 targets (one unit per history
 // chunk of a request): writes this layer's dK | dV rows ([N_hist] rows of
-// pitch ldkv, dK in columns [0, D), dV in [D, 2D)) and their transpose in
-// 32-row blocks (row r, column c of layer l at
-// ((r / 32) ldt + 2 D l + c) 32 + r % 32, ldt columns per block row) for the
-// history rows of every unit, and each unit's dq partial ([chunk][n_tgt][D],
+// pitch ldkv, dK in columns [0, D), dV in [D, 2D)) for the history rows of
+// every unit, and each unit's dq partial ([chunk][n_tgt][D],
 // scaled by 1/sqrt(d_h)).  Q: fp32 queries scaled by log2(e)/sqrt(d_h); a,
 // da: attention output and its gradient; lse: the forward's natural
 // log-sum-exp per (target, head).
@@ -72,8 +70,6 @@ struct FastAttnBwd {
   const float *Q, *a, *da, *lse;
   bf16_bits* dKV;
   int64_t ldkv;
-  bf16_bits* dKVT;
-  int64_t ldt;
   float* dq_part;
   int64_t n_tgt;
 };

@@ -1,23 +1,26 @@
-// MFMA GEMM with bf16 operands and fp32 accumulation for the backward pass's
-// history-side products:
+// MFMA GEMM with bf16 operands and fp32 accumulation for the backward pass:
 //   C[M,N] (fp32) = alpha * op(A) op(B)  (+ C when accumulating)
 // Products: the per-layer K/V of the history ([K | V] = X [W_K | W_V], one
 // product for both), the projection weight gradients ([dW_K | dW_V] =
-// X^T [dK | dV], K = history rows, split over K) and the history gradient
-// (dX += [dK | dV] [W_K | W_V]^T).
+// X^T [dK | dV], K = history rows, split over K), the history gradient
+// (dX += [dK | dV] [W_K | W_V]^T) and the target-side products of the
+// training window (weight gradients with K = targets).
 //
 // 128 x 128 output tile per workgroup of four waves (2 x 2), each wave 64 x 64
 // as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  64-deep k tiles go global ->
 // registers (16-byte loads, the next tile's loads in flight while the current
-// one is multiplied) -> LDS (rows with k contiguous, padded by 16 bytes; one
-// buffer, 37 KB, so four workgroups share a CU) -> MFMA operands (16-byte LDS
-// reads).  An operand whose source has k contiguous is copied row by row (the
-// form every product above is arranged in, with transposed copies of X, of the
-// weights and of dK|dV); one whose source has the row index contiguous is
-// transposed on its way into LDS.  Tiles are handed to the
-// eight XCDs in contiguous ranges, so the tiles that share a row block of A
-// (and, split over K, every tile of one K range) run on one XCD and share its
-// L2.  A split over K writes per-split partial tiles that a second kernel sums.
+// one is multiplied) -> LDS (rows with k contiguous; one buffer, 37 KB, so
+// four workgroups share a CU) -> MFMA operands (16-byte LDS reads).  An
+// operand whose source has k contiguous is copied row by row into rows padded
+// by 16 bytes; one whose source has the row index contiguous (X and dK | dV
+// in [dW_K | dW_V], both operands of the target-side weight gradients) is
+// transposed on its way into LDS: each thread turns an 8-row x 4-k block of
+// registers into 8-byte runs, written into unpadded rows whose 16-byte units
+// are permuted per row group so that neither the writes nor the operand reads
+// meet bank conflicts.  Tiles are handed to the eight XCDs in contiguous
+// ranges, so the tiles that share a row block of A (and, split over K, every
+// tile of one K range) run on one XCD and share its L2.  A split over K
+// writes per-split partial tiles that a second kernel sums.
 #include <algorithm>
 
 #include "common.h"
@@ -38,7 +41,9 @@ __device__ __forceinline__ f32x16 mfma_bf(const bf16x8& a, const bf16x8& b, cons
 }
 
 // One operand tile: 128 rows x 64 k = 1024 vectors of 8 bf16, four per thread.
-// kcontig: element (row, k) at src[row * ld + k]; else at src[k * ld + row].
+// kcontig: element (row, k) at src[row * ld + k]; else at src[k * ld + row],
+// and then thread t holds the rows 8 (t % 16) .. + 7 of the four k rows
+// 4 (t / 16) .. + 3, which it transposes on the way into LDS.
 // Vectors are whole or absent: the caller guarantees that the contiguous
 // extent (K, or the row count) is a multiple of 8 and chunk ends are multiples
 // of BK.
@@ -47,15 +52,15 @@ __device__ __forceinline__ void load_tile(u16x8 (&r)[4], const bf16_bits* __rest
                                           int nrows, int k0, int kend) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const int v = threadIdx.x + 256 * i;
     bool ok;
     int64_t off;
     if (kcontig) {
+      const int v = threadIdx.x + 256 * i;
       const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
       ok = row0 + row < nrows && k0 + kk < kend;
       off = (int64_t)(row0 + row) * ld + k0 + kk;
     } else {
-      const int kk = v / (BM / 8), row = (v % (BM / 8)) * 8;
+      const int row = (threadIdx.x % 16) * 8, kk = (threadIdx.x / 16) * 4 + i;
       ok = k0 + kk < kend && row0 + row < nrows;
       off = (int64_t)(k0 + kk) * ld + row0 + row;
     }
@@ -63,41 +68,42 @@ __device__ __forceinline__ void load_tile(u16x8 (&r)[4], const bf16_bits* __rest
   }
 }
 
-// The same tile of an operand stored as its transpose in 32-row blocks:
-// element (row, k) at src[((k / 32) ld + row) 32 + k % 32]; vectors of 8 k
-// stay inside a block.
-__device__ __forceinline__ void load_tile_blk(u16x8 (&r)[4], const bf16_bits* __restrict__ src, int64_t ld,
-                                              int row0, int nrows, int k0, int kend) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int v = threadIdx.x + 256 * i;
-    const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
-    const int k = k0 + kk;
-    const bool ok = row0 + row < nrows && k < kend;
-    r[i] = ok ? *reinterpret_cast<const u16x8*>(src + (((int64_t)(k >> 5) * ld + row0 + row) << 5) + (k & 31))
-              : u16x8{0, 0, 0, 0, 0, 0, 0, 0};
-  }
+// LDS offset (bf16 elements) of the 8-k unit u (k = 8u .. 8u + 7) of row m.
+// Rows with k contiguous in the source: padded rows of LROW.  Transposed
+// rows: unpadded rows of BK whose 16-byte units are permuted by (m / 8) % 8,
+// so that both the transposing writes (16 row groups of a wave, 8 bytes
+// each) and the MFMA operand reads (32 rows, 16 bytes each) spread over
+// all banks.
+template <bool kcontig>
+__device__ __forceinline__ int lds_unit(int m, int u) {
+  return kcontig ? m * LROW + 8 * u : m * BK + 8 * (u ^ ((m / 8) % 8));
 }
 
 template <bool kcontig>
 __device__ __forceinline__ void store_tile(bf16_bits* __restrict__ lds, const u16x8 (&r)[4]) {
+  if (kcontig) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int v = threadIdx.x + 256 * i;
-    if (kcontig) {
+    for (int i = 0; i < 4; ++i) {
+      const int v = threadIdx.x + 256 * i;
       const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
-      *reinterpret_cast<u16x8*>(lds + row * LROW + kk) = r[i];
-    } else {
-      const int kk = v / (BM / 8), row = (v % (BM / 8)) * 8;
+      *reinterpret_cast<u16x8*>(lds + lds_unit<true>(row, kk / 8)) = r[i];
+    }
+  } else {
+    // 8 rows x 4 k of registers -> per row, 4 consecutive k (8 bytes)
+    const int row = (threadIdx.x % 16) * 8, kq = threadIdx.x / 16;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) lds[(row + e) * LROW + kk] = r[i][e];
+    for (int e = 0; e < 8; ++e) {
+      uint2 w;
+      w.x = (uint32_t)r[0][e] | ((uint32_t)r[1][e] << 16);
+      w.y = (uint32_t)r[2][e] | ((uint32_t)r[3][e] << 16);
+      *reinterpret_cast<uint2*>(lds + lds_unit<false>(row + e, kq / 2) + (kq % 2) * 4) = w;
     }
   }
 }
 
 // op(A) element (m, k): A[m * lda + k] if A_KC else A[k * lda + m].
 // op(B) element (k, n): B[n * ldb + k] if B_KC else B[k * ldb + n].
-template <bool A_KC, bool B_KC, bool B_BLK = false>
+template <bool A_KC, bool B_KC>
 __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, const bf16_bits* __restrict__ A,
                                                         int64_t lda, const bf16_bits* __restrict__ B, int64_t ldb,
                                                         float* __restrict__ C, int64_t ldc, float alpha,
@@ -123,10 +129,7 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
   f32x16 acc[2][2] = {};
   u16x8 ra[4], rb[4];
   load_tile<A_KC>(ra, A, lda, m0, M, kb, ke);
-  if (B_BLK)
-    load_tile_blk(rb, B, ldb, n0, N, kb, ke);
-  else
-    load_tile<B_KC>(rb, B, ldb, n0, N, kb, ke);
+  load_tile<B_KC>(rb, B, ldb, n0, N, kb, ke);
   store_tile<A_KC>(As, ra);
   store_tile<B_KC>(Bs, rb);
   __syncthreads();
@@ -134,10 +137,7 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
     const bool more = k0 + BK < ke;
     if (more) {
       load_tile<A_KC>(ra, A, lda, m0, M, k0 + BK, ke);
-      if (B_BLK)
-        load_tile_blk(rb, B, ldb, n0, N, k0 + BK, ke);
-      else
-        load_tile<B_KC>(rb, B, ldb, n0, N, k0 + BK, ke);
+      load_tile<B_KC>(rb, B, ldb, n0, N, k0 + BK, ke);
     }
     const bf16_bits* as = As;
     const bf16_bits* bs = Bs;
@@ -146,8 +146,8 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
       bf16x8 a[2], b[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        a[i] = *reinterpret_cast<const bf16x8*>(as + (wm + 32 * i + r32) * LROW + ks * 16 + hi * 8);
-        b[i] = *reinterpret_cast<const bf16x8*>(bs + (wn + 32 * i + r32) * LROW + ks * 16 + hi * 8);
+        a[i] = *reinterpret_cast<const bf16x8*>(as + lds_unit<A_KC>(wm + 32 * i + r32, 2 * ks + hi));
+        b[i] = *reinterpret_cast<const bf16x8*>(bs + lds_unit<B_KC>(wn + 32 * i + r32, 2 * ks + hi));
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
@@ -272,12 +272,11 @@ hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
                      int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
                      int64_t part_floats, hipStream_t st) {
   if (M == 0 || N == 0) return hipSuccess;
-  const bool a_kc = !transA, b_kc = transB != 0, b_blk = transB == 2;
+  const bool a_kc = !transA, b_kc = transB != 0;
   // whole 16-byte vectors: the contiguous extent of each operand is a
   // multiple of 8 elements and every row starts 16-byte aligned
   if ((a_kc ? K : M) % 8 || (b_kc ? K : N) % 8 || lda % 8 || ldb % 8 || !al16(A) || !al16(B))
     return hipErrorInvalidValue;
-  if (b_blk && (K % 32 || !a_kc)) return hipErrorInvalidValue;
   const int tm = static_cast<int>(ceil_div(M, BM)), tn = static_cast<int>(ceil_div(N, BN));
   const int64_t tiles = (int64_t)tm * tn;
   int splits = 1;
@@ -294,10 +293,7 @@ hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
 #define STCA_MG(AK, BKC)                                                                                    \
   hipLaunchKernelGGL((mfma_gemm_kernel<AK, BKC>), dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, M, N, \
                      K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, tm, tn, static_cast<int>(work), p)
-  if (b_blk)
-    hipLaunchKernelGGL((mfma_gemm_kernel<true, true, true>), dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, M,
-                       N, K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, tm, tn, static_cast<int>(work), p);
-  else if (a_kc && b_kc) STCA_MG(true, true);
+  if (a_kc && b_kc) STCA_MG(true, true);
   else if (a_kc) STCA_MG(true, false);
   else if (b_kc) STCA_MG(false, true);
   else STCA_MG(false, false);

@@ -593,7 +593,7 @@ __global__ void relu_mask_kernel(float* __restrict__ dh, const float* __restrict
 // outside the buffers (the scheduler reports them).
 __global__ void zero_untargeted_kernel(const int32_t* __restrict__ hoff, const int32_t* __restrict__ toff,
                                        int n_requests, int64_t n_hist, bf16_bits* __restrict__ dKV, int64_t ldkv,
-                                       int cols, bf16_bits* __restrict__ dKVT, int64_t ldt, int blocked) {
+                                       int cols, bf16_bits* __restrict__ dKVT, int64_t ldt) {
   const int r = blockIdx.x;
   int64_t h0, h1;
   if (r < n_requests) {
@@ -606,11 +606,11 @@ __global__ void zero_untargeted_kernel(const int32_t* __restrict__ hoff, const i
     h0 = n_hist;
     h1 = ldt;
   }
-  if (h1 <= h0) return;
+  if (h1 <= h0 || !dKVT) return;
   const int64_t w = h1 - h0, cnt = w * cols;
   for (int64_t e = threadIdx.x; e < cnt; e += blockDim.x) {
     const int64_t c = e / w, row = h0 + e % w;
-    dKVT[blocked ? ((row >> 5) * cols + c) * 32 + (row & 31) : c * ldt + row] = 0;
+    dKVT[c * ldt + row] = 0;
   }
 }
 
@@ -753,10 +753,9 @@ hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st)
 }
 
 hipError_t zero_untargeted(const int32_t* hoff, const int32_t* toff, int n_requests, int64_t n_hist,
-                           bf16_bits* dKV, int64_t ldkv, int cols, bf16_bits* dKVT, int64_t ldt, int blocked,
-                           hipStream_t st) {
+                           bf16_bits* dKV, int64_t ldkv, int cols, bf16_bits* dKVT, int64_t ldt, hipStream_t st) {
   hipLaunchKernelGGL(zero_untargeted_kernel, dim3(static_cast<unsigned>(n_requests + 1)), dim3(256), 0, st, hoff,
-                     toff, n_requests, n_hist, dKV, ldkv, cols, dKVT, ldt, blocked);
+                     toff, n_requests, n_hist, dKV, ldkv, cols, dKVT, ldt);
   return hipGetLastError();
 }
 

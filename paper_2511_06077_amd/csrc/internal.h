@@ -29,8 +29,6 @@ hipError_t gemm_generic(int a_bf16, int b_bf16, int M, int N, int K, const void*
 // with few output tiles split K when `part` holds splits * M * N floats
 // (gemm_mfma_part_floats gives the most any split asks for).
 int64_t gemm_mfma_part_floats(int M, int N, int K);
-// transB = 2: B given as its transpose in 32-row blocks, element (k, n) at
-// B[((k / 32) ldb + n) 32 + k % 32] (K a multiple of 32).
 hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
                      int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
                      int64_t part_floats, hipStream_t st);
@@ -71,12 +69,9 @@ hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const flo
                          float scale, hipStream_t st);
 hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st);
 // Zero the history rows of requests without targets in dKV ([N_hist][ldkv]
-// bf16, columns [0, cols)) and the matching entries of its transpose dKVT,
-// and dKVT's padding rows [n_hist, ldt).  dKVT is [cols][ldt], or with
-// `blocked` in 32-row blocks: row r, column c at ((r / 32) cols + c) 32 +
-// r % 32, ldt rows in all.
+// bf16, columns [0, cols)) and, when dKVT is given ([cols][ldt]), the
+// matching entries of that transpose and its padding rows [n_hist, ldt).
 hipError_t zero_untargeted(const int32_t* hoff, const int32_t* toff, int n_requests, int64_t n_hist,
-                           bf16_bits* dKV, int64_t ldkv, int cols, bf16_bits* dKVT, int64_t ldt, int blocked,
-                           hipStream_t st);
+                           bf16_bits* dKV, int64_t ldkv, int cols, bf16_bits* dKVT, int64_t ldt, hipStream_t st);
 
 }  // namespace stca

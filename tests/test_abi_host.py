@@ -199,6 +199,9 @@ def test_fused_backward_selection(monkeypatch):
     monkeypatch.setenv("STCA_BWD", "generic")
     assert stca.stca_backward_launch_count(dims(), small) == 6 + 7 * n
     generic = stca.stca_workspace_size(dims(), long, True)
-    # the fp32 K|V of every layer, less the fused form's packed weights (W_K,
-    # W_V, W_O, W_Q, W_O^T; W_1, W_2, W_1^T, W_2^T) and bf16 copies of a, u, h, s
-    assert generic - fused >= 4 * n * 100000 * 2 * d - 2 * n * (5 * d * d + 4 * d * F) - 2 * n * 40 * (3 * d + F)
+    # the fp32 K|V of every layer and the bf16 transposed copies of X and of
+    # every layer's dK|dV, less the fused form's packed weights (W_K, W_V,
+    # W_O, W_Q, W_O^T; W_1, W_2, W_1^T, W_2^T) and bf16 copies of a, u, h, s
+    rows = 100000
+    assert generic - fused >= (4 * n * rows * 2 * d + 2 * rows * d + 2 * n * 2 * d * rows
+                               - 2 * n * (5 * d * d + 4 * d * F) - 2 * n * 40 * (3 * d + F))
