@@ -96,7 +96,7 @@ struct Layout {
   // fused backward: every layer's weights as bf16 operand tiles (and the
   // transposes of W_2, W_1, W_O), and the region of the recomputed
   // per-layer tensors (RecordLayout)
-  size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp, fw2t, fw1t, fwot, rec;
+  size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp, fw2t, fw1t, fwot, fwqt, rec;
   size_t b_hid, b_dhid, b_ds, b_u, b_du, b_a, b_dq, b_s;  // bf16 copies of backward operands (bf16 path)
   int64_t gpart_floats, nh8;
   size_t total;
@@ -203,6 +203,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->fw2t = m.take(2 * n * d * F);
       L->fw1t = m.take(2 * n * d * F);
       L->fwot = m.take(2 * n * d * d);
+      L->fwqt = m.take(2 * n * d * d);
     }
     // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
     // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
@@ -585,7 +586,8 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       pj.job[6] = {w->w2, at<char>(ws, L.fw2t), d, F, 0, 1};
       pj.job[7] = {w->w1, at<char>(ws, L.fw1t), F, d, 0, 1};
       pj.job[8] = {w->wo, at<char>(ws, L.fwot), d, d, 0, 1};
-      HIPCHK(fast_pack_many(pj, 9, n, st));
+      pj.job[9] = {w->wq, at<char>(ws, L.fwqt), d, d, 0, 1};
+      HIPCHK(fast_pack_many(pj, 10, n, st));
     }
   }
   // persistent grid of the fused kernels: one workgroup per CU
@@ -724,6 +726,13 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       ug.W2TP = at<char>(ws, L.fw2t);
       ug.W1TP = at<char>(ws, L.fw1t);
       ug.WoTP = at<char>(ws, L.fwot);
+      if (i + 1 < n) {
+        // ds = du + dq W_Q^T of layer i + 1, formed inside the update
+        ug.du_in = du;
+        ug.dq16 = at<bf16_bits>(ws, L.b_dq);
+        ug.WqTP = at<char>(ws, L.fwqt);
+        ug.q_layer = i + 1;
+      }
       HIPCHK(fast_update_grad(d, ug, st));
       HIPCHK(gemm_mfma(F, d, nti, FH16(i), F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, 0, gp, gpf,
                        st));
@@ -808,9 +817,13 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       if (!L.bfused) HIPCHK(convert(0, 1, s, at<bf16_bits>(ws, L.b_s), nt * d, st));
       HIPCHK(gemm_mfma(d, d, nti, s16, d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,
                        dw->dwq + (size_t)i * d * d, d, 1.f, 0, at<float>(ws, L.gpart), L.gpart_floats, st));
-      HIPCHK(hipMemcpyAsync(ds2, du, 4 * nt * d, hipMemcpyDeviceToDevice, st));
-      HIPCHK(gemm_mfma(nti, d, d, at<bf16_bits>(ws, L.b_dq), d, 0, static_cast<const bf16_bits*>(Wq), d, 1, ds2, d,
-                       1.f, 1, nullptr, 0, st));
+      // ds of the layer below = du + dq W_Q^T: the fused form's next update
+      // forms it; the last one (the target gradient) is a product here
+      if (!L.bfused || i == 0) {
+        HIPCHK(hipMemcpyAsync(ds2, du, 4 * nt * d, hipMemcpyDeviceToDevice, st));
+        HIPCHK(gemm_mfma(nti, d, d, at<bf16_bits>(ws, L.b_dq), d, 0, static_cast<const bf16_bits*>(Wq), d, 1, ds2,
+                         d, 1.f, 1, nullptr, 0, st));
+      }
     } else {
       HIPCHK(gemm(0, 0, d, d, nt, s, d, 1, dq, d, 0, dw->dwq + (size_t)i * d * d, d, 1.f, kEpiStore, nullptr, 0,
                   nullptr));

@@ -216,8 +216,11 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
 }
 
 // Reverse of the update: dH = (ds W_2^T) where h > 0, du = ds + dH W_1^T,
-// da = du W_O^T.  Same tiling as the recomputation, one bf16 term per
-// activation (these products only carry gradients).
+// da = du W_O^T, and first, when the next layer's query gradient is given,
+// ds = du' + dq W_Q^T (the gradient of this layer's output state through the
+// next layer's residual path and its queries).  Same tiling as the
+// recomputation, one bf16 term per activation (these products only carry
+// gradients).
 template <int D>
 __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A) {
   constexpr int NW = D / 32;
@@ -277,17 +280,37 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
   const bf16x8* W1TP = static_cast<const bf16x8*>(A.W1TP);
   const bf16x8* WoTP = static_cast<const bf16x8*>(A.WoTP);
 
-  // ds (bf16) into LDS, and its bf16 copy
-  for (int c = threadIdx.x; c < 32 * D / 4; c += 64 * NW) {
-    const int row = c / (D / 4), col = (c % (D / 4)) * 4;
-    float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (tb + row < A.n_tgt) x = *reinterpret_cast<const float4*>(A.ds + (tb + row) * D + col);
-    const uint2 v = make_uint2(pack2(x.x, x.y), pack2(x.z, x.w));
-    *reinterpret_cast<uint2*>(act + row * AROW + col) = v;
-    if (tb + row < A.n_tgt) *reinterpret_cast<uint2*>(A.ds16_out + (tb + row) * D + col) = v;
+  f32x16 du;
+  if (A.dq16) {
+    // ds = du' + dq W_Q^T: dq (bf16) into LDS, this wave's 32 columns of ds
+    for (int c = threadIdx.x; c < 32 * D / 8; c += 64 * NW) {
+      const int row = c / (D / 8), col = (c % (D / 8)) * 8;
+      uint4 x = make_uint4(0, 0, 0, 0);
+      if (tb + row < A.n_tgt) x = *reinterpret_cast<const uint4*>(A.dq16 + (tb + row) * D + col);
+      *reinterpret_cast<uint4*>(act + row * AROW + col) = x;
+    }
+    __syncthreads();
+    const bf16x8* WqTP = static_cast<const bf16x8*>(A.WqTP);
+    du = gemm(WqTP + ((int64_t)(A.q_layer * NW + w) * KS) * 64, act, f32x16{});
+    const f32x16 dprev = load32(A.du_in, D, 32 * w);
+#pragma unroll
+    for (int v = 0; v < 16; ++v) du[v] += dprev[v];
+    __syncthreads();  // every wave is done with dq
+    put_tile(act, 32 * w, du);
+    store16(A.ds16_out, D, 32 * w, du);
+  } else {
+    // ds (bf16) into LDS, and its bf16 copy
+    for (int c = threadIdx.x; c < 32 * D / 4; c += 64 * NW) {
+      const int row = c / (D / 4), col = (c % (D / 4)) * 4;
+      float4 x = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (tb + row < A.n_tgt) x = *reinterpret_cast<const float4*>(A.ds + (tb + row) * D + col);
+      const uint2 v = make_uint2(pack2(x.x, x.y), pack2(x.z, x.w));
+      *reinterpret_cast<uint2*>(act + row * AROW + col) = v;
+      if (tb + row < A.n_tgt) *reinterpret_cast<uint2*>(A.ds16_out + (tb + row) * D + col) = v;
+    }
+    du = load32(A.ds, D, 32 * w);
   }
   __syncthreads();
-  f32x16 du = load32(A.ds, D, 32 * w);
   for (int c = 0; c < F / D; ++c) {
     const int col = c * D + 32 * w;
     f32x16 dh = gemm(W2TP + ((int64_t)A.layer * (F / 32) + c * NW + w) * KS * 64, act, f32x16{});

@@ -118,6 +118,9 @@ hipError_t fast_update_precise(int D, const UpdatePrecise& f, hipStream_t st);
 // bf16 operands with fp32 sums; writes dH and bf16 copies of ds and du for
 // the weight-gradient products.  Weights: the transposes of W_2, W_1, W_O
 // packed as bf16 operand tiles (PackJob.trans).
+// With dq16 set, the gradient of s' is formed first, ds = du_in + dq16 W_Q^T
+// (W_Q of layer q_layer, packed transposed in WqTP; du_in may be du_out:
+// each element is read before the same thread writes it), and ds is unused.
 struct UpdateGrad {
   int layer, F;
   int64_t n_tgt;
@@ -126,6 +129,10 @@ struct UpdateGrad {
   float *du_out, *da_out;
   bf16_bits *ds16_out, *dh16_out, *du16_out;
   const void *W2TP, *W1TP, *WoTP;
+  const float* du_in;      // [n_tgt][D]
+  const bf16_bits* dq16;   // [n_tgt][D]
+  const void* WqTP;
+  int q_layer;
 };
 hipError_t fast_update_grad(int D, const UpdateGrad& f, hipStream_t st);
 
