@@ -562,13 +562,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   // of X^T, [W_K | W_V]^T and (dK | dV)^T); fp32 inputs keep fp32 products.
   if (bf) {
     const bf16_bits* X = static_cast<const bf16_bits*>(hist);
+    if (!rec_out)
+      HIPCHK(pack_wkv(static_cast<const bf16_bits*>(w->wk), static_cast<const bf16_bits*>(w->wv), n, d, wkv_all,
+                      st));
     for (int i = 0; i < n && !rec_out; ++i) {
       const bf16_bits* Wk = reinterpret_cast<const bf16_bits*>(W(w->wk, i, (size_t)d * d));
       const bf16_bits* Wv = reinterpret_cast<const bf16_bits*>(W(w->wv, i, (size_t)d * d));
-      HIPCHK(hipMemcpy2DAsync(wkv_all + (size_t)i * 2 * d, (size_t)n * 2 * d * 2, Wk, d * 2, d * 2, d,
-                              hipMemcpyDeviceToDevice, st));
-      HIPCHK(hipMemcpy2DAsync(wkv_all + (size_t)i * 2 * d + d, (size_t)n * 2 * d * 2, Wv, d * 2, d * 2, d,
-                              hipMemcpyDeviceToDevice, st));
       if (!L.bfused) {
         HIPCHK(transpose_bf16(Wk, d, d, d, WKVT(i), d, d, st));
         HIPCHK(transpose_bf16(Wv, d, d, d, WKVT(i) + (size_t)d * d, d, d, st));
@@ -863,12 +862,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     else
       HIPCHK(gemm_mfma(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
                        L.gpart_floats, st));
-    for (int i = 0; i < n; ++i) {
-      HIPCHK(hipMemcpy2DAsync(dw->dwk + (size_t)i * d * d, d * 4, dwkv + (size_t)i * 2 * d, (size_t)n * 2 * d * 4,
-                              d * 4, d, hipMemcpyDeviceToDevice, st));
-      HIPCHK(hipMemcpy2DAsync(dw->dwv + (size_t)i * d * d, d * 4, dwkv + (size_t)i * 2 * d + d,
-                              (size_t)n * 2 * d * 4, d * 4, d, hipMemcpyDeviceToDevice, st));
-    }
+    HIPCHK(split_dwkv(dwkv, n, d, dw->dwk, dw->dwv, st));
     HIPCHK(rec.mark("dw_kv"));
     HIPCHK(gemm_mfma(static_cast<int>(nh), d, n * 2 * d, static_cast<const bf16_bits*>(dkv), n * 2 * d, 0, wkv_all,
                      n * 2 * d, 1, dhist, d, 1.f, 0, nullptr, 0, st));

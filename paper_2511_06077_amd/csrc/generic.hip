@@ -614,6 +614,32 @@ __global__ void zero_untargeted_kernel(const int32_t* __restrict__ hoff, const i
   }
 }
 
+// [W_K^0 | W_V^0 | W_K^1 | ...] ([d][n 2d] bf16) from the stacked W_K, W_V
+// ([n][d][d]); one thread per 8 columns
+__global__ void pack_wkv_kernel(const bf16_bits* __restrict__ wk, const bf16_bits* __restrict__ wv, int n, int d,
+                                bf16_bits* __restrict__ wkv) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int per_row = n * 2 * d / 8;
+  if (g >= (int64_t)d * per_row) return;
+  const int r = static_cast<int>(g / per_row), c = static_cast<int>(g % per_row) * 8;
+  const int i = c / (2 * d), cc = c % (2 * d);
+  const bf16_bits* src = (cc < d ? wk : wv) + ((int64_t)i * d + r) * d + cc % d;
+  *reinterpret_cast<uint4*>(wkv + (int64_t)r * n * 2 * d + c) = *reinterpret_cast<const uint4*>(src);
+}
+
+// dW_K^i, dW_V^i ([n][d][d] fp32) from [dW_K^0 | dW_V^0 | ...] ([d][n 2d]);
+// one thread per 4 columns
+__global__ void split_dwkv_kernel(const float* __restrict__ dwkv, int n, int d, float* __restrict__ dwk,
+                                  float* __restrict__ dwv) {
+  const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int per_row = n * 2 * d / 4;
+  if (g >= (int64_t)d * per_row) return;
+  const int r = static_cast<int>(g / per_row), c = static_cast<int>(g % per_row) * 4;
+  const int i = c / (2 * d), cc = c % (2 * d);
+  float* dst = (cc < d ? dwk : dwv) + ((int64_t)i * d + r) * d + cc % d;
+  *reinterpret_cast<float4*>(dst) = *reinterpret_cast<const float4*>(dwkv + (int64_t)r * n * 2 * d + c);
+}
+
 template <typename S, typename D>
 __global__ void convert_kernel(const S* __restrict__ src, D* __restrict__ dst, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -773,6 +799,22 @@ hipError_t convert(int src_bf16, int dst_bf16, const void* src, void* dst, int64
                        (bf16_bits*)dst, n);
   else
     hipLaunchKernelGGL((convert_kernel<float, float>), g, dim3(256), 0, st, (const float*)src, (float*)dst, n);
+  return hipGetLastError();
+}
+
+hipError_t pack_wkv(const bf16_bits* wk, const bf16_bits* wv, int n, int d, bf16_bits* wkv, hipStream_t st) {
+  if (d % 8) return hipErrorInvalidValue;
+  const int64_t threads = (int64_t)d * n * 2 * d / 8;
+  if (threads == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_wkv_kernel, grid1(threads, 256), dim3(256), 0, st, wk, wv, n, d, wkv);
+  return hipGetLastError();
+}
+
+hipError_t split_dwkv(const float* dwkv, int n, int d, float* dwk, float* dwv, hipStream_t st) {
+  if (d % 4) return hipErrorInvalidValue;
+  const int64_t threads = (int64_t)d * n * 2 * d / 4;
+  if (threads == 0) return hipSuccess;
+  hipLaunchKernelGGL(split_dwkv_kernel, grid1(threads, 256), dim3(256), 0, st, dwkv, n, d, dwk, dwv);
   return hipGetLastError();
 }
 

@@ -44,6 +44,11 @@ hipError_t merge_generic(int d_head, int n_heads, int64_t n_tgt, const int32_t* 
                          hipStream_t st);
 hipError_t convert(int src_bf16, int dst_bf16, const void* src, void* dst, int64_t n, hipStream_t st);
 hipError_t fill_f32(float* dst, float v, int64_t n, hipStream_t st);
+// [W_K^0 | W_V^0 | W_K^1 | ...] ([d][n 2d] bf16) from the stacked W_K, W_V
+// ([n][d][d] bf16, 16-byte aligned; d a multiple of 8).
+hipError_t pack_wkv(const bf16_bits* wk, const bf16_bits* wv, int n, int d, bf16_bits* wkv, hipStream_t st);
+// dW_K^i and dW_V^i ([n][d][d] fp32) from [dW_K^0 | dW_V^0 | ...] ([d][n 2d]).
+hipError_t split_dwkv(const float* dwkv, int n, int d, float* dwk, float* dwv, hipStream_t st);
 // generic backward pieces
 // dKV ([N_hist] rows of 2d, row pitch ldkv elements; fp32 or bf16 when
 // dkv_bf16) is written for every history row of a request with targets, and
