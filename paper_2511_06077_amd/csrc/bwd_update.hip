@@ -100,15 +100,17 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
     }
     return v;
   };
-  // acc += W^T act^T over KS k-steps, packed weight tile Wp ([KS][64] vectors)
+  // acc += W^T act^T over KS k-steps, packed weight tile Wp ([KS][64] vectors;
+  // every fragment requested before the first product, one L2 round trip)
   auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits (*src)[32 * AROW], f32x16 acc) {
-#pragma unroll 4
-    for (int k = 0; k < KS; ++k) {
-      const bf16x8 wt = Wp[k * 64 + lane];
+    bf16x8 wt[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) wt[k] = Wp[k * 64 + lane];
+#pragma unroll
+    for (int k = 0; k < KS; ++k)
 #pragma unroll
       for (int term = 0; term < 3; ++term)
-        acc = mma(wt, *reinterpret_cast<const bf16x8*>(src[term] + tcol * AROW + 8 * hi + 16 * k), acc);
-    }
+        acc = mma(wt[k], *reinterpret_cast<const bf16x8*>(src[term] + tcol * AROW + 8 * hi + 16 * k), acc);
     return acc;
   };
   const bf16x8* WoP = static_cast<const bf16x8*>(A.WoP);
@@ -237,9 +239,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
   const int KSF = F / 16;
 
   auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits* src, f32x16 acc) {
-#pragma unroll 4
+    bf16x8 wt[KS];
+#pragma unroll
+    for (int k = 0; k < KS; ++k) wt[k] = Wp[k * 64 + lane];
+#pragma unroll
     for (int k = 0; k < KS; ++k)
-      acc = mma(Wp[k * 64 + lane], *reinterpret_cast<const bf16x8*>(src + tcol * AROW + 8 * hi + 16 * k), acc);
+      acc = mma(wt[k], *reinterpret_cast<const bf16x8*>(src + tcol * AROW + 8 * hi + 16 * k), acc);
     return acc;
   };
   // a wave's tile (lane = target, elements = columns col0 + 8 q + 4 hi + e)
