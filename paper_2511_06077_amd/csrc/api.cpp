@@ -312,6 +312,7 @@ stca_status_t forward_reordered(const Layout& L, const stca_batch_t* b, const vo
     HIPCHK(rec.mark("pack"));
   }
   FastUpdate f{};
+  f.tg = ceil_div(static_cast<int64_t>(L.nt), 32) < device_cus() ? 16 : 32;
   f.n_layers = n;
   f.F = F;
   f.n_tgt = L.nt;
@@ -392,6 +393,7 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   }
   const size_t kv_layer = (size_t)L.nblocks * kBlockTokens * 2 * d * 2;
   FastUpdate f{};
+  f.tg = ceil_div(static_cast<int64_t>(L.nt), 32) < device_cus() ? 16 : 32;
   f.n_layers = n;
   f.F = F;
   f.n_tgt = L.nt;

@@ -19,6 +19,7 @@ struct FastUpdate {
   void* out;
   void* QN;
   const void *WoP, *W1P, *W2P, *WqP;
+  int tg;  // targets per workgroup: 32, or 16 to spread few targets over more CUs
 };
 
 // Repack W [n_layers][K][N] (bf16) into MFMA operand order, as bf16 or fp16.

@@ -701,7 +701,10 @@ __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __rest
 }
 
 // ------------------------------------------------ K4: target update
-// One workgroup per 32 targets, one wave per 32 output dimensions.
+// One workgroup per tg = 32 targets (or 16, when 32-target groups would leave
+// CUs idle: the MFMA tiles then carry 16 empty target columns, and each CU
+// still streams every weight of the layer once), one wave per 32 output
+// dimensions.
 // mode 0 (init): s^(0) = x_t, Q^(0) = x_t W_Q^0.
 // mode 1 (layer i): merge the attention partials into a, then
 //   u = s + a W_O;  s' = u + ReLU(u W_1) W_2;  Q' = s' W_Q^{i+1} (if i+1 < n).
@@ -721,6 +724,7 @@ struct UpdateArgs {
   bf16_bits* out;              // final layer output, nullable
   f16x8* QN;                   // next queries
   const f16x8 *WoP, *W1P, *W2P, *WqP;  // packed (fp16), all layers
+  int tg;                      // targets per workgroup (16 or 32)
 };
 
 template <int D, int NC>
@@ -734,9 +738,11 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   uint16_t* hid = lds + 32 * AROW;      // [32][AROW]: D hidden columns at a time
   const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int tcol = lane % 32, hi = lane / 32;
-  const int64_t tb = (int64_t)blockIdx.x * 32;
+  const int tg = A.tg;  // rows tg..31 of the 32-row tiles stay zero
+  const int64_t tb = (int64_t)blockIdx.x * tg;
   const int64_t t = tb + tcol;
-  const bool tok = t < A.n_tgt;
+  const bool tok = tcol < tg && t < A.n_tgt;
+  auto live = [&](int row) { return row < tg && tb + row < A.n_tgt; };
 
   // fp32 result of D^T tile: lane holds dims 32w + 4hi + 8g + k for g, k < 4
   auto store_f32 = [&](float* dst, const f32x16& v) {
@@ -794,12 +800,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
     for (int c = threadIdx.x; c < 32 * D / 8; c += 64 * NW) {
       const int row = c / (D / 8), col8 = c % (D / 8);
       uint4 v = make_uint4(0, 0, 0, 0);
-      if (tb + row < A.n_tgt) v = *reinterpret_cast<const uint4*>(A.tgt + (tb + row) * D + col8 * 8);
+      if (live(row)) v = *reinterpret_cast<const uint4*>(A.tgt + (tb + row) * D + col8 * 8);
       const bf16_bits* e = reinterpret_cast<const bf16_bits*>(&v);
       uint16_t* a8 = act + row * AROW + col8 * 8;
 #pragma unroll
       for (int i = 0; i < 8; ++i) a8[i] = f16_bits(to_f32(e[i]));
-      if (tb + row < A.n_tgt) {
+      if (live(row)) {
         float* so = A.s_out + (tb + row) * D + col8 * 8;
 #pragma unroll
         for (int i = 0; i < 8; ++i) so[i] = to_f32(e[i]);
@@ -818,7 +824,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       float av[16];
 #pragma unroll
       for (int i = 0; i < 16; ++i) av[i] = 0.f;
-      if (tt < A.n_tgt) {
+      if (live(row)) {
         const int nch = A.tchunks[tt];
         float2 ml[kMaxChunks];
 #pragma unroll
@@ -1050,8 +1056,9 @@ hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st) {
   A.W1P = (const f16x8*)f.W1P;
   A.W2P = (const f16x8*)f.W2P;
   A.WqP = (const f16x8*)f.WqP;
+  A.tg = f.tg == 16 ? 16 : 32;
   if (f.n_tgt == 0) return hipSuccess;
-  dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
+  dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, A.tg)));
   const size_t lds = (size_t)32 * (D + 8) * 2 * (f.mode == 0 ? 1 : 2);
 #define STCA_UPD(DD)                                                                         \
   if (f.F == 4 * (DD))                                                                      \
