@@ -146,20 +146,41 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
 #pragma unroll
         for (int i = 0; i < 16; ++i) av[i] = 0.f;
         if (tt < A.n_tgt) {
+          // every chunk's (max, sum) requested at once, the accumulators four
+          // chunks at a time (sums in chunk order)
           const int nch = A.tchunks[tt];
-          float M = -INFINITY;
-          for (int c = 0; c < nch; ++c) M = fmaxf(M, A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j].x);
-          float L = 0.f;
-          for (int c = 0; c < nch; ++c) {
-            const float2 ml = A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j];
-            const float wc = exp2f(ml.x - M);
-            L += wc * ml.y;
-            const float4* pa =
-                reinterpret_cast<const float4*>(A.part_acc + ((int64_t)c * A.n_tgt + tt) * D + j * DH + half * 16);
+          float2 ml[kMaxChunks];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-              const float4 x = pa[q];
-              av[4 * q] += wc * x.x, av[4 * q + 1] += wc * x.y, av[4 * q + 2] += wc * x.z, av[4 * q + 3] += wc * x.w;
+          for (int c = 0; c < kMaxChunks; ++c)
+            ml[c] = c < nch ? A.part_ml[((int64_t)c * A.n_tgt + tt) * H + j] : make_float2(-INFINITY, 0.f);
+          float M = ml[0].x;
+#pragma unroll
+          for (int c = 1; c < kMaxChunks; ++c) M = fmaxf(M, ml[c].x);
+          float L = 0.f, wc[kMaxChunks];
+#pragma unroll
+          for (int c = 0; c < kMaxChunks; ++c) {
+            wc[c] = c < nch ? exp2f(ml[c].x - M) : 0.f;
+            L += wc[c] * ml[c].y;
+          }
+#pragma unroll
+          for (int c0 = 0; c0 < kMaxChunks; c0 += 4) {
+            if (c0 >= nch) break;
+            float4 x[4][4];
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) {
+              const float4* pa = reinterpret_cast<const float4*>(
+                  A.part_acc + ((int64_t)(c0 + cc) * A.n_tgt + tt) * D + j * DH + half * 16);
+#pragma unroll
+              for (int q = 0; q < 4; ++q) x[cc][q] = c0 + cc < nch ? pa[q] : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int cc = 0; cc < 4; ++cc) {
+              const float w = wc[c0 + cc];
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                av[4 * q] += w * x[cc][q].x, av[4 * q + 1] += w * x[cc][q].y;
+                av[4 * q + 2] += w * x[cc][q].z, av[4 * q + 3] += w * x[cc][q].w;
+              }
             }
           }
           const float inv = 1.f / L;
