@@ -31,7 +31,7 @@ __device__ __forceinline__ uint32_t pack2(float x, float y) {
   return (uint32_t)from_f32<bf16_bits>(x) | ((uint32_t)from_f32<bf16_bits>(y) << 16);
 }
 
-template <int D>
+template <int D, int NC>
 __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePrecise A) {
   constexpr int NW = D / 32;
   constexpr int H = D / DH;
@@ -100,12 +100,17 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
     }
     return v;
   };
-  // acc += W^T act^T over KS k-steps, packed weight tile Wp ([KS][64] vectors;
-  // every fragment requested before the first product, one L2 round trip)
-  auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits (*src)[32 * AROW], f32x16 acc) {
-    bf16x8 wt[KS];
+  // acc += W^T act^T over KS k-steps with the packed weight tile's fragments
+  // in registers (fetched from Wp, [KS][64] vectors, in one L2 round trip).
+  // With NC (hidden chunks, F / D) known at compile time, each product's
+  // fragments are fetched one product ahead into the other of two register
+  // sets, so the weight stream overlaps the previous product; the chunk loop
+  // is then fully unrolled.  NC = 0 (any other F) fetches right before.
+  auto fetch = [&](bf16x8 (&r)[KS], const bf16x8* __restrict__ Wp) {
 #pragma unroll
-    for (int k = 0; k < KS; ++k) wt[k] = Wp[k * 64 + lane];
+    for (int k = 0; k < KS; ++k) r[k] = Wp[k * 64 + lane];
+  };
+  auto gemm_r = [&](const bf16x8 (&wt)[KS], const bf16_bits (*src)[32 * AROW], f32x16 acc) {
 #pragma unroll
     for (int k = 0; k < KS; ++k)
 #pragma unroll
@@ -113,13 +118,19 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
         acc = mma(wt[k], *reinterpret_cast<const bf16x8*>(src[term] + tcol * AROW + 8 * hi + 16 * k), acc);
     return acc;
   };
+  auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits (*src)[32 * AROW], f32x16 acc) {
+    bf16x8 wt[KS];
+    fetch(wt, Wp);
+    return gemm_r(wt, src, acc);
+  };
+  constexpr bool PF = NC > 0;
   const bf16x8* WoP = static_cast<const bf16x8*>(A.WoP);
   const bf16x8* W1P = static_cast<const bf16x8*>(A.W1P);
   const bf16x8* W2P = static_cast<const bf16x8*>(A.W2P);
   const bf16x8* WqP = static_cast<const bf16x8*>(A.WqP);
   const float qscale = kLog2e * rsqrtf(static_cast<float>(DH));
 
-  f32x16 s_next;
+  f32x16 s_next, q;
   if (A.mode == 0) {
     // s^(0) = x_t
     for (int c = threadIdx.x; c < 32 * D / 4; c += 64 * NW) {
@@ -135,7 +146,16 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
       put4(act, row, col, x[0], x[1], x[2], x[3]);
     }
     __syncthreads();
+    q = gemm(WqP + ((int64_t)w * KS) * 64, act, f32x16{});
   } else {
+    const int ql = A.layer + 1;
+    const bool next_q = ql < A.n_layers;
+    auto w1_tile = [&](int c) { return W1P + ((int64_t)A.layer * (F / 32) + c * NW + w) * KS * 64; };
+    auto w2_tile = [&](int c) { return W2P + ((int64_t)(A.layer * NW + w) * (F / 16) + c * KS) * 64; };
+    const bf16x8* wo_tile = WoP + ((int64_t)(A.layer * NW + w) * KS) * 64;
+    const bf16x8* wq_tile = WqP + ((int64_t)(ql * NW + w) * KS) * 64;
+    bf16x8 wa[KS], wb[KS];
+    if (PF) fetch(wa, wo_tile);  // lands during the merge
     // merge the chunk partials: two threads per (target, head), 16 dims each
     {
       const int pair = threadIdx.x >> 1, half = threadIdx.x & 1;
@@ -203,36 +223,47 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
       }
     }
     __syncthreads();
+    if (PF) fetch(wb, w1_tile(0));
     // u = s + a W_O
-    f32x16 u = gemm(WoP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, load_tile(A.s_in, D, 32 * w));
+    f32x16 u = PF ? gemm_r(wa, act, load_tile(A.s_in, D, 32 * w)) : gemm(wo_tile, act, load_tile(A.s_in, D, 32 * w));
     store_tile(A.u_out, D, 32 * w, u);
     store_tile16(A.u16_out, D, 32 * w, u);
+    __builtin_amdgcn_sched_barrier(0);
+    if (PF) fetch(wa, w2_tile(0));
     __syncthreads();  // every wave is done reading a
     put_tile(act, 32 * w, u);
     __syncthreads();
     // s' = u + ReLU(u W_1) W_2, D hidden columns at a time
     s_next = u;
-    const int KSF = F / 16;
-    for (int c = 0; c < F / D; ++c) {
-      f32x16 h = gemm(W1P + ((int64_t)A.layer * (F / 32) + c * NW + w) * KS * 64, act, f32x16{});
+#pragma unroll
+    for (int c = 0; c < (PF ? NC : F / D); ++c) {
+      f32x16 h = PF ? gemm_r(wb, act, f32x16{}) : gemm(w1_tile(c), act, f32x16{});
 #pragma unroll
       for (int v = 0; v < 16; ++v) h[v] = fmaxf(h[v], 0.f);
       store_tile(A.h_out, F, c * D + 32 * w, h);
       store_tile16(A.h16_out, F, c * D + 32 * w, h);
+      __builtin_amdgcn_sched_barrier(0);
+      if (PF) {
+        if (c + 1 < NC)
+          fetch(wb, w1_tile(c + 1));
+        else if (next_q)
+          fetch(wb, wq_tile);
+      }
       put_tile(hid, 32 * w, h);
       __syncthreads();
-      s_next = gemm(W2P + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64, hid, s_next);
+      s_next = PF ? gemm_r(wa, hid, s_next) : gemm(w2_tile(c), hid, s_next);
+      __builtin_amdgcn_sched_barrier(0);
+      if (PF && c + 1 < NC) fetch(wa, w2_tile(c + 1));
       __syncthreads();  // hid is rewritten by the next chunk
     }
     store_tile(A.s_out, D, 32 * w, s_next);
     store_tile16(A.s16_out, D, 32 * w, s_next);
-    if (A.layer + 1 >= A.n_layers) return;
+    if (!next_q) return;
     put_tile(act, 32 * w, s_next);  // act (u) was last read before the previous barrier
     __syncthreads();
+    q = PF ? gemm_r(wb, act, f32x16{}) : gemm(wq_tile, act, f32x16{});
   }
   // next queries q' = s' W_Q^{next}, scaled into log2 units
-  const int ql = A.mode == 0 ? 0 : A.layer + 1;
-  f32x16 q = gemm(WqP + ((int64_t)(ql * NW + w) * KS) * 64, act, f32x16{});
 #pragma unroll
   for (int v = 0; v < 16; ++v) q[v] *= qscale;
   store_tile(A.q_out, D, 32 * w, q);
@@ -244,7 +275,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_precise_kernel(UpdatePre
 // next layer's residual path and its queries).  Same tiling as the
 // recomputation, one bf16 term per activation (these products only carry
 // gradients).
-template <int D>
+template <int D, int NC>
 __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A) {
   constexpr int NW = D / 32;
   constexpr int KS = D / 16;
@@ -259,15 +290,25 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
   const int F = A.F;
   const int KSF = F / 16;
 
-  auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits* src, f32x16 acc) {
-    bf16x8 wt[KS];
+  // weight fragments in registers, fetched one product ahead into the other
+  // of two register sets when NC (F / D) is known at compile time, as in
+  // the recomputation
+  auto fetch = [&](bf16x8 (&r)[KS], const bf16x8* __restrict__ Wp) {
 #pragma unroll
-    for (int k = 0; k < KS; ++k) wt[k] = Wp[k * 64 + lane];
+    for (int k = 0; k < KS; ++k) r[k] = Wp[k * 64 + lane];
+  };
+  auto gemm_r = [&](const bf16x8 (&wt)[KS], const bf16_bits* src, f32x16 acc) {
 #pragma unroll
     for (int k = 0; k < KS; ++k)
       acc = mma(wt[k], *reinterpret_cast<const bf16x8*>(src + tcol * AROW + 8 * hi + 16 * k), acc);
     return acc;
   };
+  auto gemm = [&](const bf16x8* __restrict__ Wp, const bf16_bits* src, f32x16 acc) {
+    bf16x8 wt[KS];
+    fetch(wt, Wp);
+    return gemm_r(wt, src, acc);
+  };
+  constexpr bool PF = NC > 0;
   // a wave's tile (lane = target, elements = columns col0 + 8 q + 4 hi + e)
   auto put_tile = [&](bf16_bits* buf, int col0, const f32x16& v) {
 #pragma unroll
@@ -305,6 +346,11 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
   const bf16x8* W2TP = static_cast<const bf16x8*>(A.W2TP);
   const bf16x8* W1TP = static_cast<const bf16x8*>(A.W1TP);
   const bf16x8* WoTP = static_cast<const bf16x8*>(A.WoTP);
+  auto w2t_tile = [&](int c) { return W2TP + ((int64_t)A.layer * (F / 32) + c * NW + w) * KS * 64; };
+  auto w1t_tile = [&](int c) { return W1TP + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64; };
+  const bf16x8* wot_tile = WoTP + ((int64_t)(A.layer * NW + w) * KS) * 64;
+  bf16x8 wa[KS], wb[KS];  // wb: W_2^T of chunk c (then W_O^T), wa: W_Q^T, then W_1^T of chunk c
+  if (PF) fetch(wb, w2t_tile(0));
 
   f32x16 du;
   if (A.dq16) {
@@ -317,7 +363,13 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
     }
     __syncthreads();
     const bf16x8* WqTP = static_cast<const bf16x8*>(A.WqTP);
-    du = gemm(WqTP + ((int64_t)(A.q_layer * NW + w) * KS) * 64, act, f32x16{});
+    const bf16x8* wqt_tile = WqTP + ((int64_t)(A.q_layer * NW + w) * KS) * 64;
+    if (PF) {
+      fetch(wa, wqt_tile);
+      du = gemm_r(wa, act, f32x16{});
+    } else {
+      du = gemm(wqt_tile, act, f32x16{});
+    }
     const f32x16 dprev = load32(A.du_in, D, 32 * w);
 #pragma unroll
     for (int v = 0; v < 16; ++v) du[v] += dprev[v];
@@ -336,24 +388,31 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
     }
     du = load32(A.ds, D, 32 * w);
   }
+  __builtin_amdgcn_sched_barrier(0);
+  if (PF) fetch(wa, w1t_tile(0));
   __syncthreads();
-  for (int c = 0; c < F / D; ++c) {
+#pragma unroll
+  for (int c = 0; c < (PF ? NC : F / D); ++c) {
     const int col = c * D + 32 * w;
-    f32x16 dh = gemm(W2TP + ((int64_t)A.layer * (F / 32) + c * NW + w) * KS * 64, act, f32x16{});
+    f32x16 dh = PF ? gemm_r(wb, act, f32x16{}) : gemm(w2t_tile(c), act, f32x16{});
     const f32x16 h = load32(A.h, F, col);
 #pragma unroll
     for (int v = 0; v < 16; ++v) dh[v] = h[v] > 0.f ? dh[v] : 0.f;
     store16(A.dh16_out, F, col, dh);
+    __builtin_amdgcn_sched_barrier(0);
+    if (PF) fetch(wb, c + 1 < NC ? w2t_tile(c + 1) : wot_tile);
     put_tile(hid, 32 * w, dh);
     __syncthreads();
-    du = gemm(W1TP + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64, hid, du);
+    du = PF ? gemm_r(wa, hid, du) : gemm(w1t_tile(c), hid, du);
+    __builtin_amdgcn_sched_barrier(0);
+    if (PF && c + 1 < NC) fetch(wa, w1t_tile(c + 1));
     __syncthreads();  // hid is rewritten by the next chunk
   }
   store32(A.du_out, D, 32 * w, du);
   store16(A.du16_out, D, 32 * w, du);
   put_tile(act, 32 * w, du);  // act (ds) was last read before the previous barrier
   __syncthreads();
-  const f32x16 da = gemm(WoTP + ((int64_t)(A.layer * NW + w) * KS) * 64, act, f32x16{});
+  const f32x16 da = PF ? gemm_r(wb, act, f32x16{}) : gemm(wot_tile, act, f32x16{});
   store32(A.da_out, D, 32 * w, da);
 }
 
@@ -363,7 +422,11 @@ hipError_t fast_update_precise(int D, const UpdatePrecise& f, hipStream_t st) {
   if (f.n_tgt == 0) return hipSuccess;
   if (f.F % D != 0) return hipErrorInvalidValue;
   dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
-#define STCA_UPDP(DD) hipLaunchKernelGGL(update_precise_kernel<DD>, g, dim3(64 * (DD / 32)), 0, st, f)
+#define STCA_UPDP(DD)                                                                              \
+  if (f.F == 4 * (DD))                                                                             \
+    hipLaunchKernelGGL((update_precise_kernel<DD, 4>), g, dim3(64 * (DD / 32)), 0, st, f);         \
+  else                                                                                             \
+    hipLaunchKernelGGL((update_precise_kernel<DD, 0>), g, dim3(64 * (DD / 32)), 0, st, f)
   switch (D) {
     case 64: STCA_UPDP(64); break;
     case 128: STCA_UPDP(128); break;
@@ -378,7 +441,11 @@ hipError_t fast_update_grad(int D, const UpdateGrad& f, hipStream_t st) {
   if (f.n_tgt == 0) return hipSuccess;
   if (f.F % D != 0) return hipErrorInvalidValue;
   dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, 32)));
-#define STCA_UPDG(DD) hipLaunchKernelGGL(update_grad_kernel<DD>, g, dim3(64 * (DD / 32)), 0, st, f)
+#define STCA_UPDG(DD)                                                                              \
+  if (f.F == 4 * (DD))                                                                             \
+    hipLaunchKernelGGL((update_grad_kernel<DD, 4>), g, dim3(64 * (DD / 32)), 0, st, f);            \
+  else                                                                                             \
+    hipLaunchKernelGGL((update_grad_kernel<DD, 0>), g, dim3(64 * (DD / 32)), 0, st, f)
   switch (D) {
     case 64: STCA_UPDG(64); break;
     case 128: STCA_UPDG(128); break;
