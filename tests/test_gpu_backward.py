@@ -84,6 +84,29 @@ def test_fused_projection_gradients(torch, chunk_override, d, h):
     check(b, gpu_grads(torch, b), TOL["bf16"])
 
 
+@pytest.mark.parametrize("d,h,mult", [(128, 4, 2), (64, 2, 3)])
+def test_fused_other_ffn_width(torch, chunk_override, d, h, mult):
+    """An FFN width other than 4 d (still a multiple of d, so the fused
+    backward takes the batch): the update kernels' path without the
+    compile-time chunk count.  The fast forward's output, stca_forward_train's
+    output and every gradient against the oracle."""
+    from paper_2511_06077_amd.device import DeviceBatch, to_device
+    chunk_override(2)
+    b = W.make_custom_batch("gffn", [1, 33, 130, 64, 7, 300], [2, 31, 0, 17, 1, 32], d_model=d, n_heads=h,
+                            n_layers=2, dtype="bf16", seed=43, with_grad=True, ffn_mult=mult)
+    db = DeviceBatch(b, backward=True)
+    y_fast = db.forward().float().cpu().numpy().astype(np.float64)
+    y_train = db.forward_train().float().cpu().numpy().astype(np.float64)
+    g = db.backward(to_device(b.grad_out, "cuda"), use_record=True)
+    torch.cuda.synchronize()
+    ref_y = O.forward(b.f64(), keep=False)["out"]
+    for name, y in (("forward", y_fast), ("forward_train", y_train)):
+        err = float(np.max(np.abs(y - ref_y).max(axis=1) / np.abs(ref_y).max(axis=1)))
+        print(f"[grad] F = {mult} d {name} y err {err:.1e}", flush=True)
+        assert err <= TOL["bf16"], (name, err)
+    check(b, {k: v.cpu().numpy().astype(np.float64) for k, v in g.items()}, TOL["bf16"])
+
+
 def test_fused_and_generic_backward_agree(torch, chunk_override, monkeypatch):
     """The same batch through the fused backward and through the K|V product
     with the exact fp32 attention (STCA_BWD=generic): both within the bar of
