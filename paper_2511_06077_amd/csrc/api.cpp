@@ -808,12 +808,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                               bf ? n * 2 * d : 2 * d, bf, bf ? dkvt + (size_t)i * 2 * d * nh8 : nullptr, nh8, nt,
                               st));
     }
-    HIPCHK(reduce_chunks(nt, d, tch, dqp, dq, 1.f, st));
+    // dq: fp32 for the fp32 products, else only its bf16 copy
+    HIPCHK(reduce_chunks(nt, d, tch, dqp, bf ? nullptr : dq, bf ? at<bf16_bits>(ws, L.b_dq) : nullptr, 1.f, st));
     HIPCHK(rec.mark("attn_bwd"));
     // q = s Wq
     if (bf) {
       const int nti = static_cast<int>(nt);
-      HIPCHK(convert(0, 1, dq, at<bf16_bits>(ws, L.b_dq), nt * d, st));
       const bf16_bits* s16 = L.bfused ? FS16(i) : at<bf16_bits>(ws, L.b_s);
       if (!L.bfused) HIPCHK(convert(0, 1, s, at<bf16_bits>(ws, L.b_s), nt * d, st));
       HIPCHK(gemm_mfma(d, d, nti, s16, d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,

@@ -574,13 +574,16 @@ __global__ __launch_bounds__(256) void attn_bwd_q_kernel(
 }
 
 __global__ void reduce_chunks_kernel(int64_t n_tgt, int d, const int32_t* __restrict__ tchunks,
-                                     const float* __restrict__ part, float* __restrict__ out, float scale) {
+                                     const float* __restrict__ part, float* __restrict__ out,
+                                     bf16_bits* __restrict__ out16, float scale) {
   const int64_t idx = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= n_tgt * d) return;
   const int64_t t = idx / d;
   float v = 0.f;
   for (int c = 0; c < tchunks[t]; ++c) v += part[(int64_t)c * n_tgt * d + idx];
-  out[idx] = v * scale;
+  v *= scale;
+  if (out) out[idx] = v;
+  if (out16) out16[idx] = from_f32<bf16_bits>(v);
 }
 
 __global__ void relu_mask_kernel(float* __restrict__ dh, const float* __restrict__ pre, int64_t n) {
@@ -765,10 +768,10 @@ hipError_t attn_bwd_generic(int d_head, int n_heads, const Unit* units, int64_t 
 }
 
 hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const float* part, float* out,
-                         float scale, hipStream_t st) {
+                         bf16_bits* out16, float scale, hipStream_t st) {
   if (n_tgt == 0) return hipSuccess;
   hipLaunchKernelGGL(reduce_chunks_kernel, grid1(n_tgt * d, 256), dim3(256), 0, st, n_tgt, d, tchunks, part,
-                     out, scale);
+                     out, out16, scale);
   return hipGetLastError();
 }
 

@@ -70,8 +70,10 @@ hipError_t attn_bwd_mfma(int d_head, int n_heads, const Unit* units, int64_t max
                          const int32_t* toff, const float* Q, const float* KV, int d, const float* a, const float* da,
                          const float* lse, float* dq_part, void* dKV, int64_t ldkv, int dkv_bf16, bf16_bits* dKVT,
                          int64_t ldt, int64_t n_tgt, hipStream_t st);
+// out (fp32) and out16 (bf16, rounded from the same fp32 value), either may
+// be null: the scaled sum of each target's chunk partials
 hipError_t reduce_chunks(int64_t n_tgt, int d, const int32_t* tchunks, const float* part, float* out,
-                         float scale, hipStream_t st);
+                         bf16_bits* out16, float scale, hipStream_t st);
 hipError_t relu_mask_mul(float* dh, const float* pre, int64_t n, hipStream_t st);
 // Zero the history rows of requests without targets in dKV ([N_hist][ldkv]
 // bf16, columns [0, cols)) and, when dKVT is given ([cols][ldt]), the
