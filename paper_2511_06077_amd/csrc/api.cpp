@@ -820,7 +820,21 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                        dw->dwq + (size_t)i * d * d, d, 1.f, 0, at<float>(ws, L.gpart), L.gpart_floats, st));
       // ds of the layer below = du + dq W_Q^T: the fused form's next update
       // forms it; the last one (the target gradient) is a product here
-      if (!L.bfused || i == 0) {
+      if (L.bfused && i == 0) {
+        UpdateGrad fin{};
+        fin.layer = 0;
+        fin.W2TP = at<char>(ws, L.fw2t);  // valid but unread in this mode
+        fin.W1TP = at<char>(ws, L.fw1t);
+        fin.WoTP = at<char>(ws, L.fwot);
+        fin.F = F;
+        fin.n_tgt = nt;
+        fin.du_in = du;
+        fin.dq16 = at<bf16_bits>(ws, L.b_dq);
+        fin.WqTP = at<char>(ws, L.fwqt);
+        fin.q_layer = 0;
+        fin.ds_out = ds2;
+        HIPCHK(fast_update_grad(d, fin, st));
+      } else if (!L.bfused) {
         HIPCHK(hipMemcpyAsync(ds2, du, 4 * nt * d, hipMemcpyDeviceToDevice, st));
         HIPCHK(gemm_mfma(nti, d, d, at<bf16_bits>(ws, L.b_dq), d, 0, static_cast<const bf16_bits*>(Wq), d, 1, ds2,
                          d, 1.f, 1, nullptr, 0, st));

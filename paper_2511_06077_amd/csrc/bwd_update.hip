@@ -350,7 +350,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
   auto w1t_tile = [&](int c) { return W1TP + ((int64_t)(A.layer * NW + w) * KSF + c * KS) * 64; };
   const bf16x8* wot_tile = WoTP + ((int64_t)(A.layer * NW + w) * KS) * 64;
   bf16x8 wa[KS], wb[KS];  // wb: W_2^T of chunk c (then W_O^T), wa: W_Q^T, then W_1^T of chunk c
-  if (PF) fetch(wb, w2t_tile(0));
+  if (PF && !A.ds_out) fetch(wb, w2t_tile(0));
 
   f32x16 du;
   if (A.dq16) {
@@ -373,6 +373,10 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_grad_kernel(UpdateGrad A
     const f32x16 dprev = load32(A.du_in, D, 32 * w);
 #pragma unroll
     for (int v = 0; v < 16; ++v) du[v] += dprev[v];
+    if (A.ds_out) {
+      store32(A.ds_out, D, 32 * w, du);
+      return;
+    }
     __syncthreads();  // every wave is done with dq
     put_tile(act, 32 * w, du);
     store16(A.ds16_out, D, 32 * w, du);

@@ -122,6 +122,8 @@ hipError_t fast_update_precise(int D, const UpdatePrecise& f, hipStream_t st);
 // With dq16 set, the gradient of s' is formed first, ds = du_in + dq16 W_Q^T
 // (W_Q of layer q_layer, packed transposed in WqTP; du_in may be du_out:
 // each element is read before the same thread writes it), and ds is unused.
+// With ds_out set as well, only that ds is formed and written (fp32), and
+// nothing else is read or written.
 struct UpdateGrad {
   int layer, F;
   int64_t n_tgt;
@@ -134,6 +136,7 @@ struct UpdateGrad {
   const bf16_bits* dq16;   // [n_tgt][D]
   const void* WqTP;
   int q_layer;
+  float* ds_out;
 };
 hipError_t fast_update_grad(int D, const UpdateGrad& f, hipStream_t st);
 
