@@ -225,9 +225,11 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->gpart_floats = 0;
     if (bf) {
       const int di = static_cast<int>(d), Fi = static_cast<int>(F), nti = static_cast<int>(nt);
+      // (the fused form runs the three target-side weight gradients of a
+      // layer as one group, whose splits share the buffer)
       L->gpart_floats = std::max({gemm_mfma_part_floats(di, 2 * di * static_cast<int>(n), static_cast<int>(nh8)),
-                                  gemm_mfma_part_floats(Fi, di, nti), gemm_mfma_part_floats(di, Fi, nti),
-                                  gemm_mfma_part_floats(di, di, nti)});
+                                  gemm_mfma_part_floats(Fi, di, nti) + gemm_mfma_part_floats(di, Fi, nti) +
+                                      gemm_mfma_part_floats(di, di, nti)});
     }
     L->gpart = bf ? m.take(4 * L->gpart_floats) : 0;
     if (L->bfused) {
@@ -735,12 +737,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
         ug.q_layer = i + 1;
       }
       HIPCHK(fast_update_grad(d, ug, st));
-      HIPCHK(gemm_mfma(F, d, nti, FH16(i), F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, 0, gp, gpf,
-                       st));
-      HIPCHK(gemm_mfma(d, F, nti, FU16(i), d, 1, B(L.b_dhid), F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, 0, gp, gpf,
-                       st));
-      HIPCHK(gemm_mfma(d, d, nti, FA16(i), d, 1, B(L.b_du), d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, 0, gp, gpf,
-                       st));
+      // dW_2 = h^T ds, dW_1 = u^T dH, dW_O = a^T du: one grouped launch
+      const GemmSpec wg[3] = {
+          {F, d, nti, FH16(i), F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, 0},
+          {d, F, nti, FU16(i), d, 1, B(L.b_dhid), F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, 0},
+          {d, d, nti, FA16(i), d, 1, B(L.b_du), d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, 0}};
+      HIPCHK(gemm_mfma_group(wg, 3, gp, gpf, st));
     } else if (bf) {
       const int nti = static_cast<int>(nt);
       float* gp = at<float>(ws, L.gpart);

@@ -103,20 +103,39 @@ __device__ __forceinline__ void store_tile(bf16_bits* __restrict__ lds, const u1
 
 // op(A) element (m, k): A[m * lda + k] if A_KC else A[k * lda + m].
 // op(B) element (k, n): B[n * ldb + k] if B_KC else B[k * ldb + n].
-template <bool A_KC, bool B_KC>
-__global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, const bf16_bits* __restrict__ A,
-                                                        int64_t lda, const bf16_bits* __restrict__ B, int64_t ldb,
-                                                        float* __restrict__ C, int64_t ldc, float alpha,
-                                                        int accumulate, int k_chunk, int n_tiles_m, int n_tiles_n,
-                                                        int n_work, float* __restrict__ part) {
-  __shared__ __attribute__((aligned(16))) bf16_bits As[BM * LROW];
-  __shared__ __attribute__((aligned(16))) bf16_bits Bs[BN * LROW];
-  // contiguous range of work items per XCD (workgroups are dealt to XCDs
-  // round robin by their linear index)
-  const int lid = blockIdx.x;
+// One work item (output tile, K split) of a product.
+struct GemmProblem {
+  int M, N, K;
+  const bf16_bits* A;
+  int64_t lda;
+  const bf16_bits* B;
+  int64_t ldb;
+  float* C;
+  int64_t ldc;
+  float alpha;
+  int accumulate, k_chunk, n_tiles_m, n_tiles_n, splits;
+  int work_begin;  // first work item of this product in a grouped launch
+  float* part;     // per-split partial tiles, or null (no split)
+};
+
+// workgroups are dealt to the XCDs round robin by their linear index: give
+// each XCD a contiguous range of work items
+__device__ __forceinline__ int xcd_work_id() {
   const int per = gridDim.x / kXcds;
-  const int w_id = (lid % kXcds) * per + lid / kXcds;
-  if (w_id >= n_work) return;
+  return (blockIdx.x % kXcds) * per + blockIdx.x / kXcds;
+}
+
+template <bool A_KC, bool B_KC>
+__device__ __forceinline__ void gemm_work(const GemmProblem& P, int w_id, bf16_bits* __restrict__ As,
+                                          bf16_bits* __restrict__ Bs) {
+  const int M = P.M, N = P.N, K = P.K, k_chunk = P.k_chunk, n_tiles_m = P.n_tiles_m, n_tiles_n = P.n_tiles_n;
+  const bf16_bits* __restrict__ A = P.A;
+  const bf16_bits* __restrict__ B = P.B;
+  const int64_t lda = P.lda, ldb = P.ldb, ldc = P.ldc;
+  float* __restrict__ C = P.C;
+  float* __restrict__ part = P.part;
+  const float alpha = P.alpha;
+  const int accumulate = P.accumulate;
   const int tiles = n_tiles_m * n_tiles_n;
   const int split = w_id / tiles, t = w_id % tiles;
   const int m0 = (t / n_tiles_n) * BM, n0 = (t % n_tiles_n) * BN;
@@ -183,6 +202,36 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(int M, int N, int K, con
     }
 }
 
+template <bool A_KC, bool B_KC>
+__global__ __launch_bounds__(256) void mfma_gemm_kernel(GemmProblem P, int n_work) {
+  __shared__ __attribute__((aligned(16))) bf16_bits As[BM * LROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits Bs[BN * LROW];
+  const int w_id = xcd_work_id();
+  if (w_id >= n_work) return;
+  gemm_work<A_KC, B_KC>(P, w_id, As, Bs);
+}
+
+// Up to kMaxGroup products (same operand forms) in one launch, their work
+// items numbered consecutively.
+constexpr int kMaxGroup = 3;
+struct GemmGroup {
+  GemmProblem p[kMaxGroup];
+  int n;
+};
+
+template <bool A_KC, bool B_KC>
+__global__ __launch_bounds__(256) void mfma_gemm_group_kernel(GemmGroup G, int n_work) {
+  __shared__ __attribute__((aligned(16))) bf16_bits As[BM * LROW];
+  __shared__ __attribute__((aligned(16))) bf16_bits Bs[BN * LROW];
+  const int w_id = xcd_work_id();
+  if (w_id >= n_work) return;
+  int q = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroup; ++i)
+    if (i < G.n && w_id >= G.p[i].work_begin) q = i;
+  gemm_work<A_KC, B_KC>(G.p[q], w_id - G.p[q].work_begin, As, Bs);
+}
+
 __global__ void split_sum_kernel(const float* __restrict__ part, int splits, int M, int N, float* __restrict__ C,
                                  int64_t ldc, float alpha, int accumulate) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -191,6 +240,25 @@ __global__ void split_sum_kernel(const float* __restrict__ part, int splits, int
   for (int k = 0; k < splits; ++k) s += part[(int64_t)k * M * N + i];
   float* c = C + (i / N) * ldc + i % N;
   *c = accumulate ? *c + alpha * s : alpha * s;
+}
+
+// split_sum_kernel over every split product of a group, one thread per
+// output element, the products' elements numbered consecutively
+__global__ void split_sum_group_kernel(GemmGroup G) {
+  int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  for (int q = 0; q < G.n; ++q) {
+    const GemmProblem& P = G.p[q];
+    if (!P.part) continue;
+    const int64_t mn = (int64_t)P.M * P.N;
+    if (i < mn) {
+      float s = 0.f;
+      for (int k = 0; k < P.splits; ++k) s += P.part[(int64_t)k * mn + i];
+      float* c = P.C + (i / P.N) * P.ldc + i % P.N;
+      *c = P.accumulate ? *c + P.alpha * s : P.alpha * s;
+      return;
+    }
+    i -= mn;
+  }
 }
 
 bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
@@ -268,17 +336,17 @@ int64_t gemm_mfma_part_floats(int M, int N, int K) {
   return s > 1 ? s * M * N : 0;
 }
 
-hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
-                     int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
-                     int64_t part_floats, hipStream_t st) {
-  if (M == 0 || N == 0) return hipSuccess;
+namespace {
+// Validate one product and plan its split over K (work items = tiles x splits).
+hipError_t plan_problem(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
+                        int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
+                        int64_t part_floats, GemmProblem* P, int64_t* work) {
   const bool a_kc = !transA, b_kc = transB != 0;
   // whole 16-byte vectors: the contiguous extent of each operand is a
   // multiple of 8 elements and every row starts 16-byte aligned
   if ((a_kc ? K : M) % 8 || (b_kc ? K : N) % 8 || lda % 8 || ldb % 8 || !al16(A) || !al16(B))
     return hipErrorInvalidValue;
   const int tm = static_cast<int>(ceil_div(M, BM)), tn = static_cast<int>(ceil_div(N, BN));
-  const int64_t tiles = (int64_t)tm * tn;
   int splits = 1;
   if (part) {
     splits = static_cast<int>(k_splits(M, N, K));
@@ -286,21 +354,78 @@ hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
   }
   const int k_chunk = std::max(BK, static_cast<int>(round_up(ceil_div(K, splits), BK)));
   splits = static_cast<int>(ceil_div(K, k_chunk));
-  float* p = splits > 1 ? part : nullptr;
-  const int64_t work = tiles * splits;
+  *P = GemmProblem{M, N, K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, tm, tn, splits, 0,
+                   splits > 1 ? part : nullptr};
+  *work = (int64_t)tm * tn * splits;
+  return hipSuccess;
+}
+
+template <typename Launch>
+hipError_t by_form(bool a_kc, bool b_kc, Launch launch) {
+  if (a_kc && b_kc) launch(std::integral_constant<int, 3>{});
+  else if (a_kc) launch(std::integral_constant<int, 2>{});
+  else if (b_kc) launch(std::integral_constant<int, 1>{});
+  else launch(std::integral_constant<int, 0>{});
+  return hipSuccess;
+}
+}  // namespace
+
+hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
+                     int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
+                     int64_t part_floats, hipStream_t st) {
+  if (M == 0 || N == 0) return hipSuccess;
+  GemmProblem P;
+  int64_t work = 0;
+  hipError_t e = plan_problem(M, N, K, A, lda, transA, B, ldb, transB, C, ldc, alpha, accumulate, part,
+                              part_floats, &P, &work);
+  if (e != hipSuccess) return e;
   const int64_t grid = round_up(work, kXcds);
   if (grid > 0x7fffffff) return hipErrorInvalidValue;
-#define STCA_MG(AK, BKC)                                                                                    \
-  hipLaunchKernelGGL((mfma_gemm_kernel<AK, BKC>), dim3(static_cast<unsigned>(grid)), dim3(256), 0, st, M, N, \
-                     K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, tm, tn, static_cast<int>(work), p)
-  if (a_kc && b_kc) STCA_MG(true, true);
-  else if (a_kc) STCA_MG(true, false);
-  else if (b_kc) STCA_MG(false, true);
-  else STCA_MG(false, false);
-#undef STCA_MG
-  if (p)
+  by_form(!transA, transB != 0, [&](auto f) {
+    constexpr int F = decltype(f)::value;
+    hipLaunchKernelGGL((mfma_gemm_kernel<(F & 2) != 0, (F & 1) != 0>), dim3(static_cast<unsigned>(grid)), dim3(256),
+                       0, st, P, static_cast<int>(work));
+  });
+  if (P.part)
     hipLaunchKernelGGL(split_sum_kernel, dim3(static_cast<unsigned>(ceil_div((int64_t)M * N, 256))), dim3(256), 0,
-                       st, p, splits, M, N, C, ldc, alpha, accumulate);
+                       st, P.part, P.splits, M, N, C, ldc, alpha, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t gemm_mfma_group(const GemmSpec* specs, int n, float* part, int64_t part_floats, hipStream_t st) {
+  if (n < 1 || n > kMaxGroup) return hipErrorInvalidValue;
+  GemmGroup G{};
+  int64_t total = 0, part_used = 0, sum_threads = 0;
+  int form = -1;
+  for (int i = 0; i < n; ++i) {
+    const GemmSpec& g = specs[i];
+    if (g.M == 0 || g.N == 0) return hipErrorInvalidValue;
+    const int f = (!g.transA ? 2 : 0) | (g.transB != 0 ? 1 : 0);
+    if (form >= 0 && f != form) return hipErrorInvalidValue;  // one operand form per launch
+    form = f;
+    int64_t work = 0;
+    float* p = part ? part + part_used : nullptr;
+    hipError_t e = plan_problem(g.M, g.N, g.K, g.A, g.lda, g.transA, g.B, g.ldb, g.transB, g.C, g.ldc, g.alpha,
+                                g.accumulate, p, part ? part_floats - part_used : 0, &G.p[i], &work);
+    if (e != hipSuccess) return e;
+    G.p[i].work_begin = static_cast<int>(total);
+    total += work;
+    if (G.p[i].part) {
+      part_used += (int64_t)G.p[i].splits * g.M * g.N;
+      sum_threads += (int64_t)g.M * g.N;
+    }
+  }
+  G.n = n;
+  const int64_t grid = round_up(total, kXcds);
+  if (grid > 0x7fffffff) return hipErrorInvalidValue;
+  by_form(form & 2, form & 1, [&](auto f) {
+    constexpr int F = decltype(f)::value;
+    hipLaunchKernelGGL((mfma_gemm_group_kernel<(F & 2) != 0, (F & 1) != 0>), dim3(static_cast<unsigned>(grid)),
+                       dim3(256), 0, st, G, static_cast<int>(total));
+  });
+  if (sum_threads > 0)
+    hipLaunchKernelGGL(split_sum_group_kernel, dim3(static_cast<unsigned>(ceil_div(sum_threads, 256))), dim3(256), 0,
+                       st, G);
   return hipGetLastError();
 }
 
