@@ -225,11 +225,11 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     L->gpart_floats = 0;
     if (bf) {
       const int di = static_cast<int>(d), Fi = static_cast<int>(F), nti = static_cast<int>(nt);
-      // (the fused form runs the three target-side weight gradients of a
-      // layer as one group, whose splits share the buffer)
+      // (the fused form runs the target-side weight gradients of a layer,
+      // with dW_Q of the layer above, as one group whose splits share it)
       L->gpart_floats = std::max({gemm_mfma_part_floats(di, 2 * di * static_cast<int>(n), static_cast<int>(nh8)),
                                   gemm_mfma_part_floats(Fi, di, nti) + gemm_mfma_part_floats(di, Fi, nti) +
-                                      gemm_mfma_part_floats(di, di, nti)});
+                                      2 * gemm_mfma_part_floats(di, di, nti)});
     }
     L->gpart = bf ? m.take(4 * L->gpart_floats) : 0;
     if (L->bfused) {
@@ -737,12 +737,15 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
         ug.q_layer = i + 1;
       }
       HIPCHK(fast_update_grad(d, ug, st));
-      // dW_2 = h^T ds, dW_1 = u^T dH, dW_O = a^T du: one grouped launch
-      const GemmSpec wg[3] = {
+      // dW_2 = h^T ds, dW_1 = u^T dH, dW_O = a^T du, and dW_Q = s^T dq of
+      // layer i + 1: one grouped launch
+      const GemmSpec wg[4] = {
           {F, d, nti, FH16(i), F, 1, B(L.b_ds), d, 0, dw->dw2 + (size_t)i * F * d, d, 1.f, 0},
           {d, F, nti, FU16(i), d, 1, B(L.b_dhid), F, 0, dw->dw1 + (size_t)i * d * F, F, 1.f, 0},
-          {d, d, nti, FA16(i), d, 1, B(L.b_du), d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, 0}};
-      HIPCHK(gemm_mfma_group(wg, 3, gp, gpf, st));
+          {d, d, nti, FA16(i), d, 1, B(L.b_du), d, 0, dw->dwo + (size_t)i * d * d, d, 1.f, 0},
+          {d, d, nti, FS16(i + 1 < n ? i + 1 : i), d, 1, B(L.b_dq), d, 0, dw->dwq + (size_t)(i + 1) * d * d, d, 1.f,
+           0}};
+      HIPCHK(gemm_mfma_group(wg, i + 1 < n ? 4 : 3, gp, gpf, st));
     } else if (bf) {
       const int nti = static_cast<int>(nt);
       float* gp = at<float>(ws, L.gpart);
@@ -818,8 +821,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       const int nti = static_cast<int>(nt);
       const bf16_bits* s16 = L.bfused ? FS16(i) : at<bf16_bits>(ws, L.b_s);
       if (!L.bfused) HIPCHK(convert(0, 1, s, at<bf16_bits>(ws, L.b_s), nt * d, st));
-      HIPCHK(gemm_mfma(d, d, nti, s16, d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,
-                       dw->dwq + (size_t)i * d * d, d, 1.f, 0, at<float>(ws, L.gpart), L.gpart_floats, st));
+      // dW_Q = s^T dq: in the fused form it joins the next layer's group of
+      // weight gradients (its operands stay until the next attention
+      // backward), the last one runs alone
+      if (!L.bfused || i == 0)
+        HIPCHK(gemm_mfma(d, d, nti, s16, d, 1, at<bf16_bits>(ws, L.b_dq), d, 0,
+                         dw->dwq + (size_t)i * d * d, d, 1.f, 0, at<float>(ws, L.gpart), L.gpart_floats, st));
       // ds of the layer below = du + dq W_Q^T: the fused form's next update
       // forms it; the last one (the target gradient) is a product here
       if (L.bfused && i == 0) {

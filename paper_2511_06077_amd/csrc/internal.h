@@ -32,7 +32,7 @@ int64_t gemm_mfma_part_floats(int M, int N, int K);
 hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
                      int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
                      int64_t part_floats, hipStream_t st);
-// Up to three gemm_mfma products with the same operand forms (transA,
+// Up to four gemm_mfma products with the same operand forms (transA,
 // transB) in one launch (and one launch summing their splits), so that small
 // products fill the chip together; `part` is shared, the products' splits in
 // order (the sum of their gemm_mfma_part_floats holds every split).
