@@ -322,12 +322,14 @@ hipError_t transpose_bf16(const bf16_bits* src, int64_t lds, int R, int C, bf16_
 }
 
 namespace {
-// Splits over K of a product with few output tiles: enough partial tiles to
-// fill the chip (about 1024 workgroups), each split at least 256 deep.
+// Splits over K of a product with few output tiles: enough partial tiles for
+// about 2048 workgroups (two rounds of the four a CU holds, so one round's
+// loads overlap the other's products: [dW_K | dW_V] at the training window
+// 0.86 -> 0.82 ms against 1024), each split at least 256 deep.
 int64_t k_splits(int M, int N, int K) {
   const int64_t tiles = ceil_div(M, BM) * ceil_div(N, BN);
   if (tiles >= 256 || K < 1024) return 1;
-  return std::max<int64_t>(1, std::min<int64_t>(ceil_div(1024, tiles), K / 256));
+  return std::max<int64_t>(1, std::min<int64_t>(ceil_div(2048, tiles), K / 256));
 }
 }  // namespace
 
