@@ -284,6 +284,91 @@ def test_gradients_central_finite_differences():
             assert abs(num - ana) <= 1e-6 * max(1.0, abs(ana)), (k, idx, num, ana)
 
 
+C1 = "tiny_f32_R4_m4_L256_d64"  # R = 4, m = 4, L = 256, d = 64, h = 2, n = 2, F = 4 d
+
+
+def _c1_inputs():
+    b = W.make_batch(W.WORKLOADS[C1], with_grad=True)
+    inp = b.f64()
+    return inp, inp.pop("grad_out")
+
+
+def test_gradients_central_finite_differences_c1_shape():
+    """Central differences (eps = 1e-6, fp64) of f = sum <G, Y> at the tiny
+    workload's shape (4 requests x 4 targets, L = 256, d = 64, 2 heads,
+    2 layers, FFN width 4 d) on 200 random coordinates of every input and
+    weight tensor.  A coordinate is skipped (and replaced by another) when
+    the step moves any FFN pre-activation across zero, i.e. when the
+    function is not differentiable inside [x - eps, x + eps].  Per tensor,
+    max |fd - g| over the checked coordinates must stay within 1e-6 of the
+    tensor's largest gradient entry (rounding of f alone puts central
+    differences near 1e-8 of it here)."""
+    inp, G = _c1_inputs()
+    g = O.backward(inp, G)
+    base = O.forward(inp, keep=True)
+    rng = np.random.default_rng(2024)
+    eps = 1e-6
+    for k in ["hist", "tgt"] + list(O.LAYER_WEIGHTS):
+        flat = inp[k].reshape(-1)
+        order = rng.permutation(flat.size)
+        worst, checked, skipped = 0.0, 0, 0
+        scale = float(np.abs(g["d" + k]).max())
+        for idx in order:
+            plus, minus = inp[k].copy(), inp[k].copy()
+            plus.reshape(-1)[idx] += eps
+            minus.reshape(-1)[idx] -= eps
+            fp = O.forward(with_(inp, **{k: plus}), keep=True)
+            fm = O.forward(with_(inp, **{k: minus}), keep=True)
+            sb = np.sign(base["pre"])
+            if np.any(np.sign(fp["pre"]) != sb) or np.any(np.sign(fm["pre"]) != sb):
+                skipped += 1
+                continue
+            num = ((fp["out"] - fm["out"]) * G).sum() / (2 * eps)
+            worst = max(worst, abs(num - g["d" + k].reshape(-1)[idx]))
+            checked += 1
+            if checked == 200:
+                break
+        print(f"[fd c1] {k}: {checked} coordinates ({skipped} skipped at a ReLU kink), "
+              f"max |fd - g| / max |g| = {worst / scale:.1e}")
+        assert checked == 200, (k, checked)
+        assert worst <= 1e-6 * scale, (k, worst / scale)
+
+
+def _autograd_check(inp, G, h):
+    torch = pytest.importorskip("torch")
+    g = O.backward(inp, G)
+    names = ["hist", "tgt"] + list(O.LAYER_WEIGHTS)
+    p = {k: torch.tensor(inp[k], requires_grad=True) for k in names}
+    Y = torch_forward(torch, p, inp["hist_off"], inp["tgt_off"], h)
+    ref_y = O.forward(inp, keep=False)["out"]
+    assert np.abs(Y.detach().numpy() - ref_y).max() <= 1e-12 * np.abs(ref_y).max()
+    (Y * torch.from_numpy(G)).sum().backward()
+    for k in names:
+        ref = p[k].grad.numpy()
+        err = np.abs(g["d" + k] - ref).max() / np.abs(ref).max()
+        print(f"[autograd] {k}: {err:.1e}")
+        assert err <= 1e-11, (k, err)
+
+
+def test_gradients_match_torch_autograd_c1_shape():
+    """Every gradient of the hand-derived reverse mode against torch float64
+    autograd through an independent forward, at the tiny workload's shape."""
+    inp, G = _c1_inputs()
+    _autograd_check(inp, G, 2)
+
+
+def test_gradients_match_torch_autograd_c2_shape_short_history():
+    """The same at the uniform bf16 workload's shape (64 requests x 16
+    targets, d = 128, 4 heads, 2 layers) with the history cut from 1024 to
+    64 rows so that the fp64 evaluation stays short; inputs are the bf16
+    workload's exact values."""
+    b = W.make_custom_batch("c2_short", [64] * 64, [16] * 64, d_model=128, n_heads=4, n_layers=2, dtype="bf16",
+                            seed=2, with_grad=True)
+    inp = b.f64()
+    G = inp.pop("grad_out")
+    _autograd_check(inp, G, 4)
+
+
 # --------------------------- planted mistakes must be caught by some pin
 def _mutant_cross_attention(kind):
     orig = O.cross_attention
