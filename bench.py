@@ -243,7 +243,6 @@ def main() -> int:
         kernels[lab] = ent
     dom = max((k for k in kernels if kernel_work(k, b, es) != (0.0, 0.0)),
               key=lambda k: kernels[k]["ms_per_step"])
-    kv_mode = os.environ.get("STCA_KV", "fused")
     flop, byts = kernel_work(dom, b, es)
     roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, peak_tf)
     roof["kernel"] = dom
@@ -273,7 +272,7 @@ def main() -> int:
         "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == "bf16" else "f32",
         "data": "synthetic",
-        "config": {"workload": wl.name, "kv": kv_mode, "requests": wl.n_requests,
+        "config": {"workload": wl.name, "requests": wl.n_requests,
                    "targets_per_request": wl.n_targets or list(wl.tgt_range),
                    "hist_len": wl.hist_len or list(wl.hist_range), "d_model": wl.d_model,
                    "heads": wl.n_heads, "layers": wl.n_layers, "ffn_hidden": wl.ffn_hidden},
@@ -578,38 +577,27 @@ def ablation(wl: W.Workload, args):
     import torch
     from paper_2511_06077_amd.device import DeviceBatch
     out = {}
-    if os.environ.get("STCA_KV") != "materialize":
-        os.environ["STCA_KV"] = "materialize"
-        try:
-            db = DeviceBatch(W.make_batch(wl, with_grad=False), device="cuda:0")
-            ms, per = timed_forward(db, max(3, args.steps // 4), 1)
-            ms /= max(3, args.steps // 4)
-            out["materialized_kv"] = {"ms_per_step": ms, "targets_per_s": db.b.n_tgt_total / (ms * 1e-3),
-                                      "kernels_ms_per_step": {k: float(np.sum(v)) / max(3, args.steps // 4)
-                                                              for k, v in per.items()}}
-            del db
-            torch.cuda.empty_cache()
-        finally:
-            del os.environ["STCA_KV"]
+    k_steps = max(3, args.steps // 4)
+    db = DeviceBatch(W.make_batch(wl, with_grad=False), device="cuda:0", kv="materialize")
+    ms, per = timed_forward(db, k_steps, 1)
+    ms /= k_steps
+    out["materialized_kv"] = {"ms_per_step": ms, "targets_per_s": db.b.n_tgt_total / (ms * 1e-3),
+                              "kernels_ms_per_step": {k: float(np.sum(v)) / k_steps for k, v in per.items()}}
+    del db
+    torch.cuda.empty_cache()
     if wl.n_targets > 1 and wl.hist_range is None:
         # one target per request: the reordered attention (App. A.2.2), and
         # the standard form on the same batch
         one = W.Workload(wl.name + "_m1", wl.n_requests, wl.d_model, wl.n_heads, wl.n_layers, wl.dtype, wl.seed,
                          hist_len=wl.hist_len, n_targets=1)
         bo = W.make_batch(one)
-        for key, mode in (("one_target_per_request", None), ("one_target_per_request_standard", "standard")):
-            if mode:
-                os.environ["STCA_ATTN"] = mode
-            try:
-                db = DeviceBatch(bo, device="cuda:0")
-                k = max(3, args.steps // 4)
-                ms = plain_forward(db, k, 2) / k
-                out[key] = {"ms_per_step": ms, "targets_per_s": one.n_requests / (ms * 1e-3),
-                            "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
-                del db
-                torch.cuda.empty_cache()
-            finally:
-                os.environ.pop("STCA_ATTN", None)
+        for key, mode in (("one_target_per_request", "auto"), ("one_target_per_request_standard", "standard")):
+            db = DeviceBatch(bo, device="cuda:0", attn=mode)
+            ms = plain_forward(db, k_steps, 2) / k_steps
+            out[key] = {"ms_per_step": ms, "targets_per_s": one.n_requests / (ms * 1e-3),
+                        "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
+            del db
+            torch.cuda.empty_cache()
     if wl.n_targets > 1 and wl.hist_range is None:
         # the same number of targets as 16 requests of 256: K/V written once
         # and read once per 128 targets, against the fused form's projection
@@ -617,20 +605,14 @@ def ablation(wl: W.Workload, args):
         many = W.Workload(wl.name + "_m256", max(1, wl.n_requests * wl.n_targets // 256), wl.d_model, wl.n_heads,
                           wl.n_layers, wl.dtype, wl.seed, hist_len=wl.hist_len, n_targets=256)
         bm = W.make_batch(many)
-        for key, mode in (("many_targets_per_request", None), ("many_targets_per_request_fused", "fused")):
-            if mode:
-                os.environ["STCA_KV"] = mode
-            try:
-                db = DeviceBatch(bm, device="cuda:0")
-                k = max(3, args.steps // 4)
-                ms = plain_forward(db, k, 2) / k
-                out[key] = {"requests": many.n_requests, "targets": bm.n_tgt_total, "ms_per_step": ms,
-                            "targets_per_s": bm.n_tgt_total / (ms * 1e-3),
-                            "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
-                del db
-                torch.cuda.empty_cache()
-            finally:
-                os.environ.pop("STCA_KV", None)
+        for key, mode in (("many_targets_per_request", "auto"), ("many_targets_per_request_fused", "fused")):
+            db = DeviceBatch(bm, device="cuda:0", kv=mode)
+            ms = plain_forward(db, k_steps, 2) / k_steps
+            out[key] = {"requests": many.n_requests, "targets": bm.n_tgt_total, "ms_per_step": ms,
+                        "targets_per_s": bm.n_tgt_total / (ms * 1e-3),
+                        "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
+            del db
+            torch.cuda.empty_cache()
     # instance-wise layout on a slice of requests that fits comfortably, scaled
     b = W.make_batch(wl, requests=list(range(min(wl.n_requests, 8))), with_grad=False)
     nb = W.replicate_per_target(b)

@@ -26,6 +26,22 @@
  *    w1 [n_layers][d][ffn_hidden], w2 [n_layers][ffn_hidden][d].
  *  - Storage dtype (STCA_F32 or STCA_BF16) applies to hist, tgt, the weights,
  *    out and dout; accumulation is always fp32; gradients are fp32.
+ *  - Range of the bf16 path.  bf16 storage keeps two bytes per value inside
+ *    the kernels as well, but in fp16 (three more mantissa bits, which the
+ *    attention's accuracy needs): the projected K and V, the queries, the
+ *    softmax weights and the target update's activations are fp16 MFMA
+ *    operands (fp32 accumulation), so each must stay below 65504 in
+ *    magnitude (the fp32 state and the fp32 sums have no such limit).  The
+ *    inputs themselves may use the whole bf16 range.  The forward's target
+ *    update checks every value it rounds to fp16 (input targets, merged
+ *    attention output, activations, next queries); an overflowed V, or a K
+ *    whose overflow drives a score to plus infinity, reaches it as a
+ *    non-finite attention output.  A violation is recorded in the workspace
+ *    and stca_device_status() then returns STCA_ERR_RANGE; outputs of such a
+ *    call are undefined.  A K entry whose overflow drives its score to minus
+ *    infinity only removes that history row from the softmax and is not
+ *    detected.  The backward's fp16 operands (two-term, hi + lo) have the same
+ *    range and are not checked.  Non-finite inputs propagate.
  *  - Request r owns hist rows [hist_off[r], hist_off[r+1]) and tgt rows
  *    [tgt_off[r], tgt_off[r+1]).  offsets[0] = 0, non-decreasing,
  *    offsets[R] = n_hist / n_tgt.  A request with targets must have at least
@@ -54,24 +70,65 @@ extern "C" {
 typedef enum {
   STCA_OK = 0,
   STCA_ERR_INVALID_ARG = -1, /* bad pointer, size or offsets */
-  STCA_ERR_UNSUPPORTED = -2, /* valid but not implemented shape/dtype */
+  STCA_ERR_UNSUPPORTED = -2, /* valid but not implemented shape/dtype/form */
   STCA_ERR_WORKSPACE = -3,   /* workspace or saved buffer too small */
-  STCA_ERR_HIP = -4          /* a HIP runtime call or launch failed */
+  STCA_ERR_HIP = -4,         /* a HIP runtime call or launch failed */
+  STCA_ERR_RANGE = -5        /* (device status only) an fp16 intermediate of the bf16 path
+                                overflowed or a non-finite value appeared; see below */
 } stca_status_t;
 
 typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
 
-/* Model shape.  d_model % n_heads == 0 and ffn_hidden a multiple of 32.
- * STCA_BF16 with d_head = d_model / n_heads = 32, d_model in {64, 128, 256}
- * and ffn_hidden a multiple of 256 runs on the bf16 MFMA kernels; every other shape with d_head in
- * {8, 16, 32, 64} (either dtype) runs on the generic fp32-arithmetic kernels
- * (stca_path tells which). */
+/* Execution forms of the bf16 MFMA path (0 = automatic everywhere).  The
+ * generic fp32-arithmetic path has one form of each and ignores them.
+ *
+ * kv_form  STCA_KV_AUTO: each layer's K/V is projected inside the attention
+ *          kernel and never stored, except when the host offsets show a
+ *          request with more than 64 targets: then one GEMM writes every
+ *          layer's K/V to the workspace once and the attention reads it once
+ *          per 128 targets.  STCA_KV_FUSED: always the former.
+ *          STCA_KV_MATERIALIZE: always the latter.
+ * attn_form STCA_ATTN_AUTO: the reordered single-query form of App. A.2.2
+ *          (Eq. attn-optimized: scores u . x with u = q W_K^T, output
+ *          (P X) W_V; no K/V) when the host offsets show every request with
+ *          at most 32 / n_heads targets, else the standard form.
+ *          STCA_ATTN_STANDARD: always the standard form.
+ *          STCA_ATTN_REORDERED: the reordered form; STCA_ERR_UNSUPPORTED for
+ *          a batch the automatic rule would not give it.
+ * bwd_form STCA_BWD_AUTO: the backward keeps K/V inside its attention kernels
+ *          when d_h = 32, ffn_hidden is a multiple of d_model and the host
+ *          offsets show at most 32 targets per request; otherwise K | V are
+ *          formed by a GEMM and the attention runs in exact fp32.
+ *          STCA_BWD_GENERIC: always the latter.  STCA_BWD_FUSED: the former;
+ *          STCA_ERR_UNSUPPORTED for a batch the automatic rule would not give
+ *          it.
+ * chunk_blocks: history chunk length, in 32-row blocks, of the attention's
+ *          split over a request's history (at most 16 chunks per request, so
+ *          long histories get longer chunks); 0 = chosen from the batch size
+ *          and the number of compute units.
+ * Out-of-range values are STCA_ERR_INVALID_ARG. */
+typedef enum { STCA_KV_AUTO = 0, STCA_KV_FUSED = 1, STCA_KV_MATERIALIZE = 2 } stca_kv_form_t;
+typedef enum { STCA_ATTN_AUTO = 0, STCA_ATTN_STANDARD = 1, STCA_ATTN_REORDERED = 2 } stca_attn_form_t;
+typedef enum { STCA_BWD_AUTO = 0, STCA_BWD_FUSED = 1, STCA_BWD_GENERIC = 2 } stca_bwd_form_t;
+
+/* Model shape and execution forms.  d_model % n_heads == 0 and ffn_hidden a
+ * multiple of 32.  STCA_BF16 with d_head = d_model / n_heads = 32, d_model in
+ * {64, 128, 256} and ffn_hidden a multiple of 256 runs on the bf16 MFMA
+ * kernels; every other shape with d_head in {8, 16, 32, 64} (either dtype)
+ * runs on the generic fp32-arithmetic kernels (stca_path tells which).
+ * Every size and launch decision depends only on this structure and the
+ * batch, so a workspace sized for a (dims, batch) pair fits every call with
+ * the same pair.  Zero-initialise the structure to get the automatic forms. */
 typedef struct {
   int32_t d_model;
   int32_t n_heads;
   int32_t n_layers;
   int32_t ffn_hidden;
-  int32_t dtype; /* stca_dtype_t */
+  int32_t dtype;        /* stca_dtype_t */
+  int32_t kv_form;      /* stca_kv_form_t */
+  int32_t attn_form;    /* stca_attn_form_t */
+  int32_t bwd_form;     /* stca_bwd_form_t */
+  int32_t chunk_blocks; /* >= 0 */
 } stca_dims_t;
 
 /* A packed ragged batch (App. A.4: flattened rows plus segment boundaries). */
@@ -132,10 +189,8 @@ stca_status_t stca_saved_layout(const stca_dims_t* dims, const stca_batch_t* bat
  *  saved nullable; when given (stca_saved_size bytes) the per-layer
  *        intermediates (see stca_saved_layout_t) are written there
  *  ws    device workspace of ws_bytes >= stca_workspace_size(dims, batch, 0)
- * On the bf16 MFMA path each layer's K/V is projected inside the attention
- * kernel and never stored; with the environment variable STCA_KV=materialize
- * (read at every call, including stca_workspace_size) one GEMM first writes
- * every layer's K/V to the workspace and the attention streams it. */
+ * The bf16 MFMA path's forms of K/V and of the attention follow
+ * dims->kv_form and dims->attn_form. */
 stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch,
                            const void* hist, const void* tgt, const stca_weights_t* w,
                            void* out, void* saved, void* ws, size_t ws_bytes,
@@ -314,8 +369,11 @@ stca_status_t stca_forward_paper_profiled(const stca_dims_t* dims, const stca_ba
                                           void* z, void* saved, void* ws, size_t ws_bytes, hipStream_t stream,
                                           hipEvent_t* events, int n_events, const char** labels);
 
-/* Reads (synchronising on `stream`) the status the device scheduler recorded
- * in `ws` during the last call that used it: STCA_OK or STCA_ERR_INVALID_ARG. */
+/* Reads (synchronising on `stream`) the status the kernels recorded in `ws`
+ * during the last call that used it: STCA_ERR_INVALID_ARG when the device
+ * scheduler found bad offsets, else STCA_ERR_RANGE when the forward's target
+ * update found an fp16 intermediate out of range or a non-finite attention
+ * output (bf16 path, see "Range of the bf16 path"), else STCA_OK. */
 stca_status_t stca_device_status(const void* ws, hipStream_t stream);
 
 /* Static description of a status code. */

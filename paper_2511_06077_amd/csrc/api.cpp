@@ -15,38 +15,33 @@ using namespace stca::api;
 
 namespace {
 
-// The bf16 path projects the history inside the attention kernel by default
-// (K/V never reach HBM).  STCA_KV=materialize selects the two-kernel form
-// instead: one GEMM writes every layer's K/V, then the attention streams it.
-bool materialize_kv() {
-  const char* e = std::getenv("STCA_KV");
-  return e && std::strcmp(e, "materialize") == 0;
-}
+// Form choices of the bf16 path.  Each follows stca_dims_t's execution
+// fields (0 = automatic) and the batch alone, so a workspace sized for a
+// (dims, batch) pair fits every call made with the same pair.
 
-// The bf16 path evaluates attention in the reordered form (scores u . x with
-// u = q W_K^j^T, output (P X) W_V^j; no K/V at all) when every request has
-// at most 32 / H targets, which the host offsets must show; the standard form
-// otherwise.  STCA_ATTN=standard / reordered forces either (reordered still
-// needs host offsets and at most 32 / H targets per request, else standard).
-bool reordered_for(const stca_dims_t* dims, const stca_batch_t* b) {
-  const char* e = std::getenv("STCA_ATTN");
-  if (e && std::strcmp(e, "standard") == 0) return false;
-  if (!b->tgt_off_host) return false;
+// Reordered attention (scores u . x with u = q W_K^j^T, output (P X) W_V^j;
+// no K/V at all): automatic when the host offsets show every request with at
+// most 32 / H targets (one 32-column MFMA tile of (target, head) rows);
+// STCA_ATTN_REORDERED asks for it and is unsupported for other batches.
+// Returns 1 (reordered), 0 (standard) or a negative status.
+int reordered_for(const stca_dims_t* dims, const stca_batch_t* b) {
+  if (dims->attn_form == STCA_ATTN_STANDARD) return 0;
+  bool ok = b->tgt_off_host != nullptr;
   const int cap = 32 / (dims->d_model / dims->n_heads == 32 ? dims->n_heads : 1 << 30);
-  if (cap < 1) return false;
-  for (int r = 0; r < b->n_requests; ++r)
-    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > cap) return false;
-  return true;
+  ok = ok && cap >= 1;
+  for (int r = 0; ok && r < b->n_requests; ++r)
+    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > cap) ok = false;
+  if (dims->attn_form == STCA_ATTN_REORDERED && !ok) return STCA_ERR_UNSUPPORTED;
+  return ok ? 1 : 0;
 }
 
 // Requests with more than kTargetGroup targets: the fused kernel would
-// project their history once per 64-target group, so the bf16 path writes
-// K/V once instead and runs the attention in units of up to kWideGroup
-// targets (K/V read once per 128 targets).  Needs host offsets; STCA_KV=fused
-// keeps the fused form.
-bool wide_groups_for(const stca_batch_t* b) {
-  const char* e = std::getenv("STCA_KV");
-  if (e && std::strcmp(e, "fused") == 0) return false;
+// project their history once per 64-target group, so the automatic choice
+// writes K/V once instead and runs the attention in units of up to
+// kWideGroup targets (K/V read once per 128 targets).  Needs host offsets;
+// STCA_KV_FUSED keeps the fused form.
+bool wide_groups_for(const stca_dims_t* dims, const stca_batch_t* b) {
+  if (dims->kv_form == STCA_KV_FUSED) return false;
   if (!b->tgt_off_host) return false;
   for (int r = 0; r < b->n_requests; ++r)
     if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > kTargetGroup) return true;
@@ -58,17 +53,17 @@ bool wide_groups_for(const stca_batch_t* b) {
 // when d_h = 32, the FFN width is a multiple of d and every request has at
 // most 32 targets, which the host offsets must show; otherwise K | V are
 // formed by a GEMM, the attention runs exactly in fp32 and the target side as
-// separate GEMMs.  STCA_BWD=generic forces the latter.
-bool fused_bwd_for(const stca_dims_t* dims, const stca_batch_t* b) {
-  const char* e = std::getenv("STCA_BWD");
-  if (e && std::strcmp(e, "generic") == 0) return false;
-  if (dims->dtype != STCA_BF16 || dims->d_model / dims->n_heads != 32) return false;
-  if (dims->d_model != 64 && dims->d_model != 128 && dims->d_model != 256) return false;
-  if (dims->ffn_hidden % dims->d_model != 0) return false;
-  if (!b->tgt_off_host) return false;
-  for (int r = 0; r < b->n_requests; ++r)
-    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > 32) return false;
-  return true;
+// separate GEMMs.  STCA_BWD_GENERIC forces the latter; STCA_BWD_FUSED asks for
+// the former and is unsupported for other batches.  1 / 0 / negative status.
+int fused_bwd_for(const stca_dims_t* dims, const stca_batch_t* b) {
+  if (dims->bwd_form == STCA_BWD_GENERIC) return 0;
+  bool ok = dims->dtype == STCA_BF16 && dims->d_model / dims->n_heads == 32 &&
+            (dims->d_model == 64 || dims->d_model == 128 || dims->d_model == 256) &&
+            dims->ffn_hidden % dims->d_model == 0 && b->tgt_off_host != nullptr;
+  for (int r = 0; ok && r < b->n_requests; ++r)
+    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > 32) ok = false;
+  if (dims->bwd_form == STCA_BWD_FUSED && !ok) return STCA_ERR_UNSUPPORTED;
+  return ok ? 1 : 0;
 }
 
 struct Layout {
@@ -79,6 +74,7 @@ struct Layout {
   int64_t max_units;
   bool any_narrow, any_wide;  // requests with 1..32 / 33+ targets (both true without host offsets)
   bool reord;                 // reordered attention (bf16 path)
+  bool mat;                   // K/V written to the workspace by one GEMM (bf16 path)
   bool wide;                  // materialised K/V, units of up to kWideGroup targets (bf16 path)
   bool bfused;                // backward with the history projection inside the attention kernels
   int group;                  // targets per attention unit
@@ -124,9 +120,12 @@ RecordLayout record_layout(const Layout& L) {
   return R;
 }
 
-bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backward, bool with_saved, Layout* L) {
+stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backward, bool with_saved,
+                          Layout* L) {
   const int p = path_of(dims);
-  if (p < 0 || check_batch(b) != STCA_OK) return false;
+  if (p < 0) return static_cast<stca_status_t>(p);
+  const stca_status_t bst = check_batch(b);
+  if (bst != STCA_OK) return bst;
   L->path = p;
   L->d = dims->d_model;
   L->h = dims->n_heads;
@@ -136,10 +135,16 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
   L->nh = b->n_hist;
   L->nt = b->n_tgt;
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
-  L->reord = p == 1 && !with_backward && reordered_for(dims, b);
+  L->reord = false;
+  if (p == 1 && !with_backward) {
+    const int r = reordered_for(dims, b);
+    if (r < 0) return static_cast<stca_status_t>(r);
+    L->reord = r == 1;
+  }
   L->bfused = false;
-  L->wide = p == 1 && !with_backward && !L->reord && wide_groups_for(b);
-  L->chunk_blocks = chunk_blocks_for(b, device_cus(), L->reord ? 1 : 4);
+  L->wide = p == 1 && !with_backward && !L->reord && wide_groups_for(dims, b);
+  L->mat = p == 1 && !with_backward && !L->reord && (L->wide || dims->kv_form == STCA_KV_MATERIALIZE);
+  L->chunk_blocks = chunk_blocks_for(b, device_cus(), L->reord ? 1 : 4, dims->chunk_blocks);
   L->group = L->reord ? 32 / L->h : (L->wide ? kWideGroup : kTargetGroup);
   L->max_units = max_units_for(b, L->chunk_blocks, L->group);
   L->any_narrow = L->any_wide = true;
@@ -172,7 +177,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
       L->wqp = m.take(2 * n * d * d);
       L->w1p = m.take(2 * n * d * F);
       L->w2p = m.take(2 * n * d * F);
-      L->kv = (materialize_kv() || L->wide) && !L->reord ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
+      L->kv = L->mat ? m.take(2 * n * L->nblocks * kBlockTokens * 2 * d) : 0;
       if (L->reord) {
         const size_t h = L->h;
         L->un = m.take(2 * 2 * nt * h * d);  // bf16 hi and lo terms
@@ -191,7 +196,9 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     }
   } else {
     const bool bf = dims->dtype == STCA_BF16;
-    L->bfused = bf && fused_bwd_for(dims, b);
+    const int fb = fused_bwd_for(dims, b);
+    if (fb < 0) return static_cast<stca_status_t>(fb);
+    L->bfused = bf && fb == 1;
     L->kvs = L->bfused ? 0 : m.take(4 * n * nh * 2 * d);  // every layer's K | V rows, fp32
     if (L->bfused) {
       L->fwkp = m.take(2 * n * d * d);
@@ -263,7 +270,7 @@ bool make_layout(const stca_dims_t* dims, const stca_batch_t* b, int with_backwa
     }
   }
   L->total = m.off;
-  return true;
+  return STCA_OK;
 }
 
 bool saved_layout(const stca_dims_t* dims, const stca_batch_t* b, stca_saved_layout_t* s) {
@@ -328,6 +335,7 @@ stca_status_t forward_reordered(const Layout& L, const stca_batch_t* b, const vo
   f.W2P = at<char>(ws, L.w2p);
   f.WqP = at<char>(ws, L.wqp);
   f.out = out;
+  f.range = &hdr->range;
   auto state = [&](int i) -> float* {
     if (saved) return at<float>(saved, SL.s) + (size_t)i * L.nt * d;
     return at<float>(ws, (i % 2) ? L.state_b : L.state_a);
@@ -385,7 +393,7 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
     HIPCHK(fast_pack_many(pj, 6, n, st));
     HIPCHK(rec.mark("pack"));
   }
-  const bool mat = materialize_kv() || L.wide;
+  const bool mat = L.mat;
   char* kv = at<char>(ws, L.kv);
   if (mat) {
     if (L.nh > 0)
@@ -409,6 +417,7 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   f.W2P = at<char>(ws, L.w2p);
   f.WqP = at<char>(ws, L.wqp);
   f.out = out;
+  f.range = &hdr->range;
   // s^(i) lives in saved.s[i] when saving, else alternates between two buffers
   auto state = [&](int i) -> float* {
     if (saved) return at<float>(saved, SL.s) + (size_t)i * L.nt * d;
@@ -906,7 +915,7 @@ int stca_path(const stca_dims_t* dims) { return path_of(dims); }
 
 size_t stca_workspace_size(const stca_dims_t* dims, const stca_batch_t* batch, int with_backward) {
   Layout L;
-  if (!make_layout(dims, batch, with_backward, false, &L)) return 0;
+  if (make_layout(dims, batch, with_backward, false, &L) != STCA_OK) return 0;
   return L.total;
 }
 
@@ -934,7 +943,8 @@ stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch, c
   if ((batch->n_tgt > 0 && !out) || (out && !aligned16(out)) || (saved && !aligned16(saved)))
     return STCA_ERR_INVALID_ARG;
   Layout L;
-  make_layout(dims, batch, 0, saved != nullptr, &L);
+  st = make_layout(dims, batch, 0, saved != nullptr, &L);
+  if (st != STCA_OK) return st;
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
   stca_saved_layout_t SL{};
   saved_layout(dims, batch, &SL);
@@ -945,10 +955,10 @@ stca_status_t stca_forward(const stca_dims_t* dims, const stca_batch_t* batch, c
 
 int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
   Layout L;
-  if (!make_layout(dims, batch, 0, false, &L)) return -1;
+  if (make_layout(dims, batch, 0, false, &L) != STCA_OK) return -1;
   // sched, one repack launch, the initial update, then per layer
   if (L.path == 1 && L.reord) return 1 + 1 + 1 + 1 + 4 * L.n - 1;
-  if (L.path == 1) return materialize_kv() || L.wide ? 1 + 1 + 1 + 1 + 2 * L.n : 1 + 1 + 1 + 3 * L.n;
+  if (L.path == 1) return L.mat ? 1 + 1 + 1 + 1 + 2 * L.n : 1 + 1 + 1 + 3 * L.n;
   return 1 + 1 + 8 * L.n + 1;
 }
 
@@ -961,7 +971,8 @@ stca_status_t stca_forward_profiled(const stca_dims_t* dims, const stca_batch_t*
   if ((batch->n_tgt > 0 && !out) || (out && !aligned16(out)) || (saved && !aligned16(saved)) || !events)
     return STCA_ERR_INVALID_ARG;
   Layout L;
-  make_layout(dims, batch, 0, saved != nullptr, &L);
+  st = make_layout(dims, batch, 0, saved != nullptr, &L);
+  if (st != STCA_OK) return st;
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
   if (n_events < stca_forward_launch_count(dims, batch) + 1) return STCA_ERR_INVALID_ARG;
   stca_saved_layout_t SL{};
@@ -987,7 +998,8 @@ stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch, 
   for (const void* q : ptrs)
     if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
   Layout L;
-  make_layout(dims, batch, 1, true, &L);
+  st = make_layout(dims, batch, 1, true, &L);
+  if (st != STCA_OK) return st;
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
   Rec none;
   return backward_generic(L, dims->dtype == STCA_BF16, batch, hist, tgt, w, dout, dhist, dtgt, dw, ws, stream, none);
@@ -995,7 +1007,7 @@ stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch, 
 
 int stca_backward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch) {
   Layout L;
-  if (!make_layout(dims, batch, 1, true, &L)) return -1;
+  if (make_layout(dims, batch, 1, true, &L) != STCA_OK) return -1;
   // sched, prep, 4 per layer (recomputation), prep, then per layer 5 (fp32)
   // or 3 plus the two history-side products of every layer (bf16), out
   // fused: sched, prep, the initial update, 2 per layer (attention, update), prep,
@@ -1018,7 +1030,8 @@ stca_status_t stca_backward_profiled(const stca_dims_t* dims, const stca_batch_t
   for (const void* q : ptrs)
     if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
   Layout L;
-  make_layout(dims, batch, 1, true, &L);
+  st = make_layout(dims, batch, 1, true, &L);
+  if (st != STCA_OK) return st;
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
   Rec rec;
   rec.ev = events;
@@ -1030,7 +1043,7 @@ stca_status_t stca_backward_profiled(const stca_dims_t* dims, const stca_batch_t
 
 size_t stca_train_record_size(const stca_dims_t* dims, const stca_batch_t* batch) {
   Layout L;
-  if (!make_layout(dims, batch, 1, true, &L) || !L.bfused) return 0;
+  if (make_layout(dims, batch, 1, true, &L) != STCA_OK || !L.bfused) return 0;
   return record_layout(L).total;
 }
 
@@ -1042,7 +1055,8 @@ stca_status_t stca_forward_train(const stca_dims_t* dims, const stca_batch_t* ba
   if ((batch->n_tgt > 0 && !out) || (out && !aligned16(out)) || !record || !aligned16(record))
     return STCA_ERR_INVALID_ARG;
   Layout L;
-  make_layout(dims, batch, 1, true, &L);
+  st = make_layout(dims, batch, 1, true, &L);
+  if (st != STCA_OK) return st;
   if (!L.bfused) return STCA_ERR_UNSUPPORTED;
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
   Rec none;
@@ -1064,7 +1078,8 @@ stca_status_t stca_backward_record(const stca_dims_t* dims, const stca_batch_t* 
   for (const void* q : ptrs)
     if (q && !aligned16(q)) return STCA_ERR_INVALID_ARG;
   Layout L;
-  make_layout(dims, batch, 1, true, &L);
+  st = make_layout(dims, batch, 1, true, &L);
+  if (st != STCA_OK) return st;
   if (!L.bfused) return STCA_ERR_UNSUPPORTED;
   if (ws_bytes < L.total) return STCA_ERR_WORKSPACE;
   Rec none;
@@ -1076,7 +1091,8 @@ stca_status_t stca_device_status(const void* ws, hipStream_t stream) {
   WsHeader h;
   if (hipMemcpyAsync(&h, ws, sizeof(h), hipMemcpyDeviceToHost, stream) != hipSuccess) return STCA_ERR_HIP;
   if (hipStreamSynchronize(stream) != hipSuccess) return STCA_ERR_HIP;
-  return static_cast<stca_status_t>(h.status);
+  if (h.status != STCA_OK) return static_cast<stca_status_t>(h.status);
+  return h.range ? STCA_ERR_RANGE : STCA_OK;
 }
 
 const char* stca_status_string(stca_status_t s) {
@@ -1086,6 +1102,7 @@ const char* stca_status_string(stca_status_t s) {
     case STCA_ERR_UNSUPPORTED: return "unsupported shape or dtype";
     case STCA_ERR_WORKSPACE: return "workspace or saved buffer too small";
     case STCA_ERR_HIP: return "HIP runtime error";
+    case STCA_ERR_RANGE: return "an fp16 intermediate overflowed or a value was not finite";
   }
   return "unknown status";
 }

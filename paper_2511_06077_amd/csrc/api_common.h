@@ -4,7 +4,6 @@
 #pragma once
 
 #include <cstdint>
-#include <cstdlib>
 #include <cstring>
 
 #include "common.h"
@@ -31,6 +30,10 @@ inline int path_of(const stca_dims_t* d) {
   if (!d) return STCA_ERR_INVALID_ARG;
   if (d->d_model <= 0 || d->n_heads <= 0 || d->n_layers <= 0 || d->ffn_hidden <= 0 ||
       d->d_model % d->n_heads != 0 || (d->dtype != STCA_F32 && d->dtype != STCA_BF16))
+    return STCA_ERR_INVALID_ARG;
+  if (d->kv_form < STCA_KV_AUTO || d->kv_form > STCA_KV_MATERIALIZE || d->attn_form < STCA_ATTN_AUTO ||
+      d->attn_form > STCA_ATTN_REORDERED || d->bwd_form < STCA_BWD_AUTO || d->bwd_form > STCA_BWD_GENERIC ||
+      d->chunk_blocks < 0)
     return STCA_ERR_INVALID_ARG;
   const int dh = d->d_model / d->n_heads;
   if (d->ffn_hidden % 32 != 0) return STCA_ERR_UNSUPPORTED;
@@ -73,14 +76,10 @@ inline int device_cus() {
 // Chunk length (in 32-row blocks) of the split over history rows: aim at about
 // `per_cu` attention units per CU (four for the standard form; one for the
 // reordered form, whose units stream X with little work per block and whose
-// merge cost grows with the chunk count).  STCA_CHUNK_BLOCKS overrides it (a
-// tuning and testing knob: forcing small chunks exercises the partial-result
-// merge).
-inline int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu) {
-  if (const char* e = std::getenv("STCA_CHUNK_BLOCKS")) {
-    int v = std::atoi(e);
-    if (v >= 1) return v;
-  }
+// merge cost grows with the chunk count).  A positive `forced` (the caller's
+// stca_dims_t.chunk_blocks) replaces the choice.
+inline int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu, int forced) {
+  if (forced >= 1) return forced;
   const int64_t nb = ceil_div(b->n_hist, kBlockTokens);
   int64_t c = ceil_div(nb, per_cu * static_cast<int64_t>(n_cu));
   if (c < 8) c = 8;

@@ -20,6 +20,7 @@ constexpr int kWideGroup = 128;   // targets per unit of the materialised-K/V at
 constexpr int kMaxChunks = 16;    // at most this many history chunks per request
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
+constexpr float kF16Max = 65504.f;  // largest finite fp16 value
 
 // One unit of attention work: targets [t0, t0+nt) of request r against the
 // 32-row history blocks [b0, b1); rows outside [l0, l1) belong to neighbouring
@@ -33,7 +34,8 @@ struct WsHeader {
   int32_t status;    // stca_status_t recorded by the device scheduler
   int32_t n_units;   // units the scheduler emitted
   int32_t n_narrow;  // units [0, n_narrow) have at most 32 targets, the rest more
-  int32_t pad[61];
+  int32_t range;     // nonzero: an fp16 intermediate overflowed or a value was not finite
+  int32_t pad[60];
 };
 
 __device__ __forceinline__ float to_f32(float x) { return x; }

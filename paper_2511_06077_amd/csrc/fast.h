@@ -20,6 +20,7 @@ struct FastUpdate {
   void* QN;
   const void *WoP, *W1P, *W2P, *WqP;
   int tg;  // targets per workgroup: 32, or 16 to spread few targets over more CUs
+  int32_t* range;  // set to 1 when a value rounded to fp16 (or the merged attention) is not a finite fp16
 };
 
 // Repack W [n_layers][K][N] (bf16) into MFMA operand order, as bf16 or fp16.

@@ -725,6 +725,7 @@ struct UpdateArgs {
   f16x8* QN;                   // next queries
   const f16x8 *WoP, *W1P, *W2P, *WqP;  // packed (fp16), all layers
   int tg;                      // targets per workgroup (16 or 32)
+  int32_t* range;              // written 1 when a value rounded to fp16 is out of its range
 };
 
 template <int D, int NC>
@@ -743,6 +744,17 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   const int64_t t = tb + tcol;
   const bool tok = tcol < tg && t < A.n_tgt;
   auto live = [&](int row) { return row < tg && tb + row < A.n_tgt; };
+  // fp16 range check of every value this thread rounds to fp16 (and of the
+  // merged attention output, where an overflowed K or V shows as a
+  // non-finite value); NaN fails the comparison as well
+  // (a running maximum of the bits of |x| as an unsigned integer: every
+  // finite value orders below the infinity and every NaN above it, so one
+  // register remembers the largest and any non-finite value)
+  uint32_t big = 0;
+  auto chk = [&](float x) { big = max(big, __float_as_uint(fabsf(x))); };
+  auto report = [&]() {
+    if (big > __float_as_uint(kF16Max)) *A.range = 1;
+  };
 
   // fp32 result of D^T tile: lane holds dims 32w + 4hi + 8g + k for g, k < 4
   auto store_f32 = [&](float* dst, const f32x16& v) {
@@ -753,6 +765,8 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
   };
   auto put_act = [&](uint16_t* buf, int col0, const f32x16& v) {
     uint16_t* p = buf + tcol * AROW + col0 + 4 * hi;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) chk(v[i]);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
       uint2 pk;
@@ -804,7 +818,10 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       const bf16_bits* e = reinterpret_cast<const bf16_bits*>(&v);
       uint16_t* a8 = act + row * AROW + col8 * 8;
 #pragma unroll
-      for (int i = 0; i < 8; ++i) a8[i] = f16_bits(to_f32(e[i]));
+      for (int i = 0; i < 8; ++i) {
+        chk(to_f32(e[i]));
+        a8[i] = f16_bits(to_f32(e[i]));
+      }
       if (live(row)) {
         float* so = A.s_out + (tb + row) * D + col8 * 8;
 #pragma unroll
@@ -874,7 +891,10 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
       }
       uint16_t* p = act + row * AROW + j * DH + half * 16;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) p[i] = f16_bits(av[i]);
+      for (int i = 0; i < 16; ++i) {
+        chk(av[i]);
+        p[i] = f16_bits(av[i]);
+      }
     }
     __syncthreads();
     if (PF) fetch(wb, w1_tile(0));  // after the merge, whose registers it would otherwise share
@@ -934,7 +954,10 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
         }
       }
     }
-    if (ql < 0) return;
+    if (ql < 0) {
+      report();
+      return;
+    }
     put_act(act, 32 * w, s_next);  // act (u) was last read before the previous barrier
     __syncthreads();
   }
@@ -944,10 +967,13 @@ __global__ __launch_bounds__(64 * (D / 32)) void update_kernel(UpdateArgs A) {
 #pragma unroll
   for (int v = 0; v < 16; ++v) q[v] *= qs;
   if (tok) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) chk(q[v]);
     f16x8* qn = A.QN + (t * D + 32 * w) / 8;
     qn[hi] = pack8h(q, 0);
     qn[2 + hi] = pack8h(q, 8);
   }
+  report();
 }
 
 }  // namespace
@@ -1057,7 +1083,9 @@ hipError_t fast_update(int D, const FastUpdate& f, hipStream_t st) {
   A.W2P = (const f16x8*)f.W2P;
   A.WqP = (const f16x8*)f.WqP;
   A.tg = f.tg == 16 ? 16 : 32;
+  A.range = f.range;
   if (f.n_tgt == 0) return hipSuccess;
+  if (!f.range) return hipErrorInvalidValue;
   dim3 g(static_cast<unsigned>(ceil_div(f.n_tgt, A.tg)));
   const size_t lds = (size_t)32 * (D + 8) * 2 * (f.mode == 0 ? 1 : 2);
 #define STCA_UPD(DD)                                                                         \

@@ -125,6 +125,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
     hdr->n_units = static_cast<int32_t>(total < max_units ? total : max_units);
     hdr->n_narrow = static_cast<int32_t>(total_narrow < max_units ? total_narrow : max_units);
     hdr->status = (bad || total > max_units) ? STCA_ERR_INVALID_ARG : STCA_OK;
+    hdr->range = 0;  // set by later kernels of the call that find an fp16 overflow
   }
 }
 

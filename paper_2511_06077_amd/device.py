@@ -31,7 +31,9 @@ class DeviceBatch:
     buffer the backward pass needs)."""
 
     def __init__(self, b: Batch, device="cuda", keep_saved: bool = False, backward: bool = False,
-                 host_offsets: bool = True):
+                 host_offsets: bool = True, **forms):
+        """forms: kv, attn, bwd (names of stca.FORMS) and chunk_blocks, passed
+        through stca_dims_t."""
         torch = _torch()
         self.b = b
         wl = b.wl
@@ -46,7 +48,7 @@ class DeviceBatch:
         self.hoff = torch.from_numpy(self.hoff_h).to(device)
         self.toff = torch.from_numpy(self.toff_h).to(device)
         self.dims = stca.dims(wl.d_model, wl.n_heads, wl.n_layers, wl.ffn_hidden,
-                              stca.STCA_BF16 if self.bf16 else stca.STCA_F32)
+                              stca.STCA_BF16 if self.bf16 else stca.STCA_F32, **forms)
         self.batch = stca.batch(b.n_requests, b.n_hist, b.n_tgt_total, self.hoff, self.toff,
                                 self.hoff_h if host_offsets else None, self.toff_h if host_offsets else None)
         self.weights = stca.weights(*(self.w[k] for k in WEIGHT_NAMES))
@@ -129,7 +131,7 @@ class PaperDeviceBatch:
     """A batch with paper-exact weights on the GPU, for stca_forward_paper."""
 
     def __init__(self, b: Batch, weights: dict, device="cuda", keep_saved: bool = False,
-                 host_offsets: bool = True):
+                 host_offsets: bool = True, chunk_blocks: int = 0):
         torch = _torch()
         self.b = b
         wl = b.wl
@@ -144,7 +146,7 @@ class PaperDeviceBatch:
         self.hoff = torch.from_numpy(self.hoff_h).to(device)
         self.toff = torch.from_numpy(self.toff_h).to(device)
         self.dims = stca.dims(wl.d_model, wl.n_heads, wl.n_layers, wl.ffn_hidden,
-                              stca.STCA_BF16 if self.bf16 else stca.STCA_F32)
+                              stca.STCA_BF16 if self.bf16 else stca.STCA_F32, chunk_blocks=chunk_blocks)
         self.batch = stca.batch(b.n_requests, b.n_hist, b.n_tgt_total, self.hoff, self.toff,
                                 self.hoff_h if host_offsets else None, self.toff_h if host_offsets else None)
         self.weights = stca.paper_weights(**self.w)

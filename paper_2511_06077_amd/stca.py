@@ -14,7 +14,17 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(PKG, "libstca.so")
 
 STCA_OK, STCA_ERR_INVALID_ARG, STCA_ERR_UNSUPPORTED, STCA_ERR_WORKSPACE, STCA_ERR_HIP = 0, -1, -2, -3, -4
+STCA_ERR_RANGE = -5
 STCA_F32, STCA_BF16 = 0, 1
+# execution forms (stca_dims_t.kv_form / attn_form / bwd_form); 0 = automatic
+STCA_KV_AUTO, STCA_KV_FUSED, STCA_KV_MATERIALIZE = 0, 1, 2
+STCA_ATTN_AUTO, STCA_ATTN_STANDARD, STCA_ATTN_REORDERED = 0, 1, 2
+STCA_BWD_AUTO, STCA_BWD_FUSED, STCA_BWD_GENERIC = 0, 1, 2
+FORMS = {
+    "kv": {"auto": STCA_KV_AUTO, "fused": STCA_KV_FUSED, "materialize": STCA_KV_MATERIALIZE},
+    "attn": {"auto": STCA_ATTN_AUTO, "standard": STCA_ATTN_STANDARD, "reordered": STCA_ATTN_REORDERED},
+    "bwd": {"auto": STCA_BWD_AUTO, "fused": STCA_BWD_FUSED, "generic": STCA_BWD_GENERIC},
+}
 
 EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca_forward", "stca_backward",
             "stca_device_status", "stca_status_string", "stca_path", "stca_forward_launch_count",
@@ -28,7 +38,8 @@ PAPER_WEIGHT_FIELDS = ("ffn_u", "ffn_v", "ffn_o", "wq", "wk", "wv", "wo", "wc", 
 
 class stca_dims_t(ctypes.Structure):
     _fields_ = [("d_model", ctypes.c_int32), ("n_heads", ctypes.c_int32), ("n_layers", ctypes.c_int32),
-                ("ffn_hidden", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+                ("ffn_hidden", ctypes.c_int32), ("dtype", ctypes.c_int32), ("kv_form", ctypes.c_int32),
+                ("attn_form", ctypes.c_int32), ("bwd_form", ctypes.c_int32), ("chunk_blocks", ctypes.c_int32)]
 
 
 class stca_batch_t(ctypes.Structure):
@@ -169,8 +180,12 @@ def _ptr(t) -> Optional[int]:
     return t.data_ptr()
 
 
-def dims(d_model: int, n_heads: int, n_layers: int, ffn_hidden: int, dtype: int) -> stca_dims_t:
-    return stca_dims_t(d_model, n_heads, n_layers, ffn_hidden, dtype)
+def dims(d_model: int, n_heads: int, n_layers: int, ffn_hidden: int, dtype: int, kv: str = "auto",
+         attn: str = "auto", bwd: str = "auto", chunk_blocks: int = 0) -> stca_dims_t:
+    """Model shape and execution forms (names as in FORMS; chunk_blocks 0 =
+    automatic)."""
+    return stca_dims_t(d_model, n_heads, n_layers, ffn_hidden, dtype, FORMS["kv"][kv], FORMS["attn"][attn],
+                       FORMS["bwd"][bwd], chunk_blocks)
 
 
 def batch(n_requests: int, n_hist: int, n_tgt: int, hist_off, tgt_off, hist_off_host=None,

@@ -44,9 +44,10 @@ GOOD_DIMS = dict(d_model=256, n_heads=8, n_layers=4, ffn_hidden=1024, dtype=stca
 
 
 def dims(**kw):
+    forms = {k: kw.pop(k) for k in ("kv", "attn", "bwd", "chunk_blocks") if k in kw}
     a = dict(GOOD_DIMS)
     a.update(kw)
-    return stca.dims(a["d_model"], a["n_heads"], a["n_layers"], a["ffn_hidden"], a["dtype"])
+    return stca.dims(a["d_model"], a["n_heads"], a["n_layers"], a["ffn_hidden"], a["dtype"], **forms)
 
 
 def fake_weights():
@@ -128,20 +129,17 @@ def test_saved_layout_is_disjoint_and_sized():
     assert lay.total == stca.stca_saved_size(dims(), b)
 
 
-def test_materialized_kv_needs_workspace_for_every_layer(monkeypatch):
+def test_materialized_kv_needs_workspace_for_every_layer():
     b, keep = fake_batch([0, 40, 100], [0, 3, 9])
     fused = stca.stca_workspace_size(dims(), b)
-    monkeypatch.setenv("STCA_KV", "materialize")
-    mat = stca.stca_workspace_size(dims(), b)
+    mat = stca.stca_workspace_size(dims(kv="materialize"), b)
     assert mat >= fused + 2 * 4 * 128 * 2 * 256  # 100 rows -> 4 blocks of 32, K and V, 4 layers, fp16
 
 
-def test_reordered_form_selection(monkeypatch):
+def test_reordered_form_selection():
     """Requests with at most 32 / h targets (host offsets known) run the
     reordered attention: its launch sequence is 3 + 4 n launches against the
     standard form's 3 + 3 n."""
-    monkeypatch.delenv("STCA_ATTN", raising=False)
-    monkeypatch.delenv("STCA_KV", raising=False)
     n = GOOD_DIMS["n_layers"]
     small, keep1 = fake_batch([0, 40, 100, 101], [0, 4, 5, 8])   # m = 4, 1, 3 <= 32 / 8
     wide, keep2 = fake_batch([0, 40, 100], [0, 5, 9])            # m = 5
@@ -150,32 +148,33 @@ def test_reordered_form_selection(monkeypatch):
     assert stca.stca_forward_launch_count(dims(d_model=128, n_heads=4), wide) == 3 + 4 * n  # 32 / 4 = 8
     nohost = stca.batch(3, 101, 8, 0x10000, 0x20000, None, None)
     assert stca.stca_forward_launch_count(dims(), nohost) == 3 + 3 * n
-    monkeypatch.setenv("STCA_ATTN", "standard")
-    assert stca.stca_forward_launch_count(dims(), small) == 3 + 3 * n
+    assert stca.stca_forward_launch_count(dims(attn="standard"), small) == 3 + 3 * n
+    assert stca.stca_forward_launch_count(dims(attn="reordered"), small) == 3 + 4 * n
+    # asking for the reordered form where it does not apply is unsupported
+    assert stca.stca_forward_launch_count(dims(attn="reordered"), wide) == -1
+    assert call_forward(dims(attn="reordered"), wide) == stca.STCA_ERR_UNSUPPORTED
+    assert stca.stca_workspace_size(dims(attn="reordered"), wide) == 0
 
 
-def test_wide_groups_selection(monkeypatch):
+def test_wide_groups_selection():
     """A request with more than 64 targets switches the bf16 path to K/V
-    written once (4 + 2 n launches); STCA_KV=fused keeps the fused form."""
-    monkeypatch.delenv("STCA_ATTN", raising=False)
-    monkeypatch.delenv("STCA_KV", raising=False)
+    written once (4 + 2 n launches); kv_form STCA_KV_FUSED keeps the fused form."""
     n = GOOD_DIMS["n_layers"]
     many, keep = fake_batch([0, 400, 500], [0, 65, 70])
     few, keep2 = fake_batch([0, 400, 500], [0, 64, 70])
     assert stca.stca_forward_launch_count(dims(), many) == 4 + 2 * n
     assert stca.stca_forward_launch_count(dims(), few) == 3 + 3 * n
-    monkeypatch.setenv("STCA_KV", "fused")
-    assert stca.stca_forward_launch_count(dims(), many) == 3 + 3 * n
+    assert stca.stca_forward_launch_count(dims(kv="fused"), many) == 3 + 3 * n
+    assert stca.stca_forward_launch_count(dims(kv="materialize"), few) == 4 + 2 * n
 
 
-def test_fused_backward_selection(monkeypatch):
+def test_fused_backward_selection():
     """The bf16 backward keeps K | V inside its attention kernels (7 + 5 n
     phases, no K|V product per layer) when the host offsets show at most 32
     targets per request; more targets, no host offsets, fp32 storage, an FFN
-    width that is not a multiple of d or STCA_BWD=generic take the K|V product and the exact fp32 attention
+    width that is not a multiple of d or bwd_form STCA_BWD_GENERIC take the K|V product and the exact fp32 attention
     (6 + 7 n, 4 + 9 n for fp32), and only that form sizes the fp32 K|V
     buffer of every layer into the workspace."""
-    monkeypatch.delenv("STCA_BWD", raising=False)
     n = GOOD_DIMS["n_layers"]
     small, keep1 = fake_batch([0, 40, 100, 101], [0, 32, 33, 40])   # m = 32, 1, 7
     big, keep2 = fake_batch([0, 40, 100], [0, 33, 40])               # m = 33
@@ -196,12 +195,41 @@ def test_fused_backward_selection(monkeypatch):
     long, keep3 = fake_batch([0, 60000, 100000], [0, 32, 40])
     d, F = GOOD_DIMS["d_model"], GOOD_DIMS["ffn_hidden"]
     fused = stca.stca_workspace_size(dims(), long, True)
-    monkeypatch.setenv("STCA_BWD", "generic")
-    assert stca.stca_backward_launch_count(dims(), small) == 6 + 7 * n
-    generic = stca.stca_workspace_size(dims(), long, True)
+    assert stca.stca_backward_launch_count(dims(bwd="generic"), small) == 6 + 7 * n
+    assert stca.stca_backward_launch_count(dims(bwd="fused"), small) == 7 + 5 * n
+    assert stca.stca_backward_launch_count(dims(bwd="fused"), big) == -1  # unsupported there
+    assert stca.stca_workspace_size(dims(bwd="fused"), big, True) == 0
+    generic = stca.stca_workspace_size(dims(bwd="generic"), long, True)
     # the fp32 K|V of every layer and the bf16 transposed copies of X and of
     # every layer's dK|dV, less the fused form's packed weights (W_K, W_V,
     # W_O, W_Q, W_O^T; W_1, W_2, W_1^T, W_2^T) and bf16 copies of a, u, h, s
     rows = 100000
     assert generic - fused >= (4 * n * rows * 2 * d + 2 * rows * d + 2 * n * 2 * d * rows
                                - 2 * n * (5 * d * d + 4 * d * F) - 2 * n * 40 * (3 * d + F))
+
+
+def test_form_fields_are_validated():
+    """Out-of-range execution forms and negative chunk lengths are invalid
+    arguments, reported by every call before anything is launched."""
+    b, keep = fake_batch([0, 40, 100], [0, 3, 9])
+    for bad in (dict(kv_form=3), dict(attn_form=-1), dict(bwd_form=7), dict(chunk_blocks=-2)):
+        d = dims()
+        for k, v in bad.items():
+            setattr(d, k, v)
+        assert stca.stca_path(d) == stca.STCA_ERR_INVALID_ARG, bad
+        assert stca.stca_workspace_size(d, b) == 0, bad
+        assert call_forward(d, b) == stca.STCA_ERR_INVALID_ARG, bad
+
+
+def test_workspace_depends_only_on_arguments(monkeypatch):
+    """Sizes and launch plans follow the arguments alone: the same (dims,
+    batch) gives the same size whatever the process environment holds, and a
+    forced chunk length changes the plan only through dims."""
+    b, keep = fake_batch([0, 4000, 10000], [0, 3, 9])
+    sizes = [stca.stca_workspace_size(dims(), b), stca.stca_workspace_size(dims(), b, True)]
+    for k in ("STCA_KV", "STCA_ATTN", "STCA_BWD", "STCA_CHUNK_BLOCKS"):
+        monkeypatch.setenv(k, "1")
+    assert [stca.stca_workspace_size(dims(), b), stca.stca_workspace_size(dims(), b, True)] == sizes
+    # chunks longer than any history: one unit per request instead of the
+    # default's chunks of 8 blocks
+    assert stca.stca_workspace_size(dims(chunk_blocks=1000), b) < sizes[0]

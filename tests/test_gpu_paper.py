@@ -11,7 +11,7 @@ import pytest
 
 from oracle import stca_paper_oracle as P
 from paper_2511_06077_amd import workload as W
-from test_gpu_forward import TOL, rowerr
+from test_gpu_forward import LSE_ABS, LSE_REL, TOL, rowerr
 
 pytestmark = pytest.mark.gpu
 
@@ -23,19 +23,9 @@ def torch():
     return t
 
 
-@pytest.fixture
-def chunk_override(monkeypatch):
-    def set_(v):
-        if v is None:
-            monkeypatch.delenv("STCA_CHUNK_BLOCKS", raising=False)
-        else:
-            monkeypatch.setenv("STCA_CHUNK_BLOCKS", str(v))
-    return set_
-
-
-def run_paper(torch, b, weights, keep_saved=True, host_offsets=True):
+def run_paper(torch, b, weights, keep_saved=True, host_offsets=True, chunk_blocks=0):
     from paper_2511_06077_amd.device import PaperDeviceBatch
-    db = PaperDeviceBatch(b, weights, keep_saved=keep_saved, host_offsets=host_offsets)
+    db = PaperDeviceBatch(b, weights, keep_saved=keep_saved, host_offsets=host_offsets, chunk_blocks=chunk_blocks)
     z = db.forward()
     torch.cuda.synchronize()
     out = {"z": z.float().cpu().numpy().astype(np.float64)}
@@ -63,9 +53,12 @@ def check(b, weights, got, tol, tgt_rows=None, hist_rows=None, requests=None):
         e["o"] = max(rowerr(got["o"][tgt_rows, i], ref["o"][i]) for i in range(M))
         e["xt"] = max(rowerr(got["xt"][i][hist_rows], ref["xt"][i]) for i in range(M))
         e["lse"] = float(np.abs(got["lse"][:, tgt_rows] - ref["lse"]).max()) if ref["lse"].size else 0.0
-    print(f"[paper parity] {b.wl.name}: " + " ".join(f"err({k})={v:.2e}" for k, v in e.items()), flush=True)
+    dt = "f32" if tol < 1e-3 else "bf16"
+    lse_bar = max(LSE_ABS[dt], LSE_REL[dt] * float(np.abs(ref["lse"]).max())) if ref["lse"].size else 0.0
+    print(f"[paper parity] {b.wl.name}: " + " ".join(f"err({k})={v:.2e}" for k, v in e.items())
+          + f" (lse bar {lse_bar:.1e})", flush=True)
     for k, v in e.items():
-        assert v <= (50 * tol if k == "lse" else tol), (k, v)
+        assert v <= (lse_bar if k == "lse" else tol), (k, v)
 
 
 EDGE_L = [1, 7, 31, 32, 33, 63, 65, 200, 1023, 1, 40, 64, 129]
@@ -75,15 +68,14 @@ EDGE_M = [1, 17, 0, 64, 33, 32, 1, 15, 2, 0, 31, 16, 70]
 @pytest.mark.parametrize("dtype,d,h,n,F", [("bf16", 256, 8, 2, 1024), ("bf16", 128, 4, 3, 512),
                                            ("bf16", 64, 2, 1, 256), ("f32", 64, 2, 2, 256),
                                            ("f32", 32, 2, 3, 64)])
-@pytest.mark.parametrize("chunk", [None, 1])
-def test_paper_edge_parity(torch, chunk_override, dtype, d, h, n, F, chunk):
+@pytest.mark.parametrize("chunk", [0, 1])
+def test_paper_edge_parity(torch, dtype, d, h, n, F, chunk):
     """Ragged tails (history lengths not multiples of 32, 0..70 targets per
     request, empty target segments) on both kernel families."""
-    chunk_override(chunk)
     b = W.make_custom_batch("paper_edge", EDGE_L, EDGE_M, d_model=d, n_heads=h, n_layers=n, dtype=dtype, seed=61)
     b.wl = W.Workload(b.wl.name, b.wl.n_requests, d, h, n, dtype, b.wl.seed, ffn_mult=F // d)
     weights = W.make_paper_weights(b.wl)
-    got, db = run_paper(torch, b, weights)
+    got, db = run_paper(torch, b, weights, chunk_blocks=chunk)
     from paper_2511_06077_amd import stca
     assert stca.stca_path(db.dims) == (1 if dtype == "bf16" else 0)
     check(b, weights, got, TOL[dtype])
@@ -103,8 +95,9 @@ def test_paper_device_offsets(torch):
 
 def test_paper_headline_shape_sampled(torch):
     """128 requests x 32 targets, L = 10240, d = 256, 8 heads, 4 layers, r = 4
-    (bf16), in the benchmark's launch configuration; the oracle checks two
-    sampled requests (requests are independent)."""
+    (bf16), in the benchmark's launch configuration; the oracle checks a
+    seeded sample of 16 requests (requests are independent), on every saved
+    tensor including the transformed histories."""
     from paper_2511_06077_amd.device import PaperDeviceBatch
     wl = W.WORKLOADS[W.HEADLINE]
     b = W.make_batch(wl)
@@ -112,14 +105,14 @@ def test_paper_headline_shape_sampled(torch):
     db = PaperDeviceBatch(b, weights, keep_saved=True)
     z = db.forward()
     torch.cuda.synchronize()
+    req = np.sort(np.random.default_rng(6).choice(wl.n_requests, 16, replace=False))
+    trow = torch.from_numpy(np.concatenate([np.arange(b.tgt_off[r], b.tgt_off[r + 1]) for r in req])).cuda()
+    hrow = torch.from_numpy(np.concatenate([np.arange(b.hist_off[r], b.hist_off[r + 1]) for r in req])).cuda()
     np64 = lambda x: x.float().cpu().numpy().astype(np.float64)  # noqa: E731
-    for r in (5, 127):
-        t0, t1 = int(b.tgt_off[r]), int(b.tgt_off[r + 1])
-        h0, h1 = int(b.hist_off[r]), int(b.hist_off[r + 1])
-        got = {"z": np64(z[t0:t1]), "q": np64(db.saved_tensor("q")[:, t0:t1]),
-               "a": np64(db.saved_tensor("a")[:, t0:t1]), "o": np64(db.saved_tensor("o")[t0:t1]),
-               "lse": np64(db.saved_tensor("lse")[:, t0:t1]), "xt": np64(db.saved_tensor("xt")[:, h0:h1])}
-        check(b, weights, got, TOL["bf16"], tgt_rows=slice(None), hist_rows=slice(None), requests=[r])
+    got = {"z": np64(z[trow]), "q": np64(db.saved_tensor("q")[:, trow]), "a": np64(db.saved_tensor("a")[:, trow]),
+           "o": np64(db.saved_tensor("o")[trow]), "lse": np64(db.saved_tensor("lse")[:, trow]),
+           "xt": np64(db.saved_tensor("xt")[:, hrow])}
+    check(b, weights, got, TOL["bf16"], tgt_rows=slice(None), hist_rows=slice(None), requests=req)
 
 
 def test_paper_profiled_labels(torch):

@@ -21,17 +21,6 @@ def torch():
     return t
 
 
-@pytest.fixture
-def env(monkeypatch):
-    def set_(**kv):
-        for k, v in kv.items():
-            if v is None:
-                monkeypatch.delenv(k, raising=False)
-            else:
-                monkeypatch.setenv(k, str(v))
-    return set_
-
-
 def small_m(cap, n):
     """Target counts 0..cap cycling over n requests (every count appears)."""
     return [i % (cap + 1) for i in range(n)]
@@ -41,37 +30,33 @@ HIST = [1, 7, 31, 32, 33, 65, 300, 1023, 40, 129]
 
 
 @pytest.mark.parametrize("d,h", [(256, 8), (128, 4), (64, 2)])
-@pytest.mark.parametrize("chunk", [None, 1, 3])
-def test_reordered_parity(torch, env, d, h, chunk):
-    env(STCA_CHUNK_BLOCKS=chunk, STCA_ATTN=None)
+@pytest.mark.parametrize("chunk", [0, 1, 3])
+def test_reordered_parity(torch, d, h, chunk):
     cap = 32 // h
     b = W.make_custom_batch("reord", HIST, small_m(cap, len(HIST)), d_model=d, n_heads=h, n_layers=2,
                             dtype="bf16", seed=31)
-    y, a, lse, db = run_gpu(torch, b)
+    y, a, lse, db = run_gpu(torch, b, attn="reordered", chunk_blocks=chunk)
     from paper_2511_06077_amd import stca
     assert stca.stca_forward_launch_count(db.dims, db.batch) == 3 + 4 * 2  # the reordered sequence ran
     check_against_oracle(b, y, a, lse, TOL["bf16"])
 
 
-def test_reordered_matches_standard(torch, env):
+def test_reordered_matches_standard(torch):
     b = W.make_custom_batch("reord_vs_std", [2048, 513, 96, 1], [4, 1, 3, 2], d_model=256, n_heads=8, n_layers=3,
                             dtype="bf16", seed=32)
-    env(STCA_ATTN=None)
-    y, a, lse, _ = run_gpu(torch, b)
-    env(STCA_ATTN="standard")
-    ys, as_, lses, _ = run_gpu(torch, b)
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered")
+    ys, as_, lses, _ = run_gpu(torch, b, attn="standard")
     e_y, e_a = rowerr(y, ys), max(rowerr(a[i], as_[i]) for i in range(3))
     print(f"[reord] reordered vs standard: err(Y)={e_y:.2e} err(a)={e_a:.2e}")
     assert e_y <= TOL["bf16"] and e_a <= TOL["bf16"]
     check_against_oracle(b, y, a, lse, TOL["bf16"])
 
 
-def test_reordered_single_history_item(torch, env):
+def test_reordered_single_history_item(torch):
     """P1: L = 1 makes a^(i) the layer's V row whatever the scores."""
-    env(STCA_ATTN=None)
     b = W.make_custom_batch("reord_l1", [1, 1, 1], [4, 1, 2], d_model=256, n_heads=8, n_layers=2, dtype="bf16",
                             seed=33)
-    y, a, lse, _ = run_gpu(torch, b)
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered")
     f = b.f64()
     for r in range(3):
         t0, t1 = b.tgt_off[r], b.tgt_off[r + 1]
@@ -80,12 +65,11 @@ def test_reordered_single_history_item(torch, env):
             assert rowerr(a[i, t0:t1], np.broadcast_to(v, (t1 - t0, v.size))) <= TOL["bf16"]
 
 
-def test_reordered_zero_scores(torch, env):
+def test_reordered_zero_scores(torch):
     """P2: W_Q = 0 gives the mean of V and lse = log L."""
-    env(STCA_ATTN=None)
     b = W.make_custom_batch("reord_zq", [100, 37], [3, 4], d_model=256, n_heads=8, n_layers=2, dtype="bf16", seed=34)
     b.weights["wq"][:] = 0
-    y, a, lse, _ = run_gpu(torch, b)
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered")
     f = b.f64()
     for r in range(2):
         X = f["hist"][b.hist_off[r]:b.hist_off[r + 1]]
@@ -96,20 +80,19 @@ def test_reordered_zero_scores(torch, env):
             np.testing.assert_allclose(lse[i, t0:t1], np.log(X.shape[0]), atol=1e-3)
 
 
-def test_reordered_peaked(torch, env):
-    env(STCA_CHUNK_BLOCKS=2, STCA_ATTN=None)
+def test_reordered_peaked(torch):
+    """W_Q scaled by 8 (near one-hot attention, large running-maximum jumps)."""
     b = W.make_custom_batch("reord_peak", [300, 129, 77], [2, 4, 1], d_model=256, n_heads=8, n_layers=2,
-                            dtype="bf16", seed=35, scale_q=1.5)
-    y, a, lse, _ = run_gpu(torch, b)
+                            dtype="bf16", seed=35, scale_q=8.0)
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered", chunk_blocks=2)
     check_against_oracle(b, y, a, lse, TOL["bf16"])
 
 
-def test_reordered_repeat_bitwise(torch, env):
-    env(STCA_ATTN=None)
+def test_reordered_repeat_bitwise(torch):
     b = W.make_custom_batch("reord_rep", [700, 65, 1], [1, 4, 2], d_model=256, n_heads=8, n_layers=2, dtype="bf16",
                             seed=36)
     from paper_2511_06077_amd.device import DeviceBatch
-    db = DeviceBatch(b)
+    db = DeviceBatch(b, attn="reordered")
     y1 = db.forward().clone()
     y2 = db.forward().clone()
     torch.cuda.synchronize()
