@@ -209,6 +209,24 @@ stca_status_t stca_backward(const stca_dims_t* dims, const stca_batch_t* batch,
                             const stca_wgrads_t* dw, void* ws, size_t ws_bytes,
                             hipStream_t stream);
 
+/* Forward without a workspace argument, for callers that cannot allocate
+ * device memory (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid allocation).  The same computation and results as
+ * stca_forward, with the workspace in a device array of the library of
+ * STCA_NOALLOC_SCRATCH_BYTES bytes, one per GPU, set up on the first call on
+ * that GPU (with it current) and held until the process ends; nothing is
+ * allocated by any call.  Returns STCA_ERR_WORKSPACE, before anything is
+ * launched, when stca_workspace_size(dims, batch, 0) exceeds that size; other
+ * errors as stca_forward.  Every call on a GPU uses that GPU's one array:
+ * calls that may overlap on the same GPU (other streams, other threads) race
+ * and must be serialised by the caller.  Nothing in the array needs to start
+ * at zero; the device-side status of such a call (stca_device_status) is not
+ * readable, so give host offsets to have them checked. */
+#define STCA_NOALLOC_SCRATCH_BYTES ((size_t)256 << 20)
+stca_status_t stca_forward_noalloc(const stca_dims_t* dims, const stca_batch_t* batch, const void* hist,
+                                   const void* tgt, const stca_weights_t* w, void* out, void* saved,
+                                   hipStream_t stream);
+
 /* Training step in two calls, for batches the fused backward takes (bf16,
  * d_h = 32, FFN width a multiple of d, host offsets showing at most 32
  * targets per request): the forward writes, besides out, a training record

@@ -32,7 +32,8 @@ EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca
             "stca_sl_beta", "stca_sl_sample", "stca_sl_allocate", "stca_sl_pack",
             "stca_paper_workspace_size", "stca_paper_saved_size", "stca_paper_saved_layout", "stca_forward_paper",
             "stca_paper_launch_count", "stca_forward_paper_profiled", "stca_train_record_size", "stca_forward_train",
-            "stca_backward_record")
+            "stca_backward_record", "stca_forward_noalloc")
+NOALLOC_SCRATCH_BYTES = 256 << 20  # STCA_NOALLOC_SCRATCH_BYTES
 PAPER_WEIGHT_FIELDS = ("ffn_u", "ffn_v", "ffn_o", "wq", "wk", "wv", "wo", "wc", "wz", "z_u", "z_v", "z_o")
 
 
@@ -137,6 +138,9 @@ def lib():
                                            P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                            ctypes.c_void_p, P(stca_wgrads_t), ctypes.c_void_p, ctypes.c_size_t,
                                            ctypes.c_void_p]
+        L.stca_forward_noalloc.restype = ctypes.c_int
+        L.stca_forward_noalloc.argtypes = [P(stca_dims_t), P(stca_batch_t), ctypes.c_void_p, ctypes.c_void_p,
+                                           P(stca_weights_t), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
         I32P = P(ctypes.c_int32)
         L.stca_sl_beta.restype = ctypes.c_double
         L.stca_sl_beta.argtypes = [ctypes.c_double, ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
@@ -241,6 +245,16 @@ def stca_backward(d, b, hist, tgt, w, dout, dhist, dtgt, dw, ws, ws_bytes: int, 
                              _ptr(stream))
     if check and st != STCA_OK:
         raise StcaError(st, "stca_backward")
+    return st
+
+
+def stca_forward_noalloc(d, b, hist, tgt, w, out, saved, stream=None, check: bool = True) -> int:
+    """stca_forward with the library's own per-GPU scratch array as the
+    workspace (no workspace argument, nothing allocated)."""
+    st = lib().stca_forward_noalloc(ctypes.byref(d), ctypes.byref(b), _ptr(hist), _ptr(tgt), ctypes.byref(w),
+                                    _ptr(out), _ptr(saved), _ptr(stream))
+    if check and st != STCA_OK:
+        raise StcaError(st, "stca_forward_noalloc")
     return st
 
 
