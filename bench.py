@@ -4,12 +4,19 @@
 One step = one stca_forward over the whole batch (per layer: the history K/V
 projection fused into the multi-target attention, then the target update),
 inputs already resident in HBM.  Prints one JSON line: targets scored per
-second over the K timed steps, the dominant kernel against its roofline (HIP
-events recorded on the library's stream around every launch, in a second pass
-of K steps so that the events stay out of the timed region), and the fp64 CPU
-oracle timed on a bounded sample of the same workload.
+second over the K timed steps of the headline workload (128 requests x 32
+targets, L = 10240), the dominant kernel against its roofline (HIP events
+recorded on the library's stream around every launch, in a second pass of K
+steps so that the events stay out of the timed region), and the fp64 CPU
+oracle timed on a bounded sample of the same workload.  Sub-records of the
+same line: `ablation` (the headline batch in the instance-wise, non-RLB
+layout, one target per request, materialised K/V, many targets per
+request), `train_step` (forward + backward at the training window, with its
+own roofline and CPU baseline) and `configs` (every workload: throughput,
+roofline fraction and the non-RLB ablation).
 
-    python bench.py [--steps K] [--warmup W] [--workload NAME] [--ablation]
+    python bench.py [--steps K] [--warmup W] [--workload NAME] [--quick]
+                    [--backward [--sl]] [--paper]
 """
 from __future__ import annotations
 
@@ -92,9 +99,10 @@ def measured_traffic(workload: str, kernel: str):
     return None
 
 
-def cpu_baseline(wl: W.Workload, budget_s: float):
+def cpu_baseline(wl: W.Workload, budget_s: float, backward: bool = False):
     """The fp64 oracle, as it is, on requests of the same workload taken in
-    order until the time budget is spent."""
+    order until the time budget is spent: its forward, or (backward) its
+    forward and hand-derived backward (all gradients)."""
     from oracle import stca_oracle as O
     try:
         from threadpoolctl import threadpool_info
@@ -104,17 +112,22 @@ def cpu_baseline(wl: W.Workload, budget_s: float):
     L, m = W.request_shapes(wl)
     done_t, done_r, spent = 0, 0, 0.0
     for r in range(wl.n_requests):
-        sub = W.make_batch(wl, requests=[r], with_grad=False, threads=1)
+        sub = W.make_batch(wl, requests=[r], with_grad=backward, threads=1)
         inp = sub.f64()
         t0 = time.perf_counter()
-        O.forward(inp, keep=False)
+        if backward:
+            O.backward(inp, inp["grad_out"])
+        else:
+            O.forward(inp, keep=False)
         spent += time.perf_counter() - t0
         done_t += int(m[r])
         done_r += 1
         if spent >= budget_s:
             break
-    return {"value": done_t / spent, "unit": "targets/s", "cores": int(cores), "kind": "oracle",
-            "sample": f"first {done_r} of {wl.n_requests} requests of {wl.name} ({done_t} targets), "
+    what = "forward + backward" if backward else "forward"
+    return {"value": done_t / spent, "unit": "targets trained/s" if backward else "targets/s", "cores": int(cores),
+            "kind": "oracle",
+            "sample": f"{what} of the first {done_r} of {wl.n_requests} requests of {wl.name} ({done_t} targets), "
                       f"{spent:.1f} s of fp64 CPU work"}
 
 
@@ -176,19 +189,122 @@ def timed_forward(db, steps: int, warmup: int):
     return total_ms, per
 
 
+def kernel_table(per: dict, b, steps: int, es: int, peak_tf: float) -> dict:
+    """Per-kernel durations (HIP events) with their algorithmic rates."""
+    kernels = {}
+    for lab, v in per.items():
+        launches = len(v) // steps
+        ms = float(np.mean(v))
+        flop, byts = kernel_work(lab, b, es)
+        ent = {"launches_per_step": launches, "ms_per_launch": ms, "ms_per_step": ms * launches}
+        if flop or byts:
+            ent.update({"tflops": flop / (ms * 1e-3) / 1e12, "gbs": byts / (ms * 1e-3) / 1e9,
+                        "mfma_frac": flop / (ms * 1e-3) / 1e12 / peak_tf,
+                        "hbm_frac": byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS})
+        kernels[lab] = ent
+    return kernels
+
+
+def design_bound_ms(b, es: int, peak_tf: float) -> float:
+    """The fused design's own bound: per layer X read once and the K/V
+    projection plus attention at the matrix-core peak (K and V never reach
+    HBM), plus the target update at peak."""
+    wl = b.wl
+    L = b.hist_len[b.n_tgt > 0].astype(np.float64)
+    m = b.n_tgt[b.n_tgt > 0].astype(np.float64)
+    dm = wl.d_model
+    c = accounting.stage_costs(b.hist_len, b.n_tgt, dm, wl.n_layers, es)
+    fused_flop = wl.n_layers * (4.0 * L.sum() * dm * dm + 4.0 * (m * L).sum() * dm)
+    fused_bytes = wl.n_layers * es * L.sum() * dm
+    return (max(fused_flop / (peak_tf * 1e12), fused_bytes / (PEAK_HBM_GBS * 1e9))
+            + c["update"]["flop"] / (peak_tf * 1e12)) * 1e3
+
+
+def measure_forward(db, steps: int, warmup: int, settle_s: float, events: bool = True) -> dict:
+    """Settling steps, W warm-up steps, K timed plain steps (the value), then
+    (events) K more steps with a HIP event around every launch for the
+    per-kernel table and the dominant kernel's roofline."""
+    b, wl = db.b, db.b.wl
+    es = 2 if wl.dtype == "bf16" else 4
+    peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
+    n_settle = settle(db.forward, settle_s) if settle_s > 0 else 0
+    ms = plain_forward(db, steps, warmup) / steps
+    out = {"workload": wl.name, "requests": int(b.n_requests), "targets": int(b.n_tgt_total),
+           "history_rows": int(b.n_hist), "ms_per_step": ms, "targets_per_s": b.n_tgt_total / (ms * 1e-3),
+           "settle_steps": n_settle, "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
+    if not events:
+        return out
+    ev_total, per = timed_forward(db, steps, 1)
+    kernels = kernel_table(per, b, steps, es, peak_tf)
+    dom = max((k for k in kernels if kernel_work(k, b, es) != (0.0, 0.0)), key=lambda k: kernels[k]["ms_per_step"])
+    flop, byts = kernel_work(dom, b, es)
+    roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, peak_tf)
+    roof["kernel"] = dom
+    roof["traffic"] = measured_traffic(wl.name, dom)
+    c = accounting.stage_costs(b.hist_len, b.n_tgt, wl.d_model, wl.n_layers, es)
+    path_ms = sum(max(v["flop"] / (peak_tf * 1e12), v["bytes"] / (PEAK_HBM_GBS * 1e9)) for v in c.values()) * 1e3
+    dms = design_bound_ms(b, es, peak_tf)
+    out.update({"roofline": roof, "kernels": kernels, "ms_per_step_with_kernel_events": ev_total / steps,
+                "path_roofline": {"ms": path_ms, "frac": path_ms / ms,
+                                  "targets_per_s": b.n_tgt_total / (path_ms * 1e-3)},
+                "fused_design_roofline": {"ms": dms, "frac": dms / ms,
+                                          "targets_per_s": b.n_tgt_total / (dms * 1e-3)}})
+    return out
+
+
+def instance_wise(db, backward: bool = False, **forms):
+    """The same samples in the instance-wise layout of App. A.3: every target
+    becomes a request of its own carrying a copy of its request's history
+    (the non-RLB layout, history re-encoded per target).  Built on the GPU by
+    a row gather from the request-level batch; targets (and upstream
+    gradients) keep their order."""
+    import torch
+    from paper_2511_06077_amd.device import DeviceBatch
+    b = db.b
+    reps = b.n_tgt.astype(np.int64)
+    L = np.repeat(b.hist_len.astype(np.int64), reps)
+    ones = np.ones(int(reps.sum()), dtype=np.int64)
+    hoff = W.offsets(L)
+    shift = np.repeat(b.hist_off[:-1].astype(np.int64), reps) - hoff[:-1].astype(np.int64)
+    dev = db.device
+    idx = torch.arange(int(hoff[-1]), device=dev, dtype=torch.int64)
+    idx += torch.repeat_interleave(torch.from_numpy(shift).to(dev), torch.from_numpy(L).to(dev))
+    hist = db.hist.index_select(0, idx)
+    del idx
+    nb = W.Batch(b.wl, np.repeat(b.requests, reps), L, ones, hoff, W.offsets(ones), None, None, b.weights, None)
+    return DeviceBatch.from_tensors(nb, hist, db.tgt, db.w, device=dev, backward=backward, **forms)
+
+
+def non_rlb_forward(db, steps: int) -> dict:
+    """The instance-wise layout of the same batch, timed with the same
+    kernels (standard attention form) and with the form chosen automatically
+    (one target per request: the reordered attention)."""
+    import torch
+    out = {}
+    for key, attn in (("standard_form", "standard"), ("auto_form", "auto")):
+        nb = instance_wise(db, attn=attn)
+        ms = plain_forward(nb, steps, 2) / steps
+        out[key] = {"requests": int(nb.b.n_requests), "history_rows": int(nb.b.n_hist), "ms_per_step": ms,
+                    "targets_per_s": nb.b.n_tgt_total / (ms * 1e-3),
+                    "launches": stca.stca_forward_launch_count(nb.dims, nb.batch)}
+        del nb
+        torch.cuda.empty_cache()
+    return out
+
+
 def main() -> int:
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default=W.HEADLINE, choices=sorted(W.WORKLOADS))
-    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget (0: skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0, help="oracle time budget per baseline (0: skip)")
     ap.add_argument("--settle-seconds", type=float, default=1.0,
                     help="untimed steps for this long before the warm-up (GPU clock ramp)")
-    ap.add_argument("--ablation", action="store_true",
-                    help="also time one target per request and the instance-wise (non-RLB) layout")
+    ap.add_argument("--quick", action="store_true",
+                    help="only the headline record (no ablation, training-step or per-config sub-records)")
     ap.add_argument("--backward", action="store_true",
-                    help="time forward + backward steps (the training window workload by default)")
+                    help="instead: forward + backward steps (the training window workload by default)")
     ap.add_argument("--sl", action="store_true",
                     help="with --backward: a stochastic-length batch (Beta lengths, alpha 0.02, L_avg 2048 of 10240)")
     ap.add_argument("--paper", action="store_true",
@@ -207,7 +323,11 @@ def main() -> int:
     if args.copy_gib > 0:
         return copy_calibration(args)
     if args.backward:
-        return train_step(args)
+        rec = train_record(args, W.WORKLOADS[args.workload if args.workload != W.HEADLINE
+                                             else "train_bf16_R256_m16_L2048_d256"], args.steps, args.warmup,
+                           sl=args.sl)
+        print(json.dumps(rec), flush=True)
+        return 0
     if args.paper:
         return paper_step(args)
     from paper_2511_06077_amd.device import DeviceBatch
@@ -217,51 +337,17 @@ def main() -> int:
     log(f"[bench] generated {wl.name}: {b.n_hist} history rows, {b.n_tgt_total} targets ({time.time() - t0:.1f} s)")
     db = DeviceBatch(b, device="cuda:0")
     log(f"[bench] workspace {db.ws_bytes / 2**30:.2f} GiB; path {stca.stca_path(db.dims)}")
-    n_settle = settle(db.forward, args.settle_seconds)
-    log(f"[bench] {n_settle} settling steps")
-    # the timed region: W warm-up steps, then exactly K plain steps
-    ms_step = plain_forward(db, args.steps, args.warmup) / args.steps
-    # per-kernel durations: the same K steps again with a HIP event recorded
-    # on the library's stream around every launch (the events themselves add
-    # a few microseconds per launch, so they stay out of the timed region)
-    ev_total_ms, per = timed_forward(db, args.steps, 1)
-    ev_ms = ev_total_ms / args.steps
-    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step; {ev_ms:.3f} with per-kernel events")
-
-    es = 2 if wl.dtype == "bf16" else 4
-    peak_tf = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_FP32_TFLOPS
-    kernels = {}
-    for lab, v in per.items():
-        launches = len(v) // args.steps
-        ms = float(np.mean(v))
-        flop, byts = kernel_work(lab, b, es)
-        ent = {"launches_per_step": launches, "ms_per_launch": ms, "ms_per_step": ms * launches}
-        if flop or byts:
-            ent.update({"tflops": flop / (ms * 1e-3) / 1e12, "gbs": byts / (ms * 1e-3) / 1e9,
-                        "mfma_frac": flop / (ms * 1e-3) / 1e12 / peak_tf,
-                        "hbm_frac": byts / (ms * 1e-3) / 1e9 / PEAK_HBM_GBS})
-        kernels[lab] = ent
-    dom = max((k for k in kernels if kernel_work(k, b, es) != (0.0, 0.0)),
-              key=lambda k: kernels[k]["ms_per_step"])
-    flop, byts = kernel_work(dom, b, es)
-    roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, peak_tf)
-    roof["kernel"] = dom
-    roof["traffic"] = measured_traffic(wl.name, dom)
-    c = accounting.stage_costs(b.hist_len, b.n_tgt, wl.d_model, wl.n_layers, es)
-    roof_ms = sum(max(v["flop"] / (peak_tf * 1e12), v["bytes"] / (PEAK_HBM_GBS * 1e9)) for v in c.values()) * 1e3
-    # the same bound for the fused design, whose only compulsory history
-    # traffic is one read of X per layer (K and V never reach HBM)
-    L = b.hist_len[b.n_tgt > 0].astype(np.float64)
-    m = b.n_tgt[b.n_tgt > 0].astype(np.float64)
-    dm = wl.d_model
-    fused_flop = wl.n_layers * (4.0 * L.sum() * dm * dm + 4.0 * (m * L).sum() * dm)
-    fused_bytes = wl.n_layers * es * L.sum() * dm
-    design_ms = (max(fused_flop / (peak_tf * 1e12), fused_bytes / (PEAK_HBM_GBS * 1e9))
-                 + c["update"]["flop"] / (peak_tf * 1e12)) * 1e3
-    value = b.n_tgt_total / (ms_step * 1e-3)
+    # the timed region: W warm-up steps, then exactly K plain steps; per-kernel
+    # durations come from the same K steps again with a HIP event recorded on
+    # the library's stream around every launch (the events themselves add a
+    # few microseconds per launch, so they stay out of the timed region)
+    head = measure_forward(db, args.steps, args.warmup, args.settle_seconds)
+    ms_step = head["ms_per_step"]
+    log(f"[bench] {args.steps} steps: {ms_step:.3f} ms/step; {head['ms_per_step_with_kernel_events']:.3f} "
+        f"with per-kernel events")
     rec = {
         "metric": "targets scored/sec, STCA forward",
-        "value": value,
+        "value": head["targets_per_s"],
         "unit": "targets/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -276,24 +362,65 @@ def main() -> int:
                    "targets_per_request": wl.n_targets or list(wl.tgt_range),
                    "hist_len": wl.hist_len or list(wl.hist_range), "d_model": wl.d_model,
                    "heads": wl.n_heads, "layers": wl.n_layers, "ffn_hidden": wl.ffn_hidden},
-        "roofline": roof,
-        "path_roofline": {"ms": roof_ms, "frac": roof_ms / ms_step,
-                          "targets_per_s": b.n_tgt_total / (roof_ms * 1e-3)},
-        "fused_design_roofline": {"ms": design_ms, "frac": design_ms / ms_step,
-                                  "targets_per_s": b.n_tgt_total / (design_ms * 1e-3)},
-        "kernels": kernels,
-        "ms_per_step_with_kernel_events": ev_ms,
-        "settle_steps": n_settle,
+        "roofline": head["roofline"],
+        "path_roofline": head["path_roofline"],
+        "fused_design_roofline": head["fused_design_roofline"],
+        "kernels": head["kernels"],
+        "ms_per_step_with_kernel_events": head["ms_per_step_with_kernel_events"],
+        "settle_steps": head["settle_steps"],
     }
-    if args.ablation:
-        rec["ablation"] = ablation(wl, args)
+    sub_steps = max(5, args.steps // 5)
+    if not args.quick:
+        log("[bench] ablation")
+        rec["ablation"] = ablation(db, args, sub_steps)
     del db
     torch.cuda.empty_cache()
+    if not args.quick:
+        log("[bench] training step")
+        rec["train_step"] = train_record(args, W.WORKLOADS["train_bf16_R256_m16_L2048_d256"], sub_steps,
+                                         max(2, args.warmup // 2), with_non_rlb=True)
+        log("[bench] per-configuration records")
+        rec["configs"] = config_records(args, rec, sub_steps)
     if args.cpu_seconds > 0:
         log("[bench] timing the CPU oracle")
         rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds)
     print(json.dumps(rec), flush=True)
     return 0
+
+
+def config_records(args, rec: dict, steps: int) -> dict:
+    """Every workload: throughput, the dominant kernel's roofline fraction,
+    the fused design's bound, and the same batch in the instance-wise
+    (non-RLB) layout.  The headline and training-window entries restate the
+    line's own measurements."""
+    import torch
+    from paper_2511_06077_amd.device import DeviceBatch
+    out = {}
+    for name in ("tiny_f32_R4_m4_L256_d64", "uniform_bf16_R64_m16_L1024_d128",
+                 "ragged_bf16_R256_L512-10240_m1-64_d256"):
+        wl = W.WORKLOADS[name]
+        db = DeviceBatch(W.make_batch(wl, with_grad=False), device="cuda:0")
+        r = measure_forward(db, steps, 3, 0.2)
+        r.pop("kernels")
+        nr = instance_wise(db, attn="standard")
+        ms = plain_forward(nr, steps, 2) / steps
+        r["non_rlb"] = {"requests": int(nr.b.n_requests), "history_rows": int(nr.b.n_hist), "ms_per_step": ms,
+                        "targets_per_s": nr.b.n_tgt_total / (ms * 1e-3), "form": "standard attention, same kernels"}
+        r["rlb_gain"] = ms / r["ms_per_step"]
+        out[name] = r
+        del db, nr
+        torch.cuda.empty_cache()
+        log(f"[bench] {name}: {r['ms_per_step']:.3f} ms/step, non-RLB {ms:.3f} ms/step")
+    head = {k: rec[k] for k in ("ms_per_step", "roofline", "path_roofline", "fused_design_roofline")}
+    head["targets_per_s"] = rec["value"]
+    nr = rec["ablation"]["non_rlb"]["standard_form"]
+    head["non_rlb"] = dict(nr, form="standard attention, same kernels")
+    head["rlb_gain"] = nr["ms_per_step"] / rec["ms_per_step"]
+    out[rec["config"]["workload"]] = head
+    t = rec["train_step"]
+    out[t["config"]["workload"]] = dict({k: t[k] for k in ("ms_per_step", "roofline", "non_rlb", "rlb_gain")},
+                                        targets_per_s=t["value"], step="forward + backward")
+    return out
 
 
 def paper_kernel_work(label: str, b: W.Batch):
@@ -429,26 +556,28 @@ def backward_phase_work(label: str, b: W.Batch, fused: bool):
     return 0.0, 0.0, 0.0
 
 
-def train_step(args) -> int:
+def train_record(args, wl: W.Workload, steps: int, warmup: int, sl: bool = False,
+                 with_non_rlb: bool = False) -> dict:
     """Forward + backward of the training window: one step = the forward then
     the backward (all gradients) over the whole batch, inputs resident
     (stca_forward_train + stca_backward_record where the batch qualifies,
-    else stca_forward + stca_backward).  The recomputing backward's phases are
-    then timed with HIP events in a second pass."""
+    else stca_forward + stca_backward).  The phases are then timed with HIP
+    events in a pass of the recomputing backward (stca_backward_profiled),
+    whose attention-backward phase is the same kernels on the same inputs as
+    in the two-call step; that phase's roofline is the record's `roofline`.
+    The CPU baseline is the oracle's forward and hand-derived backward."""
     import torch
     from paper_2511_06077_amd.device import DeviceBatch, to_device
-    name = args.workload if args.workload != W.HEADLINE else "train_bf16_R256_m16_L2048_d256"
-    wl = W.WORKLOADS[name]
     sl_info = None
-    if args.sl:
+    if sl:
         # stochastic-length batch: full histories of L_infer = 10240 rows cut
         # to Beta-sampled temporal suffixes (alpha = 0.02, L_avg = 2048)
-        from paper_2511_06077_amd import sl
+        from paper_2511_06077_amd import sl as SL
         full_wl = W.Workload(wl.name + "_L10240", wl.n_requests, wl.d_model, wl.n_heads, wl.n_layers, wl.dtype,
                              wl.seed, hist_len=10240, n_targets=wl.n_targets, backward=True)
         t0 = time.time()
         full = W.make_batch(full_wl, with_grad=True)
-        b, sl_info = sl.sl_batch(full, wl.seed, alpha=0.02, l_min=8, l_avg=2048, l_max=10240)
+        b, sl_info = SL.sl_batch(full, wl.seed, alpha=0.02, l_min=8, l_avg=2048, l_max=10240)
         del full
         log(f"[bench] stochastic-length batch: {b.n_hist} of {wl.n_requests * 10240} rows kept "
             f"({time.time() - t0:.1f} s)")
@@ -458,59 +587,51 @@ def train_step(args) -> int:
     db = DeviceBatch(b, device="cuda:0", backward=True)
     dout = to_device(b.grad_out, "cuda:0")
 
-    # A training step: the forward then the backward over the whole batch.
-    # Batches the fused backward takes run it as stca_forward_train (which
-    # keeps a training record) and stca_backward_record; the others as
-    # stca_forward and the recomputing stca_backward.
-    use_rec = db.record is not None
+    def timed_step(dbx, k, w):
+        use_rec = dbx.record is not None
 
-    def fwd_call():
-        if use_rec:
-            db.forward_train()
-        else:
-            db.forward()
+        def fwd():
+            dbx.forward_train() if use_rec else dbx.forward()
 
-    def bwd_call():
-        db.backward(dout, use_record=use_rec)
+        def bwd():
+            dbx.backward(dout, use_record=use_rec)
+        for _ in range(w):
+            fwd()
+            bwd()
+        torch.cuda.synchronize()
+        stream = torch.cuda.current_stream()
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        # forward and backward timed separately (each backward reads the record
+        # of the last forward_train, which stays valid across backward calls)
+        e[0].record(stream)
+        for _ in range(k):
+            fwd()
+        e[1].record(stream)
+        for _ in range(k):
+            bwd()
+        e[2].record(stream)
+        torch.cuda.synchronize()
+        return e[0].elapsed_time(e[1]) / k, e[1].elapsed_time(e[2]) / k, use_rec
 
-    def step():
-        fwd_call()
-        bwd_call()
-
-    settle(step, args.settle_seconds)
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    stream = torch.cuda.current_stream()
-    e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
-    # forward and backward timed separately (each backward reads the record of
-    # the last forward_train, which stays valid across backward calls)
-    e[0].record(stream)
-    for _ in range(args.steps):
-        fwd_call()
-    e[1].record(stream)
-    for _ in range(args.steps):
-        bwd_call()
-    e[2].record(stream)
-    torch.cuda.synchronize()
-    fwd = e[0].elapsed_time(e[1]) / args.steps
-    bwd = e[1].elapsed_time(e[2]) / args.steps
+    settle(lambda: (db.forward(), db.backward(dout)), args.settle_seconds)
+    fwd, bwd, use_rec = timed_step(db, steps, warmup)
     ms = fwd + bwd
+    stream = torch.cuda.current_stream()
     # the recomputing backward (what stca_backward alone costs), for reference
     e2 = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
     e2[0].record(stream)
-    for _ in range(args.steps):
+    for _ in range(steps):
         db.backward(dout)
     e2[1].record(stream)
     torch.cuda.synchronize()
-    bwd_recompute = e2[0].elapsed_time(e2[1]) / args.steps
+    bwd_recompute = e2[0].elapsed_time(e2[1]) / steps
     # phases of the recomputing backward (stca_backward_profiled), timed on
     # the library's stream
     g = db.backward(dout)
     dw = stca.wgrads(g["dwq"], g["dwk"], g["dwv"], g["dwo"], g["dw1"], g["dw2"])
     nl = stca.stca_backward_launch_count(db.dims, db.batch)
     per = {}
-    for _ in range(args.steps):
+    for _ in range(steps):
         ev = stca.HipEvents(nl + 1)
         stca.stca_backward_profiled(db.dims, db.batch, db.hist, db.tgt, db.weights, dout, g["dhist"], g["dtgt"],
                                     dw, db.bws, db.bws_bytes, stream.cuda_stream, ev.ev, ev.labels)
@@ -521,7 +642,7 @@ def train_step(args) -> int:
     fused = "kv_gemm" not in per  # the attention kernels project the history themselves
     phases = {}
     for lab, v in per.items():
-        occ = len(v) // args.steps
+        occ = len(v) // steps
         t = float(np.mean(v))
         ent = {"per_step": occ, "ms_each": t, "ms_per_step": t * occ}
         flop, byts, peak = backward_phase_work(lab, b, fused)
@@ -533,20 +654,34 @@ def train_step(args) -> int:
     flop, byts, peak = backward_phase_work(dom, b, fused)
     roof = roofline_entry(dom, phases[dom]["ms_each"], flop, byts, peak)
     roof["kernel"] = dom
+    roof["traffic"] = None
     bound_ms = sum(max(f / (pk * 1e12), by / (PEAK_HBM_GBS * 1e9)) * phases[k]["per_step"] * 1e3
                    for k in phases for f, by, pk in [backward_phase_work(k, b, fused)] if f)
-    print(json.dumps({
+    rec = {
         "metric": "targets trained/sec, STCA forward+backward", "value": b.n_tgt_total / (ms * 1e-3),
-        "unit": "targets/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "unit": "targets/s", "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": wl.name, "requests": wl.n_requests, "targets_per_request": wl.n_targets,
                    "hist_len": wl.hist_len, "d_model": wl.d_model, "heads": wl.n_heads, "layers": wl.n_layers},
         "stochastic_length": sl_info,
         "training_record": use_rec, "forward_ms": fwd, "backward_ms": bwd,
-        "backward_recomputing_ms": bwd_recompute, "backward_roofline": roof,
-        "backward_phase_bound_ms": bound_ms, "backward_phases": phases}), flush=True)
-    return 0
+        "backward_recomputing_ms": bwd_recompute, "roofline": roof,
+        "backward_phase_bound_ms": bound_ms, "backward_phase_bound_frac": bound_ms / bwd_recompute,
+        "backward_phases": phases}
+    if with_non_rlb:
+        nr = instance_wise(db, backward=True)
+        f2, b2, rec2 = timed_step(nr, max(2, steps // 4), 1)
+        rec["non_rlb"] = {"requests": int(nr.b.n_requests), "history_rows": int(nr.b.n_hist),
+                          "ms_per_step": f2 + b2, "forward_ms": f2, "backward_ms": b2, "training_record": rec2,
+                          "targets_per_s": nr.b.n_tgt_total / ((f2 + b2) * 1e-3)}
+        rec["rlb_gain"] = (f2 + b2) / ms
+        del nr
+    del db
+    torch.cuda.empty_cache()
+    if args.cpu_seconds > 0 and not sl:
+        rec["cpu_baseline"] = cpu_baseline(wl, args.cpu_seconds, backward=True)
+    return rec
 
 
 def copy_calibration(args) -> int:
@@ -571,60 +706,48 @@ def copy_calibration(args) -> int:
     return 0
 
 
-def ablation(wl: W.Workload, args):
-    """The same kernels on (a) one target per request and (b) the instance-wise
-    layout: every target its own request with a copy of the history."""
+def ablation(db, args, steps: int) -> dict:
+    """The headline batch in other layouts and forms: (a) the instance-wise
+    (non-RLB) layout, every target its own request with a copy of the
+    history (App. A.3), with the same kernels and with the automatic form;
+    (b) one target per request, reordered (App. A.2.2) and standard form;
+    (c) K/V materialised by one GEMM and streamed; (d) the same number of
+    targets as 16 requests of 256 (K/V written once, read once per 128
+    targets) against the fused form."""
     import torch
     from paper_2511_06077_amd.device import DeviceBatch
-    out = {}
-    k_steps = max(3, args.steps // 4)
-    db = DeviceBatch(W.make_batch(wl, with_grad=False), device="cuda:0", kv="materialize")
-    ms, per = timed_forward(db, k_steps, 1)
-    ms /= k_steps
-    out["materialized_kv"] = {"ms_per_step": ms, "targets_per_s": db.b.n_tgt_total / (ms * 1e-3),
-                              "kernels_ms_per_step": {k: float(np.sum(v)) / k_steps for k, v in per.items()}}
-    del db
+    wl = db.b.wl
+    out = {"non_rlb": non_rlb_forward(db, max(3, steps // 2))}
+    out["rlb_gain"] = out["non_rlb"]["standard_form"]["ms_per_step"] / (plain_forward(db, steps, 2) / steps)
+    dm = DeviceBatch(db.b, device="cuda:0", kv="materialize")
+    ms, per = timed_forward(dm, steps, 1)
+    ms /= steps
+    out["materialized_kv"] = {"ms_per_step": ms, "targets_per_s": dm.b.n_tgt_total / (ms * 1e-3),
+                              "kernels_ms_per_step": {k: float(np.sum(v)) / steps for k, v in per.items()}}
+    del dm
     torch.cuda.empty_cache()
     if wl.n_targets > 1 and wl.hist_range is None:
-        # one target per request: the reordered attention (App. A.2.2), and
-        # the standard form on the same batch
         one = W.Workload(wl.name + "_m1", wl.n_requests, wl.d_model, wl.n_heads, wl.n_layers, wl.dtype, wl.seed,
                          hist_len=wl.hist_len, n_targets=1)
         bo = W.make_batch(one)
         for key, mode in (("one_target_per_request", "auto"), ("one_target_per_request_standard", "standard")):
-            db = DeviceBatch(bo, device="cuda:0", attn=mode)
-            ms = plain_forward(db, k_steps, 2) / k_steps
+            d1 = DeviceBatch(bo, device="cuda:0", attn=mode)
+            ms = plain_forward(d1, steps, 2) / steps
             out[key] = {"ms_per_step": ms, "targets_per_s": one.n_requests / (ms * 1e-3),
-                        "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
-            del db
+                        "launches": stca.stca_forward_launch_count(d1.dims, d1.batch)}
+            del d1
             torch.cuda.empty_cache()
-    if wl.n_targets > 1 and wl.hist_range is None:
-        # the same number of targets as 16 requests of 256: K/V written once
-        # and read once per 128 targets, against the fused form's projection
-        # per 64-target group
         many = W.Workload(wl.name + "_m256", max(1, wl.n_requests * wl.n_targets // 256), wl.d_model, wl.n_heads,
                           wl.n_layers, wl.dtype, wl.seed, hist_len=wl.hist_len, n_targets=256)
         bm = W.make_batch(many)
         for key, mode in (("many_targets_per_request", "auto"), ("many_targets_per_request_fused", "fused")):
-            db = DeviceBatch(bm, device="cuda:0", kv=mode)
-            ms = plain_forward(db, k_steps, 2) / k_steps
+            d2 = DeviceBatch(bm, device="cuda:0", kv=mode)
+            ms = plain_forward(d2, steps, 2) / steps
             out[key] = {"requests": many.n_requests, "targets": bm.n_tgt_total, "ms_per_step": ms,
                         "targets_per_s": bm.n_tgt_total / (ms * 1e-3),
-                        "launches": stca.stca_forward_launch_count(db.dims, db.batch)}
-            del db
+                        "launches": stca.stca_forward_launch_count(d2.dims, d2.batch)}
+            del d2
             torch.cuda.empty_cache()
-    # instance-wise layout on a slice of requests that fits comfortably, scaled
-    b = W.make_batch(wl, requests=list(range(min(wl.n_requests, 8))), with_grad=False)
-    nb = W.replicate_per_target(b)
-    for name, bb in (("rlb_slice", b), ("non_rlb_slice", nb)):
-        db = DeviceBatch(bb, device="cuda:0")
-        ms, _ = timed_forward(db, 3, 1)
-        ms /= 3
-        out[name] = {"requests": int(b.n_requests), "targets": int(bb.n_tgt_total), "ms": ms,
-                     "targets_per_s": bb.n_tgt_total / (ms * 1e-3)}
-        del db
-        torch.cuda.empty_cache()
-    out["rlb_speedup_on_slice"] = out["non_rlb_slice"]["ms"] / out["rlb_slice"]["ms"]
     return out
 
 

@@ -34,15 +34,29 @@ class DeviceBatch:
                  host_offsets: bool = True, **forms):
         """forms: kv, attn, bwd (names of stca.FORMS) and chunk_blocks, passed
         through stca_dims_t."""
+        self._setup(b, to_device(b.hist, device), to_device(b.tgt, device),
+                    {k: to_device(b.weights[k], device) for k in WEIGHT_NAMES}, device, keep_saved, backward,
+                    host_offsets, forms)
+
+    @classmethod
+    def from_tensors(cls, b: Batch, hist, tgt, weights: dict, device="cuda", keep_saved: bool = False,
+                     backward: bool = False, host_offsets: bool = True, **forms):
+        """A batch whose rows are already device tensors (b supplies the shapes
+        and offsets; its row arrays are not read)."""
+        self = cls.__new__(cls)
+        self._setup(b, hist, tgt, weights, device, keep_saved, backward, host_offsets, forms)
+        return self
+
+    def _setup(self, b, hist, tgt, weights, device, keep_saved, backward, host_offsets, forms):
         torch = _torch()
         self.b = b
         wl = b.wl
         self.device = torch.device(device)
         self.bf16 = wl.dtype == "bf16"
         self.sdtype = torch.bfloat16 if self.bf16 else torch.float32
-        self.hist = to_device(b.hist, device)
-        self.tgt = to_device(b.tgt, device)
-        self.w = {k: to_device(b.weights[k], device) for k in WEIGHT_NAMES}
+        self.hist = hist
+        self.tgt = tgt
+        self.w = weights
         self.hoff_h = np.ascontiguousarray(b.hist_off, dtype=np.int32)
         self.toff_h = np.ascontiguousarray(b.tgt_off, dtype=np.int32)
         self.hoff = torch.from_numpy(self.hoff_h).to(device)
