@@ -20,19 +20,24 @@ namespace {
 // (dims, batch) pair fits every call made with the same pair.
 
 // Reordered attention (scores u . x with u = q W_K^j^T, output (P X) W_V^j;
-// no K/V at all): automatic when the host offsets show every request with at
-// most 32 / H targets (one 32-column MFMA tile of (target, head) rows);
-// STCA_ATTN_REORDERED asks for it and is unsupported for other batches.
-// Returns 1 (reordered), 0 (standard) or a negative status.
+// no K/V at all), which needs the host offsets.  Units of one request's
+// targets over all heads: up to 32 rows (t, j) per unit when every request
+// has at most 32 / H targets (reord_attn_kernel, four X blocks per round),
+// else up to 256 rows (reord_wide_kernel).  Automatic for the former;
+// STCA_ATTN_REORDERED takes either and is unsupported for a batch with a
+// request of more than 256 / H targets.  Returns 2 (wide units), 1 (narrow
+// units), 0 (standard form) or a negative status.
 int reordered_for(const stca_dims_t* dims, const stca_batch_t* b) {
   if (dims->attn_form == STCA_ATTN_STANDARD) return 0;
-  bool ok = b->tgt_off_host != nullptr;
-  const int cap = 32 / (dims->d_model / dims->n_heads == 32 ? dims->n_heads : 1 << 30);
-  ok = ok && cap >= 1;
-  for (int r = 0; ok && r < b->n_requests; ++r)
-    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > cap) ok = false;
-  if (dims->attn_form == STCA_ATTN_REORDERED && !ok) return STCA_ERR_UNSUPPORTED;
-  return ok ? 1 : 0;
+  const bool dh32 = dims->d_model / dims->n_heads == 32;
+  int64_t mmax = 0;
+  for (int r = 0; b->tgt_off_host && r < b->n_requests; ++r)
+    mmax = std::max<int64_t>(mmax, b->tgt_off_host[r + 1] - b->tgt_off_host[r]);
+  const bool ok = b->tgt_off_host != nullptr && dh32;
+  const int64_t narrow_cap = 32 / dims->n_heads, wide_cap = 256 / dims->n_heads;
+  if (ok && mmax <= narrow_cap) return 1;
+  if (dims->attn_form == STCA_ATTN_REORDERED) return ok && mmax <= wide_cap ? 2 : STCA_ERR_UNSUPPORTED;
+  return 0;
 }
 
 // Requests with more than kTargetGroup targets: the fused kernel would
@@ -74,6 +79,7 @@ struct Layout {
   int64_t max_units;
   bool any_narrow, any_wide;  // requests with 1..32 / 33+ targets (both true without host offsets)
   bool reord;                 // reordered attention (bf16 path)
+  bool reord_wide;            // ... in units of up to 256 rows (t, j)
   bool mat;                   // K/V written to the workspace by one GEMM (bf16 path)
   bool wide;                  // materialised K/V, units of up to kWideGroup targets (bf16 path)
   bool bfused;                // backward with the history projection inside the attention kernels
@@ -135,17 +141,18 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
   L->nh = b->n_hist;
   L->nt = b->n_tgt;
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
-  L->reord = false;
+  L->reord = L->reord_wide = false;
   if (p == 1 && !with_backward) {
     const int r = reordered_for(dims, b);
     if (r < 0) return static_cast<stca_status_t>(r);
-    L->reord = r == 1;
+    L->reord = r >= 1;
+    L->reord_wide = r == 2;
   }
   L->bfused = false;
   L->wide = p == 1 && !with_backward && !L->reord && wide_groups_for(dims, b);
   L->mat = p == 1 && !with_backward && !L->reord && (L->wide || dims->kv_form == STCA_KV_MATERIALIZE);
   L->chunk_blocks = chunk_blocks_for(b, device_cus(), L->reord ? 1 : 4, dims->chunk_blocks);
-  L->group = L->reord ? 32 / L->h : (L->wide ? kWideGroup : kTargetGroup);
+  L->group = L->reord ? (L->reord_wide ? 256 : 32) / L->h : (L->wide ? kWideGroup : kTargetGroup);
   L->max_units = max_units_for(b, L->chunk_blocks, L->group);
   L->any_narrow = L->any_wide = true;
   if (b->tgt_off_host) {
@@ -347,8 +354,12 @@ stca_status_t forward_reordered(const Layout& L, const stca_batch_t* b, const vo
   HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
   HIPCHK(fast_reord_qu(d, f.QN, w->wk, at<char>(ws, L.un), L.nt, st)); HIPCHK(rec.mark("reord_u"));
   for (int i = 0; i < n; ++i) {
-    HIPCHK(fast_reord_attn(d, units, hdr, L.max_units, at<char>(ws, L.un), hist, L.nh, at<float>(ws, L.part_y),
-                           at<char>(ws, L.part_ml), L.nt, st));
+    if (L.reord_wide)
+      HIPCHK(fast_reord_wide(d, units, hdr, L.max_units, at<char>(ws, L.un), hist, L.nh, at<float>(ws, L.part_y),
+                             at<char>(ws, L.part_ml), L.nt, &hdr->range, st));
+    else
+      HIPCHK(fast_reord_attn(d, units, hdr, L.max_units, at<char>(ws, L.un), hist, L.nh, at<float>(ws, L.part_y),
+                             at<char>(ws, L.part_ml), L.nt, st));
     HIPCHK(rec.mark("reord_attn"));
     HIPCHK(fast_reord_merge(d, at<float>(ws, L.part_y), at<char>(ws, L.part_ml), tch, at<char>(ws, L.wvp16), i,
                             at<float>(ws, L.a2), at<char>(ws, L.ml2), at<int32_t>(ws, L.tch2),

@@ -152,6 +152,12 @@ hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, 
 hipError_t fast_reord_attn(int D, const Unit* units, const WsHeader* hdr, int64_t max_units, const void* UN,
                            const void* X, int64_t n_hist, float* part_y, void* part_ml, int64_t n_tgt,
                            hipStream_t st);
+// Units of up to 256 / H targets (up to 256 rows (t, j)): the same partials
+// as fast_reord_attn (reord_wide_kernel, fp16 products on X rounded from
+// bf16 in LDS; an X value beyond the fp16 range sets *range).
+hipError_t fast_reord_wide(int D, const Unit* units, const WsHeader* hdr, int64_t max_units, const void* UN,
+                           const void* X, int64_t n_hist, float* part_y, void* part_ml, int64_t n_tgt,
+                           int32_t* range, hipStream_t st);
 hipError_t fast_reord_merge(int D, const float* part_y, const void* part_ml, const int32_t* tchunks,
                             const void* WvP16, int layer, float* a_out, void* ml_out, int32_t* tch_out,
                             float* save_lse, int64_t n_tgt, hipStream_t st);

@@ -43,6 +43,7 @@
 
 #include "common.h"
 #include "fast.h"
+#include "ring.h"
 
 namespace stca {
 
@@ -427,32 +428,6 @@ __global__ __launch_bounds__(64 * H) void attn_kernel(const Unit* __restrict__ u
 constexpr int kStages = 4;
 constexpr int kSegPitch = 1024 + 16;  // one direct-load segment (64 lanes x 16 B) plus padding
 
-// s_waitcnt on vector memory: at most n (rounded down to even, <= 6) of this
-// wave's vector memory operations still outstanding; LDS operations drained.
-__device__ __forceinline__ void wait_vm(int n) {
-  // gfx9 immediate: vmcnt[3:0], expcnt[6:4] = 7 (no wait), lgkmcnt[11:8] = 0
-  if (n >= 6)
-    __builtin_amdgcn_s_waitcnt(0x0076);
-  else if (n >= 4)
-    __builtin_amdgcn_s_waitcnt(0x0074);
-  else if (n >= 2)
-    __builtin_amdgcn_s_waitcnt(0x0072);
-  else
-    __builtin_amdgcn_s_waitcnt(0x0070);
-}
-
-// Direct global-to-LDS load of 16 bytes per lane: lane i's bytes land at
-// lds + 16 i (lds wave-uniform).  Issued as inline assembly so that the
-// compiler does not treat every later LDS read as possibly aliasing it (it
-// would wait for all loads in flight before each read); the kernel waits for
-// these loads itself (wait_vm).  The compiler's own vector-memory waits only
-// become more conservative, as the counter retires operations in order.
-__device__ __forceinline__ void dma16(const void* src, const unsigned char* lds) {
-  const uint32_t m0 =
-      static_cast<uint32_t>(reinterpret_cast<uintptr_t>((const __attribute__((address_space(3))) unsigned char*)lds));
-  asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(src), "{m0}"(__builtin_amdgcn_readfirstlane(m0)));
-}
-
 // The value unchanged, but opaque to the compiler: quantities derived from it
 // are recomputed where used instead of being hoisted out of the loop and kept
 // live (or spilled) across it.
@@ -460,11 +435,6 @@ __device__ __forceinline__ int opaque(int v) {
   asm volatile("" : "+v"(v));
   return v;
 }
-
-// Workgroup barrier without the fences of __syncthreads (whose release would
-// wait for every load in flight, including the ring's prefetches); the memory
-// clobber keeps the compiler from moving LDS accesses across it.
-__device__ __forceinline__ void ring_barrier() { asm volatile("s_barrier" ::: "memory"); }
 
 template <int D, int NG>
 __global__ __launch_bounds__(64 * (D / 32)) void fused_kernel(const Unit* __restrict__ units,

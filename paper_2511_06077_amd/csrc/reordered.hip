@@ -24,6 +24,7 @@
 // cheaper than converting X.
 #include "common.h"
 #include "fast.h"
+#include "ring.h"
 
 namespace stca {
 
@@ -321,6 +322,213 @@ __global__ __launch_bounds__(128 * kWaves) void reord_attn_kernel(const Unit* __
   }
 }
 
+// ----------------------------------------------- attention, wide units
+// Units of up to 256 rows (t, j) (up to 256 / H targets of one request, all
+// heads), one history chunk each: eight waves, wave w owning the rows
+// [32 w, 32 w + 32) as the 32 columns of its tiles (waves past the unit's
+// rows only load).  X blocks arrive by direct global-to-LDS loads into a
+// ring of four tiles, three blocks ahead; each wave loads a fixed share of
+// every block (whole 1 KB segments) and, once its own loads of a block have
+// landed, rounds its share from bf16 to fp16 in place, one block ahead of
+// its use, so that one barrier per block both publishes a converted tile and
+// frees the oldest slot.  Per block and wave:
+//   S^T (32 history rows x 32 rows (t, j)) = X U^T on the fp16 MFMA, K = d:
+//     A = X rows (16-byte LDS reads, MFMA row i = history row blk_row(i)),
+//     B = U of the wave's rows (fp16, registers);
+//   online softmax per column, with the reference maximum moved only when a
+//     block exceeds it by kSlack (weights <= 2^kSlack, fine in fp16);
+//   Y^T (d x 32) += X^T P^T, K = 32 history rows: B = P^T straight from the
+//     S^T registers (k-step s: MFMA rows 16 s + 4 hi + {0..3, 8..11}),
+//     A = X^T by transposing LDS reads of the same history rows.
+// The unit's partials (y per row, running max and sum) go out as chunk c
+// of the reordered form's records, merged by reord_merge_kernel.
+constexpr int kWideWaves = 8;
+constexpr int kWideRows = 32 * kWideWaves;  // (t, j) rows a unit holds
+constexpr int kWideStages = 4;
+
+template <int RPS>
+__device__ __forceinline__ int wide_row(int i) {
+  return RPS * (i % (32 / RPS)) + i / (32 / RPS);
+}
+
+template <int D>
+__global__ __launch_bounds__(64 * kWideWaves) void reord_wide_kernel(const Unit* __restrict__ units,
+                                                                     const WsHeader* __restrict__ hdr,
+                                                                     const __bf16* __restrict__ UN,
+                                                                     const bf16_bits* __restrict__ X,
+                                                                     int64_t n_hist, float* __restrict__ part_y,
+                                                                     float2* __restrict__ part_ml, int64_t n_tgt,
+                                                                     int32_t* __restrict__ range) {
+  constexpr int H = D / DH;
+  constexpr int KS = D / 16;
+  constexpr int NDT = D / 32;
+  constexpr int CPR = D / 8;               // 16-byte chunks per X row
+  constexpr int RPS = 64 / CPR;            // rows per 1 KB segment
+  constexpr int NSEG = 32 / RPS;           // segments per block
+  constexpr int SPW = (NSEG + kWideWaves - 1) / kWideWaves;  // segments a wave loads (the last waves may load none)
+  constexpr int TILE = NSEG * kSegPitch;
+  __shared__ __attribute__((aligned(16))) unsigned char xs[kWideStages * TILE];
+  const int u = blockIdx.x;
+  if (u >= hdr->n_units) return;
+  const Unit un = units[u];
+  const int w = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int tcol = lane % 32, hi = lane / 32;
+  const int R = un.nt * H;
+  const bool active = 32 * w < R;
+  const int nb = un.b1 - un.b0;
+  auto rowoff = [](int row) { return (row / RPS) * kSegPitch + (row % RPS) * 2 * D; };
+
+  // U of the wave's rows (bf16 hi + lo terms, combined into one fp16
+  // operand): B operand of S^T, lane (row tcol, hi) holds model dims
+  // 16 ks + 8 hi .. + 7
+  f16x8 ub[KS];
+  {
+    const int rho = 32 * w + tcol;
+    const bool ok = active && rho < R;
+    const __bf16* up = UN + ((int64_t)un.t0 * H + (ok ? rho : 0)) * 2 * D + 8 * hi;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 h8 = ok ? *reinterpret_cast<const bf16x8*>(up + 16 * ks) : zero8b();
+      const bf16x8 l8 = ok ? *reinterpret_cast<const bf16x8*>(up + D + 16 * ks) : zero8b();
+#pragma unroll
+      for (int i = 0; i < 8; ++i) ub[ks][i] = static_cast<_Float16>(static_cast<float>(h8[i]) + static_cast<float>(l8[i]));
+    }
+  }
+
+  // this wave's share of block k: segments w + 8 i
+  auto issue = [&](int k) {
+    if (k >= nb) return;
+    unsigned char* slot = xs + (k % kWideStages) * TILE;
+    const int64_t b = un.b0 + k;
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int seg = w + kWideWaves * i;
+      if (seg < NSEG) {
+        const int e = seg * 64 + lane;
+        const int64_t grow = min(b * 32 + e / CPR, n_hist - 1);
+        dma16(X + grow * D + (e % CPR) * 8, slot + seg * kSegPitch);
+      }
+    }
+  };
+  // round this wave's share of block k from bf16 to fp16 in place (its own
+  // loads of the block must have landed); |x| beyond the fp16 range is
+  // recorded
+  uint32_t big = 0;
+  auto convert = [&](int k) {
+    if (k >= nb) return;
+    unsigned char* slot = xs + (k % kWideStages) * TILE;
+#pragma unroll
+    for (int i = 0; i < SPW; ++i) {
+      const int seg = w + kWideWaves * i;
+      if (seg < NSEG) {
+        uint4* p = reinterpret_cast<uint4*>(slot + seg * kSegPitch + 16 * lane);
+        const uint4 v = *p;
+        const uint32_t in[4] = {v.x, v.y, v.z, v.w};
+        uint32_t outw[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const float lo = __uint_as_float(in[q] << 16), hv = __uint_as_float(in[q] & 0xffff0000u);
+          big = max(big, max(__float_as_uint(fabsf(lo)), __float_as_uint(fabsf(hv))));
+          outw[q] = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<_Float16>(lo)) |
+                    ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<_Float16>(hv)) << 16);
+        }
+        *p = make_uint4(outw[0], outw[1], outw[2], outw[3]);
+      }
+    }
+  };
+  // loads in flight after a block's own: SPW per newer block issued
+  auto wait_own = [&](int newer) { wait_vm(SPW * newer); };
+
+  f32x16 Y[NDT];
+#pragma unroll
+  for (int dt = 0; dt < NDT; ++dt) Y[dt] = f32x16{};
+  float m = -INFINITY, l = 0.f;
+
+  // lane addresses: S^T A operand (MFMA row tcol, dims 16 ks + 8 hi) and the
+  // transposing reads of the Y^T A operand (group g of 16 lanes: model dims
+  // 32 dt + 16 (g % 2) + 4 (lane % 4) .. + 3 of MFMA rows 16 s + 4 hi +
+  // (lane % 16) / 4, and the same + 8)
+  const int xa = rowoff(wide_row<RPS>(tcol)) + 16 * hi;
+  const int g16 = lane / 16, sl = lane % 16;
+  const int ta0 = 2 * (16 * (g16 % 2) + 4 * (sl % 4));
+
+  wait_vm(0);  // U is in registers: the loop issues no load the compiler counts
+  for (int k = 0; k < kWideStages - 1; ++k) issue(k);
+  wait_own(min(nb - 1, kWideStages - 2));
+  convert(0);
+  for (int k = 0; k < nb; ++k) {
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's converted writes are done
+    ring_barrier();  // block k converted by every wave; block k - 1 read by every wave
+    issue(k + kWideStages - 1);
+    // own loads of block k + 1: newer blocks in flight are k + 2 and k + 3
+    wait_own(max(0, min(nb - 1, k + kWideStages - 1) - (k + 1)));
+    convert(k + 1);
+    if (!active) continue;
+    const unsigned char* tile = xs + (k % kWideStages) * TILE;
+    const int b = un.b0 + k;
+    f32x16 s = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) s = mfma16(*reinterpret_cast<const f16x8*>(tile + xa + 32 * ks), ub[ks], s);
+    if (b * 32 < un.l0 || b * 32 + 32 > un.l1) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int tok = b * 32 + wide_row<RPS>(8 * (v / 4) + 4 * hi + (v % 4));
+        if (tok < un.l0 || tok >= un.l1) s[v] = -INFINITY;
+      }
+    }
+    float bm = s[0];
+#pragma unroll
+    for (int v = 1; v < 16; ++v) bm = fmaxf(bm, s[v]);
+    bm = fmaxf(bm, __shfl_xor(bm, 32));
+    if (__builtin_amdgcn_ballot_w64(bm > m + kSlack)) {
+      const float mn = fmaxf(m, bm);
+      const float sc = m == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m - mn);
+      m = mn;
+      l *= sc;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt) Y[dt] *= sc;
+    }
+    float ps = 0.f;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      s[v] = __builtin_amdgcn_exp2f(s[v] - m);
+      ps += s[v];
+    }
+    l += ps;
+    const f16x8 p0 = pack8(s, 0), p1 = pack8(s, 8);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+#pragma unroll
+      for (int ss = 0; ss < 2; ++ss) {
+        const int r0 = wide_row<RPS>(16 * ss + 4 * hi + sl / 4);
+        const int r1 = wide_row<RPS>(16 * ss + 8 + 4 * hi + sl / 4);
+        // (whole-vector casts: casting the four 16-bit elements one by one
+        // made this compiler permute them)
+        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+        const h4 a0 = __builtin_bit_cast(h4, lds_read_tr16(tile + rowoff(r0) + 64 * dt + ta0));
+        const h4 a1 = __builtin_bit_cast(h4, lds_read_tr16(tile + rowoff(r1) + 64 * dt + ta0));
+        const f16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+        Y[dt] = mfma16(a, ss ? p1 : p0, Y[dt]);
+      }
+    }
+  }
+  if (big > __float_as_uint(kF16Max)) *range = 1;
+  if (!active) return;
+  const float lt = l + __shfl_xor(l, 32);
+  const int rho = 32 * w + tcol;
+  if (rho < R) {
+    const int64_t prow = ((int64_t)un.c * n_tgt + un.t0 + rho / H) * H + rho % H;
+    float* py = part_y + prow * D + 4 * hi;
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int g = 0; g < 4; ++g)
+        *reinterpret_cast<float4*>(py + 32 * dt + 8 * g) =
+            make_float4(Y[dt][4 * g], Y[dt][4 * g + 1], Y[dt][4 * g + 2], Y[dt][4 * g + 3]);
+    if (hi == 0) part_ml[prow] = make_float2(m, lt);
+  }
+}
+
 // ---------------------------------------------------------------- merge
 // One wave per (32 targets, head j): it merges the chunk partials of y_tj
 // into fp16 rows in LDS (two lanes per target, half of the d columns each),
@@ -454,6 +662,25 @@ hipError_t fast_reord_attn(int D, const Unit* units, const WsHeader* hdr, int64_
     default: return hipErrorInvalidValue;
   }
 #undef STCA_RA
+  return hipGetLastError();
+}
+
+hipError_t fast_reord_wide(int D, const Unit* units, const WsHeader* hdr, int64_t max_units, const void* UN,
+                           const void* X, int64_t n_hist, float* part_y, void* part_ml, int64_t n_tgt,
+                           int32_t* range, hipStream_t st) {
+  if (max_units == 0) return hipSuccess;
+  if (!range) return hipErrorInvalidValue;
+#define STCA_RW(DD)                                                                                         \
+  hipLaunchKernelGGL(reord_wide_kernel<DD>, dim3(static_cast<unsigned>(max_units)), dim3(64 * kWideWaves), 0, \
+                     st, units, hdr, (const __bf16*)UN, (const bf16_bits*)X, n_hist, part_y, (float2*)part_ml, \
+                     n_tgt, range)
+  switch (D) {
+    case 64: STCA_RW(64); break;
+    case 128: STCA_RW(128); break;
+    case 256: STCA_RW(256); break;
+    default: return hipErrorInvalidValue;
+  }
+#undef STCA_RW
   return hipGetLastError();
 }
 

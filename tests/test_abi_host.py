@@ -150,10 +150,16 @@ def test_reordered_form_selection():
     assert stca.stca_forward_launch_count(dims(), nohost) == 3 + 3 * n
     assert stca.stca_forward_launch_count(dims(attn="standard"), small) == 3 + 3 * n
     assert stca.stca_forward_launch_count(dims(attn="reordered"), small) == 3 + 4 * n
-    # asking for the reordered form where it does not apply is unsupported
-    assert stca.stca_forward_launch_count(dims(attn="reordered"), wide) == -1
-    assert call_forward(dims(attn="reordered"), wide) == stca.STCA_ERR_UNSUPPORTED
-    assert stca.stca_workspace_size(dims(attn="reordered"), wide) == 0
+    # asked for, the reordered form takes up to 256 / h targets per request
+    # (wide units of up to 256 rows (t, j)); more is unsupported
+    assert stca.stca_forward_launch_count(dims(attn="reordered"), wide) == 3 + 4 * n
+    top, keep3 = fake_batch([0, 40, 100], [0, 32, 40])
+    over, keep4 = fake_batch([0, 40, 100], [0, 33, 40])
+    assert stca.stca_forward_launch_count(dims(attn="reordered"), top) == 3 + 4 * n
+    assert stca.stca_forward_launch_count(dims(attn="reordered"), over) == -1
+    assert call_forward(dims(attn="reordered"), over) == stca.STCA_ERR_UNSUPPORTED
+    assert stca.stca_workspace_size(dims(attn="reordered"), over) == 0
+    assert stca.stca_forward_launch_count(dims(attn="reordered", d_model=64, n_heads=2), over) == 3 + 4 * n
 
 
 def test_wide_groups_selection():

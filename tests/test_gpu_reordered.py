@@ -97,3 +97,84 @@ def test_reordered_repeat_bitwise(torch):
     y2 = db.forward().clone()
     torch.cuda.synchronize()
     assert torch.equal(y1, y2)
+
+
+# wide units: up to 256 / h targets per request (256 rows (t, j) per unit)
+WIDE_HIST = [1, 7, 31, 33, 65, 300, 1023, 40, 129, 2048]
+
+
+@pytest.mark.parametrize("d,h", [(256, 8), (128, 4), (64, 2)])
+@pytest.mark.parametrize("chunk", [0, 1, 3])
+def test_reordered_wide_parity(torch, d, h, chunk):
+    """Requests of up to 256 / h targets (1..8 column tiles of rows (t, j),
+    full and partial), history tails and several chunks, against the oracle."""
+    cap = 256 // h
+    m = [cap, 1, cap - 1, 5, 0, cap // 2 + 3, 2, 17 % (cap + 1), cap, 9]
+    b = W.make_custom_batch("reord_wide", WIDE_HIST, m, d_model=d, n_heads=h, n_layers=2, dtype="bf16", seed=37)
+    y, a, lse, db = run_gpu(torch, b, attn="reordered", chunk_blocks=chunk)
+    from paper_2511_06077_amd import stca
+    assert stca.stca_forward_launch_count(db.dims, db.batch) == 3 + 4 * 2
+    assert db.device_status() == 0
+    check_against_oracle(b, y, a, lse, TOL["bf16"])
+
+
+def test_reordered_wide_matches_standard(torch):
+    b = W.make_custom_batch("reord_wide_vs_std", [2048, 513, 96, 1], [32, 17, 3, 8], d_model=256, n_heads=8,
+                            n_layers=3, dtype="bf16", seed=38)
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered")
+    ys, as_, _, _ = run_gpu(torch, b, attn="standard")
+    e_y, e_a = rowerr(y, ys), max(rowerr(a[i], as_[i]) for i in range(3))
+    print(f"[reord wide] reordered vs standard: err(Y)={e_y:.2e} err(a)={e_a:.2e}")
+    assert e_y <= TOL["bf16"] and e_a <= TOL["bf16"]
+    check_against_oracle(b, y, a, lse, TOL["bf16"])
+
+
+def test_reordered_wide_special_cases(torch):
+    """P1 (L = 1: a is the V row) and P2 (W_Q = 0: a is the mean of V, lse =
+    log L) in wide units, and W_Q x 8 (peaked softmax)."""
+    b = W.make_custom_batch("rw_l1", [1, 1], [32, 7], d_model=256, n_heads=8, n_layers=2, dtype="bf16", seed=39)
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered")
+    f = b.f64()
+    for r in range(2):
+        t0, t1 = b.tgt_off[r], b.tgt_off[r + 1]
+        for i in range(2):
+            v = f["hist"][r] @ f["wv"][i]
+            assert rowerr(a[i, t0:t1], np.broadcast_to(v, (t1 - t0, v.size))) <= TOL["bf16"]
+    b = W.make_custom_batch("rw_zq", [100, 37], [30, 9], d_model=256, n_heads=8, n_layers=2, dtype="bf16", seed=40)
+    b.weights["wq"][:] = 0
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered")
+    f = b.f64()
+    for r in range(2):
+        X = f["hist"][b.hist_off[r]:b.hist_off[r + 1]]
+        t0, t1 = b.tgt_off[r], b.tgt_off[r + 1]
+        for i in range(2):
+            mv = (X @ f["wv"][i]).mean(axis=0)
+            assert rowerr(a[i, t0:t1], np.broadcast_to(mv, (t1 - t0, mv.size))) <= TOL["bf16"]
+            np.testing.assert_allclose(lse[i, t0:t1], np.log(X.shape[0]), atol=1e-3)
+    b = W.make_custom_batch("rw_peak", [300, 129, 77], [32, 20, 1], d_model=256, n_heads=8, n_layers=2,
+                            dtype="bf16", seed=41, scale_q=8.0)
+    y, a, lse, _ = run_gpu(torch, b, attn="reordered", chunk_blocks=2)
+    check_against_oracle(b, y, a, lse, TOL["bf16"])
+
+
+def test_reordered_wide_range_is_reported(torch):
+    """Wide units round X to fp16 in LDS: a history value of 1e5 (valid
+    bf16, beyond fp16) is recorded as STCA_ERR_RANGE."""
+    from paper_2511_06077_amd import stca
+    from paper_2511_06077_amd.device import DeviceBatch
+    b = W.make_custom_batch("rw_range", [100, 37], [30, 9], d_model=256, n_heads=8, n_layers=1, dtype="bf16",
+                            seed=42)
+    db = DeviceBatch(b, attn="reordered")
+    db.forward()
+    assert db.device_status() == stca.STCA_OK
+    b.hist[50, 7] = W.to_bf16_bits(np.array([1e5], dtype=np.float32))[0]
+    db = DeviceBatch(b, attn="reordered")
+    db.forward()
+    assert db.device_status() == stca.STCA_ERR_RANGE
+
+
+def test_reordered_wide_long_history_sampled_parity(torch):
+    """The headline workload (128 requests x 32 targets, L = 10240) in the
+    reordered form (8 column tiles per unit), oracle on 16 sampled requests."""
+    from test_gpu_forward import _sampled_parity
+    _sampled_parity(torch, "long_bf16_R128_m32_L10240_d256", 16, 7, attn="reordered")
