@@ -346,8 +346,17 @@ constexpr int kWideWaves = 8;
 constexpr int kWideRows = 32 * kWideWaves;  // (t, j) rows a unit holds
 constexpr int kWideStages = 4;
 
+// History row of MFMA row i within a block (RPS rows per 1 KB segment,
+// segments 16 bytes apart in the bank order).  The 16-byte row reads of S^T
+// send lanes i = 0..15 to sixteen different segments.  At d = 256 the order
+// also serves the transposing reads of Y^T: writing i = 16 s + 8 e + 4 h + k,
+// the rows k = 0..3 of a read group (fixed s, e, h) lie in segments
+// 4 k + 2 e + h, i.e. 64 bytes apart in the bank order, so the two 16-lane
+// groups of a half-wave (32-byte column slices side by side) cover the 64
+// banks once; with fewer segments per block (d < 256) they share banks.
 template <int RPS>
 __device__ __forceinline__ int wide_row(int i) {
+  if (RPS == 2) return 2 * (4 * (i & 3) + 2 * ((i >> 3) & 1) + ((i >> 2) & 1)) + (i >> 4);
   return RPS * (i % (32 / RPS)) + i / (32 / RPS);
 }
 
@@ -414,27 +423,29 @@ __global__ __launch_bounds__(64 * kWideWaves) void reord_wide_kernel(const Unit*
   // loads of the block must have landed); |x| beyond the fp16 range is
   // recorded
   uint32_t big = 0;
+  auto conv_ptr = [&](int k, int i) {
+    return reinterpret_cast<uint2*>(xs + (k % kWideStages) * TILE + (w + kWideWaves * i) * kSegPitch + 16 * lane);
+  };
+  // bf16 -> fp16 of four values (two dwords)
+  auto conv = [&](const uint2& v) {
+    const uint32_t in[2] = {v.x, v.y};
+    uint32_t outw[2];
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const float lo = __uint_as_float(in[q] << 16), hv = __uint_as_float(in[q] & 0xffff0000u);
+      big = max(big, max(__float_as_uint(fabsf(lo)), __float_as_uint(fabsf(hv))));
+      outw[q] = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<_Float16>(lo)) |
+                ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<_Float16>(hv)) << 16);
+    }
+    return make_uint2(outw[0], outw[1]);
+  };
   auto convert = [&](int k) {
     if (k >= nb) return;
-    unsigned char* slot = xs + (k % kWideStages) * TILE;
 #pragma unroll
-    for (int i = 0; i < SPW; ++i) {
-      const int seg = w + kWideWaves * i;
-      if (seg < NSEG) {
-        uint4* p = reinterpret_cast<uint4*>(slot + seg * kSegPitch + 16 * lane);
-        const uint4 v = *p;
-        const uint32_t in[4] = {v.x, v.y, v.z, v.w};
-        uint32_t outw[4];
+    for (int i = 0; i < SPW; ++i)
+      if (w + kWideWaves * i < NSEG)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const float lo = __uint_as_float(in[q] << 16), hv = __uint_as_float(in[q] & 0xffff0000u);
-          big = max(big, max(__float_as_uint(fabsf(lo)), __float_as_uint(fabsf(hv))));
-          outw[q] = (uint32_t)__builtin_bit_cast(uint16_t, static_cast<_Float16>(lo)) |
-                    ((uint32_t)__builtin_bit_cast(uint16_t, static_cast<_Float16>(hv)) << 16);
-        }
-        *p = make_uint4(outw[0], outw[1], outw[2], outw[3]);
-      }
-    }
+        for (int h = 0; h < 2; ++h) conv_ptr(k, i)[h] = conv(conv_ptr(k, i)[h]);
   };
   // loads in flight after a block's own: SPW per newer block issued
   auto wait_own = [&](int newer) { wait_vm(SPW * newer); };
@@ -461,14 +472,28 @@ __global__ __launch_bounds__(64 * kWideWaves) void reord_wide_kernel(const Unit*
     ring_barrier();  // block k converted by every wave; block k - 1 read by every wave
     issue(k + kWideStages - 1);
     // own loads of block k + 1: newer blocks in flight are k + 2 and k + 3
-    wait_own(max(0, min(nb - 1, k + kWideStages - 1) - (k + 1)));
-    convert(k + 1);
-    if (!active) continue;
+    const int newer = max(0, min(nb - 1, k + kWideStages - 1) - (k + 1));
+    if (!active) {
+      wait_own(newer);
+      convert(k + 1);
+      continue;
+    }
     const unsigned char* tile = xs + (k % kWideStages) * TILE;
     const int b = un.b0 + k;
+    // X operands read kAhead k-steps ahead of their MFMAs (the scheduling
+    // barriers keep the compiler from sinking the reads next to their use)
+    constexpr int kAhead = 2;
     f32x16 s = {};
+    f16x8 xo[kAhead];
 #pragma unroll
-    for (int ks = 0; ks < KS; ++ks) s = mfma16(*reinterpret_cast<const f16x8*>(tile + xa + 32 * ks), ub[ks], s);
+    for (int i = 0; i < kAhead; ++i) xo[i] = *reinterpret_cast<const f16x8*>(tile + xa + 32 * i);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const f16x8 x = xo[ks % kAhead];
+      if (ks + kAhead < KS) xo[ks % kAhead] = *reinterpret_cast<const f16x8*>(tile + xa + 32 * (ks + kAhead));
+      s = mfma16(x, ub[ks], s);
+      __builtin_amdgcn_sched_barrier(0);
+    }
     if (b * 32 < un.l0 || b * 32 + 32 > un.l1) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
@@ -496,21 +521,41 @@ __global__ __launch_bounds__(64 * kWideWaves) void reord_wide_kernel(const Unit*
     }
     l += ps;
     const f16x8 p0 = pack8(s, 0), p1 = pack8(s, 8);
+    // this wave's share of block k + 1 is rounded to fp16 during the Y^T
+    // products (its loads have long landed; the LDS round trips overlap the
+    // MFMAs), 8 bytes per lane at a time: part p (segment p / 2, half p % 2)
+    // read at product 4 p, converted and written back at product 4 p + 2
+    const bool conv_next = k + 1 < nb;
+    wait_own(newer);
+    uint2 cv = {};
+    auto conv_owns = [&](int part) { return conv_next && part < 2 * SPW && w + kWideWaves * (part / 2) < NSEG; };
+    // A operands of Y^T: step q = ss NDT + dt, read one step ahead
+    auto xt_op = [&](int q) {
+      const int dt = q % NDT, ss = q / NDT;
+      const int r0 = wide_row<RPS>(16 * ss + 4 * hi + sl / 4);
+      const int r1 = wide_row<RPS>(16 * ss + 8 + 4 * hi + sl / 4);
+      // (whole-vector casts: casting the four 16-bit elements one by one
+      // made this compiler permute them)
+      typedef _Float16 h4 __attribute__((ext_vector_type(4)));
+      const h4 a0 = __builtin_bit_cast(h4, lds_read_tr16(tile + rowoff(r0) + 64 * dt + ta0));
+      const h4 a1 = __builtin_bit_cast(h4, lds_read_tr16(tile + rowoff(r1) + 64 * dt + ta0));
+      return __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
+    };
+    f16x8 an = xt_op(0);
 #pragma unroll
-    for (int dt = 0; dt < NDT; ++dt) {
-#pragma unroll
-      for (int ss = 0; ss < 2; ++ss) {
-        const int r0 = wide_row<RPS>(16 * ss + 4 * hi + sl / 4);
-        const int r1 = wide_row<RPS>(16 * ss + 8 + 4 * hi + sl / 4);
-        // (whole-vector casts: casting the four 16-bit elements one by one
-        // made this compiler permute them)
-        typedef _Float16 h4 __attribute__((ext_vector_type(4)));
-        const h4 a0 = __builtin_bit_cast(h4, lds_read_tr16(tile + rowoff(r0) + 64 * dt + ta0));
-        const h4 a1 = __builtin_bit_cast(h4, lds_read_tr16(tile + rowoff(r1) + 64 * dt + ta0));
-        const f16x8 a = __builtin_shufflevector(a0, a1, 0, 1, 2, 3, 4, 5, 6, 7);
-        Y[dt] = mfma16(a, ss ? p1 : p0, Y[dt]);
-      }
+    for (int q = 0; q < 2 * NDT; ++q) {
+      const f16x8 a = an;
+      if (q + 1 < 2 * NDT) an = xt_op(q + 1);
+      Y[q % NDT] = mfma16(a, q / NDT ? p1 : p0, Y[q % NDT]);
+      if (q % 4 == 0 && q + 2 < 2 * NDT && conv_owns(q / 4)) cv = conv_ptr(k + 1, q / 8)[(q / 4) % 2];
+      if (q % 4 == 2 && conv_owns(q / 4)) conv_ptr(k + 1, q / 8)[(q / 4) % 2] = conv(cv);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    // parts the products did not cover (d = 64)
+#pragma unroll
+    for (int part = 0; part < 2 * SPW; ++part)
+      if (4 * part + 2 >= 2 * NDT && conv_owns(part))
+        conv_ptr(k + 1, part / 2)[part % 2] = conv(conv_ptr(k + 1, part / 2)[part % 2]);
   }
   if (big > __float_as_uint(kF16Max)) *range = 1;
   if (!active) return;
