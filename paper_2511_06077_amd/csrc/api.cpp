@@ -21,24 +21,36 @@ namespace {
 
 // Reordered attention (scores u . x with u = q W_K^j^T, output (P X) W_V^j;
 // no K/V at all), which needs the host offsets.  Units of one request's
-// targets over all heads: up to 32 rows (t, j) per unit when every request
-// has at most 32 / H targets (reord_attn_kernel, four X blocks per round),
-// else up to 256 rows (reord_wide_kernel).  Automatic for the former;
-// STCA_ATTN_REORDERED takes either and is unsupported for a batch with a
-// request of more than 256 / H targets.  Returns 2 (wide units), 1 (narrow
-// units), 0 (standard form) or a negative status.
+// targets over all heads: up to 32 rows (t, j) per unit for requests with at
+// most 32 / H targets (reord_attn_kernel, four X blocks per round), else up
+// to 256 rows (reord_wide_kernel).  Automatic choice, per request: requests
+// with at most 32 / H targets take the reordered form and the others the
+// standard form, in the same call when the batch holds both kinds (their
+// work is cheapest that way: 4 m H L d flop against 4 L d^2 + 4 m L d).
+// STCA_ATTN_REORDERED puts every request in the reordered form and is
+// unsupported for a batch with a request of more than 256 / H targets.
+// Returns 3 (both forms, per request), 2 (every request, wide units), 1
+// (every request, narrow units), 0 (standard form) or a negative status.
 int reordered_for(const stca_dims_t* dims, const stca_batch_t* b) {
   if (dims->attn_form == STCA_ATTN_STANDARD) return 0;
   const bool dh32 = dims->d_model / dims->n_heads == 32;
-  int64_t mmax = 0;
-  for (int r = 0; b->tgt_off_host && r < b->n_requests; ++r)
-    mmax = std::max<int64_t>(mmax, b->tgt_off_host[r + 1] - b->tgt_off_host[r]);
-  const bool ok = b->tgt_off_host != nullptr && dh32;
   const int64_t narrow_cap = 32 / dims->n_heads, wide_cap = 256 / dims->n_heads;
+  int64_t mmax = 0;
+  bool any_small = false;
+  for (int r = 0; b->tgt_off_host && r < b->n_requests; ++r) {
+    const int64_t m = b->tgt_off_host[r + 1] - b->tgt_off_host[r];
+    mmax = std::max(mmax, m);
+    any_small |= m >= 1 && m <= narrow_cap;
+  }
+  const bool ok = b->tgt_off_host != nullptr && dh32;
   if (ok && mmax <= narrow_cap) return 1;
   if (dims->attn_form == STCA_ATTN_REORDERED) return ok && mmax <= wide_cap ? 2 : STCA_ERR_UNSUPPORTED;
-  return 0;
+  return ok && any_small ? 3 : 0;
 }
+
+// The target-count bound of requests in the reordered form when a batch runs
+// both forms.
+inline int mixed_cap(const stca_dims_t* dims) { return 32 / dims->n_heads; }
 
 // Requests with more than kTargetGroup targets: the fused kernel would
 // project their history once per 64-target group, so the automatic choice
@@ -78,8 +90,13 @@ struct Layout {
   int chunk_blocks;
   int64_t max_units;
   bool any_narrow, any_wide;  // requests with 1..32 / 33+ targets (both true without host offsets)
-  bool reord;                 // reordered attention (bf16 path)
+  bool reord;                 // some requests in the reordered form (bf16 path)
   bool reord_wide;            // ... in units of up to 256 rows (t, j)
+  bool mixed;                 // ... and the others in the standard form
+  int reord_lo, reord_hi;     // target counts of the requests in the reordered form
+  int std_lo;                 // requests with at least this many targets take the standard form
+  int chunk_blocks2, group2;  // reordered schedule
+  int64_t max_units2;
   bool mat;                   // K/V written to the workspace by one GEMM (bf16 path)
   bool wide;                  // materialised K/V, units of up to kWideGroup targets (bf16 path)
   bool bfused;                // backward with the history projection inside the attention kernels
@@ -88,8 +105,9 @@ struct Layout {
   size_t hdr, units, tchunks, part_acc, part_ml, state_a, state_b;
   // fast
   size_t qn, wkp, wvp, wop, w1p, w2p, wqp, kv;
-  // reordered
-  size_t un, part_y, a2, ml2, tch2, wvp16;
+  // reordered: U, the y partials with their (max, sum) and chunk counts, its
+  // schedule (its own header and units when both forms run), fp16 W_V
+  size_t un, part_y, ml_r, tch_r, hdr2, units2, wvp16;
   // generic forward
   size_t kv32, q32, abuf, ubuf, hid;
   // backward (generic)
@@ -141,24 +159,46 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
   L->nh = b->n_hist;
   L->nt = b->n_tgt;
   L->nblocks = ceil_div(b->n_hist, kBlockTokens);
-  L->reord = L->reord_wide = false;
+  L->reord = L->reord_wide = L->mixed = false;
   if (p == 1 && !with_backward) {
     const int r = reordered_for(dims, b);
     if (r < 0) return static_cast<stca_status_t>(r);
     L->reord = r >= 1;
     L->reord_wide = r == 2;
+    L->mixed = r == 3;
   }
+  // requests [std_lo, inf) targets: standard form; [reord_lo, reord_hi]: reordered
+  L->std_lo = L->mixed ? mixed_cap(dims) + 1 : (L->reord ? 1 << 30 : 1);
+  L->reord_lo = 1;
+  L->reord_hi = L->mixed ? mixed_cap(dims) : (L->reord ? 1 << 30 : 0);
   L->bfused = false;
-  L->wide = p == 1 && !with_backward && !L->reord && wide_groups_for(dims, b);
-  L->mat = p == 1 && !with_backward && !L->reord && (L->wide || dims->kv_form == STCA_KV_MATERIALIZE);
-  L->chunk_blocks = chunk_blocks_for(b, device_cus(), L->reord ? 1 : 4, dims->chunk_blocks);
-  L->group = L->reord ? (L->reord_wide ? 256 : 32) / L->h : (L->wide ? kWideGroup : kTargetGroup);
-  L->max_units = max_units_for(b, L->chunk_blocks, L->group);
-  L->any_narrow = L->any_wide = true;
-  if (b->tgt_off_host) {
+  const bool std_part = !L->reord || L->mixed;
+  L->wide = p == 1 && !with_backward && std_part && wide_groups_for(dims, b);
+  L->mat = p == 1 && !with_backward && std_part && (L->wide || dims->kv_form == STCA_KV_MATERIALIZE);
+  L->chunk_blocks = chunk_blocks_for(b, device_cus(), 4, dims->chunk_blocks);
+  L->group = L->wide ? kWideGroup : kTargetGroup;
+  L->max_units = std_part ? max_units_for(b, L->chunk_blocks, L->group, L->std_lo) : 0;
+  // the reordered schedule spreads its own requests' rows over the chip
+  int64_t rows2 = b->n_hist;
+  if (L->mixed) {
+    rows2 = 0;
+    for (int r = 0; r < b->n_requests; ++r) {
+      const int64_t m = b->tgt_off_host[r + 1] - b->tgt_off_host[r];
+      if (m >= L->reord_lo && m <= L->reord_hi) rows2 += b->hist_off_host[r + 1] - b->hist_off_host[r];
+    }
+  }
+  L->chunk_blocks2 = chunk_blocks_for(b, device_cus(), 1, dims->chunk_blocks, rows2);
+  // (a small reordered share of a mixed batch in chunks of at least 512
+  // rows: its merge cost grows with the chunk count)
+  if (L->mixed && dims->chunk_blocks == 0) L->chunk_blocks2 = std::max(L->chunk_blocks2, 16);
+  L->group2 = (L->reord_wide ? 256 : 32) / L->h;
+  L->max_units2 = L->reord ? max_units_for(b, L->chunk_blocks2, L->group2, L->reord_lo, L->reord_hi) : 0;
+  L->any_narrow = L->any_wide = std_part;
+  if (b->tgt_off_host && std_part) {
     L->any_narrow = L->any_wide = false;
     for (int r = 0; r < b->n_requests; ++r) {
       const int64_t m = b->tgt_off_host[r + 1] - b->tgt_off_host[r];
+      if (m < L->std_lo) continue;
       // target groups are `group` wide; the last group of a request is what may be narrow
       for (int64_t g0 = 0; g0 < m; g0 += L->group) {
         if (m - g0 > 32) L->any_wide = true;
@@ -189,10 +229,11 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
         const size_t h = L->h;
         L->un = m.take(2 * 2 * nt * h * d);  // bf16 hi and lo terms
         L->part_y = m.take(4 * kMaxChunks * nt * h * d);
-        L->a2 = m.take(4 * nt * d);
-        L->ml2 = m.take(8 * nt * h);
-        L->tch2 = m.take(4 * (nt + 1));
+        L->ml_r = m.take(8 * kMaxChunks * nt * h);
+        L->tch_r = m.take(4 * (nt + 1));
         L->wvp16 = m.take(2 * n * d * d);
+        L->hdr2 = m.take(sizeof(WsHeader));
+        L->units2 = m.take(sizeof(Unit) * (L->max_units2 + 1));
       }
     } else {
       L->kv32 = m.take(4 * nh * 2 * d);
@@ -308,111 +349,58 @@ stca_status_t check_common(const stca_dims_t* dims, const stca_batch_t* b, const
 }
 
 // ---------------------------------------------------------------- forward
-// Reordered form (App. A.2.2): per layer U = Q W_K^j^T, attention over X,
-// merge with W_V^j, then the same target update as the standard form.
-stca_status_t forward_reordered(const Layout& L, const stca_batch_t* b, const void* hist, const void* tgt,
-                                const stca_weights_t* w, void* out, void* saved, const stca_saved_layout_t& SL,
-                                void* ws, hipStream_t st, Rec& rec) {
-  const int d = L.d, n = L.n, F = L.F;
-  WsHeader* hdr = at<WsHeader>(ws, L.hdr);
-  Unit* units = at<Unit>(ws, L.units);
-  int32_t* tch = at<int32_t>(ws, L.tchunks);
-  {
-    PackJobs pj{};
-    pj.job[0] = {w->wv, at<char>(ws, L.wvp16), d, d, 1};
-    pj.job[1] = {w->wo, at<char>(ws, L.wop), d, d, 1};
-    pj.job[2] = {w->wq, at<char>(ws, L.wqp), d, d, 1};
-    pj.job[3] = {w->w1, at<char>(ws, L.w1p), d, F, 1};
-    pj.job[4] = {w->w2, at<char>(ws, L.w2p), F, d, 1};
-    HIPCHK(fast_pack_many(pj, 5, n, st));
-    HIPCHK(rec.mark("pack"));
-  }
-  FastUpdate f{};
-  f.tg = ceil_div(static_cast<int64_t>(L.nt), 32) < device_cus() ? 16 : 32;
-  f.n_layers = n;
-  f.F = F;
-  f.n_tgt = L.nt;
-  f.tgt = tgt;
-  f.tchunks = at<int32_t>(ws, L.tch2);
-  f.part_acc = at<float>(ws, L.a2);
-  f.part_ml = at<char>(ws, L.ml2);
-  f.QN = at<char>(ws, L.qn);
-  f.WoP = at<char>(ws, L.wop);
-  f.W1P = at<char>(ws, L.w1p);
-  f.W2P = at<char>(ws, L.w2p);
-  f.WqP = at<char>(ws, L.wqp);
-  f.out = out;
-  f.range = &hdr->range;
-  auto state = [&](int i) -> float* {
-    if (saved) return at<float>(saved, SL.s) + (size_t)i * L.nt * d;
-    return at<float>(ws, (i % 2) ? L.state_b : L.state_a);
-  };
-  const size_t wlayer = (size_t)d * d * 2;  // bytes of one layer's bf16 W_K
-  f.mode = 0;
-  f.layer = 0;
-  f.s_out = state(0);
-  HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
-  HIPCHK(fast_reord_qu(d, f.QN, w->wk, at<char>(ws, L.un), L.nt, st)); HIPCHK(rec.mark("reord_u"));
-  for (int i = 0; i < n; ++i) {
-    if (L.reord_wide)
-      HIPCHK(fast_reord_wide(d, units, hdr, L.max_units, at<char>(ws, L.un), hist, L.nh, at<float>(ws, L.part_y),
-                             at<char>(ws, L.part_ml), L.nt, &hdr->range, st));
-    else
-      HIPCHK(fast_reord_attn(d, units, hdr, L.max_units, at<char>(ws, L.un), hist, L.nh, at<float>(ws, L.part_y),
-                             at<char>(ws, L.part_ml), L.nt, st));
-    HIPCHK(rec.mark("reord_attn"));
-    HIPCHK(fast_reord_merge(d, at<float>(ws, L.part_y), at<char>(ws, L.part_ml), tch, at<char>(ws, L.wvp16), i,
-                            at<float>(ws, L.a2), at<char>(ws, L.ml2), at<int32_t>(ws, L.tch2),
-                            saved ? at<float>(saved, SL.lse) + (size_t)i * L.nt * L.h : nullptr, L.nt, st));
-    HIPCHK(rec.mark("reord_merge"));
-    f.mode = 1;
-    f.layer = i;
-    f.s_in = state(i);
-    f.s_out = i + 1 < n ? state(i + 1) : nullptr;
-    f.save_a = saved ? at<float>(saved, SL.a) + (size_t)i * L.nt * d : nullptr;
-    f.save_u = saved ? at<float>(saved, SL.u) + (size_t)i * L.nt * d : nullptr;
-    f.save_lse = nullptr;  // written by the merge
-    HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
-    if (i + 1 < n) {
-      HIPCHK(fast_reord_qu(d, f.QN, static_cast<const char*>(w->wk) + (i + 1) * wlayer, at<char>(ws, L.un), L.nt,
-                           st));
-      HIPCHK(rec.mark("reord_u"));
-    }
-  }
-  return STCA_OK;
-}
-
+// The bf16 path.  Requests in the standard form: per layer the history
+// projected to K/V inside the attention kernel (or K/V written once and
+// streamed), partials per history chunk.  Requests in the reordered form
+// (App. A.2.2): per layer U = Q W_K^j^T, attention over X itself, merge with
+// W_V^j into a single-chunk partial.  Each form has its own schedule; then
+// one target update per layer merges every target's partials.
 stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* hist, const void* tgt,
                            const stca_weights_t* w, void* out, void* saved, const stca_saved_layout_t& SL,
                            void* ws, hipStream_t st, Rec& rec) {
   HIPCHK(rec.start());
   const int d = L.d, n = L.n, F = L.F;
+  const bool std_part = !L.reord || L.mixed, reo_part = L.reord;
   WsHeader* hdr = at<WsHeader>(ws, L.hdr);
   Unit* units = at<Unit>(ws, L.units);
   int32_t* tch = at<int32_t>(ws, L.tchunks);
-  HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, L.group, units, L.max_units,
-                      tch, hdr, st)); HIPCHK(rec.mark("sched"));
-  if (L.reord) return forward_reordered(L, b, hist, tgt, w, out, saved, SL, ws, st, rec);
+  // the reordered schedule: its own header and units when both forms run,
+  // else the workspace's
+  WsHeader* hdr2 = L.mixed ? at<WsHeader>(ws, L.hdr2) : hdr;
+  Unit* units2 = reo_part ? at<Unit>(ws, L.units2) : nullptr;
+  int32_t* tch_r = reo_part ? at<int32_t>(ws, L.tch_r) : nullptr;
+  if (std_part)
+    HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, L.group, units,
+                        L.max_units, tch, hdr, st, L.std_lo));
+  if (std_part) HIPCHK(rec.mark("sched"));
+  if (reo_part)
+    HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks2, L.group2, units2,
+                        L.max_units2, tch_r, hdr2, st, L.reord_lo, L.reord_hi));
+  if (reo_part) HIPCHK(rec.mark("sched"));
   {
     PackJobs pj{};
-    pj.job[0] = {w->wk, at<char>(ws, L.wkp), d, d, 0};
-    pj.job[1] = {w->wv, at<char>(ws, L.wvp), d, d, 0};
-    pj.job[2] = {w->wo, at<char>(ws, L.wop), d, d, 1};
-    pj.job[3] = {w->wq, at<char>(ws, L.wqp), d, d, 1};
-    pj.job[4] = {w->w1, at<char>(ws, L.w1p), d, F, 1};
-    pj.job[5] = {w->w2, at<char>(ws, L.w2p), F, d, 1};
-    HIPCHK(fast_pack_many(pj, 6, n, st));
+    int nj = 0;
+    if (std_part) {
+      pj.job[nj++] = {w->wk, at<char>(ws, L.wkp), d, d, 0};
+      pj.job[nj++] = {w->wv, at<char>(ws, L.wvp), d, d, 0};
+    }
+    if (reo_part) pj.job[nj++] = {w->wv, at<char>(ws, L.wvp16), d, d, 1};
+    pj.job[nj++] = {w->wo, at<char>(ws, L.wop), d, d, 1};
+    pj.job[nj++] = {w->wq, at<char>(ws, L.wqp), d, d, 1};
+    pj.job[nj++] = {w->w1, at<char>(ws, L.w1p), d, F, 1};
+    pj.job[nj++] = {w->w2, at<char>(ws, L.w2p), F, d, 1};
+    HIPCHK(fast_pack_many(pj, nj, n, st));
     HIPCHK(rec.mark("pack"));
   }
-  const bool mat = L.mat;
   char* kv = at<char>(ws, L.kv);
-  if (mat) {
+  if (L.mat) {
     if (L.nh > 0)
       HIPCHK(fast_proj(d, hist, L.nh, L.nblocks, at<char>(ws, L.wkp), at<char>(ws, L.wvp), kv, n,
                        fast_proj_parts(n, L.nblocks, device_cus()), st));
     HIPCHK(rec.mark("proj"));
   }
   const size_t kv_layer = (size_t)L.nblocks * kBlockTokens * 2 * d * 2;
+  const size_t wlayer = (size_t)d * d * 2;  // bytes of one layer's bf16 W_K
   FastUpdate f{};
   f.tg = ceil_div(static_cast<int64_t>(L.nt), 32) < device_cus() ? 16 : 32;
   f.n_layers = n;
@@ -439,16 +427,20 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   f.s_out = state(0);
   HIPCHK(fast_update(d, f, st)); HIPCHK(rec.mark("update"));
   const int grid = static_cast<int>(std::min<int64_t>(L.max_units, 8 * (int64_t)device_cus()));
-  // the fused kernel keeps two half-head workgroups per CU resident (two
-  // 256-VGPR waves per SIMD) and loops over its units, loading its weight
-  // columns once: one workgroup pair ("stream") per CU
+  // the fused kernel is persistent: one workgroup per CU, looping over its
+  // units with its weight columns loaded once
   const int fgrid = static_cast<int>(std::max<int64_t>(1, std::min<int64_t>(L.max_units, device_cus())));
   for (int i = 0; i < n; ++i) {
-    if (mat) {
+    if (reo_part) {
+      HIPCHK(fast_reord_qu(d, f.QN, static_cast<const char*>(w->wk) + i * wlayer, at<char>(ws, L.un), tch_r, L.nt,
+                           st));
+      HIPCHK(rec.mark("reord_u"));
+    }
+    if (std_part && L.mat) {
       HIPCHK(fast_attn(d, units, hdr, grid, f.QN, kv + i * kv_layer, at<float>(ws, L.part_acc),
                        at<char>(ws, L.part_ml), L.nt, st));
       HIPCHK(rec.mark("attn"));
-    } else {
+    } else if (std_part) {
       for (int wide = 0; wide < 2; ++wide) {
         if (!(wide ? L.any_wide : L.any_narrow)) {  // no request of this width: nothing to launch
           HIPCHK(rec.mark(wide ? "fused_wide" : "fused"));
@@ -458,6 +450,19 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
                           at<float>(ws, L.part_acc), at<char>(ws, L.part_ml), L.nt, st));
         HIPCHK(rec.mark(wide ? "fused_wide" : "fused"));
       }
+    }
+    if (reo_part) {
+      if (L.reord_wide)
+        HIPCHK(fast_reord_wide(d, units2, hdr2, L.max_units2, at<char>(ws, L.un), hist, L.nh,
+                               at<float>(ws, L.part_y), at<char>(ws, L.ml_r), L.nt, &hdr->range, st));
+      else
+        HIPCHK(fast_reord_attn(d, units2, hdr2, L.max_units2, at<char>(ws, L.un), hist, L.nh,
+                               at<float>(ws, L.part_y), at<char>(ws, L.ml_r), L.nt, st));
+      HIPCHK(rec.mark("reord_attn"));
+      // a of the reordered requests as their single chunk of the update's partials
+      HIPCHK(fast_reord_merge(d, at<float>(ws, L.part_y), at<char>(ws, L.ml_r), tch_r, at<char>(ws, L.wvp16), i,
+                              at<float>(ws, L.part_acc), at<char>(ws, L.part_ml), tch, L.nt, st));
+      HIPCHK(rec.mark("reord_merge"));
     }
     f.mode = 1;
     f.layer = i;
@@ -968,8 +973,14 @@ int stca_forward_launch_count(const stca_dims_t* dims, const stca_batch_t* batch
   Layout L;
   if (make_layout(dims, batch, 0, false, &L) != STCA_OK) return -1;
   // sched, one repack launch, the initial update, then per layer
-  if (L.path == 1 && L.reord) return 1 + 1 + 1 + 1 + 4 * L.n - 1;
-  if (L.path == 1) return L.mat ? 1 + 1 + 1 + 1 + 2 * L.n : 1 + 1 + 1 + 3 * L.n;
+  if (L.path == 1) {
+    const bool std_part = !L.reord || L.mixed, reo_part = L.reord;
+    // schedules, one repack launch, the initial update, the K/V GEMM; per
+    // layer: U, the standard form's attention (two fused launches or one
+    // over materialised K/V), the reordered attention and merge, the update
+    const int per_layer = (reo_part ? 3 : 0) + (std_part ? (L.mat ? 1 : 2) : 0) + 1;
+    return (std_part ? 1 : 0) + (reo_part ? 1 : 0) + 1 + 1 + (L.mat ? 1 : 0) + per_layer * L.n;
+  }
   return 1 + 1 + 8 * L.n + 1;
 }
 

@@ -76,20 +76,22 @@ inline int device_cus() {
 // Chunk length (in 32-row blocks) of the split over history rows: aim at about
 // `per_cu` attention units per CU (four for the standard form; one for the
 // reordered form, whose units stream X with little work per block and whose
-// merge cost grows with the chunk count).  A positive `forced` (the caller's
+// merge cost grows with the chunk count), over `rows` history rows (the
+// whole batch by default).  A positive `forced` (the caller's
 // stca_dims_t.chunk_blocks) replaces the choice.
-inline int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu, int forced) {
+inline int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu, int forced, int64_t rows = -1) {
   if (forced >= 1) return forced;
-  const int64_t nb = ceil_div(b->n_hist, kBlockTokens);
+  const int64_t nb = ceil_div(rows >= 0 ? rows : b->n_hist, kBlockTokens);
   int64_t c = ceil_div(nb, per_cu * static_cast<int64_t>(n_cu));
   if (c < 8) c = 8;
   if (c > (1 << 20)) c = 1 << 20;
   return static_cast<int>(c);
 }
 
-inline int64_t max_units_for(const stca_batch_t* b, int chunk_blocks, int group) {
+inline int64_t max_units_for(const stca_batch_t* b, int chunk_blocks, int group, int m_lo = 1,
+                             int m_hi = 1 << 30) {
   if (b->hist_off_host)
-    return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks, group);
+    return host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, chunk_blocks, group, m_lo, m_hi);
   return (ceil_div(b->n_tgt, group) + b->n_requests) * kMaxChunks;
 }
 

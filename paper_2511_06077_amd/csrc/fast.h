@@ -145,10 +145,12 @@ hipError_t fast_update_grad(int D, const UpdateGrad& f, hipStream_t st);
 // 32 / H targets: U = per-head Q W_K^j^T (bf16 hi and lo terms
 // [n_tgt][H][2][D]), the attention
 // over X writing per-chunk y partials ([16][n_tgt][H][D] fp32 and (max, sum)
-// [16][n_tgt][H]), and the merge that forms a = y W_V^j (fp32 [n_tgt][D]) with
-// single-chunk records (ml_out (0, 1), tch_out 1) for fast_update.
+// [16][n_tgt][H]), and the merge that forms a = y W_V^j (fp32 [n_tgt][D]) as
+// a single-chunk record for fast_update (ml_out (log2-sum-exp, 1), tch_out 1)
+// for every target with a nonzero chunk count in `tchunks`.
 size_t reord_attn_lds(int D);
-hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, int64_t n_tgt, hipStream_t st);
+hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, const int32_t* tchunks,
+                         int64_t n_tgt, hipStream_t st);
 hipError_t fast_reord_attn(int D, const Unit* units, const WsHeader* hdr, int64_t max_units, const void* UN,
                            const void* X, int64_t n_hist, float* part_y, void* part_ml, int64_t n_tgt,
                            hipStream_t st);
@@ -160,6 +162,6 @@ hipError_t fast_reord_wide(int D, const Unit* units, const WsHeader* hdr, int64_
                            int32_t* range, hipStream_t st);
 hipError_t fast_reord_merge(int D, const float* part_y, const void* part_ml, const int32_t* tchunks,
                             const void* WvP16, int layer, float* a_out, void* ml_out, int32_t* tch_out,
-                            float* save_lse, int64_t n_tgt, hipStream_t st);
+                            int64_t n_tgt, hipStream_t st);
 
 }  // namespace stca

@@ -6,11 +6,13 @@
 namespace stca {
 
 // ---- scheduler (sched.hip)
-// `group`: targets per unit (1..kWideGroup).
+// `group`: targets per unit (1..kWideGroup).  Only requests with m_lo..m_hi
+// targets get units (and chunk counts); the others keep a zero chunk count.
 hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
                         int chunk_blocks, int group, Unit* units, int64_t max_units, int32_t* tchunks,
-                        WsHeader* hdr, hipStream_t st);
-int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks, int group);
+                        WsHeader* hdr, hipStream_t st, int m_lo = 1, int m_hi = 1 << 30);
+int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks, int group,
+                         int m_lo = 1, int m_hi = 1 << 30);
 
 // ---- generic fp32-arithmetic path (generic.hip)
 enum GemmEpi { kEpiStore = 0, kEpiAddRes = 1, kEpiRelu = 2 };

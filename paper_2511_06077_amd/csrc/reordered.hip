@@ -95,15 +95,20 @@ __device__ __forceinline__ f16x8 bf8_to_h8(const uint4& v) {
 // W_K^j (dims x head dims) Q_j^T: the B operand is the wave's slice of the
 // permuted QN row (k-step s holds head dims 16 s + 4 hi + {0..3, 8..11}), the A
 // operand W_K[dim][32 j + the same head dims].
+// Targets with a zero chunk count in `tchunks` (requests in the standard form
+// when a batch runs both forms) get no U; a wave whose 32 targets have none
+// to form exits.
 template <int D>
 __global__ __launch_bounds__(64) void reord_qu_kernel(const f16x8* __restrict__ QN, const bf16_bits* __restrict__ Wk,
-                                                      __bf16* __restrict__ UN, int64_t n_tgt) {
+                                                      __bf16* __restrict__ UN, const int32_t* __restrict__ tchunks,
+                                                      int64_t n_tgt) {
   constexpr int H = D / DH;
   const int j = blockIdx.y;
   const int lane = threadIdx.x;
   const int tcol = lane % 32, hi = lane / 32;
   const int64_t t = (int64_t)blockIdx.x * 32 + tcol;
-  const bool live = t < n_tgt;
+  const bool live = t < n_tgt && tchunks[t] > 0;
+  if (__builtin_amdgcn_ballot_w64(live) == 0) return;
   f16x8 qb[2];
 #pragma unroll
   for (int s = 0; s < 2; ++s) qb[s] = live ? QN[(t * D + 32 * j + 16 * s + 8 * hi) / 8] : zero8();
@@ -578,16 +583,18 @@ __global__ __launch_bounds__(64 * kWideWaves) void reord_wide_kernel(const Unit*
 // One wave per (32 targets, head j): it merges the chunk partials of y_tj
 // into fp16 rows in LDS (two lanes per target, half of the d columns each),
 // then forms a_j^T = W_V^j^T y_j^T (A operand: the packed fp16 W_V, whose
-// column block j is head j) and writes a (fp32) with a single-chunk
-// (max 0, sum 1) record per (target, head) for the update kernel.
+// column block j is head j) and writes a (fp32) as the single chunk of the
+// update kernel's partials: chunk count 1, (max, sum) = (the scores'
+// log2-sum-exp, 1), so the update's merge returns a and the lse unchanged.
+// Targets whose chunk count is 0 (requests in the standard form when a
+// batch runs both forms) are left alone.
 template <int D>
 __global__ __launch_bounds__(64) void reord_merge_kernel(const float* __restrict__ part_y,
                                                         const float2* __restrict__ part_ml,
                                                         const int32_t* __restrict__ tchunks,
                                                         const f16x8* __restrict__ WvP16, int layer,
                                                         float* __restrict__ a_out, float2* __restrict__ ml_out,
-                                                        int32_t* __restrict__ tch_out, float* __restrict__ save_lse,
-                                                        int64_t n_tgt) {
+                                                        int32_t* __restrict__ tch_out, int64_t n_tgt) {
   constexpr int H = D / DH;
   constexpr int KS = D / 16;
   constexpr int YROW = D + 8;  // padded fp16 row
@@ -599,35 +606,58 @@ __global__ __launch_bounds__(64) void reord_merge_kernel(const float* __restrict
     const int row = lane / 2, part = lane % 2;  // columns [part D/2, (part + 1) D/2)
     const int64_t t = tb + row;
     uint16_t* y = ys + row * YROW + part * (D / 2);
-    if (t < n_tgt) {
-      const int nch = tchunks[t];
-      float M = -INFINITY;
-      for (int c = 0; c < nch; ++c) M = fmaxf(M, part_ml[((int64_t)c * n_tgt + t) * H + j].x);
+    const int nch = t < n_tgt ? tchunks[t] : 0;
+    if (__builtin_amdgcn_ballot_w64(nch > 0) == 0) return;  // no target of this wave in the reordered form
+    if (nch > 0) {
+      // every chunk's (max, sum) requested at once, and each chunk's weight
+      float2 mlc[kMaxChunks];
+#pragma unroll
+      for (int c = 0; c < kMaxChunks; ++c)
+        mlc[c] = c < nch ? part_ml[((int64_t)c * n_tgt + t) * H + j] : make_float2(-INFINITY, 0.f);
+      float M = mlc[0].x;
+#pragma unroll
+      for (int c = 1; c < kMaxChunks; ++c) M = fmaxf(M, mlc[c].x);
       float L = 0.f;
-      for (int c = 0; c < nch; ++c) L += __builtin_amdgcn_exp2f(part_ml[((int64_t)c * n_tgt + t) * H + j].x - M) *
-                                         part_ml[((int64_t)c * n_tgt + t) * H + j].y;
+      float wch[kMaxChunks];
+#pragma unroll
+      for (int c = 0; c < kMaxChunks; ++c) {
+        wch[c] = c < nch ? __builtin_amdgcn_exp2f(mlc[c].x - M) : 0.f;
+        L += wch[c] * mlc[c].y;
+      }
       const float inv = 1.f / L;
+#pragma unroll
+      for (int c = 0; c < kMaxChunks; ++c) wch[c] *= inv;
       for (int c0 = 0; c0 < D / 2; c0 += 16) {
         float acc[16];
 #pragma unroll
         for (int i = 0; i < 16; ++i) acc[i] = 0.f;
-        for (int c = 0; c < nch; ++c) {
-          const float2 ml = part_ml[((int64_t)c * n_tgt + t) * H + j];
-          const float wc = __builtin_amdgcn_exp2f(ml.x - M) * inv;
-          const float4* py = reinterpret_cast<const float4*>(part_y + (((int64_t)c * n_tgt + t) * H + j) * D +
-                                                             part * (D / 2) + c0);
+        // four chunks' loads in flight at a time (one memory round trip per
+        // four chunks instead of one per chunk)
+        for (int cb = 0; cb < nch; cb += 4) {
+          float4 v[4][4];
+          float wc[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const float4 v = py[q];
-            acc[4 * q] += wc * v.x, acc[4 * q + 1] += wc * v.y, acc[4 * q + 2] += wc * v.z, acc[4 * q + 3] += wc * v.w;
+          for (int cc = 0; cc < 4; ++cc) {
+            const int c = cb + cc < nch ? cb + cc : cb;
+            wc[cc] = cb + cc < nch ? wch[cb + cc < kMaxChunks ? cb + cc : 0] : 0.f;
+            const float4* py = reinterpret_cast<const float4*>(part_y + (((int64_t)c * n_tgt + t) * H + j) * D +
+                                                               part * (D / 2) + c0);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[cc][q] = py[q];
           }
+#pragma unroll
+          for (int cc = 0; cc < 4; ++cc)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              acc[4 * q] += wc[cc] * v[cc][q].x, acc[4 * q + 1] += wc[cc] * v[cc][q].y;
+              acc[4 * q + 2] += wc[cc] * v[cc][q].z, acc[4 * q + 3] += wc[cc] * v[cc][q].w;
+            }
         }
 #pragma unroll
         for (int i = 0; i < 16; ++i) y[c0 + i] = __builtin_bit_cast(uint16_t, static_cast<_Float16>(acc[i]));
       }
       if (part == 0) {
-        if (save_lse) save_lse[t * H + j] = (M + log2f(L)) * kLn2;
-        ml_out[t * H + j] = make_float2(0.f, 1.f);
+        ml_out[t * H + j] = make_float2(M + log2f(L), 1.f);
         if (j == 0) tch_out[t] = 1;
       }
     } else {
@@ -646,7 +676,7 @@ __global__ __launch_bounds__(64) void reord_merge_kernel(const float* __restrict
   for (int ks = 0; ks < KS; ++ks) acc = mfma16(wr[ks], *reinterpret_cast<const f16x8*>(yb + 16 * ks), acc);
   // lane holds a[t][32 j + 8 g + 4 hi + k] for g, k < 4
   const int64_t t = tb + tcol;
-  if (t < n_tgt) {
+  if (t < n_tgt && tchunks[t] > 0) {
     float* ap = a_out + t * D + 32 * j + 4 * hi;
 #pragma unroll
     for (int g = 0; g < 4; ++g)
@@ -671,12 +701,13 @@ hipError_t allow_lds(K kernel, size_t bytes) {
 
 size_t reord_attn_lds(int D) { return reord_main_lds(D) + (size_t)32 * (D + 8) * 2; }
 
-hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, int64_t n_tgt, hipStream_t st) {
+hipError_t fast_reord_qu(int D, const void* QN, const void* Wk_layer, void* UN, const int32_t* tchunks,
+                         int64_t n_tgt, hipStream_t st) {
   if (n_tgt == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(ceil_div(n_tgt, 32)), D / DH);
 #define STCA_QU(DD)                                                                                              \
   hipLaunchKernelGGL(reord_qu_kernel<DD>, g, dim3(64), 0, st, (const f16x8*)QN, (const bf16_bits*)Wk_layer, \
-                     (__bf16*)UN, n_tgt)
+                     (__bf16*)UN, tchunks, n_tgt)
   switch (D) {
     case 64: STCA_QU(64); break;
     case 128: STCA_QU(128); break;
@@ -731,12 +762,12 @@ hipError_t fast_reord_wide(int D, const Unit* units, const WsHeader* hdr, int64_
 
 hipError_t fast_reord_merge(int D, const float* part_y, const void* part_ml, const int32_t* tchunks,
                             const void* WvP16, int layer, float* a_out, void* ml_out, int32_t* tch_out,
-                            float* save_lse, int64_t n_tgt, hipStream_t st) {
+                            int64_t n_tgt, hipStream_t st) {
   if (n_tgt == 0) return hipSuccess;
   dim3 g(static_cast<unsigned>(ceil_div(n_tgt, 32)), D / DH);
 #define STCA_RM(DD)                                                                                             \
   hipLaunchKernelGGL(reord_merge_kernel<DD>, g, dim3(64), 0, st, part_y, (const float2*)part_ml, tchunks,      \
-                     (const f16x8*)WvP16, layer, a_out, (float2*)ml_out, tch_out, save_lse, n_tgt)
+                     (const f16x8*)WvP16, layer, a_out, (float2*)ml_out, tch_out, n_tgt)
   switch (D) {
     case 64: STCA_RM(64); break;
     case 128: STCA_RM(128); break;

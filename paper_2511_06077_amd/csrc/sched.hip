@@ -13,7 +13,9 @@
 //
 // One workgroup of 1024 threads; each thread owns a contiguous run of requests.
 // Invalid segments produce no units and set the workspace status, so no later
-// kernel reads outside the buffers whatever the offsets hold.
+// kernel reads outside the buffers whatever the offsets hold.  Only requests
+// with m_lo..m_hi targets get units (a batch can be split between two forms
+// of the attention, each with its own schedule); every request is validated.
 #include "common.h"
 #include "internal.h"
 
@@ -29,7 +31,7 @@ struct ReqPlan {
 };
 
 __device__ ReqPlan plan_request(const int32_t* hoff, const int32_t* toff, int r, int64_t n_hist,
-                                int64_t n_tgt, int chunk_blocks, int group) {
+                                int64_t n_tgt, int chunk_blocks, int group, int m_lo, int m_hi) {
   ReqPlan p{};
   p.h0 = hoff[r];
   p.h1 = hoff[r + 1];
@@ -39,7 +41,7 @@ __device__ ReqPlan plan_request(const int32_t* hoff, const int32_t* toff, int r,
          (p.t1 == p.t0 || p.h1 > p.h0);
   p.nch = 0;
   p.ng = 0;
-  if (!p.ok || p.t1 == p.t0) return p;
+  if (!p.ok || p.t1 == p.t0 || p.t1 - p.t0 < m_lo || p.t1 - p.t0 > m_hi) return p;
   p.bl = p.h0 / kBlockTokens;
   const int32_t bh = static_cast<int32_t>(ceil_div(p.h1, kBlockTokens));
   const int32_t nb = bh - p.bl;
@@ -71,7 +73,7 @@ __device__ int64_t block_scan(int64_t* scan, int64_t mine) {
 __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __restrict__ hoff,
                                                               const int32_t* __restrict__ toff, int R,
                                                               int64_t n_hist, int64_t n_tgt,
-                                                              int chunk_blocks, int group,
+                                                              int chunk_blocks, int group, int m_lo, int m_hi,
                                                               Unit* __restrict__ units,
                                                               int64_t max_units,
                                                               int32_t* __restrict__ tchunks,
@@ -89,7 +91,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
   int64_t narrow = 0, wide = 0;
   bool any_bad = false;
   for (int r = rb; r < re; ++r) {
-    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks, group);
+    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks, group, m_lo, m_hi);
     any_bad |= !p.ok;
     for (int g = 0; g < p.ng; ++g) (group_size(p, g, group) > 32 ? wide : narrow) += p.nch;
   }
@@ -100,7 +102,7 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
   int64_t uw = total_narrow + block_scan(scan, wide);
   const int64_t total = total_narrow + scan[kSchedThreads - 1];
   for (int r = rb; r < re; ++r) {
-    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks, group);
+    ReqPlan p = plan_request(hoff, toff, r, n_hist, n_tgt, chunk_blocks, group, m_lo, m_hi);
     if (p.nch == 0) continue;
     const int32_t bh = static_cast<int32_t>(ceil_div(p.h1, kBlockTokens));
     for (int g = 0; g < p.ng; ++g) {
@@ -133,19 +135,20 @@ __global__ __launch_bounds__(kSchedThreads) void sched_kernel(const int32_t* __r
 
 hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
                         int chunk_blocks, int group, Unit* units, int64_t max_units, int32_t* tchunks,
-                        WsHeader* hdr, hipStream_t st) {
+                        WsHeader* hdr, hipStream_t st, int m_lo, int m_hi) {
   if (group < 1 || group > kWideGroup) return hipErrorInvalidValue;
   hipLaunchKernelGGL(sched_kernel, dim3(1), dim3(kSchedThreads), 0, st, hoff, toff, R, n_hist, n_tgt,
-                     chunk_blocks, group, units, max_units, tchunks, hdr);
+                     chunk_blocks, group, m_lo, m_hi, units, max_units, tchunks, hdr);
   return hipGetLastError();
 }
 
 // Host mirror of plan_request for exact unit counts when host offsets exist.
-int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks, int group) {
+int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks, int group, int m_lo,
+                         int m_hi) {
   int64_t n = 0;
   for (int r = 0; r < R; ++r) {
     const int64_t h0 = hoff[r], h1 = hoff[r + 1], t0 = toff[r], t1 = toff[r + 1];
-    if (t1 == t0) continue;
+    if (t1 == t0 || t1 - t0 < m_lo || t1 - t0 > m_hi) continue;
     const int64_t nb = ceil_div(h1, kBlockTokens) - h0 / kBlockTokens;
     int64_t nch = ceil_div(nb, chunk_blocks);
     nch = nch < 1 ? 1 : (nch > kMaxChunks ? kMaxChunks : nch);

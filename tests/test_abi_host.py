@@ -139,12 +139,17 @@ def test_materialized_kv_needs_workspace_for_every_layer():
 def test_reordered_form_selection():
     """Requests with at most 32 / h targets (host offsets known) run the
     reordered attention: its launch sequence is 3 + 4 n launches against the
-    standard form's 3 + 3 n."""
+    standard form's 3 + 3 n; a batch with both kinds of request runs each in
+    its own form."""
     n = GOOD_DIMS["n_layers"]
     small, keep1 = fake_batch([0, 40, 100, 101], [0, 4, 5, 8])   # m = 4, 1, 3 <= 32 / 8
     wide, keep2 = fake_batch([0, 40, 100], [0, 5, 9])            # m = 5
     assert stca.stca_forward_launch_count(dims(), small) == 3 + 4 * n
-    assert stca.stca_forward_launch_count(dims(), wide) == 3 + 3 * n
+    # m = 5 and m = 4: each request in its own form (two schedules; per layer
+    # U, two fused launches, the reordered attention and merge, the update)
+    assert stca.stca_forward_launch_count(dims(), wide) == 4 + 6 * n
+    big, keep5 = fake_batch([0, 40, 100], [0, 5, 14])
+    assert stca.stca_forward_launch_count(dims(), big) == 3 + 3 * n
     assert stca.stca_forward_launch_count(dims(d_model=128, n_heads=4), wide) == 3 + 4 * n  # 32 / 4 = 8
     nohost = stca.batch(3, 101, 8, 0x10000, 0x20000, None, None)
     assert stca.stca_forward_launch_count(dims(), nohost) == 3 + 3 * n

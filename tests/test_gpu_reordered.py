@@ -178,3 +178,27 @@ def test_reordered_wide_long_history_sampled_parity(torch):
     reordered form (8 column tiles per unit), oracle on 16 sampled requests."""
     from test_gpu_forward import _sampled_parity
     _sampled_parity(torch, "long_bf16_R128_m32_L10240_d256", 16, 7, attn="reordered")
+
+
+@pytest.mark.parametrize("d,h", [(256, 8), (128, 4), (64, 2)])
+@pytest.mark.parametrize("chunk", [0, 2])
+@pytest.mark.parametrize("kv", ["auto", "materialize"])
+def test_mixed_forms_parity(torch, d, h, chunk, kv):
+    """A batch with requests of 1 .. 32 / h targets (reordered form) and of
+    more (standard form; fused or materialised K/V) runs each request in its
+    own form in one call: two schedules, one target update.  Against the
+    oracle, and within the bar of the same batch in the standard form."""
+    from paper_2511_06077_amd import stca
+    cap = 32 // h
+    L = [700, 33, 1, 129, 2048, 65, 7, 300, 31, 1024]
+    M = [cap, cap + 1, 1, 40, 2, 0, 64, cap, 17, 1]
+    b = W.make_custom_batch("mixed", L, M, d_model=d, n_heads=h, n_layers=2, dtype="bf16", seed=44)
+    y, a, lse, db = run_gpu(torch, b, kv=kv, chunk_blocks=chunk)
+    n_launch = stca.stca_forward_launch_count(db.dims, db.batch)
+    assert n_launch == (5 + 5 * 2 if kv == "materialize" else 4 + 6 * 2), n_launch
+    assert db.device_status() == 0
+    check_against_oracle(b, y, a, lse, TOL["bf16"])
+    ys, as_, _, _ = run_gpu(torch, b, kv=kv, attn="standard", chunk_blocks=chunk)
+    e_y, e_a = rowerr(y, ys), max(rowerr(a[i], as_[i]) for i in range(2))
+    print(f"[mixed] per-request forms vs standard form: err(Y)={e_y:.2e} err(a)={e_a:.2e}", flush=True)
+    assert e_y <= TOL["bf16"] and e_a <= TOL["bf16"]
