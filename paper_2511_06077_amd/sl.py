@@ -2,7 +2,12 @@
 details"): a batch of full histories is cut to Beta-sampled temporal suffixes
 under a token budget and packed without padding, by the library's host
 functions (stca_sl_sample, stca_sl_allocate, stca_sl_pack); the result is an
-ordinary ragged batch for stca_forward / stca_backward."""
+ordinary ragged batch for stca_forward / stca_backward.
+
+The row gather that assembles the packed batch (the kept suffix rows of the
+full histories, by the index stca_sl_pack returns) is data preparation on
+the host, as a data loader would do it; no computation of the method takes
+place in it."""
 from __future__ import annotations
 
 from dataclasses import replace
