@@ -282,7 +282,8 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
       const int di = static_cast<int>(d), Fi = static_cast<int>(F), nti = static_cast<int>(nt);
       // (the fused form runs the target-side weight gradients of a layer,
       // with dW_Q of the layer above, as one group whose splits share it)
-      L->gpart_floats = std::max({gemm_mfma_part_floats(di, 2 * di * static_cast<int>(n), static_cast<int>(nh8)),
+      L->gpart_floats = std::max({gemm_ring_part_floats(di, 2 * di * static_cast<int>(n), static_cast<int>(nh8),
+                                                        device_cus()),
                                   gemm_mfma_part_floats(Fi, di, nti) + gemm_mfma_part_floats(di, Fi, nti) +
                                       2 * gemm_mfma_part_floats(di, di, nti)});
     }
@@ -905,17 +906,18 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     // dX = sum_i [dK^i | dV^i] [W_K^i | W_V^i]^T as one product with
     // K = n 2d, written once
     float* dwkv = at<float>(ws, L.dwkv);
+    const int n_cu = device_cus();
     if (L.bfused)
-      HIPCHK(gemm_mfma(d, n * 2 * d, static_cast<int>(nh), static_cast<const bf16_bits*>(hist), d, 1,
+      HIPCHK(gemm_ring(d, n * 2 * d, static_cast<int>(nh), static_cast<const bf16_bits*>(hist), d, 1,
                        static_cast<const bf16_bits*>(dkv), n * 2 * d, 0, dwkv, n * 2 * d, 1.f, 0,
-                       at<float>(ws, L.gpart), L.gpart_floats, st));
+                       at<float>(ws, L.gpart), L.gpart_floats, n_cu, st));
     else
-      HIPCHK(gemm_mfma(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
-                       L.gpart_floats, st));
+      HIPCHK(gemm_ring(d, n * 2 * d, nh8, xt, nh8, 0, dkvt, nh8, 1, dwkv, n * 2 * d, 1.f, 0, at<float>(ws, L.gpart),
+                       L.gpart_floats, n_cu, st));
     HIPCHK(split_dwkv(dwkv, n, d, dw->dwk, dw->dwv, st));
     HIPCHK(rec.mark("dw_kv"));
-    HIPCHK(gemm_mfma(static_cast<int>(nh), d, n * 2 * d, static_cast<const bf16_bits*>(dkv), n * 2 * d, 0, wkv_all,
-                     n * 2 * d, 1, dhist, d, 1.f, 0, nullptr, 0, st));
+    HIPCHK(gemm_ring(static_cast<int>(nh), d, n * 2 * d, static_cast<const bf16_bits*>(dkv), n * 2 * d, 0, wkv_all,
+                     n * 2 * d, 1, dhist, d, 1.f, 0, nullptr, 0, n_cu, st));
     HIPCHK(rec.mark("dx"));
   }
   HIPCHK(convert(0, 0, ds, dtgt, nt * d, st));

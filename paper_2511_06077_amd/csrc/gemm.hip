@@ -9,22 +9,23 @@
 // 128 x 128 output tile per workgroup of four waves (2 x 2), each wave 64 x 64
 // as 2 x 2 v_mfma_f32_32x32x16_bf16 tiles.  64-deep k tiles go global ->
 // registers (16-byte loads, the next tile's loads in flight while the current
-// one is multiplied) -> LDS (rows with k contiguous; one buffer, 37 KB, so
-// four workgroups share a CU) -> MFMA operands (16-byte LDS reads).  An
-// operand whose source has k contiguous is copied row by row into rows padded
-// by 16 bytes; one whose source has the row index contiguous (X and dK | dV
-// in [dW_K | dW_V], both operands of the target-side weight gradients) is
-// transposed on its way into LDS: each thread turns an 8-row x 4-k block of
-// registers into 8-byte runs, written into unpadded rows whose 16-byte units
-// are permuted per row group so that neither the writes nor the operand reads
-// meet bank conflicts.  Tiles are handed to the eight XCDs in contiguous
-// ranges, so the tiles that share a row block of A (and, split over K, every
-// tile of one K range) run on one XCD and share its L2.  A split over K
-// writes per-split partial tiles that a second kernel sums.
+// one is multiplied) -> LDS (one buffer, 37 KB, so four workgroups share a
+// CU) -> MFMA operands.  An operand whose source has k contiguous is copied
+// row by row into rows padded by 16 bytes and read back 16 bytes per lane.
+// One whose source has the row index contiguous (X and dK | dV in
+// [dW_K | dW_V], both operands of the target-side weight gradients) keeps
+// that layout in LDS (one 256-byte row per k, 16-byte units permuted per
+// k row) and is read back with gfx950's transposing LDS reads, which hand
+// each lane four consecutive k of its own row.  Neither form meets LDS bank
+// conflicts on writes or reads.  Tiles are handed to the eight XCDs in
+// contiguous ranges, so the tiles that share a row block of A (and, split
+// over K, every tile of one K range) run on one XCD and share its L2.  A
+// split over K writes per-split partial tiles that a second kernel sums.
 #include <algorithm>
 
 #include "common.h"
 #include "internal.h"
+#include "ring.h"
 
 namespace stca {
 
@@ -40,27 +41,27 @@ __device__ __forceinline__ f32x16 mfma_bf(const bf16x8& a, const bf16x8& b, cons
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
 }
 
-// One operand tile: 128 rows x 64 k = 1024 vectors of 8 bf16, four per thread.
-// kcontig: element (row, k) at src[row * ld + k]; else at src[k * ld + row],
-// and then thread t holds the rows 8 (t % 16) .. + 7 of the four k rows
-// 4 (t / 16) .. + 3, which it transposes on the way into LDS.
-// Vectors are whole or absent: the caller guarantees that the contiguous
-// extent (K, or the row count) is a multiple of 8 and chunk ends are multiples
-// of BK.
+// One operand tile: 128 rows x 64 k = 1024 vectors of 8 bf16, four per thread
+// (vector v = thread + 256 i).  kcontig: element (row, k) at src[row * ld + k],
+// vector v = row v / 8, k 8 (v % 8) .. + 7; else at src[k * ld + row],
+// vector v = k v / 16, rows 8 (v % 16) .. + 7 (16 threads read one 256-byte
+// run of a k row).  Vectors are whole or absent: the caller guarantees that
+// the contiguous extent (K, or the row count) is a multiple of 8 and chunk
+// ends are multiples of BK.
 template <bool kcontig>
 __device__ __forceinline__ void load_tile(u16x8 (&r)[4], const bf16_bits* __restrict__ src, int64_t ld, int row0,
                                           int nrows, int k0, int kend) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
+    const int v = threadIdx.x + 256 * i;
     bool ok;
     int64_t off;
     if (kcontig) {
-      const int v = threadIdx.x + 256 * i;
       const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
       ok = row0 + row < nrows && k0 + kk < kend;
       off = (int64_t)(row0 + row) * ld + k0 + kk;
     } else {
-      const int row = (threadIdx.x % 16) * 8, kk = (threadIdx.x / 16) * 4 + i;
+      const int kk = v / (BM / 8), row = (v % (BM / 8)) * 8;
       ok = k0 + kk < kend && row0 + row < nrows;
       off = (int64_t)(k0 + kk) * ld + row0 + row;
     }
@@ -68,37 +69,40 @@ __device__ __forceinline__ void load_tile(u16x8 (&r)[4], const bf16_bits* __rest
   }
 }
 
-// LDS offset (bf16 elements) of the 8-k unit u (k = 8u .. 8u + 7) of row m.
-// Rows with k contiguous in the source: padded rows of LROW.  Transposed
-// rows: unpadded rows of BK whose 16-byte units are permuted by (m / 8) % 8,
-// so that both the transposing writes (16 row groups of a wave, 8 bytes
-// each) and the MFMA operand reads (32 rows, 16 bytes each) spread over
-// all banks.
-template <bool kcontig>
-__device__ __forceinline__ int lds_unit(int m, int u) {
-  return kcontig ? m * LROW + 8 * u : m * BK + 8 * (u ^ ((m / 8) % 8));
-}
+// LDS offsets, in bf16 elements.  k contiguous: the 8-k unit u (k = 8u ..
+// 8u + 7) of row m in padded rows of LROW (144 bytes: the 16 lanes of a
+// 16-byte read phase, 16 consecutive rows, start 9 units apart mod 16 and
+// cover all 64 banks).  Rows contiguous: k row k is 256 bytes (128 rows m,
+// exactly the 64 banks) whose 16-byte units are permuted by 4 (k % 4), so
+// that the four k rows a transposing read gathers (same 64-byte run of m)
+// fall on four disjoint quarters of the banks.
+__device__ __forceinline__ int lds_kc(int m, int u) { return m * LROW + 8 * u; }
+__device__ __forceinline__ int lds_rc(int k, int m) { return k * BM + 8 * ((m / 8) ^ (4 * (k % 4))) + m % 8; }
 
 template <bool kcontig>
 __device__ __forceinline__ void store_tile(bf16_bits* __restrict__ lds, const u16x8 (&r)[4]) {
-  if (kcontig) {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int v = threadIdx.x + 256 * i;
-      const int row = v / (BK / 8), kk = (v % (BK / 8)) * 8;
-      *reinterpret_cast<u16x8*>(lds + lds_unit<true>(row, kk / 8)) = r[i];
-    }
-  } else {
-    // 8 rows x 4 k of registers -> per row, 4 consecutive k (8 bytes)
-    const int row = (threadIdx.x % 16) * 8, kq = threadIdx.x / 16;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      uint2 w;
-      w.x = (uint32_t)r[0][e] | ((uint32_t)r[1][e] << 16);
-      w.y = (uint32_t)r[2][e] | ((uint32_t)r[3][e] << 16);
-      *reinterpret_cast<uint2*>(lds + lds_unit<false>(row + e, kq / 2) + (kq % 2) * 4) = w;
-    }
+  for (int i = 0; i < 4; ++i) {
+    const int v = threadIdx.x + 256 * i;
+    const int off = kcontig ? lds_kc(v / (BK / 8), v % (BK / 8)) : lds_rc(v / (BM / 8), (v % (BM / 8)) * 8);
+    *reinterpret_cast<u16x8*>(lds + off) = r[i];
   }
+}
+
+// MFMA operand of 32 rows m0 .. m0 + 31 for k-step ks (k = 16 ks .. + 15):
+// lane l holds row m0 + l % 32, k = 16 ks + 8 (l / 32) + e, e = 0..7.  Rows
+// contiguous in LDS: two transposing reads, each giving four k; within a
+// 16-lane group (16 rows m) lane j addresses k row j / 4 of the four and the
+// four rows m 4 (j % 4) .. + 3, and receives its own row m's four k.
+template <bool kcontig>
+__device__ __forceinline__ bf16x8 read_op(const bf16_bits* __restrict__ lds, int m0, int ks, int lane) {
+  if (kcontig) return *reinterpret_cast<const bf16x8*>(lds + lds_kc(m0 + lane % 32, 2 * ks + lane / 32));
+  const int j = lane % 16;
+  const int m = m0 + 16 * ((lane / 16) % 2) + 4 * (j % 4);
+  const int k = 16 * ks + 8 * (lane / 32) + j / 4;
+  const tr16x4 lo = lds_read_tr16(reinterpret_cast<const unsigned char*>(lds + lds_rc(k, m)));
+  const tr16x4 hi = lds_read_tr16(reinterpret_cast<const unsigned char*>(lds + lds_rc(k + 4, m)));
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
 }
 
 // op(A) element (m, k): A[m * lda + k] if A_KC else A[k * lda + m].
@@ -165,8 +169,8 @@ __device__ __forceinline__ void gemm_work(const GemmProblem& P, int w_id, bf16_b
       bf16x8 a[2], b[2];
 #pragma unroll
       for (int i = 0; i < 2; ++i) {
-        a[i] = *reinterpret_cast<const bf16x8*>(as + lds_unit<A_KC>(wm + 32 * i + r32, 2 * ks + hi));
-        b[i] = *reinterpret_cast<const bf16x8*>(bs + lds_unit<B_KC>(wn + 32 * i + r32, 2 * ks + hi));
+        a[i] = read_op<A_KC>(as, wm + 32 * i, ks, lane);
+        b[i] = read_op<B_KC>(bs, wn + 32 * i, ks, lane);
       }
 #pragma unroll
       for (int i = 0; i < 2; ++i)

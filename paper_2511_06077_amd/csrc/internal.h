@@ -52,6 +52,16 @@ struct GemmSpec {
   int accumulate;
 };
 hipError_t gemm_mfma_group(const GemmSpec* specs, int n, float* part, int64_t part_floats, hipStream_t st);
+// The same product for the long history-row operands ([dW_K | dW_V] with K =
+// history rows, dX with M = history rows): one persistent workgroup per CU
+// (n_cu of them), operand tiles streamed into an LDS ring by direct loads.
+// Same conventions and requirements as gemm_mfma (accumulating products
+// without a split over K are left to gemm_mfma); splits over K need
+// gemm_ring_part_floats floats in `part`.
+int64_t gemm_ring_part_floats(int M, int N, int K, int n_cu);
+hipError_t gemm_ring(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
+                     int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
+                     int64_t part_floats, int n_cu, hipStream_t st);
 // dst[c][r] = src[r][c] (bf16; R x C source, row pitches lds / ldd); dst
 // columns R..Rp-1 are zeroed.
 hipError_t transpose_bf16(const bf16_bits* src, int64_t lds, int R, int C, bf16_bits* dst, int64_t ldd, int Rp,
