@@ -92,9 +92,9 @@ def measured_traffic(workload: str, kernel: str):
         rec = json.load(open(path))
         if rec.get("workload") != workload or kernel not in rec.get("kernels", {}):
             continue
-        src = os.path.join(ROOT, rec["source"])
-        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
-            return None
+        for src, sha in rec["sources"].items():
+            if hashlib.sha256(open(os.path.join(ROOT, src), "rb").read()).hexdigest() != sha:
+                return None
         return rec["kernels"][kernel]["bytes"]
     return None
 
@@ -310,6 +310,10 @@ def main() -> int:
     ap.add_argument("--paper", action="store_true",
                     help="instead: the paper-exact stack (stca_forward_paper: SwiGLU + LayerNorm history transform "
                          "per layer, query fusion, head token z) on the same workload")
+    ap.add_argument("--kv", default="auto", choices=["auto", "fused", "materialize"],
+                    help="history K/V form of the headline record (auto: the library's choice)")
+    ap.add_argument("--attn", default="auto", choices=["auto", "standard", "reordered"],
+                    help="attention form of the headline record (auto: the library's choice)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead: time a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -335,7 +339,7 @@ def main() -> int:
     t0 = time.time()
     b = W.make_batch(wl, with_grad=False)
     log(f"[bench] generated {wl.name}: {b.n_hist} history rows, {b.n_tgt_total} targets ({time.time() - t0:.1f} s)")
-    db = DeviceBatch(b, device="cuda:0")
+    db = DeviceBatch(b, device="cuda:0", kv=args.kv, attn=args.attn)
     log(f"[bench] workspace {db.ws_bytes / 2**30:.2f} GiB; path {stca.stca_path(db.dims)}")
     # the timed region: W warm-up steps, then exactly K plain steps; per-kernel
     # durations come from the same K steps again with a HIP event recorded on
@@ -361,7 +365,9 @@ def main() -> int:
         "config": {"workload": wl.name, "requests": wl.n_requests,
                    "targets_per_request": wl.n_targets or list(wl.tgt_range),
                    "hist_len": wl.hist_len or list(wl.hist_range), "d_model": wl.d_model,
-                   "heads": wl.n_heads, "layers": wl.n_layers, "ffn_hidden": wl.ffn_hidden},
+                   "heads": wl.n_heads, "layers": wl.n_layers, "ffn_hidden": wl.ffn_hidden,
+                   **({"kv_form": args.kv} if args.kv != "auto" else {}),
+                   **({"attn_form": args.attn} if args.attn != "auto" else {})},
         "roofline": head["roofline"],
         "path_roofline": head["path_roofline"],
         "fused_design_roofline": head["fused_design_roofline"],
@@ -654,7 +660,7 @@ def train_record(args, wl: W.Workload, steps: int, warmup: int, sl: bool = False
     flop, byts, peak = backward_phase_work(dom, b, fused)
     roof = roofline_entry(dom, phases[dom]["ms_each"], flop, byts, peak)
     roof["kernel"] = dom
-    roof["traffic"] = None
+    roof["traffic"] = measured_traffic(wl.name, dom) if not sl else None
     bound_ms = sum(max(f / (pk * 1e12), by / (PEAK_HBM_GBS * 1e9)) * phases[k]["per_step"] * 1e3
                    for k in phases for f, by, pk in [backward_phase_work(k, b, fused)] if f)
     rec = {
