@@ -95,13 +95,19 @@ typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
  *          STCA_ATTN_STANDARD: always the standard form.
  *          STCA_ATTN_REORDERED: the reordered form; STCA_ERR_UNSUPPORTED for
  *          a batch the automatic rule would not give it.
- * bwd_form STCA_BWD_AUTO: the backward keeps K/V inside its attention kernels
- *          when d_h = 32, ffn_hidden is a multiple of d_model and the host
- *          offsets show at most 32 targets per request; otherwise K | V are
- *          formed by a GEMM and the attention runs in exact fp32.
- *          STCA_BWD_GENERIC: always the latter.  STCA_BWD_FUSED: the former;
- *          STCA_ERR_UNSUPPORTED for a batch the automatic rule would not give
- *          it.
+ * bwd_form STCA_BWD_AUTO: with d_h = 32, ffn_hidden a multiple of d_model and
+ *          host offsets showing at most 32 targets per request, the
+ *          backward on bf16 storage runs in the reordered form (the
+ *          attention gradients through u = q W_K^T and h = da W_V^T per
+ *          target and head, no K, V, dK or dV; Sec. 3.1's reordering applied
+ *          to the backward) when d_model is 128 or 256 and every request has
+ *          at most 128 / n_heads targets, else in the fused form (K/V formed
+ *          inside the attention kernels, dK | dV written for the
+ *          history-side products); otherwise K | V are formed by a GEMM and
+ *          the attention runs in exact fp32 (generic).
+ *          STCA_BWD_GENERIC: always the generic form.  STCA_BWD_FUSED: the
+ *          fused form.  STCA_BWD_REORDERED: the reordered form.  Each is
+ *          STCA_ERR_UNSUPPORTED for a batch outside its conditions.
  * chunk_blocks: history chunk length, in 32-row blocks, of the attention's
  *          split over a request's history (at most 16 chunks per request, so
  *          long histories get longer chunks); 0 = chosen from the batch size
@@ -109,7 +115,7 @@ typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
  * Out-of-range values are STCA_ERR_INVALID_ARG. */
 typedef enum { STCA_KV_AUTO = 0, STCA_KV_FUSED = 1, STCA_KV_MATERIALIZE = 2 } stca_kv_form_t;
 typedef enum { STCA_ATTN_AUTO = 0, STCA_ATTN_STANDARD = 1, STCA_ATTN_REORDERED = 2 } stca_attn_form_t;
-typedef enum { STCA_BWD_AUTO = 0, STCA_BWD_FUSED = 1, STCA_BWD_GENERIC = 2 } stca_bwd_form_t;
+typedef enum { STCA_BWD_AUTO = 0, STCA_BWD_FUSED = 1, STCA_BWD_GENERIC = 2, STCA_BWD_REORDERED = 3 } stca_bwd_form_t;
 
 /* Model shape and execution forms.  d_model % n_heads == 0 and ffn_hidden a
  * multiple of 32.  STCA_BF16 with d_head = d_model / n_heads = 32, d_model in

@@ -26,7 +26,7 @@ FLAGS = [
     "-I", os.path.join(ROOT, "include"),
 ]
 SOURCES = ["sched.hip", "generic.hip", "attn_mfma.hip", "fast.hip", "bwd_fused.hip", "bwd_update.hip",
-           "reordered.hip", "gemm.hip", "gemm_ring.hip", "paper.hip", "api.cpp", "api_paper.cpp", "sl_batch.cpp", "noalloc.hip"]
+           "reordered.hip", "gemm.hip", "gemm_ring.hip", "bwd_reordered.hip", "paper.hip", "api.cpp", "api_paper.cpp", "sl_batch.cpp", "noalloc.hip"]
 
 
 def _compile(src: str, extra) -> str:

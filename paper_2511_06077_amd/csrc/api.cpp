@@ -70,17 +70,27 @@ bool wide_groups_for(const stca_dims_t* dims, const stca_batch_t* b) {
 // when d_h = 32, the FFN width is a multiple of d and every request has at
 // most 32 targets, which the host offsets must show; otherwise K | V are
 // formed by a GEMM, the attention runs exactly in fp32 and the target side as
-// separate GEMMs.  STCA_BWD_GENERIC forces the latter; STCA_BWD_FUSED asks for
-// the former and is unsupported for other batches.  1 / 0 / negative status.
+// separate GEMMs.  Within the fused conditions, d_model of 128 or 256 and at
+// most kRbPairs / n_heads targets per request allow the reordered form (no
+// K, V, dK, dV; the automatic choice there).  STCA_BWD_GENERIC forces the
+// generic form; STCA_BWD_FUSED and STCA_BWD_REORDERED ask for theirs and are
+// unsupported for other batches.  2 (reordered) / 1 (fused) / 0 (generic) /
+// negative status.
 int fused_bwd_for(const stca_dims_t* dims, const stca_batch_t* b) {
   if (dims->bwd_form == STCA_BWD_GENERIC) return 0;
   bool ok = dims->dtype == STCA_BF16 && dims->d_model / dims->n_heads == 32 &&
             (dims->d_model == 64 || dims->d_model == 128 || dims->d_model == 256) &&
             dims->ffn_hidden % dims->d_model == 0 && b->tgt_off_host != nullptr;
-  for (int r = 0; ok && r < b->n_requests; ++r)
-    if (b->tgt_off_host[r + 1] - b->tgt_off_host[r] > 32) ok = false;
-  if (dims->bwd_form == STCA_BWD_FUSED && !ok) return STCA_ERR_UNSUPPORTED;
-  return ok ? 1 : 0;
+  bool rd = ok && (dims->d_model == 128 || dims->d_model == 256) && b->hist_off_host != nullptr;
+  for (int r = 0; ok && r < b->n_requests; ++r) {
+    const int64_t m = b->tgt_off_host[r + 1] - b->tgt_off_host[r];
+    if (m > 32) ok = false;
+    if (m * dims->n_heads > kRbPairs) rd = false;
+  }
+  rd = rd && ok;
+  if (dims->bwd_form == STCA_BWD_FUSED) return ok ? 1 : STCA_ERR_UNSUPPORTED;
+  if (dims->bwd_form == STCA_BWD_REORDERED) return rd ? 2 : STCA_ERR_UNSUPPORTED;
+  return rd ? 2 : ok ? 1 : 0;
 }
 
 struct Layout {
@@ -100,6 +110,7 @@ struct Layout {
   bool mat;                   // K/V written to the workspace by one GEMM (bf16 path)
   bool wide;                  // materialised K/V, units of up to kWideGroup targets (bf16 path)
   bool bfused;                // backward with the history projection inside the attention kernels
+  bool brd;                   // ... in the reordered form (no K, V, dK, dV)
   int group;                  // targets per attention unit
   // common
   size_t hdr, units, tchunks, part_acc, part_ml, state_a, state_b;
@@ -118,6 +129,11 @@ struct Layout {
   // per-layer tensors (RecordLayout)
   size_t fwkp, fwvp, fwop, fw1p, fw2p, fwqp, fw2t, fw1t, fwot, fwqt, rec;
   size_t b_hid, b_dhid, b_ds, b_u, b_du, b_a, b_dq, b_s;  // bf16 copies of backward operands (bf16 path)
+  // reordered backward: E, every request's dX operand, U (fp16), pair
+  // statistics, Z and Y, bf16 q and da; the per-request schedule and the
+  // dX schedule (units of up to 128 rows)
+  size_t rb_e, rb_w, rb_u16, rb_st, rb_z, rb_y, rb_q16, rb_da16, rb_hdr, rb_units, rb_hdrx, rb_unitsx, rb_tch;
+  int64_t rb_maxx;
   int64_t gpart_floats, nh8;
   size_t total;
 };
@@ -246,7 +262,8 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
     const bool bf = dims->dtype == STCA_BF16;
     const int fb = fused_bwd_for(dims, b);
     if (fb < 0) return static_cast<stca_status_t>(fb);
-    L->bfused = bf && fb == 1;
+    L->bfused = bf && fb >= 1;
+    L->brd = bf && fb == 2;
     L->kvs = L->bfused ? 0 : m.take(4 * n * nh * 2 * d);  // every layer's K | V rows, fp32
     if (L->bfused) {
       L->fwkp = m.take(2 * n * d * d);
@@ -262,7 +279,7 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
     }
     // dK | dV: fp32 [N_hist][2d] for one layer; bf16 for every layer, rows
     // [N_hist][n 2d] (layer i in columns [2d i, 2d (i + 1)))
-    L->dkv = m.take(bf ? 2 * nh * n * 2 * d : 4 * nh * 2 * d);
+    L->dkv = L->brd ? 0 : m.take(bf ? 2 * nh * n * 2 * d : 4 * nh * 2 * d);
     // bf16 history-side products: [W_K | W_V] per layer, and for the
     // unfused form its transpose, X^T and every layer's (dK | dV)^T
     // ([n 2d][nh8]) with the history rows padded to a multiple of 8 (the
@@ -270,11 +287,11 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
     L->nh8 = round_up(static_cast<int64_t>(nh), 8);
     const size_t nh8 = static_cast<size_t>(L->nh8);
     const bool tcopies = bf && !L->bfused;
-    L->wkv = bf ? m.take(2 * n * d * 2 * d) : 0;
+    L->wkv = bf && !L->brd ? m.take(2 * n * d * 2 * d) : 0;
     L->wkvt = tcopies ? m.take(2 * n * d * 2 * d) : 0;
     L->xt = tcopies ? m.take(2 * d * nh8) : 0;
     L->dkvt = tcopies ? m.take(2 * n * 2 * d * nh8) : 0;
-    L->dwkv = bf ? m.take(4 * d * n * 2 * d) : 0;   // [d][n 2d] fp32
+    L->dwkv = bf && !L->brd ? m.take(4 * d * n * 2 * d) : 0;   // [d][n 2d] fp32
     // split-K partials: the largest of [dW_K | dW_V] (K = history rows) and
     // the target-side weight gradients (K = targets)
     L->gpart_floats = 0;
@@ -282,8 +299,9 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
       const int di = static_cast<int>(d), Fi = static_cast<int>(F), nti = static_cast<int>(nt);
       // (the fused form runs the target-side weight gradients of a layer,
       // with dW_Q of the layer above, as one group whose splits share it)
-      L->gpart_floats = std::max({gemm_ring_part_floats(di, 2 * di * static_cast<int>(n), static_cast<int>(nh8),
-                                                        device_cus()),
+      L->gpart_floats = std::max({L->brd ? 2 * L->h * gemm_mfma_part_floats(di, 32, nti)
+                                         : gemm_ring_part_floats(di, 2 * di * static_cast<int>(n),
+                                                                 static_cast<int>(nh8), device_cus()),
                                   gemm_mfma_part_floats(Fi, di, nti) + gemm_mfma_part_floats(di, Fi, nti) +
                                       2 * gemm_mfma_part_floats(di, di, nti)});
     }
@@ -316,6 +334,23 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
       L->b_a = m.take(2 * nt * d);
       L->b_dq = m.take(2 * nt * d);
       L->b_s = m.take(2 * nt * d);
+    }
+    if (L->brd) {
+      const size_t R = static_cast<size_t>(b->n_requests), hm = kRbPairs;
+      L->rb_e = m.take(2 * nh * n * 2 * hm);
+      L->rb_w = m.take(2 * R * n * 2 * hm * d);
+      L->rb_u16 = m.take(2 * R * hm * d);
+      L->rb_st = m.take(8 * R * hm);
+      L->rb_z = m.take(2 * L->h * nt * d);
+      L->rb_y = m.take(2 * L->h * nt * d);
+      L->rb_q16 = m.take(2 * nt * d);
+      L->rb_da16 = m.take(2 * nt * d);
+      L->rb_hdr = m.take(sizeof(WsHeader));
+      L->rb_units = m.take(sizeof(Unit) * std::max<size_t>(R, 1));
+      L->rb_hdrx = m.take(sizeof(WsHeader));
+      L->rb_maxx = std::max<int64_t>(1, host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, 4, 32));
+      L->rb_unitsx = m.take(sizeof(Unit) * static_cast<size_t>(L->rb_maxx));
+      L->rb_tch = m.take(4 * std::max<size_t>(nt, 1));
     }
   }
   L->total = m.off;
@@ -545,8 +580,16 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   HIPCHK(rec.start());
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, L.group, units, L.max_units, tch,
                       hdr, st));
+  if (L.brd) {
+    // one unit per request for the reordered attention backward, units of at
+    // most 128 rows for dX
+    HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, 1 << 30, 32, at<Unit>(ws, L.rb_units),
+                        std::max(1, b->n_requests), at<int32_t>(ws, L.rb_tch), at<WsHeader>(ws, L.rb_hdr), st));
+    HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, 4, 32, at<Unit>(ws, L.rb_unitsx), L.rb_maxx,
+                        at<int32_t>(ws, L.rb_tch), at<WsHeader>(ws, L.rb_hdrx), st));
+  }
   HIPCHK(rec.mark("sched"));
-  void* dkv = at<char>(ws, L.dkv);
+  void* dkv = L.brd ? nullptr : at<char>(ws, L.dkv);
   // the recomputed per-layer tensors: in the workspace, or the training record
   const RecordLayout R = L.bfused ? record_layout(L) : RecordLayout{};
   char* rb = !L.bfused ? nullptr
@@ -592,7 +635,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   // of X^T, [W_K | W_V]^T and (dK | dV)^T); fp32 inputs keep fp32 products.
   if (bf) {
     const bf16_bits* X = static_cast<const bf16_bits*>(hist);
-    if (!rec_out)
+    if (!rec_out && !L.brd)
       HIPCHK(pack_wkv(static_cast<const bf16_bits*>(w->wk), static_cast<const bf16_bits*>(w->wv), n, d, wkv_all,
                       st));
     for (int i = 0; i < n && !rec_out; ++i) {
@@ -714,7 +757,9 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   HIPCHK(convert(bf, 0, dout, ds, nt * d, st));
   // rows of requests without targets keep a zero gradient (and dK|dV^T's
   // padding columns stay zero)
-  if (bf) {
+  if (L.brd) {
+    HIPCHK(rb_zero_untargeted(b->hist_off, b->tgt_off, b->n_requests, dhist, d, st));
+  } else if (bf) {
     HIPCHK(zero_untargeted(b->hist_off, b->tgt_off, b->n_requests, nh, static_cast<bf16_bits*>(dkv), n * 2 * d,
                            n * 2 * d, dkvt, nh8, st));
   } else {
@@ -815,8 +860,63 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     HIPCHK(rec.mark("target_gemm"));
     // attention (softmax weights rebuilt from the same q, K, V and lse that
     // gave a, so rowsum(dA * A) matches them)
-    void* dkv_i = bf ? static_cast<void*>(static_cast<bf16_bits*>(dkv) + (size_t)i * 2 * d) : dkv;
-    if (L.bfused) {
+    void* dkv_i = L.brd ? nullptr : bf ? static_cast<void*>(static_cast<bf16_bits*>(dkv) + (size_t)i * 2 * d) : dkv;
+    if (L.brd) {
+      // reordered form: U, H and statistics per request, then one pass over
+      // the history (E, Z, Y), then dW_K^j, dW_V^j and dq^j from Z and Y
+      const bf16_bits* Wk = reinterpret_cast<const bf16_bits*>(W(w->wk, i, (size_t)d * d));
+      const bf16_bits* Wv = reinterpret_cast<const bf16_bits*>(W(w->wv, i, (size_t)d * d));
+      bf16_bits* q16 = at<bf16_bits>(ws, L.rb_q16);
+      bf16_bits* da16 = at<bf16_bits>(ws, L.rb_da16);
+      bf16_bits* Z = at<bf16_bits>(ws, L.rb_z);
+      bf16_bits* Y = at<bf16_bits>(ws, L.rb_y);
+      RbPrep pp{};
+      pp.tgt_off = b->tgt_off;
+      pp.n_requests = b->n_requests;
+      pp.layer = i;
+      pp.n_layers = n;
+      pp.Q = RQ(i);
+      pp.da = da;
+      pp.a = a;
+      pp.lse = RL(i);
+      pp.Wk = Wk;
+      pp.Wv = Wv;
+      pp.U16 = at<_Float16>(ws, L.rb_u16);
+      pp.Wr = at<bf16_bits>(ws, L.rb_w);
+      pp.stats = at<float>(ws, L.rb_st);
+      pp.q16 = q16;
+      pp.da16 = da16;
+      HIPCHK(rb_prep(d, pp, st));
+      RbAttn ra{};
+      ra.units = at<Unit>(ws, L.rb_units);
+      ra.hdr = at<WsHeader>(ws, L.rb_hdr);
+      ra.X = hist;
+      ra.n_hist = nh;
+      ra.n_tgt = nt;
+      ra.layer = i;
+      ra.n_layers = n;
+      ra.U16 = pp.U16;
+      ra.Wr = pp.Wr;
+      ra.stats = pp.stats;
+      ra.E = at<bf16_bits>(ws, L.rb_e);
+      ra.lde = (int64_t)n * 2 * kRbPairs;
+      ra.Z = Z;
+      ra.Y = Y;
+      HIPCHK(rb_attn(d, ra, b->n_requests, st));
+      HIPCHK(rec.mark("attn_bwd"));
+      const int nti = static_cast<int>(nt);
+      GemmSpec g[2 * 8], gq[8];
+      for (int j = 0; j < h; ++j) {
+        const size_t zo = (size_t)j * nt * d;
+        g[j] = {d, 32, nti, Z + zo, d, 1, q16 + 32 * j, d, 0, dw->dwk + (size_t)i * d * d + 32 * j, d, kLn2, 0};
+        g[h + j] = {d, 32, nti, Y + zo, d, 1, da16 + 32 * j, d, 0, dw->dwv + (size_t)i * d * d + 32 * j, d, 1.f, 0};
+        gq[j] = {nti, 32, d, Z + zo, d, 0, Wk + 32 * j, d, 0, dq + 32 * j, d, 1.f / std::sqrt(32.f), 0};
+      }
+      HIPCHK(gemm_mfma_group(g, 2 * h, at<float>(ws, L.gpart), L.gpart_floats, st));
+      HIPCHK(gemm_mfma_group(gq, h, nullptr, 0, st));
+      HIPCHK(convert(0, 1, dq, at<bf16_bits>(ws, L.b_dq), nt * d, st));
+      HIPCHK(rec.mark("kv_grads"));
+    } else if (L.bfused) {
       FastAttnBwd f{};
       f.units = units;
       f.hdr = hdr;
@@ -840,8 +940,10 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
                               st));
     }
     // dq: fp32 for the fp32 products, else only its bf16 copy
-    HIPCHK(reduce_chunks(nt, d, tch, dqp, bf ? nullptr : dq, bf ? at<bf16_bits>(ws, L.b_dq) : nullptr, 1.f, st));
-    HIPCHK(rec.mark("attn_bwd"));
+    if (!L.brd) {
+      HIPCHK(reduce_chunks(nt, d, tch, dqp, bf ? nullptr : dq, bf ? at<bf16_bits>(ws, L.b_dq) : nullptr, 1.f, st));
+      HIPCHK(rec.mark("attn_bwd"));
+    }
     // q = s Wq
     if (bf) {
       const int nti = static_cast<int>(nt);
@@ -899,7 +1001,14 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
     }
     std::swap(ds, ds2);
   }
-  if (bf) {
+  if (L.brd) {
+    // dX = E W_r over every layer's pairs (K = n 2 kRbPairs), per request
+    const int64_t kr = (int64_t)n * 2 * kRbPairs;
+    HIPCHK(gemm_ring_units(d, static_cast<int>(kr), at<bf16_bits>(ws, L.rb_e), kr, at<bf16_bits>(ws, L.rb_w), d,
+                           kr * d, dhist, d, at<Unit>(ws, L.rb_unitsx), at<WsHeader>(ws, L.rb_hdrx), device_cus(),
+                           st));
+    HIPCHK(rec.mark("dx"));
+  } else if (bf) {
     // [dW_K^i | dW_V^i] for every layer = X^T [dK^i | dV^i] (one product over
     // the history rows: the fused form reads X and dK | dV row-major, the
     // unfused one their transposed copies), then
@@ -1036,6 +1145,9 @@ int stca_backward_launch_count(const stca_dims_t* dims, const stca_batch_t* batc
   // or 3 plus the two history-side products of every layer (bf16), out
   // fused: sched, prep, the initial update, 2 per layer (attention, update), prep,
   // 3 per layer, dW_KV, dX, out
+  // reordered: ... 4 per layer (target side, attention, K/V-side gradients,
+  // target side), dX, out
+  if (L.brd) return 6 + 6 * L.n;
   if (L.bfused) return 7 + 5 * L.n;
   return dims->dtype == STCA_BF16 ? 6 + 7 * L.n : 4 + 9 * L.n;
 }

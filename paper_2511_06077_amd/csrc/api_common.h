@@ -32,7 +32,7 @@ inline int path_of(const stca_dims_t* d) {
       d->d_model % d->n_heads != 0 || (d->dtype != STCA_F32 && d->dtype != STCA_BF16))
     return STCA_ERR_INVALID_ARG;
   if (d->kv_form < STCA_KV_AUTO || d->kv_form > STCA_KV_MATERIALIZE || d->attn_form < STCA_ATTN_AUTO ||
-      d->attn_form > STCA_ATTN_REORDERED || d->bwd_form < STCA_BWD_AUTO || d->bwd_form > STCA_BWD_GENERIC ||
+      d->attn_form > STCA_ATTN_REORDERED || d->bwd_form < STCA_BWD_AUTO || d->bwd_form > STCA_BWD_REORDERED ||
       d->chunk_blocks < 0)
     return STCA_ERR_INVALID_ARG;
   const int dh = d->d_model / d->n_heads;

@@ -1,0 +1,344 @@
+// Attention backward in the reordered form (bf16 storage, d_h = 32, at most
+// 128 / n_heads targets per request).
+//
+// The forward's reordering (Sec. 3.1, Eq. attn-optimized: the score of
+// target t and head j is x_l . u_tj with u_tj = q_tj W_K^j^T, and the head
+// output is (sum_l p_tl x_l) W_V^j) carries over to the gradients, so that
+// neither K, V nor their gradients are formed.  With q scaled by
+// log2(e)/sqrt(d_h) (scores in log2 units), per request, layer and head j
+// and the softmax gradient de_tl = p_tl (dp_tl - D_t):
+//   dp_tl = da_tj . v_l = x_l . h_tj,           h_tj = da_tj W_V^j^T
+//   dX_l  = sum_j sum_t ln(2) de_tl u_tj + p_tl h_tj       (over every layer)
+//   dW_K^j = ln(2) sum_t z_tj^T q_tj,  dW_V^j = sum_t y_tj^T da_tj
+//   dq_tj = z_tj W_K^j / sqrt(d_h)
+// with z_tj = sum_l de_tl x_l and y_tj = sum_l p_tl x_l.  The (target, head)
+// pairs of a request are the rows of U and H (HM = 128 of them, index
+// j' = head * M + t, M = 128 / n_heads, padded with zero rows).
+//
+//   rb_prep_kernel:  per request, U (fp16 for the scores; bf16 with H into
+//                    the request's dX operand W_r), the softmax statistics
+//                    (log2-unit lse, D) and bf16 copies of q and da.
+//   rb_attn_kernel:  per request, history blocks of 32 rows streamed into an
+//                    LDS ring by direct loads; four waves (one per SIMD, the
+//                    registers of a whole SIMD lane each), wave w takes the
+//                    32 pairs 32 w ..: S = X U^T (fp16) and dP = X H^T
+//                    (bf16), P and dE, [ln(2) dE | P] into this layer's
+//                    columns of E, and Z += dE^T X, Y += P^T X.  Z and Y
+//                    (bf16, [head][target][D]) are written at the end of
+//                    the request.
+// The products that follow (dq, dW_K, dW_V from Z and Y; dX = E W_r after
+// the last layer) are GEMMs.
+#include "common.h"
+#include "fast.h"
+#include "ring.h"
+
+namespace stca {
+
+namespace {
+
+constexpr int DH = 32;
+constexpr int HM = kRbPairs;  // (target, head) pairs per request, padded
+constexpr int kRbStages = 4;  // X blocks in the LDS ring
+
+__device__ __forceinline__ f32x16 mma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x16 mma(const f16x8& a, const f16x8& b, const f32x16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 pack_b(const f32x16& a, int off) {
+  bf16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<__bf16>(a[off + i]);
+  return r;
+}
+
+// bf16 bits -> fp16 (exact in fp16's normal range)
+__device__ __forceinline__ f16x8 bf_to_f16(const bf16x8& x) {
+  f16x8 r;
+#pragma unroll
+  for (int i = 0; i < 8; ++i) r[i] = static_cast<_Float16>(static_cast<float>(x[i]));
+  return r;
+}
+
+// v ~ hi + lo, both bf16
+__device__ __forceinline__ void split_bf(float v, __bf16& hi, __bf16& lo) {
+  hi = static_cast<__bf16>(v);
+  lo = static_cast<__bf16>(v - static_cast<float>(hi));
+}
+
+// LDS position of 16-byte unit u of X-tile row r (D / 8 units per row): the
+// permutation u ^ (4 (r % 4) + (r / 4) % 4) spreads both the 16 rows of a
+// row read (same unit) and the 4 rows x 4 units of a transposing read over
+// the banks.
+__device__ __forceinline__ int xpos(int r, int u) { return u ^ (4 * (r % 4) + (r / 4) % 4); }
+
+// the source of every direct load past the last history row
+__device__ const uint4 kRbZero16[1] = {};
+
+}  // namespace
+
+namespace {
+
+// ---- per request: U, H, statistics, bf16 q and da
+template <int D>
+__global__ __launch_bounds__(64 * (D / 32)) void rb_prep_kernel(RbPrep A) {
+  constexpr int H = D / DH;
+  constexpr int M = HM / H;   // target slots per head
+  constexpr int MT = (M + 31) / 32;
+  const int r = blockIdx.x;
+  if (r >= A.n_requests) return;
+  const int h = threadIdx.x / 64, lane = threadIdx.x % 64, l32 = lane % 32, hi = lane / 32;
+  const int64_t t0 = A.tgt_off[r];
+  const int m = static_cast<int>(A.tgt_off[r + 1] - t0);
+  if (m == 0) return;
+  const int cols = h * DH;
+  _Float16* U16 = A.U16 + (int64_t)r * HM * D;
+  bf16_bits* Wu = A.Wr + (((int64_t)r * A.n_layers + A.layer) * 2) * HM * D;
+  bf16_bits* Wh = Wu + (int64_t)HM * D;
+  for (int rt = 0; rt < MT; ++rt) {
+    // A operands: row i = target slot 32 rt + l32, k = head dims 16 s + 8 hi + e
+    const int t = 32 * rt + l32;
+    const bool tok = t < m && t < M;
+    bf16x8 qh[2], ql[2], dh[2], dl[2];
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const int c = cols + 16 * s + 8 * hi + e;
+        const float q = tok ? A.Q[(t0 + t) * D + c] : 0.f;
+        const float g = tok ? A.da[(t0 + t) * D + c] : 0.f;
+        __bf16 a, b;
+        split_bf(q, a, b);
+        qh[s][e] = a, ql[s][e] = b;
+        split_bf(g, a, b);
+        dh[s][e] = a, dl[s][e] = b;
+      }
+    }
+#pragma unroll
+    for (int dt = 0; dt < D / 32; ++dt) {
+      const int dim = 32 * dt + l32;
+      f32x16 u = {}, hv = {};
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        const bf16x8 wk = *reinterpret_cast<const bf16x8*>(A.Wk + (int64_t)dim * D + cols + 16 * s + 8 * hi);
+        const bf16x8 wv = *reinterpret_cast<const bf16x8*>(A.Wv + (int64_t)dim * D + cols + 16 * s + 8 * hi);
+        u = mma(qh[s], wk, u);
+        u = mma(ql[s], wk, u);
+        hv = mma(dh[s], wv, hv);
+        hv = mma(dl[s], wv, hv);
+      }
+      // lane = dim, element v = target slot 32 rt + 8 (v / 4) + 4 hi + v % 4
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int tt = 32 * rt + 8 * (v / 4) + 4 * hi + v % 4;
+        if (tt < M) {
+          const int64_t o = (int64_t)(h * M + tt) * D + dim;
+          U16[o] = static_cast<_Float16>(u[v]);
+          Wu[o] = from_f32<bf16_bits>(u[v]);
+          Wh[o] = from_f32<bf16_bits>(hv[v]);
+        }
+      }
+    }
+  }
+  // statistics of the pairs (t, h), and the bf16 copies of q and da
+  for (int t = lane; t < M; t += 64) {
+    float lse2 = INFINITY, dsum = 0.f;
+    if (t < m) {
+      lse2 = A.lse[(t0 + t) * H + h] * kLog2e;
+      for (int c = 0; c < DH; ++c) dsum += A.da[(t0 + t) * D + cols + c] * A.a[(t0 + t) * D + cols + c];
+    }
+    A.stats[((int64_t)r * HM + h * M + t) * 2] = lse2;
+    A.stats[((int64_t)r * HM + h * M + t) * 2 + 1] = dsum;
+  }
+  for (int e = lane; e < m * DH; e += 64) {
+    const int64_t o = (t0 + e / DH) * D + cols + e % DH;
+    A.q16[o] = from_f32<bf16_bits>(A.Q[o]);
+    A.da16[o] = from_f32<bf16_bits>(A.da[o]);
+  }
+}
+
+// ---- per request: S, dP, P, dE, E, Z, Y
+template <int N>
+__device__ __forceinline__ void wait_loads() {  // at most N vector memory operations outstanding
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void rb_attn_kernel(RbAttn A) {
+  constexpr int KS = D / 16;       // k-steps of the score products
+  constexpr int DT = D / 32;       // 32-column tiles of Z and Y
+  constexpr int TB = 32 * D * 2;   // bytes of one X block in LDS
+  constexpr int CH = TB / 1024;    // 1 KB direct-load runs per block
+  static_assert(CH % 4 == 0, "whole runs per wave");
+  constexpr int PER = CH / 4;      // direct loads per wave per block
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[kRbStages * TB];
+
+  const Unit* __restrict__ units = static_cast<const Unit*>(A.units);
+  const WsHeader* __restrict__ hdr = static_cast<const WsHeader*>(A.hdr);
+  if (static_cast<int>(blockIdx.x) >= hdr->n_units) return;
+  const Unit un = units[blockIdx.x];
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);  // pair tile: pairs 32 wave ..
+  const int lane = threadIdx.x % 64, l32 = lane % 32, hi = lane / 32;
+  const int r = un.r;
+  const int64_t t0 = un.t0;
+  const int m = un.nt;
+  const int jp = 32 * wave + l32;  // this lane's pair (result column)
+  const bf16_bits* __restrict__ X = static_cast<const bf16_bits*>(A.X);
+  constexpr int M = HM / (D / DH);
+
+  // B operands of the score products: the tile's U (fp16) and H (bf16) rows
+  f16x8 ub[KS];
+  bf16x8 hb[KS];
+  {
+    const f16x8* su = reinterpret_cast<const f16x8*>(A.U16 + ((int64_t)r * HM + jp) * D);
+    const bf16x8* sh =
+        reinterpret_cast<const bf16x8*>(A.Wr + ((((int64_t)r * A.n_layers + A.layer) * 2 + 1) * HM + jp) * D);
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      ub[ks] = su[2 * ks + hi];
+      hb[ks] = sh[2 * ks + hi];
+    }
+  }
+  const float lse2 = A.stats[((int64_t)r * HM + jp) * 2];
+  const float dsum = A.stats[((int64_t)r * HM + jp) * 2 + 1];
+  f32x16 accz[DT], accy[DT];
+#pragma unroll
+  for (int i = 0; i < DT; ++i) accz[i] = accy[i] = f32x16{};
+
+  // ring of X blocks b0 .. b1 - 1 (rows past the batch come from a zero vector)
+  const int b0 = un.b0, nb = un.b1 - un.b0;
+  auto issue = [&](int k) {
+    const unsigned char* s = ring + (k % kRbStages) * TB;
+    const int64_t row0 = (int64_t)(b0 + k) * 32;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int q = wave + 4 * i;
+      const int o = 1024 * q + 16 * lane;
+      const int row = o / (2 * D), p = (o % (2 * D)) / 16;
+      const int u = xpos(row, p);  // the permutation is an involution
+      const int64_t g = row0 + row;
+      dma16(g < A.n_hist ? static_cast<const void*>(X + g * D + 8 * u) : static_cast<const void*>(kRbZero16),
+            s + 1024 * q);
+    }
+  };
+  int issued = 0;
+  for (; issued < kRbStages - 1 && issued < nb; ++issued) issue(issued);
+  const int64_t lde = A.lde;
+  bf16_bits* __restrict__ ecol = A.E + (int64_t)A.layer * 2 * HM + jp;
+  const int j16 = lane % 16, g16 = (lane / 16) % 2;
+  for (int k = 0; k < nb; ++k) {
+    // block k landed (later blocks may still be in flight)
+    const int later = issued - k - 1;
+    if (later >= 2)
+      wait_loads<2 * PER>();
+    else if (later >= 1)
+      wait_loads<PER>();
+    else
+      wait_loads<0>();
+    ring_barrier();
+    if (issued < nb) {
+      issue(issued);
+      ++issued;
+    }
+    const unsigned char* tile = ring + (k % kRbStages) * TB;
+    // S^T and dP^T: result lane = pair, element v = row 8 (v / 4) + 4 hi + v % 4
+    f32x16 sc = {}, dp = {};
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const bf16x8 x = *reinterpret_cast<const bf16x8*>(tile + l32 * (2 * D) + 16 * xpos(l32, 2 * ks + hi));
+      sc = mma(bf_to_f16(x), ub[ks], sc);
+      dp = mma(x, hb[ks], dp);
+    }
+    const int64_t brow = (int64_t)(b0 + k) * 32;
+    // P, dE = P (dP - D); E row g: [ln(2) dE | P] in this layer's columns
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t g = brow + 8 * (v / 4) + 4 * hi + v % 4;
+      const bool ok = g >= un.l0 && g < un.l1;
+      const float p = ok ? __builtin_amdgcn_exp2f(sc[v] - lse2) : 0.f;
+      const float de = p * (dp[v] - dsum);
+      if (ok) {
+        bf16_bits* e = ecol + g * lde;
+        e[0] = from_f32<bf16_bits>(kLn2 * de);
+        e[HM] = from_f32<bf16_bits>(p);
+      }
+      sc[v] = p;
+      dp[v] = de;
+    }
+    const bf16x8 pa[2] = {pack_b(sc, 0), pack_b(sc, 8)};
+    const bf16x8 ea[2] = {pack_b(dp, 0), pack_b(dp, 8)};
+    // Z += dE^T X, Y += P^T X: the A operands are the tiles above (element p
+    // of k-step s is row 16 s + 4 hi + (p < 4 ? p : p + 4)); the B operand
+    // holds the same rows of X's columns, two transposing reads each
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+#pragma unroll
+      for (int dt = 0; dt < DT; ++dt) {
+        const int col = 32 * dt + 16 * g16 + 4 * (j16 % 4);
+        const int ra = 16 * s + 4 * hi + j16 / 4, rb = ra + 8;
+        const tr16x4 lo = lds_read_tr16(tile + ra * (2 * D) + 16 * xpos(ra, col / 8) + 2 * (col % 8));
+        const tr16x4 up = lds_read_tr16(tile + rb * (2 * D) + 16 * xpos(rb, col / 8) + 2 * (col % 8));
+        const bf16x8 xb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+        accz[dt] = mma(ea[s], xb, accz[dt]);
+        accy[dt] = mma(pa[s], xb, accy[dt]);
+      }
+    }
+  }
+  // Z and Y rows of the tile's pairs: lane = column dim, element v = pair
+  // 32 wave + 8 (v / 4) + 4 hi + v % 4 = head * M + target slot
+#pragma unroll
+  for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int pr = 32 * wave + 8 * (v / 4) + 4 * hi + v % 4;
+      const int hh = pr / M, tt = pr % M;
+      if (tt < m) {
+        const int64_t o = ((int64_t)hh * A.n_tgt + t0 + tt) * D + 32 * dt + l32;
+        A.Z[o] = from_f32<bf16_bits>(accz[dt][v]);
+        A.Y[o] = from_f32<bf16_bits>(accy[dt][v]);
+      }
+    }
+  }
+}
+
+__global__ void rb_zero_rows_kernel(const int32_t* __restrict__ hoff, const int32_t* __restrict__ toff,
+                                    int n_requests, float* __restrict__ dst, int cols) {
+  const int r = blockIdx.x;
+  if (r >= n_requests || toff[r + 1] != toff[r]) return;
+  const int64_t cnt = (int64_t)(hoff[r + 1] - hoff[r]) * cols;
+  float* p = dst + (int64_t)hoff[r] * cols;
+  for (int64_t e = threadIdx.x; e < cnt; e += blockDim.x) p[e] = 0.f;
+}
+
+}  // namespace
+
+hipError_t rb_prep(int D, const RbPrep& a, hipStream_t st) {
+  if (a.n_requests == 0) return hipSuccess;
+#define STCA_RBP(DD) hipLaunchKernelGGL(rb_prep_kernel<DD>, dim3(a.n_requests), dim3(64 * (DD / 32)), 0, st, a)
+  if (D == 256) STCA_RBP(256);
+  else if (D == 128) STCA_RBP(128);
+  else return hipErrorInvalidValue;
+#undef STCA_RBP
+  return hipGetLastError();
+}
+
+hipError_t rb_attn(int D, const RbAttn& a, int grid, hipStream_t st) {
+  if (grid == 0) return hipSuccess;
+#define STCA_RBA(DD) hipLaunchKernelGGL(rb_attn_kernel<DD>, dim3(grid), dim3(256), 0, st, a)
+  if (D == 256) STCA_RBA(256);
+  else if (D == 128) STCA_RBA(128);
+  else return hipErrorInvalidValue;
+#undef STCA_RBA
+  return hipGetLastError();
+}
+
+hipError_t rb_zero_untargeted(const int32_t* hoff, const int32_t* toff, int n_requests, float* dst, int cols,
+                              hipStream_t st) {
+  if (n_requests == 0) return hipSuccess;
+  hipLaunchKernelGGL(rb_zero_rows_kernel, dim3(n_requests), dim3(256), 0, st, hoff, toff, n_requests, dst, cols);
+  return hipGetLastError();
+}
+
+}  // namespace stca

@@ -93,6 +93,47 @@ struct FastAttnFwdPrecise {
   int64_t n_tgt;
 };
 hipError_t fast_attn_fwd_precise(int D, const FastAttnFwdPrecise& f, int grid, hipStream_t st);
+// Attention backward in the reordered form (bwd_reordered.hip): requests of
+// at most kRbPairs / n_heads targets; pair j' = head * M + target slot
+// (M = kRbPairs / n_heads), zero-padded per request.
+constexpr int kRbPairs = 128;
+// Per layer and request: U = q W_K^j^T per pair (U16: fp16 [R][kRbPairs][D];
+// also bf16 in the request's dX operand), H = da W_V^j^T (bf16), the
+// statistics (log2-unit lse, D = da . a per pair; [R][kRbPairs][2]) and bf16
+// copies of q and da ([n_tgt][D]).  Wr: [R][n_layers][2][kRbPairs][D], this
+// layer's U rows then H rows.
+struct RbPrep {
+  const int32_t* tgt_off;
+  int n_requests, layer, n_layers;
+  const float *Q, *da, *a, *lse;  // Q scaled by log2(e)/sqrt(d_h); lse natural, [n_tgt][H]
+  const bf16_bits *Wk, *Wv;       // this layer's [D][D]
+  _Float16* U16;
+  bf16_bits* Wr;
+  float* stats;
+  bf16_bits *q16, *da16;
+};
+hipError_t rb_prep(int D, const RbPrep& a, hipStream_t st);
+// Per request unit (one unit per request with targets): E (this layer's
+// columns [layer 2 kRbPairs, + 2 kRbPairs) of rows [N_hist][lde], bf16:
+// ln(2) dE then P per pair), Z = dE^T X and Y = P^T X (bf16
+// [n_heads][n_tgt][D]).
+struct RbAttn {
+  const void* units;
+  const void* hdr;
+  const void* X;
+  int64_t n_hist, n_tgt;
+  int layer, n_layers;
+  const _Float16* U16;
+  const bf16_bits* Wr;
+  const float* stats;
+  bf16_bits* E;
+  int64_t lde;
+  bf16_bits *Z, *Y;
+};
+hipError_t rb_attn(int D, const RbAttn& a, int grid, hipStream_t st);
+// Zero the rows [hoff[r], hoff[r + 1]) x cols (fp32) of every request without targets.
+hipError_t rb_zero_untargeted(const int32_t* hoff, const int32_t* toff, int n_requests, float* dst, int cols,
+                              hipStream_t st);
 // Target-side recomputation for the backward (bwd_update.hip), fp32-accurate
 // on the bf16 matrix cores.  mode 0: s^(0) = x_t (s_out), q^(0) (q_out).
 // mode 1 (layer): merge the partials into a (a_out) and lse (lse_out), u =

@@ -217,7 +217,7 @@ __global__ __launch_bounds__(256) void mfma_gemm_kernel(GemmProblem P, int n_wor
 
 // Up to kMaxGroup products (same operand forms) in one launch, their work
 // items numbered consecutively.
-constexpr int kMaxGroup = 4;
+constexpr int kMaxGroup = 16;
 struct GemmGroup {
   GemmProblem p[kMaxGroup];
   int n;

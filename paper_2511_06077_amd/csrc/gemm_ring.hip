@@ -124,11 +124,19 @@ struct RingProblem {
   float alpha;
   int accumulate, k_chunk, tiles_m, tiles_n, splits, n_work;
   float* part;  // per-split partial tiles, or null (no split)
+  // unit mode (units non-null): work item u covers rows
+  // [max(32 b0, l0), min(32 b1, l1)) of unit u (of hdr->n_units), all N and
+  // all K, with B advanced by b_stride per request
+  const Unit* units;
+  const WsHeader* hdr;
+  int64_t b_stride;
 };
 
-// Work item in flight: output tile, K range and progress through it.
+// Work item in flight: output rows (from m0, below mend, BM per tile), K
+// range, and progress (ks over tiles x kpt k-steps).
 struct Cursor {
-  int round, ks, nks, m0, n0, kb, ke, split;
+  int round, ks, nks, kpt, m0, mend, n0, kb, ke, split;
+  int64_t bofs;
   bool done;
 };
 
@@ -137,6 +145,29 @@ __device__ __forceinline__ void set_item(const RingProblem& P, Cursor& c) {
   // Workgroups are dealt to the XCDs round robin: in each round, XCD x takes
   // a contiguous range of work items (those of one K range share an operand).
   const int G = gridDim.x, b = blockIdx.x;
+  c.ks = 0;
+  if (P.units) {
+    const int n = P.hdr->n_units;
+    for (;;) {  // the next unit with rows (units are never empty; the check keeps the loop safe)
+      const int id = c.round * G + (b % kXcds) * (G / kXcds) + b / kXcds;
+      if (id >= n) {
+        c.done = true;
+        return;
+      }
+      const Unit u = P.units[id];
+      c.m0 = max(u.b0 * kBlockTokens, u.l0);
+      c.mend = min(u.b1 * kBlockTokens, u.l1);
+      c.n0 = 0;
+      c.kb = 0;
+      c.ke = P.K;
+      c.split = 0;
+      c.bofs = (int64_t)u.r * P.b_stride;
+      c.kpt = (P.K + BK - 1) / BK;
+      c.nks = c.mend > c.m0 ? c.kpt * ((c.mend - c.m0 + BM - 1) / BM) : 0;
+      if (c.nks > 0) return;
+      ++c.round;
+    }
+  }
   const int id = c.round * G + (b % kXcds) * (G / kXcds) + b / kXcds;
   if (id >= P.n_work) {
     c.done = true;
@@ -146,11 +177,12 @@ __device__ __forceinline__ void set_item(const RingProblem& P, Cursor& c) {
   c.split = id / tiles;
   const int t = id % tiles;
   c.m0 = (t / P.tiles_n) * BM;
+  c.mend = P.M;
   c.n0 = (t % P.tiles_n) * BN;
   c.kb = c.split * P.k_chunk;
   c.ke = min(P.K, c.kb + P.k_chunk);
-  c.ks = 0;
-  c.nks = (c.ke - c.kb + BK - 1) / BK;
+  c.bofs = 0;
+  c.nks = c.kpt = (c.ke - c.kb + BK - 1) / BK;
 }
 
 template <int BM, int BN, int BK>
@@ -209,16 +241,16 @@ __global__ __launch_bounds__(kRingThreads, 2) void ring_gemm_kernel(RingProblem 
   const int lane = threadIdx.x % 64;
   const int wm = (wave % WM) * 64, wn = (wave / WM) * 64;
 
-  Cursor ci{0, 0, 0, 0, 0, 0, 0, 0, false};
+  Cursor ci{0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, false};
   set_item<BM, BN, BK>(P, ci);
   if (ci.done) return;
   Cursor cc = ci;
 
   auto issue = [&](int slot) {
     const unsigned char* s = ring + slot * SB;
-    const int k0 = ci.kb + ci.ks * BK;
-    TA::load(P.A, P.lda, ci.m0, P.M, k0, ci.ke, s, wave, lane);
-    TB::load(P.B, P.ldb, ci.n0, P.N, k0, ci.ke, s + TA::kBytes, wave, lane);
+    const int k0 = ci.kb + (ci.ks % ci.kpt) * BK;
+    TA::load(P.A, P.lda, ci.m0 + (ci.ks / ci.kpt) * BM, ci.mend, k0, ci.ke, s, wave, lane);
+    TB::load(P.B + ci.bofs, P.ldb, ci.n0, P.N, k0, ci.ke, s + TA::kBytes, wave, lane);
     advance<BM, BN, BK>(P, ci);
   };
 
@@ -257,16 +289,17 @@ __global__ __launch_bounds__(kRingThreads, 2) void ring_gemm_kernel(RingProblem 
 #pragma unroll
         for (int j = 0; j < TN; ++j) acc[i][j] = mfma_bf(a[i], b[j], acc[i][j]);
     }
-    if (cc.ks + 1 == cc.nks) {
-      const int m0 = cc.m0 + wm, n0 = cc.n0 + wn;
-      const bool full = cc.m0 + BM <= P.M && cc.n0 + BN <= P.N;
+    if ((cc.ks + 1) % cc.kpt == 0) {
+      const int mt = cc.m0 + (cc.ks / cc.kpt) * BM;
+      const int m0 = mt + wm, n0 = cc.n0 + wn;
+      const bool full = mt + BM <= cc.mend && cc.n0 + BN <= P.N;
       if (P.part) {
         float* out = P.part + (int64_t)cc.split * P.M * P.N;
         if (full) put_tile<TM, TN, false>(acc, out, P.N, m0, n0, P.M, P.N, 1.f, lane);
         else put_tile<TM, TN, true>(acc, out, P.N, m0, n0, P.M, P.N, 1.f, lane);
       } else {
-        if (full) put_tile<TM, TN, false>(acc, P.C, P.ldc, m0, n0, P.M, P.N, P.alpha, lane);
-        else put_tile<TM, TN, true>(acc, P.C, P.ldc, m0, n0, P.M, P.N, P.alpha, lane);
+        if (full) put_tile<TM, TN, false>(acc, P.C, P.ldc, m0, n0, cc.mend, P.N, P.alpha, lane);
+        else put_tile<TM, TN, true>(acc, P.C, P.ldc, m0, n0, cc.mend, P.N, P.alpha, lane);
       }
     }
     advance<BM, BN, BK>(P, cc);
@@ -344,7 +377,8 @@ hipError_t gemm_ring(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
   const int64_t work = tm * tn * splits;
   if (work > 0x7fffffff) return hipErrorInvalidValue;
   RingProblem P{M, N, K, A, lda, B, ldb, C, ldc, alpha, accumulate, k_chunk, static_cast<int>(tm),
-                static_cast<int>(tn), splits, static_cast<int>(work), splits > 1 ? part : nullptr};
+                static_cast<int>(tn), splits, static_cast<int>(work), splits > 1 ? part : nullptr, nullptr, nullptr,
+                0};
   // one workgroup per CU (the ring takes most of the LDS), a multiple of
   // the XCD count
   const int64_t grid = round_up(std::min<int64_t>(work, n_cu), kXcds);
@@ -357,6 +391,20 @@ hipError_t gemm_ring(int M, int N, int K, const bf16_bits* A, int64_t lda, int t
   if (P.part)
     hipLaunchKernelGGL(ring_split_sum_kernel, dim3(static_cast<unsigned>(ceil_div((int64_t)M * N, 256))), dim3(256),
                        0, st, P.part, P.splits, M, N, C, ldc, alpha, accumulate);
+  return hipGetLastError();
+}
+
+hipError_t gemm_ring_units(int N, int K, const bf16_bits* A, int64_t lda, const bf16_bits* B, int64_t ldb,
+                           int64_t b_stride, float* C, int64_t ldc, const Unit* units, const WsHeader* hdr,
+                           int n_cu, hipStream_t st) {
+  if (N == 0 || K == 0) return hipSuccess;
+  if (K % 8 || N % 8 || lda % 8 || ldb % 8 || b_stride % 8 || !al16(A) || !al16(B) || n_cu < 1)
+    return hipErrorInvalidValue;
+  RingProblem P{0, N, K, A, lda, B, ldb, C, ldc, 1.f, 0, K, 1, static_cast<int>(ceil_div(N, 256)), 1, 0, nullptr,
+                units, hdr, b_stride};
+  if (N > 256) return hipErrorInvalidValue;  // one tile spans N
+  hipLaunchKernelGGL((ring_gemm_kernel<true, false, 128, 256, kBK, kNS>), dim3(static_cast<unsigned>(round_up(n_cu, kXcds))),
+                     dim3(kRingThreads), 0, st, P);
   return hipGetLastError();
 }
 

@@ -34,7 +34,7 @@ int64_t gemm_mfma_part_floats(int M, int N, int K);
 hipError_t gemm_mfma(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
                      int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
                      int64_t part_floats, hipStream_t st);
-// Up to four gemm_mfma products with the same operand forms (transA,
+// Up to sixteen gemm_mfma products with the same operand forms (transA,
 // transB) in one launch (and one launch summing their splits), so that small
 // products fill the chip together; `part` is shared, the products' splits in
 // order (the sum of their gemm_mfma_part_floats holds every split).
@@ -62,6 +62,13 @@ int64_t gemm_ring_part_floats(int M, int N, int K, int n_cu);
 hipError_t gemm_ring(int M, int N, int K, const bf16_bits* A, int64_t lda, int transA, const bf16_bits* B,
                      int64_t ldb, int transB, float* C, int64_t ldc, float alpha, int accumulate, float* part,
                      int64_t part_floats, int n_cu, hipStream_t st);
+// The same kernel over the units of a schedule (hdr->n_units of them): unit
+// u's rows [max(32 b0, l0), min(32 b1, l1)) of C ([rows][ldc] fp32, N <= 256
+// columns) = A rows (bf16, k contiguous, lda) times B + r * b_stride (bf16
+// [K][ldb], rows contiguous), r the unit's request.
+hipError_t gemm_ring_units(int N, int K, const bf16_bits* A, int64_t lda, const bf16_bits* B, int64_t ldb,
+                           int64_t b_stride, float* C, int64_t ldc, const Unit* units, const WsHeader* hdr,
+                           int n_cu, hipStream_t st);
 // dst[c][r] = src[r][c] (bf16; R x C source, row pitches lds / ldd); dst
 // columns R..Rp-1 are zeroed.
 hipError_t transpose_bf16(const bf16_bits* src, int64_t lds, int R, int C, bf16_bits* dst, int64_t ldd, int Rp,

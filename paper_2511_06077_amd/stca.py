@@ -19,11 +19,12 @@ STCA_F32, STCA_BF16 = 0, 1
 # execution forms (stca_dims_t.kv_form / attn_form / bwd_form); 0 = automatic
 STCA_KV_AUTO, STCA_KV_FUSED, STCA_KV_MATERIALIZE = 0, 1, 2
 STCA_ATTN_AUTO, STCA_ATTN_STANDARD, STCA_ATTN_REORDERED = 0, 1, 2
-STCA_BWD_AUTO, STCA_BWD_FUSED, STCA_BWD_GENERIC = 0, 1, 2
+STCA_BWD_AUTO, STCA_BWD_FUSED, STCA_BWD_GENERIC, STCA_BWD_REORDERED = 0, 1, 2, 3
 FORMS = {
     "kv": {"auto": STCA_KV_AUTO, "fused": STCA_KV_FUSED, "materialize": STCA_KV_MATERIALIZE},
     "attn": {"auto": STCA_ATTN_AUTO, "standard": STCA_ATTN_STANDARD, "reordered": STCA_ATTN_REORDERED},
-    "bwd": {"auto": STCA_BWD_AUTO, "fused": STCA_BWD_FUSED, "generic": STCA_BWD_GENERIC},
+    "bwd": {"auto": STCA_BWD_AUTO, "fused": STCA_BWD_FUSED, "generic": STCA_BWD_GENERIC,
+            "reordered": STCA_BWD_REORDERED},
 }
 
 EXPORTED = ("stca_workspace_size", "stca_saved_size", "stca_saved_layout", "stca_forward", "stca_backward",
