@@ -513,9 +513,16 @@ def paper_step(args) -> int:
     return 0
 
 
-def backward_phase_work(label: str, b: W.Batch, fused: bool):
+def backward_phase_work(label: str, b: W.Batch, fused: bool, reordered: bool = False):
     """Algorithmic (flop, bytes, peak TFLOP/s) of one occurrence of a backward
     phase (stca_backward_profiled's markers), as the kernels are designed.
+
+    reordered (d = 128/256, at most 128 / n_heads targets per request): per
+    layer one pass over X forms S = X U^T, dP = X H^T, Z = dE^T X and
+    Y = P^T X over the request's m H (target, head) pairs (8 L m H d flop)
+    and writes [ln2 dE | P] (bf16, 4 L m H bytes); dq, dW_K, dW_V come from Z
+    and Y (6 m d^2 flop); dX = E W_r after the layers (4 n L m H d flop,
+    reads every layer's E, writes dX in fp32).
 
     fused (requests of at most 32 targets): the recomputed attention and the
     attention backward each project the history inside the kernel (X read
@@ -532,6 +539,14 @@ def backward_phase_work(label: str, b: W.Batch, fused: bool):
     Ls = float(b.hist_len[b.n_tgt > 0].sum())
     mL = float((b.n_tgt.astype(np.float64) * b.hist_len).sum())
     mt = float(b.n_tgt.sum())
+    H = wl.n_heads
+    if reordered:
+        if label == "attn_bwd":
+            return 8 * H * mL * d, 2 * Ls * d + 4 * H * mL, PEAK_BF16_TFLOPS
+        if label == "kv_grads":
+            return 6 * mt * d * d, 4 * H * mt * d + 8 * mt * d, PEAK_BF16_TFLOPS
+        if label == "dx":
+            return 4 * n * H * mL * d, n * 4 * H * mL + 4 * Ls * d, PEAK_BF16_TFLOPS
     if label == "kv_gemm":
         return 4 * Ls * d * d, 2 * Ls * d + 8 * Ls * d, PEAK_BF16_TFLOPS
     if label == "dw_kv":  # X (or X^T) read once, every layer's dK | dV (or its transpose)
@@ -646,23 +661,24 @@ def train_record(args, wl: W.Workload, steps: int, warmup: int, sl: bool = False
             per.setdefault(ev.label(k), []).append(ev.elapsed_ms(k, k + 1))
         ev.close()
     fused = "kv_gemm" not in per  # the attention kernels project the history themselves
+    reordered = "kv_grads" in per  # the reordered form: no K, V, dK, dV
     phases = {}
     for lab, v in per.items():
         occ = len(v) // steps
         t = float(np.mean(v))
         ent = {"per_step": occ, "ms_each": t, "ms_per_step": t * occ}
-        flop, byts, peak = backward_phase_work(lab, b, fused)
+        flop, byts, peak = backward_phase_work(lab, b, fused, reordered)
         if flop:
             ent.update({"tflops": flop / (t * 1e-3) / 1e12, "gbs": byts / (t * 1e-3) / 1e9,
                         "mfma_frac": flop / (t * 1e-3) / 1e12 / peak, "hbm_frac": byts / (t * 1e-3) / 1e9 / PEAK_HBM_GBS})
         phases[lab] = ent
-    dom = max((k for k in phases if backward_phase_work(k, b, fused)[0]), key=lambda k: phases[k]["ms_per_step"])
-    flop, byts, peak = backward_phase_work(dom, b, fused)
+    dom = max((k for k in phases if backward_phase_work(k, b, fused, reordered)[0]), key=lambda k: phases[k]["ms_per_step"])
+    flop, byts, peak = backward_phase_work(dom, b, fused, reordered)
     roof = roofline_entry(dom, phases[dom]["ms_each"], flop, byts, peak)
     roof["kernel"] = dom
     roof["traffic"] = measured_traffic(wl.name, dom) if not sl else None
     bound_ms = sum(max(f / (pk * 1e12), by / (PEAK_HBM_GBS * 1e9)) * phases[k]["per_step"] * 1e3
-                   for k in phases for f, by, pk in [backward_phase_work(k, b, fused)] if f)
+                   for k in phases for f, by, pk in [backward_phase_work(k, b, fused, reordered)] if f)
     rec = {
         "metric": "targets trained/sec, STCA forward+backward", "value": b.n_tgt_total / (ms * 1e-3),
         "unit": "targets/s", "n_gpus": 1, "steps": steps, "warmup": warmup, "ms_per_step": ms,

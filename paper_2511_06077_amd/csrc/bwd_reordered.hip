@@ -164,6 +164,16 @@ template <int N>
 __device__ __forceinline__ void wait_loads() {  // at most N vector memory operations outstanding
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4));
 }
+// at most `later` (0 .. L) blocks of PER loads each still in flight
+template <int PER, int L>
+__device__ __forceinline__ void wait_later(int later) {
+  if constexpr (L > 0) {
+    if (later >= L) return wait_loads<L * PER>();
+    return wait_later<PER, L - 1>(later);
+  } else {
+    wait_loads<0>();
+  }
+}
 
 template <int D>
 __global__ __launch_bounds__(256) void rb_attn_kernel(RbAttn A) {
@@ -230,13 +240,7 @@ __global__ __launch_bounds__(256) void rb_attn_kernel(RbAttn A) {
   const int j16 = lane % 16, g16 = (lane / 16) % 2;
   for (int k = 0; k < nb; ++k) {
     // block k landed (later blocks may still be in flight)
-    const int later = issued - k - 1;
-    if (later >= 2)
-      wait_loads<2 * PER>();
-    else if (later >= 1)
-      wait_loads<PER>();
-    else
-      wait_loads<0>();
+    wait_later<PER, kRbStages - 2>(issued - k - 1);
     ring_barrier();
     if (issued < nb) {
       issue(issued);
