@@ -99,22 +99,52 @@ __global__ __launch_bounds__(64 * (D / 32)) void rb_prep_kernel(RbPrep A) {
   bf16_bits* Wh = Wu + (int64_t)HM * D;
   for (int rt = 0; rt < MT; ++rt) {
     // A operands: row i = target slot 32 rt + l32, k = head dims 16 s + 8 hi + e
+    // (fp32 q and da split into two bf16 terms); the same registers give the
+    // pair statistic D = da . a and the bf16 copies of q and da
     const int t = 32 * rt + l32;
     const bool tok = t < m && t < M;
     bf16x8 qh[2], ql[2], dh[2], dl[2];
+    float dsum = 0.f;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
+      const int64_t o = (t0 + (tok ? t : 0)) * D + cols + 16 * s + 8 * hi;
+      float q[8], g[8], av[8];
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const float4 q4 = tok ? *reinterpret_cast<const float4*>(A.Q + o + 4 * half) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 g4 = tok ? *reinterpret_cast<const float4*>(A.da + o + 4 * half) : make_float4(0.f, 0.f, 0.f, 0.f);
+        const float4 a4 = tok ? *reinterpret_cast<const float4*>(A.a + o + 4 * half) : make_float4(0.f, 0.f, 0.f, 0.f);
+        q[4 * half] = q4.x, q[4 * half + 1] = q4.y, q[4 * half + 2] = q4.z, q[4 * half + 3] = q4.w;
+        g[4 * half] = g4.x, g[4 * half + 1] = g4.y, g[4 * half + 2] = g4.z, g[4 * half + 3] = g4.w;
+        av[4 * half] = a4.x, av[4 * half + 1] = a4.y, av[4 * half + 2] = a4.z, av[4 * half + 3] = a4.w;
+      }
+      uint4 q16, g16;
+      uint32_t* qw = reinterpret_cast<uint32_t*>(&q16);
+      uint32_t* gw = reinterpret_cast<uint32_t*>(&g16);
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const int c = cols + 16 * s + 8 * hi + e;
-        const float q = tok ? A.Q[(t0 + t) * D + c] : 0.f;
-        const float g = tok ? A.da[(t0 + t) * D + c] : 0.f;
         __bf16 a, b;
-        split_bf(q, a, b);
+        split_bf(q[e], a, b);
         qh[s][e] = a, ql[s][e] = b;
-        split_bf(g, a, b);
+        split_bf(g[e], a, b);
         dh[s][e] = a, dl[s][e] = b;
+        dsum += g[e] * av[e];
       }
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        qw[e] = (uint32_t)from_f32<bf16_bits>(q[2 * e]) | ((uint32_t)from_f32<bf16_bits>(q[2 * e + 1]) << 16);
+        gw[e] = (uint32_t)from_f32<bf16_bits>(g[2 * e]) | ((uint32_t)from_f32<bf16_bits>(g[2 * e + 1]) << 16);
+      }
+      if (tok) {
+        *reinterpret_cast<uint4*>(A.q16 + o) = q16;
+        *reinterpret_cast<uint4*>(A.da16 + o) = g16;
+      }
+    }
+    dsum += __shfl_xor(dsum, 32);  // the two lane halves hold 16 dims each
+    if (t < M && hi == 0) {
+      float* st = A.stats + ((int64_t)r * HM + h * M + t) * 2;
+      st[0] = tok ? A.lse[(t0 + t) * H + h] * kLog2e : INFINITY;
+      st[1] = tok ? dsum : 0.f;
     }
 #pragma unroll
     for (int dt = 0; dt < D / 32; ++dt) {
@@ -141,21 +171,6 @@ __global__ __launch_bounds__(64 * (D / 32)) void rb_prep_kernel(RbPrep A) {
         }
       }
     }
-  }
-  // statistics of the pairs (t, h), and the bf16 copies of q and da
-  for (int t = lane; t < M; t += 64) {
-    float lse2 = INFINITY, dsum = 0.f;
-    if (t < m) {
-      lse2 = A.lse[(t0 + t) * H + h] * kLog2e;
-      for (int c = 0; c < DH; ++c) dsum += A.da[(t0 + t) * D + cols + c] * A.a[(t0 + t) * D + cols + c];
-    }
-    A.stats[((int64_t)r * HM + h * M + t) * 2] = lse2;
-    A.stats[((int64_t)r * HM + h * M + t) * 2 + 1] = dsum;
-  }
-  for (int e = lane; e < m * DH; e += 64) {
-    const int64_t o = (t0 + e / DH) * D + cols + e % DH;
-    A.q16[o] = from_f32<bf16_bits>(A.Q[o]);
-    A.da16[o] = from_f32<bf16_bits>(A.da[o]);
   }
 }
 
