@@ -314,6 +314,8 @@ def main() -> int:
                     help="history K/V form of the headline record (auto: the library's choice)")
     ap.add_argument("--attn", default="auto", choices=["auto", "standard", "reordered"],
                     help="attention form of the headline record (auto: the library's choice)")
+    ap.add_argument("--bwd", default="auto", choices=["auto", "fused", "reordered", "generic"],
+                    help="with --backward: the backward form (auto: the library's choice)")
     ap.add_argument("--copy-gib", type=float, default=0.0,
                     help="instead: time a plain device-to-device copy of this many GiB (HBM counter calibration)")
     args = ap.parse_args()
@@ -605,7 +607,7 @@ def train_record(args, wl: W.Workload, steps: int, warmup: int, sl: bool = False
         wl = b.wl
     else:
         b = W.make_batch(wl, with_grad=True)
-    db = DeviceBatch(b, device="cuda:0", backward=True)
+    db = DeviceBatch(b, device="cuda:0", backward=True, bwd=getattr(args, "bwd", "auto"))
     dout = to_device(b.grad_out, "cuda:0")
 
     def timed_step(dbx, k, w):
@@ -685,7 +687,8 @@ def train_record(args, wl: W.Workload, steps: int, warmup: int, sl: bool = False
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": "bf16" if wl.dtype == "bf16" else "f32", "data": "synthetic",
         "config": {"workload": wl.name, "requests": wl.n_requests, "targets_per_request": wl.n_targets,
-                   "hist_len": wl.hist_len, "d_model": wl.d_model, "heads": wl.n_heads, "layers": wl.n_layers},
+                   "hist_len": wl.hist_len, "d_model": wl.d_model, "heads": wl.n_heads, "layers": wl.n_layers,
+                   **({"bwd_form": args.bwd} if getattr(args, "bwd", "auto") != "auto" else {})},
         "stochastic_length": sl_info,
         "training_record": use_rec, "forward_ms": fwd, "backward_ms": bwd,
         "backward_recomputing_ms": bwd_recompute, "roofline": roof,

@@ -100,8 +100,10 @@ typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
  *          backward on bf16 storage runs in the reordered form (the
  *          attention gradients through u = q W_K^T and h = da W_V^T per
  *          target and head, no K, V, dK or dV; Sec. 3.1's reordering applied
- *          to the backward) when d_model is 128 or 256 and every request has
- *          at most 128 / n_heads targets, else in the fused form (K/V formed
+ *          to the backward) when d_model is 128 or 256, every request has
+ *          at most 128 / n_heads targets and no request's history is longer
+ *          than twice one compute unit's share of the batch's history
+ *          blocks, else in the fused form (K/V formed
  *          inside the attention kernels, dK | dV written for the
  *          history-side products); otherwise K | V are formed by a GEMM and
  *          the attention runs in exact fp32 (generic).

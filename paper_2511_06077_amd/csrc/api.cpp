@@ -72,7 +72,8 @@ bool wide_groups_for(const stca_dims_t* dims, const stca_batch_t* b) {
 // formed by a GEMM, the attention runs exactly in fp32 and the target side as
 // separate GEMMs.  Within the fused conditions, d_model of 128 or 256 and at
 // most kRbPairs / n_heads targets per request allow the reordered form (no
-// K, V, dK, dV; the automatic choice there).  STCA_BWD_GENERIC forces the
+// K, V, dK, dV; the automatic choice there when the batch's histories are
+// balanced over the CUs).  STCA_BWD_GENERIC forces the
 // generic form; STCA_BWD_FUSED and STCA_BWD_REORDERED ask for theirs and are
 // unsupported for other batches.  2 (reordered) / 1 (fused) / 0 (generic) /
 // negative status.
@@ -90,6 +91,21 @@ int fused_bwd_for(const stca_dims_t* dims, const stca_batch_t* b) {
   rd = rd && ok;
   if (dims->bwd_form == STCA_BWD_FUSED) return ok ? 1 : STCA_ERR_UNSUPPORTED;
   if (dims->bwd_form == STCA_BWD_REORDERED) return rd ? 2 : STCA_ERR_UNSUPPORTED;
+  // automatic: the reordered form when no request's history is much longer
+  // than one CU's share of the batch (its attention pass streams a request
+  // per unit and splits long requests into chunks whose Z, Y partials cost
+  // extra traffic; on bimodal stochastic-length batches the fused form is
+  // faster)
+  if (rd) {
+    int64_t total = 0, longest = 0;
+    for (int r = 0; r < b->n_requests; ++r) {
+      if (b->tgt_off_host[r + 1] == b->tgt_off_host[r]) continue;
+      const int64_t nb = ceil_div(b->hist_off_host[r + 1], kBlockTokens) - b->hist_off_host[r] / kBlockTokens;
+      total += nb;
+      longest = std::max(longest, nb);
+    }
+    rd = longest <= 2 * ceil_div(total, device_cus());
+  }
   return rd ? 2 : ok ? 1 : 0;
 }
 
@@ -133,7 +149,9 @@ struct Layout {
   // statistics, Z and Y, bf16 q and da; the per-request schedule and the
   // dX schedule (units of up to 128 rows)
   size_t rb_e, rb_w, rb_u16, rb_st, rb_z, rb_y, rb_q16, rb_da16, rb_hdr, rb_units, rb_hdrx, rb_unitsx, rb_tch;
-  int64_t rb_maxx;
+  size_t rb_tchx, rb_zp, rb_yp, rb_first;
+  int64_t rb_maxx, rb_maxu;
+  int rb_cb;  // history chunk length (blocks) of the reordered attention's units
   int64_t gpart_floats, nh8;
   size_t total;
 };
@@ -346,7 +364,16 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
       L->rb_q16 = m.take(2 * nt * d);
       L->rb_da16 = m.take(2 * nt * d);
       L->rb_hdr = m.take(sizeof(WsHeader));
-      L->rb_units = m.take(sizeof(Unit) * std::max<size_t>(R, 1));
+      // about one unit per CU over the whole batch: long requests are cut into
+      // history chunks whose Z, Y partials are summed afterwards
+      L->rb_cb = chunk_blocks_for(b, device_cus(), 1, dims->chunk_blocks);
+      L->rb_maxu = std::max<int64_t>(1, host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests,
+                                                         L->rb_cb, 32));
+      L->rb_units = m.take(sizeof(Unit) * static_cast<size_t>(L->rb_maxu));
+      L->rb_zp = m.take(4 * static_cast<size_t>(L->rb_maxu) * hm * d);
+      L->rb_yp = m.take(4 * static_cast<size_t>(L->rb_maxu) * hm * d);
+      L->rb_first = m.take(4 * std::max<size_t>(R, 1));
+      L->rb_tchx = m.take(4 * std::max<size_t>(nt, 1));
       L->rb_hdrx = m.take(sizeof(WsHeader));
       L->rb_maxx = std::max<int64_t>(1, host_count_units(b->hist_off_host, b->tgt_off_host, b->n_requests, 4, 32));
       L->rb_unitsx = m.take(sizeof(Unit) * static_cast<size_t>(L->rb_maxx));
@@ -581,12 +608,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, L.group, units, L.max_units, tch,
                       hdr, st));
   if (L.brd) {
-    // one unit per request for the reordered attention backward, units of at
-    // most 128 rows for dX
-    HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, 1 << 30, 32, at<Unit>(ws, L.rb_units),
-                        std::max(1, b->n_requests), at<int32_t>(ws, L.rb_tch), at<WsHeader>(ws, L.rb_hdr), st));
+    // history chunks of the requests for the reordered attention backward,
+    // units of at most 128 rows for dX
+    HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.rb_cb, 32, at<Unit>(ws, L.rb_units),
+                        L.rb_maxu, at<int32_t>(ws, L.rb_tch), at<WsHeader>(ws, L.rb_hdr), st));
     HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, 4, 32, at<Unit>(ws, L.rb_unitsx), L.rb_maxx,
-                        at<int32_t>(ws, L.rb_tch), at<WsHeader>(ws, L.rb_hdrx), st));
+                        at<int32_t>(ws, L.rb_tchx), at<WsHeader>(ws, L.rb_hdrx), st));
   }
   HIPCHK(rec.mark("sched"));
   void* dkv = L.brd ? nullptr : at<char>(ws, L.dkv);
@@ -902,7 +929,12 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
       ra.lde = (int64_t)n * 2 * kRbPairs;
       ra.Z = Z;
       ra.Y = Y;
-      HIPCHK(rb_attn(d, ra, b->n_requests, st));
+      ra.tchunks = at<int32_t>(ws, L.rb_tch);
+      ra.Zp = at<float>(ws, L.rb_zp);
+      ra.Yp = at<float>(ws, L.rb_yp);
+      ra.first = at<int32_t>(ws, L.rb_first);
+      HIPCHK(rb_attn(d, ra, static_cast<int>(L.rb_maxu), st));
+      HIPCHK(rb_reduce(d, b->tgt_off, b->n_requests, ra.tchunks, ra.first, ra.Zp, ra.Yp, Z, Y, nt, st));
       HIPCHK(rec.mark("attn_bwd"));
       const int nti = static_cast<int>(nt);
       GemmSpec g[2 * 8], gq[8];

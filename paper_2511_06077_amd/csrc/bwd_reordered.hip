@@ -18,7 +18,7 @@
 //   rb_prep_kernel:  per request, U (fp16 for the scores; bf16 with H into
 //                    the request's dX operand W_r), the softmax statistics
 //                    (log2-unit lse, D) and bf16 copies of q and da.
-//   rb_attn_kernel:  per request, history blocks of 32 rows streamed into an
+//   rb_attn_kernel:  per unit (a history chunk of a request), history blocks of 32 rows streamed into an
 //                    LDS ring by direct loads; four waves (one per SIMD, the
 //                    registers of a whole SIMD lane each), wave w takes the
 //                    32 pairs 32 w ..: S = X U^T (fp16) and dP = X H^T
@@ -306,19 +306,68 @@ __global__ __launch_bounds__(256) void rb_attn_kernel(RbAttn A) {
     }
   }
   // Z and Y rows of the tile's pairs: lane = column dim, element v = pair
-  // 32 wave + 8 (v / 4) + 4 hi + v % 4 = head * M + target slot
+  // 32 wave + 8 (v / 4) + 4 hi + v % 4 = head * M + target slot; a request
+  // of several chunks leaves fp32 partials for rb_reduce
+  if (A.tchunks[t0] == 1) {
 #pragma unroll
-  for (int dt = 0; dt < DT; ++dt) {
+    for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int pr = 32 * wave + 8 * (v / 4) + 4 * hi + v % 4;
-      const int hh = pr / M, tt = pr % M;
-      if (tt < m) {
-        const int64_t o = ((int64_t)hh * A.n_tgt + t0 + tt) * D + 32 * dt + l32;
-        A.Z[o] = from_f32<bf16_bits>(accz[dt][v]);
-        A.Y[o] = from_f32<bf16_bits>(accy[dt][v]);
+      for (int v = 0; v < 16; ++v) {
+        const int pr = 32 * wave + 8 * (v / 4) + 4 * hi + v % 4;
+        const int hh = pr / M, tt = pr % M;
+        if (tt < m) {
+          const int64_t o = ((int64_t)hh * A.n_tgt + t0 + tt) * D + 32 * dt + l32;
+          A.Z[o] = from_f32<bf16_bits>(accz[dt][v]);
+          A.Y[o] = from_f32<bf16_bits>(accy[dt][v]);
+        }
       }
     }
+  } else {
+    if (un.c == 0 && threadIdx.x == 0) A.first[r] = blockIdx.x;
+#pragma unroll
+    for (int dt = 0; dt < DT; ++dt) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int pr = 32 * wave + 8 * (v / 4) + 4 * hi + v % 4;
+        const int64_t o = ((int64_t)blockIdx.x * HM + pr) * D + 32 * dt + l32;
+        A.Zp[o] = accz[dt][v];
+        A.Yp[o] = accy[dt][v];
+      }
+    }
+  }
+}
+
+// Z, Y (bf16 [head][target][D]) of a request of several chunks: the sum of
+// the partials of its units first[r] .. first[r] + chunks - 1
+template <int D>
+__global__ __launch_bounds__(256) void rb_reduce_kernel(const int32_t* __restrict__ toff, int n_requests,
+                                                        const int32_t* __restrict__ tchunks,
+                                                        const int32_t* __restrict__ first, const float* __restrict__ Zp,
+                                                        const float* __restrict__ Yp, bf16_bits* __restrict__ Z,
+                                                        bf16_bits* __restrict__ Y, int64_t n_tgt) {
+  constexpr int H = D / DH, M = HM / H;
+  const int r = blockIdx.x;
+  if (r >= n_requests) return;
+  const int64_t t0 = toff[r];
+  const int m = static_cast<int>(toff[r + 1] - t0);
+  if (m == 0) return;
+  const int nch = tchunks[t0];
+  if (nch <= 1) return;
+  const int u0 = first[r];
+  const int64_t cnt = (int64_t)H * m * D;
+  for (int64_t e = threadIdx.x; e < cnt; e += blockDim.x) {
+    const int hh = static_cast<int>(e / ((int64_t)m * D));
+    const int tt = static_cast<int>((e / D) % m);
+    const int dd = static_cast<int>(e % D);
+    float z = 0.f, y = 0.f;
+    for (int c = 0; c < nch; ++c) {
+      const int64_t o = ((int64_t)(u0 + c) * HM + hh * M + tt) * D + dd;
+      z += Zp[o];
+      y += Yp[o];
+    }
+    const int64_t q = ((int64_t)hh * n_tgt + t0 + tt) * D + dd;
+    Z[q] = from_f32<bf16_bits>(z);
+    Y[q] = from_f32<bf16_bits>(y);
   }
 }
 
@@ -350,6 +399,19 @@ hipError_t rb_attn(int D, const RbAttn& a, int grid, hipStream_t st) {
   else if (D == 128) STCA_RBA(128);
   else return hipErrorInvalidValue;
 #undef STCA_RBA
+  return hipGetLastError();
+}
+
+hipError_t rb_reduce(int D, const int32_t* tgt_off, int n_requests, const int32_t* tchunks, const int32_t* first,
+                     const float* Zp, const float* Yp, bf16_bits* Z, bf16_bits* Y, int64_t n_tgt, hipStream_t st) {
+  if (n_requests == 0) return hipSuccess;
+#define STCA_RBR(DD)                                                                                              \
+  hipLaunchKernelGGL(rb_reduce_kernel<DD>, dim3(n_requests), dim3(256), 0, st, tgt_off, n_requests, tchunks, first, \
+                     Zp, Yp, Z, Y, n_tgt)
+  if (D == 256) STCA_RBR(256);
+  else if (D == 128) STCA_RBR(128);
+  else return hipErrorInvalidValue;
+#undef STCA_RBR
   return hipGetLastError();
 }
 

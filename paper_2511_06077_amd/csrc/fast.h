@@ -113,10 +113,13 @@ struct RbPrep {
   bf16_bits *q16, *da16;
 };
 hipError_t rb_prep(int D, const RbPrep& a, hipStream_t st);
-// Per request unit (one unit per request with targets): E (this layer's
+// Per unit (a history chunk of a request, all its targets): E (this layer's
 // columns [layer 2 kRbPairs, + 2 kRbPairs) of rows [N_hist][lde], bf16:
-// ln(2) dE then P per pair), Z = dE^T X and Y = P^T X (bf16
-// [n_heads][n_tgt][D]).
+// ln(2) dE then P per pair), and the chunk's Z = dE^T X and Y = P^T X: into
+// Z, Y (bf16 [n_heads][n_tgt][D]) directly for a request of one chunk
+// (tchunks of its first target), else as fp32 partials Zp, Yp
+// ([unit][kRbPairs][D]) that rb_reduce sums; `first` records each request's
+// first unit.
 struct RbAttn {
   const void* units;
   const void* hdr;
@@ -129,8 +132,14 @@ struct RbAttn {
   bf16_bits* E;
   int64_t lde;
   bf16_bits *Z, *Y;
+  const int32_t* tchunks;
+  float *Zp, *Yp;
+  int32_t* first;
 };
 hipError_t rb_attn(int D, const RbAttn& a, int grid, hipStream_t st);
+// Z, Y of the requests of several chunks: the sum of their units' partials.
+hipError_t rb_reduce(int D, const int32_t* tgt_off, int n_requests, const int32_t* tchunks, const int32_t* first,
+                     const float* Zp, const float* Yp, bf16_bits* Z, bf16_bits* Y, int64_t n_tgt, hipStream_t st);
 // Zero the rows [hoff[r], hoff[r + 1]) x cols (fp32) of every request without targets.
 hipError_t rb_zero_untargeted(const int32_t* hoff, const int32_t* toff, int n_requests, float* dst, int cols,
                               hipStream_t st);

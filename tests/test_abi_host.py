@@ -183,7 +183,8 @@ def test_fused_backward_selection():
     """The bf16 backward keeps K | V inside its attention kernels (7 + 5 n
     phases, no K|V product per layer) when the host offsets show at most 32
     targets per request, and runs in the reordered form (6 + 6 n) when d is
-    128 or 256 and every request has at most 128 / n_heads targets; more
+    128 or 256, every request has at most 128 / n_heads targets and the
+    histories are balanced over the CUs; more
     targets, no host offsets, fp32 storage, an FFN
     width that is not a multiple of d or bwd_form STCA_BWD_GENERIC take the K|V product and the exact fp32 attention
     (6 + 7 n, 4 + 9 n for fp32), and only that form sizes the fp32 K|V
@@ -193,9 +194,14 @@ def test_fused_backward_selection():
     big, keep2 = fake_batch([0, 40, 100], [0, 33, 40])               # m = 33
     nohost = stca.batch(3, 101, 40, 0x10000, 0x20000, None, None)
     assert stca.stca_backward_launch_count(dims(), small) == 7 + 5 * n
-    # d = 128: 32 targets x 4 heads fit the reordered form's 128 pairs
-    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4), small) == 6 + 6 * n
-    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4, bwd="fused"), small) == 7 + 5 * n
+    # d = 128: 32 targets x 4 heads fit the reordered form's 128 pairs; the
+    # automatic rule takes it for histories balanced over the CUs (here at
+    # most two 32-row blocks per request), the fused form for the ragged batch
+    even, keep4 = fake_batch([0, 64, 128, 192], [0, 32, 33, 40])
+    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4), even) == 6 + 6 * n
+    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4), small) == 7 + 5 * n
+    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4, bwd="reordered"), small) == 6 + 6 * n
+    assert stca.stca_backward_launch_count(dims(d_model=128, n_heads=4, bwd="fused"), even) == 7 + 5 * n
     assert stca.stca_backward_launch_count(dims(d_model=64, n_heads=2), small) == 7 + 5 * n
     assert stca.stca_backward_launch_count(dims(), big) == 6 + 7 * n
     assert stca.stca_backward_launch_count(dims(), nohost) == 6 + 7 * n

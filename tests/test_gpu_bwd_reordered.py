@@ -7,7 +7,6 @@ Metric and bars as in test_gpu_backward (|g - g_ref|_inf / |g_ref|_inf,
 import numpy as np
 import pytest
 
-from oracle import stca_oracle as O
 from paper_2511_06077_amd import workload as W
 from test_gpu_backward import GRADS, TOL, check, gpu_grads, tensor_err
 
@@ -82,13 +81,19 @@ def test_reordered_training_record(torch):
 
 
 def test_reordered_is_the_automatic_choice(torch):
-    """The training window's shape (16 targets x 8 heads = 128 pairs per
-    request) takes the reordered form by itself: no dK | dV phase."""
+    """16 targets x 8 heads = 128 pairs per request and histories balanced
+    over the CUs (the training window's shape, here 64 rows each) take the
+    reordered form by itself (no dK | dV phase); every gradient against the
+    oracle.  The ragged edge batch, with one history much longer than a CU's
+    share, takes the fused form."""
     from paper_2511_06077_amd import stca
     from paper_2511_06077_amd.device import DeviceBatch
-    b = edge_batch(256, 8, 89)
+    b = W.make_custom_batch("gauto", [64] * 12, [16, 3, 16, 1, 9, 16, 16, 2, 16, 7, 16, 16], d_model=256,
+                            n_heads=8, n_layers=2, dtype="bf16", seed=89, with_grad=True)
     db = DeviceBatch(b, backward=True)
     n = b.wl.n_layers
     assert stca.stca_backward_launch_count(db.dims, db.batch) == 6 + 6 * n
-    ref = O.backward(b.f64(), b.f64()["grad_out"])
-    assert ref["dhist"].shape[0] == b.n_hist
+    check(b, gpu_grads(torch, b), TOL["bf16"])
+    e = edge_batch(256, 8, 89)
+    de = DeviceBatch(e, backward=True)
+    assert stca.stca_backward_launch_count(de.dims, de.batch) == 7 + 5 * e.wl.n_layers
