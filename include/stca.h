@@ -88,13 +88,16 @@ typedef enum { STCA_F32 = 0, STCA_BF16 = 1 } stca_dtype_t;
  *          layer's K/V to the workspace once and the attention reads it once
  *          per 128 targets.  STCA_KV_FUSED: always the former.
  *          STCA_KV_MATERIALIZE: always the latter.
- * attn_form STCA_ATTN_AUTO: the reordered single-query form of App. A.2.2
- *          (Eq. attn-optimized: scores u . x with u = q W_K^T, output
- *          (P X) W_V; no K/V) when the host offsets show every request with
- *          at most 32 / n_heads targets, else the standard form.
+ * attn_form STCA_ATTN_AUTO: with d_h = 32 and host offsets, the requests
+ *          with at most 32 / n_heads targets run in the reordered
+ *          single-query form of App. A.2.2 (Eq. attn-optimized: scores
+ *          u . x with u = q W_K^T, output (P X) W_V; no K/V) and the others
+ *          in the standard form, in the same call; without host offsets the
+ *          standard form.
  *          STCA_ATTN_STANDARD: always the standard form.
- *          STCA_ATTN_REORDERED: the reordered form; STCA_ERR_UNSUPPORTED for
- *          a batch the automatic rule would not give it.
+ *          STCA_ATTN_REORDERED: every request in the reordered form, for
+ *          requests of up to 256 / n_heads targets (d_h = 32, host offsets
+ *          given); STCA_ERR_UNSUPPORTED for other batches.
  * bwd_form STCA_BWD_AUTO: with d_h = 32, ffn_hidden a multiple of d_model and
  *          host offsets showing at most 32 targets per request, the
  *          backward on bf16 storage runs in the reordered form (the
