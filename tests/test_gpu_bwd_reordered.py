@@ -97,3 +97,13 @@ def test_reordered_is_the_automatic_choice(torch):
     e = edge_batch(256, 8, 89)
     de = DeviceBatch(e, backward=True)
     assert stca.stca_backward_launch_count(de.dims, de.batch) == 7 + 5 * e.wl.n_layers
+
+
+def test_reordered_long_history(torch):
+    """A history of 3000 rows: the attention pass cuts it into chunks whose Z,
+    Y partials are summed, and the dX product's units (at most 16 history
+    chunks per request) span several 128-row tiles.  Every gradient against
+    the oracle."""
+    b = W.make_custom_batch("glong", [3000, 64, 517], [16, 5, 9], d_model=256, n_heads=8, n_layers=2,
+                            dtype="bf16", seed=97, with_grad=True)
+    check(b, gpu_grads(torch, b, bwd="reordered"), TOL["bf16"])
