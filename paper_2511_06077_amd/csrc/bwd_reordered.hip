@@ -28,6 +28,8 @@
 //                    the request.
 // The products that follow (dq, dW_K, dW_V from Z and Y; dX = E W_r after
 // the last layer) are GEMMs.
+#include <type_traits>
+
 #include "common.h"
 #include "fast.h"
 #include "ring.h"
@@ -38,7 +40,7 @@ namespace {
 
 constexpr int DH = 32;
 constexpr int HM = kRbPairs;  // (target, head) pairs per request, padded
-constexpr int kRbStages = 4;  // X blocks in the LDS ring
+constexpr int kRbStages = 5;  // X blocks in the LDS ring
 
 __device__ __forceinline__ f32x16 mma(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -73,6 +75,13 @@ __device__ __forceinline__ void split_bf(float v, __bf16& hi, __bf16& lo) {
 // row read (same unit) and the 4 rows x 4 units of a transposing read over
 // the banks.
 __device__ __forceinline__ int xpos(int r, int u) { return u ^ (4 * (r % 4) + (r / 4) % 4); }
+
+// The lane index, opaque to the compiler: addresses derived from it are
+// formed where they are used instead of being kept live across a loop.
+__device__ __forceinline__ int opaque_lane(int v) {
+  asm volatile("" : "+v"(v));
+  return v;
+}
 
 // the source of every direct load past the last history row
 __device__ const uint4 kRbZero16[1] = {};
@@ -190,56 +199,59 @@ __device__ __forceinline__ void wait_later(int later) {
   }
 }
 
+// Eight waves, two per pair tile t (32 pairs each), in two roles that share
+// the tile's SIMD: role 0 scores the block (S = X U^T on an fp16 copy of X),
+// forms P, writes E's P columns and accumulates Y += P^T X; role 1 forms
+// dP = X H^T and, one block later, when role 0's P of that block has come
+// through LDS, dE = P (dP - D), E's dE columns and Z += dE^T X.  Each wave
+// so holds one set of score operands (U or H rows) and one set of
+// accumulators (Y or Z), which fit two waves per SIMD.  The ring keeps five
+// blocks: the two in use (k for both roles, k - 1 for role 1's Z) and three
+// in flight.
 template <int D>
-__global__ __launch_bounds__(256) void rb_attn_kernel(RbAttn A) {
+__global__ __launch_bounds__(512) void rb_attn_kernel(RbAttn A) {
   constexpr int KS = D / 16;       // k-steps of the score products
   constexpr int DT = D / 32;       // 32-column tiles of Z and Y
   constexpr int TB = 32 * D * 2;   // bytes of one X block in LDS
   constexpr int CH = TB / 1024;    // 1 KB direct-load runs per block
-  static_assert(CH % 4 == 0, "whole runs per wave");
-  constexpr int PER = CH / 4;      // direct loads per wave per block
-  __shared__ __attribute__((aligned(1024))) unsigned char ring[kRbStages * TB];
+  static_assert(CH % 8 == 0, "whole runs per wave");
+  constexpr int PER = CH / 8;      // direct loads per wave per block
+  constexpr int STG = kRbStages;
+  constexpr int AHEAD = STG - 2;   // blocks in flight beyond the two in use
+  static_assert(AHEAD >= 1, "ring too short");
+  __shared__ __attribute__((aligned(1024))) unsigned char ring[STG * TB];
+  __shared__ __attribute__((aligned(1024))) unsigned char t16[2 * TB];  // fp16 copies of blocks k, k + 1
+  __shared__ __attribute__((aligned(16))) float4 pex[2][4][4][64];      // P of block k per pair tile (role 0 -> 1)
+  __shared__ __attribute__((aligned(16))) float4 dpx[4][4][64];         // role 1: dP of the previous block
 
   const Unit* __restrict__ units = static_cast<const Unit*>(A.units);
   const WsHeader* __restrict__ hdr = static_cast<const WsHeader*>(A.hdr);
   if (static_cast<int>(blockIdx.x) >= hdr->n_units) return;
   const Unit un = units[blockIdx.x];
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);  // pair tile: pairs 32 wave ..
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+  const int tile_id = wave % 4, role = wave / 4;  // the pairs 32 tile_id ..
   const int lane = threadIdx.x % 64, l32 = lane % 32, hi = lane / 32;
   const int r = un.r;
   const int64_t t0 = un.t0;
   const int m = un.nt;
-  const int jp = 32 * wave + l32;  // this lane's pair (result column)
+  const int jp = 32 * tile_id + l32;  // this lane's pair (result column)
   const bf16_bits* __restrict__ X = static_cast<const bf16_bits*>(A.X);
   constexpr int M = HM / (D / DH);
 
-  // B operands of the score products: the tile's U (fp16) and H (bf16) rows
-  f16x8 ub[KS];
-  bf16x8 hb[KS];
-  {
-    const f16x8* su = reinterpret_cast<const f16x8*>(A.U16 + ((int64_t)r * HM + jp) * D);
-    const bf16x8* sh =
-        reinterpret_cast<const bf16x8*>(A.Wr + ((((int64_t)r * A.n_layers + A.layer) * 2 + 1) * HM + jp) * D);
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      ub[ks] = su[2 * ks + hi];
-      hb[ks] = sh[2 * ks + hi];
-    }
-  }
   const float lse2 = A.stats[((int64_t)r * HM + jp) * 2];
   const float dsum = A.stats[((int64_t)r * HM + jp) * 2 + 1];
-  f32x16 accz[DT], accy[DT];
+  f32x16 acc[DT];  // role 0: Y, role 1: Z
 #pragma unroll
-  for (int i = 0; i < DT; ++i) accz[i] = accy[i] = f32x16{};
+  for (int i = 0; i < DT; ++i) acc[i] = f32x16{};
 
   // ring of X blocks b0 .. b1 - 1 (rows past the batch come from a zero vector)
   const int b0 = un.b0, nb = un.b1 - un.b0;
   auto issue = [&](int k) {
-    const unsigned char* s = ring + (k % kRbStages) * TB;
+    const unsigned char* s = ring + (k % STG) * TB;
     const int64_t row0 = (int64_t)(b0 + k) * 32;
 #pragma unroll
     for (int i = 0; i < PER; ++i) {
-      const int q = wave + 4 * i;
+      const int q = wave + 8 * i;
       const int o = 1024 * q + 16 * lane;
       const int row = o / (2 * D), p = (o % (2 * D)) / 16;
       const int u = xpos(row, p);  // the permutation is an involution
@@ -248,90 +260,180 @@ __global__ __launch_bounds__(256) void rb_attn_kernel(RbAttn A) {
             s + 1024 * q);
     }
   };
-  int issued = 0;
-  for (; issued < kRbStages - 1 && issued < nb; ++issued) issue(issued);
+  // fp16 copy of block k for the score products, same byte layout, made by
+  // all 512 threads (two 16-byte units each at D = 256)
+  auto convert = [&](int k) {
+    const unsigned char* src = ring + (k % STG) * TB;
+    unsigned char* dst = t16 + (k % 2) * TB;
+#pragma unroll
+    for (int i = 0; i < TB / (16 * 512); ++i) {
+      const int off = 16 * (static_cast<int>(threadIdx.x) + 512 * i);
+      *reinterpret_cast<f16x8*>(dst + off) = bf_to_f16(*reinterpret_cast<const bf16x8*>(src + off));
+    }
+  };
   const int64_t lde = A.lde;
-  bf16_bits* __restrict__ ecol = A.E + (int64_t)A.layer * 2 * HM + jp;
-  const int j16 = lane % 16, g16 = (lane / 16) % 2;
-  for (int k = 0; k < nb; ++k) {
-    // block k landed (later blocks may still be in flight)
-    wait_later<PER, kRbStages - 2>(issued - k - 1);
-    ring_barrier();
-    if (issued < nb) {
-      issue(issued);
-      ++issued;
-    }
-    const unsigned char* tile = ring + (k % kRbStages) * TB;
-    // S^T and dP^T: result lane = pair, element v = row 8 (v / 4) + 4 hi + v % 4
-    f32x16 sc = {}, dp = {};
-#pragma unroll
-    for (int ks = 0; ks < KS; ++ks) {
-      const bf16x8 x = *reinterpret_cast<const bf16x8*>(tile + l32 * (2 * D) + 16 * xpos(l32, 2 * ks + hi));
-      sc = mma(bf_to_f16(x), ub[ks], sc);
-      dp = mma(x, hb[ks], dp);
-    }
-    const int64_t brow = (int64_t)(b0 + k) * 32;
-    // P, dE = P (dP - D); E row g: [ln(2) dE | P] in this layer's columns
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t g = brow + 8 * (v / 4) + 4 * hi + v % 4;
-      const bool ok = g >= un.l0 && g < un.l1;
-      const float p = ok ? __builtin_amdgcn_exp2f(sc[v] - lse2) : 0.f;
-      const float de = p * (dp[v] - dsum);
-      if (ok) {
-        bf16_bits* e = ecol + g * lde;
-        e[0] = from_f32<bf16_bits>(kLn2 * de);
-        e[HM] = from_f32<bf16_bits>(p);
-      }
-      sc[v] = p;
-      dp[v] = de;
-    }
-    const bf16x8 pa[2] = {pack_b(sc, 0), pack_b(sc, 8)};
-    const bf16x8 ea[2] = {pack_b(dp, 0), pack_b(dp, 8)};
-    // Z += dE^T X, Y += P^T X: the A operands are the tiles above (element p
-    // of k-step s is row 16 s + 4 hi + (p < 4 ? p : p + 4)); the B operand
-    // holds the same rows of X's columns, two transposing reads each
+  bf16_bits* __restrict__ ecol = A.E + (int64_t)A.layer * 2 * HM + jp + (role == 0 ? HM : 0);
+  // acc[dt] += op^T X(block in `tile`): op = the 32 x 32 tile of P or dE in
+  // result order (element p of k-step s is row 16 s + 4 hi + (p < 4 ? p : p + 4)),
+  // X's columns by transposing reads of the same rows
+  // With the permutation xpos, the byte address of row ra = 16 s + 4 hi +
+  // j16 / 4 (rb = ra + 8), column col = 32 dt + 16 g16 + 4 (j16 % 4) is
+  // (tb ^ 64 (dt % 4) [^ 32 for rb]) + 256 (dt / 4) + 16 s 2D [+ 8 2D for rb]
+  // with one per-lane base tb; it is formed from an opaque lane index per
+  // call, so no per-(s, dt) address is held across the loop.
+  auto accumulate = [&](const unsigned char* tile, const bf16x8 (&op)[2]) {
+    const int ln = opaque_lane(lane), jj = ln % 16, gg = (ln / 16) % 2, hh = ln / 32;
+    const int a4 = jj / 4, c4 = 2 * gg + (jj % 4) / 2;
+    const int tb = (4 * hh + a4) * (2 * D) + 16 * (c4 ^ hh) + 8 * ((jj % 4) & 1) + 64 * a4;
 #pragma unroll
     for (int s = 0; s < 2; ++s) {
 #pragma unroll
       for (int dt = 0; dt < DT; ++dt) {
-        const int col = 32 * dt + 16 * g16 + 4 * (j16 % 4);
-        const int ra = 16 * s + 4 * hi + j16 / 4, rb = ra + 8;
-        const tr16x4 lo = lds_read_tr16(tile + ra * (2 * D) + 16 * xpos(ra, col / 8) + 2 * (col % 8));
-        const tr16x4 up = lds_read_tr16(tile + rb * (2 * D) + 16 * xpos(rb, col / 8) + 2 * (col % 8));
+        const int o = (tb ^ (64 * (dt % 4))) + 256 * (dt / 4) + 16 * s * (2 * D);
+        const tr16x4 lo = lds_read_tr16(tile + o);
+        const tr16x4 up = lds_read_tr16(tile + (o ^ 32) + 8 * (2 * D));
         const bf16x8 xb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
-        accz[dt] = mma(ea[s], xb, accz[dt]);
-        accy[dt] = mma(pa[s], xb, accy[dt]);
+        acc[dt] = mma(op[s], xb, acc[dt]);
       }
     }
-  }
-  // Z and Y rows of the tile's pairs: lane = column dim, element v = pair
-  // 32 wave + 8 (v / 4) + 4 hi + v % 4 = head * M + target slot; a request
-  // of several chunks leaves fp32 partials for rb_reduce
+  };
+  // byte address of row l32, 16-byte unit 2 ks + hi of a tile: sb ^ 32 ks
+  auto score_base = [&]() {
+    const int ln = opaque_lane(lane), r = ln % 32, h = ln / 32;
+    return r * (2 * D) + ((16 * h) ^ (16 * (4 * (r % 4) + (r / 4) % 4)));
+  };
+  // E entries of block k (values in result order): this role's columns of
+  // the rows inside the unit
+  auto store_e = [&](int k, const f32x16& val, float scale) {
+    const int64_t brow = (int64_t)(b0 + k) * 32;
+    if (brow >= un.l0 && brow + 32 <= un.l1) {
+      bf16_bits* __restrict__ eb = ecol + (brow + 4 * hi) * lde;
+#pragma unroll
+      for (int v = 0; v < 16; ++v) eb[(8 * (v / 4) + v % 4) * lde] = from_f32<bf16_bits>(scale * val[v]);
+    } else {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t g = brow + 8 * (v / 4) + 4 * hi + v % 4;
+        if (g >= un.l0 && g < un.l1) ecol[g * lde] = from_f32<bf16_bits>(scale * val[v]);
+      }
+    }
+  };
+
+  // One wave's walk over the blocks; both roles pass the same barriers.
+  auto run = [&](auto role_tag) {
+    constexpr int ROLE = decltype(role_tag)::value;
+    // B operands of this role's score product: U (fp16) or H (bf16) rows
+    typedef typename std::conditional<ROLE == 0, f16x8, bf16x8>::type OpT;
+    OpT bop[KS];
+    {
+      const OpT* src = ROLE == 0
+                           ? reinterpret_cast<const OpT*>(A.U16 + ((int64_t)r * HM + jp) * D)
+                           : reinterpret_cast<const OpT*>(
+                                 A.Wr + ((((int64_t)r * A.n_layers + A.layer) * 2 + 1) * HM + jp) * D);
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) bop[ks] = src[2 * ks + hi];
+    }
+    // role 1: dE, E's dE columns and Z for block k (its dP in this wave's
+    // dpx, kept in LDS rather than registers until its P arrives in pex[k % 2])
+    auto finish_de = [&](int k) {
+      f32x16 de;
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const float4 p4 = pex[k % 2][tile_id][i][lane];
+        const float4 d4 = dpx[tile_id][i][lane];
+        de[4 * i] = p4.x * (d4.x - dsum);
+        de[4 * i + 1] = p4.y * (d4.y - dsum);
+        de[4 * i + 2] = p4.z * (d4.z - dsum);
+        de[4 * i + 3] = p4.w * (d4.w - dsum);
+      }
+      store_e(k, de, kLn2);
+      const bf16x8 ea[2] = {pack_b(de, 0), pack_b(de, 8)};
+      accumulate(ring + (k % STG) * TB, ea);
+    };
+    int issued = 0;
+    for (; issued < AHEAD && issued < nb; ++issued) issue(issued);
+    wait_later<PER, AHEAD>(issued - 1);  // block 0 landed
+    ring_barrier();
+    convert(0);
+    for (int k = 0; k < nb; ++k) {
+      // block k + 1 landed (later ones may still be in flight); the barrier
+      // publishes it, block k's fp16 copy and the P of block k - 1, and every
+      // wave is done with block k - 2, whose slot the next load takes
+      wait_later<PER, AHEAD>(issued - k - 2);
+      ring_barrier();
+      if (issued < nb) {
+        issue(issued);
+        ++issued;
+      }
+      if (k + 1 < nb) convert(k + 1);
+      const unsigned char* tile = ring + (k % STG) * TB;
+      // result lane = pair, element v = row 8 (v / 4) + 4 hi + v % 4
+      f32x16 sc = {};
+      if (ROLE == 0) {
+        const unsigned char* tile16 = t16 + (k % 2) * TB;
+        const int sb = score_base();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) sc = mma(*reinterpret_cast<const OpT*>(tile16 + (sb ^ (32 * ks))), bop[ks], sc);
+        const int64_t brow = (int64_t)(b0 + k) * 32;
+        if (brow >= un.l0 && brow + 32 <= un.l1) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) sc[v] = __builtin_amdgcn_exp2f(sc[v] - lse2);
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int64_t g = brow + 8 * (v / 4) + 4 * hi + v % 4;
+            sc[v] = g >= un.l0 && g < un.l1 ? __builtin_amdgcn_exp2f(sc[v] - lse2) : 0.f;
+          }
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          pex[k % 2][tile_id][i][lane] = make_float4(sc[4 * i], sc[4 * i + 1], sc[4 * i + 2], sc[4 * i + 3]);
+        store_e(k, sc, 1.f);
+        const bf16x8 pa[2] = {pack_b(sc, 0), pack_b(sc, 8)};
+        accumulate(tile, pa);
+      } else {
+        // the previous block first, so that its dP is free before this one's forms
+        if (k > 0) finish_de(k - 1);
+        const int sb = score_base();
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) sc = mma(*reinterpret_cast<const OpT*>(tile + (sb ^ (32 * ks))), bop[ks], sc);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          dpx[tile_id][i][lane] = make_float4(sc[4 * i], sc[4 * i + 1], sc[4 * i + 2], sc[4 * i + 3]);
+      }
+    }
+    // the last block's P (every wave passes the barrier: no loads remain)
+    wait_loads<0>();
+    ring_barrier();
+    if (ROLE == 1 && nb > 0) finish_de(nb - 1);
+  };
+  if (role == 0)
+    run(std::integral_constant<int, 0>{});
+  else
+    run(std::integral_constant<int, 1>{});
+  // Z (role 1) or Y (role 0) rows of the tile's pairs: lane = column dim,
+  // element v = pair 32 tile_id + 8 (v / 4) + 4 hi + v % 4 = head * M +
+  // target slot; a request of several chunks leaves fp32 partials for rb_reduce
   if (A.tchunks[t0] == 1) {
+    bf16_bits* __restrict__ out = role == 0 ? A.Y : A.Z;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int pr = 32 * wave + 8 * (v / 4) + 4 * hi + v % 4;
+        const int pr = 32 * tile_id + 8 * (v / 4) + 4 * hi + v % 4;
         const int hh = pr / M, tt = pr % M;
-        if (tt < m) {
-          const int64_t o = ((int64_t)hh * A.n_tgt + t0 + tt) * D + 32 * dt + l32;
-          A.Z[o] = from_f32<bf16_bits>(accz[dt][v]);
-          A.Y[o] = from_f32<bf16_bits>(accy[dt][v]);
-        }
+        if (tt < m) out[((int64_t)hh * A.n_tgt + t0 + tt) * D + 32 * dt + l32] = from_f32<bf16_bits>(acc[dt][v]);
       }
     }
   } else {
     if (un.c == 0 && threadIdx.x == 0) A.first[r] = blockIdx.x;
+    float* __restrict__ outp = role == 0 ? A.Yp : A.Zp;
 #pragma unroll
     for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int pr = 32 * wave + 8 * (v / 4) + 4 * hi + v % 4;
-        const int64_t o = ((int64_t)blockIdx.x * HM + pr) * D + 32 * dt + l32;
-        A.Zp[o] = accz[dt][v];
-        A.Yp[o] = accy[dt][v];
+        const int pr = 32 * tile_id + 8 * (v / 4) + 4 * hi + v % 4;
+        outp[((int64_t)blockIdx.x * HM + pr) * D + 32 * dt + l32] = acc[dt][v];
       }
     }
   }
@@ -394,7 +496,7 @@ hipError_t rb_prep(int D, const RbPrep& a, hipStream_t st) {
 
 hipError_t rb_attn(int D, const RbAttn& a, int grid, hipStream_t st) {
   if (grid == 0) return hipSuccess;
-#define STCA_RBA(DD) hipLaunchKernelGGL(rb_attn_kernel<DD>, dim3(grid), dim3(256), 0, st, a)
+#define STCA_RBA(DD) hipLaunchKernelGGL(rb_attn_kernel<DD>, dim3(grid), dim3(512), 0, st, a)
   if (D == 256) STCA_RBA(256);
   else if (D == 128) STCA_RBA(128);
   else return hipErrorInvalidValue;
