@@ -18,14 +18,14 @@
 //   rb_prep_kernel:  per request, U (fp16 for the scores; bf16 with H into
 //                    the request's dX operand W_r), the softmax statistics
 //                    (log2-unit lse, D) and bf16 copies of q and da.
-//   rb_attn_kernel:  per unit (a history chunk of a request), history blocks of 32 rows streamed into an
-//                    LDS ring by direct loads; four waves (one per SIMD, the
-//                    registers of a whole SIMD lane each), wave w takes the
-//                    32 pairs 32 w ..: S = X U^T (fp16) and dP = X H^T
-//                    (bf16), P and dE, [ln(2) dE | P] into this layer's
-//                    columns of E, and Z += dE^T X, Y += P^T X.  Z and Y
-//                    (bf16, [head][target][D]) are written at the end of
-//                    the request.
+//   rb_attn_kernel:  per unit (a history chunk of a request), history
+//                    blocks of 32 rows streamed into an LDS ring by direct
+//                    loads; eight waves, two per tile of 32 pairs: one forms
+//                    S = X U^T (fp16) and P, and Y += P^T X; the other
+//                    dP = X H^T (bf16) and, one block later, dE, the
+//                    [ln(2) dE | P] words of this layer's columns of E and
+//                    Z += dE^T X.  Z and Y (bf16, [head][target][D]) are
+//                    written at the end of the request.
 // The products that follow (dq, dW_K, dW_V from Z and Y; dX = E W_r after
 // the last layer) are GEMMs.
 #include <type_traits>
