@@ -434,11 +434,11 @@ stca_status_t forward_fast(const Layout& L, const stca_batch_t* b, const void* h
   int32_t* tch_r = reo_part ? at<int32_t>(ws, L.tch_r) : nullptr;
   if (std_part)
     HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, L.group, units,
-                        L.max_units, tch, hdr, st, L.std_lo));
+                        L.max_units, tch, hdr, st, L.std_lo, 1 << 30, device_cus()));
   if (std_part) HIPCHK(rec.mark("sched"));
   if (reo_part)
     HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks2, L.group2, units2,
-                        L.max_units2, tch_r, hdr2, st, L.reord_lo, L.reord_hi));
+                        L.max_units2, tch_r, hdr2, st, L.reord_lo, L.reord_hi, device_cus()));
   if (reo_part) HIPCHK(rec.mark("sched"));
   {
     PackJobs pj{};
@@ -549,7 +549,7 @@ stca_status_t forward_generic(const Layout& L, int bf, const stca_batch_t* b, co
   Unit* units = at<Unit>(ws, L.units);
   int32_t* tch = at<int32_t>(ws, L.tchunks);
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, L.nh, L.nt, L.chunk_blocks, L.group, units, L.max_units,
-                      tch, hdr, st)); HIPCHK(rec.mark("sched"));
+                      tch, hdr, st, 1, 1 << 30, device_cus())); HIPCHK(rec.mark("sched"));
   float* kv = at<float>(ws, L.kv32);
   float* q = at<float>(ws, L.q32);
   float* hid = at<float>(ws, L.hid);
@@ -606,7 +606,7 @@ stca_status_t backward_generic(const Layout& L, int bf, const stca_batch_t* b, c
   int32_t* tch = at<int32_t>(ws, L.tchunks);
   HIPCHK(rec.start());
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, L.group, units, L.max_units, tch,
-                      hdr, st));
+                      hdr, st, 1, 1 << 30, device_cus()));
   if (L.brd) {
     // history chunks of the requests for the reordered attention backward,
     // units of at most 128 rows for dX

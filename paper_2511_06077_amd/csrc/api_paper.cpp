@@ -150,7 +150,7 @@ stca_status_t forward_paper(const PaperLayout& L, int bf, const stca_batch_t* b,
   auto W = [&](const void* base, size_t elems) { return static_cast<const char*>(base) + elems * es; };
   auto qbuf = [&](int i) { return saved ? at<float>(saved, SL.q) + (size_t)i * nt * d : at<float>(ws, L.q); };
   HIPCHK(launch_sched(b->hist_off, b->tgt_off, b->n_requests, nh, nt, L.chunk_blocks, kTargetGroup, units,
-                      L.max_units, tch, hdr, st));
+                      L.max_units, tch, hdr, st, 1, 1 << 30, device_cus()));
   HIPCHK(rec.mark("sched"));
   if (L.path == 1) {
     HIPCHK(swiglu_pack(w->ffn_u, w->ffn_v, w->ffn_o, n, d, F, at<char>(ws, L.wsp), st));

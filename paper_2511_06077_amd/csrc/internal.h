@@ -8,9 +8,13 @@ namespace stca {
 // ---- scheduler (sched.hip)
 // `group`: targets per unit (1..kWideGroup).  Only requests with m_lo..m_hi
 // targets get units (and chunk counts); the others keep a zero chunk count.
+// deal > 0: within each width class, units in descending order of their
+// history blocks, complete rounds of `deal` units alternating in direction
+// (for persistent kernels of `deal` workgroups that take units round-robin
+// and place every partial by its chunk index); 0: request and chunk order.
 hipError_t launch_sched(const int32_t* hoff, const int32_t* toff, int R, int64_t n_hist, int64_t n_tgt,
                         int chunk_blocks, int group, Unit* units, int64_t max_units, int32_t* tchunks,
-                        WsHeader* hdr, hipStream_t st, int m_lo = 1, int m_hi = 1 << 30);
+                        WsHeader* hdr, hipStream_t st, int m_lo = 1, int m_hi = 1 << 30, int deal = 0);
 int64_t host_count_units(const int32_t* hoff, const int32_t* toff, int R, int chunk_blocks, int group,
                          int m_lo = 1, int m_hi = 1 << 30);
 
