@@ -43,12 +43,32 @@ def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
 
 
-def kernel_work(label: str, b: W.Batch, es: int):
+def reordered_requests(b: W.Batch, attn_form: int) -> np.ndarray:
+    """Requests the library runs in the reordered form (its per-request rule,
+    host offsets given, d_h = 32): every one when the form is forced or no
+    request has more than 32 / h targets; otherwise, in the automatic choice,
+    those with at most 32 / h targets; none in the standard form."""
+    wl = b.wl
+    m = b.n_tgt
+    if attn_form == stca.STCA_ATTN_STANDARD or wl.d_model // wl.n_heads != 32:
+        return np.zeros(m.shape, dtype=bool)
+    cap = 32 // wl.n_heads
+    live = m > 0
+    if attn_form == stca.STCA_ATTN_REORDERED or (m[live] <= cap).all():
+        return live
+    return live & (m <= cap)
+
+
+def kernel_work(label: str, b: W.Batch, es: int, attn_form: int = stca.STCA_ATTN_AUTO):
     """Algorithmic (flop, bytes) of one launch of a kernel, from the method's
     compulsory work (accounting.stage_costs) divided over launches."""
     wl = b.wl
     c = accounting.stage_costs(b.hist_len, b.n_tgt, wl.d_model, wl.n_layers, es)
     n = wl.n_layers
+    d = wl.d_model
+    L = b.hist_len.astype(np.float64)
+    m = b.n_tgt.astype(np.float64)
+    reord = reordered_requests(b, attn_form)
     if label == "proj":
         # all layers in one launch; rows of requests without targets still count
         Ls = float(b.hist_len.sum())
@@ -58,12 +78,13 @@ def kernel_work(label: str, b: W.Batch, es: int):
     if label in ("fused", "fused_wide"):
         # one layer: project the rows of the requests this launch serves
         # (X read once) and attend; units with up to 32 targets go to "fused"
-        L = b.hist_len.astype(np.float64)
-        m = b.n_tgt.astype(np.float64)
-        sel = (m > 0) & ((m <= 32) if label == "fused" else (m > 32))
-        d = wl.d_model
+        sel = (m > 0) & ~reord & ((m <= 32) if label == "fused" else (m > 32))
         return (4.0 * L[sel].sum() * d * d + 4.0 * (m[sel] * L[sel]).sum() * d,
                 es * L[sel].sum() * d)
+    if label == "reord_attn":
+        # one layer of the reordered form (Eq. attn-optimized): scores X U^T and
+        # P^T X over the m h (target, head) rows of each request, X read once
+        return (4.0 * (L[reord] * m[reord]).sum() * d * wl.n_heads, es * L[reord].sum() * d)
     if label == "update":
         return c["update"]["flop"] / n, 0.0
     return 0.0, 0.0
@@ -189,13 +210,13 @@ def timed_forward(db, steps: int, warmup: int):
     return total_ms, per
 
 
-def kernel_table(per: dict, b, steps: int, es: int, peak_tf: float) -> dict:
+def kernel_table(per: dict, b, steps: int, es: int, peak_tf: float, attn_form: int = stca.STCA_ATTN_AUTO) -> dict:
     """Per-kernel durations (HIP events) with their algorithmic rates."""
     kernels = {}
     for lab, v in per.items():
         launches = len(v) // steps
         ms = float(np.mean(v))
-        flop, byts = kernel_work(lab, b, es)
+        flop, byts = kernel_work(lab, b, es, attn_form)
         ent = {"launches_per_step": launches, "ms_per_launch": ms, "ms_per_step": ms * launches}
         if flop or byts:
             ent.update({"tflops": flop / (ms * 1e-3) / 1e12, "gbs": byts / (ms * 1e-3) / 1e9,
@@ -235,9 +256,11 @@ def measure_forward(db, steps: int, warmup: int, settle_s: float, events: bool =
     if not events:
         return out
     ev_total, per = timed_forward(db, steps, 1)
-    kernels = kernel_table(per, b, steps, es, peak_tf)
-    dom = max((k for k in kernels if kernel_work(k, b, es) != (0.0, 0.0)), key=lambda k: kernels[k]["ms_per_step"])
-    flop, byts = kernel_work(dom, b, es)
+    af = db.dims.attn_form
+    kernels = kernel_table(per, b, steps, es, peak_tf, af)
+    dom = max((k for k in kernels if kernel_work(k, b, es, af) != (0.0, 0.0)),
+              key=lambda k: kernels[k]["ms_per_step"])
+    flop, byts = kernel_work(dom, b, es, af)
     roof = roofline_entry(dom, kernels[dom]["ms_per_launch"], flop, byts, peak_tf)
     roof["kernel"] = dom
     roof["traffic"] = measured_traffic(wl.name, dom)
