@@ -238,8 +238,8 @@ __global__ __launch_bounds__(512) void rb_attn_kernel(RbAttn A) {
   const bf16_bits* __restrict__ X = static_cast<const bf16_bits*>(A.X);
   constexpr int M = HM / (D / DH);
 
-  const float lse2 = A.stats[((int64_t)r * HM + jp) * 2];
-  const float dsum = A.stats[((int64_t)r * HM + jp) * 2 + 1];
+  float lse2 = A.stats[((int64_t)r * HM + jp) * 2];
+  float dsum = A.stats[((int64_t)r * HM + jp) * 2 + 1];
   f32x16 acc[DT];  // role 0: Y, role 1: Z
 #pragma unroll
   for (int i = 0; i < DT; ++i) acc[i] = f32x16{};
@@ -285,16 +285,26 @@ __global__ __launch_bounds__(512) void rb_attn_kernel(RbAttn A) {
     const int ln = opaque_lane(lane), jj = ln % 16, gg = (ln / 16) % 2, hh = ln / 32;
     const int a4 = jj / 4, c4 = 2 * gg + (jj % 4) / 2;
     const int tb = (4 * hh + a4) * (2 * D) + 16 * (c4 ^ hh) + 8 * ((jj % 4) & 1) + 64 * a4;
+    // X^T operand of product i = s DT + dt
+    auto operand = [&](int i) {
+      const int s = i / DT, dt = i % DT;
+      const int o = (tb ^ (64 * (dt % 4))) + 256 * (dt / 4) + 16 * s * (2 * D);
+      const tr16x4 lo = lds_read_tr16(tile + o);
+      const tr16x4 up = lds_read_tr16(tile + (o ^ 32) + 8 * (2 * D));
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
+    // operands read two products ahead (scheduling barriers keep the
+    // compiler from sinking the reads next to their use)
+    constexpr int NA = 2;
+    bf16x8 xb[NA];
 #pragma unroll
-    for (int s = 0; s < 2; ++s) {
+    for (int i = 0; i < NA; ++i) xb[i] = operand(i);
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
-        const int o = (tb ^ (64 * (dt % 4))) + 256 * (dt / 4) + 16 * s * (2 * D);
-        const tr16x4 lo = lds_read_tr16(tile + o);
-        const tr16x4 up = lds_read_tr16(tile + (o ^ 32) + 8 * (2 * D));
-        const bf16x8 xb = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7));
-        acc[dt] = mma(op[s], xb, acc[dt]);
-      }
+    for (int i = 0; i < 2 * DT; ++i) {
+      const bf16x8 x = xb[i % NA];
+      if (i + NA < 2 * DT) xb[i % NA] = operand(i + NA);
+      acc[i % DT] = mma(op[i / DT], x, acc[i % DT]);
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
   // byte address of row l32, 16-byte unit 2 ks + hi of a tile: sb ^ 32 ks
@@ -333,6 +343,28 @@ __global__ __launch_bounds__(512) void rb_attn_kernel(RbAttn A) {
 #pragma unroll
       for (int ks = 0; ks < KS; ++ks) bop[ks] = src[2 * ks + hi];
     }
+    // These loads land before the ring's first load is issued: the compiler
+    // does not see the ring's loads, and would otherwise wait for these inside
+    // the loop with counts that, in issue order, also drain the ring's
+    // prefetches and the E stores at every block.
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(bop[ks]));
+    asm volatile("" : "+v"(lse2), "+v"(dsum));
+    // this role's score product of a block: sc = X(block) op^T
+    auto score = [&](const unsigned char* tile, f32x16& sc) {
+      const int sb = score_base();
+      constexpr int NA = 2;  // operands read two k-steps ahead
+      OpT xa[NA];
+#pragma unroll
+      for (int i = 0; i < NA; ++i) xa[i] = *reinterpret_cast<const OpT*>(tile + (sb ^ (32 * i)));
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const OpT x = xa[ks % NA];
+        if (ks + NA < KS) xa[ks % NA] = *reinterpret_cast<const OpT*>(tile + (sb ^ (32 * (ks + NA))));
+        sc = mma(x, bop[ks], sc);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    };
     // role 1: dE, E's dE columns and Z for block k (its dP in this wave's
     // dpx, kept in LDS rather than registers until its P arrives in pex[k % 2])
     auto finish_de = [&](int k) {
@@ -371,9 +403,7 @@ __global__ __launch_bounds__(512) void rb_attn_kernel(RbAttn A) {
       f32x16 sc = {};
       if (ROLE == 0) {
         const unsigned char* tile16 = t16 + (k % 2) * TB;
-        const int sb = score_base();
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) sc = mma(*reinterpret_cast<const OpT*>(tile16 + (sb ^ (32 * ks))), bop[ks], sc);
+        score(tile16, sc);
         const int64_t brow = (int64_t)(b0 + k) * 32;
         if (brow >= un.l0 && brow + 32 <= un.l1) {
 #pragma unroll
@@ -394,9 +424,7 @@ __global__ __launch_bounds__(512) void rb_attn_kernel(RbAttn A) {
       } else {
         // the previous block first, so that its dP is free before this one's forms
         if (k > 0) finish_de(k - 1);
-        const int sb = score_base();
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) sc = mma(*reinterpret_cast<const OpT*>(tile + (sb ^ (32 * ks))), bop[ks], sc);
+        score(tile, sc);
 #pragma unroll
         for (int i = 0; i < 4; ++i)
           dpx[tile_id][i][lane] = make_float4(sc[4 * i], sc[4 * i + 1], sc[4 * i + 2], sc[4 * i + 3]);
