@@ -443,13 +443,19 @@ __global__ __launch_bounds__(64 * (D / 32)) void fwd_precise_kernel(FastAttnFwdP
 #pragma unroll
     for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(t + (2 * wave + i) * kSegPitch + lane * 16) = xr[i];
   };
+  // -1 the compiler cannot fold: the residual a - hi written as
+  // fma(hi, -1, a) takes mixed-precision FMAs (an fp16 operand widened
+  // inside the instruction, the fp16 result rounded once) instead of a
+  // widening conversion and a subtraction per element; the value is the same
+  float neg1 = -1.f;
+  asm volatile("" : "+s"(neg1));
   // hi and lo fp16 terms of 8 consecutive result elements
   auto split = [&](const f32x16& a, int off, f16x8& h, f16x8& l) {
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const _Float16 x = static_cast<_Float16>(a[off + i]);
       h[i] = x;
-      l[i] = static_cast<_Float16>(a[off + i] - static_cast<float>(x));
+      l[i] = static_cast<_Float16>(__builtin_fmaf(static_cast<float>(x), neg1, a[off + i]));
     }
   };
 
@@ -470,7 +476,7 @@ __global__ __launch_bounds__(64 * (D / 32)) void fwd_precise_kernel(FastAttnFwdP
         for (int e = 0; e < 4; ++e) {
           const _Float16 x = static_cast<_Float16>(qv[e]);
           qh[s][4 * half + e] = x;
-          ql[s][4 * half + e] = static_cast<_Float16>(qv[e] - static_cast<float>(x));
+          ql[s][4 * half + e] = static_cast<_Float16>(__builtin_fmaf(static_cast<float>(x), neg1, qv[e]));
         }
       }
     }
