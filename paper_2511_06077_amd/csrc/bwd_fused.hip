@@ -30,6 +30,7 @@
 // forward's; the gradient products run on bf16 operands with fp32 sums.
 #include "common.h"
 #include "fast.h"
+#include "ring.h"
 
 namespace stca {
 
@@ -387,6 +388,18 @@ __global__ __launch_bounds__(64 * (D / 32)) void bwd_fused_kernel(FastAttnBwd A)
 // target, elements = rows), O^T = V^T P^T (lane = target, elements = head
 // dims); the result is the same per-chunk partial (unnormalised O, running
 // max in log2 units, sum).
+// A unit descriptor read as wave-uniform values: the values are waited for
+// where the unit is read, not at their first use inside a loop (where, for a
+// kernel whose direct loads the compiler does not see, its wait would also
+// drain those loads at every step).
+__device__ __forceinline__ Unit uniform_unit(const Unit* units, int i) {
+  const Unit u = units[i];
+  return Unit{__builtin_amdgcn_readfirstlane(u.r),  __builtin_amdgcn_readfirstlane(u.t0),
+              __builtin_amdgcn_readfirstlane(u.nt), __builtin_amdgcn_readfirstlane(u.c),
+              __builtin_amdgcn_readfirstlane(u.b0), __builtin_amdgcn_readfirstlane(u.b1),
+              __builtin_amdgcn_readfirstlane(u.l0), __builtin_amdgcn_readfirstlane(u.l1)};
+}
+
 template <int D>
 __global__ __launch_bounds__(64 * (D / 32)) void fwd_precise_kernel(FastAttnFwdPrecise A) {
   constexpr int H = D / DH;
@@ -396,7 +409,8 @@ __global__ __launch_bounds__(64 * (D / 32)) void fwd_precise_kernel(FastAttnFwdP
   constexpr int NS = 32 / RPS;
   constexpr int TILE = NS * kSegPitch;
   static_assert(NS == 2 * H, "two segments per wave");
-  __shared__ __attribute__((aligned(16))) unsigned char xs[2 * TILE];
+  constexpr int STG = 4;  // X blocks in the LDS ring (STG - 1 in flight)
+  __shared__ __attribute__((aligned(16))) unsigned char xs[STG * TILE];
 
   const Unit* __restrict__ units = static_cast<const Unit*>(A.units);
   const WsHeader* __restrict__ hdr = static_cast<const WsHeader*>(A.hdr);
@@ -417,31 +431,35 @@ __global__ __launch_bounds__(64 * (D / 32)) void fwd_precise_kernel(FastAttnFwdP
       wv[ks] = pv[ks * 64];
     }
   }
+  // the weights land before the ring's first load (the compiler does not
+  // see the ring's direct loads, and would otherwise wait for the weights
+  // inside the loop with counts that also drain the ring's prefetches)
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) asm volatile("" : "+v"(wk[ks]), "+v"(wv[ks]));
+  // X blocks by direct global-to-LDS loads, each wave two 1 KB segments
+  // of every block, STG - 1 blocks ahead
   int lu = blockIdx.x;
-  Unit lun = units[lu];
+  Unit lun = uniform_unit(units, lu);
   int lb = lun.b0;
-  u32x4 xr[2];
-  auto fetch = [&]() -> bool {
-    if (lu >= nu) return false;
+  int p_load = 0;  // blocks issued so far
+  auto issue = [&]() {
+    if (lu >= nu) return;
+    unsigned char* slot = xs + (p_load % STG) * TILE;
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
-      const int e = (2 * wave + i) * 64 + lane;
+      const int seg = 2 * wave + i;
+      const int e = seg * 64 + lane;
       const int64_t grow = min((int64_t)lb * 32 + e / CPR, A.n_hist - 1);
-      xr[i] = *reinterpret_cast<const u32x4*>(X + grow * D + (e % CPR) * 8);
+      dma16(X + grow * D + (e % CPR) * 8, slot + seg * kSegPitch);
     }
+    ++p_load;
     if (++lb >= lun.b1) {
       lu += gridDim.x;
       if (lu < nu) {
-        lun = units[lu];
+        lun = uniform_unit(units, lu);
         lb = lun.b0;
       }
     }
-    return true;
-  };
-  auto put = [&](int slot) {
-    unsigned char* t = xs + slot * TILE;
-#pragma unroll
-    for (int i = 0; i < 2; ++i) *reinterpret_cast<u32x4*>(t + (2 * wave + i) * kSegPitch + lane * 16) = xr[i];
   };
   // -1 the compiler cannot fold: the residual a - hi written as
   // fma(hi, -1, a) takes mixed-precision FMAs (an fp16 operand widened
@@ -485,20 +503,23 @@ __global__ __launch_bounds__(64 * (D / 32)) void fwd_precise_kernel(FastAttnFwdP
     l = 0.f;
   };
 
-  bool have = fetch();
-  if (have) put(0);
+#pragma unroll
+  for (int i = 0; i < STG - 1; ++i) issue();
   int cu = blockIdx.x;
-  Unit cun = units[cu];
+  Unit cun = uniform_unit(units, cu);
   int cb = cun.b0;
   for (int p = 0; cu < nu; ++p) {
     lane = opaque(lane);
     tcol = opaque(tcol);
     hi = opaque(hi);
-    __syncthreads();
-    have = fetch();
+    // this wave's parts of block p landed (later ones may be in flight); the
+    // barrier publishes everyone's, and the slot of block p - 1 is free
+    wait_vm(2 * (p_load - 1 - p));
+    ring_barrier();
+    if (p_load < p + STG) issue();
     if (cb == cun.b0) init(cun);
     const unsigned char* xp =
-        xs + (p % 2) * TILE + (tcol % NS) * kSegPitch + (tcol / NS) * (2 * D) + 16 * hi;
+        xs + (p % STG) * TILE + (tcol % NS) * kSegPitch + (tcol / NS) * (2 * D) + 16 * hi;
     f32x16 ak = {}, av = {};
     {
       bf16x8 xo[kXAhead];
@@ -568,13 +589,12 @@ __global__ __launch_bounds__(64 * (D / 32)) void fwd_precise_kernel(FastAttnFwdP
       }
       cu += gridDim.x;
       if (cu < nu) {
-        cun = units[cu];
+        cun = uniform_unit(units, cu);
         cb = cun.b0;
       }
     } else {
       ++cb;
     }
-    if (have) put((p + 1) % 2);
   }
 }
 
