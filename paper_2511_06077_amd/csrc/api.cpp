@@ -209,7 +209,7 @@ stca_status_t make_layout(const stca_dims_t* dims, const stca_batch_t* b, int wi
   const bool std_part = !L->reord || L->mixed;
   L->wide = p == 1 && !with_backward && std_part && wide_groups_for(dims, b);
   L->mat = p == 1 && !with_backward && std_part && (L->wide || dims->kv_form == STCA_KV_MATERIALIZE);
-  L->chunk_blocks = chunk_blocks_for(b, device_cus(), 4, dims->chunk_blocks);
+  L->chunk_blocks = chunk_blocks_auto(b, device_cus(), dims->chunk_blocks, L->std_lo);
   L->group = L->wide ? kWideGroup : kTargetGroup;
   L->max_units = std_part ? max_units_for(b, L->chunk_blocks, L->group, L->std_lo) : 0;
   // the reordered schedule spreads its own requests' rows over the chip

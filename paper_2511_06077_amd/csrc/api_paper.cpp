@@ -57,7 +57,7 @@ bool make_paper_layout(const stca_dims_t* dims, const stca_batch_t* b, PaperLayo
   L->dh = L->d / L->h;
   L->nh = b->n_hist;
   L->nt = b->n_tgt;
-  L->chunk_blocks = chunk_blocks_for(b, device_cus(), 4, dims->chunk_blocks);
+  L->chunk_blocks = chunk_blocks_auto(b, device_cus(), dims->chunk_blocks);
   L->max_units = max_units_for(b, L->chunk_blocks, kTargetGroup);
   L->any_narrow = L->any_wide = true;
   if (b->tgt_off_host) {
