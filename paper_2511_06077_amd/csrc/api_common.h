@@ -106,7 +106,7 @@ inline int chunk_blocks_auto(const stca_batch_t* b, int n_cu, int forced, int m_
   if (forced >= 1 || !b->hist_off_host || !b->tgt_off_host || n_cu < 1) return chunk_blocks_for(b, n_cu, 4, forced);
   int best = 0;
   int64_t best_span = -1;
-  std::vector<int64_t> jobs[2], load;
+  std::vector<int64_t> jobs[2], load, cnt;
   for (int per_cu = 1; per_cu <= 4; per_cu *= 2) {
     const int c = chunk_blocks_for(b, n_cu, per_cu, 0);
     jobs[0].clear();
@@ -126,10 +126,20 @@ inline int chunk_blocks_auto(const stca_batch_t* b, int n_cu, int forced, int m_
       for (int64_t g = 0; g < groups; ++g)
         for (int64_t k = 0; k < nch; ++k) jobs[m > 32].push_back(std::min<int64_t>(cb, nbr - k * cb) + 1);
     }
+    if (jobs[0].size() + jobs[1].size() > (1u << 18)) return chunk_blocks_for(b, n_cu, 4, 0);  // bound the host work
     int64_t span = 0;
     for (auto& j : jobs) {
       if (j.empty()) continue;
-      std::sort(j.begin(), j.end(), std::greater<int64_t>());
+      // descending order; sizes are at most c + 1, so count them when c is small
+      if (c <= (1 << 16)) {
+        cnt.assign(c + 2, 0);
+        for (const int64_t x : j) ++cnt[x];
+        size_t i = 0;
+        for (int64_t x = c + 1; x >= 0; --x)
+          for (int64_t k = 0; k < cnt[x]; ++k) j[i++] = x;
+      } else {
+        std::sort(j.begin(), j.end(), std::greater<int64_t>());
+      }
       load.assign(n_cu, 0);
       for (size_t i = 0; i < j.size(); ++i) {
         const size_t round = i / n_cu, pos = i % n_cu;
