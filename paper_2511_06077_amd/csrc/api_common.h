@@ -130,12 +130,14 @@ inline int chunk_blocks_auto(const stca_batch_t* b, int n_cu, int forced, int m_
     int64_t span = 0;
     for (auto& j : jobs) {
       if (j.empty()) continue;
-      // descending order; sizes are at most c + 1, so count them when c is small
-      if (c <= (1 << 16)) {
-        cnt.assign(c + 2, 0);
+      // descending order: counted when the sizes are small (a request of more
+      // than kMaxChunks chunks has chunks longer than c)
+      const int64_t top = *std::max_element(j.begin(), j.end());
+      if (top <= (1 << 16)) {
+        cnt.assign(top + 1, 0);
         for (const int64_t x : j) ++cnt[x];
         size_t i = 0;
-        for (int64_t x = c + 1; x >= 0; --x)
+        for (int64_t x = top; x >= 0; --x)
           for (int64_t k = 0; k < cnt[x]; ++k) j[i++] = x;
       } else {
         std::sort(j.begin(), j.end(), std::greater<int64_t>());
