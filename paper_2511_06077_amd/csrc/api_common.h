@@ -92,8 +92,8 @@ inline int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu, int for
 }
 
 // Chunk length of the standard form's units: with host offsets, the one of
-// one, two or four units per CU whose estimated makespan is least (fewer
-// units on ties).  The estimate cuts the requests the standard form serves
+// one, two, four or eight units per CU whose estimated makespan is least
+// (fewer units on ties).  The estimate cuts the requests the standard form serves
 // (targets in [m_lo, m_hi]) as the device scheduler does and deals their
 // units (those of up to 32 and of more targets run in separate launches, so
 // their makespans add) in descending size,
@@ -101,13 +101,14 @@ inline int chunk_blocks_for(const stca_batch_t* b, int n_cu, int per_cu, int for
 // scheduler does, and charges each unit one block of fixed cost (its query
 // load, partial stores and merge).  Equal histories then run one unit per
 // CU when the chunks divide evenly (headline batch 1.45 -> 1.41 ms per step),
-// while ragged ones keep four units per CU (two: 2.68 against 2.15 ms).
+// while ragged ones take many (the ragged batch: eight per CU, 2.06 ms per
+// step; four 2.13, two 2.68).
 inline int chunk_blocks_auto(const stca_batch_t* b, int n_cu, int forced, int m_lo = 1, int m_hi = 1 << 30) {
   if (forced >= 1 || !b->hist_off_host || !b->tgt_off_host || n_cu < 1) return chunk_blocks_for(b, n_cu, 4, forced);
   int best = 0;
   int64_t best_span = -1;
   std::vector<int64_t> jobs[2], load, cnt;
-  for (int per_cu = 1; per_cu <= 4; per_cu *= 2) {
+  for (int per_cu = 1; per_cu <= 8; per_cu *= 2) {
     const int c = chunk_blocks_for(b, n_cu, per_cu, 0);
     jobs[0].clear();
     jobs[1].clear();
