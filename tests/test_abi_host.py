@@ -255,3 +255,33 @@ def test_workspace_depends_only_on_arguments(monkeypatch):
     # chunks longer than any history: one unit per request instead of the
     # default's chunks of 8 blocks
     assert stca.stca_workspace_size(dims(chunk_blocks=1000), b) < sizes[0]
+
+
+def _chunk_for(n_hist, per_cu, n_cu=256):
+    """The library's chunk length for `per_cu` units per CU (blocks of 32 rows, at least 8)."""
+    nb = -(-n_hist // 32)
+    return max(8, -(-nb // (per_cu * n_cu)))
+
+
+def test_chunk_rule_equal_histories_take_one_unit_per_cu():
+    # 128 requests x 10240 rows, 32 targets each: two chunks of 160 blocks per
+    # request give one unit per CU, which the makespan estimate prefers to
+    # the finer cuts (same balance, fewer units); the workspace (its unit
+    # table and chunk partials) follows the chosen chunk length
+    b, keep = fake_batch(np.arange(129) * 10240, np.arange(129) * 32)
+    auto = stca.stca_workspace_size(dims(), b)
+    assert auto == stca.stca_workspace_size(dims(chunk_blocks=_chunk_for(10240 * 128, 1)), b)
+    assert auto < stca.stca_workspace_size(dims(chunk_blocks=_chunk_for(10240 * 128, 4)), b)
+
+
+def test_chunk_rule_ragged_histories_take_finer_cuts():
+    # unequal histories balance better in smaller chunks: the choice is one of
+    # the finer candidates, never one unit per CU
+    rng = np.random.default_rng(7)
+    L = [int(x) for x in rng.integers(512, 10241, size=256)]
+    m = [int(x) for x in rng.integers(5, 65, size=256)]  # above the reordered form's 4 targets
+    b, keep = fake_batch(np.concatenate([[0], np.cumsum(L)]), np.concatenate([[0], np.cumsum(m)]))
+    auto = stca.stca_workspace_size(dims(), b)
+    sizes = {p: stca.stca_workspace_size(dims(chunk_blocks=_chunk_for(sum(L), p)), b) for p in (1, 2, 4, 8)}
+    assert auto in (sizes[4], sizes[8])
+    assert auto != sizes[1]
